@@ -1,0 +1,114 @@
+"""CPU fp64 oracle for the gated linear attention (GLA) layer.
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+benchmark's ``cpu_baseline`` leg may import this package; the product path
+(``paper_2312_06635_amd``) never does, and the two share no code.
+
+``fwd`` / ``bwd`` call the plain C recurrence in ``gla_oracle.c`` (paper,
+Sec. 4.1, Eq. 3, and its reverse mode); ``forms`` holds the independent numpy
+formulations (chunkwise form of Sec. 4.2 with the secondary chunking of
+Sec. 4.3, the log-space parallel form of Eq. 4, and the closed-form gate
+gradient) that pin the recurrence.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "gla_oracle.c")
+_LIB = os.path.join(_HERE, "libgla_oracle.so")
+_lib = None
+
+
+def build(force: bool = False) -> str:
+    """Compile gla_oracle.c with gcc into oracle/libgla_oracle.so."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(
+            ["gcc", "-O2", "-fPIC", "-shared", "-std=c99", "-pthread", "-o", tmp, _SRC, "-lm"]
+        )
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        build()
+        lib = ctypes.CDLL(_LIB)
+        dp = ctypes.POINTER(ctypes.c_double)
+        i64 = ctypes.c_int64
+        lib.gla_oracle_fwd.argtypes = [i64, i64, i64, i64, dp, dp, dp, dp, dp, dp, dp, ctypes.c_int]
+        lib.gla_oracle_fwd.restype = ctypes.c_int
+        lib.gla_oracle_bwd.argtypes = [i64, i64, i64, i64, dp, dp, dp, dp, dp, dp, dp,
+                                       dp, dp, dp, dp, dp, ctypes.c_int, i64]
+        lib.gla_oracle_bwd.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def _as_f64(x):
+    if x is None:
+        return None
+    if hasattr(x, "detach"):  # torch tensor
+        x = x.detach().to("cpu").double().numpy()
+    return np.ascontiguousarray(x, dtype=np.float64)
+
+
+def _ptr(a):
+    if a is None:
+        return ctypes.POINTER(ctypes.c_double)()
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+def default_threads() -> int:
+    return max(1, len(os.sched_getaffinity(0)))
+
+
+def fwd(q, k, v, log_alpha, S0=None, want_state=True, nthreads=None):
+    """Recurrent forward (Eq. 3) in fp64.
+
+    q, k, log_alpha: [..., T, d_k]; v: [..., T, d_v]; S0: [..., d_k, d_v] or None.
+    Leading dims are flattened into independent heads.  Returns (o, S_T) as
+    float64 numpy arrays with the input's leading shape (S_T None if not wanted).
+    """
+    q, k, v, la, S0 = (_as_f64(x) for x in (q, k, v, log_alpha, S0))
+    lead = q.shape[:-2]
+    T, K = q.shape[-2:]
+    V = v.shape[-1]
+    BH = int(np.prod(lead)) if lead else 1
+    o = np.empty(lead + (T, V), np.float64)
+    ST = np.empty(lead + (K, V), np.float64) if want_state else None
+    rc = _load().gla_oracle_fwd(BH, T, K, V, _ptr(q), _ptr(k), _ptr(v), _ptr(la), _ptr(S0),
+                                _ptr(o), _ptr(ST), nthreads or default_threads())
+    if rc != 0:
+        raise RuntimeError(f"gla_oracle_fwd failed ({rc})")
+    return o, ST
+
+
+def bwd(q, k, v, log_alpha, dO, S0=None, dST=None, nthreads=None, ckpt=64):
+    """Back-propagation through the recurrence of Eq. 3 in fp64.
+
+    Loss convention: L = sum(o * dO) + sum(S_T * dS_T).
+    Returns dict with dq, dk, dv, dlog_alpha, dS0 (float64 numpy arrays).
+    """
+    q, k, v, la, dO, S0, dST = (_as_f64(x) for x in (q, k, v, log_alpha, dO, S0, dST))
+    lead = q.shape[:-2]
+    T, K = q.shape[-2:]
+    V = v.shape[-1]
+    BH = int(np.prod(lead)) if lead else 1
+    dq = np.empty_like(q)
+    dk = np.empty_like(q)
+    dla = np.empty_like(q)
+    dv = np.empty_like(v)
+    dS0 = np.empty(lead + (K, V), np.float64)
+    rc = _load().gla_oracle_bwd(BH, T, K, V, _ptr(q), _ptr(k), _ptr(v), _ptr(la), _ptr(S0),
+                                _ptr(dO), _ptr(dST), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dla),
+                                _ptr(dS0), nthreads or default_threads(), ckpt)
+    if rc != 0:
+        raise RuntimeError(f"gla_oracle_bwd failed ({rc})")
+    return {"dq": dq, "dk": dk, "dv": dv, "dlog_alpha": dla, "dS0": dS0}

@@ -1,0 +1,257 @@
+"""Pins of the fp64 CPU oracle against what the paper and the mathematics fix.
+
+The oracle (plain recurrence of Sec. 4.1, Eq. 3 and its reverse mode) is checked
+against hand-derived worked examples, textbook closed forms (ungated causal
+linear attention, constant decay), the log-space parallel form (Eq. 4), an
+independent chunkwise reimplementation (Sec. 4.2/4.3), central finite
+differences, the closed-form gate gradient, and invariants (causality,
+linearity, segment split, vanishing gate).  CPU only.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import forms
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def rel(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    return np.abs(a - b).max() / max(np.abs(b).max(), 1e-300)
+
+
+def rand_case(rng, T, K, V, gate_scale=1.0, with_s0=False):
+    q = rng.standard_normal((T, K))
+    k = rng.standard_normal((T, K)) / np.sqrt(K)
+    v = rng.standard_normal((T, V))
+    x = rng.standard_normal((T, K))
+    la = -np.logaddexp(0.0, -x) * gate_scale       # log sigmoid(x), <= 0
+    S0 = rng.standard_normal((K, V)) * 0.3 if with_s0 else None
+    return q, k, v, la, S0
+
+
+# ---------------------------------------------------------------- worked examples
+
+def test_golden_scalar_recurrence_and_gradient():
+    g = json.load(open(os.path.join(GOLDEN, "scalar_T3.json")))
+    col = lambda x: np.asarray(x, np.float64).reshape(-1, 1)
+    q, k, v = col(g["q"]), col(g["k"]), col(g["v"])
+    la = np.log(col(g["alpha"]))
+    S0 = np.array([[g["S0"]]])
+    o, ST = oracle.fwd(q, k, v, la, S0)
+    assert np.allclose(o[:, 0], g["o"], rtol=1e-14, atol=0)
+    assert np.isclose(ST[0, 0], g["S_T"], rtol=1e-14)
+    gr = oracle.bwd(q, k, v, la, col(g["dO"]), S0=S0)
+    for name in ("dq", "dk", "dv", "dlog_alpha"):
+        assert np.allclose(gr[name][:, 0], g[name], rtol=1e-13, atol=1e-15), name
+    assert np.isclose(gr["dS0"][0, 0], g["dS0"], rtol=1e-14)
+
+
+def test_golden_gate_acts_on_key_rows():
+    g = json.load(open(os.path.join(GOLDEN, "diag_gate_K2.json")))
+    a = lambda x: np.asarray(x, np.float64)
+    o, ST = oracle.fwd(a(g["q"]), a(g["k"]), a(g["v"]), np.log(a(g["alpha"])))
+    assert np.allclose(o, a(g["o"]), rtol=1e-14)
+    assert np.allclose(ST, a(g["S_T"]), rtol=1e-14)
+
+
+# ---------------------------------------------------------------- closed forms
+
+def test_ungated_equals_causal_linear_attention():
+    rng = np.random.default_rng(1)
+    q, k, v, _, S0 = rand_case(rng, 37, 5, 7, with_s0=True)
+    la = np.zeros_like(q)
+    o, ST = oracle.fwd(q, k, v, la, S0)
+    assert rel(o, forms.causal_linear_attention(q, k, v, S0)) < 1e-12
+    assert rel(ST, S0 + k.T @ v) < 1e-12
+
+
+def test_constant_decay_equals_decay_mask():
+    rng = np.random.default_rng(2)
+    q, k, v, _, _ = rand_case(rng, 41, 6, 4)
+    gamma = 0.87
+    la = np.full_like(q, np.log(gamma))
+    o, _ = oracle.fwd(q, k, v, la)
+    assert rel(o, forms.decay_mask_attention(q, k, v, gamma)) < 1e-12
+
+
+@pytest.mark.parametrize("gate_scale", [1 / 16, 1.0, 6.0])
+def test_recurrence_equals_logspace_parallel_form(gate_scale):
+    rng = np.random.default_rng(3)
+    q, k, v, la, S0 = rand_case(rng, 29, 6, 5, gate_scale=gate_scale, with_s0=True)
+    o, _ = oracle.fwd(q, k, v, la, S0)
+    assert rel(o, forms.parallel_logspace(q, k, v, la, S0)) < 1e-12
+
+
+def test_vanishing_gate_keeps_only_the_diagonal():
+    rng = np.random.default_rng(4)
+    q, k, v, _, S0 = rand_case(rng, 19, 4, 3, with_s0=True)
+    la = np.full_like(q, -50.0)
+    o, _ = oracle.fwd(q, k, v, la, S0)
+    ref = (q * k).sum(1, keepdims=True) * v
+    assert rel(o, ref) < 1e-12
+
+
+# ---------------------------------------------------------------- chunk form
+
+@pytest.mark.parametrize("C,c", [(1, 1), (4, 2), (8, 8), (16, 8), (16, 4), (48, 16), (48, 48),
+                                 (6, 3)])
+def test_recurrence_equals_chunk_form(C, c):
+    rng = np.random.default_rng(5)
+    T = 48
+    q, k, v, la, S0 = rand_case(rng, T, 6, 5, gate_scale=1 / 16, with_s0=True)
+    o, ST = oracle.fwd(q, k, v, la, S0)
+    oc, STc = forms.chunk_fwd(q, k, v, la, C, c, S0)
+    assert rel(o, oc) < 1e-12
+    assert rel(ST, STc) < 1e-12
+
+
+def test_chunk_form_strong_decay_stays_finite():
+    rng = np.random.default_rng(6)
+    q, k, v, _, _ = rand_case(rng, 32, 4, 3)
+    la = -rng.uniform(5, 40, size=q.shape)
+    o, _ = oracle.fwd(q, k, v, la)
+    oc, _ = forms.chunk_fwd(q, k, v, la, 16, 4)
+    assert np.isfinite(oc).all()
+    assert rel(o, oc) < 1e-12
+
+
+# ---------------------------------------------------------------- gradients
+
+def _loss(q, k, v, la, S0, dO, dST):
+    o, ST = oracle.fwd(q, k, v, la, S0, nthreads=1)
+    return (o * dO).sum() + (ST * dST).sum()
+
+
+def test_gradients_match_central_finite_differences():
+    rng = np.random.default_rng(7)
+    T, K, V = 6, 3, 2
+    q, k, v, la, S0 = rand_case(rng, T, K, V, gate_scale=0.5, with_s0=True)
+    dO = rng.standard_normal((T, V))
+    dST = rng.standard_normal((K, V))
+    g = oracle.bwd(q, k, v, la, dO, S0=S0, dST=dST, nthreads=1, ckpt=4)
+    args = {"q": q, "k": k, "v": v, "la": la, "S0": S0}
+    grads = {"q": g["dq"], "k": g["dk"], "v": g["dv"], "la": g["dlog_alpha"], "S0": g["dS0"]}
+    h = 1e-6
+    for name, x in args.items():
+        fd = np.zeros_like(x)
+        for idx in np.ndindex(x.shape):
+            xp = x.copy(); xp[idx] += h
+            xm = x.copy(); xm[idx] -= h
+            ap = dict(args); ap[name] = xp
+            am = dict(args); am[name] = xm
+            fd[idx] = (_loss(ap["q"], ap["k"], ap["v"], ap["la"], ap["S0"], dO, dST)
+                       - _loss(am["q"], am["k"], am["v"], am["la"], am["S0"], dO, dST)) / (2 * h)
+        assert rel(grads[name], fd) < 1e-7, name
+
+
+@pytest.mark.parametrize("with_state", [False, True])
+def test_bptt_equals_chunk_form_backward(with_state):
+    rng = np.random.default_rng(8)
+    T, K, V = 64, 8, 6
+    q, k, v, la, S0 = rand_case(rng, T, K, V, gate_scale=1 / 4, with_s0=with_state)
+    dO = rng.standard_normal((T, V))
+    dST = rng.standard_normal((K, V)) if with_state else None
+    g = oracle.bwd(q, k, v, la, dO, S0=S0, dST=dST, ckpt=7)
+    gc = forms.chunk_bwd(q, k, v, la, dO, 16, 4, S0=S0, dST=dST)
+    for name in ("dq", "dk", "dv", "dlog_alpha", "dS0"):
+        assert rel(g[name], gc[name]) < 1e-11, name
+
+
+def test_direct_gate_gradient_equals_closed_form():
+    """Mao et al.'s direct formula (what O2 computes) equals the closed form of
+    Sec. 4.3 with the sign q (.) dq - k (.) dk; the opposite sign fails."""
+    rng = np.random.default_rng(9)
+    T, K, V = 40, 5, 4
+    q, k, v, la, _ = rand_case(rng, T, K, V, gate_scale=0.3)
+    dO = rng.standard_normal((T, V))
+    g = oracle.bwd(q, k, v, la, dO)
+    cf = forms.dlog_alpha_closed_form(q, k, g["dq"], g["dk"])
+    assert rel(g["dlog_alpha"], cf) < 1e-11
+    flipped = np.flip(np.cumsum(np.flip(k * g["dk"] - q * g["dq"], 0), 0), 0)
+    assert rel(g["dlog_alpha"], flipped) > 0.1
+
+
+def test_ungated_gradients_equal_parallel_form_gradients():
+    """With alpha = 1 and S0 = 0 the backward of FlashLinearAttention with one
+    chunk (App. B, Alg. 2, C = L): dQ = (dO V^T (.) M) K, dK = (V dO^T (.) M^T) Q,
+    dV = (Q K^T (.) M)^T dO."""
+    rng = np.random.default_rng(10)
+    T, K, V = 23, 4, 6
+    q, k, v, _, _ = rand_case(rng, T, K, V)
+    dO = rng.standard_normal((T, V))
+    g = oracle.bwd(q, k, v, np.zeros_like(q), dO)
+    M = np.tril(np.ones((T, T)))
+    assert rel(g["dq"], ((dO @ v.T) * M) @ k) < 1e-12
+    assert rel(g["dk"], ((v @ dO.T) * M.T) @ q) < 1e-12
+    assert rel(g["dv"], ((q @ k.T) * M).T @ dO) < 1e-12
+
+
+# ---------------------------------------------------------------- invariants
+
+def test_causality():
+    rng = np.random.default_rng(11)
+    q, k, v, la, S0 = rand_case(rng, 30, 4, 3, with_s0=True)
+    o, _ = oracle.fwd(q, k, v, la, S0)
+    t = 17
+    q2, k2, v2, la2 = (x.copy() for x in (q, k, v, la))
+    for x in (q2, k2, v2):
+        x[t + 1:] += rng.standard_normal(x[t + 1:].shape)
+    la2[t + 1:] -= 1.0
+    o2, _ = oracle.fwd(q2, k2, v2, la2, S0)
+    assert np.array_equal(o[: t + 1], o2[: t + 1])
+    assert not np.allclose(o[t + 1:], o2[t + 1:])
+
+
+def test_linearity_in_v():
+    rng = np.random.default_rng(12)
+    q, k, v, la, _ = rand_case(rng, 25, 4, 5)
+    v2 = rng.standard_normal(v.shape)
+    o1, _ = oracle.fwd(q, k, v, la)
+    o2, _ = oracle.fwd(q, k, v2, la)
+    o3, _ = oracle.fwd(q, k, 2.0 * v - 3.0 * v2, la)
+    assert rel(o3, 2.0 * o1 - 3.0 * o2) < 1e-12
+
+
+def test_segment_split_carries_state():
+    rng = np.random.default_rng(13)
+    q, k, v, la, S0 = rand_case(rng, 50, 5, 4, with_s0=True)
+    o, ST = oracle.fwd(q, k, v, la, S0)
+    oa, Sa = oracle.fwd(q[:21], k[:21], v[:21], la[:21], S0)
+    ob, Sb = oracle.fwd(q[21:], k[21:], v[21:], la[21:], Sa)
+    assert rel(np.concatenate([oa, ob]), o) < 1e-13
+    assert rel(Sb, ST) < 1e-13
+
+
+def test_batched_heads_threads_and_checkpoints_are_consistent():
+    rng = np.random.default_rng(14)
+    BH, T, K, V = 5, 33, 4, 6
+    q = rng.standard_normal((BH, T, K))
+    k = rng.standard_normal((BH, T, K))
+    v = rng.standard_normal((BH, T, V))
+    la = -rng.uniform(0, 0.3, (BH, T, K))
+    dO = rng.standard_normal((BH, T, V))
+    o1, S1 = oracle.fwd(q, k, v, la, nthreads=1)
+    o8, S8 = oracle.fwd(q, k, v, la, nthreads=8)
+    assert np.array_equal(o1, o8) and np.array_equal(S1, S8)
+    for h in range(BH):
+        oh, _ = oracle.fwd(q[h], k[h], v[h], la[h])
+        assert np.array_equal(oh, o1[h])
+    g1 = oracle.bwd(q, k, v, la, dO, nthreads=1, ckpt=1)
+    g2 = oracle.bwd(q, k, v, la, dO, nthreads=8, ckpt=64)
+    for name in g1:
+        assert np.array_equal(g1[name], g2[name]), name
+
+
+def test_empty_sequence():
+    q = np.zeros((0, 3)); v = np.zeros((0, 2))
+    S0 = np.ones((3, 2))
+    o, ST = oracle.fwd(q, q, v, q, S0)
+    assert o.shape == (0, 2) and np.array_equal(ST, S0)
+    g = oracle.bwd(q, q, v, q, v, S0=S0, dST=np.full((3, 2), 2.0))
+    assert np.array_equal(g["dS0"], np.full((3, 2), 2.0))
