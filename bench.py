@@ -1,0 +1,199 @@
+#!/usr/bin/env python3
+"""Benchmark of the chunkwise GLA layer, forward + backward, on one MI355X.
+
+One step = the whole hot path over one batch: gla_chunk_fwd (gate factors,
+gated operands and intra-chunk matrices; state pass and outputs) followed by
+gla_chunk_bwd reusing the forward's workspace (dq sweep; dk/dlog_alpha sweep;
+dv sweep).  Each stage is launched on its own through the C ABI's stage
+selector with a HIP event after it, so the per-kernel durations are measured
+live on the stream the kernels run on, inside the timed region.
+
+Prints one JSON line.  `value` is tokens/s (B*T per step) with all inputs
+resident in HBM; TFLOP/s uses the algorithmic FLOP count of the chunk form
+(per token-head: fwd 4 d_k d_v + (C+1)(d_k+d_v), bwd 8 d_k d_v + (C+1)(3 d_k + 2 d_v)).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import torch  # noqa: E402
+
+import workloads as W  # noqa: E402
+
+PEAK_BF16_FLOPS = 2.5e15
+PEAK_F32_FLOPS = 157.3e12
+PEAK_HBM = 8.0e12
+RIDGE = PEAK_BF16_FLOPS / PEAK_HBM
+
+STAGES = [("prep", "fwd", 1), ("fwd_main", "fwd", 2), ("bwd_dq", "bwd", 2), ("bwd_dk", "bwd", 3),
+          ("bwd_dv", "bwd", 4)]
+
+
+def algorithmic(cfg):
+    """Algorithmic FLOPs and HBM bytes per launch of each stage (and totals)."""
+    B, H, T, K, V, C = cfg["B"], cfg["H"], cfg["T"], cfg["dk"], cfg["dv"], cfg["chunk"]
+    s = 2 if cfg["io"] == "bf16" else 4
+    n = B * H * T                       # token-heads
+    g = B * H * ((T + C - 1) // C) * K * 4  # chunk decays (fp32)
+    P = n * C * s                       # intra-chunk matrices
+    dP = n * C * 4
+    st = {
+        # gate factors, Q (.) Lambda, K (.) Gamma, P: reads q, k, log_alpha
+        "prep": dict(flops=n * (C + 1) * K, bytes=n * s * 3 * K + n * s * 2 * K + P + g),
+        # state pass + output: reads Qt, Kt, v, P, gamma; writes o
+        "fwd_main": dict(flops=n * (4 * K * V + (C + 1) * V), bytes=n * s * (2 * K + 2 * V) + P + g),
+        # dq sweep: reads k, log_alpha, v, dO; writes dq and dP
+        "bwd_dq": dict(flops=n * (2 * K * V + (C + 1) * (K + V)), bytes=n * s * (3 * K + 2 * V) + dP),
+        # dk sweep: reads q, k, log_alpha, v, dO, dq, dP; writes dk, dlog_alpha
+        "bwd_dk": dict(flops=n * (4 * K * V + (C + 1) * K),
+                       bytes=n * s * (6 * K + 2 * V) + dP),
+        # dv sweep: reads Qt, Kt, P, gamma, dO; writes dv
+        "bwd_dv": dict(flops=n * (2 * K * V + (C + 1) * V), bytes=n * s * (2 * K + 2 * V) + P + g),
+    }
+    fwd = n * (4 * K * V + (C + 1) * (K + V))
+    bwd = n * (8 * K * V + (C + 1) * (3 * K + 2 * V))
+    io_bytes = n * s * (9 * K + 5 * V)
+    return st, fwd, bwd, io_bytes
+
+
+def cpu_baseline(cfg, inputs, target_s=15.0):
+    """The fp64 oracle timed on the host cores on a bounded sample of heads."""
+    import numpy as np
+
+    import oracle
+
+    oracle.build()
+    threads = oracle.default_threads()
+    BH = cfg["B"] * cfg["H"]
+    flat = {k: (v.float().reshape(BH, *v.shape[2:]) if v is not None else None) for k, v in inputs.items()}
+    # calibrate on one head, then size the sample to ~target_s of wall time
+    def run(idx, nth):
+        sl = lambda n: None if flat[n] is None else flat[n][idx].double().numpy()
+        t0 = time.perf_counter()
+        oracle.fwd(sl("q"), sl("k"), sl("v"), sl("log_alpha"), sl("S0"), nthreads=nth)
+        oracle.bwd(sl("q"), sl("k"), sl("v"), sl("log_alpha"), sl("dO"), S0=sl("S0"), dST=sl("dST"),
+                   nthreads=nth)
+        return time.perf_counter() - t0
+    t1 = run([0], 1)
+    heads = int(max(1, min(BH, threads * max(1, int(target_s / max(t1, 1e-3))))))
+    heads = max(1, min(BH, (heads // threads) * threads if heads >= threads else heads))
+    idx = list(range(heads))
+    el = run(idx, threads)
+    tokens = heads * cfg["T"] / cfg["H"]
+    del np
+    return {"value": tokens / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{heads} of {BH} heads (full T={cfg['T']}), fwd+bwd fp64 recurrence + BPTT, "
+                      f"{el:.1f} s wall; tokens counted as heads*T/H"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="gla1p3b_T2048", choices=sorted(W.CONFIGS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(heads shard across GPUs with no communication; see DESIGN.md).", file=sys.stderr)
+        sys.exit(2)
+
+    import paper_2312_06635_amd as gla
+
+    cfg = W.CONFIGS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    inp_cpu = W.make_inputs(cfg)
+    d = {k: (v.to(dev) if v is not None else None) for k, v in inp_cpu.items()}
+    B, H, T, K, V, C, c = (cfg[x] for x in ("B", "H", "T", "dk", "dv", "chunk", "subchunk"))
+    dt = d["q"].dtype
+    ws = torch.empty(gla.workspace_bytes(B, H, T, K, V, C, c, dt, op=1), dtype=torch.uint8, device=dev)
+    o = torch.empty_like(d["v"])
+    ST = torch.empty(B, H, K, V, dtype=torch.float32, device=dev) if cfg["want_state"] else None
+    grads = {"dq": torch.empty_like(d["q"]), "dk": torch.empty_like(d["k"]), "dv": torch.empty_like(d["v"]),
+             "dlog_alpha": torch.empty_like(d["log_alpha"]),
+             "dS0": torch.empty(B, H, K, V, dtype=torch.float32, device=dev) if d["S0"] is not None else None}
+    stream = torch.cuda.current_stream(dev)
+
+    def launch(stage_name, which, stage):
+        if which == "fwd":
+            gla.chunk_fwd(d["q"], d["k"], d["v"], d["log_alpha"], C, c, S0=d["S0"], workspace=ws,
+                          stage=stage, out=(o, ST))
+        else:
+            gla.chunk_bwd(d["q"], d["k"], d["v"], d["log_alpha"], d["dO"], C, c, S0=d["S0"], dST=d["dST"],
+                          workspace=ws, reuse_fwd_workspace=True, stage=stage, out=grads)
+
+    def step(events=None):
+        if events is not None:
+            events[0].record(stream)
+        for i, (nm, which, stg) in enumerate(STAGES):
+            launch(nm, which, stg)
+            if events is not None:
+                events[i + 1].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(STAGES) + 1)]
+           for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(evs[s])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    stage_ms = {nm: 0.0 for nm, _, _ in STAGES}
+    for s in range(args.steps):
+        for i, (nm, _, _) in enumerate(STAGES):
+            stage_ms[nm] += evs[s][i].elapsed_time(evs[s][i + 1]) / args.steps
+    st_alg, fwd_flops, bwd_flops, io_bytes = algorithmic(cfg)
+    ms_per_step = 1e3 * elapsed / args.steps
+    tokens = B * T
+    value = tokens * args.steps / elapsed
+    tflops = (fwd_flops + bwd_flops) * args.steps / elapsed / 1e12
+    peak = PEAK_BF16_FLOPS if cfg["io"] == "bf16" else PEAK_F32_FLOPS
+
+    dom = max(stage_ms, key=stage_ms.get)
+    a = st_alg[dom]
+    t_dom = stage_ms[dom] * 1e-3
+    ai = a["flops"] / a["bytes"]
+    if ai < RIDGE:
+        roof = {"kernel": dom, "bound": "hbm", "achieved": a["bytes"] / t_dom / 1e9, "peak": PEAK_HBM / 1e9,
+                "unit": "GB/s"}
+    else:
+        roof = {"kernel": dom, "bound": "mfma", "achieved": a["flops"] / t_dom / 1e12, "peak": peak / 1e12,
+                "unit": "TFLOP/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = None
+    roof["avg_ms"] = stage_ms[dom]
+
+    out = {
+        "metric": "GLA fwd+bwd tokens/s and TFLOP/s (% bf16 MFMA peak), 1.3B layer, T=2048",
+        "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": cfg["io"], "data": "synthetic",
+        "config": {"workload": args.workload, "B": B, "H": H, "T": T, "d_k": K, "d_v": V, "chunk": C,
+                   "subchunk": c, "parallelism": "none (1 GPU)"},
+        "tflops": tflops, "mfma_peak_frac": tflops * 1e12 / peak,
+        "hbm_io_roofline_frac": (io_bytes / PEAK_HBM) / (elapsed / args.steps),
+        "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, inp_cpu)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

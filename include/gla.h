@@ -1,0 +1,143 @@
+/*
+ * gla.h -- C ABI of the MI355X (gfx950) chunkwise gated linear attention layer.
+ *
+ * The layer (Yang et al., "Gated Linear Attention Transformers with
+ * Hardware-Efficient Training", Sec. 4.1, Eq. 3), per batch row b and head h:
+ *
+ *     S_t = Diag(alpha_t) S_{t-1} + k_t^T v_t,     o_t = q_t S_t,
+ *
+ * with alpha_t = exp(log_alpha_t) in (0, 1]^{d_k}, S_t in R^{d_k x d_v}, and
+ * S_0 = S0 (zero, or the final state of the previous segment: Sec. 2.2).  The
+ * library evaluates it in the chunkwise form of Sec. 4.2 with the secondary
+ * (sub-chunk) tiling of Sec. 4.3: an inter-chunk state pass, attention-like
+ * intra-chunk blocks (bf16 matrix-core products between sub-chunks, fp32
+ * log-space evaluation inside a sub-chunk), and the closed-form gate gradient
+ * of Sec. 4.3 in the backward.
+ *
+ * Conventions shared by every entry point
+ *   - Tensors are device pointers, contiguous row-major:
+ *       q, k, log_alpha, dq, dk, dlog_alpha : [B, H, T, d_k]   (io dtype)
+ *       v, o, dO, dv                        : [B, H, T, d_v]   (io dtype)
+ *       S0, S_T, dS_T, dS0                  : [B, H, d_k, d_v] (fp32 always)
+ *     and 16-byte aligned.  "Nullable" pointers may be NULL: an absent S0 or
+ *     dS_T means zero, an absent S_T or dS0 means "not wanted".
+ *   - The caller owns every buffer; the library never allocates or frees
+ *     device memory and keeps no mutable global state, so calls are
+ *     re-entrant.  Outputs are overwritten, never accumulated into, and must
+ *     not alias inputs.
+ *   - All work is enqueued on `stream` (a hipStream_t; NULL = the default
+ *     stream) and the call returns without synchronising.
+ *   - Argument errors are reported synchronously, before anything is
+ *     enqueued.  A failed kernel launch returns GLA_ERR_HIP; faults inside
+ *     kernels surface at the caller's next synchronisation.  No C++
+ *     exception crosses this boundary.
+ *   - Domain: log_alpha must be finite and <= 0 (alpha in (0, 1], Sec. 4.1);
+ *     log_alpha = 0 (alpha = 1) gives ungated linear attention (Sec. 2.1).
+ *     Very negative values are handled (the intra-sub-chunk decays fall back
+ *     to pairwise exponentials when a sub-chunk's decay range is large).
+ *   - There is no scale argument (Eq. 3 has none): pre-scale k if desired.
+ *
+ * Supported shapes: d_k and d_v multiples of 16 with d_k <= 256 and
+ * d_v <= 1024 (fp32 io additionally needs d_k <= 128); chunk C in {16, 32, 64}; sub-chunk c a divisor of 16 that also
+ * divides C; any T >= 0 (a last, shorter chunk is handled by masking).
+ * Other values return GLA_ERR_UNSUPPORTED.
+ */
+#ifndef GLA_H_
+#define GLA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  GLA_OK = 0,
+  GLA_ERR_NULL = 1,        /* a required pointer is NULL                       */
+  GLA_ERR_SHAPE = 2,       /* a dimension is negative or inconsistent          */
+  GLA_ERR_DTYPE = 3,       /* unknown io dtype                                 */
+  GLA_ERR_UNSUPPORTED = 4, /* valid, but outside what the kernels implement    */
+  GLA_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than required          */
+  GLA_ERR_HIP = 6          /* a HIP runtime call or kernel launch failed       */
+} gla_status;
+
+typedef enum { GLA_F32 = 0, GLA_BF16 = 1 } gla_dtype;
+
+/* Flags (bitwise OR) for gla_problem.flags. */
+enum {
+  /* gla_chunk_bwd only: the workspace still holds what gla_chunk_fwd left in
+   * it for exactly the same problem and inputs (the gated operands Q (.) Lambda,
+   * K (.) Gamma, the intra-chunk matrices P and the chunk decays gamma), so
+   * the backward skips recomputing them (paper, Sec. 3.3: materialize once
+   * vs. recompute). */
+  GLA_FLAG_REUSE_FWD_WORKSPACE = 1u << 0,
+  /* Bits 8..11 select a single stage of an entry point's launch sequence (0 =
+   * the whole sequence), so that a profiler or benchmark can time each kernel
+   * on its own stream with events.  Running the stages 1, 2, ... in order with
+   * the same arguments and workspace gives exactly the result of stage 0.
+   *   gla_chunk_fwd: 1 = gate factors, gated operands and intra-chunk P
+   *                  2 = state pass and chunk outputs
+   *   gla_chunk_bwd: 1 = as forward stage 1 (skipped with REUSE_FWD_WORKSPACE)
+   *                  2 = forward sweep over key-feature tiles: dq (and dP)
+   *                  3 = reverse sweep over key-feature tiles: dk, dlog_alpha
+   *                  4 = reverse sweep over value-column tiles: dv, dS0
+   * Out-of-range stage numbers return GLA_ERR_SHAPE. */
+  GLA_STAGE_SHIFT = 8,
+  GLA_STAGE_MASK = 0xFu << 8
+};
+
+typedef struct {
+  int32_t B, H;      /* batch rows and heads; heads are independent            */
+  int32_t T;         /* sequence length L                                      */
+  int32_t dk, dv;    /* per-head key/value widths d'_k, d'_v (Sec. 4.4)        */
+  int32_t chunk;     /* chunk length C (Sec. 2.2)                              */
+  int32_t subchunk;  /* sub-chunk length c of the secondary tiling (Sec. 4.3)  */
+  int32_t io;        /* gla_dtype of every non-state tensor                    */
+  uint32_t flags;    /* GLA_FLAG_* bits                                        */
+} gla_problem;
+
+/* Bytes of device workspace gla_chunk_fwd (op = 0) or gla_chunk_bwd (op = 1)
+ * needs for this problem; 0 if the problem is invalid.  The backward's
+ * workspace layout begins with the forward's, so a buffer sized for op = 1
+ * can be passed to both (required for GLA_FLAG_REUSE_FWD_WORKSPACE). */
+size_t gla_workspace_bytes(const gla_problem *prob, int op);
+
+/* Forward, chunkwise form (Sec. 4.2 / 4.3; the non-materialized state pass of
+ * Sec. 3.3 and App. B, Alg. 5, with the intra-chunk part of Alg. 3).
+ *   in : q, k, v, log_alpha; S0 (nullable, fp32)
+ *   out: o; S_T (nullable, fp32, the state after the last step)
+ *   workspace: device buffer of at least gla_workspace_bytes(prob, 0) bytes;
+ *   on return its contents are what GLA_FLAG_REUSE_FWD_WORKSPACE expects. */
+gla_status gla_chunk_fwd(const gla_problem *prob, const void *q, const void *k, const void *v,
+                         const void *log_alpha, const float *S0, void *o, float *S_T,
+                         void *workspace, size_t workspace_bytes, void *stream);
+
+/* Backward of gla_chunk_fwd for the loss L = sum(o * dO) + sum(S_T * dS_T)
+ * (App. B, Alg. 4/6 with the closed-form gate gradient of Sec. 4.3):
+ *   dq, dk, dv: gradients of q, k, v;
+ *   dlog_alpha: gradient w.r.t. log_alpha, = revcumsum(q*dq - k*dk)
+ *               + rowsum(S_T * dS_T) (the last term vanishes when dS_T = 0);
+ *   dS0 (nullable): gradient w.r.t. S0.
+ *   in : q, k, v, log_alpha, S0 (nullable), dO, dS_T (nullable)
+ *   workspace: at least gla_workspace_bytes(prob, 1) bytes. */
+gla_status gla_chunk_bwd(const gla_problem *prob, const void *q, const void *k, const void *v,
+                         const void *log_alpha, const float *S0, const void *dO,
+                         const float *dS_T, void *dq, void *dk, void *dv, void *dlog_alpha,
+                         float *dS0, void *workspace, size_t workspace_bytes, void *stream);
+
+/* Forward in the recurrent form (Sec. 4.1, Eq. 3), one step at a time with the
+ * state in fp32; no workspace.  prob->chunk and prob->subchunk are ignored.
+ *   in : q, k, v, log_alpha; S0 (nullable)   out: o; S_T (nullable) */
+gla_status gla_recurrent_fwd(const gla_problem *prob, const void *q, const void *k,
+                             const void *v, const void *log_alpha, const float *S0, void *o,
+                             float *S_T, void *stream);
+
+/* Static, human-readable name of a status code (never NULL). */
+const char *gla_status_string(gla_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GLA_H_ */

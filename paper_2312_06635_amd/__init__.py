@@ -1,0 +1,202 @@
+"""MI355X-native chunkwise gated linear attention (GLA) layer.
+
+Thin Python binding over the C ABI of ``libgla.so`` (declared in
+``include/gla.h``).  This module only marshals arguments: it checks tensors,
+allocates outputs and workspace with torch, and passes raw device pointers and
+the current HIP stream to the library.  Every step of the computation runs in
+the library's HIP kernels; there is no fallback of any kind: every entry point
+raises if ``libgla.so`` has not been built.
+
+Layer (paper Sec. 4.1, Eq. 3), per batch row and head:
+    S_t = Diag(exp(log_alpha_t)) S_{t-1} + k_t^T v_t,   o_t = q_t S_t.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+__all__ = [
+    "chunk_fwd", "chunk_bwd", "recurrent_fwd", "workspace_bytes", "GlaError", "library_path",
+    "GLA_OK", "GLA_ERR_NULL", "GLA_ERR_SHAPE", "GLA_ERR_DTYPE", "GLA_ERR_UNSUPPORTED",
+    "GLA_ERR_WORKSPACE", "GLA_ERR_HIP", "FLAG_REUSE_FWD_WORKSPACE", "GlaProblem", "lib",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+library_path = os.path.join(_HERE, "libgla.so")
+
+GLA_OK, GLA_ERR_NULL, GLA_ERR_SHAPE, GLA_ERR_DTYPE = 0, 1, 2, 3
+GLA_ERR_UNSUPPORTED, GLA_ERR_WORKSPACE, GLA_ERR_HIP = 4, 5, 6
+GLA_F32, GLA_BF16 = 0, 1
+FLAG_REUSE_FWD_WORKSPACE = 1
+STAGE_SHIFT = 8
+
+
+class GlaProblem(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("H", ctypes.c_int32), ("T", ctypes.c_int32),
+                ("dk", ctypes.c_int32), ("dv", ctypes.c_int32), ("chunk", ctypes.c_int32),
+                ("subchunk", ctypes.c_int32), ("io", ctypes.c_int32), ("flags", ctypes.c_uint32)]
+
+
+class GlaError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {lib().gla_status_string(status).decode()}")
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libgla.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(library_path):
+            raise ImportError(
+                f"{library_path} is missing; build it with `python -m paper_2312_06635_amd.build`")
+        L = ctypes.CDLL(library_path)
+        P = ctypes.POINTER(GlaProblem)
+        vp, sz, i32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int
+        L.gla_workspace_bytes.argtypes = [P, i32]
+        L.gla_workspace_bytes.restype = sz
+        L.gla_chunk_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.gla_chunk_fwd.restype = i32
+        L.gla_chunk_bwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.gla_chunk_bwd.restype = i32
+        L.gla_recurrent_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.gla_recurrent_fwd.restype = i32
+        L.gla_status_string.argtypes = [i32]
+        L.gla_status_string.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _io_code(dt: torch.dtype) -> int:
+    if dt == torch.bfloat16:
+        return GLA_BF16
+    if dt == torch.float32:
+        return GLA_F32
+    raise TypeError(f"unsupported dtype {dt}; use torch.bfloat16 or torch.float32")
+
+
+def _problem(q, v, chunk, subchunk, flags=0) -> GlaProblem:
+    B, H, T, dk = q.shape
+    return GlaProblem(B, H, T, dk, v.shape[-1], chunk, subchunk, _io_code(q.dtype), flags)
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _check(q, k, v, la, extra=(), states=()):
+    if q.dim() != 4:
+        raise ValueError("q must be [B, H, T, d_k]")
+    B, H, T, dk = q.shape
+    dev = q.device
+    if dev.type != "cuda":
+        raise ValueError("tensors must be on a HIP device")
+    for name, t, last in (("k", k, dk), ("log_alpha", la, dk), ("v", v, None)) + tuple(extra):
+        if t.device != dev or t.dtype != q.dtype or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous {q.dtype} tensor on {dev}")
+        if t.shape[:3] != (B, H, T) or (last is not None and t.shape[3] != last):
+            raise ValueError(f"{name} has shape {tuple(t.shape)}")
+    if not q.is_contiguous():
+        raise ValueError("q must be contiguous")
+    dv = v.shape[3]
+    for name, t in states:
+        if t is None:
+            continue
+        if t.device != dev or t.dtype != torch.float32 or not t.is_contiguous() or \
+                tuple(t.shape) != (B, H, dk, dv):
+            raise ValueError(f"{name} must be a contiguous float32 [B, H, d_k, d_v] tensor on {dev}")
+
+
+def _stream(dev):
+    return torch.cuda.current_stream(dev).cuda_stream
+
+
+def workspace_bytes(B, H, T, dk, dv, chunk, subchunk, dtype=torch.bfloat16, op=1) -> int:
+    """Workspace bytes for the forward (op=0) or backward (op=1)."""
+    p = GlaProblem(B, H, T, dk, dv, chunk, subchunk, _io_code(dtype), 0)
+    return int(lib().gla_workspace_bytes(ctypes.byref(p), op))
+
+
+def _workspace(p, op, dev, workspace):
+    need = int(lib().gla_workspace_bytes(ctypes.byref(p), op))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    if workspace.numel() * workspace.element_size() < need:
+        raise ValueError(f"workspace holds {workspace.numel()} bytes, {need} needed")
+    return workspace
+
+
+def chunk_fwd(q, k, v, log_alpha, chunk=64, subchunk=16, S0=None, output_final_state=False,
+              workspace=None, stage=0, out=None):
+    """Chunkwise GLA forward.  Returns (o, S_T or None).
+
+    stage selects one kernel of the launch sequence (see GLA_STAGE_* in
+    include/gla.h); out=(o, S_T) reuses caller-provided output tensors."""
+    _check(q, k, v, log_alpha, states=(("S0", S0),))
+    B, H, T, dk = q.shape
+    dv = v.shape[3]
+    p = _problem(q, v, chunk, subchunk, stage << STAGE_SHIFT)
+    if out is not None:
+        o, ST = out
+    else:
+        o = torch.empty_like(v)
+        ST = torch.empty(B, H, dk, dv, dtype=torch.float32, device=q.device) if output_final_state else None
+    ws = _workspace(p, 0, q.device, workspace)
+    st = lib().gla_chunk_fwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(S0),
+                             _ptr(o), _ptr(ST), _ptr(ws), ws.numel() * ws.element_size(),
+                             _stream(q.device))
+    if st != GLA_OK:
+        raise GlaError(st, "gla_chunk_fwd")
+    return o, ST
+
+
+def chunk_bwd(q, k, v, log_alpha, dO, chunk=64, subchunk=16, S0=None, dST=None,
+              want_dS0=False, workspace=None, reuse_fwd_workspace=False, stage=0, out=None):
+    """Chunkwise GLA backward for L = sum(o * dO) + sum(S_T * dS_T).
+
+    Returns dict(dq, dk, dv, dlog_alpha, dS0).  With reuse_fwd_workspace the
+    given workspace must still hold what chunk_fwd left for the same inputs.
+    stage and out as in chunk_fwd (out is a dict shaped like the result)."""
+    _check(q, k, v, log_alpha, extra=(("dO", dO, v.shape[3]),), states=(("S0", S0), ("dST", dST)))
+    B, H, T, dk = q.shape
+    dv = v.shape[3]
+    flags = (FLAG_REUSE_FWD_WORKSPACE if reuse_fwd_workspace else 0) | (stage << STAGE_SHIFT)
+    p = _problem(q, v, chunk, subchunk, flags)
+    if reuse_fwd_workspace and workspace is None:
+        raise ValueError("reuse_fwd_workspace needs the workspace the forward used")
+    if out is not None:
+        dq, dkk, dvv, dla, dS0 = (out[n] for n in ("dq", "dk", "dv", "dlog_alpha", "dS0"))
+    else:
+        dq = torch.empty_like(q)
+        dkk = torch.empty_like(k)
+        dvv = torch.empty_like(v)
+        dla = torch.empty_like(log_alpha)
+        dS0 = torch.empty(B, H, dk, dv, dtype=torch.float32, device=q.device) if want_dS0 else None
+    ws = _workspace(p, 1, q.device, workspace)
+    st = lib().gla_chunk_bwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(S0),
+                             _ptr(dO), _ptr(dST), _ptr(dq), _ptr(dkk), _ptr(dvv), _ptr(dla),
+                             _ptr(dS0), _ptr(ws), ws.numel() * ws.element_size(),
+                             _stream(q.device))
+    if st != GLA_OK:
+        raise GlaError(st, "gla_chunk_bwd")
+    return {"dq": dq, "dk": dkk, "dv": dvv, "dlog_alpha": dla, "dS0": dS0}
+
+
+def recurrent_fwd(q, k, v, log_alpha, S0=None, output_final_state=False):
+    """Step-by-step recurrent forward (Eq. 3).  Returns (o, S_T or None)."""
+    _check(q, k, v, log_alpha, states=(("S0", S0),))
+    B, H, T, dk = q.shape
+    dv = v.shape[3]
+    p = _problem(q, v, 16, 16)
+    o = torch.empty_like(v)
+    ST = torch.empty(B, H, dk, dv, dtype=torch.float32, device=q.device) if output_final_state else None
+    st = lib().gla_recurrent_fwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha),
+                                 _ptr(S0), _ptr(o), _ptr(ST), _stream(q.device))
+    if st != GLA_OK:
+        raise GlaError(st, "gla_recurrent_fwd")
+    return o, ST

@@ -1,0 +1,181 @@
+// gla_api.cpp -- the C ABI declared in include/gla.h: argument validation,
+// workspace layout and kernel sequencing.  No device memory is allocated here.
+#include "gla.h"
+
+#include <hip/hip_runtime.h>
+
+#include "gla_launch.hpp"
+
+#define GLA_EXPORT extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+using gla::Shape;
+using gla::Work;
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Validates the problem and fills the internal shape.  The rules are the
+// supported-shape list of include/gla.h.
+gla_status make_shape(const gla_problem *p, Shape &s) {
+  if (!p) return GLA_ERR_NULL;
+  if (p->io != GLA_F32 && p->io != GLA_BF16) return GLA_ERR_DTYPE;
+  if (p->B < 0 || p->H < 0 || p->T < 0 || p->dk <= 0 || p->dv <= 0 || p->chunk <= 0 ||
+      p->subchunk <= 0)
+    return GLA_ERR_SHAPE;
+  if (p->chunk % p->subchunk != 0) return GLA_ERR_SHAPE;
+  if (p->dk % 16 != 0 || p->dv % 16 != 0 || p->dk > 256 || p->dv > 1024) return GLA_ERR_UNSUPPORTED;
+  if (p->chunk != 16 && p->chunk != 32 && p->chunk != 64) return GLA_ERR_UNSUPPORTED;
+  if (16 % p->subchunk != 0) return GLA_ERR_UNSUPPORTED;
+  const int64_t BH = (int64_t)p->B * p->H;
+  if (BH > (1 << 24)) return GLA_ERR_UNSUPPORTED;
+  s.BH = (int)BH;
+  s.T = p->T;
+  s.K = p->dk;
+  s.V = p->dv;
+  s.C = p->chunk;
+  s.c = p->subchunk;
+  s.N = (p->T + p->chunk - 1) / p->chunk;
+  s.io = p->io == GLA_BF16 ? gla::IO_BF16 : gla::IO_F32;
+  if (s.N > 65535) return GLA_ERR_UNSUPPORTED;
+  return GLA_OK;
+}
+
+gla_status check_lds(const Shape &s, bool bwd) {
+  if (gla::lds_prep(s) > gla::kMaxLds || gla::lds_fwd_main(s) > gla::kMaxLds)
+    return GLA_ERR_UNSUPPORTED;
+  if (bwd && (gla::lds_bwd_dq(s) > gla::kMaxLds || gla::lds_bwd_dk(s) > gla::kMaxLds ||
+              gla::lds_bwd_dv(s) > gla::kMaxLds))
+    return GLA_ERR_UNSUPPORTED;
+  return GLA_OK;
+}
+
+// Workspace layout; op 1 extends op 0.  Returns the total byte count and, if
+// base is non-null, the region pointers.
+size_t layout(const Shape &s, int op, char *base, Work *w) {
+  const size_t es = s.esz();
+  const size_t rows = (size_t)s.BH * s.T, chunks = (size_t)s.BH * s.N;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes);
+    return base ? (void *)(base + at) : nullptr;
+  };
+  void *Qt = take(rows * s.K * es);
+  void *Kt = take(rows * s.K * es);
+  void *P = take(chunks * s.C * s.C * es);
+  void *gam = take(chunks * s.K * sizeof(float));
+  void *dP = nullptr, *cST = nullptr, *dq_lo = nullptr;
+  if (op == 1) {
+    dP = take(chunks * s.C * s.C * sizeof(float));
+    cST = take((size_t)s.BH * s.K * sizeof(float));
+    if (s.io == gla::IO_BF16) dq_lo = take(rows * s.K * 2);
+  }
+  if (w) {
+    w->Qt = Qt; w->Kt = Kt; w->P = P; w->gam = (float *)gam;
+    w->dP = (float *)dP; w->cST = (float *)cST; w->dq_lo = dq_lo;
+  }
+  return off;
+}
+
+gla_status hip_status(hipError_t e) { return e == hipSuccess ? GLA_OK : GLA_ERR_HIP; }
+
+}  // namespace
+
+GLA_EXPORT const char *gla_status_string(gla_status st) {
+  switch (st) {
+    case GLA_OK: return "GLA_OK";
+    case GLA_ERR_NULL: return "GLA_ERR_NULL: a required pointer is NULL";
+    case GLA_ERR_SHAPE: return "GLA_ERR_SHAPE: a dimension is negative or inconsistent";
+    case GLA_ERR_DTYPE: return "GLA_ERR_DTYPE: unknown io dtype";
+    case GLA_ERR_UNSUPPORTED: return "GLA_ERR_UNSUPPORTED: shape outside what the kernels implement";
+    case GLA_ERR_WORKSPACE: return "GLA_ERR_WORKSPACE: workspace NULL or too small";
+    case GLA_ERR_HIP: return "GLA_ERR_HIP: a HIP call or kernel launch failed";
+  }
+  return "GLA_ERR_UNKNOWN";
+}
+
+GLA_EXPORT size_t gla_workspace_bytes(const gla_problem *prob, int op) {
+  Shape s;
+  if (make_shape(prob, s) != GLA_OK || (op != 0 && op != 1)) return 0;
+  return layout(s, op, nullptr, nullptr);
+}
+
+GLA_EXPORT gla_status gla_chunk_fwd(const gla_problem *prob, const void *q, const void *k,
+                                    const void *v, const void *log_alpha, const float *S0,
+                                    void *o, float *S_T, void *workspace, size_t workspace_bytes,
+                                    void *stream) {
+  Shape s;
+  gla_status st = make_shape(prob, s);
+  if (st != GLA_OK) return st;
+  if ((st = check_lds(s, false)) != GLA_OK) return st;
+  const unsigned stage = (prob->flags & GLA_STAGE_MASK) >> GLA_STAGE_SHIFT;
+  if (stage > 2) return GLA_ERR_SHAPE;
+  const bool any = (int64_t)s.BH * s.T > 0;
+  if (any && (!q || !k || !v || !log_alpha || !o)) return GLA_ERR_NULL;
+  const size_t need = layout(s, 0, nullptr, nullptr);
+  if (any && (!workspace || workspace_bytes < need)) return GLA_ERR_WORKSPACE;
+  hipStream_t hs = (hipStream_t)stream;
+  if (s.BH == 0) return GLA_OK;
+  if (s.T == 0)
+    return hip_status(gla::launch_copy_state((int64_t)s.BH * s.K * s.V, S0, S_T, hs));
+  Work w;
+  layout(s, 0, (char *)workspace, &w);
+  hipError_t e = hipSuccess;
+  if (stage == 0 || stage == 1) e = gla::launch_prep(s, q, k, log_alpha, w, hs);
+  if (e == hipSuccess && (stage == 0 || stage == 2)) e = gla::launch_fwd_main(s, v, S0, o, S_T, w, hs);
+  return hip_status(e);
+}
+
+GLA_EXPORT gla_status gla_chunk_bwd(const gla_problem *prob, const void *q, const void *k,
+                                    const void *v, const void *log_alpha, const float *S0,
+                                    const void *dO, const float *dS_T, void *dq, void *dk,
+                                    void *dv, void *dlog_alpha, float *dS0, void *workspace,
+                                    size_t workspace_bytes, void *stream) {
+  Shape s;
+  gla_status st = make_shape(prob, s);
+  if (st != GLA_OK) return st;
+  if ((st = check_lds(s, true)) != GLA_OK) return st;
+  const unsigned stage = (prob->flags & GLA_STAGE_MASK) >> GLA_STAGE_SHIFT;
+  if (stage > 4) return GLA_ERR_SHAPE;
+  const bool any = (int64_t)s.BH * s.T > 0;
+  if (any && (!q || !k || !v || !log_alpha || !dO || !dq || !dk || !dv || !dlog_alpha))
+    return GLA_ERR_NULL;
+  const size_t need = layout(s, 1, nullptr, nullptr);
+  if (any && (!workspace || workspace_bytes < need)) return GLA_ERR_WORKSPACE;
+  hipStream_t hs = (hipStream_t)stream;
+  if (s.BH == 0) return GLA_OK;
+  if (s.T == 0)
+    return hip_status(gla::launch_copy_state((int64_t)s.BH * s.K * s.V, dS_T, dS0, hs));
+  auto run = [stage](unsigned k) { return stage == 0 || stage == k; };
+  Work w;
+  layout(s, 1, (char *)workspace, &w);
+  hipError_t e = hipSuccess;
+  if (run(1) && !(prob->flags & GLA_FLAG_REUSE_FWD_WORKSPACE))
+    e = gla::launch_prep(s, q, k, log_alpha, w, hs);
+  if (e == hipSuccess && run(2)) e = gla::launch_bwd_dq(s, k, log_alpha, v, S0, dO, dS_T, dq, w, hs);
+  if (e == hipSuccess && run(3))
+    e = gla::launch_bwd_dk(s, q, k, log_alpha, v, dO, dS_T, dq, dk, dlog_alpha, w, hs);
+  if (e == hipSuccess && run(4)) e = gla::launch_bwd_dv(s, dO, dS_T, dv, dS0, w, hs);
+  return hip_status(e);
+}
+
+GLA_EXPORT gla_status gla_recurrent_fwd(const gla_problem *prob, const void *q, const void *k,
+                                        const void *v, const void *log_alpha, const float *S0,
+                                        void *o, float *S_T, void *stream) {
+  if (!prob) return GLA_ERR_NULL;
+  gla_problem p = *prob;
+  p.chunk = 16;  // the recurrent form ignores the chunk fields
+  p.subchunk = 16;
+  Shape s;
+  gla_status st = make_shape(&p, s);
+  if (st != GLA_OK) return st;
+  const bool any = (int64_t)s.BH * s.T > 0;
+  if (any && (!q || !k || !v || !log_alpha || !o)) return GLA_ERR_NULL;
+  hipStream_t hs = (hipStream_t)stream;
+  if (s.BH == 0) return GLA_OK;
+  if (s.T == 0)
+    return hip_status(gla::launch_copy_state((int64_t)s.BH * s.K * s.V, S0, S_T, hs));
+  return hip_status(gla::launch_recurrent(s, q, k, v, log_alpha, S0, o, S_T, hs));
+}

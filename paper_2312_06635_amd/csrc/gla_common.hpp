@@ -1,0 +1,230 @@
+// gla_common.hpp -- device building blocks shared by the GLA kernels (gfx950).
+//
+// Matrix-core tiles are 16x16 outputs with a 32-deep reduction per step:
+//   bf16 : one v_mfma_f32_16x16x32_bf16
+//   fp32 : eight v_mfma_f32_16x16x4_f32 (so the fp32 path never rounds to bf16)
+// A "fragment" is the 8 reduction-slot values one lane contributes.  For lane
+// l = 16 g + j (g = l / 16 in 0..3, j = l % 16):
+//   A operand : row j of the 16-row tile, reduction slots 8g .. 8g+7
+//   B operand : column j of the tile,    reduction slots 8g .. 8g+7
+//   D (acc)   : column j, rows 4g .. 4g+3 (4 fp32 per lane)
+// Any slot-to-index mapping is valid as long as A and B agree; the state
+// accumulators use the "permuted" mapping that a 16x16 accumulator pair
+// provides directly (see acc_frag / ld_row_perm).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gla {
+
+typedef __bf16 bf16;
+typedef bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef float f8 __attribute__((ext_vector_type(8)));
+typedef short s4 __attribute__((ext_vector_type(4)));
+typedef short s8 __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) s4 lds_s4;
+
+template <typename T> struct Mma;
+
+template <> struct Mma<bf16> {
+  using frag = bf16x8;
+  static __device__ __forceinline__ f4 mma(f4 c, frag a, frag b) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+};
+
+template <> struct Mma<float> {
+  using frag = f8;
+  static __device__ __forceinline__ f4 mma(f4 c, frag a, frag b) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[i], c, 0, 0, 0);
+    return c;
+  }
+};
+
+template <typename T> using frag_t = typename Mma<T>::frag;
+
+template <typename T> __device__ __forceinline__ f4 mma(f4 c, frag_t<T> a, frag_t<T> b) {
+  return Mma<T>::mma(c, a, b);
+}
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+__device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
+
+template <typename T> __device__ __forceinline__ T cvt(float x);
+template <> __device__ __forceinline__ float cvt<float>(float x) { return x; }
+template <> __device__ __forceinline__ bf16 cvt<bf16>(float x) { return (bf16)x; }
+
+__device__ __forceinline__ f4 zero4() { return f4{0.f, 0.f, 0.f, 0.f}; }
+
+// ---------------------------------------------------------------- fragments
+// All loaders read LDS tiles stored row-major with leading dimension `ld`
+// (in elements).
+
+// A/B fragment whose reduction index runs along a row:
+// lane (g, j) gets X[r0 + j][c0 + 8g + i], i = 0..7.
+template <typename T>
+__device__ __forceinline__ frag_t<T> ld_row(const T *X, int ld, int r0, int c0) {
+  const int l = lane_id();
+  const T *p = X + (r0 + (l & 15)) * ld + c0 + 8 * (l >> 4);
+  if constexpr (sizeof(T) == 2) {
+    return *(const bf16x8 *)p;
+  } else {
+    f4 a = *(const f4 *)p, b = *(const f4 *)(p + 4);
+    return f8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  }
+}
+
+// Same, in the permuted slot order of an accumulator pair (see acc_frag):
+// lane (g, j) gets X[r0 + j][c0 + 4g + i] for i < 4 and X[r0 + j][c0 + 16 + 4g + i - 4].
+template <typename T>
+__device__ __forceinline__ frag_t<T> ld_row_perm(const T *X, int ld, int r0, int c0) {
+  const int l = lane_id();
+  const T *p = X + (r0 + (l & 15)) * ld + c0 + 4 * (l >> 4);
+  if constexpr (sizeof(T) == 2) {
+    bf16x4 a = *(const bf16x4 *)p, b = *(const bf16x4 *)(p + 16);
+    return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  } else {
+    f4 a = *(const f4 *)p, b = *(const f4 *)(p + 16);
+    return f8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  }
+}
+
+// Fragment whose reduction index runs down a column (a transposed read):
+// lane (g, j) gets X[r0 + 8g + i][c0 + j], i = 0..7.  For bf16 this is two
+// gfx950 LDS transpose reads: with lane j of a 16-lane group pointing at
+// X[R + j/4][c0 + 4 (j%4)], ds_read_b64_tr_b16 returns X[R + m][c0 + j],
+// m = 0..3, to lane j.
+template <typename T>
+__device__ __forceinline__ frag_t<T> ld_col(const T *X, int ld, int r0, int c0) {
+  const int l = lane_id(), g = l >> 4, j = l & 15;
+  if constexpr (sizeof(T) == 2) {
+    const T *p0 = X + (r0 + 8 * g + (j >> 2)) * ld + c0 + 4 * (j & 3);
+    const T *p1 = p0 + 4 * ld;
+    s4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4 *)(p0));
+    s4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4 *)(p1));
+    s8 r = s8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    return __builtin_bit_cast(bf16x8, r);
+  } else {
+    const T *p = X + (r0 + 8 * g) * ld + c0 + j;
+    f8 r;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) r[i] = p[i * ld];
+    return r;
+  }
+}
+
+// Column fragment read from an fp32 tile, converted to T.
+template <typename T>
+__device__ __forceinline__ frag_t<T> ld_col_f32(const float *X, int ld, int r0, int c0) {
+  const int l = lane_id();
+  const float *p = X + (r0 + 8 * (l >> 4)) * ld + c0 + (l & 15);
+  frag_t<T> r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r[i] = cvt<T>(p[i * ld]);
+  return r;
+}
+
+// Row fragment read from an fp32 tile, converted to T.
+template <typename T>
+__device__ __forceinline__ frag_t<T> ld_row_f32(const float *X, int ld, int r0, int c0) {
+  const int l = lane_id();
+  const float *p = X + (r0 + (l & 15)) * ld + c0 + 8 * (l >> 4);
+  f4 a = *(const f4 *)p, b = *(const f4 *)(p + 4);
+  frag_t<T> r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    r[i] = cvt<T>(a[i]);
+    r[4 + i] = cvt<T>(b[i]);
+  }
+  return r;
+}
+
+// B (or A) fragment taken straight from two stacked 16x16 accumulators
+// lo = rows [0,16), hi = rows [16,32) of a 32-row slab: lane (g, j) holds
+// rows 4g..4g+3 of column j in each, which become slots 0..3 and 4..7.
+// The matching operand must be read with ld_row_perm.
+template <typename T> __device__ __forceinline__ frag_t<T> acc_frag(f4 lo, f4 hi) {
+  frag_t<T> r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    r[i] = cvt<T>(lo[i]);
+    r[4 + i] = cvt<T>(hi[i]);
+  }
+  return r;
+}
+
+// ---------------------------------------------------------------- staging
+// Cooperative copy of a [rows x cols] tile from global memory (leading
+// dimension gld) into LDS (leading dimension lld).  Rows >= rv or columns
+// >= cv are filled with zeros; `cols` must be a multiple of 16 / sizeof(T)
+// and both leading dimensions keep 16-byte alignment.
+template <typename T>
+__device__ __forceinline__ void stage_tile(T *dst, int lld, const T *src, int64_t gld, int rows,
+                                           int cols, int rv, int cv) {
+  constexpr int EV = 16 / sizeof(T);
+  const int vpr = cols / EV;
+  const int total = rows * vpr;
+  for (int idx = threadIdx.x; idx < total; idx += blockDim.x) {
+    const int r = idx / vpr, c = (idx - r * vpr) * EV;
+    uint4 val = make_uint4(0, 0, 0, 0);
+    if (r < rv && c < cv) val = *(const uint4 *)(src + (int64_t)r * gld + c);
+    *(uint4 *)(dst + r * lld + c) = val;
+  }
+}
+
+// Register-staged tile copy for software pipelining: load() issues this
+// thread's share of a [rows x cols] tile as 16-byte global loads into
+// registers (rows >= rv or columns >= cv read as zero) without waiting for
+// them; store() later writes the registers into LDS.  Issuing the loads of
+// chunk n+1 right after the barrier that publishes chunk n lets their latency
+// overlap the compute of chunk n.  NV bounds the vectors per thread for a
+// 256-thread workgroup.
+template <typename T, int NV> struct TileRegs {
+  uint4 r[NV];
+  __device__ __forceinline__ void load(const T *src, int64_t gld, int rows, int cols, int rv, int cv) {
+    constexpr int EV = 16 / sizeof(T);
+    const int vpr = cols / EV, total = rows * vpr;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int idx = threadIdx.x + i * 256;
+      r[i] = make_uint4(0, 0, 0, 0);
+      if (idx < total) {
+        const int row = idx / vpr, c = (idx - row * vpr) * EV;
+        if (row < rv && c < cv) r[i] = *(const uint4 *)(src + row * gld + c);
+      }
+    }
+  }
+  __device__ __forceinline__ void store(T *dst, int lld, int rows, int cols) const {
+    constexpr int EV = 16 / sizeof(T);
+    const int vpr = cols / EV, total = rows * vpr;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int idx = threadIdx.x + i * 256;
+      if (idx < total) {
+        const int row = idx / vpr, c = (idx - row * vpr) * EV;
+        *(uint4 *)(dst + row * lld + c) = r[i];
+      }
+    }
+  }
+};
+
+// XCD-aware block mapping: consecutive workgroup ids are dealt round-robin to
+// the 8 XCDs, so when the head count is a multiple of 8 the tiles of one head
+// are all given ids with the same residue mod 8 (one XCD, one L2), letting
+// them share the head's per-chunk operands through that L2.
+__device__ __forceinline__ void xcd_map(int nheads, int ntiles, int &head, int &tile) {
+  const int id = blockIdx.x;
+  if ((nheads & 7) == 0) {
+    const int xcd = id & 7, s = id >> 3;
+    tile = s % ntiles;
+    head = (s / ntiles) * 8 + xcd;
+  } else {
+    head = id / ntiles;
+    tile = id - head * ntiles;
+  }
+}
+
+}  // namespace gla

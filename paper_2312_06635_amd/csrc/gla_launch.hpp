@@ -1,0 +1,58 @@
+// gla_launch.hpp -- internal interface between the C-ABI layer and the kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace gla {
+
+enum Io { IO_F32 = 0, IO_BF16 = 1 };
+
+// One validated problem.  N = number of chunks (the last may be shorter).
+struct Shape {
+  int BH, T, K, V, C, c, N;
+  int io;
+  int esz() const { return io == IO_BF16 ? 2 : 4; }
+};
+
+// Device workspace regions (see gla_api.cpp for the layout).
+struct Work {
+  void *Qt = nullptr;     // [BH][T][K] io : q (.) Lambda   (Lambda = b_t / b_{chunk start})
+  void *Kt = nullptr;     // [BH][T][K] io : k (.) Gamma    (Gamma  = b_{chunk end} / b_t)
+  void *P = nullptr;      // [BH][N][C][C] io : intra-chunk matrix, lower triangle
+  float *gam = nullptr;   // [BH][N][K] fp32 : chunk decay gamma = b_{chunk end} / b_{chunk start}
+  float *dP = nullptr;    // [BH][N][C][C] fp32 : (dO V^T) (.) M per chunk (backward)
+  float *cST = nullptr;   // [BH][K] fp32 : rowsum(S_T (.) dS_T) (backward)
+  void *dq_lo = nullptr;  // [BH][T][K] bf16 : dq - bf16(dq), so dq reaches the gate gradient
+                          //   with ~16 mantissa bits (bf16 io only)
+};
+
+// Returns hipSuccess or the launch error.  Shapes are validated by the caller.
+hipError_t launch_prep(const Shape &s, const void *q, const void *k, const void *la,
+                       const Work &w, hipStream_t st);
+hipError_t launch_fwd_main(const Shape &s, const void *v, const float *S0, void *o, float *ST,
+                           const Work &w, hipStream_t st);
+hipError_t launch_bwd_dq(const Shape &s, const void *k, const void *la, const void *v,
+                         const float *S0, const void *dO, const float *dST, void *dq,
+                         const Work &w, hipStream_t st);
+hipError_t launch_bwd_dk(const Shape &s, const void *q, const void *k, const void *la,
+                         const void *v, const void *dO, const float *dST, const void *dq,
+                         void *dk, void *dla, const Work &w, hipStream_t st);
+// (bwd_dq also writes w.dq_lo; bwd_dk reads it)
+hipError_t launch_bwd_dv(const Shape &s, const void *dO, const float *dST, void *dv, float *dS0,
+                         const Work &w, hipStream_t st);
+hipError_t launch_recurrent(const Shape &s, const void *q, const void *k, const void *v,
+                            const void *la, const float *S0, void *o, float *ST, hipStream_t st);
+// T == 0 edge: S_T = S0 (or 0); dS0 = dS_T (or 0).
+hipError_t launch_copy_state(int64_t n, const float *src, float *dst, hipStream_t st);
+
+// LDS bytes each kernel needs (0 means the shape is not supported).
+size_t lds_prep(const Shape &s);
+size_t lds_fwd_main(const Shape &s);
+size_t lds_bwd_dq(const Shape &s);
+size_t lds_bwd_dk(const Shape &s);
+size_t lds_bwd_dv(const Shape &s);
+
+constexpr size_t kMaxLds = 160 * 1024;
+
+}  // namespace gla

@@ -1,0 +1,315 @@
+// gla_prep.hip -- per-chunk gate factors, gated operands and the intra-chunk
+// matrix P of the chunkwise GLA form (paper Sec. 4.2 and 4.3).
+//
+// One workgroup per (chunk, head); wave w owns the 16-row block w of the
+// chunk and each lane owns the features k = lane + 64 f.  With B the
+// chunk-local inclusive cumsum of log alpha (so exp(B) = b_t / b_{chunk start}):
+//   Qt    = q (.) exp(B)              (Q (.) Lambda)
+//   Kt    = k (.) exp(B_last - B)      (K (.) Gamma)
+//   gamma = exp(B_last)                (chunk decay)
+//   P[i][j] = sum_k q_ik k_jk exp(B_ik - B_jk) for j <= i, else 0  (Eq. 4)
+// P is tiled in 16x16 blocks (I, J):
+//   * I > J ("orange", between sub-chunks): a matrix-core product of operands
+//     normalised at block boundaries, so that every exponent is <= 0:
+//       (q_I (.) exp(B - z_I)) diag(exp(z_I - zend_J)) (k_J (.) exp(zend_J - B))^T
+//     with z_I the log decay at the start of block I and zend_J at the end of J.
+//   * I = J ("pink", inside a sub-chunk): fp32 on the vector ALUs, no matrix
+//     cores.  The pairwise decay exp(B_i - B_j) is split at the block start as
+//     exp(B_i - z) exp(z - B_j); the second factor grows with the block's own
+//     decay, so when that exceeds exp(kWideRange) for any feature the block
+//     falls back to one exponential per (i, j, k) triple.
+// Sub-chunks shorter than 16 (c < 16) lie inside the diagonal blocks and are
+// therefore evaluated in fp32 too.
+#include "gla_common.hpp"
+#include "gla_launch.hpp"
+
+namespace gla {
+
+constexpr float kWideRange = 60.0f;
+
+struct PrepArgs {
+  const void *q, *k, *la;
+  void *Qt, *Kt, *P;
+  float *gam;
+  int T, K, Kp, C, N, ldk;
+};
+
+// Entry e of a 16x16 lower triangle (diagonal included), row-major.
+__host__ __device__ constexpr int tri_row(int e) {
+  int i = 0;
+  while ((i + 1) * (i + 2) / 2 <= e) ++i;
+  return i;
+}
+__host__ __device__ constexpr int tri_col(int e) { return e - tri_row(e) * (tri_row(e) + 1) / 2; }
+
+// Reduce-scatter across the 64 lanes of a wave: on return, lane l holds the
+// sum over all lanes of x[l].
+template <int H> __device__ __forceinline__ void rs_step(float (&x)[64], int l) {
+  const bool up = (l & H) != 0;
+#pragma unroll
+  for (int e = 0; e < H; ++e) {
+    const float send = up ? x[e] : x[e + H];
+    const float keep = up ? x[e + H] : x[e];
+    x[e] = keep + __shfl_xor(send, H);
+  }
+}
+__device__ __forceinline__ float reduce_scatter64(float (&x)[64]) {
+  const int l = lane_id();
+  rs_step<32>(x, l);
+  rs_step<16>(x, l);
+  rs_step<8>(x, l);
+  rs_step<4>(x, l);
+  rs_step<2>(x, l);
+  rs_step<1>(x, l);
+  return x[0];
+}
+
+__device__ __forceinline__ float allreduce64(float x) {
+#pragma unroll
+  for (int h = 32; h >= 1; h >>= 1) x += __shfl_xor(x, h);
+  return x;
+}
+
+// Pair index of the non-adjacent block pairs (I, J), J <= I - 2, for C <= 64.
+__device__ __forceinline__ int pair_index(int I, int J) { return I == 2 ? 0 : (J == 0 ? 1 : 2); }
+
+template <typename T, int FPL>
+__global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int n = blockIdx.x, bh = blockIdx.y;
+  const int w = wave_id(), l = lane_id(), g = l >> 4, j16 = l & 15;
+  const int C = a.C, K = a.K, Kp = a.Kp, nb = C >> 4, ldk = a.ldk;
+  const int t0 = n * C;
+  const int rv = min(C, a.T - t0);
+  const int64_t base = ((int64_t)bh * a.T + t0) * K;
+  T *sQh = (T *)smem;
+  T *sKs = sQh + C * ldk;
+  float *sTot = (float *)(sKs + C * ldk);  // [nb][Kp] per-block sums of log alpha
+  float *sG = sTot + 4 * Kp;              // [3][Kp] exp(sum of tot strictly between I and J)
+
+  const T *q = (const T *)a.q + base, *k = (const T *)a.k + base, *la = (const T *)a.la + base;
+  T *Qt = (T *)a.Qt + base, *Kt = (T *)a.Kt + base;
+  T *Pg = (T *)a.P + ((int64_t)bh * a.N + n) * C * C;
+
+  // 1. block-local cumsum of log alpha.
+  float Bloc[16][FPL], tot[FPL];
+#pragma unroll
+  for (int f = 0; f < FPL; ++f) {
+    const int kf = l + 64 * f;
+    float c = 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = 16 * w + r;
+      c += (row < rv && kf < K) ? (float)la[row * K + kf] : 0.f;
+      Bloc[r][f] = c;
+    }
+    tot[f] = c;
+    if (kf < Kp) sTot[w * Kp + kf] = c;
+  }
+  __syncthreads();
+
+  float pre[FPL], Bl[FPL];
+#pragma unroll
+  for (int f = 0; f < FPL; ++f) {
+    const int kf = l + 64 * f;
+    pre[f] = 0.f;
+    Bl[f] = 0.f;
+    if (kf < Kp) {
+      for (int w2 = 0; w2 < nb; ++w2) {
+        const float t = sTot[w2 * Kp + kf];
+        if (w2 < w) pre[f] += t;
+        Bl[f] += t;
+      }
+      if (w == 2) sG[0 * Kp + kf] = __expf(sTot[1 * Kp + kf]);
+      if (w == 3) {
+        sG[1 * Kp + kf] = __expf(sTot[1 * Kp + kf] + sTot[2 * Kp + kf]);
+        sG[2 * Kp + kf] = __expf(sTot[2 * Kp + kf]);
+      }
+    }
+  }
+
+  // 2. gated operands.
+  float qh[16][FPL], kh[16][FPL];
+  bool wide = false;
+#pragma unroll
+  for (int f = 0; f < FPL; ++f) {
+    const int kf = l + 64 * f;
+    const bool fv = kf < K;
+    const float ez = __expf(pre[f]);                  // b_{block start} / b_{chunk start}
+    const float ekt = __expf(Bl[f] - pre[f] - tot[f]);  // b_{chunk end} / b_{block end}
+    const float eup = __expf(-tot[f]);                // b_{block start} / b_{block end} >= 1
+    if (fv && -tot[f] > kWideRange) wide = true;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = 16 * w + r;
+      const bool ok = fv && row < rv;
+      const float qv = ok ? (float)q[row * K + kf] : 0.f;
+      const float kv = ok ? (float)k[row * K + kf] : 0.f;
+      const float qhv = qv * __expf(Bloc[r][f]);            // <= |q|
+      const float ksv = kv * __expf(tot[f] - Bloc[r][f]);   // <= |k|
+      qh[r][f] = qhv;
+      kh[r][f] = ksv * eup;
+      if (ok) {
+        Qt[row * K + kf] = cvt<T>(qhv * ez);
+        Kt[row * K + kf] = cvt<T>(ksv * ekt);
+      }
+      if (kf < Kp) {
+        sQh[row * ldk + kf] = cvt<T>(qhv);
+        sKs[row * ldk + kf] = cvt<T>(ksv);
+      }
+    }
+    if (w == 0 && fv) a.gam[((int64_t)bh * a.N + n) * K + kf] = __expf(Bl[f]);
+  }
+
+  // 3. diagonal ("pink") block w in fp32.
+  const int d0 = 16 * w;
+  {
+    float x[64];
+    float r0, r1, rt = 0.f;
+    if (!__any(wide)) {
+#pragma unroll
+      for (int e = 0; e < 64; ++e) {
+        float s = 0.f;
+#pragma unroll
+        for (int f = 0; f < FPL; ++f) s += qh[tri_row(e)][f] * kh[tri_col(e)][f];
+        x[e] = s;
+      }
+      r0 = reduce_scatter64(x);
+#pragma unroll
+      for (int e = 0; e < 64; ++e) {
+        float s = 0.f;
+#pragma unroll
+        for (int f = 0; f < FPL; ++f) s += qh[tri_row(64 + e)][f] * kh[tri_col(64 + e)][f];
+        x[e] = s;
+      }
+      r1 = reduce_scatter64(x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float s = 0.f;
+#pragma unroll
+        for (int f = 0; f < FPL; ++f) s += qh[tri_row(128 + e)][f] * kh[tri_col(128 + e)][f];
+        s = allreduce64(s);
+        if (l == e) rt = s;
+      }
+    } else {
+      // Large decay inside the block: one exponential per (i, j, k).
+      float qv[16][FPL], kv[16][FPL], Bv[16][FPL];
+#pragma unroll
+      for (int f = 0; f < FPL; ++f) {
+        const int kf = l + 64 * f;
+        float c = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = d0 + r;
+          const bool ok = kf < K && row < rv;
+          c += ok ? (float)la[row * K + kf] : 0.f;
+          Bv[r][f] = c;
+          qv[r][f] = ok ? (float)q[row * K + kf] : 0.f;
+          kv[r][f] = ok ? (float)k[row * K + kf] : 0.f;
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < 64; ++e) {
+        float s = 0.f;
+        const int i = tri_row(e), jj = tri_col(e);
+#pragma unroll
+        for (int f = 0; f < FPL; ++f) s += qv[i][f] * kv[jj][f] * __expf(Bv[i][f] - Bv[jj][f]);
+        x[e] = s;
+      }
+      r0 = reduce_scatter64(x);
+#pragma unroll
+      for (int e = 0; e < 64; ++e) {
+        float s = 0.f;
+        const int i = tri_row(64 + e), jj = tri_col(64 + e);
+#pragma unroll
+        for (int f = 0; f < FPL; ++f) s += qv[i][f] * kv[jj][f] * __expf(Bv[i][f] - Bv[jj][f]);
+        x[e] = s;
+      }
+      r1 = reduce_scatter64(x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float s = 0.f;
+        const int i = tri_row(128 + e), jj = tri_col(128 + e);
+#pragma unroll
+        for (int f = 0; f < FPL; ++f) s += qv[i][f] * kv[jj][f] * __expf(Bv[i][f] - Bv[jj][f]);
+        s = allreduce64(s);
+        if (l == e) rt = s;
+      }
+    }
+    Pg[(d0 + tri_row(l)) * C + d0 + tri_col(l)] = cvt<T>(r0);
+    Pg[(d0 + tri_row(64 + l)) * C + d0 + tri_col(64 + l)] = cvt<T>(r1);
+    if (l < 8) Pg[(d0 + tri_row(128 + l)) * C + d0 + tri_col(128 + l)] = cvt<T>(rt);
+    // zeros: strict upper triangle of the diagonal block and every block J > w
+    {
+      const int i = l >> 2;
+#pragma unroll
+      for (int c4 = 0; c4 < 4; ++c4) {
+        const int jj = 4 * (l & 3) + c4;
+        if (jj > i) Pg[(d0 + i) * C + d0 + jj] = cvt<T>(0.f);
+      }
+      for (int idx = l; idx < 16 * (C - d0 - 16); idx += 64) {
+        const int rr = idx / (C - d0 - 16), cc = idx - rr * (C - d0 - 16);
+        Pg[(d0 + rr) * C + d0 + 16 + cc] = cvt<T>(0.f);
+      }
+    }
+  }
+  __syncthreads();
+
+  // 4. off-diagonal ("orange") blocks (w, J < w) on the matrix cores.
+  for (int J = 0; J < w; ++J) {
+    f4 acc = zero4();
+    for (int s = 0; s < Kp / 32; ++s) {
+      frag_t<T> af = ld_row(sQh, ldk, d0, 32 * s);
+      if (J <= w - 2) {
+        const float *gp = sG + pair_index(w, J) * Kp + 32 * s + 8 * g;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) af[i] = cvt<T>((float)af[i] * gp[i]);
+      }
+      frag_t<T> bf = ld_row(sKs, ldk, 16 * J, 32 * s);
+      acc = mma<T>(acc, af, bf);
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) Pg[(d0 + 4 * g + r) * C + 16 * J + j16] = cvt<T>(acc[r]);
+  }
+}
+
+static int round_up(int x, int m) { return (x + m - 1) / m * m; }
+
+size_t lds_prep(const Shape &s) {
+  const int Kp = round_up(s.K, 32), ldk = Kp + 32 / s.esz();
+  return (size_t)2 * s.C * ldk * s.esz() + (size_t)7 * Kp * sizeof(float);
+}
+
+template <typename T, int FPL>
+static hipError_t launch_prep_t(const Shape &s, const PrepArgs &a, size_t lds, hipStream_t st) {
+  static bool attr = false;
+  if (!attr) {
+    hipFuncSetAttribute((const void *)prep_kernel<T, FPL>,
+                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    attr = true;
+  }
+  dim3 grid(s.N, s.BH), block(64 * (s.C / 16));
+  hipLaunchKernelGGL((prep_kernel<T, FPL>), grid, block, lds, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_prep(const Shape &s, const void *q, const void *k, const void *la,
+                       const Work &w, hipStream_t st) {
+  PrepArgs a;
+  a.q = q; a.k = k; a.la = la;
+  a.Qt = w.Qt; a.Kt = w.Kt; a.P = w.P; a.gam = w.gam;
+  a.T = s.T; a.K = s.K; a.Kp = round_up(s.K, 32); a.C = s.C; a.N = s.N;
+  a.ldk = a.Kp + 32 / s.esz();
+  const size_t lds = lds_prep(s);
+  const int fpl = (s.K + 63) / 64;
+  if (s.io == IO_BF16) {
+    if (fpl == 1) return launch_prep_t<bf16, 1>(s, a, lds, st);
+    if (fpl == 2) return launch_prep_t<bf16, 2>(s, a, lds, st);
+    return launch_prep_t<bf16, 4>(s, a, lds, st);
+  }
+  if (fpl == 1) return launch_prep_t<float, 1>(s, a, lds, st);
+  if (fpl == 2) return launch_prep_t<float, 2>(s, a, lds, st);
+  return launch_prep_t<float, 4>(s, a, lds, st);
+}
+
+}  // namespace gla

@@ -1,0 +1,131 @@
+"""The C-ABI library: it loads, exports every symbol include/gla.h declares (and
+nothing else), and rejects bad arguments before touching the device.  CPU only:
+no call here reaches a kernel launch."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2312_06635_amd as gla
+from paper_2312_06635_amd import build as glabuild
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gla.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(gla.library_path):
+        glabuild.build()
+    return gla.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(gla_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    assert declared_functions() == ["gla_chunk_bwd", "gla_chunk_fwd", "gla_recurrent_fwd",
+                                    "gla_status_string", "gla_workspace_bytes"]
+
+
+def test_every_declared_symbol_is_exported(L):
+    for name in declared_functions():
+        assert hasattr(L, name), name
+
+
+def test_only_the_boundary_is_exported(L):
+    out = subprocess.run(["nm", "-D", "--defined-only", gla.library_path], capture_output=True,
+                         text=True, check=True).stdout
+    syms = {line.split()[-1] for line in out.splitlines() if " T " in line}
+    assert set(declared_functions()) <= syms
+    assert not [s for s in syms if s.startswith("gla_") and s not in declared_functions()]
+
+
+def test_status_strings(L):
+    for code in range(7):
+        s = L.gla_status_string(code).decode()
+        assert s.startswith("GLA_OK" if code == 0 else "GLA_ERR")
+    assert L.gla_status_string(99).decode() == "GLA_ERR_UNKNOWN"
+
+
+def P(**kw):
+    base = dict(B=2, H=3, T=200, dk=64, dv=128, chunk=64, subchunk=16, io=gla.GLA_BF16, flags=0)
+    base.update(kw)
+    return gla.GlaProblem(**base)
+
+
+def test_workspace_bytes(L):
+    p = P()
+    fwd = L.gla_workspace_bytes(ctypes.byref(p), 0)
+    bwd = L.gla_workspace_bytes(ctypes.byref(p), 1)
+    BH, T, K, C, N = 6, 200, 64, 64, 4
+    assert fwd >= 2 * BH * T * K * 2 + BH * N * C * C * 2 + BH * N * K * 4
+    assert bwd >= fwd + BH * N * C * C * 4
+    assert fwd % 256 == 0 and bwd % 256 == 0
+    p32 = P(io=gla.GLA_F32)
+    assert L.gla_workspace_bytes(ctypes.byref(p32), 0) > fwd
+    assert L.gla_workspace_bytes(ctypes.byref(p), 2) == 0
+    assert L.gla_workspace_bytes(None, 0) == 0
+    assert L.gla_workspace_bytes(ctypes.byref(P(dk=24)), 0) == 0
+
+
+def fwd_call(L, p, ptr=1, ws=1, ws_bytes=1 << 40):
+    return L.gla_chunk_fwd(ctypes.byref(p) if p is not None else None, ptr, ptr, ptr, ptr, None,
+                           ptr, None, ws, ws_bytes, None)
+
+
+def bwd_call(L, p, ptr=1, ws=1, ws_bytes=1 << 40):
+    return L.gla_chunk_bwd(ctypes.byref(p), ptr, ptr, ptr, ptr, None, ptr, None, ptr, ptr, ptr,
+                           ptr, None, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(io=7), gla.GLA_ERR_DTYPE),
+    (dict(T=-1), gla.GLA_ERR_SHAPE),
+    (dict(B=-2), gla.GLA_ERR_SHAPE),
+    (dict(dk=0), gla.GLA_ERR_SHAPE),
+    (dict(chunk=64, subchunk=48), gla.GLA_ERR_SHAPE),
+    (dict(dk=24), gla.GLA_ERR_UNSUPPORTED),
+    (dict(dk=272), gla.GLA_ERR_UNSUPPORTED),
+    (dict(dv=2048), gla.GLA_ERR_UNSUPPORTED),
+    (dict(chunk=128, subchunk=16), gla.GLA_ERR_UNSUPPORTED),
+    (dict(chunk=64, subchunk=32), gla.GLA_ERR_UNSUPPORTED),
+    (dict(io=gla.GLA_F32, dk=256), gla.GLA_ERR_UNSUPPORTED),
+])
+def test_invalid_problems_are_rejected(L, kw, code):
+    assert fwd_call(L, P(**kw)) == code
+    assert bwd_call(L, P(**kw)) == code
+
+
+def test_null_problem_and_pointers(L):
+    assert fwd_call(L, None) == gla.GLA_ERR_NULL
+    assert fwd_call(L, P(), ptr=None) == gla.GLA_ERR_NULL
+    assert bwd_call(L, P(), ptr=None) == gla.GLA_ERR_NULL
+    p = P()
+    assert L.gla_recurrent_fwd(None, 1, 1, 1, 1, None, 1, None, None) == gla.GLA_ERR_NULL
+    assert L.gla_recurrent_fwd(ctypes.byref(p), None, 1, 1, 1, None, 1, None, None) == gla.GLA_ERR_NULL
+
+
+def test_workspace_is_checked(L):
+    p = P()
+    need = L.gla_workspace_bytes(ctypes.byref(p), 0)
+    assert fwd_call(L, p, ws=None) == gla.GLA_ERR_WORKSPACE
+    assert fwd_call(L, p, ws_bytes=need - 1) == gla.GLA_ERR_WORKSPACE
+    needb = L.gla_workspace_bytes(ctypes.byref(p), 1)
+    assert bwd_call(L, p, ws_bytes=needb - 1) == gla.GLA_ERR_WORKSPACE
+
+
+def test_empty_batch_needs_nothing(L):
+    p = P(B=0)
+    assert fwd_call(L, p, ptr=None, ws=None, ws_bytes=0) == gla.GLA_OK
+    assert bwd_call(L, p, ptr=None, ws=None, ws_bytes=0) == gla.GLA_OK
+
+
+def test_stage_selector_is_validated(L):
+    assert fwd_call(L, P(flags=3 << 8)) == gla.GLA_ERR_SHAPE
+    assert bwd_call(L, P(flags=5 << 8)) == gla.GLA_ERR_SHAPE
+    assert fwd_call(L, P(B=0, flags=3 << 8), ptr=None, ws=None, ws_bytes=0) == gla.GLA_ERR_SHAPE

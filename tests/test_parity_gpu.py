@@ -1,0 +1,249 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 CPU oracle.
+
+Bar: per output tensor, max|x - ref| / max|ref| <= 1e-4 for fp32 inputs and
+<= 2e-2 for bf16 inputs (fp32 accumulation).  Small cases compare every
+element; the full-size workloads are run in the benchmark's configuration and
+compared on sampled heads, which the oracle computes exactly (heads are
+independent).  Every input is seeded and synthetic (workloads.py).
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def gla():
+    import paper_2312_06635_amd as m
+    return m
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    gla().lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def rel(x, ref):
+    x = np.asarray(x, np.float64)
+    ref = np.asarray(ref, np.float64)
+    den = np.abs(ref).max() if ref.size else 0.0
+    if den == 0.0:
+        return float(np.abs(x).max()) if x.size else 0.0
+    return float(np.abs(x - ref).max() / den)
+
+
+def to_dev(inp):
+    return {k: (v.cuda() if v is not None else None) for k, v in inp.items()}
+
+
+def heads(t, idx):
+    """[B,H,...] tensor -> float64 numpy of the flat heads idx."""
+    if t is None:
+        return None
+    t = t.detach().float().cpu()
+    return t.reshape(-1, *t.shape[2:])[idx].double().numpy()
+
+
+def run_gpu(inp, chunk, subchunk, want_state, reuse=True):
+    g = gla()
+    d = to_dev(inp)
+    ws = torch.empty(g.workspace_bytes(*d["q"].shape[:3], d["q"].shape[3], d["v"].shape[3], chunk,
+                                       subchunk, d["q"].dtype, op=1), dtype=torch.uint8, device="cuda")
+    o, ST = g.chunk_fwd(d["q"], d["k"], d["v"], d["log_alpha"], chunk, subchunk, S0=d["S0"],
+                        output_final_state=want_state, workspace=ws)
+    gr = g.chunk_bwd(d["q"], d["k"], d["v"], d["log_alpha"], d["dO"], chunk, subchunk, S0=d["S0"],
+                     dST=d["dST"], want_dS0=True, workspace=ws, reuse_fwd_workspace=reuse)
+    torch.cuda.synchronize()
+    return o, ST, gr
+
+
+def compare(inp, o, ST, gr, idx, io, label):
+    tol = TOL[io]
+    q, k, v, la, dO = (heads(inp[n], idx) for n in ("q", "k", "v", "log_alpha", "dO"))
+    S0, dST = heads(inp["S0"], idx), heads(inp["dST"], idx)
+    ro, rST = oracle.fwd(q, k, v, la, S0)
+    rg = oracle.bwd(q, k, v, la, dO, S0=S0, dST=dST)
+    errs = {"o": rel(heads(o, idx), ro)}
+    if ST is not None:
+        errs["S_T"] = rel(heads(ST, idx), rST)
+    for name in ("dq", "dk", "dv", "dlog_alpha", "dS0"):
+        errs[name] = rel(heads(gr[name], idx), rg[name])
+    say(label, {k2: f"{v2:.2e}" for k2, v2 in errs.items()})
+    bad = {k2: v2 for k2, v2 in errs.items() if not v2 <= tol}
+    assert not bad, f"{label}: {bad} > {tol}"
+
+
+def small_case(name, io, B, H, T, dk, dv, chunk, subchunk, seed, **kw):
+    cfg = W._cfg(name, B, H, T, dk, dv, chunk, subchunk, io, seed, gate_mu=kw.get("gate_mu", 0.0),
+                 s0_std=kw.get("s0_std", 0.0))
+    return cfg
+
+
+SMALL = [
+    # exact tiny workload (fp32, C=16, c=8, d_k=16, d_v=32)
+    dict(cfg=W.CONFIGS["tiny_fp32"]),
+    # fp32 through the matrix-core paths: several chunks, ragged tail
+    dict(cfg=small_case("f32_ragged", "f32", 1, 2, 200, 64, 128, 64, 16, 11)),
+    dict(cfg=small_case("f32_C32_c8", "f32", 1, 1, 96, 128, 256, 32, 8, 12)),
+    dict(cfg=small_case("f32_C16_wideV", "f32", 1, 1, 70, 32, 1024, 16, 16, 13)),
+    dict(cfg=small_case("f32_state", "f32", 2, 1, 130, 64, 64, 64, 4, 14, s0_std=0.1),
+         dST_std=0.1),
+    # bf16 at the workload shapes, shorter sequences
+    dict(cfg=small_case("bf16_1p3b", "bf16", 1, 2, 256, 256, 512, 64, 16, 15)),
+    dict(cfg=small_case("bf16_340m", "bf16", 2, 1, 320, 128, 256, 64, 16, 16)),
+    dict(cfg=small_case("bf16_340m_ungated", "bf16", 2, 1, 320, 128, 256, 64, 16, 16),
+         alpha_one=True),
+    dict(cfg=small_case("bf16_long", "bf16", 1, 2, 640, 256, 512, 64, 16, 17, gate_mu=2.0,
+                        s0_std=0.1), dST_std=0.1),
+    dict(cfg=small_case("bf16_sweep", "bf16", 2, 2, 256, 128, 128, 64, 16, 18)),
+    dict(cfg=small_case("bf16_ragged_C16", "bf16", 1, 3, 77, 64, 96, 16, 4, 19)),
+    dict(cfg=small_case("bf16_T1", "bf16", 1, 1, 1, 32, 48, 64, 16, 20, s0_std=0.1), dST_std=0.1),
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c["cfg"]["name"] for c in SMALL])
+def test_small_parity(case):
+    cfg = case["cfg"]
+    say("case", cfg["name"], {k: cfg[k] for k in ("B", "H", "T", "dk", "dv", "chunk", "subchunk", "io")})
+    inp = W.make_inputs(cfg, alpha_one=case.get("alpha_one", False), dST_std=case.get("dST_std", 0.0))
+    o, ST, gr = run_gpu(inp, cfg["chunk"], cfg["subchunk"], want_state=True)
+    compare(inp, o, ST, gr, list(range(cfg["B"] * cfg["H"])), cfg["io"], cfg["name"])
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_strong_decay_uses_pairwise_exponentials(io):
+    """Per-step log gates down to -8 push a 16-row block's decay far past the
+    factorised range; the diagonal blocks then use one exponential per pair."""
+    cfg = small_case("strong_decay_" + io, io, 1, 2, 128, 64, 64, 64, 16, 21)
+    inp = W.make_inputs(cfg)
+    g = torch.Generator().manual_seed(5)
+    la = -torch.rand(inp["log_alpha"].shape, generator=g) * 8.0
+    inp["log_alpha"] = la.to(inp["q"].dtype)
+    o, ST, gr = run_gpu(inp, 64, 16, want_state=True)
+    for t in (o, ST, gr["dq"], gr["dk"], gr["dv"], gr["dlog_alpha"]):
+        assert torch.isfinite(t.float()).all()
+    compare(inp, o, ST, gr, [0, 1], io, cfg["name"])
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_recurrent_forward(io):
+    cfg = small_case("rec_" + io, io, 1, 2, 150, 64, 96, 64, 16, 22, s0_std=0.1)
+    inp = W.make_inputs(cfg)
+    d = to_dev(inp)
+    o, ST = gla().recurrent_fwd(d["q"], d["k"], d["v"], d["log_alpha"], S0=d["S0"],
+                                output_final_state=True)
+    torch.cuda.synchronize()
+    idx = [0, 1]
+    ro, rST = oracle.fwd(*(heads(inp[n], idx) for n in ("q", "k", "v", "log_alpha")),
+                         heads(inp["S0"], idx))
+    e1, e2 = rel(heads(o, idx), ro), rel(heads(ST, idx), rST)
+    say("recurrent", io, e1, e2)
+    assert e1 <= TOL[io] and e2 <= TOL[io]
+
+
+def test_empty_sequence_and_batch():
+    g = gla()
+    for T in (0,):
+        q = torch.zeros(2, 1, T, 32, device="cuda", dtype=torch.bfloat16)
+        v = torch.zeros(2, 1, T, 48, device="cuda", dtype=torch.bfloat16)
+        S0 = torch.randn(2, 1, 32, 48, device="cuda")
+        o, ST = g.chunk_fwd(q, q, v, q, 64, 16, S0=S0, output_final_state=True)
+        dST = torch.randn(2, 1, 32, 48, device="cuda")
+        gr = g.chunk_bwd(q, q, v, q, v, 64, 16, S0=S0, dST=dST, want_dS0=True)
+        o2, ST2 = g.recurrent_fwd(q, q, v, q, S0=S0, output_final_state=True)
+        torch.cuda.synchronize()
+        assert o.shape == (2, 1, 0, 48) and torch.equal(ST, S0) and torch.equal(ST2, S0)
+        assert torch.equal(gr["dS0"], dST)
+    q = torch.zeros(0, 4, 64, 32, device="cuda", dtype=torch.bfloat16)
+    v = torch.zeros(0, 4, 64, 48, device="cuda", dtype=torch.bfloat16)
+    o, _ = g.chunk_fwd(q, q, v, q, 64, 16)
+    assert o.shape == (0, 4, 64, 48)
+
+
+def test_deterministic_and_workspace_reuse_is_exact():
+    cfg = small_case("det", "bf16", 1, 2, 192, 128, 256, 64, 16, 23, s0_std=0.1)
+    inp = W.make_inputs(cfg, dST_std=0.1)
+    o1, S1, g1 = run_gpu(inp, 64, 16, True, reuse=True)
+    o2, S2, g2 = run_gpu(inp, 64, 16, True, reuse=False)
+    assert torch.equal(o1, o2) and torch.equal(S1, S2)
+    for name in g1:
+        assert torch.equal(g1[name], g2[name]), name
+
+
+def test_segment_split_matches_one_call():
+    """Carrying the final state into the next call (truncated backprop through
+    time, Sec. 5) reproduces the single long call."""
+    g = gla()
+    cfg = small_case("split", "f32", 1, 2, 256, 64, 128, 64, 16, 24)
+    d = to_dev(W.make_inputs(cfg))
+    o, ST = g.chunk_fwd(d["q"], d["k"], d["v"], d["log_alpha"], 64, 16, output_final_state=True)
+    sl = lambda t, a, b: t[:, :, a:b].contiguous()
+    oa, Sa = g.chunk_fwd(*(sl(d[n], 0, 100) for n in ("q", "k", "v", "log_alpha")), 64, 16,
+                         output_final_state=True)
+    ob, Sb = g.chunk_fwd(*(sl(d[n], 100, 256) for n in ("q", "k", "v", "log_alpha")), 64, 16,
+                         S0=Sa, output_final_state=True)
+    torch.cuda.synchronize()
+    assert rel(torch.cat([oa, ob], 2).cpu(), o.cpu()) < 1e-4
+    assert rel(Sb.cpu(), ST.cpu()) < 1e-4
+
+
+# ----------------------------------------------------------------- full sizes
+
+FULL = [("gla1p3b_T2048", False, 0.0), ("gla340m_T2048", False, 0.0), ("gla340m_T2048", True, 0.0),
+        ("long_T16384", False, 0.0), ("long_T16384", False, 0.1)] + \
+       [(f"sweep_T{T}", False, 0.0) for T in W.SWEEP_T]
+
+
+@pytest.mark.parametrize("name,alpha_one,dst", FULL,
+                         ids=[f"{n}{'-ungated' if a else ''}{'-dST' if d else ''}" for n, a, d in FULL])
+def test_full_size_sampled_heads(name, alpha_one, dst):
+    cfg = W.CONFIGS[name]
+    say("full", name, "alpha_one" if alpha_one else "", "dST" if dst else "")
+    inp = W.make_inputs(cfg, alpha_one=alpha_one, dST_std=dst)
+    o, ST, gr = run_gpu(inp, cfg["chunk"], cfg["subchunk"], want_state=True)
+    for t in (o, ST, gr["dq"], gr["dk"], gr["dv"], gr["dlog_alpha"], gr["dS0"]):
+        assert torch.isfinite(t.float()).all()
+    BH = cfg["B"] * cfg["H"]
+    idx = [0, BH - 1] if cfg["T"] <= 4096 else [BH - 1]
+    compare(inp, o, ST, gr, idx, cfg["io"], name)
+
+
+def test_stage_by_stage_equals_whole_call():
+    """The stage selector (used by the benchmark to time each kernel) runs the
+    same kernels: stages in order reproduce the whole call exactly."""
+    g = gla()
+    cfg = small_case("stages", "bf16", 1, 2, 200, 128, 256, 64, 16, 25, s0_std=0.1)
+    d = to_dev(W.make_inputs(cfg, dST_std=0.1))
+    args = (d["q"], d["k"], d["v"], d["log_alpha"])
+    ws = torch.empty(g.workspace_bytes(1, 2, 200, 128, 256, 64, 16, torch.bfloat16, op=1),
+                     dtype=torch.uint8, device="cuda")
+    o, ST = g.chunk_fwd(*args, 64, 16, S0=d["S0"], output_final_state=True, workspace=ws)
+    ref = g.chunk_bwd(*args, d["dO"], 64, 16, S0=d["S0"], dST=d["dST"], want_dS0=True, workspace=ws,
+                      reuse_fwd_workspace=True)
+    o2, ST2 = torch.empty_like(o), torch.empty_like(ST)
+    for s in (1, 2):
+        g.chunk_fwd(*args, 64, 16, S0=d["S0"], workspace=ws, stage=s, out=(o2, ST2))
+    out = {k: torch.empty_like(v) for k, v in ref.items()}
+    for s in (2, 3, 4):
+        g.chunk_bwd(*args, d["dO"], 64, 16, S0=d["S0"], dST=d["dST"], workspace=ws,
+                    reuse_fwd_workspace=True, stage=s, out=out)
+    torch.cuda.synchronize()
+    assert torch.equal(o, o2) and torch.equal(ST, ST2)
+    for k in ref:
+        assert torch.equal(ref[k], out[k]), k
