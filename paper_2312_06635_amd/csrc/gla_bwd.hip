@@ -29,6 +29,12 @@ namespace gla {
 constexpr float kWideRangeB = 60.0f;
 
 static int round_up(int x, int m) { return (x + m - 1) / m * m; }
+// Smallest power of two >= max(x, lo) (tile widths must be powers of two).
+static int pow2_at_least(int x, int lo) {
+  int p = lo;
+  while (p < x) p *= 2;
+  return p;
+}
 
 __device__ __forceinline__ int pair_idx(int I, int J) { return I == 2 ? 0 : (J == 0 ? 1 : 2); }
 
@@ -117,8 +123,8 @@ __device__ __forceinline__ void inter_product(f4 (&acc)[4][2], const T *X, int l
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
       for (int I = 0; I < nb; ++I)
-        acc[I][kb] = mma_f32_x16(acc[I][kb], ld_row_perm_lo_f32((const float *)X, ldv, 16 * I, 16 * w),
-                                 st[0][kb]);
+          acc[I][kb] = mma_f32_x16(acc[I][kb], ld_row_perm_lo_f32((const float *)X, ldv, 16 * I, 16 * w),
+                                   st[0][kb]);
   } else {
 #pragma unroll
     for (int p = 0; p < NVB / 2; ++p)
@@ -211,18 +217,22 @@ template <typename T> __device__ __forceinline__ f4 mma_split3(f4 acc, const f8 
 __device__ __forceinline__ void reduce_partials(f4 (&acc)[4][2], float *red, int nb, int C, int w,
                                                 int g, int j) {
   if (w >= 2)
-    for (int I = 0; I < nb; ++I)
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+    for (int I = 0; I < 4; ++I)
+      if (I < nb)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) red[(w - 2) * C * 32 + (16 * I + 4 * g + r) * 32 + 16 * kb + j] = acc[I][kb][r];
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) red[(w - 2) * C * 32 + (16 * I + 4 * g + r) * 32 + 16 * kb + j] = acc[I][kb][r];
   __syncthreads();
   if (w < 2)
-    for (int I = 0; I < nb; ++I)
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+    for (int I = 0; I < 4; ++I)
+      if (I < nb)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) red[w * C * 32 + (16 * I + 4 * g + r) * 32 + 16 * kb + j] += acc[I][kb][r];
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) red[w * C * 32 + (16 * I + 4 * g + r) * 32 + 16 * kb + j] += acc[I][kb][r];
   __syncthreads();
 }
 
@@ -313,17 +323,16 @@ __global__ void __launch_bounds__(256) bwd_dq_kernel(KArgs a, KLds L) {
 
   TileRegs<T, NS> pV, pD;
   TileRegs<T, NI> pLa, pK;
+  const int64_t hK = (int64_t)bh * a.T * K, hV = (int64_t)bh * a.T * V;  // head bases
   auto load_in = [&](int n) {
     const int rv = min(C, a.T - n * C);
-    const int64_t rb = (int64_t)bh * a.T + n * C;
-    pLa.load(lain + rb * K + k0, K, Cp, 32, rv, K - k0);
-    pK.load(kin + rb * K + k0, K, Cp, 32, rv, K - k0);
+    pLa.load(lain + hK + (n * C * K + k0), K, Cp, 32, rv, K - k0);
+    pK.load(kin + hK + (n * C * K + k0), K, Cp, 32, rv, K - k0);
   };
   auto load_slab = [&](int n, int sl) {
     const int rv = min(C, a.T - n * C);
-    const int64_t rb = (int64_t)bh * a.T + n * C;
-    pV.load(vin + rb * V + sl * VS, V, Cp, VS, rv, V - sl * VS);
-    pD.load(dOin + rb * V + sl * VS, V, Cp, VS, rv, V - sl * VS);
+    pV.load(vin + hV + (n * C * V + sl * VS), V, Cp, VS, rv, V - sl * VS);
+    pD.load(dOin + hV + (n * C * V + sl * VS), V, Cp, VS, rv, V - sl * VS);
   };
   __syncthreads();
   load_in(0);
@@ -559,21 +568,22 @@ __global__ void __launch_bounds__(256) bwd_dk_kernel(KArgs a, KLds L) {
   TileRegs<T, NS> pV, pD;
   TileRegs<T, NI> pQ, pK, pLa, pDq, pDql;
   TileRegs<float, NP> pP;
+  const int64_t hK = (int64_t)bh * a.T * K, hV = (int64_t)bh * a.T * V;  // head bases
+  const float *dPh = a.dP + (int64_t)bh * a.N * C * C;
   auto load_in = [&](int n) {
     const int rv = min(C, a.T - n * C);
-    const int64_t rb = (int64_t)bh * a.T + n * C;
-    pQ.load(qin + rb * K + k0, K, Cp, 32, rv, K - k0);
-    pK.load(kin + rb * K + k0, K, Cp, 32, rv, K - k0);
-    pLa.load(lain + rb * K + k0, K, Cp, 32, rv, K - k0);
-    pDq.load(dqin + rb * K + k0, K, Cp, 32, rv, K - k0);
-    if constexpr (SPLIT) pDql.load(dqlin + rb * K + k0, K, Cp, 32, rv, K - k0);
-    pP.load(a.dP + ((int64_t)bh * a.N + n) * C * C, C, Cp, Cp, C, C);
+    const int off = n * C * K + k0;
+    pQ.load(qin + hK + off, K, Cp, 32, rv, K - k0);
+    pK.load(kin + hK + off, K, Cp, 32, rv, K - k0);
+    pLa.load(lain + hK + off, K, Cp, 32, rv, K - k0);
+    pDq.load(dqin + hK + off, K, Cp, 32, rv, K - k0);
+    if constexpr (SPLIT) pDql.load(dqlin + hK + off, K, Cp, 32, rv, K - k0);
+    pP.load(dPh + n * C * C, C, Cp, Cp, C, C);
   };
   auto load_slab = [&](int n, int sl) {
     const int rv = min(C, a.T - n * C);
-    const int64_t rb = (int64_t)bh * a.T + n * C;
-    pV.load(vin + rb * V + sl * VS, V, Cp, VS, rv, V - sl * VS);
-    pD.load(dOin + rb * V + sl * VS, V, Cp, VS, rv, V - sl * VS);
+    pV.load(vin + hV + (n * C * V + sl * VS), V, Cp, VS, rv, V - sl * VS);
+    pD.load(dOin + hV + (n * C * V + sl * VS), V, Cp, VS, rv, V - sl * VS);
   };
   __syncthreads();
   load_in(a.N - 1);
@@ -772,14 +782,16 @@ __global__ void __launch_bounds__(256) bwd_dv_kernel(DvArgs a) {
   TileRegs<T, NQ> pq, pk;
   TileRegs<T, NX> pd, pp;
   float pg = 0.f;
+  const T *Qh = Qt + (int64_t)bh * a.T * K, *Kh = Kt + (int64_t)bh * a.T * K;
+  const T *dOh = dOin + (int64_t)bh * a.T * V + v0, *Ph = Pm + (int64_t)bh * a.N * C * C;
+  const float *gh = a.gam + (int64_t)bh * a.N * K;
   auto load_chunk = [&](int n) {
-    const int t0 = n * C, rv = min(C, a.T - t0);
-    const int64_t rb = (int64_t)bh * a.T + t0;
-    pq.load(Qt + rb * K, K, Cp, Kp, rv, K);
-    pk.load(Kt + rb * K, K, Cp, Kp, rv, K);
-    pd.load(dOin + rb * V + v0, V, Cp, a.Tv, rv, V - v0);
-    pp.load(Pm + ((int64_t)bh * a.N + n) * C * C, C, Cp, Cp, C, C);
-    pg = (int)threadIdx.x < K ? a.gam[((int64_t)bh * a.N + n) * K + threadIdx.x] : 0.f;
+    const int rv = min(C, a.T - n * C);
+    pq.load(Qh + n * C * K, K, Cp, Kp, rv, K);
+    pk.load(Kh + n * C * K, K, Cp, Kp, rv, K);
+    pd.load(dOh + n * C * V, V, Cp, a.Tv, rv, V - v0);
+    pp.load(Ph + n * C * C, C, Cp, Cp, C, C);
+    pg = (int)threadIdx.x < K ? gh[n * K + threadIdx.x] : 0.f;
   };
   load_chunk(a.N - 1);
   for (int n = a.N - 1; n >= 0; --n) {
@@ -793,17 +805,24 @@ __global__ void __launch_bounds__(256) bwd_dv_kernel(DvArgs a) {
     __syncthreads();
     if (n > 0) load_chunk(n - 1);
     if (active) {
-      for (int J = 0; J < C / 16; ++J) {
-        f4 acc = zero4();
+      const int nJ = C / 16;
+      f4 acc[4] = {zero4(), zero4(), zero4(), zero4()};
 #pragma unroll
-        for (int s = 0; s < KBP / 2; ++s)
-          acc = mma<T>(acc, ld_row_perm<T>(sK, ldk, 16 * J, 32 * s), acc_frag<T>(dS[2 * s], dS[2 * s + 1]));
+      for (int s = 0; s < KBP / 2; ++s) {
+        const frag_t<T> bs = acc_frag<T>(dS[2 * s], dS[2 * s + 1]);
+#pragma unroll
+        for (int J = 0; J < 4; ++J)
+          if (J < nJ) acc[J] = mma<T>(acc[J], ld_row_perm<T>(sK, ldk, 16 * J, 32 * s), bs);
+      }
+#pragma unroll
+      for (int J = 0; J < 4; ++J) {
+        if (J >= nJ) continue;
         for (int s = (16 * J) / 32; s < Cp / 32; ++s)
-          acc = mma<T>(acc, ld_col<T>(sP, ldp, 32 * s, 16 * J), ld_col<T>(sdO, ldv, 32 * s, 16 * w));
+          acc[J] = mma<T>(acc[J], ld_col<T>(sP, ldp, 32 * s, 16 * J), ld_col<T>(sdO, ldv, 32 * s, 16 * w));
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int row = 16 * J + 4 * g + r;
-          if (row < rv && colv) dvo[(rb + row) * V + col] = cvt<T>(acc[r]);
+          if (row < rv && colv) dvo[(rb + row) * V + col] = cvt<T>(acc[J][r]);
         }
       }
 #pragma unroll
@@ -833,9 +852,9 @@ size_t lds_bwd_dq(const Shape &s) { return (size_t)k_lds(s, n_in_dq(s)).total; }
 size_t lds_bwd_dk(const Shape &s) { return (size_t)k_lds(s, n_in_dk(s)).total; }
 
 static void dv_geometry(const Shape &s, int &Kp, int &Cp, int &Tv, int &ldk, int &ldv, int &ldp) {
-  Kp = round_up(s.K, 32);
+  Kp = pow2_at_least(s.K, 32);
   Cp = round_up(s.C, 32);
-  Tv = s.V >= 64 ? 64 : round_up(s.V, 16);
+  Tv = pow2_at_least(s.V < 64 ? s.V : 64, 16);
   const int pad = 32 / s.esz();
   ldk = Kp + pad;
   ldv = Tv + pad;
@@ -932,11 +951,7 @@ static hipError_t dispatch_dv(const DvArgs &a, int waves, size_t lds, hipStream_
   switch (a.Kp / 16) {
     case 2: return run_dv<T, 2>(a, waves, lds, st);
     case 4: return run_dv<T, 4>(a, waves, lds, st);
-    case 6: return run_dv<T, 6>(a, waves, lds, st);
     case 8: return run_dv<T, 8>(a, waves, lds, st);
-    case 10: return run_dv<T, 10>(a, waves, lds, st);
-    case 12: return run_dv<T, 12>(a, waves, lds, st);
-    case 14: return run_dv<T, 14>(a, waves, lds, st);
     default: return run_dv<T, 16>(a, waves, lds, st);
   }
 }

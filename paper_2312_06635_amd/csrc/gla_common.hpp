@@ -51,7 +51,9 @@ template <typename T> __device__ __forceinline__ f4 mma(f4 c, frag_t<T> a, frag_
 }
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
-__device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
+// The wave index is uniform across a wave; reading it through readfirstlane
+// lets the compiler keep it (and every branch on it) in scalar registers.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
 template <typename T> __device__ __forceinline__ T cvt(float x);
 template <> __device__ __forceinline__ float cvt<float>(float x) { return x; }
@@ -184,29 +186,36 @@ __device__ __forceinline__ void stage_tile(T *dst, int lld, const T *src, int64_
 // 256-thread workgroup.
 template <typename T, int NV> struct TileRegs {
   uint4 r[NV];
-  __device__ __forceinline__ void load(const T *src, int64_t gld, int rows, int cols, int rv, int cv) {
+  // Thread t covers vectors t, t + 256, ...; with vpr = cols / EV a power of two
+  // dividing 256 (the case for every tile here) its row steps by 256 / vpr and
+  // its column stays fixed, so no division is needed.
+  __device__ __forceinline__ static void geom(int cols, int &row0, int &rstep, int &c, int &vpr) {
     constexpr int EV = 16 / sizeof(T);
-    const int vpr = cols / EV, total = rows * vpr;
+    vpr = cols / EV;
+    const int sh = 31 - __builtin_clz(vpr);
+    row0 = (int)threadIdx.x >> sh;
+    rstep = 256 >> sh;
+    c = ((int)threadIdx.x & (vpr - 1)) * EV;
+  }
+  // src must be uniform across the workgroup and row * gld + c must fit in
+  // 32 bits, so the loads use a scalar base plus a 32-bit vector offset.
+  __device__ __forceinline__ void load(const T *src, int gld, int rows, int cols, int rv, int cv) {
+    int row0, rstep, c, vpr;
+    geom(cols, row0, rstep, c, vpr);
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
-      const int idx = threadIdx.x + i * 256;
+      const int row = row0 + i * rstep;
       r[i] = make_uint4(0, 0, 0, 0);
-      if (idx < total) {
-        const int row = idx / vpr, c = (idx - row * vpr) * EV;
-        if (row < rv && c < cv) r[i] = *(const uint4 *)(src + row * gld + c);
-      }
+      if (row < rows && row < rv && c < cv) r[i] = *(const uint4 *)(src + (row * gld + c));
     }
   }
   __device__ __forceinline__ void store(T *dst, int lld, int rows, int cols) const {
-    constexpr int EV = 16 / sizeof(T);
-    const int vpr = cols / EV, total = rows * vpr;
+    int row0, rstep, c, vpr;
+    geom(cols, row0, rstep, c, vpr);
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
-      const int idx = threadIdx.x + i * 256;
-      if (idx < total) {
-        const int row = idx / vpr, c = (idx - row * vpr) * EV;
-        *(uint4 *)(dst + row * lld + c) = r[i];
-      }
+      const int row = row0 + i * rstep;
+      if (row < rows) *(uint4 *)(dst + row * lld + c) = r[i];
     }
   }
 };

@@ -16,6 +16,12 @@
 namespace gla {
 
 static int round_up(int x, int m) { return (x + m - 1) / m * m; }
+// Smallest power of two >= max(x, lo) (tile widths must be powers of two).
+static int pow2_at_least(int x, int lo) {
+  int p = lo;
+  while (p < x) p *= 2;
+  return p;
+}
 
 struct MainArgs {
   const void *Qt, *Kt, *P, *v;
@@ -60,14 +66,16 @@ __global__ void __launch_bounds__(256) fwd_main_kernel(MainArgs a) {
   TileRegs<T, NQ> pq, pk;
   TileRegs<T, NX> pv, pp;
   float pg = 0.f;
+  const T *Qh = Qt + (int64_t)bh * a.T * K, *Kh = Kt + (int64_t)bh * a.T * K;
+  const T *vh = vin + (int64_t)bh * a.T * V + v0, *Ph = Pm + (int64_t)bh * a.N * C * C;
+  const float *gh = a.gam + (int64_t)bh * a.N * K;
   auto load_chunk = [&](int n) {
-    const int t0 = n * C, rv = min(C, a.T - t0);
-    const int64_t rb = (int64_t)bh * a.T + t0;
-    pq.load(Qt + rb * K, K, Cp, Kp, rv, K);
-    pk.load(Kt + rb * K, K, Cp, Kp, rv, K);
-    pv.load(vin + rb * V + v0, V, Cp, a.Tv, rv, V - v0);
-    pp.load(Pm + ((int64_t)bh * a.N + n) * C * C, C, C, Cp, C, C);
-    pg = (int)threadIdx.x < K ? a.gam[((int64_t)bh * a.N + n) * K + threadIdx.x] : 0.f;
+    const int rv = min(C, a.T - n * C);
+    pq.load(Qh + n * C * K, K, Cp, Kp, rv, K);
+    pk.load(Kh + n * C * K, K, Cp, Kp, rv, K);
+    pv.load(vh + n * C * V, V, Cp, a.Tv, rv, V - v0);
+    pp.load(Ph + n * C * C, C, C, Cp, C, C);
+    pg = (int)threadIdx.x < K ? gh[n * K + threadIdx.x] : 0.f;
   };
   load_chunk(0);
   for (int n = 0; n < a.N; ++n) {
@@ -82,18 +90,25 @@ __global__ void __launch_bounds__(256) fwd_main_kernel(MainArgs a) {
     if (n + 1 < a.N) load_chunk(n + 1);
 
     if (active) {
-      for (int I = 0; I < C / 16; ++I) {
-        f4 acc = zero4();
+      const int nI = C / 16;
+      f4 acc[4] = {zero4(), zero4(), zero4(), zero4()};
 #pragma unroll
-        for (int s = 0; s < KBP / 2; ++s)
-          acc = mma<T>(acc, ld_row_perm<T>(sQ, ldk, 16 * I, 32 * s), acc_frag<T>(S[2 * s], S[2 * s + 1]));
+      for (int s = 0; s < KBP / 2; ++s) {
+        const frag_t<T> bs = acc_frag<T>(S[2 * s], S[2 * s + 1]);
+#pragma unroll
+        for (int I = 0; I < 4; ++I)
+          if (I < nI) acc[I] = mma<T>(acc[I], ld_row_perm<T>(sQ, ldk, 16 * I, 32 * s), bs);
+      }
+#pragma unroll
+      for (int I = 0; I < 4; ++I) {
+        if (I >= nI) continue;
         const int js = (16 * I + 16 + 31) >> 5;
         for (int s = 0; s < js; ++s)
-          acc = mma<T>(acc, ld_row<T>(sP, ldp, 16 * I, 32 * s), ld_col<T>(sV, ldv, 32 * s, 16 * w));
+          acc[I] = mma<T>(acc[I], ld_row<T>(sP, ldp, 16 * I, 32 * s), ld_col<T>(sV, ldv, 32 * s, 16 * w));
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int row = 16 * I + 4 * g + r;
-          if (row < rv && colv) o[(rb + row) * V + col] = cvt<T>(acc[r]);
+          if (row < rv && colv) o[(rb + row) * V + col] = cvt<T>(acc[I][r]);
         }
       }
 #pragma unroll
@@ -118,9 +133,9 @@ __global__ void __launch_bounds__(256) fwd_main_kernel(MainArgs a) {
 }
 
 static void main_geometry(const Shape &s, int &Kp, int &Cp, int &Tv, int &ldk, int &ldv, int &ldp) {
-  Kp = round_up(s.K, 32);
+  Kp = pow2_at_least(s.K, 32);
   Cp = round_up(s.C, 32);
-  Tv = s.V >= 64 ? 64 : round_up(s.V, 16);
+  Tv = pow2_at_least(s.V < 64 ? s.V : 64, 16);
   const int pad = 32 / s.esz();
   ldk = Kp + pad;
   ldv = Tv + pad;
@@ -150,11 +165,7 @@ static hipError_t dispatch_main(const MainArgs &a, int waves, size_t lds, hipStr
   switch (a.Kp / 16) {
     case 2: return launch_main_t<T, 2>(a, waves, lds, st);
     case 4: return launch_main_t<T, 4>(a, waves, lds, st);
-    case 6: return launch_main_t<T, 6>(a, waves, lds, st);
     case 8: return launch_main_t<T, 8>(a, waves, lds, st);
-    case 10: return launch_main_t<T, 10>(a, waves, lds, st);
-    case 12: return launch_main_t<T, 12>(a, waves, lds, st);
-    case 14: return launch_main_t<T, 14>(a, waves, lds, st);
     default: return launch_main_t<T, 16>(a, waves, lds, st);
   }
 }

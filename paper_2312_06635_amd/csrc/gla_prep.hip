@@ -73,6 +73,21 @@ __device__ __forceinline__ float allreduce64(float x) {
 // Pair index of the non-adjacent block pairs (I, J), J <= I - 2, for C <= 64.
 __device__ __forceinline__ int pair_index(int I, int J) { return I == 2 ? 0 : (J == 0 ? 1 : 2); }
 
+// FPL consecutive elements as one aligned vector access.
+template <typename T, int N> struct alignas(sizeof(T) * N) VecN { T e[N]; };
+template <typename T, int N> __device__ __forceinline__ void ldvec(const T *p, bool ok, float (&o)[N]) {
+  VecN<T, N> v;
+  if (ok) v = *(const VecN<T, N> *)p;
+#pragma unroll
+  for (int i = 0; i < N; ++i) o[i] = ok ? (float)v.e[i] : 0.f;
+}
+template <typename T, int N> __device__ __forceinline__ void stvec(T *p, const float (&x)[N]) {
+  VecN<T, N> v;
+#pragma unroll
+  for (int i = 0; i < N; ++i) v.e[i] = cvt<T>(x[i]);
+  *(VecN<T, N> *)p = v;
+}
+
 template <typename T, int FPL>
 __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -90,31 +105,43 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
   const T *q = (const T *)a.q + base, *k = (const T *)a.k + base, *la = (const T *)a.la + base;
   T *Qt = (T *)a.Qt + base, *Kt = (T *)a.Kt + base;
   T *Pg = (T *)a.P + ((int64_t)bh * a.N + n) * C * C;
+  // lane l owns the FPL consecutive features k0 .. k0 + FPL - 1
+  const int k0 = FPL * l;
+  const bool fv = k0 < K;     // K is a multiple of 16, so all FPL are valid together
+  const bool fp = k0 < Kp;    // inside the zero-padded LDS tiles
 
   // 1. block-local cumsum of log alpha.
   float Bloc[16][FPL], tot[FPL];
+  {
+    float c[FPL];
 #pragma unroll
-  for (int f = 0; f < FPL; ++f) {
-    const int kf = l + 64 * f;
-    float c = 0.f;
+    for (int f = 0; f < FPL; ++f) c[f] = 0.f;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int row = 16 * w + r;
-      c += (row < rv && kf < K) ? (float)la[row * K + kf] : 0.f;
-      Bloc[r][f] = c;
+      float x[FPL];
+      ldvec<T, FPL>(la + row * K + k0, fv && row < rv, x);
+#pragma unroll
+      for (int f = 0; f < FPL; ++f) {
+        c[f] += x[f];
+        Bloc[r][f] = c[f];
+      }
     }
-    tot[f] = c;
-    if (kf < Kp) sTot[w * Kp + kf] = c;
+#pragma unroll
+    for (int f = 0; f < FPL; ++f) {
+      tot[f] = c[f];
+      if (fp) sTot[w * Kp + k0 + f] = c[f];
+    }
   }
   __syncthreads();
 
   float pre[FPL], Bl[FPL];
 #pragma unroll
   for (int f = 0; f < FPL; ++f) {
-    const int kf = l + 64 * f;
+    const int kf = k0 + f;
     pre[f] = 0.f;
     Bl[f] = 0.f;
-    if (kf < Kp) {
+    if (fp) {
       for (int w2 = 0; w2 < nb; ++w2) {
         const float t = sTot[w2 * Kp + kf];
         if (w2 < w) pre[f] += t;
@@ -131,34 +158,48 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
   // 2. gated operands.
   float qh[16][FPL], kh[16][FPL];
   bool wide = false;
+  float ez[FPL], ekt[FPL], eup[FPL];
 #pragma unroll
   for (int f = 0; f < FPL; ++f) {
-    const int kf = l + 64 * f;
-    const bool fv = kf < K;
-    const float ez = __expf(pre[f]);                  // b_{block start} / b_{chunk start}
-    const float ekt = __expf(Bl[f] - pre[f] - tot[f]);  // b_{chunk end} / b_{block end}
-    const float eup = __expf(-tot[f]);                // b_{block start} / b_{block end} >= 1
+    ez[f] = __expf(pre[f]);                    // b_{block start} / b_{chunk start}
+    ekt[f] = __expf(Bl[f] - pre[f] - tot[f]);  // b_{chunk end} / b_{block end}
+    eup[f] = __expf(-tot[f]);                  // b_{block start} / b_{block end} >= 1
     if (fv && -tot[f] > kWideRange) wide = true;
+  }
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = 16 * w + r;
-      const bool ok = fv && row < rv;
-      const float qv = ok ? (float)q[row * K + kf] : 0.f;
-      const float kv = ok ? (float)k[row * K + kf] : 0.f;
-      const float qhv = qv * __expf(Bloc[r][f]);            // <= |q|
-      const float ksv = kv * __expf(tot[f] - Bloc[r][f]);   // <= |k|
+  for (int r = 0; r < 16; ++r) {
+    const int row = 16 * w + r;
+    const bool ok = fv && row < rv;
+    float qv[FPL], kv[FPL], o1[FPL], o2[FPL], o3[FPL], o4[FPL];
+    ldvec<T, FPL>(q + row * K + k0, ok, qv);
+    ldvec<T, FPL>(k + row * K + k0, ok, kv);
+#pragma unroll
+    for (int f = 0; f < FPL; ++f) {
+      const float qhv = qv[f] * __expf(Bloc[r][f]);           // <= |q|
+      const float ksv = kv[f] * __expf(tot[f] - Bloc[r][f]);  // <= |k|
       qh[r][f] = qhv;
-      kh[r][f] = ksv * eup;
-      if (ok) {
-        Qt[row * K + kf] = cvt<T>(qhv * ez);
-        Kt[row * K + kf] = cvt<T>(ksv * ekt);
-      }
-      if (kf < Kp) {
-        sQh[row * ldk + kf] = cvt<T>(qhv);
-        sKs[row * ldk + kf] = cvt<T>(ksv);
-      }
+      kh[r][f] = ksv * eup[f];
+      o1[f] = qhv * ez[f];
+      o2[f] = ksv * ekt[f];
+      o3[f] = qhv;
+      o4[f] = ksv;
     }
-    if (w == 0 && fv) a.gam[((int64_t)bh * a.N + n) * K + kf] = __expf(Bl[f]);
+    if (ok) {
+      stvec<T, FPL>(Qt + row * K + k0, o1);
+      stvec<T, FPL>(Kt + row * K + k0, o2);
+    }
+    if (fp) {
+      stvec<T, FPL>(sQh + row * ldk + k0, o3);
+      stvec<T, FPL>(sKs + row * ldk + k0, o4);
+    }
+  }
+  if (w == 0 && fv) {
+    float gv[FPL];
+#pragma unroll
+    for (int f = 0; f < FPL; ++f) gv[f] = __expf(Bl[f]);
+    float *gp = a.gam + ((int64_t)bh * a.N + n) * K + k0;
+#pragma unroll
+    for (int f = 0; f < FPL; ++f) gp[f] = gv[f];
   }
 
   // 3. diagonal ("pink") block w in fp32.
@@ -194,18 +235,21 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
     } else {
       // Large decay inside the block: one exponential per (i, j, k).
       float qv[16][FPL], kv[16][FPL], Bv[16][FPL];
+      float c[FPL];
 #pragma unroll
-      for (int f = 0; f < FPL; ++f) {
-        const int kf = l + 64 * f;
-        float c = 0.f;
+      for (int f = 0; f < FPL; ++f) c[f] = 0.f;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = d0 + r;
-          const bool ok = kf < K && row < rv;
-          c += ok ? (float)la[row * K + kf] : 0.f;
-          Bv[r][f] = c;
-          qv[r][f] = ok ? (float)q[row * K + kf] : 0.f;
-          kv[r][f] = ok ? (float)k[row * K + kf] : 0.f;
+      for (int r = 0; r < 16; ++r) {
+        const int row = d0 + r;
+        const bool ok = fv && row < rv;
+        float xl[FPL];
+        ldvec<T, FPL>(la + row * K + k0, ok, xl);
+        ldvec<T, FPL>(q + row * K + k0, ok, qv[r]);
+        ldvec<T, FPL>(k + row * K + k0, ok, kv[r]);
+#pragma unroll
+        for (int f = 0; f < FPL; ++f) {
+          c[f] += xl[f];
+          Bv[r][f] = c[f];
         }
       }
 #pragma unroll
