@@ -39,14 +39,18 @@ gla_status make_shape(const gla_problem *p, Shape &s) {
   s.N = (p->T + p->chunk - 1) / p->chunk;
   s.io = p->io == GLA_BF16 ? gla::IO_BF16 : gla::IO_F32;
   if (s.N > 65535) return GLA_ERR_UNSUPPORTED;
+  // one head's rows of any tensor must span less than 2 GiB (32-bit buffer offsets)
+  const int64_t wmax = p->dk > p->dv ? p->dk : p->dv;
+  if ((int64_t)p->T * wmax * s.esz() >= (int64_t)1 << 31) return GLA_ERR_UNSUPPORTED;
   return GLA_OK;
 }
 
+// A kernel's LDS need of 0 means it has no variant for the shape.
+bool lds_bad(size_t bytes) { return bytes == 0 || bytes > gla::kMaxLds; }
+
 gla_status check_lds(const Shape &s, bool bwd) {
-  if (gla::lds_prep(s) > gla::kMaxLds || gla::lds_fwd_main(s) > gla::kMaxLds)
-    return GLA_ERR_UNSUPPORTED;
-  if (bwd && (gla::lds_bwd_dq(s) > gla::kMaxLds || gla::lds_bwd_dk(s) > gla::kMaxLds ||
-              gla::lds_bwd_dv(s) > gla::kMaxLds))
+  if (lds_bad(gla::lds_prep(s)) || lds_bad(gla::lds_fwd_main(s))) return GLA_ERR_UNSUPPORTED;
+  if (bwd && (lds_bad(gla::lds_bwd_dq(s)) || lds_bad(gla::lds_bwd_dk(s)) || lds_bad(gla::lds_bwd_dv(s))))
     return GLA_ERR_UNSUPPORTED;
   return GLA_OK;
 }

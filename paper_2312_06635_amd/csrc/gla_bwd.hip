@@ -740,132 +740,10 @@ __global__ void __launch_bounds__(256) bwd_dk_kernel(KArgs a, KLds L) {
   }
 }
 
-// ------------------------------------------------------------------ bwd_dv
-struct DvArgs {
-  const void *Qt, *Kt, *P, *dO;
-  const float *gam, *dST;
-  void *dv;
-  float *dS0;
-  int BH, T, K, Kp, V, C, Cp, N, Tv, ntiles, ldk, ldv, ldp;
-};
-
-template <typename T, int KBP>
-__global__ void __launch_bounds__(256) bwd_dv_kernel(DvArgs a) {
-  extern __shared__ __attribute__((aligned(16))) char smem[];
-  constexpr int NQ = sizeof(T) == 2 ? (KBP / 2 > 0 ? KBP / 2 : 1) : KBP;
-  constexpr int NX = sizeof(T) == 2 ? 2 : 4;
-  int bh, tile;
-  xcd_map(a.BH, a.ntiles, bh, tile);
-  const int w = wave_id(), l = lane_id(), g = l >> 4, j = l & 15;
-  const int K = a.K, V = a.V, C = a.C, Cp = a.Cp, Kp = a.Kp;
-  const int ldk = a.ldk, ldv = a.ldv, ldp = a.ldp;
-  const int v0 = tile * a.Tv;
-  const bool active = 16 * w < a.Tv;
-  const int col = v0 + 16 * w + j;
-  const bool colv = active && col < V;
-  T *sQ = (T *)smem;
-  T *sK = sQ + Cp * ldk;
-  T *sdO = sK + Cp * ldk;
-  T *sP = sdO + Cp * ldv;
-  float *sGam = (float *)(sP + Cp * ldp);
-
-  f4 dS[KBP];
-#pragma unroll
-  for (int kb = 0; kb < KBP; ++kb)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int kr = 16 * kb + 4 * g + r;
-      dS[kb][r] = (a.dST && kr < K && colv) ? a.dST[((int64_t)bh * K + kr) * V + col] : 0.f;
-    }
-  const T *Qt = (const T *)a.Qt, *Kt = (const T *)a.Kt, *Pm = (const T *)a.P, *dOin = (const T *)a.dO;
-  T *dvo = (T *)a.dv;
-  TileRegs<T, NQ> pq, pk;
-  TileRegs<T, NX> pd, pp;
-  float pg = 0.f;
-  const T *Qh = Qt + (int64_t)bh * a.T * K, *Kh = Kt + (int64_t)bh * a.T * K;
-  const T *dOh = dOin + (int64_t)bh * a.T * V + v0, *Ph = Pm + (int64_t)bh * a.N * C * C;
-  const float *gh = a.gam + (int64_t)bh * a.N * K;
-  auto load_chunk = [&](int n) {
-    const int rv = min(C, a.T - n * C);
-    pq.load(Qh + n * C * K, K, Cp, Kp, rv, K);
-    pk.load(Kh + n * C * K, K, Cp, Kp, rv, K);
-    pd.load(dOh + n * C * V, V, Cp, a.Tv, rv, V - v0);
-    pp.load(Ph + n * C * C, C, Cp, Cp, C, C);
-    pg = (int)threadIdx.x < K ? gh[n * K + threadIdx.x] : 0.f;
-  };
-  load_chunk(a.N - 1);
-  for (int n = a.N - 1; n >= 0; --n) {
-    const int t0 = n * C, rv = min(C, a.T - t0);
-    const int64_t rb = (int64_t)bh * a.T + t0;
-    pq.store(sQ, ldk, Cp, Kp);
-    pk.store(sK, ldk, Cp, Kp);
-    pd.store(sdO, ldv, Cp, a.Tv);
-    pp.store(sP, ldp, Cp, Cp);
-    if ((int)threadIdx.x < Kp) sGam[threadIdx.x] = pg;
-    __syncthreads();
-    if (n > 0) load_chunk(n - 1);
-    if (active) {
-      const int nJ = C / 16;
-      f4 acc[4] = {zero4(), zero4(), zero4(), zero4()};
-#pragma unroll
-      for (int s = 0; s < KBP / 2; ++s) {
-        const frag_t<T> bs = acc_frag<T>(dS[2 * s], dS[2 * s + 1]);
-#pragma unroll
-        for (int J = 0; J < 4; ++J)
-          if (J < nJ) acc[J] = mma<T>(acc[J], ld_row_perm<T>(sK, ldk, 16 * J, 32 * s), bs);
-      }
-#pragma unroll
-      for (int J = 0; J < 4; ++J) {
-        if (J >= nJ) continue;
-        for (int s = (16 * J) / 32; s < Cp / 32; ++s)
-          acc[J] = mma<T>(acc[J], ld_col<T>(sP, ldp, 32 * s, 16 * J), ld_col<T>(sdO, ldv, 32 * s, 16 * w));
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = 16 * J + 4 * g + r;
-          if (row < rv && colv) dvo[(rb + row) * V + col] = cvt<T>(acc[J][r]);
-        }
-      }
-#pragma unroll
-      for (int kb = 0; kb < KBP; ++kb) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) dS[kb][r] *= sGam[16 * kb + 4 * g + r];
-        for (int s = 0; s < Cp / 32; ++s)
-          dS[kb] = mma<T>(dS[kb], ld_col<T>(sQ, ldk, 32 * s, 16 * kb), ld_col<T>(sdO, ldv, 32 * s, 16 * w));
-      }
-    }
-    __syncthreads();
-  }
-  if (a.dS0 && colv) {
-#pragma unroll
-    for (int kb = 0; kb < KBP; ++kb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int kr = 16 * kb + 4 * g + r;
-        if (kr < K) a.dS0[((int64_t)bh * K + kr) * V + col] = dS[kb][r];
-      }
-  }
-}
-
 // ------------------------------------------------------------------ launchers
 
 size_t lds_bwd_dq(const Shape &s) { return (size_t)k_lds(s, n_in_dq(s)).total; }
 size_t lds_bwd_dk(const Shape &s) { return (size_t)k_lds(s, n_in_dk(s)).total; }
-
-static void dv_geometry(const Shape &s, int &Kp, int &Cp, int &Tv, int &ldk, int &ldv, int &ldp) {
-  Kp = pow2_at_least(s.K, 32);
-  Cp = round_up(s.C, 32);
-  Tv = pow2_at_least(s.V < 64 ? s.V : 64, 16);
-  const int pad = 32 / s.esz();
-  ldk = Kp + pad;
-  ldv = Tv + pad;
-  ldp = Cp + pad;
-}
-
-size_t lds_bwd_dv(const Shape &s) {
-  int Kp, Cp, Tv, ldk, ldv, ldp;
-  dv_geometry(s, Kp, Cp, Tv, ldk, ldv, ldp);
-  return (size_t)s.esz() * (2 * Cp * ldk + Cp * ldv + Cp * ldp) + (size_t)Kp * sizeof(float);
-}
 
 template <typename Kern, typename... Args>
 static hipError_t launch_generic(Kern kern, dim3 grid, dim3 block, size_t lds, hipStream_t st,
@@ -937,34 +815,6 @@ hipError_t launch_bwd_dk(const Shape &s, const void *q, const void *k, const voi
   a.q = q; a.k = k; a.la = la; a.v = v; a.dO = dO; a.dST = dST; a.dq_in = dq; a.dq_lo_in = w.dq_lo;
   a.dk = dk; a.dla = dla; a.dP = w.dP; a.cST = dST ? w.cST : nullptr;
   return run_k<false>(s, a, k_lds(s, n_in_dk(s)), st);
-}
-
-template <typename T, int KBP>
-static hipError_t run_dv(const DvArgs &a, int waves, size_t lds, hipStream_t st) {
-  static bool attr = false;
-  return launch_generic(bwd_dv_kernel<T, KBP>, dim3(a.BH * a.ntiles), dim3(64 * waves), lds, st,
-                        attr, a);
-}
-
-template <typename T>
-static hipError_t dispatch_dv(const DvArgs &a, int waves, size_t lds, hipStream_t st) {
-  switch (a.Kp / 16) {
-    case 2: return run_dv<T, 2>(a, waves, lds, st);
-    case 4: return run_dv<T, 4>(a, waves, lds, st);
-    case 8: return run_dv<T, 8>(a, waves, lds, st);
-    default: return run_dv<T, 16>(a, waves, lds, st);
-  }
-}
-
-hipError_t launch_bwd_dv(const Shape &s, const void *dO, const float *dST, void *dv, float *dS0,
-                         const Work &w, hipStream_t st) {
-  DvArgs a;
-  a.Qt = w.Qt; a.Kt = w.Kt; a.P = w.P; a.dO = dO; a.gam = w.gam; a.dST = dST; a.dv = dv; a.dS0 = dS0;
-  a.BH = s.BH; a.T = s.T; a.K = s.K; a.V = s.V; a.C = s.C; a.N = s.N;
-  dv_geometry(s, a.Kp, a.Cp, a.Tv, a.ldk, a.ldv, a.ldp);
-  a.ntiles = (s.V + a.Tv - 1) / a.Tv;
-  const size_t lds = lds_bwd_dv(s);
-  return s.io == IO_BF16 ? dispatch_dv<bf16>(a, 4, lds, st) : dispatch_dv<float>(a, 4, lds, st);
 }
 
 }  // namespace gla

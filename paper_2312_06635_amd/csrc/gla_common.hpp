@@ -220,6 +220,57 @@ template <typename T, int NV> struct TileRegs {
   }
 };
 
+// Buffer resource over [base, base + bytes): buffer loads at byte offsets at
+// or beyond `bytes` return zeros instead of touching memory.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// Clamp a byte count to the 32-bit range of a buffer resource.
+__device__ __forceinline__ uint32_t rsrc_bytes(int64_t bytes) {
+  return bytes <= 0 ? 0u : (bytes >= 0xFFFFFFF0LL ? 0xFFFFFFF0u : (uint32_t)bytes);
+}
+
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+// Register-staged [ROWS x COLS] tile copy, global -> LDS, for NT threads, with
+// compile-time geometry.  init() fixes each thread's byte offsets once (row
+// stride gld elements; rows >= rvalid or columns >= cvalid get an offset past
+// any buffer, so they read as zero); load() issues the 16-byte buffer loads
+// without waiting; store() writes the registers into an LDS tile with leading
+// dimension ld.  COLS * sizeof(T) / 16 must be a power of two dividing NT.
+template <typename T, int ROWS, int COLS, int NT> struct TileLd {
+  static constexpr int EV = 16 / sizeof(T);
+  static constexpr int VPR = COLS / EV;
+  static constexpr int RSTEP = NT / VPR;
+  static constexpr int NV = (ROWS + RSTEP - 1) / RSTEP;
+  static_assert(VPR > 0 && (VPR & (VPR - 1)) == 0 && NT % VPR == 0, "tile geometry");
+  uint32_t off[NV];
+  u32x4 r[NV];
+  __device__ __forceinline__ void init(int gld, int rvalid, int cvalid) {
+    const int row0 = (int)threadIdx.x / VPR, c = ((int)threadIdx.x % VPR) * EV;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int row = row0 + i * RSTEP;
+      const bool ok = row < ROWS && row < rvalid && c < cvalid;
+      off[i] = ok ? (uint32_t)(row * gld + c) * (uint32_t)sizeof(T) : 0x80000000u;
+    }
+  }
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+      r[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, off[i], 0, 0));
+  }
+  __device__ __forceinline__ void store(T *dst, int ld) const {
+    const int row0 = (int)threadIdx.x / VPR, c = ((int)threadIdx.x % VPR) * EV;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int row = row0 + i * RSTEP;
+      if (ROWS % RSTEP == 0 || row < ROWS) *(u32x4 *)(dst + row * ld + c) = r[i];
+    }
+  }
+};
+
 // XCD-aware block mapping: consecutive workgroup ids are dealt round-robin to
 // the 8 XCDs, so when the head count is a multiple of 8 the tiles of one head
 // are all given ids with the same residue mod 8 (one XCD, one L2), letting

@@ -1,185 +1,9 @@
-// gla_fwd.hip -- forward state pass + chunk output of the chunkwise GLA form,
-// and the step-by-step recurrent forward.
-//
-// fwd_main: one workgroup per (head, tile of Tv value columns), sequential
-// over the chunks (the non-materialised state pass of Sec. 3.3 / App. B,
-// Alg. 5).  Wave w keeps the fp32 state columns S[:, 16w .. 16w+16) of the
-// tile in matrix-core accumulators for the whole sequence.  The columns of S
-// evolve independently (the gate of Eq. 3 scales rows), so no state is shared
-// between workgroups.  For each chunk n, with the operands made by prep:
-//   O_n     = (Q (.) Lambda)_n S_[n] + P_n V_n          (Sec. 4.2; P holds the
-//                                                        intra-chunk part)
-//   S_[n+1] = Diag(gamma_n) S_[n] + (K (.) Gamma)_n^T V_n
+// gla_fwd.hip -- the step-by-step recurrent forward (Sec. 4.1, Eq. 3) and the
+// T = 0 state copy.  The chunkwise state pass lives in gla_vsweep.hip.
 #include "gla_common.hpp"
 #include "gla_launch.hpp"
 
 namespace gla {
-
-static int round_up(int x, int m) { return (x + m - 1) / m * m; }
-// Smallest power of two >= max(x, lo) (tile widths must be powers of two).
-static int pow2_at_least(int x, int lo) {
-  int p = lo;
-  while (p < x) p *= 2;
-  return p;
-}
-
-struct MainArgs {
-  const void *Qt, *Kt, *P, *v;
-  const float *gam, *S0;
-  void *o;
-  float *ST;
-  int BH, T, K, Kp, V, C, Cp, N, Tv, ntiles, ldk, ldv, ldp;
-};
-
-template <typename T, int KBP>
-__global__ void __launch_bounds__(256) fwd_main_kernel(MainArgs a) {
-  extern __shared__ __attribute__((aligned(16))) char smem[];
-  constexpr int NQ = sizeof(T) == 2 ? (KBP / 2 > 0 ? KBP / 2 : 1) : KBP;  // Q/K tile vectors per thread
-  constexpr int NX = sizeof(T) == 2 ? 2 : 4;                             // V and P tiles
-  int bh, tile;
-  xcd_map(a.BH, a.ntiles, bh, tile);
-  const int w = wave_id(), l = lane_id(), g = l >> 4, j = l & 15;
-  const int K = a.K, V = a.V, C = a.C, Cp = a.Cp, Kp = a.Kp;
-  const int ldk = a.ldk, ldv = a.ldv, ldp = a.ldp;
-  const int v0 = tile * a.Tv;
-  const bool active = 16 * w < a.Tv;  // waves beyond the tile width only help with loads
-  const int col = v0 + 16 * w + j;
-  const bool colv = active && col < V;
-  T *sQ = (T *)smem;
-  T *sK = sQ + Cp * ldk;
-  T *sV = sK + Cp * ldk;
-  T *sP = sV + Cp * ldv;
-  float *sGam = (float *)(sP + C * ldp);
-
-  f4 S[KBP];
-#pragma unroll
-  for (int kb = 0; kb < KBP; ++kb)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int kr = 16 * kb + 4 * g + r;
-      S[kb][r] = (a.S0 && kr < K && colv) ? a.S0[((int64_t)bh * K + kr) * V + col] : 0.f;
-    }
-
-  const T *Qt = (const T *)a.Qt, *Kt = (const T *)a.Kt, *Pm = (const T *)a.P;
-  const T *vin = (const T *)a.v;
-  T *o = (T *)a.o;
-  TileRegs<T, NQ> pq, pk;
-  TileRegs<T, NX> pv, pp;
-  float pg = 0.f;
-  const T *Qh = Qt + (int64_t)bh * a.T * K, *Kh = Kt + (int64_t)bh * a.T * K;
-  const T *vh = vin + (int64_t)bh * a.T * V + v0, *Ph = Pm + (int64_t)bh * a.N * C * C;
-  const float *gh = a.gam + (int64_t)bh * a.N * K;
-  auto load_chunk = [&](int n) {
-    const int rv = min(C, a.T - n * C);
-    pq.load(Qh + n * C * K, K, Cp, Kp, rv, K);
-    pk.load(Kh + n * C * K, K, Cp, Kp, rv, K);
-    pv.load(vh + n * C * V, V, Cp, a.Tv, rv, V - v0);
-    pp.load(Ph + n * C * C, C, C, Cp, C, C);
-    pg = (int)threadIdx.x < K ? gh[n * K + threadIdx.x] : 0.f;
-  };
-  load_chunk(0);
-  for (int n = 0; n < a.N; ++n) {
-    const int t0 = n * C, rv = min(C, a.T - t0);
-    const int64_t rb = (int64_t)bh * a.T + t0;
-    pq.store(sQ, ldk, Cp, Kp);
-    pk.store(sK, ldk, Cp, Kp);
-    pv.store(sV, ldv, Cp, a.Tv);
-    pp.store(sP, ldp, C, Cp);
-    if ((int)threadIdx.x < Kp) sGam[threadIdx.x] = pg;
-    __syncthreads();
-    if (n + 1 < a.N) load_chunk(n + 1);
-
-    if (active) {
-      const int nI = C / 16;
-      f4 acc[4] = {zero4(), zero4(), zero4(), zero4()};
-#pragma unroll
-      for (int s = 0; s < KBP / 2; ++s) {
-        const frag_t<T> bs = acc_frag<T>(S[2 * s], S[2 * s + 1]);
-#pragma unroll
-        for (int I = 0; I < 4; ++I)
-          if (I < nI) acc[I] = mma<T>(acc[I], ld_row_perm<T>(sQ, ldk, 16 * I, 32 * s), bs);
-      }
-#pragma unroll
-      for (int I = 0; I < 4; ++I) {
-        if (I >= nI) continue;
-        const int js = (16 * I + 16 + 31) >> 5;
-        for (int s = 0; s < js; ++s)
-          acc[I] = mma<T>(acc[I], ld_row<T>(sP, ldp, 16 * I, 32 * s), ld_col<T>(sV, ldv, 32 * s, 16 * w));
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = 16 * I + 4 * g + r;
-          if (row < rv && colv) o[(rb + row) * V + col] = cvt<T>(acc[I][r]);
-        }
-      }
-#pragma unroll
-      for (int kb = 0; kb < KBP; ++kb) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) S[kb][r] *= sGam[16 * kb + 4 * g + r];
-        for (int s = 0; s < Cp / 32; ++s)
-          S[kb] = mma<T>(S[kb], ld_col<T>(sK, ldk, 32 * s, 16 * kb), ld_col<T>(sV, ldv, 32 * s, 16 * w));
-      }
-    }
-    __syncthreads();
-  }
-  if (a.ST && colv) {
-#pragma unroll
-    for (int kb = 0; kb < KBP; ++kb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int kr = 16 * kb + 4 * g + r;
-        if (kr < K) a.ST[((int64_t)bh * K + kr) * V + col] = S[kb][r];
-      }
-  }
-}
-
-static void main_geometry(const Shape &s, int &Kp, int &Cp, int &Tv, int &ldk, int &ldv, int &ldp) {
-  Kp = pow2_at_least(s.K, 32);
-  Cp = round_up(s.C, 32);
-  Tv = pow2_at_least(s.V < 64 ? s.V : 64, 16);
-  const int pad = 32 / s.esz();
-  ldk = Kp + pad;
-  ldv = Tv + pad;
-  ldp = Cp + pad;
-}
-
-size_t lds_fwd_main(const Shape &s) {
-  int Kp, Cp, Tv, ldk, ldv, ldp;
-  main_geometry(s, Kp, Cp, Tv, ldk, ldv, ldp);
-  return (size_t)s.esz() * (2 * Cp * ldk + Cp * ldv + Cp * ldp) + (size_t)Kp * sizeof(float);
-}
-
-template <typename T, int KBP>
-static hipError_t launch_main_t(const MainArgs &a, int waves, size_t lds, hipStream_t st) {
-  static bool attr = false;
-  if (!attr) {
-    hipFuncSetAttribute((const void *)fwd_main_kernel<T, KBP>,
-                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    attr = true;
-  }
-  hipLaunchKernelGGL((fwd_main_kernel<T, KBP>), dim3(a.BH * a.ntiles), dim3(64 * waves), lds, st, a);
-  return hipGetLastError();
-}
-
-template <typename T>
-static hipError_t dispatch_main(const MainArgs &a, int waves, size_t lds, hipStream_t st) {
-  switch (a.Kp / 16) {
-    case 2: return launch_main_t<T, 2>(a, waves, lds, st);
-    case 4: return launch_main_t<T, 4>(a, waves, lds, st);
-    case 8: return launch_main_t<T, 8>(a, waves, lds, st);
-    default: return launch_main_t<T, 16>(a, waves, lds, st);
-  }
-}
-
-hipError_t launch_fwd_main(const Shape &s, const void *v, const float *S0, void *o, float *ST,
-                           const Work &w, hipStream_t st) {
-  MainArgs a;
-  a.Qt = w.Qt; a.Kt = w.Kt; a.P = w.P; a.v = v; a.gam = w.gam; a.S0 = S0; a.o = o; a.ST = ST;
-  a.BH = s.BH; a.T = s.T; a.K = s.K; a.V = s.V; a.C = s.C; a.N = s.N;
-  main_geometry(s, a.Kp, a.Cp, a.Tv, a.ldk, a.ldv, a.ldp);
-  a.ntiles = (s.V + a.Tv - 1) / a.Tv;
-  const size_t lds = lds_fwd_main(s);
-  return s.io == IO_BF16 ? dispatch_main<bf16>(a, 4, lds, st) : dispatch_main<float>(a, 4, lds, st);
-}
 
 // ------------------------------------------------------------- recurrent form
 // Eq. 3 one step at a time.  Workgroup = (64 value columns, head); thread

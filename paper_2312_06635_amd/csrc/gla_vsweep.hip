@@ -1,0 +1,331 @@
+// gla_vsweep.hip -- the two sweeps over chunks that tile the value columns:
+//
+//   forward state pass (Sec. 4.2; the non-materialised pass of Sec. 3.3 and
+//   App. B, Alg. 5), chunks n = 0 .. N-1:
+//       O_n     = (Q (.) Lambda)_n S_[n] + P_n V_n
+//       S_[n+1] = Diag(gamma_n) S_[n] + (K (.) Gamma)_n^T V_n
+//   backward dv pass (App. B, Alg. 4/6 as corrected: the dS recurrence uses
+//   Q (.) Lambda), chunks n = N-1 .. 0:
+//       dV_n    = (K (.) Gamma)_n dS_[n+1] + P_n^T dO_n
+//       dS_[n]  = Diag(gamma_n) dS_[n+1] + (Q (.) Lambda)_n^T dO_n
+//
+// Both have the same shape: a state R (S or dS, d_k x d_v, fp32) carried
+// across chunks, an output X_n R + intra, and an update R <- gamma R + Y_n^T Z_n.
+// The columns of R evolve independently (the gate of Eq. 3 scales rows), so a
+// workgroup owns a 64-column tile of one head for the whole sequence and no
+// state crosses workgroups.
+//
+// Workgroup = 8 waves.  Wave w owns value columns 16 (w & 3) .. +16 of the tile
+// and key features [ (w >> 2) KP/2, (w >> 2 + 1) KP/2 ) of R, held as fp32
+// matrix-core accumulators.  The output contraction over key features is thus
+// split between the two halves: the upper half hands its partial to the lower
+// half through LDS, and the lower half adds the intra-chunk term and writes
+// the output.
+//
+// Key-feature order inside the accumulators: accumulator pair (2s, 2s+1) of a
+// lane in group g holds features 32 s + 8 g + (0..7), so the pair is directly
+// the A operand of the next output product, whose B operand is then one
+// contiguous 16-byte LDS read.  The update's transposed operand is read with
+// LDS transpose reads pointed at the matching permuted columns (ld_col_perm).
+//
+// The output is computed transposed (value columns x time), so each lane ends
+// with four consecutive value columns of one time row: one 8-byte (bf16) or
+// 16-byte (fp32) store.
+//
+// Tiles of chunk n+1 are fetched with buffer loads into registers while chunk
+// n computes; each lane's byte offsets are fixed for the whole sweep (rows past
+// the sequence end fall outside the buffer's range and read as zero).
+#include "gla_common.hpp"
+#include "gla_launch.hpp"
+
+namespace gla {
+
+namespace {
+
+constexpr int kThreads = 512;
+constexpr int kTile = 64;  // value columns per workgroup
+
+static int pow2_at_least(int x, int lo) {
+  int p = lo;
+  while (p < x) p *= 2;
+  return p;
+}
+
+struct SweepArgs {
+  const void *X, *Y, *Z, *P;  // X: output operand, Y: update operand, Z: value tile source
+  const float *gam;
+  const float *R0;  // initial state (nullable)
+  void *out;
+  float *RN;        // final state (nullable)
+  int BH, T, K, V, C, N, ntiles;
+};
+
+template <typename T> struct Pads;
+template <> struct Pads<bf16> {
+  // Row strides chosen so that 16-byte row reads (X, P) and transpose reads
+  // (Y, Z) of a wave's 16-lane phase touch distinct LDS banks.
+  static constexpr int row = 8, col = 32;
+};
+template <> struct Pads<float> {
+  static constexpr int row = 4, col = 4;
+};
+
+template <typename T, int KP, int CP> struct SweepLayout {
+  static constexpr int LDX = KP + Pads<T>::row;
+  static constexpr int LDY = KP + Pads<T>::col;
+  static constexpr int LDZ = kTile + Pads<T>::col;
+  static constexpr int LDP = CP + Pads<T>::row;
+  static constexpr int NI = CP / 16;
+  static constexpr size_t offX = 0;
+  static constexpr size_t offY = offX + sizeof(T) * CP * LDX;
+  static constexpr size_t offZ = offY + sizeof(T) * CP * LDY;
+  static constexpr size_t offP = offZ + sizeof(T) * CP * LDZ;
+  static constexpr size_t offG = offP + sizeof(T) * CP * LDP;
+  static constexpr size_t offO = offG + sizeof(float) * KP;
+  static constexpr size_t total = offO + sizeof(f4) * 4 * NI * 64;
+};
+
+// Fragment whose reduction index runs down a column, like ld_col, but with the
+// 16 columns taken in the permuted key-feature order of the state
+// accumulators: lane (g, j) gets X[r0 + 8g + i][c0 + 8 (j / 4) + 4 h + j % 4].
+// For bf16 each transpose read returns, to lane j of a 16-lane group, element
+// j % 4 of the 4-vector loaded by lane 4 m + j / 4 (m = 0..3), so lane 4a + b
+// points at row r0 + 8g + a, column c0 + 8 b + 4 h.
+template <typename T>
+__device__ __forceinline__ frag_t<T> ld_col_perm(const T *X, int ld, int r0, int c0, int h) {
+  const int l = lane_id(), g = l >> 4, j = l & 15;
+  if constexpr (sizeof(T) == 2) {
+    const T *p0 = X + (r0 + 8 * g + (j >> 2)) * ld + c0 + 8 * (j & 3) + 4 * h;
+    const T *p1 = p0 + 4 * ld;
+    s4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4 *)(p0));
+    s4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4 *)(p1));
+    s8 r = s8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    return __builtin_bit_cast(bf16x8, r);
+  } else {
+    const T *p = X + (r0 + 8 * g) * ld + c0 + 8 * (j >> 2) + 4 * h + (j & 3);
+    f8 r;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) r[i] = p[i * ld];
+    return r;
+  }
+}
+
+template <typename T, int KP, int CP, bool REV>
+__global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
+  using L = SweepLayout<T, KP, CP>;
+  constexpr int KH = KP / 2;     // key features per wave half
+  constexpr int NKB = KH / 16;   // state accumulators per wave
+  constexpr int NS = KH / 32;    // 32-feature steps of the output contraction
+  constexpr int NI = CP / 16;    // 16-row time blocks of a chunk
+  constexpr int NSC = CP / 32;   // 32-row time steps of the update
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  T *sX = (T *)(smem + L::offX);
+  T *sY = (T *)(smem + L::offY);
+  T *sZ = (T *)(smem + L::offZ);
+  T *sP = (T *)(smem + L::offP);
+  float *sG = (float *)(smem + L::offG);
+  f4 *sO = (f4 *)(smem + L::offO);
+
+  int bh, tile;
+  xcd_map(a.BH, a.ntiles, bh, tile);
+  const int w = wave_id(), l = lane_id(), g = l >> 4, j = l & 15;
+  const int cg = w & 3, kh = w >> 2;
+  const int K = a.K, V = a.V, C = a.C, N = a.N;
+  const int v0 = tile * kTile;
+  const int cbase = 16 * cg;                // first column of this wave, tile-local
+  const bool active = v0 + cbase < V;       // V is a multiple of 16
+  const int fbase = kh * KH;
+  const int col = v0 + cbase + j;
+
+  // ---- state
+  f4 R[NKB];
+#pragma unroll
+  for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int f = fbase + 32 * (kb >> 1) + 8 * g + 4 * (kb & 1) + r;
+      R[kb][r] = (a.R0 && active && f < K) ? a.R0[((int64_t)bh * K + f) * V + col] : 0.f;
+    }
+
+  // ---- tile loaders (per-lane offsets fixed for the sweep)
+  TileLd<T, CP, KP, kThreads> lx, ly;
+  TileLd<T, CP, kTile, kThreads> lz;
+  TileLd<T, CP, CP, kThreads> lp;
+  lx.init(K, C, K);
+  ly.init(K, C, K);
+  lz.init(V, C, V - v0);
+  lp.init(C, C, C);
+  const int esz = sizeof(T);
+  const T *Xh = (const T *)a.X + (int64_t)bh * a.T * K;
+  const T *Yh = (const T *)a.Y + (int64_t)bh * a.T * K;
+  const T *Zh = (const T *)a.Z + (int64_t)bh * a.T * V + v0;
+  const T *Ph = (const T *)a.P + (int64_t)bh * N * C * C;
+  const float *Gh = a.gam + (int64_t)bh * N * K;
+  float pg = 0.f;
+  auto fetch = [&](int n) {
+    const int t0 = n * C;
+    const uint32_t remK = rsrc_bytes((int64_t)(a.T - t0) * K * esz);
+    lx.load(make_rsrc(Xh + (int64_t)t0 * K, remK));
+    ly.load(make_rsrc(Yh + (int64_t)t0 * K, remK));
+    lz.load(make_rsrc(Zh + (int64_t)t0 * V, rsrc_bytes(((int64_t)(a.T - t0) * V - v0) * esz)));
+    lp.load(make_rsrc(Ph + (int64_t)n * C * C, (uint32_t)(C * C * esz)));
+    pg = (int)threadIdx.x < K ? Gh[(int64_t)n * K + threadIdx.x] : 0.f;
+  };
+
+  T *outh = (T *)a.out + (int64_t)bh * a.T * V;
+  fetch(REV ? N - 1 : 0);
+  for (int it = 0; it < N; ++it) {
+    const int n = REV ? N - 1 - it : it;
+    const int t0 = n * C, rv = min(C, a.T - t0);
+    lx.store(sX, L::LDX);
+    ly.store(sY, L::LDY);
+    lz.store(sZ, L::LDZ);
+    lp.store(sP, L::LDP);
+    if ((int)threadIdx.x < KP) sG[threadIdx.x] = pg;
+    __syncthreads();
+    if (it + 1 < N) fetch(REV ? n - 1 : n + 1);
+
+    f4 acc[NI];
+#pragma unroll
+    for (int I = 0; I < NI; ++I) acc[I] = zero4();
+    if (active) {
+      // output, transposed: acc[I] = R^T X^T over this wave's key features
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        const frag_t<T> ra = acc_frag<T>(R[2 * s], R[2 * s + 1]);
+#pragma unroll
+        for (int I = 0; I < NI; ++I) acc[I] = mma<T>(acc[I], ra, ld_row<T>(sX, L::LDX, 16 * I, fbase + 32 * s));
+      }
+      if (kh == 0) {
+        // intra-chunk term: O += P V (forward) or dV += P^T dO (backward)
+#pragma unroll
+        for (int I = 0; I < NI; ++I) {
+          if constexpr (!REV) {
+#pragma unroll
+            for (int sc = 0; sc <= (16 * I + 15) / 32; ++sc)
+              acc[I] = mma<T>(acc[I], ld_col<T>(sZ, L::LDZ, 32 * sc, cbase), ld_row<T>(sP, L::LDP, 16 * I, 32 * sc));
+          } else {
+#pragma unroll
+            for (int sc = (16 * I) / 32; sc < NSC; ++sc)
+              acc[I] = mma<T>(acc[I], ld_col<T>(sZ, L::LDZ, 32 * sc, cbase), ld_col<T>(sP, L::LDP, 32 * sc, 16 * I));
+          }
+        }
+      } else {
+#pragma unroll
+        for (int I = 0; I < NI; ++I) sO[(cg * NI + I) * 64 + l] = acc[I];
+      }
+      // state update: R <- gamma R + Y^T Z
+      frag_t<T> zf[NSC];
+#pragma unroll
+      for (int sc = 0; sc < NSC; ++sc) zf[sc] = ld_col<T>(sZ, L::LDZ, 32 * sc, cbase);
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb) {
+        const int c0 = fbase + 32 * (kb >> 1);
+        const f4 gm = *(const f4 *)(sG + c0 + 8 * g + 4 * (kb & 1));
+        R[kb] *= gm;
+#pragma unroll
+        for (int sc = 0; sc < NSC; ++sc)
+          R[kb] = mma<T>(R[kb], ld_col_perm<T>(sY, L::LDY, 32 * sc, c0, kb & 1), zf[sc]);
+      }
+    }
+    __syncthreads();
+    if (active && kh == 0) {
+#pragma unroll
+      for (int I = 0; I < NI; ++I) {
+        const f4 o = acc[I] + sO[(cg * NI + I) * 64 + l];
+        const int row = 16 * I + j;
+        if (row < rv) {
+          T *dst = outh + (int64_t)(t0 + row) * V + v0 + cbase + 4 * g;
+          if constexpr (sizeof(T) == 2) {
+            bf16x4 ov = bf16x4{(bf16)o[0], (bf16)o[1], (bf16)o[2], (bf16)o[3]};
+            *(bf16x4 *)dst = ov;
+          } else {
+            *(f4 *)dst = o;
+          }
+        }
+      }
+    }
+  }
+  if (a.RN && active) {
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int f = fbase + 32 * (kb >> 1) + 8 * g + 4 * (kb & 1) + r;
+        if (f < K) a.RN[((int64_t)bh * K + f) * V + col] = R[kb][r];
+      }
+  }
+}
+
+int sweep_kp(const Shape &s) { return pow2_at_least(s.K, 64); }
+int sweep_cp(const Shape &s) { return s.C <= 32 ? 32 : 64; }
+
+template <typename T, int KP, int CP>
+size_t sweep_lds() { return SweepLayout<T, KP, CP>::total; }
+
+size_t sweep_lds(const Shape &s) {
+  const int KP = sweep_kp(s), CP = sweep_cp(s);
+  if (KP > 256 || s.C > 64) return 0;
+  const bool b = s.io == IO_BF16;
+  if (!b && KP > 128) return 0;
+#define GLA_LDS_CASE(kp, cp) \
+  if (KP == kp && CP == cp) return b ? sweep_lds<bf16, kp, cp>() : sweep_lds<float, kp, cp>();
+  GLA_LDS_CASE(64, 32) GLA_LDS_CASE(64, 64) GLA_LDS_CASE(128, 32) GLA_LDS_CASE(128, 64)
+  GLA_LDS_CASE(256, 32) GLA_LDS_CASE(256, 64)
+#undef GLA_LDS_CASE
+  return 0;
+}
+
+template <typename T, int KP, int CP, bool REV>
+hipError_t launch_sweep_t(const SweepArgs &a, hipStream_t st) {
+  static bool attr = false;
+  const size_t lds = SweepLayout<T, KP, CP>::total;
+  if (!attr) {
+    (void)hipFuncSetAttribute((const void *)sweep_kernel<T, KP, CP, REV>,
+                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    attr = true;
+  }
+  hipLaunchKernelGGL((sweep_kernel<T, KP, CP, REV>), dim3(a.BH * a.ntiles), dim3(kThreads), lds, st, a);
+  return hipGetLastError();
+}
+
+template <typename T, bool REV>
+hipError_t dispatch_sweep(const Shape &s, const SweepArgs &a, hipStream_t st) {
+  const int KP = sweep_kp(s), CP = sweep_cp(s);
+#define GLA_SWEEP_CASE(kp, cp) \
+  if (KP == kp && CP == cp) return launch_sweep_t<T, kp, cp, REV>(a, st);
+  GLA_SWEEP_CASE(64, 32) GLA_SWEEP_CASE(64, 64) GLA_SWEEP_CASE(128, 32) GLA_SWEEP_CASE(128, 64)
+  if constexpr (sizeof(T) == 2) {
+    GLA_SWEEP_CASE(256, 32) GLA_SWEEP_CASE(256, 64)
+  }
+#undef GLA_SWEEP_CASE
+  return hipErrorInvalidValue;
+}
+
+SweepArgs sweep_args(const Shape &s) {
+  SweepArgs a{};
+  a.BH = s.BH; a.T = s.T; a.K = s.K; a.V = s.V; a.C = s.C; a.N = s.N;
+  a.ntiles = (s.V + kTile - 1) / kTile;
+  return a;
+}
+
+}  // namespace
+
+size_t lds_fwd_main(const Shape &s) { return sweep_lds(s); }
+size_t lds_bwd_dv(const Shape &s) { return sweep_lds(s); }
+
+hipError_t launch_fwd_main(const Shape &s, const void *v, const float *S0, void *o, float *ST,
+                           const Work &w, hipStream_t st) {
+  SweepArgs a = sweep_args(s);
+  a.X = w.Qt; a.Y = w.Kt; a.Z = v; a.P = w.P; a.gam = w.gam; a.R0 = S0; a.out = o; a.RN = ST;
+  return s.io == IO_BF16 ? dispatch_sweep<bf16, false>(s, a, st) : dispatch_sweep<float, false>(s, a, st);
+}
+
+hipError_t launch_bwd_dv(const Shape &s, const void *dO, const float *dST, void *dv, float *dS0,
+                         const Work &w, hipStream_t st) {
+  SweepArgs a = sweep_args(s);
+  a.X = w.Kt; a.Y = w.Qt; a.Z = dO; a.P = w.P; a.gam = w.gam; a.R0 = dST; a.out = dv; a.RN = dS0;
+  return s.io == IO_BF16 ? dispatch_sweep<bf16, true>(s, a, st) : dispatch_sweep<float, true>(s, a, st);
+}
+
+}  // namespace gla
