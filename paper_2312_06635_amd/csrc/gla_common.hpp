@@ -261,6 +261,13 @@ template <typename T, int ROWS, int COLS, int NT> struct TileLd {
     for (int i = 0; i < NV; ++i)
       r[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, off[i], 0, 0));
   }
+  // Same, additionally reading columns >= cvalid as zero.
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs, int cvalid) {
+    const bool ok = ((int)threadIdx.x % VPR) * EV < cvalid;
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+      r[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, ok ? off[i] : 0x80000000u, 0, 0));
+  }
   __device__ __forceinline__ void store(T *dst, int ld) const {
     const int row0 = (int)threadIdx.x / VPR, c = ((int)threadIdx.x % VPR) * EV;
 #pragma unroll
