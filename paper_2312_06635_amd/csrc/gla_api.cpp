@@ -70,6 +70,7 @@ size_t layout(const Shape &s, int op, char *base, Work *w) {
   void *Kt = take(rows * s.K * es);
   void *P = take(chunks * s.C * s.C * es);
   void *gam = take(chunks * s.K * sizeof(float));
+  void *wflag = take(chunks * 4);
   void *dP = nullptr, *cST = nullptr, *dq_lo = nullptr;
   if (op == 1) {
     dP = take(chunks * s.C * s.C * sizeof(float));
@@ -77,7 +78,7 @@ size_t layout(const Shape &s, int op, char *base, Work *w) {
     if (s.io == gla::IO_BF16) dq_lo = take(rows * s.K * 2);
   }
   if (w) {
-    w->Qt = Qt; w->Kt = Kt; w->P = P; w->gam = (float *)gam;
+    w->Qt = Qt; w->Kt = Kt; w->P = P; w->gam = (float *)gam; w->wflag = (unsigned char *)wflag;
     w->dP = (float *)dP; w->cST = (float *)cST; w->dq_lo = dq_lo;
   }
   return off;

@@ -21,6 +21,7 @@ struct Work {
   void *Kt = nullptr;     // [BH][T][K] io : k (.) Gamma    (Gamma  = b_{chunk end} / b_t)
   void *P = nullptr;      // [BH][N][C][C] io : intra-chunk matrix, lower triangle
   float *gam = nullptr;   // [BH][N][K] fp32 : chunk decay gamma = b_{chunk end} / b_{chunk start}
+  unsigned char *wflag = nullptr;  // [BH][N][4] : diagonal block of P needs pairwise decays
   float *dP = nullptr;    // [BH][N][C][C] fp32 : (dO V^T) (.) M per chunk (backward)
   float *cST = nullptr;   // [BH][K] fp32 : rowsum(S_T (.) dS_T) (backward)
   void *dq_lo = nullptr;  // [BH][T][K] bf16 : dq - bf16(dq), so dq reaches the gate gradient

@@ -13,13 +13,15 @@
 //     normalised at block boundaries, so that every exponent is <= 0:
 //       (q_I (.) exp(B - z_I)) diag(exp(z_I - zend_J)) (k_J (.) exp(zend_J - B))^T
 //     with z_I the log decay at the start of block I and zend_J at the end of J.
-//   * I = J ("pink", inside a sub-chunk): fp32 on the vector ALUs, no matrix
-//     cores.  The pairwise decay exp(B_i - B_j) is split at the block start as
-//     exp(B_i - z) exp(z - B_j); the second factor grows with the block's own
-//     decay, so when that exceeds exp(kWideRange) for any feature the block
-//     falls back to one exponential per (i, j, k) triple.
-// Sub-chunks shorter than 16 (c < 16) lie inside the diagonal blocks and are
-// therefore evaluated in fp32 too.
+//   * I = J ("pink", inside a sub-chunk): the pairwise decay exp(B_i - B_j) is
+//     split at the block start as exp(B_i - z) exp(z - B_j), which makes the
+//     block a matrix-core product of (q (.) exp(B - z)) and (k (.) exp(z - B));
+//     the second factor grows with the block's own decay, so when that
+//     exceeds exp(kWideRange) for any feature the block is left to
+//     prep_wide_kernel, which forms one exponential per (i, j, k) triple in
+//     fp32 on the vector ALUs.  A per-block flag in the workspace marks those
+//     blocks.
+// Sub-chunks shorter than 16 (c < 16) lie inside the diagonal blocks.
 #include "gla_common.hpp"
 #include "gla_launch.hpp"
 
@@ -31,6 +33,7 @@ struct PrepArgs {
   const void *q, *k, *la;
   void *Qt, *Kt, *P;
   float *gam;
+  unsigned char *wflag;  // [BH][N][4]: diagonal block needs pairwise decays
   int T, K, Kp, C, N, ldk;
 };
 
@@ -101,6 +104,7 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
   T *sKs = sQh + C * ldk;
   float *sTot = (float *)(sKs + C * ldk);  // [nb][Kp] per-block sums of log alpha
   float *sG = sTot + 4 * Kp;              // [3][Kp] exp(sum of tot strictly between I and J)
+  float *sEup = sG + 3 * Kp;              // [nb][Kp] exp(-tot): pink operand scale
 
   const T *q = (const T *)a.q + base, *k = (const T *)a.k + base, *la = (const T *)a.la + base;
   T *Qt = (T *)a.Qt + base, *Kt = (T *)a.Kt + base;
@@ -156,16 +160,17 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
   }
 
   // 2. gated operands.
-  float qh[16][FPL], kh[16][FPL];
   bool wide = false;
-  float ez[FPL], ekt[FPL], eup[FPL];
+  float ez[FPL], ekt[FPL];
 #pragma unroll
   for (int f = 0; f < FPL; ++f) {
     ez[f] = __expf(pre[f]);                    // b_{block start} / b_{chunk start}
     ekt[f] = __expf(Bl[f] - pre[f] - tot[f]);  // b_{chunk end} / b_{block end}
-    eup[f] = __expf(-tot[f]);                  // b_{block start} / b_{block end} >= 1
     if (fv && -tot[f] > kWideRange) wide = true;
+    if (fp) sEup[w * Kp + k0 + f] = __expf(-tot[f]);  // b_{block start} / b_{block end} >= 1
   }
+  const bool wide_blk = __any(wide);
+  if (l == 0) a.wflag[((int64_t)bh * a.N + n) * 4 + w] = wide_blk ? 1 : 0;
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const int row = 16 * w + r;
@@ -177,8 +182,6 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
     for (int f = 0; f < FPL; ++f) {
       const float qhv = qv[f] * __expf(Bloc[r][f]);           // <= |q|
       const float ksv = kv[f] * __expf(tot[f] - Bloc[r][f]);  // <= |k|
-      qh[r][f] = qhv;
-      kh[r][f] = ksv * eup[f];
       o1[f] = qhv * ez[f];
       o2[f] = ksv * ekt[f];
       o3[f] = qhv;
@@ -202,138 +205,134 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
     for (int f = 0; f < FPL; ++f) gp[f] = gv[f];
   }
 
-  // 3. diagonal ("pink") block w in fp32.
+  // zeros: strict upper triangle of the diagonal block and every block J > w
   const int d0 = 16 * w;
   {
-    float x[64];
-    float r0, r1, rt = 0.f;
-    if (!__any(wide)) {
+    const int i = l >> 2;
 #pragma unroll
-      for (int e = 0; e < 64; ++e) {
-        float s = 0.f;
-#pragma unroll
-        for (int f = 0; f < FPL; ++f) s += qh[tri_row(e)][f] * kh[tri_col(e)][f];
-        x[e] = s;
-      }
-      r0 = reduce_scatter64(x);
-#pragma unroll
-      for (int e = 0; e < 64; ++e) {
-        float s = 0.f;
-#pragma unroll
-        for (int f = 0; f < FPL; ++f) s += qh[tri_row(64 + e)][f] * kh[tri_col(64 + e)][f];
-        x[e] = s;
-      }
-      r1 = reduce_scatter64(x);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        float s = 0.f;
-#pragma unroll
-        for (int f = 0; f < FPL; ++f) s += qh[tri_row(128 + e)][f] * kh[tri_col(128 + e)][f];
-        s = allreduce64(s);
-        if (l == e) rt = s;
-      }
-    } else {
-      // Large decay inside the block: one exponential per (i, j, k).
-      float qv[16][FPL], kv[16][FPL], Bv[16][FPL];
-      float c[FPL];
-#pragma unroll
-      for (int f = 0; f < FPL; ++f) c[f] = 0.f;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = d0 + r;
-        const bool ok = fv && row < rv;
-        float xl[FPL];
-        ldvec<T, FPL>(la + row * K + k0, ok, xl);
-        ldvec<T, FPL>(q + row * K + k0, ok, qv[r]);
-        ldvec<T, FPL>(k + row * K + k0, ok, kv[r]);
-#pragma unroll
-        for (int f = 0; f < FPL; ++f) {
-          c[f] += xl[f];
-          Bv[r][f] = c[f];
-        }
-      }
-#pragma unroll
-      for (int e = 0; e < 64; ++e) {
-        float s = 0.f;
-        const int i = tri_row(e), jj = tri_col(e);
-#pragma unroll
-        for (int f = 0; f < FPL; ++f) s += qv[i][f] * kv[jj][f] * __expf(Bv[i][f] - Bv[jj][f]);
-        x[e] = s;
-      }
-      r0 = reduce_scatter64(x);
-#pragma unroll
-      for (int e = 0; e < 64; ++e) {
-        float s = 0.f;
-        const int i = tri_row(64 + e), jj = tri_col(64 + e);
-#pragma unroll
-        for (int f = 0; f < FPL; ++f) s += qv[i][f] * kv[jj][f] * __expf(Bv[i][f] - Bv[jj][f]);
-        x[e] = s;
-      }
-      r1 = reduce_scatter64(x);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        float s = 0.f;
-        const int i = tri_row(128 + e), jj = tri_col(128 + e);
-#pragma unroll
-        for (int f = 0; f < FPL; ++f) s += qv[i][f] * kv[jj][f] * __expf(Bv[i][f] - Bv[jj][f]);
-        s = allreduce64(s);
-        if (l == e) rt = s;
-      }
+    for (int c4 = 0; c4 < 4; ++c4) {
+      const int jj = 4 * (l & 3) + c4;
+      if (jj > i) Pg[(d0 + i) * C + d0 + jj] = cvt<T>(0.f);
     }
-    Pg[(d0 + tri_row(l)) * C + d0 + tri_col(l)] = cvt<T>(r0);
-    Pg[(d0 + tri_row(64 + l)) * C + d0 + tri_col(64 + l)] = cvt<T>(r1);
-    if (l < 8) Pg[(d0 + tri_row(128 + l)) * C + d0 + tri_col(128 + l)] = cvt<T>(rt);
-    // zeros: strict upper triangle of the diagonal block and every block J > w
-    {
-      const int i = l >> 2;
-#pragma unroll
-      for (int c4 = 0; c4 < 4; ++c4) {
-        const int jj = 4 * (l & 3) + c4;
-        if (jj > i) Pg[(d0 + i) * C + d0 + jj] = cvt<T>(0.f);
-      }
-      for (int idx = l; idx < 16 * (C - d0 - 16); idx += 64) {
-        const int rr = idx / (C - d0 - 16), cc = idx - rr * (C - d0 - 16);
-        Pg[(d0 + rr) * C + d0 + 16 + cc] = cvt<T>(0.f);
-      }
+    for (int idx = l; idx < 16 * (C - d0 - 16); idx += 64) {
+      const int rr = idx / (C - d0 - 16), cc = idx - rr * (C - d0 - 16);
+      Pg[(d0 + rr) * C + d0 + 16 + cc] = cvt<T>(0.f);
     }
   }
   __syncthreads();
 
-  // 4. off-diagonal ("orange") blocks (w, J < w) on the matrix cores.
-  for (int J = 0; J < w; ++J) {
+  // 3. blocks (w, J <= w) on the matrix cores: orange below the diagonal,
+  //    pink on it (unless the block needs pairwise decays).
+  for (int J = 0; J <= w; ++J) {
+    if (J == w && wide_blk) break;
     f4 acc = zero4();
     for (int s = 0; s < Kp / 32; ++s) {
       frag_t<T> af = ld_row(sQh, ldk, d0, 32 * s);
+      frag_t<T> bf = ld_row(sKs, ldk, 16 * J, 32 * s);
       if (J <= w - 2) {
         const float *gp = sG + pair_index(w, J) * Kp + 32 * s + 8 * g;
 #pragma unroll
         for (int i = 0; i < 8; ++i) af[i] = cvt<T>((float)af[i] * gp[i]);
+      } else if (J == w) {
+        const float *ep = sEup + w * Kp + 32 * s + 8 * g;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) bf[i] = cvt<T>((float)bf[i] * ep[i]);
       }
-      frag_t<T> bf = ld_row(sKs, ldk, 16 * J, 32 * s);
       acc = mma<T>(acc, af, bf);
     }
 #pragma unroll
-    for (int r = 0; r < 4; ++r) Pg[(d0 + 4 * g + r) * C + 16 * J + j16] = cvt<T>(acc[r]);
+    for (int r = 0; r < 4; ++r) {
+      const int row = 4 * g + r;
+      if (J < w || j16 <= row) Pg[(d0 + row) * C + 16 * J + j16] = cvt<T>(acc[r]);
+    }
   }
+}
+
+// Diagonal blocks whose decay range is too large for the factorised form:
+// P[i][j] = sum_k q_ik k_jk exp(B_ik - B_jk), one exponential per term, fp32,
+// reduced across the lanes that own the features.
+template <typename T, int FPL>
+__global__ void __launch_bounds__(256) prep_wide_kernel(PrepArgs a) {
+  const int n = blockIdx.x, bh = blockIdx.y;
+  const int w = wave_id(), l = lane_id();
+  if (!a.wflag[((int64_t)bh * a.N + n) * 4 + w]) return;
+  const int C = a.C, K = a.K;
+  const int t0 = n * C, rv = min(C, a.T - t0), d0 = 16 * w;
+  const int64_t base = ((int64_t)bh * a.T + t0) * K;
+  const T *q = (const T *)a.q + base, *k = (const T *)a.k + base, *la = (const T *)a.la + base;
+  T *Pg = (T *)a.P + ((int64_t)bh * a.N + n) * C * C;
+  const int k0 = FPL * l;
+  const bool fv = k0 < K;
+  float qv[16][FPL], kv[16][FPL], Bv[16][FPL], c[FPL];
+#pragma unroll
+  for (int f = 0; f < FPL; ++f) c[f] = 0.f;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int row = d0 + r;
+    const bool ok = fv && row < rv;
+    float xl[FPL];
+    ldvec<T, FPL>(la + row * K + k0, ok, xl);
+    ldvec<T, FPL>(q + row * K + k0, ok, qv[r]);
+    ldvec<T, FPL>(k + row * K + k0, ok, kv[r]);
+#pragma unroll
+    for (int f = 0; f < FPL; ++f) {
+      c[f] += xl[f];
+      Bv[r][f] = c[f];
+    }
+  }
+  float x[64], r0, r1, rt = 0.f;
+#pragma unroll
+  for (int e = 0; e < 64; ++e) {
+    float s = 0.f;
+    const int i = tri_row(e), jj = tri_col(e);
+#pragma unroll
+    for (int f = 0; f < FPL; ++f) s += qv[i][f] * kv[jj][f] * __expf(Bv[i][f] - Bv[jj][f]);
+    x[e] = s;
+  }
+  r0 = reduce_scatter64(x);
+#pragma unroll
+  for (int e = 0; e < 64; ++e) {
+    float s = 0.f;
+    const int i = tri_row(64 + e), jj = tri_col(64 + e);
+#pragma unroll
+    for (int f = 0; f < FPL; ++f) s += qv[i][f] * kv[jj][f] * __expf(Bv[i][f] - Bv[jj][f]);
+    x[e] = s;
+  }
+  r1 = reduce_scatter64(x);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    float s = 0.f;
+    const int i = tri_row(128 + e), jj = tri_col(128 + e);
+#pragma unroll
+    for (int f = 0; f < FPL; ++f) s += qv[i][f] * kv[jj][f] * __expf(Bv[i][f] - Bv[jj][f]);
+    s = allreduce64(s);
+    if (l == e) rt = s;
+  }
+  Pg[(d0 + tri_row(l)) * C + d0 + tri_col(l)] = cvt<T>(r0);
+  Pg[(d0 + tri_row(64 + l)) * C + d0 + tri_col(64 + l)] = cvt<T>(r1);
+  if (l < 8) Pg[(d0 + tri_row(128 + l)) * C + d0 + tri_col(128 + l)] = cvt<T>(rt);
 }
 
 static int round_up(int x, int m) { return (x + m - 1) / m * m; }
 
 size_t lds_prep(const Shape &s) {
   const int Kp = round_up(s.K, 32), ldk = Kp + 32 / s.esz();
-  return (size_t)2 * s.C * ldk * s.esz() + (size_t)7 * Kp * sizeof(float);
+  return (size_t)2 * s.C * ldk * s.esz() + (size_t)11 * Kp * sizeof(float);
 }
 
 template <typename T, int FPL>
 static hipError_t launch_prep_t(const Shape &s, const PrepArgs &a, size_t lds, hipStream_t st) {
   static bool attr = false;
   if (!attr) {
-    hipFuncSetAttribute((const void *)prep_kernel<T, FPL>,
+    (void)hipFuncSetAttribute((const void *)prep_kernel<T, FPL>,
                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     attr = true;
   }
   dim3 grid(s.N, s.BH), block(64 * (s.C / 16));
   hipLaunchKernelGGL((prep_kernel<T, FPL>), grid, block, lds, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((prep_wide_kernel<T, FPL>), grid, block, 0, st, a);
   return hipGetLastError();
 }
 
@@ -341,7 +340,7 @@ hipError_t launch_prep(const Shape &s, const void *q, const void *k, const void 
                        const Work &w, hipStream_t st) {
   PrepArgs a;
   a.q = q; a.k = k; a.la = la;
-  a.Qt = w.Qt; a.Kt = w.Kt; a.P = w.P; a.gam = w.gam;
+  a.Qt = w.Qt; a.Kt = w.Kt; a.P = w.P; a.gam = w.gam; a.wflag = w.wflag;
   a.T = s.T; a.K = s.K; a.Kp = round_up(s.K, 32); a.C = s.C; a.N = s.N;
   a.ldk = a.Kp + 32 / s.esz();
   const size_t lds = lds_prep(s);
