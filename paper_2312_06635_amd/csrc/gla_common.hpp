@@ -268,6 +268,17 @@ template <typename T, int ROWS, int COLS, int NT> struct TileLd {
     for (int i = 0; i < NV; ++i)
       r[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, ok ? off[i] : 0x80000000u, 0, 0));
   }
+  // store() into a tile whose 16-byte chunks are XOR-swizzled per row: chunk
+  // c of row r lands at chunk c ^ (((r & 3) << 2) | ((r >> 2) & 3)).
+  __device__ __forceinline__ void store_swz(T *dst, int ld) const {
+    const int row0 = (int)threadIdx.x / VPR, ch = (int)threadIdx.x % VPR;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int row = row0 + i * RSTEP;
+      const int cs = ch ^ (((row & 3) << 2) | ((row >> 2) & 3));
+      if (ROWS % RSTEP == 0 || row < ROWS) *(u32x4 *)(dst + row * ld + cs * EV) = r[i];
+    }
+  }
   __device__ __forceinline__ void store(T *dst, int ld) const {
     const int row0 = (int)threadIdx.x / VPR, c = ((int)threadIdx.x % VPR) * EV;
 #pragma unroll

@@ -53,32 +53,35 @@ struct KsArgs {
 template <typename T, int CP> struct KsLayout {
   static constexpr bool DB = sizeof(T) == 2;  // double-buffered slabs (fp32 tiles are too big)
   static constexpr int NBUF = DB ? 2 : 1;
-  static constexpr int LDV = kVS + (sizeof(T) == 2 ? 8 : 4);
-  static constexpr int LDK = kKF + (sizeof(T) == 2 ? 16 : 4);
-  static constexpr int LDF = kKF + 1;  // fp32 per-thread tiles
-  static constexpr int LDO = kKF + 4;  // fp32 tiles read as fragments
-  static constexpr int LDP = CP + 4;
+  static constexpr int LDV = kVS;  // slab rows are XOR-swizzled, not padded
   static constexpr int NB = CP / 16, NRG = CP / 4;
+  // Per-(row, feature) tiles are stored feature-major ([32 features][rows]),
+  // so a factor/final thread's four consecutive rows of one feature and a
+  // fragment's eight consecutive rows are single 8/16-byte LDS accesses.
+  static constexpr int LDT = CP + 4;                        // fp32 feature-major tiles
+  static constexpr int LDTB = CP + (sizeof(T) == 2 ? 8 : 4);  // T feature-major tiles
+  static constexpr int LDP = CP + 4;                        // dP (dq: [t][s]; dk: [s][t])
+  static constexpr int LDRG = NRG + 4;                      // row-group sums [32][NRG]
   static constexpr size_t slab = sizeof(T) * CP * LDV;
   static constexpr size_t offV = 0;
   static constexpr size_t offD = offV + NBUF * slab;
-  static constexpr size_t offBh = offD + NBUF * slab;                   // gated update operand (hi)
-  static constexpr size_t offBl = offBh + sizeof(T) * CP * LDK;         // (lo, bf16 only)
-  static constexpr size_t offO = offBl + (DB ? sizeof(T) * CP * LDK : 0);  // orange operand
-  static constexpr size_t offPk = offO + 4 * CP * LDO;                  // pink operand
-  static constexpr size_t offBloc = offPk + 4 * CP * LDO;               // block-local cumsum
-  static constexpr size_t offdP = offBloc + 4 * CP * LDF;
-  static constexpr size_t offRed = offdP + 4 * CP * LDP;                // two partial sums
-  static constexpr size_t offOr = offRed + 2 * 4 * CP * LDF;            // orange results
-  static constexpr size_t offRg = offOr + 4 * CP * LDF;                 // row-group totals [NRG][32]
-  static constexpr size_t offSc = offRg + 4 * NRG * kKF;                // per-block scale [NB][32]
-  static constexpr size_t offGp = offSc + 4 * NB * kKF;                 // pair factors [3][32]
-  static constexpr size_t offG = offGp + 4 * 3 * kKF;                   // gamma [32]
-  static constexpr size_t offCar = offG + 4 * kKF;                      // carry [2][32]
-  static constexpr size_t offRedS = offCar + 4 * 2 * kKF;               // final-state sums [8][32]
-  static constexpr size_t offFt = offRedS + 4 * 8 * kKF;                // per-thread block decay [NRG][32]
-  static constexpr size_t offGrp = offFt + 4 * NRG * kKF;               // dk: row-group sums of dA
-  static constexpr size_t total = offGrp + 4 * NRG * kKF;
+  static constexpr size_t offBh = offD + NBUF * slab;                    // gated update operand (hi)
+  static constexpr size_t offBl = offBh + sizeof(T) * kKF * LDTB;        // (lo, bf16 only)
+  static constexpr size_t offO = offBl + (DB ? sizeof(T) * kKF * LDTB : 0);  // orange operand
+  static constexpr size_t offPk = offO + 4 * kKF * LDT;                  // pink operand
+  static constexpr size_t offBloc = offPk + 4 * kKF * LDT;               // block-local cumsum
+  static constexpr size_t offdP = offBloc + 4 * kKF * LDT;
+  static constexpr size_t offRed = offdP + 4 * CP * LDP;                 // two partial sums
+  static constexpr size_t offOr = offRed + 2 * 4 * kKF * LDT;            // intra-chunk results
+  static constexpr size_t offRg = offOr + 4 * kKF * LDT;                 // row-group totals
+  static constexpr size_t offSc = offRg + 4 * kKF * LDRG;                // per-block scale [NB][32]
+  static constexpr size_t offGp = offSc + 4 * NB * kKF;                  // pair factors [3][32]
+  static constexpr size_t offG = offGp + 4 * 3 * kKF;                    // gamma [32]
+  static constexpr size_t offCar = offG + 4 * kKF;                       // carry [2][32]
+  static constexpr size_t offRedS = offCar + 4 * 2 * kKF;                // final-state sums [8][32]
+  static constexpr size_t offFt = offRedS + 4 * 8 * kKF;                 // per-thread block decay [NRG][32]
+  static constexpr size_t offGrp = offFt + 4 * NRG * kKF;                // dk: row-group sums of dA
+  static constexpr size_t total = offGrp + 4 * kKF * LDRG;
 };
 
 // (I, J) of lower-triangular block b (row-major) and of upper block u.
@@ -113,6 +116,53 @@ __device__ __forceinline__ frag_t<T> ld_col_perm(const T *X, int ld, int r0, int
   }
 }
 
+// Slab tiles (V, dO) are stored with their 16-byte chunks XOR-swizzled per
+// row, chunk c of row r at c ^ swz(r): both the 16-row fragment reads (one
+// chunk of 16 consecutive rows) and the transpose reads (4 rows x 4 chunks)
+// then touch distinct LDS banks without padding.
+__device__ __forceinline__ int swz(int row) { return ((row & 3) << 2) | ((row >> 2) & 3); }
+template <typename T> __device__ __forceinline__ int sw_off(int row, int col, int ld) {
+  constexpr int EV = 16 / sizeof(T);
+  return row * ld + ((col / EV) ^ swz(row)) * EV + col % EV;
+}
+
+// ld_row on a swizzled tile: lane (g, j) gets X[r0 + j][c0 + 8g + i].
+template <typename T>
+__device__ __forceinline__ frag_t<T> ld_row_sw(const T *X, int ld, int r0, int c0) {
+  const int l = lane_id(), row = r0 + (l & 15), col = c0 + 8 * (l >> 4);
+  if constexpr (sizeof(T) == 2) {
+    return *(const bf16x8 *)(X + sw_off<T>(row, col, ld));
+  } else {
+    const f4 a = *(const f4 *)(X + sw_off<T>(row, col, ld)), b = *(const f4 *)(X + sw_off<T>(row, col + 4, ld));
+    return f8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  }
+}
+
+// ld_col_perm on a swizzled tile.
+template <typename T>
+__device__ __forceinline__ frag_t<T> ld_col_perm_sw(const T *X, int ld, int r0, int c0, int h) {
+  const int l = lane_id(), g = l >> 4, j = l & 15;
+  if constexpr (sizeof(T) == 2) {
+    const int row = r0 + 8 * g + (j >> 2), col = c0 + 8 * (j & 3) + 4 * h;
+    s4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4 *)(X + sw_off<T>(row, col, ld)));
+    s4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4 *)(X + sw_off<T>(row + 4, col, ld)));
+    s8 r = s8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    return __builtin_bit_cast(bf16x8, r);
+  } else {
+    const int row = r0 + 8 * g, col = c0 + 8 * (j >> 2) + 4 * h + (j & 3);
+    f8 r;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) r[i] = X[sw_off<T>(row + i, col, ld)];
+    return r;
+  }
+}
+
+// Four consecutive elements as one 8-byte (bf16) or 16-byte (fp32) LDS store.
+template <typename T> __device__ __forceinline__ void store4(T *p, const T (&v)[4]) {
+  if constexpr (sizeof(T) == 2) *(bf16x4 *)p = bf16x4{v[0], v[1], v[2], v[3]};
+  else *(f4 *)p = f4{v[0], v[1], v[2], v[3]};
+}
+
 // hi + lo = the fp32 accumulator pair to ~16 mantissa bits (lo unused for fp32).
 template <typename T>
 __device__ __forceinline__ void acc_split(f4 a0, f4 a1, frag_t<T> &hi, frag_t<T> &lo) {
@@ -127,21 +177,12 @@ __device__ __forceinline__ void acc_split(f4 a0, f4 a1, frag_t<T> &hi, frag_t<T>
   }
 }
 
-// fp32 fragments from fp32 LDS tiles: row X[r0 + j][c0 + 8g + i], column
-// X[r0 + 8g + i][c0 + j].
+// fp32 fragment from an fp32 LDS tile: lane (g, j) gets X[r0 + j][c0 + 8g + i].
 __device__ __forceinline__ f8 ldf_row(const float *X, int ld, int r0, int c0) {
   const int l = lane_id();
   const float *p = X + (r0 + (l & 15)) * ld + c0 + 8 * (l >> 4);
   const f4 a = *(const f4 *)p, b = *(const f4 *)(p + 4);
   return f8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
-}
-__device__ __forceinline__ f8 ldf_col(const float *X, int ld, int r0, int c0) {
-  const int l = lane_id();
-  const float *p = X + (r0 + 8 * (l >> 4)) * ld + c0 + (l & 15);
-  f8 r;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) r[i] = p[i * ld];
-  return r;
 }
 
 // acc += a b for fp32 fragments; on the bf16 path both are split into hi + lo
@@ -183,16 +224,23 @@ struct Factors {
   bool wide;
 };
 
-template <int NRG>
+template <int NRG, int LDRG>
 __device__ __forceinline__ Factors chunk_factors(const float *sRg, const float (&c)[4], int frg, int fk,
                                                  bool fv) {
   Factors f;
   const int blk = frg >> 2;
   float ex = 0.f;
   f.pre = f.tot = f.blast = 0.f;
+  float rg[NRG];
+#pragma unroll
+  for (int p = 0; p < NRG; p += 4) {
+    const f4 v = *(const f4 *)(sRg + fk * LDRG + p);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) rg[p + e] = v[e];
+  }
 #pragma unroll
   for (int p = 0; p < NRG; ++p) {
-    const float t = sRg[p * kKF + fk];
+    const float t = rg[p];
     f.blast += t;
     if ((p >> 2) < blk) f.pre += t;
     if ((p >> 2) == blk) {
@@ -208,7 +256,7 @@ __device__ __forceinline__ Factors chunk_factors(const float *sRg, const float (
 
 // Per-chunk gate data every factor thread publishes: exp of the block-level
 // scale, gamma and the decays between non-adjacent blocks.
-template <int NB>
+template <int NB, int LDRG>
 __device__ __forceinline__ void publish_decays(float *sSc, float *sG, float *sGp, const float *sRg,
                                                const Factors &f, float scale_log, int frg, int fk,
                                                bool fv) {
@@ -219,8 +267,8 @@ __device__ __forceinline__ void publish_decays(float *sSc, float *sG, float *sGp
       float t1 = 0.f, t2 = 0.f;
 #pragma unroll
       for (int p = 0; p < 4; ++p) {
-        t1 += sRg[(4 + p) * kKF + fk];
-        t2 += sRg[(8 + p) * kKF + fk];
+        t1 += sRg[fk * LDRG + 4 + p];
+        t2 += sRg[fk * LDRG + 8 + p];
       }
       sGp[0 * kKF + fk] = __expf(t1);
       sGp[1 * kKF + fk] = __expf(t1 + t2);
@@ -303,8 +351,8 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   };
   auto store_slab = [&](int q) {
     const int b = L::DB ? (q & 1) : 0;
-    pv.store((T *)((char *)sV0 + b * L::slab), L::LDV);
-    pd.store((T *)((char *)sD0 + b * L::slab), L::LDV);
+    pv.store_swz((T *)((char *)sV0 + b * L::slab), L::LDV);
+    pd.store_swz((T *)((char *)sD0 + b * L::slab), L::LDV);
   };
 
   T *dqo = (T *)a.dq + (int64_t)bh * a.T * K, *dqlo = (T *)a.dq_lo + (int64_t)bh * a.T * K;
@@ -329,26 +377,31 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
         c[i] = s;
         kv[i] = elem_f<T>(fin_k[i]);
       }
-      if (fthr) sRg[frg * kKF + fk] = s;
+      if (fthr) sRg[fk * L::LDRG + frg] = s;
     }
     __syncthreads();
     if (fthr) {
-      const Factors f = chunk_factors<NRG>(sRg, c, frg, fk, fv);
+      const Factors f = chunk_factors<NRG, L::LDRG>(sRg, c, frg, fk, fv);
       sFt[frg * kKF + fk] = f.tot;
-      const float etot = __expf(-f.tot);
+      const float etot = __expf(-f.tot), ekt = __expf(f.blast - f.pre - f.tot);
+      f4 ko4, kp4, bl4;
+      T hi4[4], lo4[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int row = 4 * frg + i;
-        const float kt_ = kv[i] * __expf(f.blast - f.pre - f.Bloc[i]);
-        const T hi = cvt<T>(kt_);
-        sBh[row * L::LDK + fk] = hi;
-        if constexpr (SPLIT) sBl[row * L::LDK + fk] = cvt<T>(kt_ - (float)hi);
         const float ks = kv[i] * __expf(f.tot - f.Bloc[i]);
-        sKo[row * L::LDO + fk] = ks;
-        sKp[row * L::LDO + fk] = f.wide ? 0.f : ks * etot;
-        sBloc[row * L::LDF + fk] = f.Bloc[i];
+        const float kt_ = ks * ekt;
+        hi4[i] = cvt<T>(kt_);
+        lo4[i] = cvt<T>(kt_ - (float)hi4[i]);
+        ko4[i] = ks;
+        kp4[i] = f.wide ? 0.f : ks * etot;
+        bl4[i] = f.Bloc[i];
       }
-      publish_decays<NB>(sSc, sG, sGp, sRg, f, f.pre, frg, fk, fv);
+      store4<T>(sBh + fk * L::LDTB + 4 * frg, hi4);
+      if constexpr (SPLIT) store4<T>(sBl + fk * L::LDTB + 4 * frg, lo4);
+      *(f4 *)(sKo + fk * L::LDT + 4 * frg) = ko4;
+      *(f4 *)(sKp + fk * L::LDT + 4 * frg) = kp4;
+      *(f4 *)(sBloc + fk * L::LDT + 4 * frg) = bl4;
+      publish_decays<NB, L::LDRG>(sSc, sG, sGp, sRg, f, f.pre, frg, fk, fv);
     }
     if (n + 1 < N) fetch_factors(n + 1);
     __syncthreads();
@@ -357,8 +410,8 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
     frag_t<T> bh_[NSC], bl_[NSC];
 #pragma unroll
     for (int sc = 0; sc < NSC; ++sc) {
-      bh_[sc] = ld_col<T>(sBh, L::LDK, 32 * sc, 16 * kb);
-      if constexpr (SPLIT) bl_[sc] = ld_col<T>(sBl, L::LDK, 32 * sc, 16 * kb);
+      bh_[sc] = ld_row<T>(sBh, L::LDTB, 16 * kb, 32 * sc);
+      if constexpr (SPLIT) bl_[sc] = ld_row<T>(sBl, L::LDTB, 16 * kb, 32 * sc);
     }
     const float gam = sG[16 * kb + j];
     f4 acc[NB], accP[2];
@@ -384,19 +437,19 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
         if (w < NBLK) {
 #pragma unroll
           for (int s = 0; s < kVS / 32; ++s)
-            accP[0] = mma<T>(accP[0], ld_row<T>(sD, L::LDV, 16 * pI0, 32 * s), ld_row<T>(sV, L::LDV, 16 * pJ0, 32 * s));
+            accP[0] = mma<T>(accP[0], ld_row_sw<T>(sD, L::LDV, 16 * pI0, 32 * s), ld_row_sw<T>(sV, L::LDV, 16 * pJ0, 32 * s));
         }
         if (w + 8 < NBLK) {
 #pragma unroll
           for (int s = 0; s < kVS / 32; ++s)
-            accP[1] = mma<T>(accP[1], ld_row<T>(sD, L::LDV, 16 * pI1, 32 * s), ld_row<T>(sV, L::LDV, 16 * pJ1, 32 * s));
+            accP[1] = mma<T>(accP[1], ld_row_sw<T>(sD, L::LDV, 16 * pI1, 32 * s), ld_row_sw<T>(sV, L::LDV, 16 * pJ1, 32 * s));
         }
         // dq_inter += dO[:, this wave's 32 value rows] S^T
         frag_t<T> shi, slo;
         acc_split<T>(S[sl][0], S[sl][1], shi, slo);
 #pragma unroll
         for (int I = 0; I < NB; ++I) {
-          const frag_t<T> ad = ld_row<T>(sD, L::LDV, 16 * I, 32 * vq);
+          const frag_t<T> ad = ld_row_sw<T>(sD, L::LDV, 16 * I, 32 * vq);
           acc[I] = mma<T>(acc[I], ad, shi);
           if constexpr (SPLIT) acc[I] = mma<T>(acc[I], ad, slo);
         }
@@ -406,7 +459,7 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
           S[sl][h] *= gam;
 #pragma unroll
           for (int sc = 0; sc < NSC; ++sc) {
-            const frag_t<T> av = ld_col_perm<T>(sV, L::LDV, 32 * sc, 32 * vq, h);
+            const frag_t<T> av = ld_col_perm_sw<T>(sV, L::LDV, 32 * sc, 32 * vq, h);
             S[sl][h] = mma<T>(S[sl][h], av, bh_[sc]);
             if constexpr (SPLIT) S[sl][h] = mma<T>(S[sl][h], av, bl_[sc]);
           }
@@ -424,41 +477,34 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
     for (int u = 0; u < 2; ++u) {
       const int bI = u ? pI1 : pI0, bJ = u ? pJ1 : pJ0;
       if (w + 8 * u < NBLK) {
+        const int t4 = 16 * bI + 4 * g, col = 16 * bJ + j;
+        f4 v4;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int row = 16 * bI + 4 * g + r, col = 16 * bJ + j;
-          const float val = col > row ? 0.f : accP[u][r];
-          sdP[row * L::LDP + col] = val;
-          if (kt == 0 && row < C && col < C) dPg[((int64_t)n * C + row) * C + col] = val;
+          v4[r] = col > t4 + r ? 0.f : accP[u][r];
+          sdP[(t4 + r) * L::LDP + col] = v4[r];
         }
+        // the workspace holds dP transposed ([s][t]) for the dk sweep
+        if (kt == 0 && t4 < C && col < C) *(f4 *)(dPg + ((int64_t)n * C + col) * C + t4) = v4;
       }
     }
     if (kt == 0 && w < NUP) {
       int uI, uJ;
       up_block(w, uI, uJ);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = 16 * uI + 4 * g + r, col = 16 * uJ + j;
-        if (row < C && col < C) dPg[((int64_t)n * C + row) * C + col] = 0.f;
-      }
+      const int t4 = 16 * uI + 4 * g, col = 16 * uJ + j;
+      if (t4 < C && col < C) *(f4 *)(dPg + ((int64_t)n * C + col) * C + t4) = zero4();
     }
     // ---- dq_inter partials, pre-scaled by exp(log decay before the block)
 #pragma unroll
     for (int I = 0; I < NB; ++I) acc[I] *= sSc[I * kKF + 16 * kb + j];
     if (vq >= 2) {
 #pragma unroll
-      for (int I = 0; I < NB; ++I)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          sRed[(vq - 2) * CP * L::LDF + (16 * I + 4 * g + r) * L::LDF + 16 * kb + j] = acc[I][r];
+      for (int I = 0; I < NB; ++I) *(f4 *)(sRed + ((vq - 2) * kKF + 16 * kb + j) * L::LDT + 16 * I + 4 * g) = acc[I];
     }
     __syncthreads();
     if (vq < 2) {
 #pragma unroll
-      for (int I = 0; I < NB; ++I)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          sRed[vq * CP * L::LDF + (16 * I + 4 * g + r) * L::LDF + 16 * kb + j] += acc[I][r];
+      for (int I = 0; I < NB; ++I) *(f4 *)(sRed + (vq * kKF + 16 * kb + j) * L::LDT + 16 * I + 4 * g) += acc[I];
     }
     // intra-chunk term by sub-chunk blocks, for row block I: sum over J <= I of
     // dP_IJ x_J with x_J = (k (.) exp(tot_J - Bloc)) g_IJ below the diagonal and
@@ -471,14 +517,13 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
         if (32 * s > 16 * I) continue;
         const int J = 2 * s + (g >> 1);
         const float sc = J > I ? 0.f : (J <= I - 2 ? sGp[pair_idx(I, J) * kKF + 16 * kq + j] : 1.f);
-        const f8 ko = ldf_col(sKo, L::LDO, 32 * s, 16 * kq), kp = ldf_col(sKp, L::LDO, 32 * s, 16 * kq);
+        const f8 ko = ldf_row(sKo, L::LDT, 16 * kq, 32 * s), kp = ldf_row(sKp, L::LDT, 16 * kq, 32 * s);
         f8 bf;
 #pragma unroll
         for (int i = 0; i < 8; ++i) bf[i] = J == I ? kp[i] : ko[i] * sc;
         o = mma_split3<T>(o, ldf_row(sdP, L::LDP, 16 * I, 32 * s), bf);
       }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) sOr[(16 * I + 4 * g + r) * L::LDF + 16 * kq + j] = o[r];
+      *(f4 *)(sOr + (16 * kq + j) * L::LDT + 16 * I + 4 * g) = o;
     }
     __syncthreads();
 
@@ -486,18 +531,21 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
     if (fthr) {
       const int blk = frg >> 2;
       const bool wide = fv && (-sFt[frg * kKF + fk] > kWide);
+      const f4 r0 = *(const f4 *)(sRed + fk * L::LDT + 4 * frg);
+      const f4 r1 = *(const f4 *)(sRed + (kKF + fk) * L::LDT + 4 * frg);
+      const f4 op = *(const f4 *)(sOr + fk * L::LDT + 4 * frg);
+      const f4 bl4 = *(const f4 *)(sBloc + fk * L::LDT + 4 * frg);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = 4 * frg + i;
-        const float inter = sRed[row * L::LDF + fk] + sRed[CP * L::LDF + row * L::LDF + fk];
-        const float bloc = sBloc[row * L::LDF + fk];
-        float dq = __expf(bloc) * (inter + sOr[row * L::LDF + fk]);
+        const float bloc = bl4[i];
+        float dq = __expf(bloc) * (r0[i] + r1[i] + op[i]);
         if (wide && row < rv) {
           // diagonal block with pairwise decays exp(B_row - B_s)
 #pragma unroll 1
           for (int s = 16 * blk; s <= row; ++s)
             dq += sdP[row * L::LDP + s] * (float)kh_[(int64_t)(t0 + s) * K + kf] *
-                  __expf(bloc - sBloc[s * L::LDF + fk]);
+                  __expf(bloc - sBloc[fk * L::LDT + s]);
         }
         if (row < rv && fv) {
           const T hi = cvt<T>(dq);
@@ -621,8 +669,8 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
   };
   auto store_slab = [&](int q) {
     const int b = L::DB ? (q & 1) : 0;
-    pv.store((T *)((char *)sV0 + b * L::slab), L::LDV);
-    pd.store((T *)((char *)sD0 + b * L::slab), L::LDV);
+    pv.store_swz((T *)((char *)sV0 + b * L::slab), L::LDV);
+    pd.store_swz((T *)((char *)sD0 + b * L::slab), L::LDV);
   };
 
   T *dko = (T *)a.dk + (int64_t)bh * a.T * K, *dlao = (T *)a.dla + (int64_t)bh * a.T * K;
@@ -649,26 +697,32 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
         kv[i] = elem_f<T>(fin_k[i]);
         qdq[i] = qv[i] * (elem_f<T>(fin_dq[i]) + (SPLIT ? elem_f<T>(fin_dql[i]) : 0.f));
       }
-      if (fthr) sRg[frg * kKF + fk] = s;
+      if (fthr) sRg[fk * L::LDRG + frg] = s;
       pp.store(sdP, L::LDP);
     }
     __syncthreads();
     if (fthr) {
-      const Factors f = chunk_factors<NRG>(sRg, c, frg, fk, fv);
+      const Factors f = chunk_factors<NRG, L::LDRG>(sRg, c, frg, fk, fv);
       sFt[frg * kKF + fk] = f.tot;
+      const float epre = __expf(f.pre), etot = __expf(-f.tot);
+      f4 qo4, qp4, bl4;
+      T hi4[4], lo4[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int row = 4 * frg + i;
-        const float qt = qv[i] * __expf(f.pre + f.Bloc[i]);
-        const T hi = cvt<T>(qt);
-        sBh[row * L::LDK + fk] = hi;
-        if constexpr (SPLIT) sBl[row * L::LDK + fk] = cvt<T>(qt - (float)hi);
         const float qh = qv[i] * __expf(f.Bloc[i]);
-        sQo[row * L::LDO + fk] = qh;
-        sQp[row * L::LDO + fk] = f.wide ? 0.f : qh * __expf(-f.tot);
-        sBloc[row * L::LDF + fk] = f.Bloc[i];
+        const float qt = qh * epre;
+        hi4[i] = cvt<T>(qt);
+        lo4[i] = cvt<T>(qt - (float)hi4[i]);
+        qo4[i] = qh;
+        qp4[i] = f.wide ? 0.f : qh * etot;
+        bl4[i] = f.Bloc[i];
       }
-      publish_decays<NB>(sSc, sG, sGp, sRg, f, f.blast - f.pre - f.tot, frg, fk, fv);
+      store4<T>(sBh + fk * L::LDTB + 4 * frg, hi4);
+      if constexpr (SPLIT) store4<T>(sBl + fk * L::LDTB + 4 * frg, lo4);
+      *(f4 *)(sQo + fk * L::LDT + 4 * frg) = qo4;
+      *(f4 *)(sQp + fk * L::LDT + 4 * frg) = qp4;
+      *(f4 *)(sBloc + fk * L::LDT + 4 * frg) = bl4;
+      publish_decays<NB, L::LDRG>(sSc, sG, sGp, sRg, f, f.blast - f.pre - f.tot, frg, fk, fv);
     }
     if (it + 1 < N) fetch_factors(n - 1);
     __syncthreads();
@@ -677,8 +731,8 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
     frag_t<T> bh_[NSC], bl_[NSC];
 #pragma unroll
     for (int sc = 0; sc < NSC; ++sc) {
-      bh_[sc] = ld_col<T>(sBh, L::LDK, 32 * sc, 16 * kb);
-      if constexpr (SPLIT) bl_[sc] = ld_col<T>(sBl, L::LDK, 32 * sc, 16 * kb);
+      bh_[sc] = ld_row<T>(sBh, L::LDTB, 16 * kb, 32 * sc);
+      if constexpr (SPLIT) bl_[sc] = ld_row<T>(sBl, L::LDTB, 16 * kb, 32 * sc);
     }
     const float gam = sG[16 * kb + j];
     f4 acc[NB];
@@ -700,7 +754,7 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
         acc_split<T>(dS[sl][0], dS[sl][1], shi, slo);
 #pragma unroll
         for (int J = 0; J < NB; ++J) {
-          const frag_t<T> av = ld_row<T>(sV, L::LDV, 16 * J, 32 * vq);
+          const frag_t<T> av = ld_row_sw<T>(sV, L::LDV, 16 * J, 32 * vq);
           acc[J] = mma<T>(acc[J], av, shi);
           if constexpr (SPLIT) acc[J] = mma<T>(acc[J], av, slo);
         }
@@ -709,7 +763,7 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
           dS[sl][h] *= gam;
 #pragma unroll
           for (int sc = 0; sc < NSC; ++sc) {
-            const frag_t<T> ad = ld_col_perm<T>(sD, L::LDV, 32 * sc, 32 * vq, h);
+            const frag_t<T> ad = ld_col_perm_sw<T>(sD, L::LDV, 32 * sc, 32 * vq, h);
             dS[sl][h] = mma<T>(dS[sl][h], ad, bh_[sc]);
             if constexpr (SPLIT) dS[sl][h] = mma<T>(dS[sl][h], ad, bl_[sc]);
           }
@@ -727,18 +781,12 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
     for (int J = 0; J < NB; ++J) acc[J] *= sSc[J * kKF + 16 * kb + j];
     if (vq >= 2) {
 #pragma unroll
-      for (int J = 0; J < NB; ++J)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          sRed[(vq - 2) * CP * L::LDF + (16 * J + 4 * g + r) * L::LDF + 16 * kb + j] = acc[J][r];
+      for (int J = 0; J < NB; ++J) *(f4 *)(sRed + ((vq - 2) * kKF + 16 * kb + j) * L::LDT + 16 * J + 4 * g) = acc[J];
     }
     __syncthreads();
     if (vq < 2) {
 #pragma unroll
-      for (int J = 0; J < NB; ++J)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          sRed[vq * CP * L::LDF + (16 * J + 4 * g + r) * L::LDF + 16 * kb + j] += acc[J][r];
+      for (int J = 0; J < NB; ++J) *(f4 *)(sRed + (vq * kKF + 16 * kb + j) * L::LDT + 16 * J + 4 * g) += acc[J];
     }
     // intra-chunk term by sub-chunk blocks, for column block J: sum over I >= J
     // of dP_IJ^T y_I with y_I = (q (.) exp(Bloc)) g_IJ below the diagonal and
@@ -751,14 +799,13 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
         if (32 * s + 31 < 16 * J) continue;
         const int I = 2 * s + (g >> 1);
         const float sc = I < J ? 0.f : (I >= J + 2 ? sGp[pair_idx(I, J) * kKF + 16 * kq + j] : 1.f);
-        const f8 qo = ldf_col(sQo, L::LDO, 32 * s, 16 * kq), qp = ldf_col(sQp, L::LDO, 32 * s, 16 * kq);
+        const f8 qo = ldf_row(sQo, L::LDT, 16 * kq, 32 * s), qp = ldf_row(sQp, L::LDT, 16 * kq, 32 * s);
         f8 bf;
 #pragma unroll
         for (int i = 0; i < 8; ++i) bf[i] = I == J ? qp[i] : qo[i] * sc;
-        o = mma_split3<T>(o, ldf_col(sdP, L::LDP, 32 * s, 16 * J), bf);
+        o = mma_split3<T>(o, ldf_row(sdP, L::LDP, 16 * J, 32 * s), bf);
       }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) sOr[(16 * J + 4 * g + r) * L::LDF + 16 * kq + j] = o[r];
+      *(f4 *)(sOr + (16 * kq + j) * L::LDT + 16 * J + 4 * g) = o;
     }
     __syncthreads();
 
@@ -768,19 +815,22 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
       const int blk = frg >> 2;
       const float tot = sFt[frg * kKF + fk];
       const bool wide = fv && (-tot > kWide);
+      const f4 r0 = *(const f4 *)(sRed + fk * L::LDT + 4 * frg);
+      const f4 r1 = *(const f4 *)(sRed + (kKF + fk) * L::LDT + 4 * frg);
+      const f4 op = *(const f4 *)(sOr + fk * L::LDT + 4 * frg);
+      const f4 bl4 = *(const f4 *)(sBloc + fk * L::LDT + 4 * frg);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = 4 * frg + i;
-        const float inter = sRed[row * L::LDF + fk] + sRed[CP * L::LDF + row * L::LDF + fk];
-        const float bloc = sBloc[row * L::LDF + fk];
-        float dk = __expf(tot - bloc) * (inter + sOr[row * L::LDF + fk]);
+        const float bloc = bl4[i];
+        float dk = __expf(tot - bloc) * (r0[i] + r1[i] + op[i]);
         if (wide && row < rv) {
           // diagonal block with pairwise decays exp(B_t - B_row)
           const int tend = min(16 * blk + 16, rv);
 #pragma unroll 1
           for (int tt = row; tt < tend; ++tt)
-            dk += sdP[tt * L::LDP + row] * (float)qh_[(int64_t)(t0 + tt) * K + kf] *
-                  __expf(sBloc[tt * L::LDF + fk] - bloc);
+            dk += sdP[row * L::LDP + tt] * (float)qh_[(int64_t)(t0 + tt) * K + kf] *
+                  __expf(sBloc[fk * L::LDT + tt] - bloc);
         }
         dA[i] = qdq[i] - kv[i] * dk;
         if (row < rv && fv) dko[(int64_t)(t0 + row) * K + kf] = cvt<T>(dk);
@@ -791,26 +841,27 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
         s += dA[i];
         dA[i] = s;
       }
-      sGrp[frg * kKF + fk] = s;
+      sGrp[fk * L::LDRG + frg] = s;
     }
     __syncthreads();
     if (fthr) {
       const float *car = sCar + (it & 1) * kKF;
-      float later = car[fk];
+      float later = car[fk], all = car[fk];
 #pragma unroll
-      for (int p = 0; p < NRG; ++p)
-        if (p > frg) later += sGrp[p * kKF + fk];
+      for (int p = 0; p < NRG; p += 4) {
+        const f4 v = *(const f4 *)(sGrp + fk * L::LDRG + p);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          all += v[e];
+          if (p + e > frg) later += v[e];
+        }
+      }
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = 4 * frg + i;
         if (row < rv && fv) dlao[(int64_t)(t0 + row) * K + kf] = cvt<T>(dA[i] + later);
       }
-      if (frg == 0) {
-        float tot = car[fk];
-#pragma unroll
-        for (int p = 0; p < NRG; ++p) tot += sGrp[p * kKF + fk];
-        sCar[((it + 1) & 1) * kKF + fk] = tot;
-      }
+      if (frg == 0) sCar[((it + 1) & 1) * kKF + fk] = all;
     }
     __syncthreads();
   }
