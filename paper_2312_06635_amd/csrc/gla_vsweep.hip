@@ -32,9 +32,10 @@
 // with four consecutive value columns of one time row: one 8-byte (bf16) or
 // 16-byte (fp32) store.
 //
-// Tiles of chunk n+1 are fetched with buffer loads into registers while chunk
-// n computes; each lane's byte offsets are fixed for the whole sweep (rows past
-// the sequence end fall outside the buffer's range and read as zero).
+// Tiles of chunk n+2 are fetched with buffer loads into one of two register
+// sets while chunk n computes; each lane's byte offsets are fixed for the
+// whole sweep (rows past the sequence end fall outside the buffer's range and
+// read as zero).
 #include "gla_common.hpp"
 #include "gla_launch.hpp"
 
@@ -147,43 +148,51 @@ __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
       R[kb][r] = (a.R0 && active && f < K) ? a.R0[((int64_t)bh * K + f) * V + col] : 0.f;
     }
 
-  // ---- tile loaders (per-lane offsets fixed for the sweep)
-  TileLd<T, CP, KP, kThreads> lx, ly;
-  TileLd<T, CP, kTile, kThreads> lz;
-  TileLd<T, CP, CP, kThreads> lp;
-  lx.init(K, C, K);
-  ly.init(K, C, K);
-  lz.init(V, C, V - v0);
-  lp.init(C, C, C);
+  // ---- tile loaders (per-lane offsets fixed for the sweep); two register
+  // sets, so the tiles of chunk it+2 are in flight while chunk it computes
+  struct Stage {
+    TileLd<T, CP, KP, kThreads> x, y;
+    TileLd<T, CP, kTile, kThreads> z;
+    TileLd<T, CP, CP, kThreads> p;
+    float g;
+  };
+  Stage st0, st1;
+  st0.x.init(K, C, K);
+  st0.y.init(K, C, K);
+  st0.z.init(V, C, V - v0);
+  st0.p.init(C, C, C);
+  st1.x = st0.x;
+  st1.y = st0.y;
+  st1.z = st0.z;
+  st1.p = st0.p;
   const int esz = sizeof(T);
   const T *Xh = (const T *)a.X + (int64_t)bh * a.T * K;
   const T *Yh = (const T *)a.Y + (int64_t)bh * a.T * K;
   const T *Zh = (const T *)a.Z + (int64_t)bh * a.T * V + v0;
   const T *Ph = (const T *)a.P + (int64_t)bh * N * C * C;
   const float *Gh = a.gam + (int64_t)bh * N * K;
-  float pg = 0.f;
-  auto fetch = [&](int n) {
+  auto chunk_of = [&](int it) { return REV ? N - 1 - it : it; };
+  auto fetch = [&](Stage &S, int n) {
     const int t0 = n * C;
     const uint32_t remK = rsrc_bytes((int64_t)(a.T - t0) * K * esz);
-    lx.load(make_rsrc(Xh + (int64_t)t0 * K, remK));
-    ly.load(make_rsrc(Yh + (int64_t)t0 * K, remK));
-    lz.load(make_rsrc(Zh + (int64_t)t0 * V, rsrc_bytes(((int64_t)(a.T - t0) * V - v0) * esz)));
-    lp.load(make_rsrc(Ph + (int64_t)n * C * C, (uint32_t)(C * C * esz)));
-    pg = (int)threadIdx.x < K ? Gh[(int64_t)n * K + threadIdx.x] : 0.f;
+    S.x.load(make_rsrc(Xh + (int64_t)t0 * K, remK));
+    S.y.load(make_rsrc(Yh + (int64_t)t0 * K, remK));
+    S.z.load(make_rsrc(Zh + (int64_t)t0 * V, rsrc_bytes(((int64_t)(a.T - t0) * V - v0) * esz)));
+    S.p.load(make_rsrc(Ph + (int64_t)n * C * C, (uint32_t)(C * C * esz)));
+    S.g = (int)threadIdx.x < K ? Gh[(int64_t)n * K + threadIdx.x] : 0.f;
   };
 
   T *outh = (T *)a.out + (int64_t)bh * a.T * V;
-  fetch(REV ? N - 1 : 0);
-  for (int it = 0; it < N; ++it) {
-    const int n = REV ? N - 1 - it : it;
+  auto body = [&](Stage &S, int it) {
+    const int n = chunk_of(it);
     const int t0 = n * C, rv = min(C, a.T - t0);
-    lx.store(sX, L::LDX);
-    ly.store(sY, L::LDY);
-    lz.store(sZ, L::LDZ);
-    lp.store(sP, L::LDP);
-    if ((int)threadIdx.x < KP) sG[threadIdx.x] = pg;
+    S.x.store(sX, L::LDX);
+    S.y.store(sY, L::LDY);
+    S.z.store(sZ, L::LDZ);
+    S.p.store(sP, L::LDP);
+    if ((int)threadIdx.x < KP) sG[threadIdx.x] = S.g;
     __syncthreads();
-    if (it + 1 < N) fetch(REV ? n - 1 : n + 1);
+    if (it + 2 < N) fetch(S, chunk_of(it + 2));
 
     f4 acc[NI];
 #pragma unroll
@@ -245,6 +254,12 @@ __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
         }
       }
     }
+  };
+  fetch(st0, chunk_of(0));
+  if (N > 1) fetch(st1, chunk_of(1));
+  for (int it = 0; it < N; it += 2) {
+    body(st0, it);
+    if (it + 1 < N) body(st1, it + 1);
   }
   if (a.RN && active) {
 #pragma unroll
