@@ -114,6 +114,13 @@ SMALL = [
     dict(cfg=small_case("bf16_sweep", "bf16", 2, 2, 256, 128, 128, 64, 16, 18)),
     dict(cfg=small_case("bf16_ragged_C16", "bf16", 1, 3, 77, 64, 96, 16, 4, 19)),
     dict(cfg=small_case("bf16_T1", "bf16", 1, 1, 1, 32, 48, 64, 16, 20, s0_std=0.1), dST_std=0.1),
+    # bf16 edge shapes of the tiled kernels: 32-row chunks with a padded key
+    # width and a partial value slab; a key tile and a value tile that are
+    # only partly inside d_k / d_v; the widest value dimension
+    dict(cfg=small_case("bf16_C32_K96_V192", "bf16", 1, 2, 160, 96, 192, 32, 16, 23)),
+    dict(cfg=small_case("bf16_K48_V80", "bf16", 2, 1, 100, 48, 80, 64, 16, 24, s0_std=0.1),
+         dST_std=0.1),
+    dict(cfg=small_case("bf16_V1024", "bf16", 1, 1, 130, 64, 1024, 64, 16, 25)),
 ]
 
 
