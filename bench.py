@@ -94,6 +94,51 @@ def cpu_baseline(cfg, inputs, target_s=15.0):
                       f"{el:.1f} s wall; tokens counted as heads*T/H"}
 
 
+COPY_BYTES = 1 << 30
+
+
+def calibrate_copy():
+    """A plain device-to-device copy of COPY_BYTES: the reference kernel whose
+    FETCH_SIZE / WRITE_SIZE counters scale those of the layer's kernels."""
+    dev = torch.device("cuda:0")
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": COPY_BYTES, "launches": 3}), flush=True)
+
+
+def source_digest():
+    """Hash of the kernel sources, to tell whether stored counters are current."""
+    import hashlib
+    h = hashlib.sha256()
+    cdir = os.path.join(ROOT, "paper_2312_06635_amd", "csrc")
+    for name in sorted(os.listdir(cdir)):
+        with open(os.path.join(cdir, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary, or
+    None when there is none or the kernels changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    digest, found = None, None
+    with open(path) as f:
+        for line in f:
+            line = line.strip()
+            if line.startswith("source_digest:"):
+                digest = line.split(":", 1)[1].strip()
+            if line.startswith(f"traffic_bytes[{kernel}]:"):
+                found = float(line.split(":", 1)[1].strip())
+    if digest != source_digest():
+        return None
+    return found
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -101,12 +146,18 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="gla1p3b_T2048", choices=sorted(W.CONFIGS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 1 GiB device copy (reference for HBM traffic counters)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(heads shard across GPUs with no communication; see DESIGN.md).", file=sys.stderr)
+        print("bench.py measures one GPU only: heads shard across GPUs with no communication, "
+              "and no multi-GPU path is built.", file=sys.stderr)
         sys.exit(2)
+
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
 
     import paper_2312_06635_amd as gla
 
@@ -175,7 +226,7 @@ def main():
         roof = {"kernel": dom, "bound": "mfma", "achieved": a["flops"] / t_dom / 1e12, "peak": peak / 1e12,
                 "unit": "TFLOP/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None
+    roof["traffic"] = measured_traffic(args.workload, dom)
     roof["avg_ms"] = stage_ms[dom]
 
     out = {

@@ -8,9 +8,10 @@
 //   A operand : row j of the 16-row tile, reduction slots 8g .. 8g+7
 //   B operand : column j of the tile,    reduction slots 8g .. 8g+7
 //   D (acc)   : column j, rows 4g .. 4g+3 (4 fp32 per lane)
-// Any slot-to-index mapping is valid as long as A and B agree; the state
-// accumulators use the "permuted" mapping that a 16x16 accumulator pair
-// provides directly (see acc_frag / ld_row_perm).
+// Any slot-to-index mapping is valid as long as A and B agree; a 16x16
+// accumulator pair provides slots 0..3 and 4..7 from rows 4g..4g+3 of each
+// accumulator (see acc_frag), which the kernels match by permuting the order
+// in which the state's key features are laid out.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -79,21 +80,6 @@ __device__ __forceinline__ frag_t<T> ld_row(const T *X, int ld, int r0, int c0) 
   }
 }
 
-// Same, in the permuted slot order of an accumulator pair (see acc_frag):
-// lane (g, j) gets X[r0 + j][c0 + 4g + i] for i < 4 and X[r0 + j][c0 + 16 + 4g + i - 4].
-template <typename T>
-__device__ __forceinline__ frag_t<T> ld_row_perm(const T *X, int ld, int r0, int c0) {
-  const int l = lane_id();
-  const T *p = X + (r0 + (l & 15)) * ld + c0 + 4 * (l >> 4);
-  if constexpr (sizeof(T) == 2) {
-    bf16x4 a = *(const bf16x4 *)p, b = *(const bf16x4 *)(p + 16);
-    return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
-  } else {
-    f4 a = *(const f4 *)p, b = *(const f4 *)(p + 16);
-    return f8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
-  }
-}
-
 // Fragment whose reduction index runs down a column (a transposed read):
 // lane (g, j) gets X[r0 + 8g + i][c0 + j], i = 0..7.  For bf16 this is two
 // gfx950 LDS transpose reads: with lane j of a 16-lane group pointing at
@@ -118,36 +104,10 @@ __device__ __forceinline__ frag_t<T> ld_col(const T *X, int ld, int r0, int c0) 
   }
 }
 
-// Column fragment read from an fp32 tile, converted to T.
-template <typename T>
-__device__ __forceinline__ frag_t<T> ld_col_f32(const float *X, int ld, int r0, int c0) {
-  const int l = lane_id();
-  const float *p = X + (r0 + 8 * (l >> 4)) * ld + c0 + (l & 15);
-  frag_t<T> r;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) r[i] = cvt<T>(p[i * ld]);
-  return r;
-}
-
-// Row fragment read from an fp32 tile, converted to T.
-template <typename T>
-__device__ __forceinline__ frag_t<T> ld_row_f32(const float *X, int ld, int r0, int c0) {
-  const int l = lane_id();
-  const float *p = X + (r0 + (l & 15)) * ld + c0 + 8 * (l >> 4);
-  f4 a = *(const f4 *)p, b = *(const f4 *)(p + 4);
-  frag_t<T> r;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    r[i] = cvt<T>(a[i]);
-    r[4 + i] = cvt<T>(b[i]);
-  }
-  return r;
-}
-
 // B (or A) fragment taken straight from two stacked 16x16 accumulators
 // lo = rows [0,16), hi = rows [16,32) of a 32-row slab: lane (g, j) holds
 // rows 4g..4g+3 of column j in each, which become slots 0..3 and 4..7.
-// The matching operand must be read with ld_row_perm.
+// The matching operand must list the same 8 indices per lane.
 template <typename T> __device__ __forceinline__ frag_t<T> acc_frag(f4 lo, f4 hi) {
   frag_t<T> r;
 #pragma unroll
@@ -157,68 +117,6 @@ template <typename T> __device__ __forceinline__ frag_t<T> acc_frag(f4 lo, f4 hi
   }
   return r;
 }
-
-// ---------------------------------------------------------------- staging
-// Cooperative copy of a [rows x cols] tile from global memory (leading
-// dimension gld) into LDS (leading dimension lld).  Rows >= rv or columns
-// >= cv are filled with zeros; `cols` must be a multiple of 16 / sizeof(T)
-// and both leading dimensions keep 16-byte alignment.
-template <typename T>
-__device__ __forceinline__ void stage_tile(T *dst, int lld, const T *src, int64_t gld, int rows,
-                                           int cols, int rv, int cv) {
-  constexpr int EV = 16 / sizeof(T);
-  const int vpr = cols / EV;
-  const int total = rows * vpr;
-  for (int idx = threadIdx.x; idx < total; idx += blockDim.x) {
-    const int r = idx / vpr, c = (idx - r * vpr) * EV;
-    uint4 val = make_uint4(0, 0, 0, 0);
-    if (r < rv && c < cv) val = *(const uint4 *)(src + (int64_t)r * gld + c);
-    *(uint4 *)(dst + r * lld + c) = val;
-  }
-}
-
-// Register-staged tile copy for software pipelining: load() issues this
-// thread's share of a [rows x cols] tile as 16-byte global loads into
-// registers (rows >= rv or columns >= cv read as zero) without waiting for
-// them; store() later writes the registers into LDS.  Issuing the loads of
-// chunk n+1 right after the barrier that publishes chunk n lets their latency
-// overlap the compute of chunk n.  NV bounds the vectors per thread for a
-// 256-thread workgroup.
-template <typename T, int NV> struct TileRegs {
-  uint4 r[NV];
-  // Thread t covers vectors t, t + 256, ...; with vpr = cols / EV a power of two
-  // dividing 256 (the case for every tile here) its row steps by 256 / vpr and
-  // its column stays fixed, so no division is needed.
-  __device__ __forceinline__ static void geom(int cols, int &row0, int &rstep, int &c, int &vpr) {
-    constexpr int EV = 16 / sizeof(T);
-    vpr = cols / EV;
-    const int sh = 31 - __builtin_clz(vpr);
-    row0 = (int)threadIdx.x >> sh;
-    rstep = 256 >> sh;
-    c = ((int)threadIdx.x & (vpr - 1)) * EV;
-  }
-  // src must be uniform across the workgroup and row * gld + c must fit in
-  // 32 bits, so the loads use a scalar base plus a 32-bit vector offset.
-  __device__ __forceinline__ void load(const T *src, int gld, int rows, int cols, int rv, int cv) {
-    int row0, rstep, c, vpr;
-    geom(cols, row0, rstep, c, vpr);
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int row = row0 + i * rstep;
-      r[i] = make_uint4(0, 0, 0, 0);
-      if (row < rows && row < rv && c < cv) r[i] = *(const uint4 *)(src + (row * gld + c));
-    }
-  }
-  __device__ __forceinline__ void store(T *dst, int lld, int rows, int cols) const {
-    int row0, rstep, c, vpr;
-    geom(cols, row0, rstep, c, vpr);
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int row = row0 + i * rstep;
-      if (row < rows) *(uint4 *)(dst + row * lld + c) = r[i];
-    }
-  }
-};
 
 // Buffer resource over [base, base + bytes): buffer loads at byte offsets at
 // or beyond `bytes` return zeros instead of touching memory.

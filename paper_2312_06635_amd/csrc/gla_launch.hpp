@@ -22,7 +22,7 @@ struct Work {
   void *P = nullptr;      // [BH][N][C][C] io : intra-chunk matrix, lower triangle
   float *gam = nullptr;   // [BH][N][K] fp32 : chunk decay gamma = b_{chunk end} / b_{chunk start}
   unsigned char *wflag = nullptr;  // [BH][N][4] : diagonal block of P needs pairwise decays
-  float *dP = nullptr;    // [BH][N][C][C] fp32 : (dO V^T) (.) M per chunk (backward)
+  float *dP = nullptr;    // [BH][N][C][C] fp32 : (dO V^T) (.) M per chunk, stored transposed (backward)
   float *cST = nullptr;   // [BH][K] fp32 : rowsum(S_T (.) dS_T) (backward)
   void *dq_lo = nullptr;  // [BH][T][K] bf16 : dq - bf16(dq), so dq reaches the gate gradient
                           //   with ~16 mantissa bits (bf16 io only)
@@ -39,7 +39,7 @@ hipError_t launch_bwd_dq(const Shape &s, const void *k, const void *la, const vo
 hipError_t launch_bwd_dk(const Shape &s, const void *q, const void *k, const void *la,
                          const void *v, const void *dO, const float *dST, const void *dq,
                          void *dk, void *dla, const Work &w, hipStream_t st);
-// (bwd_dq also writes w.dq_lo; bwd_dk reads it)
+// (the dq sweep also writes w.dP, w.cST and w.dq_lo; the dk sweep reads them)
 hipError_t launch_bwd_dv(const Shape &s, const void *dO, const float *dST, void *dv, float *dS0,
                          const Work &w, hipStream_t st);
 hipError_t launch_recurrent(const Shape &s, const void *q, const void *k, const void *v,
