@@ -98,13 +98,15 @@ COPY_BYTES = 1 << 30
 
 
 def calibrate_copy():
-    """A plain device-to-device copy of COPY_BYTES: the reference kernel whose
-    FETCH_SIZE / WRITE_SIZE counters scale those of the layer's kernels."""
+    """A plain streaming kernel that reads and writes COPY_BYTES once each (an
+    element-wise multiply by one): the reference whose FETCH_SIZE / WRITE_SIZE
+    counters scale those of the layer's kernels."""
     dev = torch.device("cuda:0")
     src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
     dst = torch.empty_like(src)
+    torch.cuda.synchronize()
     for _ in range(3):
-        dst.copy_(src)
+        torch.mul(src, 1.0, out=dst)
     torch.cuda.synchronize()
     print(json.dumps({"copy_bytes": COPY_BYTES, "launches": 3}), flush=True)
 
