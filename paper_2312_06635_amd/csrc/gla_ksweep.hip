@@ -12,24 +12,30 @@
 //                        dlog alpha = revcumsum(q (.) dq - k (.) dk) + rowsum(S_T (.) dS_T)
 // dq, dk and the gate gradient reduce over d_v, so a workgroup owns 32 key
 // features of one head for the whole sequence and holds the transposed state
-// block (value rows x 32 features, fp32) in matrix-core accumulators.
+// (value rows x 32 features, fp32) in matrix-core accumulators.
 //
-// Workgroup = 8 waves; wave w owns features 16 (w & 1) .. +16 and, in every
-// 128-column value slab, value rows 32 (w >> 1) .. +32.  Accumulator pair
-// (2 per slab) rows are in the permuted order v = 32 vq + 8 (i / 4) + 4 h +
-// i % 4, so the pair is directly an operand whose partner is one contiguous
-// 16-byte LDS read.  The products that reduce over d_v leave one partial per
-// value quarter; these are pre-scaled, summed in two steps through LDS and
+// Workgroup = 8 waves.  Value columns stream through LDS in slabs of 256
+// (bf16; 128 for fp32); wave w holds the 32 x 32 state tile of value rows
+// 32 w .. +32 of every slab as one 32x32 accumulator, so every operand fetched
+// for the d_v-reducing products and the state update feeds a 32-wide output.
+// Accumulator row m holds value 16 (m / 16) + 8 ((m / 4) % 2) + 4 ((m / 8) % 2)
+// + m % 4 of the wave's 32, which makes the 8 values a lane holds for one
+// 16-deep step contiguous: the tile is directly an operand of the next
+// product, whose partner is one 16-byte LDS read; the update's transposed
+// operand is read with LDS transpose reads pointed at the matching permuted
+// columns.  Slab tiles are XOR-swizzled per row so that both read patterns are
+// bank-conflict free.  The products that reduce over d_v leave one partial per
+// state wave; these are pre-scaled and summed in two steps through LDS, then
 // combined per (row, feature) with the intra-chunk terms:
-//   sub-chunk blocks strictly below the diagonal: matrix-core products of fp32
-//   operands split into bf16 hi + lo (three cross terms), scaled by the decay
-//   of the blocks in between (every exponent <= 0);
-//   diagonal blocks: fp32 on the VALUs, factorised exp(B_i - z) exp(z - B_j),
-//   or pairwise exp(B_i - B_j) when a block's decay range exceeds kWide.
-// Value slabs stream through double-buffered LDS (one barrier per slab).  For
-// bf16 the state operand, the gated update operand and the dq hand-off are
-// split into bf16 hi + lo so the gate gradient's long reverse sum keeps fp32
-// accuracy.
+//   sub-chunk blocks below the diagonal and, via the factorised decay
+//   exp(B_i - z) exp(z - B_j), the diagonal ones: 16x16 matrix-core products
+//   of fp32 operands split into bf16 hi + lo (three cross terms), scaled by
+//   the decay of the blocks in between (every exponent <= 0);
+//   diagonal blocks whose decay range exceeds kWide: pairwise exp(B_i - B_j)
+//   in fp32.
+// For bf16 the state operand, the gated update operand and the dq hand-off are
+// split into bf16 hi + lo so that the gate gradient's long reverse sum keeps
+// fp32 accuracy.
 #include "gla_common.hpp"
 #include "gla_launch.hpp"
 
@@ -39,8 +45,9 @@ namespace {
 
 constexpr int kKT = 512;      // threads per workgroup
 constexpr int kKF = 32;       // key features per workgroup
-constexpr int kVS = 128;      // value columns per slab
 constexpr float kWide = 60.f;
+
+typedef float f16v __attribute__((ext_vector_type(16)));
 
 struct KsArgs {
   const void *q, *k, *la, *v, *dO, *dq_in, *dq_lo_in;
@@ -51,133 +58,167 @@ struct KsArgs {
 };
 
 template <typename T, int CP> struct KsLayout {
-  static constexpr bool DB = sizeof(T) == 2;  // double-buffered slabs (fp32 tiles are too big)
-  static constexpr int NBUF = DB ? 2 : 1;
-  static constexpr int LDV = kVS;  // slab rows are XOR-swizzled, not padded
+  static constexpr int VS = sizeof(T) == 2 ? 256 : 128;  // value columns per slab
+  static constexpr int NWS = VS / 32;                     // waves holding state
+  static constexpr int NP = NWS / 2;                      // partials left by the first reduction step
+  static constexpr int LDV = VS;                          // slab rows are XOR-swizzled, not padded
   static constexpr int NB = CP / 16, NRG = CP / 4;
   // Per-(row, feature) tiles are stored feature-major ([32 features][rows]),
   // so a factor/final thread's four consecutive rows of one feature and a
   // fragment's eight consecutive rows are single 8/16-byte LDS accesses.
-  static constexpr int LDT = CP + 4;                        // fp32 feature-major tiles
+  static constexpr int LDT = CP + 4;                          // fp32 feature-major tiles
   static constexpr int LDTB = CP + (sizeof(T) == 2 ? 8 : 4);  // T feature-major tiles
-  static constexpr int LDP = CP + 4;                        // dP (dq: [t][s]; dk: [s][t])
-  static constexpr int LDRG = NRG + 4;                      // row-group sums [32][NRG]
+  static constexpr int LDP = CP + 4;                          // dP (dq: [t][s]; dk: [s][t])
+  static constexpr int LDRG = NRG + 4;                        // row-group sums [32][NRG]
   static constexpr size_t slab = sizeof(T) * CP * LDV;
   static constexpr size_t offV = 0;
-  static constexpr size_t offD = offV + NBUF * slab;
-  static constexpr size_t offBh = offD + NBUF * slab;                    // gated update operand (hi)
-  static constexpr size_t offBl = offBh + sizeof(T) * kKF * LDTB;        // (lo, bf16 only)
-  static constexpr size_t offO = offBl + (DB ? sizeof(T) * kKF * LDTB : 0);  // orange operand
-  static constexpr size_t offPk = offO + 4 * kKF * LDT;                  // pink operand
-  static constexpr size_t offBloc = offPk + 4 * kKF * LDT;               // block-local cumsum
+  static constexpr size_t offD = offV + slab;
+  static constexpr size_t offBh = offD + slab;                          // gated update operand (hi)
+  static constexpr size_t offBl = offBh + sizeof(T) * kKF * LDTB;       // (lo, bf16 only)
+  static constexpr size_t offO = offBl + (sizeof(T) == 2 ? sizeof(T) * kKF * LDTB : 0);  // intra operand
+  static constexpr size_t offBloc = offO + 4 * kKF * LDT;               // block-local cumsum
   static constexpr size_t offdP = offBloc + 4 * kKF * LDT;
-  static constexpr size_t offRed = offdP + 4 * CP * LDP;                 // two partial sums
-  static constexpr size_t offOr = offRed + 2 * 4 * kKF * LDT;            // intra-chunk results
-  static constexpr size_t offRg = offOr + 4 * kKF * LDT;                 // row-group totals
-  static constexpr size_t offSc = offRg + 4 * kKF * LDRG;                // per-block scale [NB][32]
-  static constexpr size_t offGp = offSc + 4 * NB * kKF;                  // pair factors [3][32]
-  static constexpr size_t offG = offGp + 4 * 3 * kKF;                    // gamma [32]
-  static constexpr size_t offCar = offG + 4 * kKF;                       // carry [2][32]
-  static constexpr size_t offRedS = offCar + 4 * 2 * kKF;                // final-state sums [8][32]
-  static constexpr size_t offFt = offRedS + 4 * 8 * kKF;                 // per-thread block decay [NRG][32]
-  static constexpr size_t offGrp = offFt + 4 * NRG * kKF;                // dk: row-group sums of dA
+  static constexpr size_t offRed = offdP + 4 * CP * LDP;                // partial sums [NP]
+  static constexpr size_t offOr = offRed + 4 * NP * kKF * LDT;          // intra-chunk results
+  static constexpr size_t offRg = offOr + 4 * kKF * LDT;                // row-group totals
+  static constexpr size_t offSc = offRg + 4 * kKF * LDRG;               // per-block scale [NB][32]
+  static constexpr size_t offEt = offSc + 4 * NB * kKF;                 // diagonal-block scale [NB][32]
+  static constexpr size_t offGp = offEt + 4 * NB * kKF;                 // pair factors [3][32]
+  static constexpr size_t offG = offGp + 4 * 3 * kKF;                   // gamma [32]
+  static constexpr size_t offCar = offG + 4 * kKF;                      // carry [2][32]
+  static constexpr size_t offRedS = offCar + 4 * 2 * kKF;               // final-state sums [8][32]
+  static constexpr size_t offFt = offRedS + 4 * 8 * kKF;               // per-thread block decay [NRG][32]
+  static constexpr size_t offGrp = offFt + 4 * NRG * kKF;               // dk: row-group sums of dA
   static constexpr size_t total = offGrp + 4 * kKF * LDRG;
 };
 
-// (I, J) of lower-triangular block b (row-major) and of upper block u.
-__device__ __forceinline__ void low_block(int b, int &I, int &J) {
-  I = (b >= 1) + (b >= 3) + (b >= 6);
-  J = b - I * (I + 1) / 2;
-}
-__device__ __forceinline__ void up_block(int u, int &I, int &J) {
-  I = (u >= 3) + (u >= 5);
-  J = u - (I == 0 ? -1 : (I == 1 ? 1 : 2));
-}
 __device__ __forceinline__ int pair_idx(int I, int J) { return I == 2 ? 0 : (J == 0 ? 1 : 2); }
 
-// The permuted-order fragment of ld_col (see gla_vsweep.hip): lane (g, j)
-// gets X[r0 + 8g + i][c0 + 8 (j / 4) + 4 h + j % 4].
-template <typename T>
-__device__ __forceinline__ frag_t<T> ld_col_perm(const T *X, int ld, int r0, int c0, int h) {
-  const int l = lane_id(), g = l >> 4, j = l & 15;
-  if constexpr (sizeof(T) == 2) {
-    const T *p0 = X + (r0 + 8 * g + (j >> 2)) * ld + c0 + 8 * (j & 3) + 4 * h;
-    const T *p1 = p0 + 4 * ld;
-    s4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4 *)(p0));
-    s4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4 *)(p1));
-    s8 r = s8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
-    return __builtin_bit_cast(bf16x8, r);
-  } else {
-    const T *p = X + (r0 + 8 * g) * ld + c0 + 8 * (j >> 2) + 4 * h + (j & 3);
-    f8 r;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) r[i] = p[i * ld];
-    return r;
+// ------------------------------------------------------------- 32x32 tiles
+// v_mfma_f32_32x32x16_bf16 (or 8 x v_mfma_f32_32x32x2f32): lane l = 32 g + j
+// holds A[j][8g + i], B[8g + i][j] and D[8b + 4g + r][j] = acc[4b + r].
+template <typename T> struct Mma32;
+template <> struct Mma32<bf16> {
+  static __device__ __forceinline__ f16v mma(f16v c, bf16x8 a, bf16x8 b) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
   }
+};
+template <> struct Mma32<float> {
+  static __device__ __forceinline__ f16v mma(f16v c, f8 a, f8 b) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) c = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[i], c, 0, 0, 0);
+    return c;
+  }
+};
+template <typename T> __device__ __forceinline__ f16v mma32(f16v c, frag_t<T> a, frag_t<T> b) {
+  return Mma32<T>::mma(c, a, b);
 }
 
-// Slab tiles (V, dO) are stored with their 16-byte chunks XOR-swizzled per
-// row, chunk c of row r at c ^ swz(r): both the 16-row fragment reads (one
-// chunk of 16 consecutive rows) and the transpose reads (4 rows x 4 chunks)
-// then touch distinct LDS banks without padding.
+// Value offset (within a wave's 32) of accumulator row m.
+__device__ __forceinline__ int perm32(int m) {
+  return 16 * (m >> 4) + 8 * ((m >> 2) & 1) + 4 * ((m >> 3) & 1) + (m & 3);
+}
+// Value offset of accumulator element e of lane group g.
+__device__ __forceinline__ int acc_value(int e, int g) { return perm32(8 * (e >> 2) + 4 * g + (e & 3)); }
+
+// Slab tiles: rows of kRowB bytes (256 bf16 or 128 fp32 values) whose 16-byte
+// chunk c is stored at chunk c ^ swz(row).  The swizzle permutes the low four
+// chunk bits only and the row offset starts at bit 9, so the byte offset of
+// (row r0 + rr, chunk c0 / E + cc), with r0 a multiple of 16 and c0 a multiple
+// of 16 values above the lane's own chunk bits cc, splits into a per-lane part
+// XOR a wave-uniform column part, plus r0 kRowB: each lane keeps one base per
+// read pattern and every read is one XOR (or none) away from it.
+constexpr int kRowB = 512;
 __device__ __forceinline__ int swz(int row) { return ((row & 3) << 2) | ((row >> 2) & 3); }
-template <typename T> __device__ __forceinline__ int sw_off(int row, int col, int ld) {
-  constexpr int EV = 16 / sizeof(T);
-  return row * ld + ((col / EV) ^ swz(row)) * EV + col % EV;
+
+// Lane base of a row fragment (rows r0 + j, columns c0 + 8g; for fp32 half h
+// holds columns + 4h).
+template <typename T> __device__ __forceinline__ int row_lane_base(int h) {
+  const int l = lane_id(), j = l & 31, g = l >> 5;
+  const int ch = sizeof(T) == 2 ? g : 2 * g + h;
+  return j * kRowB + ((ch ^ swz(j)) << 4);
 }
 
-// ld_row on a swizzled tile: lane (g, j) gets X[r0 + j][c0 + 8g + i].
+// Row fragment from a slab: lane (g, j) gets X[r0 + j][c0 + 8g + i].
 template <typename T>
-__device__ __forceinline__ frag_t<T> ld_row_sw(const T *X, int ld, int r0, int c0) {
-  const int l = lane_id(), row = r0 + (l & 15), col = c0 + 8 * (l >> 4);
+__device__ __forceinline__ frag_t<T> ld_slab_row(const T *X, int lb0, int lb1, int r0, int c0) {
+  const char *p = (const char *)X + r0 * kRowB;
+  const int x = c0 * (int)sizeof(T);
   if constexpr (sizeof(T) == 2) {
-    return *(const bf16x8 *)(X + sw_off<T>(row, col, ld));
+    return *(const bf16x8 *)(p + (lb0 ^ x));
   } else {
-    const f4 a = *(const f4 *)(X + sw_off<T>(row, col, ld)), b = *(const f4 *)(X + sw_off<T>(row, col + 4, ld));
+    const f4 a = *(const f4 *)(p + (lb0 ^ x)), b = *(const f4 *)(p + (lb1 ^ x));
     return f8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
   }
 }
 
-// ld_col_perm on a swizzled tile.
+// Column fragment with permuted columns from a slab: lane (g, j) gets
+// X[r0 + 8g + i][c0 + perm32(j)], c0 a multiple of 32.  For bf16 each LDS
+// transpose read returns, to lane L of a 16-lane block, element L % 4 of the
+// 4-vector loaded by lane 4 m + L / 4 (m = 0..3), so lane 4a + b of block
+// (g, jh) points at row r0 + 8g + a (+4 for the second read) and columns
+// c0 + 16 jh + 8 (b % 2) + 4 (b / 2) + 0..3; tr_lane_base(0 / 4) are the two
+// lane bases.
+__device__ __forceinline__ int tr_lane_base(int x4) {
+  const int l = lane_id(), L = l & 15, jh = (l >> 4) & 1, g = l >> 5;
+  const int row = 8 * g + (L >> 2) + x4;
+  const int ch = 2 * jh + (L & 1);
+  return row * kRowB + ((ch ^ swz(row)) << 4) + 8 * ((L >> 1) & 1);
+}
 template <typename T>
-__device__ __forceinline__ frag_t<T> ld_col_perm_sw(const T *X, int ld, int r0, int c0, int h) {
-  const int l = lane_id(), g = l >> 4, j = l & 15;
+__device__ __forceinline__ frag_t<T> ld_slab_col_perm(const T *X, int lt0, int lt1, int r0, int c0) {
   if constexpr (sizeof(T) == 2) {
-    const int row = r0 + 8 * g + (j >> 2), col = c0 + 8 * (j & 3) + 4 * h;
-    s4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4 *)(X + sw_off<T>(row, col, ld)));
-    s4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4 *)(X + sw_off<T>(row + 4, col, ld)));
+    const char *p = (const char *)X + r0 * kRowB;
+    const int x = c0 * 2;
+    s4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4 *)(p + (lt0 ^ x)));
+    s4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4 *)(p + (lt1 ^ x)));
     s8 r = s8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
     return __builtin_bit_cast(bf16x8, r);
   } else {
-    const int row = r0 + 8 * g, col = c0 + 8 * (j >> 2) + 4 * h + (j & 3);
+    const int l = lane_id(), g = l >> 5, col = c0 + perm32(l & 31);
     f8 r;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) r[i] = X[sw_off<T>(row + i, col, ld)];
+    for (int i = 0; i < 8; ++i) {
+      const int row = r0 + 8 * g + i;
+      r[i] = X[row * (kRowB / 4) + (((col >> 2) ^ swz(row)) << 2) + (col & 3)];
+    }
     return r;
   }
 }
 
+// Plain (unswizzled) row fragment: lane (g, j) gets X[r0 + j][c0 + 8g + i].
+template <typename T>
+__device__ __forceinline__ frag_t<T> ld_row32(const T *X, int ld, int r0, int c0) {
+  const int l = lane_id();
+  const T *p = X + (r0 + (l & 31)) * ld + c0 + 8 * (l >> 5);
+  if constexpr (sizeof(T) == 2) {
+    return *(const bf16x8 *)p;
+  } else {
+    const f4 a = *(const f4 *)p, b = *(const f4 *)(p + 4);
+    return f8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  }
+}
+
+// The 8 accumulator values of 16-deep step st as an operand, split into bf16
+// hi + lo (to ~16 mantissa bits; lo unused for fp32).
+template <typename T>
+__device__ __forceinline__ void acc_split32(const f16v &acc, int st, frag_t<T> &hi, frag_t<T> &lo) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    hi[i] = cvt<T>(acc[8 * st + i]);
+    if constexpr (sizeof(T) == 2) lo[i] = cvt<T>(acc[8 * st + i] - (float)hi[i]);
+  }
+}
+
+// ------------------------------------------------------------- 16x16 tiles
 // Four consecutive elements as one 8-byte (bf16) or 16-byte (fp32) LDS store.
 template <typename T> __device__ __forceinline__ void store4(T *p, const T (&v)[4]) {
   if constexpr (sizeof(T) == 2) *(bf16x4 *)p = bf16x4{v[0], v[1], v[2], v[3]};
   else *(f4 *)p = f4{v[0], v[1], v[2], v[3]};
 }
 
-// hi + lo = the fp32 accumulator pair to ~16 mantissa bits (lo unused for fp32).
-template <typename T>
-__device__ __forceinline__ void acc_split(f4 a0, f4 a1, frag_t<T> &hi, frag_t<T> &lo) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    hi[i] = cvt<T>(a0[i]);
-    hi[4 + i] = cvt<T>(a1[i]);
-    if constexpr (sizeof(T) == 2) {
-      lo[i] = cvt<T>(a0[i] - (float)hi[i]);
-      lo[4 + i] = cvt<T>(a1[i] - (float)hi[4 + i]);
-    }
-  }
-}
-
-// fp32 fragment from an fp32 LDS tile: lane (g, j) gets X[r0 + j][c0 + 8g + i].
+// fp32 fragment from an fp32 LDS tile: lane (g, j) gets X[r0 + j][c0 + 8g + i]
+// (16x16 layout, g = l / 16).
 __device__ __forceinline__ f8 ldf_row(const float *X, int ld, int r0, int c0) {
   const int l = lane_id();
   const float *p = X + (r0 + (l & 15)) * ld + c0 + 8 * (l >> 4);
@@ -213,7 +254,14 @@ template <typename T> __device__ __forceinline__ uint32_t ld_elem(__amdgpu_buffe
   if constexpr (sizeof(T) == 2) return (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(rs, off, 0, 0);
   else return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0);
 }
+template <typename T> __device__ __forceinline__ void st_elem(__amdgpu_buffer_rsrc_t rs, uint32_t off, T v) {
+  if constexpr (sizeof(T) == 2)
+    __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, v), rs, off, 0, 0);
+  else
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned int, v), rs, off, 0, 0);
+}
 
+// ------------------------------------------------------------- gate factors
 // Cumulative-sum bookkeeping of one factor thread (feature fk, rows 4 frg ..
 // +3 of the chunk), from the chunk's row-group totals in LDS.
 struct Factors {
@@ -221,59 +269,98 @@ struct Factors {
   float pre;      // log decay of the blocks before this thread's block
   float tot;      // log decay of this thread's 16-row block
   float blast;    // log decay of the whole chunk
+  float bs[4];    // log decay of each 16-row block
   bool wide;
 };
 
 template <int NRG, int LDRG>
-__device__ __forceinline__ Factors chunk_factors(const float *sRg, const float (&c)[4], int frg, int fk,
-                                                 bool fv) {
+__device__ __forceinline__ Factors chunk_factors(const float *sRg, const float (&c)[4], int frg, int blk,
+                                                 int fk, bool fv) {
+  // blk (the thread's 16-row block) is uniform across the wave; frg % 4 (its
+  // row group inside the block) is not
   Factors f;
-  const int blk = frg >> 2;
-  float ex = 0.f;
-  f.pre = f.tot = f.blast = 0.f;
-  float rg[NRG];
+  float *bs = f.bs;
+  bs[1] = bs[2] = bs[3] = 0.f;
 #pragma unroll
-  for (int p = 0; p < NRG; p += 4) {
-    const f4 v = *(const f4 *)(sRg + fk * LDRG + p);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) rg[p + e] = v[e];
+  for (int b = 0; b < NRG / 4; ++b) {
+    const f4 v = *(const f4 *)(sRg + fk * LDRG + 4 * b);
+    bs[b] = (v[0] + v[1]) + (v[2] + v[3]);
   }
+  const f4 in_blk = *(const f4 *)(sRg + fk * LDRG + 4 * blk);
+  f.blast = 0.f;
+  f.pre = 0.f;
 #pragma unroll
-  for (int p = 0; p < NRG; ++p) {
-    const float t = rg[p];
-    f.blast += t;
-    if ((p >> 2) < blk) f.pre += t;
-    if ((p >> 2) == blk) {
-      f.tot += t;
-      if (p < frg) ex += t;
-    }
+  for (int b = 0; b < NRG / 4; ++b) {
+    f.blast += bs[b];
+    if (b < blk) f.pre += bs[b];
   }
+  f.tot = (in_blk[0] + in_blk[1]) + (in_blk[2] + in_blk[3]);
+  const int q = frg & 3;
+  const float ex = q == 0 ? 0.f : (q == 1 ? in_blk[0] : (q == 2 ? in_blk[0] + in_blk[1] : in_blk[0] + in_blk[1] + in_blk[2]));
 #pragma unroll
   for (int i = 0; i < 4; ++i) f.Bloc[i] = ex + c[i];
   f.wide = fv && (-f.tot > kWide);
   return f;
 }
 
-// Per-chunk gate data every factor thread publishes: exp of the block-level
-// scale, gamma and the decays between non-adjacent blocks.
+// Per-chunk gate data the factor threads publish: the block-level scale of the
+// inter partials, the diagonal-block operand scale exp(-tot) (zero where the
+// block needs pairwise decays), gamma and the decays between non-adjacent
+// blocks.
 template <int NB, int LDRG>
-__device__ __forceinline__ void publish_decays(float *sSc, float *sG, float *sGp, const float *sRg,
-                                               const Factors &f, float scale_log, int frg, int fk,
-                                               bool fv) {
-  if ((frg & 3) == 0) sSc[(frg >> 2) * kKF + fk] = __expf(scale_log);
+__device__ __forceinline__ void publish_decays(float *sSc, float *sEt, float *sG, float *sGp,
+                                               const Factors &f, float scale_log,
+                                               int frg, int fk, bool fv) {
+  if ((frg & 3) == 0) {
+    sSc[(frg >> 2) * kKF + fk] = __expf(scale_log);
+    sEt[(frg >> 2) * kKF + fk] = f.wide ? 0.f : __expf(-f.tot);
+  }
   if (frg == 0) {
     sG[fk] = fv ? __expf(f.blast) : 0.f;
     if constexpr (NB == 4) {
-      float t1 = 0.f, t2 = 0.f;
-#pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        t1 += sRg[fk * LDRG + 4 + p];
-        t2 += sRg[fk * LDRG + 8 + p];
-      }
-      sGp[0 * kKF + fk] = __expf(t1);
-      sGp[1 * kKF + fk] = __expf(t1 + t2);
-      sGp[2 * kKF + fk] = __expf(t2);
+      sGp[0 * kKF + fk] = __expf(f.bs[1]);
+      sGp[1 * kKF + fk] = __expf(f.bs[1] + f.bs[2]);
+      sGp[2 * kKF + fk] = __expf(f.bs[2]);
     }
+  }
+}
+
+// Reduction of the d_v-reducing partials (rows t, feature j; 32-row tiles th):
+// pre-scale by the per-(16-row block, feature) factor, then the upper half of
+// the state waves publishes to LDS ...
+template <typename L>
+__device__ __forceinline__ void partials_publish(f16v (&acc)[2], const float *sSc, float *sRed, int w,
+                                                 int g, int j) {
+  constexpr int NTT = L::NB / 2;
+  float sc[L::NB];
+#pragma unroll
+  for (int J = 0; J < L::NB; ++J) sc[J] = sSc[J * kKF + j];
+#pragma unroll
+  for (int th = 0; th < NTT; ++th)
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[th][4 * b + r] *= sc[2 * th + (b >> 1)];
+  if (w >= L::NP && w < L::NWS) {
+#pragma unroll
+    for (int th = 0; th < NTT; ++th)
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+        *(f4 *)(sRed + ((w - L::NP) * kKF + j) * L::LDT + 32 * th + 8 * b + 4 * g) =
+            f4{acc[th][4 * b], acc[th][4 * b + 1], acc[th][4 * b + 2], acc[th][4 * b + 3]};
+  }
+}
+// ... and, after a barrier, the lower half adds its partial in place.
+template <typename L>
+__device__ __forceinline__ void partials_add(const f16v (&acc)[2], float *sRed, int w, int g, int j) {
+  constexpr int NTT = L::NB / 2;
+  if (w < L::NP) {
+#pragma unroll
+    for (int th = 0; th < NTT; ++th)
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+        *(f4 *)(sRed + (w * kKF + j) * L::LDT + 32 * th + 8 * b + 4 * g) +=
+            f4{acc[th][4 * b], acc[th][4 * b + 1], acc[th][4 * b + 2], acc[th][4 * b + 3]};
   }
 }
 
@@ -281,42 +368,45 @@ __device__ __forceinline__ void publish_decays(float *sSc, float *sG, float *sGp
 template <typename T, int CP, int NSL>
 __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   using L = KsLayout<T, CP>;
-  constexpr int NB = L::NB, NRG = L::NRG, NSC = CP / 32, NBLK = NB * (NB + 1) / 2;
-  constexpr int NUP = NB * (NB - 1) / 2;
+  constexpr int VS = L::VS, NB = L::NB, NRG = L::NRG, NST = CP / 16, NTT = CP / 32;
+  constexpr int NDP = CP == 64 ? 8 : 2;  // waves whose dP unit is published
   constexpr bool SPLIT = sizeof(T) == 2;
+  static_assert(VS * sizeof(T) == kRowB, "slab row size");
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  T *sV0 = (T *)(smem + L::offV), *sD0 = (T *)(smem + L::offD);
+  T *sV = (T *)(smem + L::offV), *sD = (T *)(smem + L::offD);
   T *sBh = (T *)(smem + L::offBh), *sBl = (T *)(smem + L::offBl);
-  float *sKo = (float *)(smem + L::offO), *sKp = (float *)(smem + L::offPk);
+  float *sKo = (float *)(smem + L::offO);
   float *sBloc = (float *)(smem + L::offBloc), *sdP = (float *)(smem + L::offdP);
   float *sRed = (float *)(smem + L::offRed), *sOr = (float *)(smem + L::offOr);
   float *sRg = (float *)(smem + L::offRg), *sSc = (float *)(smem + L::offSc);
+  float *sEt = (float *)(smem + L::offEt);
   float *sGp = (float *)(smem + L::offGp), *sG = (float *)(smem + L::offG);
   float *sRedS = (float *)(smem + L::offRedS), *sFt = (float *)(smem + L::offFt);
 
   int bh, kt;
   xcd_map(a.BH, a.KT, bh, kt);
-  const int tid = threadIdx.x, w = wave_id(), l = lane_id(), g = l >> 4, j = l & 15;
-  const int kb = w & 1, vq = w >> 1;
+  const int tid = threadIdx.x, w = wave_id() & 7, l = lane_id();
+  const int g = l >> 5, j = l & 31;  // 32x32 tile lane coordinates
+  const bool sw = w < L::NWS;        // this wave holds state
   const int K = a.K, V = a.V, C = a.C, N = a.N, k0 = kt * kKF;
   const int fk = tid & 31, frg = tid >> 5;
   const bool fthr = frg < NRG;
   const int kf = k0 + fk;
   const bool fv = kf < K;
   const int esz = sizeof(T);
+  const int lb0 = row_lane_base<T>(0), lb1 = row_lane_base<T>(1);
+  const int lt0 = tr_lane_base(0), lt1 = tr_lane_base(4);
 
   for (int i = tid; i < CP * L::LDP; i += kKT) sdP[i] = 0.f;
 
-  f4 S[NSL][2];
+  f16v S[NSL];
 #pragma unroll
   for (int sl = 0; sl < NSL; ++sl)
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int vv = sl * kVS + 32 * vq + 8 * g + 4 * h + r, kq = k0 + 16 * kb + j;
-        S[sl][h][r] = (a.S0 && vv < V && kq < K) ? a.S0[((int64_t)bh * K + kq) * V + vv] : 0.f;
-      }
+    for (int e = 0; e < 16; ++e) {
+      const int vv = sl * VS + 32 * w + acc_value(e, g), kq = k0 + j;
+      S[sl][e] = (a.S0 && sw && vv < V && kq < K) ? a.S0[((int64_t)bh * K + kq) * V + vv] : 0.f;
+    }
 
   // ---- input streams
   const T *kh_ = (const T *)a.k + (int64_t)bh * a.T * K, *lah = (const T *)a.la + (int64_t)bh * a.T * K;
@@ -330,40 +420,40 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   uint32_t fin_la[4], fin_k[4];
   auto fetch_factors = [&](int n) {
     const int t0 = n * C;
-    const auto rs_la = make_rsrc(lah + (int64_t)t0 * K, rsrc_bytes((int64_t)(a.T - t0) * K * esz));
-    const auto rs_k = make_rsrc(kh_ + (int64_t)t0 * K, rsrc_bytes((int64_t)(a.T - t0) * K * esz));
+    const uint32_t bytes = rsrc_bytes((int64_t)(a.T - t0) * K * esz);
+    const auto rs_la = make_rsrc(lah + (int64_t)t0 * K, bytes);
+    const auto rs_k = make_rsrc(kh_ + (int64_t)t0 * K, bytes);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       fin_la[i] = ld_elem<T>(rs_la, eoff[i]);
       fin_k[i] = ld_elem<T>(rs_k, eoff[i]);
     }
   };
-  TileLd<T, CP, kVS, kKT> pv, pd;
-  pv.init(V, C, kVS);
-  pd.init(V, C, kVS);
+  TileLd<T, CP, VS, kKT> pv, pd;
+  pv.init(V, C, VS);
+  pd.init(V, C, VS);
   const int NQ = N * NSL;
   auto fetch_slab = [&](int q) {
-    if (q >= NQ) return;
-    const int n = q / NSL, sl = q - n * NSL, t0 = n * C, c0 = sl * kVS;
+    q = min(q, NQ - 1);  // unconditional, see fetch_factors
+    const int n = q / NSL, sl = q - n * NSL, t0 = n * C, c0 = sl * VS;
     const uint32_t bytes = rsrc_bytes(((int64_t)(a.T - t0) * V - c0) * esz);
     pv.load(make_rsrc(vh + (int64_t)t0 * V + c0, bytes), V - c0);
     pd.load(make_rsrc(dOh + (int64_t)t0 * V + c0, bytes), V - c0);
   };
-  auto store_slab = [&](int q) {
-    const int b = L::DB ? (q & 1) : 0;
-    pv.store_swz((T *)((char *)sV0 + b * L::slab), L::LDV);
-    pd.store_swz((T *)((char *)sD0 + b * L::slab), L::LDV);
-  };
 
   T *dqo = (T *)a.dq + (int64_t)bh * a.T * K, *dqlo = (T *)a.dq_lo + (int64_t)bh * a.T * K;
   float *dPg = a.dP + (int64_t)bh * N * C * C;
+  // this wave's dP unit: the 32x32 tile (t rows 32 tr.., s columns 32 tc..)
+  // over value half ph of every slab; with C = 64 waves 6 and 7 take the tile
+  // above the diagonal, which the mask zeroes, so that every wave runs the
+  // same code (with C <= 32 only waves 0 and 1 publish theirs)
+  const int dtile = CP == 64 ? w >> 1 : 0, ph = w & 1;
+  const int tr = (dtile == 1 || dtile == 2) ? 1 : 0, tc = dtile >= 2 ? 1 : 0;
+  const int pA = (lb0 ^ (ph * (kRowB / 2))) + 32 * tr * kRowB, pB = (lb0 ^ (ph * (kRowB / 2))) + 32 * tc * kRowB;
+  const int pA1 = (lb1 ^ (ph * (kRowB / 2))) + 32 * tr * kRowB, pB1 = (lb1 ^ (ph * (kRowB / 2))) + 32 * tc * kRowB;
 
   fetch_factors(0);
   fetch_slab(0);
-  if constexpr (L::DB) {
-    store_slab(0);
-    fetch_slab(1);
-  }
 
   for (int n = 0; n < N; ++n) {
     const int t0 = n * C, rv = min(C, a.T - t0);
@@ -381,10 +471,10 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
     }
     __syncthreads();
     if (fthr) {
-      const Factors f = chunk_factors<NRG, L::LDRG>(sRg, c, frg, fk, fv);
+      const Factors f = chunk_factors<NRG, L::LDRG>(sRg, c, frg, w >> 1, fk, fv);
       sFt[frg * kKF + fk] = f.tot;
-      const float etot = __expf(-f.tot), ekt = __expf(f.blast - f.pre - f.tot);
-      f4 ko4, kp4, bl4;
+      const float ekt = __expf(f.blast - f.pre - f.tot);
+      f4 ko4, bl4;
       T hi4[4], lo4[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -393,137 +483,122 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
         hi4[i] = cvt<T>(kt_);
         lo4[i] = cvt<T>(kt_ - (float)hi4[i]);
         ko4[i] = ks;
-        kp4[i] = f.wide ? 0.f : ks * etot;
         bl4[i] = f.Bloc[i];
       }
       store4<T>(sBh + fk * L::LDTB + 4 * frg, hi4);
       if constexpr (SPLIT) store4<T>(sBl + fk * L::LDTB + 4 * frg, lo4);
       *(f4 *)(sKo + fk * L::LDT + 4 * frg) = ko4;
-      *(f4 *)(sKp + fk * L::LDT + 4 * frg) = kp4;
       *(f4 *)(sBloc + fk * L::LDT + 4 * frg) = bl4;
-      publish_decays<NB, L::LDRG>(sSc, sG, sGp, sRg, f, f.pre, frg, fk, fv);
+      publish_decays<NB, L::LDRG>(sSc, sEt, sG, sGp, f, f.pre, frg, fk, fv);
     }
-    if (n + 1 < N) fetch_factors(n + 1);
+    // unconditional (the last chunk re-reads itself) so that the wait counts
+    // for the slab prefetch below stay exact
+    fetch_factors(min(n + 1, N - 1));
     __syncthreads();
 
-    // ---- slabs: dP blocks, dq_inter partials (state before the chunk), update
-    frag_t<T> bh_[NSC], bl_[NSC];
+    // ---- slabs: dP tiles, dq_inter partials (state before the chunk), update
+    frag_t<T> bh_[NST], bl_[NST];
 #pragma unroll
-    for (int sc = 0; sc < NSC; ++sc) {
-      bh_[sc] = ld_row<T>(sBh, L::LDTB, 16 * kb, 32 * sc);
-      if constexpr (SPLIT) bl_[sc] = ld_row<T>(sBl, L::LDTB, 16 * kb, 32 * sc);
+    for (int st = 0; st < NST; ++st) {
+      bh_[st] = ld_row32<T>(sBh, L::LDTB, 0, 16 * st);
+      if constexpr (SPLIT) bl_[st] = ld_row32<T>(sBl, L::LDTB, 0, 16 * st);
     }
-    const float gam = sG[16 * kb + j];
-    f4 acc[NB], accP[2];
+    const float gam = sG[j];
+    f16v acc[2], accP;
 #pragma unroll
-    for (int I = 0; I < NB; ++I) acc[I] = zero4();
-    accP[0] = accP[1] = zero4();
-    int pI0, pJ0, pI1, pJ1;
-    low_block(w, pI0, pJ0);
-    low_block(w + 8, pI1, pJ1);
+    for (int e = 0; e < 16; ++e) acc[0][e] = acc[1][e] = accP[e] = 0.f;
 #pragma unroll
     for (int sl = 0; sl < NSL; ++sl) {
       const int q = n * NSL + sl;
-      if constexpr (!L::DB) {
-        store_slab(q);
-        fetch_slab(q + 1);
-        __syncthreads();
-      }
-      const int b = L::DB ? (q & 1) : 0;
-      const T *sV = (const T *)((const char *)sV0 + b * L::slab);
-      const T *sD = (const T *)((const char *)sD0 + b * L::slab);
-      if (sl * kVS < V) {
-        // dP = dO V^T over this slab, for this wave's blocks
-        if (w < NBLK) {
+      pv.store_swz(sV, L::LDV);
+      pd.store_swz(sD, L::LDV);
+      __syncthreads();
+      fetch_slab(q + 1);
+      {
+        // dP = dO V^T for this wave's (tile, value half)
 #pragma unroll
-          for (int s = 0; s < kVS / 32; ++s)
-            accP[0] = mma<T>(accP[0], ld_row_sw<T>(sD, L::LDV, 16 * pI0, 32 * s), ld_row_sw<T>(sV, L::LDV, 16 * pJ0, 32 * s));
-        }
-        if (w + 8 < NBLK) {
+        for (int st = 0; st < VS / 32; ++st)
+          accP = mma32<T>(accP, ld_slab_row<T>(sD, pA, pA1, 0, 16 * st), ld_slab_row<T>(sV, pB, pB1, 0, 16 * st));
+        if (sw) {
+          // dq_inter += dO[:, this wave's 32 value rows] S^T
 #pragma unroll
-          for (int s = 0; s < kVS / 32; ++s)
-            accP[1] = mma<T>(accP[1], ld_row_sw<T>(sD, L::LDV, 16 * pI1, 32 * s), ld_row_sw<T>(sV, L::LDV, 16 * pJ1, 32 * s));
-        }
-        // dq_inter += dO[:, this wave's 32 value rows] S^T
-        frag_t<T> shi, slo;
-        acc_split<T>(S[sl][0], S[sl][1], shi, slo);
+          for (int st = 0; st < 2; ++st) {
+            frag_t<T> shi, slo;
+            acc_split32<T>(S[sl], st, shi, slo);
 #pragma unroll
-        for (int I = 0; I < NB; ++I) {
-          const frag_t<T> ad = ld_row_sw<T>(sD, L::LDV, 16 * I, 32 * vq);
-          acc[I] = mma<T>(acc[I], ad, shi);
-          if constexpr (SPLIT) acc[I] = mma<T>(acc[I], ad, slo);
-        }
-        // S^T <- gamma S^T + V^T (K (.) Gamma)
+            for (int th = 0; th < NTT; ++th) {
+              const frag_t<T> ad = ld_slab_row<T>(sD, lb0, lb1, 32 * th, 32 * w + 16 * st);
+              acc[th] = mma32<T>(acc[th], ad, shi);
+              if constexpr (SPLIT) acc[th] = mma32<T>(acc[th], ad, slo);
+            }
+          }
+          // S^T <- gamma S^T + V^T (K (.) Gamma)
+          S[sl] *= gam;
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          S[sl][h] *= gam;
-#pragma unroll
-          for (int sc = 0; sc < NSC; ++sc) {
-            const frag_t<T> av = ld_col_perm_sw<T>(sV, L::LDV, 32 * sc, 32 * vq, h);
-            S[sl][h] = mma<T>(S[sl][h], av, bh_[sc]);
-            if constexpr (SPLIT) S[sl][h] = mma<T>(S[sl][h], av, bl_[sc]);
+          for (int st = 0; st < NST; ++st) {
+            const frag_t<T> av = ld_slab_col_perm<T>(sV, lt0, lt1, 16 * st, 32 * w);
+            S[sl] = mma32<T>(S[sl], av, bh_[st]);
+            if constexpr (SPLIT) S[sl] = mma32<T>(S[sl], av, bl_[st]);
           }
         }
       }
-      if constexpr (L::DB) {
-        store_slab(q + 1);
-        fetch_slab(q + 2);
+      // the second value half of each dP tile hands its partial over in LDS
+      if (sl == NSL - 1 && w < NDP && ph == 1) {
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            sdP[(32 * tr + 8 * b + 4 * g + r) * L::LDP + 32 * tc + j] = accP[4 * b + r];
       }
       __syncthreads();
     }
 
-    // ---- dP to LDS (and to the workspace for the dk sweep)
+    // ---- dP: sum the two halves, mask, publish (and hand it to the dk sweep transposed)
+    if (w < NDP && ph == 0) {
+      float *pd0 = sdP + (32 * tr + 4 * g) * L::LDP + 32 * tc + j;
+      float other[16];
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int bI = u ? pI1 : pI0, bJ = u ? pJ1 : pJ0;
-      if (w + 8 * u < NBLK) {
-        const int t4 = 16 * bI + 4 * g, col = 16 * bJ + j;
+      for (int e = 0; e < 16; ++e) other[e] = pd0[(8 * (e >> 2) + (e & 3)) * L::LDP];
+      const int col = 32 * tc + j;
+      const auto rs_dp = make_rsrc(dPg + (int64_t)n * C * C, (uint32_t)(C * C * 4));
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int t4 = 32 * tr + 8 * b + 4 * g;
         f4 v4;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          v4[r] = col > t4 + r ? 0.f : accP[u][r];
-          sdP[(t4 + r) * L::LDP + col] = v4[r];
+          v4[r] = col > t4 + r ? 0.f : accP[4 * b + r] + other[4 * b + r];
+          pd0[(8 * b + r) * L::LDP] = v4[r];
         }
-        // the workspace holds dP transposed ([s][t]) for the dk sweep
-        if (kt == 0 && t4 < C && col < C) *(f4 *)(dPg + ((int64_t)n * C + col) * C + t4) = v4;
+        if (kt == 0) {
+          const uint32_t off = (t4 < C && col < C) ? (uint32_t)((col * C + t4) * 4) : 0x80000000u;
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v4), rs_dp, off, 0, 0);
+        }
       }
     }
-    if (kt == 0 && w < NUP) {
-      int uI, uJ;
-      up_block(w, uI, uJ);
-      const int t4 = 16 * uI + 4 * g, col = 16 * uJ + j;
-      if (t4 < C && col < C) *(f4 *)(dPg + ((int64_t)n * C + col) * C + t4) = zero4();
-    }
     // ---- dq_inter partials, pre-scaled by exp(log decay before the block)
-#pragma unroll
-    for (int I = 0; I < NB; ++I) acc[I] *= sSc[I * kKF + 16 * kb + j];
-    if (vq >= 2) {
-#pragma unroll
-      for (int I = 0; I < NB; ++I) *(f4 *)(sRed + ((vq - 2) * kKF + 16 * kb + j) * L::LDT + 16 * I + 4 * g) = acc[I];
-    }
+    partials_publish<L>(acc, sSc, sRed, w, g, j);
     __syncthreads();
-    if (vq < 2) {
-#pragma unroll
-      for (int I = 0; I < NB; ++I) *(f4 *)(sRed + (vq * kKF + 16 * kb + j) * L::LDT + 16 * I + 4 * g) += acc[I];
-    }
+    partials_add<L>(acc, sRed, w, g, j);
     // intra-chunk term by sub-chunk blocks, for row block I: sum over J <= I of
     // dP_IJ x_J with x_J = (k (.) exp(tot_J - Bloc)) g_IJ below the diagonal and
     // k (.) exp(-Bloc) on it (zero where the block needs pairwise decays)
     for (int t = w; t < 2 * NB; t += 8) {
-      const int I = t >> 1, kq = t & 1;
+      const int I = t >> 1, kq = t & 1, j16 = l & 15, g16 = l >> 4;
       f4 o = zero4();
 #pragma unroll
-      for (int s = 0; s < NSC; ++s) {
+      for (int s = 0; s < CP / 32; ++s) {
         if (32 * s > 16 * I) continue;
-        const int J = 2 * s + (g >> 1);
-        const float sc = J > I ? 0.f : (J <= I - 2 ? sGp[pair_idx(I, J) * kKF + 16 * kq + j] : 1.f);
-        const f8 ko = ldf_row(sKo, L::LDT, 16 * kq, 32 * s), kp = ldf_row(sKp, L::LDT, 16 * kq, 32 * s);
-        f8 bf;
+        const int J = 2 * s + (g16 >> 1);
+        const float sc = J > I ? 0.f
+                               : (J == I ? sEt[I * kKF + 16 * kq + j16]
+                                         : (J <= I - 2 ? sGp[pair_idx(I, J) * kKF + 16 * kq + j16] : 1.f));
+        f8 bf = ldf_row(sKo, L::LDT, 16 * kq, 32 * s);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) bf[i] = J == I ? kp[i] : ko[i] * sc;
+        for (int i = 0; i < 8; ++i) bf[i] *= sc;
         o = mma_split3<T>(o, ldf_row(sdP, L::LDP, 16 * I, 32 * s), bf);
       }
-      *(f4 *)(sOr + (16 * kq + j) * L::LDT + 16 * I + 4 * g) = o;
+      *(f4 *)(sOr + (16 * kq + j16) * L::LDT + 16 * I + 4 * g16) = o;
     }
     __syncthreads();
 
@@ -531,15 +606,18 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
     if (fthr) {
       const int blk = frg >> 2;
       const bool wide = fv && (-sFt[frg * kKF + fk] > kWide);
-      const f4 r0 = *(const f4 *)(sRed + fk * L::LDT + 4 * frg);
-      const f4 r1 = *(const f4 *)(sRed + (kKF + fk) * L::LDT + 4 * frg);
-      const f4 op = *(const f4 *)(sOr + fk * L::LDT + 4 * frg);
+      f4 in4 = *(const f4 *)(sOr + fk * L::LDT + 4 * frg);
+#pragma unroll
+      for (int p = 0; p < L::NP; ++p) in4 += *(const f4 *)(sRed + (p * kKF + fk) * L::LDT + 4 * frg);
       const f4 bl4 = *(const f4 *)(sBloc + fk * L::LDT + 4 * frg);
+      const uint32_t obytes = rsrc_bytes((int64_t)(a.T - t0) * K * esz);
+      const auto rs_dq = make_rsrc(dqo + (int64_t)t0 * K, obytes);
+      const auto rs_dql = make_rsrc(dqlo + (int64_t)t0 * K, obytes);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = 4 * frg + i;
         const float bloc = bl4[i];
-        float dq = __expf(bloc) * (r0[i] + r1[i] + op[i]);
+        float dq = __expf(bloc) * in4[i];
         if (wide && row < rv) {
           // diagonal block with pairwise decays exp(B_row - B_s)
 #pragma unroll 1
@@ -547,11 +625,11 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
             dq += sdP[row * L::LDP + s] * (float)kh_[(int64_t)(t0 + s) * K + kf] *
                   __expf(bloc - sBloc[fk * L::LDT + s]);
         }
-        if (row < rv && fv) {
-          const T hi = cvt<T>(dq);
-          dqo[(int64_t)(t0 + row) * K + kf] = hi;
-          if constexpr (SPLIT) dqlo[(int64_t)(t0 + row) * K + kf] = cvt<T>(dq - (float)hi);
-        }
+        // rows past the sequence end, past the chunk or of absent features
+        // fall outside the buffer range and are dropped
+        const T hi = cvt<T>(dq);
+        st_elem<T>(rs_dq, eoff[i], hi);
+        if constexpr (SPLIT) st_elem<T>(rs_dql, eoff[i], cvt<T>(dq - (float)hi));
       }
     }
   }
@@ -559,24 +637,22 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   // ---- final-state term of the gate gradient: rowsum(S_T (.) dS_T) per feature
   if (a.dST) {
     float part = 0.f;
+    if (sw) {
 #pragma unroll
-    for (int sl = 0; sl < NSL; ++sl)
+      for (int sl = 0; sl < NSL; ++sl)
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int vv = sl * kVS + 32 * vq + 8 * g + 4 * h + r, kq = k0 + 16 * kb + j;
-          if (vv < V && kq < K) part += S[sl][h][r] * a.dST[((int64_t)bh * K + kq) * V + vv];
+        for (int e = 0; e < 16; ++e) {
+          const int vv = sl * VS + 32 * w + acc_value(e, g), kq = k0 + j;
+          if (vv < V && kq < K) part += S[sl][e] * a.dST[((int64_t)bh * K + kq) * V + vv];
         }
-    part += __shfl_xor(part, 16);
+    }
     part += __shfl_xor(part, 32);
     if (g == 0) sRedS[w * kKF + j] = part;
     __syncthreads();
     if (tid < kKF && k0 + tid < K) {
-      const int kq = tid >> 4, jj = tid & 15;
       float s = 0.f;
 #pragma unroll
-      for (int v4 = 0; v4 < 4; ++v4) s += sRedS[(2 * v4 + kq) * kKF + jj];
+      for (int w2 = 0; w2 < 8; ++w2) s += sRedS[w2 * kKF + tid];
       a.cST[(int64_t)bh * K + k0 + tid] = s;
     }
   }
@@ -586,42 +662,45 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
 template <typename T, int CP, int NSL>
 __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
   using L = KsLayout<T, CP>;
-  constexpr int NB = L::NB, NRG = L::NRG, NSC = CP / 32;
+  constexpr int VS = L::VS, NB = L::NB, NRG = L::NRG, NST = CP / 16, NTT = CP / 32;
   constexpr bool SPLIT = sizeof(T) == 2;
+  static_assert(VS * sizeof(T) == kRowB, "slab row size");
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  T *sV0 = (T *)(smem + L::offV), *sD0 = (T *)(smem + L::offD);
+  T *sV = (T *)(smem + L::offV), *sD = (T *)(smem + L::offD);
   T *sBh = (T *)(smem + L::offBh), *sBl = (T *)(smem + L::offBl);
-  float *sQo = (float *)(smem + L::offO), *sQp = (float *)(smem + L::offPk);
+  float *sQo = (float *)(smem + L::offO);
   float *sBloc = (float *)(smem + L::offBloc), *sdP = (float *)(smem + L::offdP);
   float *sRed = (float *)(smem + L::offRed), *sOr = (float *)(smem + L::offOr);
   float *sRg = (float *)(smem + L::offRg), *sSc = (float *)(smem + L::offSc);
+  float *sEt = (float *)(smem + L::offEt);
   float *sGp = (float *)(smem + L::offGp), *sG = (float *)(smem + L::offG);
   float *sCar = (float *)(smem + L::offCar), *sFt = (float *)(smem + L::offFt);
   float *sGrp = (float *)(smem + L::offGrp);
 
   int bh, kt;
   xcd_map(a.BH, a.KT, bh, kt);
-  const int tid = threadIdx.x, w = wave_id(), l = lane_id(), g = l >> 4, j = l & 15;
-  const int kb = w & 1, vq = w >> 1;
+  const int tid = threadIdx.x, w = wave_id() & 7, l = lane_id();
+  const int g = l >> 5, j = l & 31;
+  const bool sw = w < L::NWS;
   const int K = a.K, V = a.V, C = a.C, N = a.N, k0 = kt * kKF;
   const int fk = tid & 31, frg = tid >> 5;
   const bool fthr = frg < NRG;
   const int kf = k0 + fk;
   const bool fv = kf < K;
   const int esz = sizeof(T);
+  const int lb0 = row_lane_base<T>(0), lb1 = row_lane_base<T>(1);
+  const int lt0 = tr_lane_base(0), lt1 = tr_lane_base(4);
 
   if (tid < kKF) sCar[tid] = (a.cST && k0 + tid < K) ? a.cST[(int64_t)bh * K + k0 + tid] : 0.f;
 
-  f4 dS[NSL][2];
+  f16v dS[NSL];
 #pragma unroll
   for (int sl = 0; sl < NSL; ++sl)
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int vv = sl * kVS + 32 * vq + 8 * g + 4 * h + r, kq = k0 + 16 * kb + j;
-        dS[sl][h][r] = (a.dST && vv < V && kq < K) ? a.dST[((int64_t)bh * K + kq) * V + vv] : 0.f;
-      }
+    for (int e = 0; e < 16; ++e) {
+      const int vv = sl * VS + 32 * w + acc_value(e, g), kq = k0 + j;
+      dS[sl][e] = (a.dST && sw && vv < V && kq < K) ? a.dST[((int64_t)bh * K + kq) * V + vv] : 0.f;
+    }
 
   const T *qh_ = (const T *)a.q + (int64_t)bh * a.T * K, *kh_ = (const T *)a.k + (int64_t)bh * a.T * K;
   const T *lah = (const T *)a.la + (int64_t)bh * a.T * K;
@@ -656,156 +735,131 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
     }
     pp.load(make_rsrc(dPg + (int64_t)n * C * C, (uint32_t)(C * C * 4)));
   };
-  TileLd<T, CP, kVS, kKT> pv, pd;
-  pv.init(V, C, kVS);
-  pd.init(V, C, kVS);
+  TileLd<T, CP, VS, kKT> pv, pd;
+  pv.init(V, C, VS);
+  pd.init(V, C, VS);
   const int NQ = N * NSL;
   auto fetch_slab = [&](int q) {
-    if (q >= NQ) return;
-    const int n = N - 1 - q / NSL, sl = q % NSL, t0 = n * C, c0 = sl * kVS;
+    q = min(q, NQ - 1);  // unconditional, see fetch_factors
+    const int n = N - 1 - q / NSL, sl = q % NSL, t0 = n * C, c0 = sl * VS;
     const uint32_t bytes = rsrc_bytes(((int64_t)(a.T - t0) * V - c0) * esz);
     pv.load(make_rsrc(vh + (int64_t)t0 * V + c0, bytes), V - c0);
     pd.load(make_rsrc(dOh + (int64_t)t0 * V + c0, bytes), V - c0);
-  };
-  auto store_slab = [&](int q) {
-    const int b = L::DB ? (q & 1) : 0;
-    pv.store_swz((T *)((char *)sV0 + b * L::slab), L::LDV);
-    pd.store_swz((T *)((char *)sD0 + b * L::slab), L::LDV);
   };
 
   T *dko = (T *)a.dk + (int64_t)bh * a.T * K, *dlao = (T *)a.dla + (int64_t)bh * a.T * K;
 
   fetch_factors(N - 1);
   fetch_slab(0);
-  if constexpr (L::DB) {
-    store_slab(0);
-    fetch_slab(1);
-  }
 
   for (int it = 0; it < N; ++it) {
     const int n = N - 1 - it;
     const int t0 = n * C, rv = min(C, a.T - t0);
     // ---- factors
-    float c[4], qv[4], kv[4], qdq[4];
+    float c[4], kv[4], qdq[4];
     {
       float s = 0.f;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         s += elem_f<T>(fin_la[i]);
         c[i] = s;
-        qv[i] = elem_f<T>(fin_q[i]);
         kv[i] = elem_f<T>(fin_k[i]);
-        qdq[i] = qv[i] * (elem_f<T>(fin_dq[i]) + (SPLIT ? elem_f<T>(fin_dql[i]) : 0.f));
+        qdq[i] = elem_f<T>(fin_q[i]) * (elem_f<T>(fin_dq[i]) + (SPLIT ? elem_f<T>(fin_dql[i]) : 0.f));
       }
       if (fthr) sRg[fk * L::LDRG + frg] = s;
-      pp.store(sdP, L::LDP);
     }
     __syncthreads();
+    pp.store(sdP, L::LDP);  // dP of this chunk, stored transposed ([s][t])
     if (fthr) {
-      const Factors f = chunk_factors<NRG, L::LDRG>(sRg, c, frg, fk, fv);
+      const Factors f = chunk_factors<NRG, L::LDRG>(sRg, c, frg, w >> 1, fk, fv);
       sFt[frg * kKF + fk] = f.tot;
-      const float epre = __expf(f.pre), etot = __expf(-f.tot);
-      f4 qo4, qp4, bl4;
+      const float epre = __expf(f.pre);
+      f4 qo4, bl4;
       T hi4[4], lo4[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float qh = qv[i] * __expf(f.Bloc[i]);
+        const float qh = elem_f<T>(fin_q[i]) * __expf(f.Bloc[i]);
         const float qt = qh * epre;
         hi4[i] = cvt<T>(qt);
         lo4[i] = cvt<T>(qt - (float)hi4[i]);
         qo4[i] = qh;
-        qp4[i] = f.wide ? 0.f : qh * etot;
         bl4[i] = f.Bloc[i];
       }
       store4<T>(sBh + fk * L::LDTB + 4 * frg, hi4);
       if constexpr (SPLIT) store4<T>(sBl + fk * L::LDTB + 4 * frg, lo4);
       *(f4 *)(sQo + fk * L::LDT + 4 * frg) = qo4;
-      *(f4 *)(sQp + fk * L::LDT + 4 * frg) = qp4;
       *(f4 *)(sBloc + fk * L::LDT + 4 * frg) = bl4;
-      publish_decays<NB, L::LDRG>(sSc, sG, sGp, sRg, f, f.blast - f.pre - f.tot, frg, fk, fv);
+      publish_decays<NB, L::LDRG>(sSc, sEt, sG, sGp, f, f.blast - f.pre - f.tot, frg, fk, fv);
     }
-    if (it + 1 < N) fetch_factors(n - 1);
+    fetch_factors(max(n - 1, 0));  // unconditional, see the dq sweep
     __syncthreads();
 
     // ---- slabs: dk_inter partials (dS after the chunk), then the dS update
-    frag_t<T> bh_[NSC], bl_[NSC];
+    frag_t<T> bh_[NST], bl_[NST];
 #pragma unroll
-    for (int sc = 0; sc < NSC; ++sc) {
-      bh_[sc] = ld_row<T>(sBh, L::LDTB, 16 * kb, 32 * sc);
-      if constexpr (SPLIT) bl_[sc] = ld_row<T>(sBl, L::LDTB, 16 * kb, 32 * sc);
+    for (int st = 0; st < NST; ++st) {
+      bh_[st] = ld_row32<T>(sBh, L::LDTB, 0, 16 * st);
+      if constexpr (SPLIT) bl_[st] = ld_row32<T>(sBl, L::LDTB, 0, 16 * st);
     }
-    const float gam = sG[16 * kb + j];
-    f4 acc[NB];
+    const float gam = sG[j];
+    f16v acc[2];
 #pragma unroll
-    for (int J = 0; J < NB; ++J) acc[J] = zero4();
+    for (int e = 0; e < 16; ++e) acc[0][e] = acc[1][e] = 0.f;
 #pragma unroll
     for (int sl = 0; sl < NSL; ++sl) {
       const int q = it * NSL + sl;
-      if constexpr (!L::DB) {
-        store_slab(q);
-        fetch_slab(q + 1);
-        __syncthreads();
-      }
-      const int b = L::DB ? (q & 1) : 0;
-      const T *sV = (const T *)((const char *)sV0 + b * L::slab);
-      const T *sD = (const T *)((const char *)sD0 + b * L::slab);
-      if (sl * kVS < V) {
-        frag_t<T> shi, slo;
-        acc_split<T>(dS[sl][0], dS[sl][1], shi, slo);
+      pv.store_swz(sV, L::LDV);
+      pd.store_swz(sD, L::LDV);
+      __syncthreads();
+      fetch_slab(q + 1);
+      if (sw) {
+        // dk_inter += V[:, this wave's 32 value rows] dS^T
 #pragma unroll
-        for (int J = 0; J < NB; ++J) {
-          const frag_t<T> av = ld_row_sw<T>(sV, L::LDV, 16 * J, 32 * vq);
-          acc[J] = mma<T>(acc[J], av, shi);
-          if constexpr (SPLIT) acc[J] = mma<T>(acc[J], av, slo);
-        }
+        for (int st = 0; st < 2; ++st) {
+          frag_t<T> shi, slo;
+          acc_split32<T>(dS[sl], st, shi, slo);
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          dS[sl][h] *= gam;
-#pragma unroll
-          for (int sc = 0; sc < NSC; ++sc) {
-            const frag_t<T> ad = ld_col_perm_sw<T>(sD, L::LDV, 32 * sc, 32 * vq, h);
-            dS[sl][h] = mma<T>(dS[sl][h], ad, bh_[sc]);
-            if constexpr (SPLIT) dS[sl][h] = mma<T>(dS[sl][h], ad, bl_[sc]);
+          for (int th = 0; th < NTT; ++th) {
+            const frag_t<T> av = ld_slab_row<T>(sV, lb0, lb1, 32 * th, 32 * w + 16 * st);
+            acc[th] = mma32<T>(acc[th], av, shi);
+            if constexpr (SPLIT) acc[th] = mma32<T>(acc[th], av, slo);
           }
         }
-      }
-      if constexpr (L::DB) {
-        store_slab(q + 1);
-        fetch_slab(q + 2);
+        // dS^T <- gamma dS^T + dO^T (Q (.) Lambda)
+        dS[sl] *= gam;
+#pragma unroll
+        for (int st = 0; st < NST; ++st) {
+          const frag_t<T> ad = ld_slab_col_perm<T>(sD, lt0, lt1, 16 * st, 32 * w);
+          dS[sl] = mma32<T>(dS[sl], ad, bh_[st]);
+          if constexpr (SPLIT) dS[sl] = mma32<T>(dS[sl], ad, bl_[st]);
+        }
       }
       __syncthreads();
     }
 
     // ---- dk_inter partials, pre-scaled by exp(B_last - B at the block's end)
-#pragma unroll
-    for (int J = 0; J < NB; ++J) acc[J] *= sSc[J * kKF + 16 * kb + j];
-    if (vq >= 2) {
-#pragma unroll
-      for (int J = 0; J < NB; ++J) *(f4 *)(sRed + ((vq - 2) * kKF + 16 * kb + j) * L::LDT + 16 * J + 4 * g) = acc[J];
-    }
+    partials_publish<L>(acc, sSc, sRed, w, g, j);
     __syncthreads();
-    if (vq < 2) {
-#pragma unroll
-      for (int J = 0; J < NB; ++J) *(f4 *)(sRed + (vq * kKF + 16 * kb + j) * L::LDT + 16 * J + 4 * g) += acc[J];
-    }
+    partials_add<L>(acc, sRed, w, g, j);
     // intra-chunk term by sub-chunk blocks, for column block J: sum over I >= J
     // of dP_IJ^T y_I with y_I = (q (.) exp(Bloc)) g_IJ below the diagonal and
     // q (.) exp(Bloc - tot_J) on it (zero where the block needs pairwise decays)
     for (int t = w; t < 2 * NB; t += 8) {
-      const int J = t >> 1, kq = t & 1;
+      const int J = t >> 1, kq = t & 1, j16 = l & 15, g16 = l >> 4;
       f4 o = zero4();
 #pragma unroll
-      for (int s = 0; s < NSC; ++s) {
+      for (int s = 0; s < CP / 32; ++s) {
         if (32 * s + 31 < 16 * J) continue;
-        const int I = 2 * s + (g >> 1);
-        const float sc = I < J ? 0.f : (I >= J + 2 ? sGp[pair_idx(I, J) * kKF + 16 * kq + j] : 1.f);
-        const f8 qo = ldf_row(sQo, L::LDT, 16 * kq, 32 * s), qp = ldf_row(sQp, L::LDT, 16 * kq, 32 * s);
-        f8 bf;
+        const int I = 2 * s + (g16 >> 1);
+        const float sc = I < J ? 0.f
+                               : (I == J ? sEt[J * kKF + 16 * kq + j16]
+                                         : (I >= J + 2 ? sGp[pair_idx(I, J) * kKF + 16 * kq + j16] : 1.f));
+        f8 bf = ldf_row(sQo, L::LDT, 16 * kq, 32 * s);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) bf[i] = I == J ? qp[i] : qo[i] * sc;
+        for (int i = 0; i < 8; ++i) bf[i] *= sc;
         o = mma_split3<T>(o, ldf_row(sdP, L::LDP, 16 * J, 32 * s), bf);
       }
-      *(f4 *)(sOr + (16 * kq + j) * L::LDT + 16 * J + 4 * g) = o;
+      *(f4 *)(sOr + (16 * kq + j16) * L::LDT + 16 * J + 4 * g16) = o;
     }
     __syncthreads();
 
@@ -815,15 +869,16 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
       const int blk = frg >> 2;
       const float tot = sFt[frg * kKF + fk];
       const bool wide = fv && (-tot > kWide);
-      const f4 r0 = *(const f4 *)(sRed + fk * L::LDT + 4 * frg);
-      const f4 r1 = *(const f4 *)(sRed + (kKF + fk) * L::LDT + 4 * frg);
-      const f4 op = *(const f4 *)(sOr + fk * L::LDT + 4 * frg);
+      f4 in4 = *(const f4 *)(sOr + fk * L::LDT + 4 * frg);
+#pragma unroll
+      for (int p = 0; p < L::NP; ++p) in4 += *(const f4 *)(sRed + (p * kKF + fk) * L::LDT + 4 * frg);
       const f4 bl4 = *(const f4 *)(sBloc + fk * L::LDT + 4 * frg);
+      const auto rs_dk = make_rsrc(dko + (int64_t)t0 * K, rsrc_bytes((int64_t)(a.T - t0) * K * esz));
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = 4 * frg + i;
         const float bloc = bl4[i];
-        float dk = __expf(tot - bloc) * (r0[i] + r1[i] + op[i]);
+        float dk = __expf(tot - bloc) * in4[i];
         if (wide && row < rv) {
           // diagonal block with pairwise decays exp(B_t - B_row)
           const int tend = min(16 * blk + 16, rv);
@@ -833,7 +888,7 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
                   __expf(sBloc[fk * L::LDT + tt] - bloc);
         }
         dA[i] = qdq[i] - kv[i] * dk;
-        if (row < rv && fv) dko[(int64_t)(t0 + row) * K + kf] = cvt<T>(dk);
+        st_elem<T>(rs_dk, eoff[i], cvt<T>(dk));
       }
       float s = 0.f;
 #pragma unroll
@@ -856,21 +911,19 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
           if (p + e > frg) later += v[e];
         }
       }
+      const auto rs_dla = make_rsrc(dlao + (int64_t)t0 * K, rsrc_bytes((int64_t)(a.T - t0) * K * esz));
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = 4 * frg + i;
-        if (row < rv && fv) dlao[(int64_t)(t0 + row) * K + kf] = cvt<T>(dA[i] + later);
-      }
+      for (int i = 0; i < 4; ++i) st_elem<T>(rs_dla, eoff[i], cvt<T>(dA[i] + later));
       if (frg == 0) sCar[((it + 1) & 1) * kKF + fk] = all;
     }
-    __syncthreads();
   }
 }
 
 // ============================================================== launchers
 int ks_cp(const Shape &s) { return s.C <= 32 ? 32 : 64; }
 int ks_nsl(const Shape &s) {
-  const int n = (s.V + kVS - 1) / kVS;
+  const int vs = s.io == IO_BF16 ? 256 : 128;
+  const int n = (s.V + vs - 1) / vs;
   return n <= 1 ? 1 : (n <= 2 ? 2 : (n <= 4 ? 4 : 8));
 }
 
