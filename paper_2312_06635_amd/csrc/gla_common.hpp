@@ -130,6 +130,7 @@ __device__ __forceinline__ uint32_t rsrc_bytes(int64_t bytes) {
 }
 
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 
 // Register-staged [ROWS x COLS] tile copy, global -> LDS, for NT threads, with
 // compile-time geometry.  init() fixes each thread's byte offsets once (row

@@ -500,8 +500,7 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
     frag_t<T> bh_[NST], bl_[NST];
 #pragma unroll
     for (int st = 0; st < NST; ++st) {
-      bh_[st] = ld_row32<T>(sBh, L::LDTB, 0, 16 * st);
-      if constexpr (SPLIT) bl_[st] = ld_row32<T>(sBl, L::LDTB, 0, 16 * st);
+
     }
     const float gam = sG[j];
     f16v acc[2], accP;
@@ -514,6 +513,7 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
       pd.store_swz(sD, L::LDV);
       __syncthreads();
       fetch_slab(q + 1);
+      __builtin_amdgcn_sched_barrier(0);
       {
         // dP = dO V^T for this wave's (tile, value half)
 #pragma unroll
@@ -537,8 +537,8 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
 #pragma unroll
           for (int st = 0; st < NST; ++st) {
             const frag_t<T> av = ld_slab_col_perm<T>(sV, lt0, lt1, 16 * st, 32 * w);
-            S[sl] = mma32<T>(S[sl], av, bh_[st]);
-            if constexpr (SPLIT) S[sl] = mma32<T>(S[sl], av, bl_[st]);
+            S[sl] = mma32<T>(S[sl], av, ld_row32<T>(sBh, L::LDTB, 0, 16 * st));
+            if constexpr (SPLIT) S[sl] = mma32<T>(S[sl], av, ld_row32<T>(sBl, L::LDTB, 0, 16 * st));
           }
         }
       }
@@ -798,8 +798,7 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
     frag_t<T> bh_[NST], bl_[NST];
 #pragma unroll
     for (int st = 0; st < NST; ++st) {
-      bh_[st] = ld_row32<T>(sBh, L::LDTB, 0, 16 * st);
-      if constexpr (SPLIT) bl_[st] = ld_row32<T>(sBl, L::LDTB, 0, 16 * st);
+
     }
     const float gam = sG[j];
     f16v acc[2];
@@ -812,6 +811,7 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
       pd.store_swz(sD, L::LDV);
       __syncthreads();
       fetch_slab(q + 1);
+      __builtin_amdgcn_sched_barrier(0);
       if (sw) {
         // dk_inter += V[:, this wave's 32 value rows] dS^T
 #pragma unroll
@@ -830,8 +830,8 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
 #pragma unroll
         for (int st = 0; st < NST; ++st) {
           const frag_t<T> ad = ld_slab_col_perm<T>(sD, lt0, lt1, 16 * st, 32 * w);
-          dS[sl] = mma32<T>(dS[sl], ad, bh_[st]);
-          if constexpr (SPLIT) dS[sl] = mma32<T>(dS[sl], ad, bl_[st]);
+          dS[sl] = mma32<T>(dS[sl], ad, ld_row32<T>(sBh, L::LDTB, 0, 16 * st));
+          if constexpr (SPLIT) dS[sl] = mma32<T>(dS[sl], ad, ld_row32<T>(sBl, L::LDTB, 0, 16 * st));
         }
       }
       __syncthreads();

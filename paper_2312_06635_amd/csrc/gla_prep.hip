@@ -91,6 +91,50 @@ template <typename T, int N> __device__ __forceinline__ void stvec(T *p, const f
   *(VecN<T, N> *)p = v;
 }
 
+// FPL consecutive elements as one buffer load / store of FPL * sizeof(T)
+// bytes, kept as raw 32-bit words (out-of-range offsets read zero / drop).
+template <typename T, int FPL>
+__device__ __forceinline__ void ldraw(__amdgpu_buffer_rsrc_t rs, uint32_t off, uint32_t (&r)[(FPL * sizeof(T) + 3) / 4]) {
+  constexpr int B = FPL * sizeof(T);
+  if constexpr (B == 2) {
+    r[0] = __builtin_amdgcn_raw_buffer_load_b16(rs, off, 0, 0);
+  } else if constexpr (B == 4) {
+    r[0] = __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0);
+  } else if constexpr (B == 8) {
+    const u32x2 v = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rs, off, 0, 0));
+    r[0] = v[0];
+    r[1] = v[1];
+  } else {
+    const u32x4 v = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r[i] = v[i];
+  }
+}
+template <typename T, int FPL>
+__device__ __forceinline__ void unpack(const uint32_t (&r)[(FPL * sizeof(T) + 3) / 4], float (&o)[FPL]) {
+#pragma unroll
+  for (int i = 0; i < FPL; ++i) {
+    if constexpr (sizeof(T) == 2) o[i] = __builtin_bit_cast(float, (r[i / 2] >> (16 * (i % 2))) << 16);
+    else o[i] = __builtin_bit_cast(float, r[i]);
+  }
+}
+template <typename T, int FPL>
+__device__ __forceinline__ void straw(__amdgpu_buffer_rsrc_t rs, uint32_t off, const float (&x)[FPL]) {
+  constexpr int B = FPL * sizeof(T);
+  VecN<T, FPL> v;
+#pragma unroll
+  for (int i = 0; i < FPL; ++i) v.e[i] = cvt<T>(x[i]);
+  if constexpr (B == 2) {
+    __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, v), rs, off, 0, 0);
+  } else if constexpr (B == 4) {
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), rs, off, 0, 0);
+  } else if constexpr (B == 8) {
+    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, v), rs, off, 0, 0);
+  } else {
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), rs, off, 0, 0);
+  }
+}
+
 template <typename T, int FPL>
 __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -114,28 +158,38 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
   const bool fv = k0 < K;     // K is a multiple of 16, so all FPL are valid together
   const bool fp = k0 < Kp;    // inside the zero-padded LDS tiles
 
-  // 1. block-local cumsum of log alpha.
-  float Bloc[16][FPL], tot[FPL];
-  {
-    float c[FPL];
+  // 0. every input row of this wave's block is requested at once (buffer
+  // loads: rows past the sequence end and absent features read zero).
+  constexpr int NW = (FPL * (int)sizeof(T) + 3) / 4;
+  const int esz = sizeof(T);
+  const uint32_t bytes = rsrc_bytes((int64_t)(a.T - t0) * K * esz);
+  const auto rs_la = make_rsrc(la, bytes), rs_q = make_rsrc(q, bytes), rs_k = make_rsrc(k, bytes);
+  const uint32_t lane_off = fv ? (uint32_t)((16 * w * K + k0) * esz) : 0x80000000u;
+  const uint32_t row_step = (uint32_t)(K * esz);
+  uint32_t rla[16][NW], rq[16][NW], rk[16][NW];
 #pragma unroll
-    for (int f = 0; f < FPL; ++f) c[f] = 0.f;
+  for (int r = 0; r < 16; ++r) ldraw<T, FPL>(rs_la, lane_off + r * row_step, rla[r]);
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    ldraw<T, FPL>(rs_q, lane_off + r * row_step, rq[r]);
+    ldraw<T, FPL>(rs_k, lane_off + r * row_step, rk[r]);
+  }
+
+  // 1. block sums of log alpha.
+  float tot[FPL];
+  {
+#pragma unroll
+    for (int f = 0; f < FPL; ++f) tot[f] = 0.f;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int row = 16 * w + r;
       float x[FPL];
-      ldvec<T, FPL>(la + row * K + k0, fv && row < rv, x);
+      unpack<T, FPL>(rla[r], x);
 #pragma unroll
-      for (int f = 0; f < FPL; ++f) {
-        c[f] += x[f];
-        Bloc[r][f] = c[f];
-      }
+      for (int f = 0; f < FPL; ++f) tot[f] += x[f];
     }
 #pragma unroll
-    for (int f = 0; f < FPL; ++f) {
-      tot[f] = c[f];
-      if (fp) sTot[w * Kp + k0 + f] = c[f];
-    }
+    for (int f = 0; f < FPL; ++f)
+      if (fp) sTot[w * Kp + k0 + f] = tot[f];
   }
   __syncthreads();
 
@@ -159,7 +213,7 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
     }
   }
 
-  // 2. gated operands.
+  // 2. gated operands, from the block-local inclusive cumsum Bloc.
   bool wide = false;
   float ez[FPL], ekt[FPL];
 #pragma unroll
@@ -171,26 +225,29 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
   }
   const bool wide_blk = __any(wide);
   if (l == 0) a.wflag[((int64_t)bh * a.N + n) * 4 + w] = wide_blk ? 1 : 0;
+  const auto rs_Qt = make_rsrc(Qt, bytes), rs_Kt = make_rsrc(Kt, bytes);
+  float c[FPL];
+#pragma unroll
+  for (int f = 0; f < FPL; ++f) c[f] = 0.f;
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const int row = 16 * w + r;
-    const bool ok = fv && row < rv;
-    float qv[FPL], kv[FPL], o1[FPL], o2[FPL], o3[FPL], o4[FPL];
-    ldvec<T, FPL>(q + row * K + k0, ok, qv);
-    ldvec<T, FPL>(k + row * K + k0, ok, kv);
+    float xl[FPL], qv[FPL], kv[FPL], o1[FPL], o2[FPL], o3[FPL], o4[FPL];
+    unpack<T, FPL>(rla[r], xl);
+    unpack<T, FPL>(rq[r], qv);
+    unpack<T, FPL>(rk[r], kv);
 #pragma unroll
     for (int f = 0; f < FPL; ++f) {
-      const float qhv = qv[f] * __expf(Bloc[r][f]);           // <= |q|
-      const float ksv = kv[f] * __expf(tot[f] - Bloc[r][f]);  // <= |k|
+      c[f] += xl[f];
+      const float qhv = qv[f] * __expf(c[f]);           // <= |q|
+      const float ksv = kv[f] * __expf(tot[f] - c[f]);  // <= |k|
       o1[f] = qhv * ez[f];
       o2[f] = ksv * ekt[f];
       o3[f] = qhv;
       o4[f] = ksv;
     }
-    if (ok) {
-      stvec<T, FPL>(Qt + row * K + k0, o1);
-      stvec<T, FPL>(Kt + row * K + k0, o2);
-    }
+    straw<T, FPL>(rs_Qt, lane_off + r * row_step, o1);
+    straw<T, FPL>(rs_Kt, lane_off + r * row_step, o2);
     if (fp) {
       stvec<T, FPL>(sQh + row * ldk + k0, o3);
       stvec<T, FPL>(sKs + row * ldk + k0, o4);
