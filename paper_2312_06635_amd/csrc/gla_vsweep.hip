@@ -166,20 +166,28 @@ __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
   st1.z = st0.z;
   st1.p = st0.p;
   const int esz = sizeof(T);
+  const uint32_t goff = (int)threadIdx.x < K ? 4u * threadIdx.x : 0x80000000u;  // gamma: lanes past K read 0
   const T *Xh = (const T *)a.X + (int64_t)bh * a.T * K;
   const T *Yh = (const T *)a.Y + (int64_t)bh * a.T * K;
   const T *Zh = (const T *)a.Z + (int64_t)bh * a.T * V + v0;
   const T *Ph = (const T *)a.P + (int64_t)bh * N * C * C;
   const float *Gh = a.gam + (int64_t)bh * N * K;
   auto chunk_of = [&](int it) { return REV ? N - 1 - it : it; };
-  auto fetch = [&](Stage &S, int n) {
+  // part 0: X tile, 1: Y tile, 2: value tile, 3: P tile and gamma
+  auto fetch_part = [&](Stage &S, int n, int part) {
     const int t0 = n * C;
     const uint32_t remK = rsrc_bytes((int64_t)(a.T - t0) * K * esz);
-    S.x.load(make_rsrc(Xh + (int64_t)t0 * K, remK));
-    S.y.load(make_rsrc(Yh + (int64_t)t0 * K, remK));
-    S.z.load(make_rsrc(Zh + (int64_t)t0 * V, rsrc_bytes(((int64_t)(a.T - t0) * V - v0) * esz)));
-    S.p.load(make_rsrc(Ph + (int64_t)n * C * C, (uint32_t)(C * C * esz)));
-    S.g = (int)threadIdx.x < K ? Gh[(int64_t)n * K + threadIdx.x] : 0.f;
+    if (part == 0) S.x.load(make_rsrc(Xh + (int64_t)t0 * K, remK));
+    if (part == 1) S.y.load(make_rsrc(Yh + (int64_t)t0 * K, remK));
+    if (part == 2) S.z.load(make_rsrc(Zh + (int64_t)t0 * V, rsrc_bytes(((int64_t)(a.T - t0) * V - v0) * esz)));
+    if (part == 3) {
+      S.p.load(make_rsrc(Ph + (int64_t)n * C * C, (uint32_t)(C * C * esz)));
+      S.g = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(make_rsrc(Gh + (int64_t)n * K, (uint32_t)(K * 4)), goff, 0, 0));
+    }
+  };
+  auto fetch = [&](Stage &S, int n) {
+#pragma unroll
+    for (int part = 0; part < 4; ++part) fetch_part(S, n, part);
   };
 
   T *outh = (T *)a.out + (int64_t)bh * a.T * V;
@@ -192,19 +200,26 @@ __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
     S.p.store(sP, L::LDP);
     if ((int)threadIdx.x < KP) sG[threadIdx.x] = S.g;
     __syncthreads();
-    if (it + 2 < N) fetch(S, chunk_of(it + 2));
 
+    // output, transposed: acc[I] = R^T X^T over this wave's key features (a
+    // wave past the last value column computes zeros).  The loads of chunk
+    // it + 2 are issued a quarter at a time between these products, so the
+    // memory pipeline drains while the matrix cores work.
+    const int nf = chunk_of(min(it + 2, N - 1));
     f4 acc[NI];
 #pragma unroll
     for (int I = 0; I < NI; ++I) acc[I] = zero4();
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      const frag_t<T> ra = acc_frag<T>(R[2 * s], R[2 * s + 1]);
+#pragma unroll
+      for (int I = 0; I < NI; ++I) acc[I] = mma<T>(acc[I], ra, ld_row<T>(sX, L::LDX, 16 * I, fbase + 32 * s));
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int part = s * 4 / NS; part < (s + 1) * 4 / NS; ++part) fetch_part(S, nf, part);
+      __builtin_amdgcn_sched_barrier(0);
+    }
     if (active) {
-      // output, transposed: acc[I] = R^T X^T over this wave's key features
-#pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const frag_t<T> ra = acc_frag<T>(R[2 * s], R[2 * s + 1]);
-#pragma unroll
-        for (int I = 0; I < NI; ++I) acc[I] = mma<T>(acc[I], ra, ld_row<T>(sX, L::LDX, 16 * I, fbase + 32 * s));
-      }
       if (kh == 0) {
         // intra-chunk term: O += P V (forward) or dV += P^T dO (backward)
 #pragma unroll
