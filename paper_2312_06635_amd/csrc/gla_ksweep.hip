@@ -433,12 +433,13 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   pv.init(V, C, VS);
   pd.init(V, C, VS);
   const int NQ = N * NSL;
-  auto fetch_slab = [&](int q) {
+  // part 0: the V slab, 1: the dO slab
+  auto fetch_slab = [&](int q, int part) {
     q = min(q, NQ - 1);  // unconditional, see fetch_factors
     const int n = q / NSL, sl = q - n * NSL, t0 = n * C, c0 = sl * VS;
     const uint32_t bytes = rsrc_bytes(((int64_t)(a.T - t0) * V - c0) * esz);
-    pv.load(make_rsrc(vh + (int64_t)t0 * V + c0, bytes), V - c0);
-    pd.load(make_rsrc(dOh + (int64_t)t0 * V + c0, bytes), V - c0);
+    if (part == 0) pv.load(make_rsrc(vh + (int64_t)t0 * V + c0, bytes), V - c0);
+    else pd.load(make_rsrc(dOh + (int64_t)t0 * V + c0, bytes), V - c0);
   };
 
   T *dqo = (T *)a.dq + (int64_t)bh * a.T * K, *dqlo = (T *)a.dq_lo + (int64_t)bh * a.T * K;
@@ -453,7 +454,8 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   const int pA1 = (lb1 ^ (ph * (kRowB / 2))) + 32 * tr * kRowB, pB1 = (lb1 ^ (ph * (kRowB / 2))) + 32 * tc * kRowB;
 
   fetch_factors(0);
-  fetch_slab(0);
+  fetch_slab(0, 0);
+  fetch_slab(0, 1);
 
   for (int n = 0; n < N; ++n) {
     const int t0 = n * C, rv = min(C, a.T - t0);
@@ -512,13 +514,19 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
       pv.store_swz(sV, L::LDV);
       pd.store_swz(sD, L::LDV);
       __syncthreads();
-      fetch_slab(q + 1);
-      __builtin_amdgcn_sched_barrier(0);
       {
-        // dP = dO V^T for this wave's (tile, value half)
+        // dP = dO V^T for this wave's (tile, value half); the next slab's
+        // loads are issued in two halves between these products (pinned by
+        // scheduling barriers) so that the memory pipeline drains meanwhile
 #pragma unroll
-        for (int st = 0; st < VS / 32; ++st)
+        for (int st = 0; st < VS / 32; ++st) {
           accP = mma32<T>(accP, ld_slab_row<T>(sD, pA, pA1, 0, 16 * st), ld_slab_row<T>(sV, pB, pB1, 0, 16 * st));
+          if (st == 0 || st == VS / 64) {
+            __builtin_amdgcn_sched_barrier(0);
+            fetch_slab(q + 1, st == 0 ? 0 : 1);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+        }
         if (sw) {
           // dq_inter += dO[:, this wave's 32 value rows] S^T
 #pragma unroll
@@ -739,18 +747,19 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
   pv.init(V, C, VS);
   pd.init(V, C, VS);
   const int NQ = N * NSL;
-  auto fetch_slab = [&](int q) {
-    q = min(q, NQ - 1);  // unconditional, see fetch_factors
+  auto fetch_slab = [&](int q, int part) {  // as in the dq sweep
+    q = min(q, NQ - 1);
     const int n = N - 1 - q / NSL, sl = q % NSL, t0 = n * C, c0 = sl * VS;
     const uint32_t bytes = rsrc_bytes(((int64_t)(a.T - t0) * V - c0) * esz);
-    pv.load(make_rsrc(vh + (int64_t)t0 * V + c0, bytes), V - c0);
-    pd.load(make_rsrc(dOh + (int64_t)t0 * V + c0, bytes), V - c0);
+    if (part == 0) pv.load(make_rsrc(vh + (int64_t)t0 * V + c0, bytes), V - c0);
+    else pd.load(make_rsrc(dOh + (int64_t)t0 * V + c0, bytes), V - c0);
   };
 
   T *dko = (T *)a.dk + (int64_t)bh * a.T * K, *dlao = (T *)a.dla + (int64_t)bh * a.T * K;
 
   fetch_factors(N - 1);
-  fetch_slab(0);
+  fetch_slab(0, 0);
+  fetch_slab(0, 1);
 
   for (int it = 0; it < N; ++it) {
     const int n = N - 1 - it;
@@ -810,12 +819,12 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
       pv.store_swz(sV, L::LDV);
       pd.store_swz(sD, L::LDV);
       __syncthreads();
-      fetch_slab(q + 1);
-      __builtin_amdgcn_sched_barrier(0);
-      if (sw) {
-        // dk_inter += V[:, this wave's 32 value rows] dS^T
+      // the next slab's loads go out in two halves between the dk_inter
+      // products (every wave, so that each issues its share of the loads)
 #pragma unroll
-        for (int st = 0; st < 2; ++st) {
+      for (int st = 0; st < 2; ++st) {
+        if (sw) {
+          // dk_inter += V[:, this wave's 32 value rows] dS^T
           frag_t<T> shi, slo;
           acc_split32<T>(dS[sl], st, shi, slo);
 #pragma unroll
@@ -825,6 +834,11 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
             if constexpr (SPLIT) acc[th] = mma32<T>(acc[th], av, slo);
           }
         }
+        __builtin_amdgcn_sched_barrier(0);
+        fetch_slab(q + 1, st);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (sw) {
         // dS^T <- gamma dS^T + dO^T (Q (.) Lambda)
         dS[sl] *= gam;
 #pragma unroll
@@ -964,7 +978,10 @@ hipError_t dispatch_ks_cp(const Shape &s, const KsArgs &a, hipStream_t st) {
     case 1: return launch_ks_t<DQ, T, CP, 1>(a, st);
     case 2: return launch_ks_t<DQ, T, CP, 2>(a, st);
     case 4: return launch_ks_t<DQ, T, CP, 4>(a, st);
-    default: return launch_ks_t<DQ, T, CP, 8>(a, st);
+    default:
+      // eight slabs only arise for fp32 (d_v <= 1024 is four 256-wide bf16 slabs)
+      if constexpr (sizeof(T) == 4) return launch_ks_t<DQ, T, CP, 8>(a, st);
+      return hipErrorInvalidValue;
   }
 }
 
