@@ -859,7 +859,9 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
     // of dP_IJ^T y_I with y_I = (q (.) exp(Bloc)) g_IJ below the diagonal and
     // q (.) exp(Bloc - tot_J) on it (zero where the block needs pairwise decays)
     for (int t = w; t < 2 * NB; t += 8) {
-      const int J = t >> 1, kq = t & 1, j16 = l & 15, g16 = l >> 4;
+      // the heavier early column blocks go to waves 4..7, which have no
+      // partial to add
+      const int J = NB - 1 - (t >> 1), kq = t & 1, j16 = l & 15, g16 = l >> 4;
       f4 o = zero4();
 #pragma unroll
       for (int s = 0; s < CP / 32; ++s) {
