@@ -515,18 +515,6 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
       pd.store_swz(sD, L::LDV);
       __syncthreads();
       {
-        // dP = dO V^T for this wave's (tile, value half); the next slab's
-        // loads are issued in two halves between these products (pinned by
-        // scheduling barriers) so that the memory pipeline drains meanwhile
-#pragma unroll
-        for (int st = 0; st < VS / 32; ++st) {
-          accP = mma32<T>(accP, ld_slab_row<T>(sD, pA, pA1, 0, 16 * st), ld_slab_row<T>(sV, pB, pB1, 0, 16 * st));
-          if (st == 0 || st == VS / 64) {
-            __builtin_amdgcn_sched_barrier(0);
-            fetch_slab(q + 1, st == 0 ? 0 : 1);
-            __builtin_amdgcn_sched_barrier(0);
-          }
-        }
         if (sw) {
           // dq_inter += dO[:, this wave's 32 value rows] S^T
 #pragma unroll
@@ -540,13 +528,28 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
               if constexpr (SPLIT) acc[th] = mma32<T>(acc[th], ad, slo);
             }
           }
-          // S^T <- gamma S^T + V^T (K (.) Gamma)
           S[sl] *= gam;
+        }
+        // dP = dO V^T for this wave's (tile, value half), interleaved with the
+        // state update S^T <- gamma S^T + V^T (K (.) Gamma) so that the two
+        // independent accumulation chains hide each other's operand reads;
+        // the next slab's loads are issued in two halves between these
+        // products (pinned by scheduling barriers) so that the memory
+        // pipeline drains meanwhile
+        constexpr int UPD = (VS / 32) / NST;  // dP steps per update step
 #pragma unroll
-          for (int st = 0; st < NST; ++st) {
-            const frag_t<T> av = ld_slab_col_perm<T>(sV, lt0, lt1, 16 * st, 32 * w);
-            S[sl] = mma32<T>(S[sl], av, ld_row32<T>(sBh, L::LDTB, 0, 16 * st));
-            if constexpr (SPLIT) S[sl] = mma32<T>(S[sl], av, ld_row32<T>(sBl, L::LDTB, 0, 16 * st));
+        for (int st = 0; st < VS / 32; ++st) {
+          accP = mma32<T>(accP, ld_slab_row<T>(sD, pA, pA1, 0, 16 * st), ld_slab_row<T>(sV, pB, pB1, 0, 16 * st));
+          if (st == 0 || st == VS / 64) {
+            __builtin_amdgcn_sched_barrier(0);
+            fetch_slab(q + 1, st == 0 ? 0 : 1);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+          if (sw && (st + 1) % UPD == 0) {
+            const int u = (st + 1) / UPD - 1;
+            const frag_t<T> av = ld_slab_col_perm<T>(sV, lt0, lt1, 16 * u, 32 * w);
+            S[sl] = mma32<T>(S[sl], av, ld_row32<T>(sBh, L::LDTB, 0, 16 * u));
+            if constexpr (SPLIT) S[sl] = mma32<T>(S[sl], av, ld_row32<T>(sBl, L::LDTB, 0, 16 * u));
           }
         }
       }
