@@ -37,9 +37,12 @@ STAGES = [("prep", "fwd", 1), ("fwd_main", "fwd", 2), ("bwd_dq", "bwd", 2), ("bw
           ("bwd_dv", "bwd", 4)]
 
 
-def algorithmic(cfg):
-    """Algorithmic FLOPs and HBM bytes per launch of each stage (and totals)."""
+def algorithmic(cfg, gate=True):
+    """Algorithmic FLOPs and HBM bytes per launch of each stage (and totals);
+    gate=False is the alpha = 1 layer, which reads no gate tensor and writes no
+    gate gradient."""
     B, H, T, K, V, C = cfg["B"], cfg["H"], cfg["T"], cfg["dk"], cfg["dv"], cfg["chunk"]
+    ga = 1 if gate else 0
     s = 2 if cfg["io"] == "bf16" else 4
     n = B * H * T                       # token-heads
     g = B * H * ((T + C - 1) // C) * K * 4  # chunk decays (fp32)
@@ -47,20 +50,20 @@ def algorithmic(cfg):
     dP = n * C * 4
     st = {
         # gate factors, Q (.) Lambda, K (.) Gamma, P: reads q, k, log_alpha
-        "prep": dict(flops=n * (C + 1) * K, bytes=n * s * 3 * K + n * s * 2 * K + P + g),
+        "prep": dict(flops=n * (C + 1) * K, bytes=n * s * (2 + ga) * K + n * s * 2 * K + P + g),
         # state pass + output: reads Qt, Kt, v, P, gamma; writes o
         "fwd_main": dict(flops=n * (4 * K * V + (C + 1) * V), bytes=n * s * (2 * K + 2 * V) + P + g),
         # dq sweep: reads k, log_alpha, v, dO; writes dq and dP
-        "bwd_dq": dict(flops=n * (2 * K * V + (C + 1) * (K + V)), bytes=n * s * (3 * K + 2 * V) + dP),
+        "bwd_dq": dict(flops=n * (2 * K * V + (C + 1) * (K + V)), bytes=n * s * ((2 + ga) * K + 2 * V) + dP),
         # dk sweep: reads q, k, log_alpha, v, dO, dq, dP; writes dk, dlog_alpha
         "bwd_dk": dict(flops=n * (4 * K * V + (C + 1) * K),
-                       bytes=n * s * (6 * K + 2 * V) + dP),
+                       bytes=n * s * ((4 + 2 * ga) * K + 2 * V) + dP),
         # dv sweep: reads Qt, Kt, P, gamma, dO; writes dv
         "bwd_dv": dict(flops=n * (2 * K * V + (C + 1) * V), bytes=n * s * (2 * K + 2 * V) + P + g),
     }
     fwd = n * (4 * K * V + (C + 1) * (K + V))
     bwd = n * (8 * K * V + (C + 1) * (3 * K + 2 * V))
-    io_bytes = n * s * (9 * K + 5 * V)
+    io_bytes = n * s * ((7 + 2 * ga) * K + 5 * V)
     return st, fwd, bwd, io_bytes
 
 
@@ -148,6 +151,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="gla1p3b_T2048", choices=sorted(W.CONFIGS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-gate", action="store_true",
+                    help="the alpha = 1 (ungated) layer: log_alpha passed as NULL")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (reference for HBM traffic counters)")
     args = ap.parse_args()
@@ -166,15 +171,17 @@ def main():
     cfg = W.CONFIGS[args.workload]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    inp_cpu = W.make_inputs(cfg)
+    inp_cpu = W.make_inputs(cfg, alpha_one=args.no_gate)
     d = {k: (v.to(dev) if v is not None else None) for k, v in inp_cpu.items()}
+    if args.no_gate:
+        d["log_alpha"] = None
     B, H, T, K, V, C, c = (cfg[x] for x in ("B", "H", "T", "dk", "dv", "chunk", "subchunk"))
     dt = d["q"].dtype
     ws = torch.empty(gla.workspace_bytes(B, H, T, K, V, C, c, dt, op=1), dtype=torch.uint8, device=dev)
     o = torch.empty_like(d["v"])
     ST = torch.empty(B, H, K, V, dtype=torch.float32, device=dev) if cfg["want_state"] else None
     grads = {"dq": torch.empty_like(d["q"]), "dk": torch.empty_like(d["k"]), "dv": torch.empty_like(d["v"]),
-             "dlog_alpha": torch.empty_like(d["log_alpha"]),
+             "dlog_alpha": torch.empty_like(d["q"]) if d["log_alpha"] is not None else None,
              "dS0": torch.empty(B, H, K, V, dtype=torch.float32, device=dev) if d["S0"] is not None else None}
     stream = torch.cuda.current_stream(dev)
 
@@ -210,7 +217,7 @@ def main():
     for s in range(args.steps):
         for i, (nm, _, _) in enumerate(STAGES):
             stage_ms[nm] += evs[s][i].elapsed_time(evs[s][i + 1]) / args.steps
-    st_alg, fwd_flops, bwd_flops, io_bytes = algorithmic(cfg)
+    st_alg, fwd_flops, bwd_flops, io_bytes = algorithmic(cfg, gate=not args.no_gate)
     ms_per_step = 1e3 * elapsed / args.steps
     tokens = B * T
     value = tokens * args.steps / elapsed
@@ -228,7 +235,7 @@ def main():
         roof = {"kernel": dom, "bound": "mfma", "achieved": a["flops"] / t_dom / 1e12, "peak": peak / 1e12,
                 "unit": "TFLOP/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = measured_traffic(args.workload, dom)
+    roof["traffic"] = None if args.no_gate else measured_traffic(args.workload, dom)
     roof["avg_ms"] = stage_ms[dom]
 
     out = {
@@ -237,7 +244,8 @@ def main():
         "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": cfg["io"], "data": "synthetic",
         "config": {"workload": args.workload, "B": B, "H": H, "T": T, "d_k": K, "d_v": V, "chunk": C,
-                   "subchunk": c, "parallelism": "none (1 GPU)"},
+                   "subchunk": c, "parallelism": "none (1 GPU)",
+                   **({"gate": "none (alpha = 1, log_alpha NULL)"} if args.no_gate else {})},
         "tflops": tflops, "mfma_peak_frac": tflops * 1e12 / peak,
         "hbm_io_roofline_frac": (io_bytes / PEAK_HBM) / (elapsed / args.steps),
         "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},

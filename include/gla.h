@@ -21,6 +21,11 @@
  *       S0, S_T, dS_T, dS0                  : [B, H, d_k, d_v] (fp32 always)
  *     and 16-byte aligned.  "Nullable" pointers may be NULL: an absent S0 or
  *     dS_T means zero, an absent S_T or dS0 means "not wanted".
+ *   - log_alpha is nullable everywhere: NULL means alpha = 1 for every t and
+ *     feature, i.e. ungated linear attention (the alpha = 1 case that the
+ *     paper's FLA algorithms of Sec. 3.3 and App. A compute).  No gate tensor
+ *     is then read, and the backward's dlog_alpha may be NULL too.  A NULL
+ *     dlog_alpha always means the gate gradient is not wanted.
  *   - The caller owns every buffer; the library never allocates or frees
  *     device memory and keeps no mutable global state, so calls are
  *     re-entrant.  Outputs are overwritten, never accumulated into, and must
@@ -105,7 +110,7 @@ size_t gla_workspace_bytes(const gla_problem *prob, int op);
 
 /* Forward, chunkwise form (Sec. 4.2 / 4.3; the non-materialized state pass of
  * Sec. 3.3 and App. B, Alg. 5, with the intra-chunk part of Alg. 3).
- *   in : q, k, v, log_alpha; S0 (nullable, fp32)
+ *   in : q, k, v, log_alpha (nullable); S0 (nullable, fp32)
  *   out: o; S_T (nullable, fp32, the state after the last step)
  *   workspace: device buffer of at least gla_workspace_bytes(prob, 0) bytes;
  *   on return its contents are what GLA_FLAG_REUSE_FWD_WORKSPACE expects. */
@@ -119,7 +124,7 @@ gla_status gla_chunk_fwd(const gla_problem *prob, const void *q, const void *k, 
  *   dlog_alpha: gradient w.r.t. log_alpha, = revcumsum(q*dq - k*dk)
  *               + rowsum(S_T * dS_T) (the last term vanishes when dS_T = 0);
  *   dS0 (nullable): gradient w.r.t. S0.
- *   in : q, k, v, log_alpha, S0 (nullable), dO, dS_T (nullable)
+ *   in : q, k, v, log_alpha (nullable), S0 (nullable), dO, dS_T (nullable)
  *   workspace: at least gla_workspace_bytes(prob, 1) bytes. */
 gla_status gla_chunk_bwd(const gla_problem *prob, const void *q, const void *k, const void *v,
                          const void *log_alpha, const float *S0, const void *dO,
@@ -128,7 +133,7 @@ gla_status gla_chunk_bwd(const gla_problem *prob, const void *q, const void *k, 
 
 /* Forward in the recurrent form (Sec. 4.1, Eq. 3), one step at a time with the
  * state in fp32; no workspace.  prob->chunk and prob->subchunk are ignored.
- *   in : q, k, v, log_alpha; S0 (nullable)   out: o; S_T (nullable) */
+ *   in : q, k, v, log_alpha (nullable); S0 (nullable)   out: o; S_T (nullable) */
 gla_status gla_recurrent_fwd(const gla_problem *prob, const void *q, const void *k,
                              const void *v, const void *log_alpha, const float *S0, void *o,
                              float *S_T, void *stream);

@@ -96,7 +96,8 @@ def _check(q, k, v, la, extra=(), states=()):
     dev = q.device
     if dev.type != "cuda":
         raise ValueError("tensors must be on a HIP device")
-    for name, t, last in (("k", k, dk), ("log_alpha", la, dk), ("v", v, None)) + tuple(extra):
+    gate = (("log_alpha", la, dk),) if la is not None else ()
+    for name, t, last in (("k", k, dk),) + gate + (("v", v, None),) + tuple(extra):
         if t.device != dev or t.dtype != q.dtype or not t.is_contiguous():
             raise ValueError(f"{name} must be a contiguous {q.dtype} tensor on {dev}")
         if t.shape[:3] != (B, H, T) or (last is not None and t.shape[3] != last):
@@ -135,8 +136,10 @@ def chunk_fwd(q, k, v, log_alpha, chunk=64, subchunk=16, S0=None, output_final_s
               workspace=None, stage=0, out=None):
     """Chunkwise GLA forward.  Returns (o, S_T or None).
 
-    stage selects one kernel of the launch sequence (see GLA_STAGE_* in
-    include/gla.h); out=(o, S_T) reuses caller-provided output tensors."""
+    log_alpha=None means alpha = 1 (ungated linear attention): no gate tensor
+    is read.  stage selects one kernel of the launch sequence (see
+    GLA_STAGE_* in include/gla.h); out=(o, S_T) reuses caller-provided output
+    tensors."""
     _check(q, k, v, log_alpha, states=(("S0", S0),))
     B, H, T, dk = q.shape
     dv = v.shape[3]
@@ -159,7 +162,8 @@ def chunk_bwd(q, k, v, log_alpha, dO, chunk=64, subchunk=16, S0=None, dST=None,
               want_dS0=False, workspace=None, reuse_fwd_workspace=False, stage=0, out=None):
     """Chunkwise GLA backward for L = sum(o * dO) + sum(S_T * dS_T).
 
-    Returns dict(dq, dk, dv, dlog_alpha, dS0).  With reuse_fwd_workspace the
+    Returns dict(dq, dk, dv, dlog_alpha, dS0); dlog_alpha is None when
+    log_alpha is None (alpha = 1, no gate gradient).  With reuse_fwd_workspace the
     given workspace must still hold what chunk_fwd left for the same inputs.
     stage and out as in chunk_fwd (out is a dict shaped like the result)."""
     _check(q, k, v, log_alpha, extra=(("dO", dO, v.shape[3]),), states=(("S0", S0), ("dST", dST)))
@@ -175,7 +179,7 @@ def chunk_bwd(q, k, v, log_alpha, dO, chunk=64, subchunk=16, S0=None, dST=None,
         dq = torch.empty_like(q)
         dkk = torch.empty_like(k)
         dvv = torch.empty_like(v)
-        dla = torch.empty_like(log_alpha)
+        dla = torch.empty_like(log_alpha) if log_alpha is not None else None
         dS0 = torch.empty(B, H, dk, dv, dtype=torch.float32, device=q.device) if want_dS0 else None
     ws = _workspace(p, 1, q.device, workspace)
     st = lib().gla_chunk_bwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(S0),
@@ -188,7 +192,8 @@ def chunk_bwd(q, k, v, log_alpha, dO, chunk=64, subchunk=16, S0=None, dST=None,
 
 
 def recurrent_fwd(q, k, v, log_alpha, S0=None, output_final_state=False):
-    """Step-by-step recurrent forward (Eq. 3).  Returns (o, S_T or None)."""
+    """Step-by-step recurrent forward (Eq. 3).  Returns (o, S_T or None);
+    log_alpha=None means alpha = 1."""
     _check(q, k, v, log_alpha, states=(("S0", S0),))
     B, H, T, dk = q.shape
     dv = v.shape[3]

@@ -118,7 +118,7 @@ GLA_EXPORT gla_status gla_chunk_fwd(const gla_problem *prob, const void *q, cons
   const unsigned stage = (prob->flags & GLA_STAGE_MASK) >> GLA_STAGE_SHIFT;
   if (stage > 2) return GLA_ERR_SHAPE;
   const bool any = (int64_t)s.BH * s.T > 0;
-  if (any && (!q || !k || !v || !log_alpha || !o)) return GLA_ERR_NULL;
+  if (any && (!q || !k || !v || !o)) return GLA_ERR_NULL;
   const size_t need = layout(s, 0, nullptr, nullptr);
   if (any && (!workspace || workspace_bytes < need)) return GLA_ERR_WORKSPACE;
   hipStream_t hs = (hipStream_t)stream;
@@ -145,8 +145,7 @@ GLA_EXPORT gla_status gla_chunk_bwd(const gla_problem *prob, const void *q, cons
   const unsigned stage = (prob->flags & GLA_STAGE_MASK) >> GLA_STAGE_SHIFT;
   if (stage > 4) return GLA_ERR_SHAPE;
   const bool any = (int64_t)s.BH * s.T > 0;
-  if (any && (!q || !k || !v || !log_alpha || !dO || !dq || !dk || !dv || !dlog_alpha))
-    return GLA_ERR_NULL;
+  if (any && (!q || !k || !v || !dO || !dq || !dk || !dv)) return GLA_ERR_NULL;
   const size_t need = layout(s, 1, nullptr, nullptr);
   if (any && (!workspace || workspace_bytes < need)) return GLA_ERR_WORKSPACE;
   hipStream_t hs = (hipStream_t)stream;
@@ -177,7 +176,7 @@ GLA_EXPORT gla_status gla_recurrent_fwd(const gla_problem *prob, const void *q, 
   gla_status st = make_shape(&p, s);
   if (st != GLA_OK) return st;
   const bool any = (int64_t)s.BH * s.T > 0;
-  if (any && (!q || !k || !v || !log_alpha || !o)) return GLA_ERR_NULL;
+  if (any && (!q || !k || !v || !o)) return GLA_ERR_NULL;
   hipStream_t hs = (hipStream_t)stream;
   if (s.BH == 0) return GLA_OK;
   if (s.T == 0)

@@ -37,7 +37,7 @@ __global__ void __launch_bounds__(256) recurrent_kernel(RecArgs a) {
     for (int i = tid; i < K; i += 256) {
       sq[i] = (float)q[(int64_t)t * K + i];
       sk[i] = (float)k[(int64_t)t * K + i];
-      sa[i] = __expf((float)la[(int64_t)t * K + i]);
+      sa[i] = a.la ? __expf((float)la[(int64_t)t * K + i]) : 1.f;  // no gate: alpha = 1
     }
     const float vt = colv ? (float)v[(int64_t)t * V + col] : 0.f;
     __syncthreads();

@@ -421,7 +421,8 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   auto fetch_factors = [&](int n) {
     const int t0 = n * C;
     const uint32_t bytes = rsrc_bytes((int64_t)(a.T - t0) * K * esz);
-    const auto rs_la = make_rsrc(lah + (int64_t)t0 * K, bytes);
+    // an absent gate (alpha = 1) reads as log alpha = 0 from an empty range
+    const auto rs_la = make_rsrc(a.la ? lah + (int64_t)t0 * K : kh_, a.la ? bytes : 0u);
     const auto rs_k = make_rsrc(kh_ + (int64_t)t0 * K, bytes);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -731,7 +732,8 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
   auto fetch_factors = [&](int n) {
     const int t0 = n * C;
     const uint32_t bytes = rsrc_bytes((int64_t)(a.T - t0) * K * esz);
-    const auto rs_la = make_rsrc(lah + (int64_t)t0 * K, bytes);
+    // an absent gate (alpha = 1) reads as log alpha = 0 from an empty range
+    const auto rs_la = make_rsrc(a.la ? lah + (int64_t)t0 * K : kh_, a.la ? bytes : 0u);
     const auto rs_q = make_rsrc(qh_ + (int64_t)t0 * K, bytes);
     const auto rs_k = make_rsrc(kh_ + (int64_t)t0 * K, bytes);
     const auto rs_dq = make_rsrc(dqh + (int64_t)t0 * K, bytes);
@@ -930,7 +932,8 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
           if (p + e > frg) later += v[e];
         }
       }
-      const auto rs_dla = make_rsrc(dlao + (int64_t)t0 * K, rsrc_bytes((int64_t)(a.T - t0) * K * esz));
+      // an absent gate gradient is dropped through an empty range
+      const auto rs_dla = make_rsrc(a.dla ? dlao + (int64_t)t0 * K : dko, a.dla ? rsrc_bytes((int64_t)(a.T - t0) * K * esz) : 0u);
 #pragma unroll
       for (int i = 0; i < 4; ++i) st_elem<T>(rs_dla, eoff[i], cvt<T>(dA[i] + later));
       if (frg == 0) sCar[((it + 1) & 1) * kKF + fk] = all;

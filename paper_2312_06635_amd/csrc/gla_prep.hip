@@ -163,7 +163,8 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
   constexpr int NW = (FPL * (int)sizeof(T) + 3) / 4;
   const int esz = sizeof(T);
   const uint32_t bytes = rsrc_bytes((int64_t)(a.T - t0) * K * esz);
-  const auto rs_la = make_rsrc(la, bytes), rs_q = make_rsrc(q, bytes), rs_k = make_rsrc(k, bytes);
+  // an absent gate (alpha = 1) reads as log alpha = 0 from an empty range
+  const auto rs_la = make_rsrc(a.la ? la : q, a.la ? bytes : 0u), rs_q = make_rsrc(q, bytes), rs_k = make_rsrc(k, bytes);
   const uint32_t lane_off = fv ? (uint32_t)((16 * w * K + k0) * esz) : 0x80000000u;
   const uint32_t row_step = (uint32_t)(K * esz);
   uint32_t rla[16][NW], rq[16][NW], rk[16][NW];
@@ -312,7 +313,7 @@ template <typename T, int FPL>
 __global__ void __launch_bounds__(256) prep_wide_kernel(PrepArgs a) {
   const int n = blockIdx.x, bh = blockIdx.y;
   const int w = wave_id(), l = lane_id();
-  if (!a.wflag[((int64_t)bh * a.N + n) * 4 + w]) return;
+  if (!a.la || !a.wflag[((int64_t)bh * a.N + n) * 4 + w]) return;  // no gate: no wide block
   const int C = a.C, K = a.K;
   const int t0 = n * C, rv = min(C, a.T - t0), d0 = 16 * w;
   const int64_t base = ((int64_t)bh * a.T + t0) * K;

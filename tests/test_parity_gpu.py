@@ -164,6 +164,36 @@ def test_recurrent_forward(io):
     assert e1 <= TOL[io] and e2 <= TOL[io]
 
 
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_absent_gate_is_alpha_one(io):
+    """log_alpha = NULL is the ungated layer (alpha = 1, the case the FLA
+    algorithms of Sec. 3.3 compute): no gate tensor is read and no gate
+    gradient written, the results are bit-identical to an all-zero gate tensor
+    and at parity with the oracle's alpha = 1 recurrence."""
+    g = gla()
+    cfg = small_case("nogate_" + io, io, 1, 2, 150, 64, 128, 64, 16, 26, s0_std=0.1)
+    inp = W.make_inputs(cfg, alpha_one=True, dST_std=0.1)
+    assert float(inp["log_alpha"].abs().max()) == 0.0
+    o, ST, gr = run_gpu(inp, 64, 16, want_state=True)
+    d = to_dev(inp)
+    ws = torch.empty(g.workspace_bytes(1, 2, 150, 64, 128, 64, 16, d["q"].dtype, op=1),
+                     dtype=torch.uint8, device="cuda")
+    o2, ST2 = g.chunk_fwd(d["q"], d["k"], d["v"], None, 64, 16, S0=d["S0"], output_final_state=True,
+                          workspace=ws)
+    gr2 = g.chunk_bwd(d["q"], d["k"], d["v"], None, d["dO"], 64, 16, S0=d["S0"], dST=d["dST"],
+                      want_dS0=True, workspace=ws, reuse_fwd_workspace=True)
+    r1, R1 = g.recurrent_fwd(d["q"], d["k"], d["v"], d["log_alpha"], S0=d["S0"], output_final_state=True)
+    r2, R2 = g.recurrent_fwd(d["q"], d["k"], d["v"], None, S0=d["S0"], output_final_state=True)
+    torch.cuda.synchronize()
+    assert gr2["dlog_alpha"] is None
+    assert torch.equal(o, o2) and torch.equal(ST, ST2), "forward"
+    assert torch.equal(r1, r2) and torch.equal(R1, R2), "recurrent"
+    for name in ("dq", "dk", "dv", "dS0"):
+        assert torch.equal(gr[name], gr2[name]), name
+    gr2["dlog_alpha"] = gr["dlog_alpha"]
+    compare(inp, o2, ST2, gr2, [0, 1], io, cfg["name"])
+
+
 def test_empty_sequence_and_batch():
     g = gla()
     for T in (0,):
