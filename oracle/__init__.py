@@ -112,3 +112,20 @@ def bwd(q, k, v, log_alpha, dO, S0=None, dST=None, nthreads=None, ckpt=64):
     if rc != 0:
         raise RuntimeError(f"gla_oracle_bwd failed ({rc})")
     return {"dq": dq, "dk": dk, "dv": dv, "dlog_alpha": dla, "dS0": dS0}
+
+
+def gate_log_alpha(z, tau):
+    """log alpha of the GLA gate from its pre-activation z (paper, Sec. 4.4 and
+    Table 1): alpha = sigmoid(z)^(1/tau), so log alpha = logsigmoid(z) / tau.
+    logsigmoid(z) = -log(1 + exp(-z)) is evaluated as min(z, 0) -
+    log1p(exp(-|z|)), which never overflows."""
+    z = _as_f64(z)
+    return (np.minimum(z, 0.0) - np.log1p(np.exp(-np.abs(z)))) / tau
+
+
+def gate_grad(z, tau, dlog_alpha):
+    """Chain rule through gate_log_alpha: d logsigmoid(z) / dz = sigmoid(-z),
+    so dL/dz = dL/dlog_alpha * sigmoid(-z) / tau, with sigmoid(-z) =
+    (1 - tanh(z / 2)) / 2."""
+    z = _as_f64(z)
+    return _as_f64(dlog_alpha) * (0.5 * (1.0 - np.tanh(0.5 * z))) / tau

@@ -255,3 +255,62 @@ def test_empty_sequence():
     assert o.shape == (0, 2) and np.array_equal(ST, S0)
     g = oracle.bwd(q, q, v, q, v, S0=S0, dST=np.full((3, 2), 2.0))
     assert np.array_equal(g["dS0"], np.full((3, 2), 2.0))
+
+
+# ---------------------------------------------------------------- gate epilogue
+
+TAU = 16.0  # the temperature the paper fixes for the gate (Sec. 4.4)
+
+
+def test_gate_epilogue_closed_forms():
+    # logsigmoid(0) = -log 2; logsigmoid(z) - logsigmoid(-z) = z exactly
+    assert abs(oracle.gate_log_alpha(np.array([0.0]), TAU)[0] + np.log(2.0) / TAU) < 1e-16
+    z = np.linspace(-60.0, 60.0, 1201)
+    d = oracle.gate_log_alpha(z, 1.0) - oracle.gate_log_alpha(-z, 1.0)
+    assert np.abs(d - z).max() < 1e-12
+    # alpha = sigmoid(z)^(1/tau) where the direct formula is safe
+    zm = np.linspace(-20.0, 20.0, 401)
+    alpha = (1.0 / (1.0 + np.exp(-zm))) ** (1.0 / TAU)
+    assert rel(np.exp(oracle.gate_log_alpha(zm, TAU)), alpha) < 1e-14
+    # tails: log alpha -> -exp(-z)/tau for large z and -> z/tau for very negative z
+    big = np.array([30.0, 40.0, 50.0])
+    assert rel(oracle.gate_log_alpha(big, TAU), -np.exp(-big) / TAU) < 1e-10
+    neg = np.array([-40.0, -50.0])
+    assert rel(oracle.gate_log_alpha(neg, TAU), neg / TAU) < 1e-15
+    assert np.all(oracle.gate_log_alpha(z, TAU) <= 0.0)
+
+
+def test_gate_gradient_matches_central_finite_differences():
+    z = np.linspace(-12.0, 12.0, 97)
+    g = np.linspace(-1.0, 2.0, 97)
+    h = 1e-5
+    fd = g * (oracle.gate_log_alpha(z + h, TAU) - oracle.gate_log_alpha(z - h, TAU)) / (2 * h)
+    assert rel(oracle.gate_grad(z, TAU, g), fd) < 1e-9
+    # sigmoid(-z) limits: 1/2 at 0, -> 1 and -> 0 in the tails
+    assert abs(oracle.gate_grad(np.array([0.0]), 1.0, np.array([1.0]))[0] - 0.5) < 1e-16
+    assert abs(oracle.gate_grad(np.array([-60.0]), 1.0, np.array([1.0]))[0] - 1.0) < 1e-15
+    assert oracle.gate_grad(np.array([60.0]), 1.0, np.array([1.0]))[0] < 1e-25
+
+
+def test_gate_preactivation_gradient_through_the_layer():
+    """dL/dz of the layer fed through the gate epilogue equals central finite
+    differences in z of the loss computed by the forward recurrence."""
+    rng = np.random.default_rng(31)
+    T, K, V = 5, 3, 2
+    q = rng.standard_normal((T, K))
+    k = rng.standard_normal((T, K)) / np.sqrt(K)
+    v = rng.standard_normal((T, V))
+    z = rng.standard_normal((T, K)) * 2.0 + 3.0
+    dO = rng.standard_normal((T, V))
+    la = oracle.gate_log_alpha(z, TAU)
+    g = oracle.bwd(q, k, v, la, dO, nthreads=1, ckpt=4)
+    dz = oracle.gate_grad(z, TAU, g["dlog_alpha"])
+    h = 1e-5
+    fd = np.zeros_like(z)
+    for idx in np.ndindex(z.shape):
+        zp = z.copy(); zp[idx] += h
+        zm = z.copy(); zm[idx] -= h
+        lp = float((oracle.fwd(q, k, v, oracle.gate_log_alpha(zp, TAU), want_state=False, nthreads=1)[0] * dO).sum())
+        lm = float((oracle.fwd(q, k, v, oracle.gate_log_alpha(zm, TAU), want_state=False, nthreads=1)[0] * dO).sum())
+        fd[idx] = (lp - lm) / (2 * h)
+    assert rel(dz, fd) < 1e-7
