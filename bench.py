@@ -153,6 +153,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gate", action="store_true",
                     help="the alpha = 1 (ungated) layer: log_alpha passed as NULL")
+    ap.add_argument("--gate-tau", type=float, default=0.0,
+                    help="> 0: pass the gate pre-activation z (alpha = sigmoid(z)^(1/tau)) instead of log alpha")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (reference for HBM traffic counters)")
     args = ap.parse_args()
@@ -175,6 +177,12 @@ def main():
     d = {k: (v.to(dev) if v is not None else None) for k, v in inp_cpu.items()}
     if args.no_gate:
         d["log_alpha"] = None
+    elif args.gate_tau > 0:
+        # gate pre-activations; log alpha = logsigmoid(z) / tau is formed in the kernels
+        gz = torch.Generator().manual_seed(cfg["seed"] + 7)
+        z = torch.randn(inp_cpu["log_alpha"].shape, generator=gz) * 2.0 + 1.0
+        d["log_alpha"] = z.to(dtype=d["q"].dtype, device=dev)
+        inp_cpu["log_alpha"] = torch.nn.functional.logsigmoid(z.double()).div(args.gate_tau).to(inp_cpu["q"].dtype)
     B, H, T, K, V, C, c = (cfg[x] for x in ("B", "H", "T", "dk", "dv", "chunk", "subchunk"))
     dt = d["q"].dtype
     ws = torch.empty(gla.workspace_bytes(B, H, T, K, V, C, c, dt, op=1), dtype=torch.uint8, device=dev)
@@ -188,10 +196,11 @@ def main():
     def launch(stage_name, which, stage):
         if which == "fwd":
             gla.chunk_fwd(d["q"], d["k"], d["v"], d["log_alpha"], C, c, S0=d["S0"], workspace=ws,
-                          stage=stage, out=(o, ST))
+                          stage=stage, out=(o, ST), gate_tau=args.gate_tau)
         else:
             gla.chunk_bwd(d["q"], d["k"], d["v"], d["log_alpha"], d["dO"], C, c, S0=d["S0"], dST=d["dST"],
-                          workspace=ws, reuse_fwd_workspace=True, stage=stage, out=grads)
+                          workspace=ws, reuse_fwd_workspace=True, stage=stage, out=grads,
+                          gate_tau=args.gate_tau)
 
     def step(events=None):
         if events is not None:
@@ -235,7 +244,7 @@ def main():
         roof = {"kernel": dom, "bound": "mfma", "achieved": a["flops"] / t_dom / 1e12, "peak": peak / 1e12,
                 "unit": "TFLOP/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None if args.no_gate else measured_traffic(args.workload, dom)
+    roof["traffic"] = None if (args.no_gate or args.gate_tau > 0) else measured_traffic(args.workload, dom)
     roof["avg_ms"] = stage_ms[dom]
 
     out = {
@@ -245,7 +254,9 @@ def main():
         "dtype": cfg["io"], "data": "synthetic",
         "config": {"workload": args.workload, "B": B, "H": H, "T": T, "d_k": K, "d_v": V, "chunk": C,
                    "subchunk": c, "parallelism": "none (1 GPU)",
-                   **({"gate": "none (alpha = 1, log_alpha NULL)"} if args.no_gate else {})},
+                   **({"gate": "none (alpha = 1, log_alpha NULL)"} if args.no_gate else {}),
+                   **({"gate": f"pre-activation z, alpha = sigmoid(z)^(1/{args.gate_tau:g})"}
+                      if args.gate_tau > 0 else {})},
         "tflops": tflops, "mfma_peak_frac": tflops * 1e12 / peak,
         "hbm_io_roofline_frac": (io_bytes / PEAK_HBM) / (elapsed / args.steps),
         "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},

@@ -100,6 +100,13 @@ typedef struct {
   int32_t subchunk;  /* sub-chunk length c of the secondary tiling (Sec. 4.3)  */
   int32_t io;        /* gla_dtype of every non-state tensor                    */
   uint32_t flags;    /* GLA_FLAG_* bits                                        */
+  float gate_tau;    /* 0: the log_alpha argument holds log alpha.  tau > 0:
+                      * it holds the gate pre-activation z of the GLA gate
+                      * alpha = sigmoid(z)^(1/tau) (Sec. 4.4; the paper uses
+                      * tau = 16), applied on the fly wherever log alpha is
+                      * read, and the backward's dlog_alpha output receives
+                      * dL/dz = dL/dlog_alpha * sigmoid(-z) / tau.  Negative,
+                      * infinite or NaN values return GLA_ERR_SHAPE.         */
 } gla_problem;
 
 /* Bytes of device workspace gla_chunk_fwd (op = 0) or gla_chunk_bwd (op = 1)

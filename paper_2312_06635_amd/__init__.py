@@ -36,7 +36,8 @@ STAGE_SHIFT = 8
 class GlaProblem(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int32), ("H", ctypes.c_int32), ("T", ctypes.c_int32),
                 ("dk", ctypes.c_int32), ("dv", ctypes.c_int32), ("chunk", ctypes.c_int32),
-                ("subchunk", ctypes.c_int32), ("io", ctypes.c_int32), ("flags", ctypes.c_uint32)]
+                ("subchunk", ctypes.c_int32), ("io", ctypes.c_int32), ("flags", ctypes.c_uint32),
+                ("gate_tau", ctypes.c_float)]
 
 
 class GlaError(RuntimeError):
@@ -80,9 +81,9 @@ def _io_code(dt: torch.dtype) -> int:
     raise TypeError(f"unsupported dtype {dt}; use torch.bfloat16 or torch.float32")
 
 
-def _problem(q, v, chunk, subchunk, flags=0) -> GlaProblem:
+def _problem(q, v, chunk, subchunk, flags=0, gate_tau=0.0) -> GlaProblem:
     B, H, T, dk = q.shape
-    return GlaProblem(B, H, T, dk, v.shape[-1], chunk, subchunk, _io_code(q.dtype), flags)
+    return GlaProblem(B, H, T, dk, v.shape[-1], chunk, subchunk, _io_code(q.dtype), flags, float(gate_tau))
 
 
 def _ptr(t):
@@ -133,17 +134,18 @@ def _workspace(p, op, dev, workspace):
 
 
 def chunk_fwd(q, k, v, log_alpha, chunk=64, subchunk=16, S0=None, output_final_state=False,
-              workspace=None, stage=0, out=None):
+              workspace=None, stage=0, out=None, gate_tau=0.0):
     """Chunkwise GLA forward.  Returns (o, S_T or None).
 
     log_alpha=None means alpha = 1 (ungated linear attention): no gate tensor
-    is read.  stage selects one kernel of the launch sequence (see
+    is read.  gate_tau > 0 means log_alpha holds the gate pre-activation z of
+    alpha = sigmoid(z)^(1/gate_tau) (the GLA gate).  stage selects one kernel of the launch sequence (see
     GLA_STAGE_* in include/gla.h); out=(o, S_T) reuses caller-provided output
     tensors."""
     _check(q, k, v, log_alpha, states=(("S0", S0),))
     B, H, T, dk = q.shape
     dv = v.shape[3]
-    p = _problem(q, v, chunk, subchunk, stage << STAGE_SHIFT)
+    p = _problem(q, v, chunk, subchunk, stage << STAGE_SHIFT, gate_tau)
     if out is not None:
         o, ST = out
     else:
@@ -159,18 +161,20 @@ def chunk_fwd(q, k, v, log_alpha, chunk=64, subchunk=16, S0=None, output_final_s
 
 
 def chunk_bwd(q, k, v, log_alpha, dO, chunk=64, subchunk=16, S0=None, dST=None,
-              want_dS0=False, workspace=None, reuse_fwd_workspace=False, stage=0, out=None):
+              want_dS0=False, workspace=None, reuse_fwd_workspace=False, stage=0, out=None,
+              gate_tau=0.0):
     """Chunkwise GLA backward for L = sum(o * dO) + sum(S_T * dS_T).
 
     Returns dict(dq, dk, dv, dlog_alpha, dS0); dlog_alpha is None when
-    log_alpha is None (alpha = 1, no gate gradient).  With reuse_fwd_workspace the
+    log_alpha is None (alpha = 1, no gate gradient), and dL/dz when gate_tau > 0
+    (log_alpha then holds the gate pre-activation z).  With reuse_fwd_workspace the
     given workspace must still hold what chunk_fwd left for the same inputs.
     stage and out as in chunk_fwd (out is a dict shaped like the result)."""
     _check(q, k, v, log_alpha, extra=(("dO", dO, v.shape[3]),), states=(("S0", S0), ("dST", dST)))
     B, H, T, dk = q.shape
     dv = v.shape[3]
     flags = (FLAG_REUSE_FWD_WORKSPACE if reuse_fwd_workspace else 0) | (stage << STAGE_SHIFT)
-    p = _problem(q, v, chunk, subchunk, flags)
+    p = _problem(q, v, chunk, subchunk, flags, gate_tau)
     if reuse_fwd_workspace and workspace is None:
         raise ValueError("reuse_fwd_workspace needs the workspace the forward used")
     if out is not None:
@@ -191,13 +195,13 @@ def chunk_bwd(q, k, v, log_alpha, dO, chunk=64, subchunk=16, S0=None, dST=None,
     return {"dq": dq, "dk": dkk, "dv": dvv, "dlog_alpha": dla, "dS0": dS0}
 
 
-def recurrent_fwd(q, k, v, log_alpha, S0=None, output_final_state=False):
+def recurrent_fwd(q, k, v, log_alpha, S0=None, output_final_state=False, gate_tau=0.0):
     """Step-by-step recurrent forward (Eq. 3).  Returns (o, S_T or None);
     log_alpha=None means alpha = 1."""
     _check(q, k, v, log_alpha, states=(("S0", S0),))
     B, H, T, dk = q.shape
     dv = v.shape[3]
-    p = _problem(q, v, 16, 16)
+    p = _problem(q, v, 16, 16, 0, gate_tau)
     o = torch.empty_like(v)
     ST = torch.empty(B, H, dk, dv, dtype=torch.float32, device=q.device) if output_final_state else None
     st = lib().gla_recurrent_fwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha),

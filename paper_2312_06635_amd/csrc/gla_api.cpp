@@ -38,6 +38,9 @@ gla_status make_shape(const gla_problem *p, Shape &s) {
   s.c = p->subchunk;
   s.N = (p->T + p->chunk - 1) / p->chunk;
   s.io = p->io == GLA_BF16 ? gla::IO_BF16 : gla::IO_F32;
+  // gate_tau: 0 (the gate argument is log alpha) or a finite tau > 0
+  if (!(p->gate_tau == 0.f || (p->gate_tau > 0.f && p->gate_tau < 3.0e38f))) return GLA_ERR_SHAPE;
+  s.inv_tau = p->gate_tau == 0.f ? 0.f : 1.f / p->gate_tau;
   if (s.N > 65535) return GLA_ERR_UNSUPPORTED;
   // one head's rows of any tensor must span less than 2 GiB (32-bit buffer offsets)
   const int64_t wmax = p->dk > p->dv ? p->dk : p->dv;

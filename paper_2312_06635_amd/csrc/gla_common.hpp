@@ -62,6 +62,23 @@ template <> __device__ __forceinline__ bf16 cvt<bf16>(float x) { return (bf16)x;
 
 __device__ __forceinline__ f4 zero4() { return f4{0.f, 0.f, 0.f, 0.f}; }
 
+// log alpha from the gate argument g: g itself when inv_tau == 0, else the
+// GLA gate epilogue alpha = sigmoid(g)^(1/tau) of Sec. 4.4, i.e. log alpha =
+// logsigmoid(g) / tau with logsigmoid(g) = min(g, 0) - log1p(e), e =
+// exp(-|g|) in (0, 1]: log1p(e) is log(1 + e), or e (1 - e / 2) below 1e-3,
+// where 1 + e would lose e's low bits (absolute error < 1e-9 either way).
+// Elements outside the sequence (ok == false) contribute log alpha = 0.
+__device__ __forceinline__ float gate_la(float g, float inv_tau, bool ok) {
+  if (inv_tau == 0.f) return g;
+  const float e = __expf(-fabsf(g));
+  const float l1p = e < 1e-3f ? e * (1.f - 0.5f * e) : __logf(1.f + e);
+  return ok ? (fminf(g, 0.f) - l1p) * inv_tau : 0.f;
+}
+// d log alpha / d g: 1, or sigmoid(-g) / tau for the gate epilogue.
+__device__ __forceinline__ float gate_dla_dg(float g, float inv_tau) {
+  return inv_tau == 0.f ? 1.f : inv_tau / (1.f + __expf(g));
+}
+
 // ---------------------------------------------------------------- fragments
 // All loaders read LDS tiles stored row-major with leading dimension `ld`
 // (in elements).

@@ -15,6 +15,7 @@ struct RecArgs {
   void *o;
   float *ST;
   int T, K, V;
+  float inv_tau;  // gate epilogue (0: la holds log alpha)
 };
 
 template <typename T>
@@ -37,7 +38,7 @@ __global__ void __launch_bounds__(256) recurrent_kernel(RecArgs a) {
     for (int i = tid; i < K; i += 256) {
       sq[i] = (float)q[(int64_t)t * K + i];
       sk[i] = (float)k[(int64_t)t * K + i];
-      sa[i] = a.la ? __expf((float)la[(int64_t)t * K + i]) : 1.f;  // no gate: alpha = 1
+      sa[i] = a.la ? __expf(gate_la((float)la[(int64_t)t * K + i], a.inv_tau, true)) : 1.f;  // no gate: alpha = 1
     }
     const float vt = colv ? (float)v[(int64_t)t * V + col] : 0.f;
     __syncthreads();
@@ -65,7 +66,7 @@ __global__ void __launch_bounds__(256) recurrent_kernel(RecArgs a) {
 
 hipError_t launch_recurrent(const Shape &s, const void *q, const void *k, const void *v,
                             const void *la, const float *S0, void *o, float *ST, hipStream_t st) {
-  RecArgs a{q, k, v, la, S0, o, ST, s.T, s.K, s.V};
+  RecArgs a{q, k, v, la, S0, o, ST, s.T, s.K, s.V, s.inv_tau};
   dim3 grid((s.V + 63) / 64, s.BH);
   if (s.io == IO_BF16)
     hipLaunchKernelGGL(recurrent_kernel<bf16>, grid, dim3(256), 0, st, a);

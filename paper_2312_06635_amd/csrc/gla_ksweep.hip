@@ -55,6 +55,7 @@ struct KsArgs {
   void *dq, *dq_lo, *dk, *dla;
   float *dP, *cST;
   int BH, T, K, V, C, N, KT;
+  float inv_tau;  // gate epilogue (0: la holds log alpha)
 };
 
 template <typename T, int CP> struct KsLayout {
@@ -365,7 +366,7 @@ __device__ __forceinline__ void partials_add(const f16v (&acc)[2], float *sRed, 
 }
 
 // ============================================================== dq sweep
-template <typename T, int CP, int NSL>
+template <typename T, int CP, int NSL, bool PRE>
 __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   using L = KsLayout<T, CP>;
   constexpr int VS = L::VS, NB = L::NB, NRG = L::NRG, NST = CP / 16, NTT = CP / 32;
@@ -463,10 +464,17 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
     // ---- factors: cumsum of log alpha, gated operands
     float c[4], kv[4];
     {
+      float x[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) x[i] = elem_f<T>(fin_la[i]);
+      if constexpr (PRE) {  // gate epilogue
+#pragma unroll
+        for (int i = 0; i < 4; ++i) x[i] = gate_la(x[i], a.inv_tau, fthr && fv && 4 * frg + i < rv);
+      }
       float s = 0.f;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        s += elem_f<T>(fin_la[i]);
+        s += x[i];
         c[i] = s;
         kv[i] = elem_f<T>(fin_k[i]);
       }
@@ -671,7 +679,7 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
 }
 
 // ============================================================== dk sweep
-template <typename T, int CP, int NSL>
+template <typename T, int CP, int NSL, bool PRE>
 __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
   using L = KsLayout<T, CP>;
   constexpr int VS = L::VS, NB = L::NB, NRG = L::NRG, NST = CP / 16, NTT = CP / 32;
@@ -770,12 +778,19 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
     const int n = N - 1 - it;
     const int t0 = n * C, rv = min(C, a.T - t0);
     // ---- factors
-    float c[4], kv[4], qdq[4];
+    float c[4], kv[4], qdq[4], zc[4];  // zc: the gate argument, for the gate gradient
     {
+      float x[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) x[i] = zc[i] = elem_f<T>(fin_la[i]);
+      if constexpr (PRE) {  // gate epilogue
+#pragma unroll
+        for (int i = 0; i < 4; ++i) x[i] = gate_la(x[i], a.inv_tau, fthr && fv && 4 * frg + i < rv);
+      }
       float s = 0.f;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        s += elem_f<T>(fin_la[i]);
+        s += x[i];
         c[i] = s;
         kv[i] = elem_f<T>(fin_k[i]);
         qdq[i] = elem_f<T>(fin_q[i]) * (elem_f<T>(fin_dq[i]) + (SPLIT ? elem_f<T>(fin_dql[i]) : 0.f));
@@ -935,7 +950,13 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
       // an absent gate gradient is dropped through an empty range
       const auto rs_dla = make_rsrc(a.dla ? dlao + (int64_t)t0 * K : dko, a.dla ? rsrc_bytes((int64_t)(a.T - t0) * K * esz) : 0u);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) st_elem<T>(rs_dla, eoff[i], cvt<T>(dA[i] + later));
+      for (int i = 0; i < 4; ++i) dA[i] += later;
+      if constexpr (PRE) {  // gate epilogue: dL/dz = dL/dlog alpha * sigmoid(-z) / tau
+#pragma unroll
+        for (int i = 0; i < 4; ++i) dA[i] *= gate_dla_dg(zc[i], a.inv_tau);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) st_elem<T>(rs_dla, eoff[i], cvt<T>(dA[i]));
       if (frg == 0) sCar[((it + 1) & 1) * kKF + fk] = all;
     }
   }
@@ -960,24 +981,33 @@ size_t ks_lds(const Shape &s) {
 KsArgs ks_args(const Shape &s) {
   KsArgs a{};
   a.BH = s.BH; a.T = s.T; a.K = s.K; a.V = s.V; a.C = s.C; a.N = s.N;
+  a.inv_tau = s.inv_tau;
   a.KT = (s.K + kKF - 1) / kKF;
   return a;
 }
 
-template <bool DQ, typename T, int CP, int NSL>
-hipError_t launch_ks_t(const KsArgs &a, hipStream_t st) {
+template <bool DQ, typename T, int CP, int NSL, bool PRE>
+hipError_t launch_ks_pre(const KsArgs &a, hipStream_t st) {
   static bool attr = false;
   const size_t lds = KsLayout<T, CP>::total;
-  const void *fn = DQ ? (const void *)dq_sweep_kernel<T, CP, NSL> : (const void *)dk_sweep_kernel<T, CP, NSL>;
+  const void *fn;
+  if constexpr (DQ) fn = (const void *)dq_sweep_kernel<T, CP, NSL, PRE>;
+  else fn = (const void *)dk_sweep_kernel<T, CP, NSL, PRE>;
   if (!attr) {
     (void)hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     attr = true;
   }
   if constexpr (DQ)
-    hipLaunchKernelGGL((dq_sweep_kernel<T, CP, NSL>), dim3(a.BH * a.KT), dim3(kKT), lds, st, a);
+    hipLaunchKernelGGL((dq_sweep_kernel<T, CP, NSL, PRE>), dim3(a.BH * a.KT), dim3(kKT), lds, st, a);
   else
-    hipLaunchKernelGGL((dk_sweep_kernel<T, CP, NSL>), dim3(a.BH * a.KT), dim3(kKT), lds, st, a);
+    hipLaunchKernelGGL((dk_sweep_kernel<T, CP, NSL, PRE>), dim3(a.BH * a.KT), dim3(kKT), lds, st, a);
   return hipGetLastError();
+}
+
+// PRE: the gate argument is the pre-activation of the gate epilogue.
+template <bool DQ, typename T, int CP, int NSL>
+hipError_t launch_ks_t(const KsArgs &a, hipStream_t st) {
+  return a.inv_tau != 0.f ? launch_ks_pre<DQ, T, CP, NSL, true>(a, st) : launch_ks_pre<DQ, T, CP, NSL, false>(a, st);
 }
 
 template <bool DQ, typename T, int CP>

@@ -12,6 +12,7 @@ enum Io { IO_F32 = 0, IO_BF16 = 1 };
 struct Shape {
   int BH, T, K, V, C, c, N;
   int io;
+  float inv_tau;  // 0: the gate argument is log alpha; else 1 / tau of the gate epilogue
   int esz() const { return io == IO_BF16 ? 2 : 4; }
 };
 

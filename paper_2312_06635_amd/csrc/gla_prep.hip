@@ -35,6 +35,7 @@ struct PrepArgs {
   float *gam;
   unsigned char *wflag;  // [BH][N][4]: diagonal block needs pairwise decays
   int T, K, Kp, C, N, ldk;
+  float inv_tau;  // gate epilogue (0: la holds log alpha)
 };
 
 // Entry e of a 16x16 lower triangle (diagonal included), row-major.
@@ -135,7 +136,8 @@ __device__ __forceinline__ void straw(__amdgpu_buffer_rsrc_t rs, uint32_t off, c
   }
 }
 
-template <typename T, int FPL>
+// PRE: the gate argument is the pre-activation of the gate epilogue.
+template <typename T, int FPL, bool PRE>
 __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int n = blockIdx.x, bh = blockIdx.y;
@@ -176,8 +178,9 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
     ldraw<T, FPL>(rs_k, lane_off + r * row_step, rk[r]);
   }
 
-  // 1. block sums of log alpha.
-  float tot[FPL];
+  // 1. block sums of log alpha (with the gate epilogue, log alpha is formed
+  // once here and kept for step 2).
+  float tot[FPL], lav[PRE ? 16 : 1][FPL];
   {
 #pragma unroll
     for (int f = 0; f < FPL; ++f) tot[f] = 0.f;
@@ -186,7 +189,14 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
       float x[FPL];
       unpack<T, FPL>(rla[r], x);
 #pragma unroll
-      for (int f = 0; f < FPL; ++f) tot[f] += x[f];
+      for (int f = 0; f < FPL; ++f) {
+        if constexpr (PRE) {
+          lav[r][f] = gate_la(x[f], a.inv_tau, fv && 16 * w + r < rv);
+          tot[f] += lav[r][f];
+        } else {
+          tot[f] += x[f];
+        }
+      }
     }
 #pragma unroll
     for (int f = 0; f < FPL; ++f)
@@ -239,7 +249,8 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
     unpack<T, FPL>(rk[r], kv);
 #pragma unroll
     for (int f = 0; f < FPL; ++f) {
-      c[f] += xl[f];
+      if constexpr (PRE) c[f] += lav[r][f];
+      else c[f] += xl[f];
       const float qhv = qv[f] * __expf(c[f]);           // <= |q|
       const float ksv = kv[f] * __expf(tot[f] - c[f]);  // <= |k|
       o1[f] = qhv * ez[f];
@@ -309,7 +320,7 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
 // Diagonal blocks whose decay range is too large for the factorised form:
 // P[i][j] = sum_k q_ik k_jk exp(B_ik - B_jk), one exponential per term, fp32,
 // reduced across the lanes that own the features.
-template <typename T, int FPL>
+template <typename T, int FPL, bool PRE>
 __global__ void __launch_bounds__(256) prep_wide_kernel(PrepArgs a) {
   const int n = blockIdx.x, bh = blockIdx.y;
   const int w = wave_id(), l = lane_id();
@@ -334,7 +345,7 @@ __global__ void __launch_bounds__(256) prep_wide_kernel(PrepArgs a) {
     ldvec<T, FPL>(k + row * K + k0, ok, kv[r]);
 #pragma unroll
     for (int f = 0; f < FPL; ++f) {
-      c[f] += xl[f];
+      c[f] += PRE ? gate_la(xl[f], a.inv_tau, ok) : xl[f];
       Bv[r][f] = c[f];
     }
   }
@@ -378,20 +389,26 @@ size_t lds_prep(const Shape &s) {
   return (size_t)2 * s.C * ldk * s.esz() + (size_t)11 * Kp * sizeof(float);
 }
 
-template <typename T, int FPL>
-static hipError_t launch_prep_t(const Shape &s, const PrepArgs &a, size_t lds, hipStream_t st) {
+template <typename T, int FPL, bool PRE>
+static hipError_t launch_prep_pre(const Shape &s, const PrepArgs &a, size_t lds, hipStream_t st) {
   static bool attr = false;
   if (!attr) {
-    (void)hipFuncSetAttribute((const void *)prep_kernel<T, FPL>,
+    (void)hipFuncSetAttribute((const void *)prep_kernel<T, FPL, PRE>,
                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     attr = true;
   }
   dim3 grid(s.N, s.BH), block(64 * (s.C / 16));
-  hipLaunchKernelGGL((prep_kernel<T, FPL>), grid, block, lds, st, a);
+  hipLaunchKernelGGL((prep_kernel<T, FPL, PRE>), grid, block, lds, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((prep_wide_kernel<T, FPL>), grid, block, 0, st, a);
+  hipLaunchKernelGGL((prep_wide_kernel<T, FPL, PRE>), grid, block, 0, st, a);
   return hipGetLastError();
+}
+
+template <typename T, int FPL>
+static hipError_t launch_prep_t(const Shape &s, const PrepArgs &a, size_t lds, hipStream_t st) {
+  return a.inv_tau != 0.f ? launch_prep_pre<T, FPL, true>(s, a, lds, st)
+                          : launch_prep_pre<T, FPL, false>(s, a, lds, st);
 }
 
 hipError_t launch_prep(const Shape &s, const void *q, const void *k, const void *la,
@@ -400,6 +417,7 @@ hipError_t launch_prep(const Shape &s, const void *q, const void *k, const void 
   a.q = q; a.k = k; a.la = la;
   a.Qt = w.Qt; a.Kt = w.Kt; a.P = w.P; a.gam = w.gam; a.wflag = w.wflag;
   a.T = s.T; a.K = s.K; a.Kp = round_up(s.K, 32); a.C = s.C; a.N = s.N;
+  a.inv_tau = s.inv_tau;
   a.ldk = a.Kp + 32 / s.esz();
   const size_t lds = lds_prep(s);
   const int fpl = (s.K + 63) / 64;

@@ -194,6 +194,45 @@ def test_absent_gate_is_alpha_one(io):
     compare(inp, o2, ST2, gr2, [0, 1], io, cfg["name"])
 
 
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_gate_preactivation_epilogue(io):
+    """gate_tau > 0: the gate argument holds the pre-activation z of the GLA
+    gate alpha = sigmoid(z)^(1/tau) (Sec. 4.4, tau = 16), applied wherever a
+    kernel reads log alpha, and the backward returns dL/dz.  Compared with the
+    oracle run on log alpha = logsigmoid(z) / tau and its chain rule, on a
+    ragged sequence (the padded rows of the last chunk must not decay)."""
+    g = gla()
+    tau = 16.0
+    cfg = small_case("preact_" + io, io, 1, 2, 200, 64, 128, 64, 16, 27, s0_std=0.1)
+    inp = W.make_inputs(cfg, dST_std=0.1)
+    gen = torch.Generator().manual_seed(9)
+    inp["log_alpha"] = (torch.randn(inp["log_alpha"].shape, generator=gen) * 2.0 + 1.0).to(inp["q"].dtype)
+    d = to_dev(inp)
+    ws = torch.empty(g.workspace_bytes(1, 2, 200, 64, 128, 64, 16, d["q"].dtype, op=1),
+                     dtype=torch.uint8, device="cuda")
+    o, ST = g.chunk_fwd(d["q"], d["k"], d["v"], d["log_alpha"], 64, 16, S0=d["S0"],
+                        output_final_state=True, workspace=ws, gate_tau=tau)
+    gr = g.chunk_bwd(d["q"], d["k"], d["v"], d["log_alpha"], d["dO"], 64, 16, S0=d["S0"], dST=d["dST"],
+                     want_dS0=True, workspace=ws, reuse_fwd_workspace=True, gate_tau=tau)
+    r, R = g.recurrent_fwd(d["q"], d["k"], d["v"], d["log_alpha"], S0=d["S0"], output_final_state=True,
+                           gate_tau=tau)
+    torch.cuda.synchronize()
+    idx = [0, 1]
+    q, k, v, z, dO = (heads(inp[n], idx) for n in ("q", "k", "v", "log_alpha", "dO"))
+    S0, dST = heads(inp["S0"], idx), heads(inp["dST"], idx)
+    la = oracle.gate_log_alpha(z, tau)
+    ro, rST = oracle.fwd(q, k, v, la, S0)
+    rg = oracle.bwd(q, k, v, la, dO, S0=S0, dST=dST)
+    errs = {"o": rel(heads(o, idx), ro), "S_T": rel(heads(ST, idx), rST),
+            "rec_o": rel(heads(r, idx), ro), "rec_S_T": rel(heads(R, idx), rST),
+            "dz": rel(heads(gr["dlog_alpha"], idx), oracle.gate_grad(z, tau, rg["dlog_alpha"]))}
+    for name in ("dq", "dk", "dv", "dS0"):
+        errs[name] = rel(heads(gr[name], idx), rg[name])
+    say(cfg["name"], {k2: f"{v2:.2e}" for k2, v2 in errs.items()})
+    bad = {k2: v2 for k2, v2 in errs.items() if not v2 <= TOL[io]}
+    assert not bad, f"{cfg['name']}: {bad} > {TOL[io]}"
+
+
 def test_empty_sequence_and_batch():
     g = gla()
     for T in (0,):
