@@ -36,6 +36,8 @@
 // For bf16 the state operand, the gated update operand and the dq hand-off are
 // split into bf16 hi + lo so that the gate gradient's long reverse sum keeps
 // fp32 accuracy.
+#include <type_traits>
+
 #include "gla_common.hpp"
 #include "gla_launch.hpp"
 
@@ -370,7 +372,7 @@ template <typename T, int CP, int NSL, bool PRE>
 __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   using L = KsLayout<T, CP>;
   constexpr int VS = L::VS, NB = L::NB, NRG = L::NRG, NST = CP / 16, NTT = CP / 32;
-  constexpr int NDP = CP == 64 ? 8 : 2;  // waves whose dP unit is published
+  constexpr int NDT = CP == 64 ? 3 : 1;  // dP tiles on or below the diagonal, one per wave 0..NDT-1
   constexpr bool SPLIT = sizeof(T) == 2;
   static_assert(VS * sizeof(T) == kRowB, "slab row size");
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -446,14 +448,13 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
 
   T *dqo = (T *)a.dq + (int64_t)bh * a.T * K, *dqlo = (T *)a.dq_lo + (int64_t)bh * a.T * K;
   float *dPg = a.dP + (int64_t)bh * N * C * C;
-  // this wave's dP unit: the 32x32 tile (t rows 32 tr.., s columns 32 tc..)
-  // over value half ph of every slab; with C = 64 waves 6 and 7 take the tile
-  // above the diagonal, which the mask zeroes, so that every wave runs the
-  // same code (with C <= 32 only waves 0 and 1 publish theirs)
-  const int dtile = CP == 64 ? w >> 1 : 0, ph = w & 1;
-  const int tr = (dtile == 1 || dtile == 2) ? 1 : 0, tc = dtile >= 2 ? 1 : 0;
-  const int pA = (lb0 ^ (ph * (kRowB / 2))) + 32 * tr * kRowB, pB = (lb0 ^ (ph * (kRowB / 2))) + 32 * tc * kRowB;
-  const int pA1 = (lb1 ^ (ph * (kRowB / 2))) + 32 * tr * kRowB, pB1 = (lb1 ^ (ph * (kRowB / 2))) + 32 * tc * kRowB;
+  // waves 0..NDT-1 each accumulate one whole 32x32 dP tile (t rows 32 tr..,
+  // s columns 32 tc..: T00, T10, T11) over every slab; the tile above the
+  // diagonal is zero.  Each SIMD still issues at most 48 products per slab.
+  const bool dpw = w < NDT;
+  const int tr = (w == 1 || w == 2) ? 1 : 0, tc = w == 2 ? 1 : 0;
+  const int pA = lb0 + 32 * tr * kRowB, pB = lb0 + 32 * tc * kRowB;
+  const int pA1 = lb1 + 32 * tr * kRowB, pB1 = lb1 + 32 * tc * kRowB;
 
   fetch_factors(0);
   fetch_slab(0, 0);
@@ -539,56 +540,55 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
           }
           S[sl] *= gam;
         }
-        // dP = dO V^T for this wave's (tile, value half), interleaved with the
-        // state update S^T <- gamma S^T + V^T (K (.) Gamma) so that the two
-        // independent accumulation chains hide each other's operand reads;
-        // the next slab's loads are issued in two halves between these
+        // dP = dO V^T for this wave's tile (waves 0..NDT-1), interleaved with
+        // the state update S^T <- gamma S^T + V^T (K (.) Gamma) so that the
+        // two independent accumulation chains hide each other's operand
+        // reads; the next slab's loads are issued in two halves between these
         // products (pinned by scheduling barriers) so that the memory
         // pipeline drains meanwhile
-        constexpr int UPD = (VS / 32) / NST;  // dP steps per update step
+        constexpr int NDS = VS / 16;   // dP steps per slab
+        constexpr int UPD = NDS / NST;  // dP steps per update step
+        auto slab_products = [&](auto with_dp) {
 #pragma unroll
-        for (int st = 0; st < VS / 32; ++st) {
-          accP = mma32<T>(accP, ld_slab_row<T>(sD, pA, pA1, 0, 16 * st), ld_slab_row<T>(sV, pB, pB1, 0, 16 * st));
-          if (st == 0 || st == VS / 64) {
-            __builtin_amdgcn_sched_barrier(0);
-            fetch_slab(q + 1, st == 0 ? 0 : 1);
-            __builtin_amdgcn_sched_barrier(0);
+          for (int st = 0; st < NDS; ++st) {
+            if constexpr (decltype(with_dp)::value)
+              accP = mma32<T>(accP, ld_slab_row<T>(sD, pA, pA1, 0, 16 * st), ld_slab_row<T>(sV, pB, pB1, 0, 16 * st));
+            if (st == 0 || st == NDS / 2) {
+              __builtin_amdgcn_sched_barrier(0);
+              fetch_slab(q + 1, st == 0 ? 0 : 1);
+              __builtin_amdgcn_sched_barrier(0);
+            }
+            if (sw && (st + 1) % UPD == 0) {
+              const int u = (st + 1) / UPD - 1;
+              const frag_t<T> av = ld_slab_col_perm<T>(sV, lt0, lt1, 16 * u, 32 * w);
+              S[sl] = mma32<T>(S[sl], av, ld_row32<T>(sBh, L::LDTB, 0, 16 * u));
+              if constexpr (SPLIT) S[sl] = mma32<T>(S[sl], av, ld_row32<T>(sBl, L::LDTB, 0, 16 * u));
+            }
           }
-          if (sw && (st + 1) % UPD == 0) {
-            const int u = (st + 1) / UPD - 1;
-            const frag_t<T> av = ld_slab_col_perm<T>(sV, lt0, lt1, 16 * u, 32 * w);
-            S[sl] = mma32<T>(S[sl], av, ld_row32<T>(sBh, L::LDTB, 0, 16 * u));
-            if constexpr (SPLIT) S[sl] = mma32<T>(S[sl], av, ld_row32<T>(sBl, L::LDTB, 0, 16 * u));
-          }
-        }
-      }
-      // the second value half of each dP tile hands its partial over in LDS
-      if (sl == NSL - 1 && w < NDP && ph == 1) {
-#pragma unroll
-        for (int b = 0; b < 4; ++b)
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            sdP[(32 * tr + 8 * b + 4 * g + r) * L::LDP + 32 * tc + j] = accP[4 * b + r];
+        };
+        if (dpw) slab_products(std::true_type{});
+        else slab_products(std::false_type{});
       }
       __syncthreads();
     }
 
-    // ---- dP: sum the two halves, mask, publish (and hand it to the dk sweep transposed)
-    if (w < NDP && ph == 0) {
-      float *pd0 = sdP + (32 * tr + 4 * g) * L::LDP + 32 * tc + j;
-      float other[16];
-#pragma unroll
-      for (int e = 0; e < 16; ++e) other[e] = pd0[(8 * (e >> 2) + (e & 3)) * L::LDP];
-      const int col = 32 * tc + j;
+    // ---- dP: mask, publish (and hand it to the dk sweep transposed; the
+    // zero tile above the diagonal is written there by wave NDT)
+    if (dpw || (CP == 64 && w == NDT && kt == 0)) {
+      const bool zero_tile = !dpw;
+      const int rt = zero_tile ? 0 : tr, ct = zero_tile ? 1 : tc;
+      float *pd0 = sdP + (32 * rt + 4 * g) * L::LDP + 32 * ct + j;
+      const int col = 32 * ct + j;
       const auto rs_dp = make_rsrc(dPg + (int64_t)n * C * C, (uint32_t)(C * C * 4));
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
-        const int t4 = 32 * tr + 8 * b + 4 * g;
+        const int t4 = 32 * rt + 8 * b + 4 * g;
         f4 v4;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          v4[r] = col > t4 + r ? 0.f : accP[4 * b + r] + other[4 * b + r];
-          pd0[(8 * b + r) * L::LDP] = v4[r];
+        for (int r = 0; r < 4; ++r) v4[r] = (zero_tile || col > t4 + r) ? 0.f : accP[4 * b + r];
+        if (!zero_tile) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) pd0[(8 * b + r) * L::LDP] = v4[r];
         }
         if (kt == 0) {
           const uint32_t off = (t4 < C && col < C) ? (uint32_t)((col * C + t4) * 4) : 0x80000000u;
