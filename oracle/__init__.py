@@ -129,3 +129,54 @@ def gate_grad(z, tau, dlog_alpha):
     (1 - tanh(z / 2)) / 2."""
     z = _as_f64(z)
     return _as_f64(dlog_alpha) * (0.5 * (1.0 - np.tanh(0.5 * z))) / tau
+
+
+# ---------------------------------------------------------------- output side
+# The GLA Transformer's per-head output (paper, Sec. 4.4): LayerNorm of each
+# head's output o_t (affine parameters per channel of the concatenated heads,
+# as in the group normalisation of the cited RetNet design) gated by
+# r_t = Swish(g_t), g_t the output-gate pre-activation (its projection is a
+# plain GEMM outside this layer): y_t = r_t (.) LN(o_t).
+
+def _sigmoid(x):
+    return 0.5 * (1.0 + np.tanh(0.5 * x))
+
+
+def output_gate_fwd(o, g, w=None, b=None, eps=1e-5):
+    """o, g: [..., H, T, d_v] (per-head rows); w, b: [H, d_v] or None (1 / 0).
+    Returns (y, mean, rstd) with mean and rstd = 1/sqrt(var + eps) per row."""
+    o, g = _as_f64(o), _as_f64(g)
+    mu = o.mean(axis=-1, keepdims=True)
+    var = ((o - mu) ** 2).mean(axis=-1, keepdims=True)
+    rstd = 1.0 / np.sqrt(var + eps)
+    xh = (o - mu) * rstd
+    H = o.shape[-3]
+    wv = np.ones((H, o.shape[-1])) if w is None else _as_f64(w)
+    bv = np.zeros((H, o.shape[-1])) if b is None else _as_f64(b)
+    ln = xh * wv[:, None, :] + bv[:, None, :]
+    r = g * _sigmoid(g)
+    return r * ln, mu[..., 0], rstd[..., 0]
+
+
+def output_gate_bwd(o, g, dy, w=None, b=None, eps=1e-5):
+    """Reverse mode of output_gate_fwd for L = sum(y * dy).
+    Returns dict(do, dg, dw, db); dw, db are [H, d_v]."""
+    o, g, dy = _as_f64(o), _as_f64(g), _as_f64(dy)
+    H, V = o.shape[-3], o.shape[-1]
+    wv = np.ones((H, V)) if w is None else _as_f64(w)
+    bv = np.zeros((H, V)) if b is None else _as_f64(b)
+    mu = o.mean(axis=-1, keepdims=True)
+    var = ((o - mu) ** 2).mean(axis=-1, keepdims=True)
+    rstd = 1.0 / np.sqrt(var + eps)
+    xh = (o - mu) * rstd
+    ln = xh * wv[:, None, :] + bv[:, None, :]
+    s = _sigmoid(g)
+    r = g * s
+    dg = dy * ln * (s * (1.0 + g * (1.0 - s)))       # d swish(g)/dg = s (1 + g (1 - s))
+    dln = dy * r
+    lead = tuple(range(o.ndim - 3))
+    dw = (dln * xh).sum(axis=lead + (o.ndim - 2,))
+    db = dln.sum(axis=lead + (o.ndim - 2,))
+    dxh = dln * wv[:, None, :]
+    do = rstd * (dxh - dxh.mean(axis=-1, keepdims=True) - xh * (dxh * xh).mean(axis=-1, keepdims=True))
+    return {"do": do, "dg": dg, "dw": dw, "db": db}

@@ -314,3 +314,60 @@ def test_gate_preactivation_gradient_through_the_layer():
         lm = float((oracle.fwd(q, k, v, oracle.gate_log_alpha(zm, TAU), want_state=False, nthreads=1)[0] * dO).sum())
         fd[idx] = (lp - lm) / (2 * h)
     assert rel(dz, fd) < 1e-7
+
+
+# ---------------------------------------------------------------- output side
+
+def _og_case(rng, B=2, H=2, T=5, V=6, affine=True):
+    o = rng.standard_normal((B, H, T, V)) * 1.5 + 0.3
+    g = rng.standard_normal((B, H, T, V)) * 2.0
+    w = 1.0 + 0.2 * rng.standard_normal((H, V)) if affine else None
+    b = 0.1 * rng.standard_normal((H, V)) if affine else None
+    return o, g, w, b
+
+
+def test_output_gate_closed_forms():
+    rng = np.random.default_rng(41)
+    o, g, _, _ = _og_case(rng, affine=False)
+    # with g -> +inf the gate is the identity (swish(g)/g -> 1): y/g is the
+    # normalised row, mean 0 and variance var/(var + eps) per row
+    big = np.full_like(g, 40.0)
+    y, mu, rstd = oracle.output_gate_fwd(o, big, eps=1e-5)
+    xh = y / 40.0
+    assert np.abs(xh.mean(-1)).max() < 1e-13
+    var = o.var(-1)
+    assert np.abs((xh ** 2).mean(-1) - var / (var + 1e-5)).max() < 1e-13
+    assert rel(mu, o.mean(-1)) < 1e-15 and rel(rstd, 1.0 / np.sqrt(var + 1e-5)) < 1e-15
+    # swish(0) = 0 closes the gate; swish(-inf) -> 0
+    assert np.abs(oracle.output_gate_fwd(o, np.zeros_like(g))[0]).max() == 0.0
+    assert np.abs(oracle.output_gate_fwd(o, np.full_like(g, -60.0))[0]).max() < 1e-20
+    # LN is invariant to a shift and a positive scale of the row
+    y1 = oracle.output_gate_fwd(o, g, eps=0.0)[0]
+    y2 = oracle.output_gate_fwd(3.0 * o - 7.0, g, eps=0.0)[0]
+    assert rel(y2, y1) < 1e-12
+    # affine: w = 2, b = 1 gives r (2 xh + 1)
+    H, V = o.shape[1], o.shape[3]
+    y3 = oracle.output_gate_fwd(o, g, np.full((H, V), 2.0), np.ones((H, V)))[0]
+    r = g / (1.0 + np.exp(-g))
+    assert rel(y3, 2.0 * oracle.output_gate_fwd(o, g)[0] + r) < 1e-13
+
+
+@pytest.mark.parametrize("affine", [False, True])
+def test_output_gate_gradients_match_central_finite_differences(affine):
+    rng = np.random.default_rng(43)
+    o, g, w, b = _og_case(rng, B=1, H=2, T=3, V=5, affine=affine)
+    dy = rng.standard_normal(o.shape)
+    got = oracle.output_gate_bwd(o, g, dy, w, b)
+    L = lambda o_, g_, w_, b_: float((oracle.output_gate_fwd(o_, g_, w_, b_)[0] * dy).sum())
+    h = 1e-6
+    args = {"o": o, "g": g} | ({"w": w, "b": b} if affine else {})
+    for name, x in args.items():
+        fd = np.zeros_like(x)
+        for idx in np.ndindex(x.shape):
+            xp = x.copy(); xp[idx] += h
+            xm = x.copy(); xm[idx] -= h
+            ap = dict(args, **{name: xp}); am = dict(args, **{name: xm})
+            fd[idx] = (L(ap["o"], ap["g"], ap.get("w"), ap.get("b"))
+                       - L(am["o"], am["g"], am.get("w"), am.get("b"))) / (2 * h)
+        key = {"o": "do", "g": "dg", "w": "dw", "b": "db"}[name]
+        assert rel(got[key], fd) < 1e-7, name
