@@ -145,6 +145,29 @@ gla_status gla_recurrent_fwd(const gla_problem *prob, const void *q, const void 
                              const void *v, const void *log_alpha, const float *S0, void *o,
                              float *S_T, void *stream);
 
+/* Output side of the layer (Sec. 4.4): per head and row, y_t = Swish(g_t) (.)
+ * LN(o_t) with LN(x) = w (.) (x - mean(x)) / sqrt(var(x) + eps) + b over the
+ * d_v features of one head (biased variance), g the output-gate
+ * pre-activation (its projection is the caller's GEMM).
+ * prob: only B, H, T, dv and io are used (dv a multiple of 16, <= 1024).
+ *   o, g, y, dy, d_o, dg : [B, H, T, d_v] (io dtype)
+ *   ln_w, ln_b, dln_w, dln_b : [H, d_v] fp32, nullable (absent w = 1, b = 0;
+ *                              an absent gradient is not computed)
+ *   stats (nullable, fp32 [B, H, T, 2]): mean and 1/sqrt(var + eps) per row
+ *   eps: finite and > 0, else GLA_ERR_SHAPE.
+ * The backward (loss L = sum(y * dy)) recomputes the row statistics; its
+ * workspace holds per-(batch row, head, 64-step block) partial sums of the
+ * affine gradients (gla_output_gate_workspace_bytes; may be 0 bytes / NULL
+ * when dln_w and dln_b are both NULL).  d_o is the dO of gla_chunk_bwd. */
+size_t gla_output_gate_workspace_bytes(const gla_problem *prob);
+gla_status gla_output_gate_fwd(const gla_problem *prob, const void *o, const void *g,
+                               const float *ln_w, const float *ln_b, float eps, void *y,
+                               float *stats, void *stream);
+gla_status gla_output_gate_bwd(const gla_problem *prob, const void *o, const void *g,
+                               const float *ln_w, const float *ln_b, float eps, const void *dy,
+                               void *d_o, void *dg, float *dln_w, float *dln_b, void *workspace,
+                               size_t workspace_bytes, void *stream);
+
 /* Static, human-readable name of a status code (never NULL). */
 const char *gla_status_string(gla_status status);
 

@@ -69,6 +69,13 @@ def lib():
         L.gla_recurrent_fwd.restype = i32
         L.gla_status_string.argtypes = [i32]
         L.gla_status_string.restype = ctypes.c_char_p
+        f32 = ctypes.c_float
+        L.gla_output_gate_workspace_bytes.argtypes = [P]
+        L.gla_output_gate_workspace_bytes.restype = sz
+        L.gla_output_gate_fwd.argtypes = [P, vp, vp, vp, vp, f32, vp, vp, vp]
+        L.gla_output_gate_fwd.restype = i32
+        L.gla_output_gate_bwd.argtypes = [P, vp, vp, vp, vp, f32, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.gla_output_gate_bwd.restype = i32
         _lib = L
     return _lib
 
@@ -209,3 +216,58 @@ def recurrent_fwd(q, k, v, log_alpha, S0=None, output_final_state=False, gate_ta
     if st != GLA_OK:
         raise GlaError(st, "gla_recurrent_fwd")
     return o, ST
+
+
+def _og_problem(o):
+    if o.dim() != 4:
+        raise ValueError("o must be [B, H, T, d_v]")
+    B, H, T, dv = o.shape
+    return GlaProblem(B, H, T, 16, dv, 64, 16, _io_code(o.dtype), 0, 0.0)
+
+
+def _og_check(o, others, affine):
+    if o.device.type != "cuda" or not o.is_contiguous():
+        raise ValueError("o must be a contiguous tensor on a HIP device")
+    for name, t in others:
+        if t.shape != o.shape or t.dtype != o.dtype or t.device != o.device or not t.is_contiguous():
+            raise ValueError(f"{name} must match o ({tuple(o.shape)}, {o.dtype})")
+    H, dv = o.shape[1], o.shape[3]
+    for name, t in affine:
+        if t is not None and (tuple(t.shape) != (H, dv) or t.dtype != torch.float32 or t.device != o.device
+                              or not t.is_contiguous()):
+            raise ValueError(f"{name} must be a contiguous float32 [H, d_v] tensor on {o.device}")
+
+
+def output_gate_fwd(o, g, ln_w=None, ln_b=None, eps=1e-5, want_stats=False):
+    """Output side of the layer: y = Swish(g) * LN(o) per head row (LN over
+    d_v with optional [H, d_v] affine parameters).  Returns (y, stats or None),
+    stats = (mean, 1/sqrt(var + eps)) per row, float32 [B, H, T, 2]."""
+    _og_check(o, (("g", g),), (("ln_w", ln_w), ("ln_b", ln_b)))
+    p = _og_problem(o)
+    y = torch.empty_like(o)
+    stats = torch.empty(*o.shape[:3], 2, dtype=torch.float32, device=o.device) if want_stats else None
+    st = lib().gla_output_gate_fwd(ctypes.byref(p), _ptr(o), _ptr(g), _ptr(ln_w), _ptr(ln_b),
+                                   ctypes.c_float(eps), _ptr(y), _ptr(stats), _stream(o.device))
+    if st != GLA_OK:
+        raise GlaError(st, "gla_output_gate_fwd")
+    return y, stats
+
+
+def output_gate_bwd(o, g, dy, ln_w=None, ln_b=None, eps=1e-5, want_affine_grads=True):
+    """Reverse mode of output_gate_fwd for L = sum(y * dy).  Returns dict(do,
+    dg, dln_w, dln_b); do is the dO of chunk_bwd; the affine gradients are
+    float32 [H, d_v] (None when not wanted)."""
+    _og_check(o, (("g", g), ("dy", dy)), (("ln_w", ln_w), ("ln_b", ln_b)))
+    p = _og_problem(o)
+    d_o, dg = torch.empty_like(o), torch.empty_like(o)
+    H, dv = o.shape[1], o.shape[3]
+    dw = torch.empty(H, dv, dtype=torch.float32, device=o.device) if want_affine_grads else None
+    db = torch.empty(H, dv, dtype=torch.float32, device=o.device) if want_affine_grads else None
+    need = int(lib().gla_output_gate_workspace_bytes(ctypes.byref(p))) if want_affine_grads else 0
+    ws = torch.empty(max(need, 1), dtype=torch.uint8, device=o.device)
+    st = lib().gla_output_gate_bwd(ctypes.byref(p), _ptr(o), _ptr(g), _ptr(ln_w), _ptr(ln_b),
+                                   ctypes.c_float(eps), _ptr(dy), _ptr(d_o), _ptr(dg), _ptr(dw), _ptr(db),
+                                   _ptr(ws), ws.numel(), _stream(o.device))
+    if st != GLA_OK:
+        raise GlaError(st, "gla_output_gate_bwd")
+    return {"do": d_o, "dg": dg, "dln_w": dw, "dln_b": db}

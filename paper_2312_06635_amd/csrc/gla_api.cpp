@@ -186,3 +186,56 @@ GLA_EXPORT gla_status gla_recurrent_fwd(const gla_problem *prob, const void *q, 
     return hip_status(gla::launch_copy_state((int64_t)s.BH * s.K * s.V, S0, S_T, hs));
   return hip_status(gla::launch_recurrent(s, q, k, v, log_alpha, S0, o, S_T, hs));
 }
+
+// ---------------------------------------------------------------- output side
+
+namespace {
+
+// The output side uses B, H, T, dv and io of the problem.
+gla_status og_check(const gla_problem *p, float eps) {
+  if (!p) return GLA_ERR_NULL;
+  if (p->io != GLA_F32 && p->io != GLA_BF16) return GLA_ERR_DTYPE;
+  if (p->B < 0 || p->H < 0 || p->T < 0 || p->dv <= 0) return GLA_ERR_SHAPE;
+  if (!(eps > 0.f && eps < 3.0e38f)) return GLA_ERR_SHAPE;
+  if (p->dv % 16 != 0 || p->dv > 1024) return GLA_ERR_UNSUPPORTED;
+  const int64_t rows = (int64_t)p->B * p->H * p->T;
+  if (rows >= (int64_t)1 << 31 || (int64_t)p->B * p->H > (1 << 24)) return GLA_ERR_UNSUPPORTED;
+  return GLA_OK;
+}
+
+}  // namespace
+
+GLA_EXPORT size_t gla_output_gate_workspace_bytes(const gla_problem *prob) {
+  if (og_check(prob, 1.f) != GLA_OK) return 0;
+  return gla::outgate_partial_bytes(prob->B, prob->H, prob->T, prob->dv);
+}
+
+GLA_EXPORT gla_status gla_output_gate_fwd(const gla_problem *prob, const void *o, const void *g,
+                                          const float *ln_w, const float *ln_b, float eps, void *y,
+                                          float *stats, void *stream) {
+  gla_status st = og_check(prob, eps);
+  if (st != GLA_OK) return st;
+  const int64_t rows = (int64_t)prob->B * prob->H * prob->T;
+  if (rows == 0) return GLA_OK;
+  if (!o || !g || !y) return GLA_ERR_NULL;
+  const int io = prob->io == GLA_BF16 ? gla::IO_BF16 : gla::IO_F32;
+  return hip_status(gla::launch_outgate_fwd(prob->B, prob->H, prob->T, prob->dv, io, o, g, ln_w, ln_b, eps, y,
+                                            stats, (hipStream_t)stream));
+}
+
+GLA_EXPORT gla_status gla_output_gate_bwd(const gla_problem *prob, const void *o, const void *g,
+                                          const float *ln_w, const float *ln_b, float eps, const void *dy,
+                                          void *d_o, void *dg, float *dln_w, float *dln_b, void *workspace,
+                                          size_t workspace_bytes, void *stream) {
+  gla_status st = og_check(prob, eps);
+  if (st != GLA_OK) return st;
+  const int64_t rows = (int64_t)prob->B * prob->H * prob->T;
+  const bool affine = dln_w || dln_b;
+  if (rows > 0 && (!o || !g || !dy || !d_o || !dg)) return GLA_ERR_NULL;
+  if (rows == 0 && (!affine || prob->H == 0)) return GLA_OK;  // (no rows: zero affine gradients below)
+  const size_t need = affine ? gla::outgate_partial_bytes(prob->B, prob->H, prob->T, prob->dv) : 0;
+  if (affine && (!workspace || workspace_bytes < need)) return GLA_ERR_WORKSPACE;
+  const int io = prob->io == GLA_BF16 ? gla::IO_BF16 : gla::IO_F32;
+  return hip_status(gla::launch_outgate_bwd(prob->B, prob->H, prob->T, prob->dv, io, o, g, ln_w, ln_b, eps, dy,
+                                            d_o, dg, dln_w, dln_b, (float *)workspace, (hipStream_t)stream));
+}

@@ -48,6 +48,14 @@ hipError_t launch_recurrent(const Shape &s, const void *q, const void *k, const 
 // T == 0 edge: S_T = S0 (or 0); dS0 = dS_T (or 0).
 hipError_t launch_copy_state(int64_t n, const float *src, float *dst, hipStream_t st);
 
+// Output side (per-head LayerNorm + Swish gate, gla_outgate.hip).
+size_t outgate_partial_bytes(int B, int H, int T, int V);
+hipError_t launch_outgate_fwd(int B, int H, int T, int V, int io, const void *o, const void *g, const float *w,
+                              const float *b, float eps, void *y, float *stats, hipStream_t st);
+hipError_t launch_outgate_bwd(int B, int H, int T, int V, int io, const void *o, const void *g, const float *w,
+                              const float *b, float eps, const void *dy, void *d_o, void *dg, float *dw,
+                              float *db, float *part, hipStream_t st);
+
 // LDS bytes each kernel needs (0 means the shape is not supported).
 size_t lds_prep(const Shape &s);
 size_t lds_fwd_main(const Shape &s);

@@ -28,8 +28,9 @@ def declared_functions():
 
 
 def test_header_declares_the_boundary():
-    assert declared_functions() == ["gla_chunk_bwd", "gla_chunk_fwd", "gla_recurrent_fwd",
-                                    "gla_status_string", "gla_workspace_bytes"]
+    assert declared_functions() == ["gla_chunk_bwd", "gla_chunk_fwd", "gla_output_gate_bwd",
+                                    "gla_output_gate_fwd", "gla_output_gate_workspace_bytes",
+                                    "gla_recurrent_fwd", "gla_status_string", "gla_workspace_bytes"]
 
 
 def test_every_declared_symbol_is_exported(L):
@@ -132,3 +133,41 @@ def test_stage_selector_is_validated(L):
     assert fwd_call(L, P(flags=3 << 8)) == gla.GLA_ERR_SHAPE
     assert bwd_call(L, P(flags=5 << 8)) == gla.GLA_ERR_SHAPE
     assert fwd_call(L, P(B=0, flags=3 << 8), ptr=None, ws=None, ws_bytes=0) == gla.GLA_ERR_SHAPE
+
+
+def og_fwd_call(L, p, eps=1e-5, ptr=1):
+    return L.gla_output_gate_fwd(ctypes.byref(p) if p is not None else None, ptr, ptr, None, None,
+                                 ctypes.c_float(eps), ptr, None, None)
+
+
+def og_bwd_call(L, p, eps=1e-5, ptr=1, ws=1, ws_bytes=1 << 40):
+    return L.gla_output_gate_bwd(ctypes.byref(p) if p is not None else None, ptr, ptr, None, None,
+                                 ctypes.c_float(eps), ptr, ptr, ptr, ptr, ptr, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,eps,code", [
+    (dict(io=7), 1e-5, gla.GLA_ERR_DTYPE),
+    (dict(T=-1), 1e-5, gla.GLA_ERR_SHAPE),
+    (dict(dv=0), 1e-5, gla.GLA_ERR_SHAPE),
+    (dict(), 0.0, gla.GLA_ERR_SHAPE),
+    (dict(), -1.0, gla.GLA_ERR_SHAPE),
+    (dict(), float("nan"), gla.GLA_ERR_SHAPE),
+    (dict(dv=24), 1e-5, gla.GLA_ERR_UNSUPPORTED),
+    (dict(dv=2048), 1e-5, gla.GLA_ERR_UNSUPPORTED),
+])
+def test_output_gate_rejects_invalid_problems(L, kw, eps, code):
+    assert og_fwd_call(L, P(**kw), eps) == code
+    assert og_bwd_call(L, P(**kw), eps) == code
+
+
+def test_output_gate_checks_pointers_and_workspace(L):
+    L.gla_output_gate_workspace_bytes.restype = ctypes.c_size_t
+    p = P()
+    need = L.gla_output_gate_workspace_bytes(ctypes.byref(p))
+    assert need == 2 * 3 * ((200 + 63) // 64) * 2 * 128 * 4
+    assert og_fwd_call(L, None) == gla.GLA_ERR_NULL
+    assert og_fwd_call(L, p, ptr=None) == gla.GLA_ERR_NULL
+    assert og_bwd_call(L, p, ptr=None) == gla.GLA_ERR_NULL
+    assert og_bwd_call(L, p, ws=None) == gla.GLA_ERR_WORKSPACE
+    assert og_bwd_call(L, p, ws_bytes=need - 1) == gla.GLA_ERR_WORKSPACE
+    assert og_fwd_call(L, P(B=0), ptr=None) == gla.GLA_OK

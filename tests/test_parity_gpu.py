@@ -6,6 +6,7 @@ element; the full-size workloads are run in the benchmark's configuration and
 compared on sampled heads, which the oracle computes exactly (heads are
 independent).  Every input is seeded and synthetic (workloads.py).
 """
+import ctypes
 import sys
 
 import numpy as np
@@ -233,6 +234,41 @@ def test_gate_preactivation_epilogue(io):
     assert not bad, f"{cfg['name']}: {bad} > {TOL[io]}"
 
 
+OG_CASES = [("f32", 2, 3, 70, 48, True), ("f32", 1, 2, 130, 1024, False), ("bf16", 2, 4, 100, 512, True),
+            ("bf16", 1, 2, 64, 256, False), ("bf16", 1, 1, 5, 80, True)]
+
+
+@pytest.mark.parametrize("io,B,H,T,V,affine", OG_CASES, ids=[f"{c[0]}_V{c[4]}_T{c[3]}" for c in OG_CASES])
+def test_output_gate(io, B, H, T, V, affine):
+    """Output side (Sec. 4.4): y = Swish(g) (.) LN(o) per head row, and its
+    reverse mode (do, dg and the per-channel affine gradients), against the
+    oracle; T not a multiple of the 64-row blocks of the backward."""
+    g_ = gla()
+    gen = torch.Generator().manual_seed(100 + V + T)
+    dt = torch.float32 if io == "f32" else torch.bfloat16
+    o = (torch.randn(B, H, T, V, generator=gen) * 1.5 + 0.3).to(dt)
+    g = (torch.randn(B, H, T, V, generator=gen) * 2.0).to(dt)
+    dy = torch.randn(B, H, T, V, generator=gen).to(dt)
+    w = (1.0 + 0.2 * torch.randn(H, V, generator=gen)) if affine else None
+    b = (0.1 * torch.randn(H, V, generator=gen)) if affine else None
+    dev = lambda t: t.cuda() if t is not None else None
+    y, stats = g_.output_gate_fwd(dev(o), dev(g), dev(w), dev(b), eps=1e-5, want_stats=True)
+    gr = g_.output_gate_bwd(dev(o), dev(g), dev(dy), dev(w), dev(b), eps=1e-5)
+    torch.cuda.synchronize()
+    f = lambda t: t.double().numpy()
+    ry, rmu, rrs = oracle.output_gate_fwd(f(o.float()), f(g.float()), None if w is None else f(w),
+                                          None if b is None else f(b), eps=1e-5)
+    rg = oracle.output_gate_bwd(f(o.float()), f(g.float()), f(dy.float()), None if w is None else f(w),
+                                None if b is None else f(b), eps=1e-5)
+    c = lambda t: t.detach().float().cpu().double().numpy()
+    errs = {"y": rel(c(y), ry), "mean": rel(c(stats[..., 0]), rmu), "rstd": rel(c(stats[..., 1]), rrs),
+            "do": rel(c(gr["do"]), rg["do"]), "dg": rel(c(gr["dg"]), rg["dg"]),
+            "dw": rel(c(gr["dln_w"]), rg["dw"]), "db": rel(c(gr["dln_b"]), rg["db"])}
+    say("output gate", io, B, H, T, V, affine, {k: f"{v:.2e}" for k, v in errs.items()})
+    bad = {k: v for k, v in errs.items() if not v <= TOL[io]}
+    assert not bad, bad
+
+
 def test_empty_sequence_and_batch():
     g = gla()
     for T in (0,):
@@ -250,6 +286,23 @@ def test_empty_sequence_and_batch():
     v = torch.zeros(0, 4, 64, 48, device="cuda", dtype=torch.bfloat16)
     o, _ = g.chunk_fwd(q, q, v, q, 64, 16)
     assert o.shape == (0, 4, 64, 48)
+    # Output side with no rows: empty outputs, and affine gradients that are
+    # written as exact zeros (the buffers start as NaN here).
+    for shape in ((2, 3, 0, 64), (0, 3, 16, 64)):
+        o = torch.zeros(*shape, device="cuda", dtype=torch.bfloat16)
+        w = torch.ones(3, 64, device="cuda")
+        y, stats = g.output_gate_fwd(o, o, w, w, want_stats=True)
+        assert y.shape == shape and stats.shape == (*shape[:3], 2)
+        dw = torch.full((3, 64), float("nan"), device="cuda")
+        db = torch.full((3, 64), float("nan"), device="cuda")
+        lib, p = g.lib(), g._og_problem(o)
+        need = int(lib.gla_output_gate_workspace_bytes(ctypes.byref(p)))
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device="cuda")
+        st = lib.gla_output_gate_bwd(ctypes.byref(p), g._ptr(o), g._ptr(o), g._ptr(w), g._ptr(w),
+                                     ctypes.c_float(1e-5), g._ptr(o), g._ptr(o), g._ptr(o),
+                                     g._ptr(dw), g._ptr(db), g._ptr(ws), ws.numel(), g._stream(o.device))
+        torch.cuda.synchronize()
+        assert st == 0 and torch.equal(dw, torch.zeros_like(dw)) and torch.equal(db, torch.zeros_like(db))
 
 
 def test_deterministic_and_workspace_reuse_is_exact():
