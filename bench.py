@@ -6,7 +6,10 @@ gated operands and intra-chunk matrices; state pass and outputs) followed by
 gla_chunk_bwd reusing the forward's workspace (dq sweep; dk/dlog_alpha sweep;
 dv sweep).  Each stage is launched on its own through the C ABI's stage
 selector with a HIP event after it, so the per-kernel durations are measured
-live on the stream the kernels run on, inside the timed region.
+live on the stream the kernels run on, inside the timed region.  With
+--output-gate the step also runs the output side (per-head LayerNorm and Swish
+output gate, Sec. 4.4) after the forward and its reverse mode, which produces
+the dO the backward sweeps consume, before them.
 
 Prints one JSON line.  `value` is tokens/s (B*T per step) with all inputs
 resident in HBM; TFLOP/s uses the algorithmic FLOP count of the chunk form
@@ -35,6 +38,9 @@ RIDGE = PEAK_BF16_FLOPS / PEAK_HBM
 
 STAGES = [("prep", "fwd", 1), ("fwd_main", "fwd", 2), ("bwd_dq", "bwd", 2), ("bwd_dk", "bwd", 3),
           ("bwd_dv", "bwd", 4)]
+# with the output side (Sec. 4.4): LN + Swish gate after the forward, its
+# reverse mode (producing the layer's dO) before the backward sweeps
+STAGES_OG = STAGES[:2] + [("og_fwd", "og", 0), ("og_bwd", "og", 1)] + STAGES[2:]
 
 
 def algorithmic(cfg, gate=True):
@@ -60,6 +66,10 @@ def algorithmic(cfg, gate=True):
                        bytes=n * s * ((4 + 2 * ga) * K + 2 * V) + dP),
         # dv sweep: reads Qt, Kt, P, gamma, dO; writes dv
         "bwd_dv": dict(flops=n * (2 * K * V + (C + 1) * V), bytes=n * s * (2 * K + 2 * V) + P + g),
+        # output side: reads o, g and the [H, d_v] affine; writes y
+        "og_fwd": dict(flops=n * V * 12, bytes=n * s * 3 * V + H * V * 8),
+        # its reverse: reads o, g, dy and the affine; writes dO, dg, dw, db
+        "og_bwd": dict(flops=n * V * 24, bytes=n * s * 5 * V + H * V * 16),
     }
     fwd = n * (4 * K * V + (C + 1) * (K + V))
     bwd = n * (8 * K * V + (C + 1) * (3 * K + 2 * V))
@@ -155,6 +165,8 @@ def main():
                     help="the alpha = 1 (ungated) layer: log_alpha passed as NULL")
     ap.add_argument("--gate-tau", type=float, default=0.0,
                     help="> 0: pass the gate pre-activation z (alpha = sigmoid(z)^(1/tau)) instead of log alpha")
+    ap.add_argument("--output-gate", action="store_true",
+                    help="include the output side (per-head LN + Swish gate, Sec. 4.4) in the step")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (reference for HBM traffic counters)")
     args = ap.parse_args()
@@ -192,9 +204,27 @@ def main():
              "dlog_alpha": torch.empty_like(d["q"]) if d["log_alpha"] is not None else None,
              "dS0": torch.empty(B, H, K, V, dtype=torch.float32, device=dev) if d["S0"] is not None else None}
     stream = torch.cuda.current_stream(dev)
+    stages = STAGES_OG if args.output_gate else STAGES
+    if args.output_gate:
+        # output-gate pre-activations, the loss gradient at y and the LN affine
+        go = torch.Generator().manual_seed(cfg["seed"] + 11)
+        og = {"g": torch.randn(B, H, T, V, generator=go).to(dt), "dy": torch.randn(B, H, T, V, generator=go).to(dt),
+              "w": 1.0 + 0.1 * torch.randn(H, V, generator=go), "b": 0.1 * torch.randn(H, V, generator=go)}
+        og = {k: v.to(dev) for k, v in og.items()}
+        y = torch.empty_like(o)
+        og_out = {"do": torch.empty_like(o), "dg": torch.empty_like(o),
+                  "dln_w": torch.empty(H, V, dtype=torch.float32, device=dev),
+                  "dln_b": torch.empty(H, V, dtype=torch.float32, device=dev)}
+        og_ws = torch.empty(max(gla.output_gate_workspace_bytes(o), 1), dtype=torch.uint8, device=dev)
+        d["dO"] = og_out["do"]  # the layer's dO is what the output side's reverse mode produces
 
     def launch(stage_name, which, stage):
-        if which == "fwd":
+        if which == "og":
+            if stage == 0:
+                gla.output_gate_fwd(o, og["g"], og["w"], og["b"], out=(y, None))
+            else:
+                gla.output_gate_bwd(o, og["g"], og["dy"], og["w"], og["b"], out=og_out, workspace=og_ws)
+        elif which == "fwd":
             gla.chunk_fwd(d["q"], d["k"], d["v"], d["log_alpha"], C, c, S0=d["S0"], workspace=ws,
                           stage=stage, out=(o, ST), gate_tau=args.gate_tau)
         else:
@@ -205,7 +235,7 @@ def main():
     def step(events=None):
         if events is not None:
             events[0].record(stream)
-        for i, (nm, which, stg) in enumerate(STAGES):
+        for i, (nm, which, stg) in enumerate(stages):
             launch(nm, which, stg)
             if events is not None:
                 events[i + 1].record(stream)
@@ -213,7 +243,7 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(STAGES) + 1)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)]
            for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -222,30 +252,36 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
 
-    stage_ms = {nm: 0.0 for nm, _, _ in STAGES}
+    stage_ms = {nm: 0.0 for nm, _, _ in stages}
     for s in range(args.steps):
-        for i, (nm, _, _) in enumerate(STAGES):
+        for i, (nm, _, _) in enumerate(stages):
             stage_ms[nm] += evs[s][i].elapsed_time(evs[s][i + 1]) / args.steps
     st_alg, fwd_flops, bwd_flops, io_bytes = algorithmic(cfg, gate=not args.no_gate)
+    if args.output_gate:
+        io_bytes += st_alg["og_fwd"]["bytes"] + st_alg["og_bwd"]["bytes"]
     ms_per_step = 1e3 * elapsed / args.steps
     tokens = B * T
     value = tokens * args.steps / elapsed
     tflops = (fwd_flops + bwd_flops) * args.steps / elapsed / 1e12
     peak = PEAK_BF16_FLOPS if cfg["io"] == "bf16" else PEAK_F32_FLOPS
 
+    def roofline(nm):
+        a, t = st_alg[nm], stage_ms[nm] * 1e-3
+        if a["flops"] / a["bytes"] < RIDGE:
+            r = {"kernel": nm, "bound": "hbm", "achieved": a["bytes"] / t / 1e9, "peak": PEAK_HBM / 1e9,
+                 "unit": "GB/s"}
+        else:
+            r = {"kernel": nm, "bound": "mfma", "achieved": a["flops"] / t / 1e12, "peak": peak / 1e12,
+                 "unit": "TFLOP/s"}
+        r["frac"] = r["achieved"] / r["peak"]
+        return r
+
     dom = max(stage_ms, key=stage_ms.get)
-    a = st_alg[dom]
-    t_dom = stage_ms[dom] * 1e-3
-    ai = a["flops"] / a["bytes"]
-    if ai < RIDGE:
-        roof = {"kernel": dom, "bound": "hbm", "achieved": a["bytes"] / t_dom / 1e9, "peak": PEAK_HBM / 1e9,
-                "unit": "GB/s"}
-    else:
-        roof = {"kernel": dom, "bound": "mfma", "achieved": a["flops"] / t_dom / 1e12, "peak": peak / 1e12,
-                "unit": "TFLOP/s"}
-    roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None if (args.no_gate or args.gate_tau > 0) else measured_traffic(args.workload, dom)
+    roof = roofline(dom)
+    plain = not (args.no_gate or args.gate_tau > 0 or args.output_gate)
+    roof["traffic"] = measured_traffic(args.workload, dom) if plain else None
     roof["avg_ms"] = stage_ms[dom]
+    stage_frac = {nm: f"{r['frac']:.3f} of {r['bound']}" for nm, r in ((nm, roofline(nm)) for nm in stage_ms)}
 
     out = {
         "metric": "GLA fwd+bwd tokens/s and TFLOP/s (% bf16 MFMA peak), 1.3B layer, T=2048",
@@ -256,10 +292,13 @@ def main():
                    "subchunk": c, "parallelism": "none (1 GPU)",
                    **({"gate": "none (alpha = 1, log_alpha NULL)"} if args.no_gate else {}),
                    **({"gate": f"pre-activation z, alpha = sigmoid(z)^(1/{args.gate_tau:g})"}
-                      if args.gate_tau > 0 else {})},
+                      if args.gate_tau > 0 else {}),
+                   **({"output_side": "per-head LN (affine) + Swish output gate, fwd + bwd"}
+                      if args.output_gate else {})},
         "tflops": tflops, "mfma_peak_frac": tflops * 1e12 / peak,
         "hbm_io_roofline_frac": (io_bytes / PEAK_HBM) / (elapsed / args.steps),
         "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
+        "stage_roofline_frac": stage_frac,
         "roofline": roof,
     }
     if not args.no_cpu_baseline:

@@ -158,7 +158,10 @@ gla_status gla_recurrent_fwd(const gla_problem *prob, const void *q, const void 
  * The backward (loss L = sum(y * dy)) recomputes the row statistics; its
  * workspace holds per-(batch row, head, 64-step block) partial sums of the
  * affine gradients (gla_output_gate_workspace_bytes; may be 0 bytes / NULL
- * when dln_w and dln_b are both NULL).  d_o is the dO of gla_chunk_bwd. */
+ * when dln_w and dln_b are both NULL or there are no rows; smaller than
+ * needed: GLA_ERR_WORKSPACE).  With no rows the affine gradients are written
+ * as zeros.  The affine gradients are summed in a fixed order, so repeated
+ * calls give the same bits.  d_o is the dO of gla_chunk_bwd. */
 size_t gla_output_gate_workspace_bytes(const gla_problem *prob);
 gla_status gla_output_gate_fwd(const gla_problem *prob, const void *o, const void *g,
                                const float *ln_w, const float *ln_b, float eps, void *y,

@@ -21,6 +21,7 @@ __all__ = [
     "chunk_fwd", "chunk_bwd", "recurrent_fwd", "workspace_bytes", "GlaError", "library_path",
     "GLA_OK", "GLA_ERR_NULL", "GLA_ERR_SHAPE", "GLA_ERR_DTYPE", "GLA_ERR_UNSUPPORTED",
     "GLA_ERR_WORKSPACE", "GLA_ERR_HIP", "FLAG_REUSE_FWD_WORKSPACE", "GlaProblem", "lib",
+    "output_gate_fwd", "output_gate_bwd", "output_gate_workspace_bytes",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -225,6 +226,12 @@ def _og_problem(o):
     return GlaProblem(B, H, T, 16, dv, 64, 16, _io_code(o.dtype), 0, 0.0)
 
 
+def output_gate_workspace_bytes(o):
+    """Device workspace (bytes) that output_gate_bwd needs for o's shape when
+    the affine gradients are wanted."""
+    return int(lib().gla_output_gate_workspace_bytes(ctypes.byref(_og_problem(o))))
+
+
 def _og_check(o, others, affine):
     if o.device.type != "cuda" or not o.is_contiguous():
         raise ValueError("o must be a contiguous tensor on a HIP device")
@@ -238,14 +245,22 @@ def _og_check(o, others, affine):
             raise ValueError(f"{name} must be a contiguous float32 [H, d_v] tensor on {o.device}")
 
 
-def output_gate_fwd(o, g, ln_w=None, ln_b=None, eps=1e-5, want_stats=False):
+def output_gate_fwd(o, g, ln_w=None, ln_b=None, eps=1e-5, want_stats=False, out=None):
     """Output side of the layer: y = Swish(g) * LN(o) per head row (LN over
     d_v with optional [H, d_v] affine parameters).  Returns (y, stats or None),
-    stats = (mean, 1/sqrt(var + eps)) per row, float32 [B, H, T, 2]."""
+    stats = (mean, 1/sqrt(var + eps)) per row, float32 [B, H, T, 2].
+    out=(y, stats) reuses preallocated outputs (stats may be None)."""
     _og_check(o, (("g", g),), (("ln_w", ln_w), ("ln_b", ln_b)))
     p = _og_problem(o)
-    y = torch.empty_like(o)
-    stats = torch.empty(*o.shape[:3], 2, dtype=torch.float32, device=o.device) if want_stats else None
+    if out is not None:
+        y, stats = out
+        _og_check(o, (("y", y),), ())
+        if stats is not None and (tuple(stats.shape) != (*o.shape[:3], 2) or stats.dtype != torch.float32
+                                  or not stats.is_contiguous()):
+            raise ValueError("stats must be a contiguous float32 [B, H, T, 2] tensor")
+    else:
+        y = torch.empty_like(o)
+        stats = torch.empty(*o.shape[:3], 2, dtype=torch.float32, device=o.device) if want_stats else None
     st = lib().gla_output_gate_fwd(ctypes.byref(p), _ptr(o), _ptr(g), _ptr(ln_w), _ptr(ln_b),
                                    ctypes.c_float(eps), _ptr(y), _ptr(stats), _stream(o.device))
     if st != GLA_OK:
@@ -253,18 +268,28 @@ def output_gate_fwd(o, g, ln_w=None, ln_b=None, eps=1e-5, want_stats=False):
     return y, stats
 
 
-def output_gate_bwd(o, g, dy, ln_w=None, ln_b=None, eps=1e-5, want_affine_grads=True):
+def output_gate_bwd(o, g, dy, ln_w=None, ln_b=None, eps=1e-5, want_affine_grads=True, out=None,
+                    workspace=None):
     """Reverse mode of output_gate_fwd for L = sum(y * dy).  Returns dict(do,
     dg, dln_w, dln_b); do is the dO of chunk_bwd; the affine gradients are
-    float32 [H, d_v] (None when not wanted)."""
+    float32 [H, d_v] (None when not wanted).  out=dict(do, dg, dln_w, dln_b)
+    reuses preallocated outputs; workspace is a uint8 device tensor of at
+    least output_gate_workspace_bytes bytes."""
     _og_check(o, (("g", g), ("dy", dy)), (("ln_w", ln_w), ("ln_b", ln_b)))
     p = _og_problem(o)
-    d_o, dg = torch.empty_like(o), torch.empty_like(o)
     H, dv = o.shape[1], o.shape[3]
-    dw = torch.empty(H, dv, dtype=torch.float32, device=o.device) if want_affine_grads else None
-    db = torch.empty(H, dv, dtype=torch.float32, device=o.device) if want_affine_grads else None
-    need = int(lib().gla_output_gate_workspace_bytes(ctypes.byref(p))) if want_affine_grads else 0
-    ws = torch.empty(max(need, 1), dtype=torch.uint8, device=o.device)
+    if out is not None:
+        d_o, dg, dw, db = out["do"], out["dg"], out.get("dln_w"), out.get("dln_b")
+        _og_check(o, (("do", d_o), ("dg", dg)), (("dln_w", dw), ("dln_b", db)))
+    else:
+        d_o, dg = torch.empty_like(o), torch.empty_like(o)
+        dw = torch.empty(H, dv, dtype=torch.float32, device=o.device) if want_affine_grads else None
+        db = torch.empty(H, dv, dtype=torch.float32, device=o.device) if want_affine_grads else None
+    if workspace is not None:
+        ws = workspace
+    else:
+        need = output_gate_workspace_bytes(o) if (dw is not None or db is not None) else 0
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=o.device)
     st = lib().gla_output_gate_bwd(ctypes.byref(p), _ptr(o), _ptr(g), _ptr(ln_w), _ptr(ln_b),
                                    ctypes.c_float(eps), _ptr(dy), _ptr(d_o), _ptr(dg), _ptr(dw), _ptr(db),
                                    _ptr(ws), ws.numel(), _stream(o.device))

@@ -234,7 +234,7 @@ GLA_EXPORT gla_status gla_output_gate_bwd(const gla_problem *prob, const void *o
   if (rows > 0 && (!o || !g || !dy || !d_o || !dg)) return GLA_ERR_NULL;
   if (rows == 0 && (!affine || prob->H == 0)) return GLA_OK;  // (no rows: zero affine gradients below)
   const size_t need = affine ? gla::outgate_partial_bytes(prob->B, prob->H, prob->T, prob->dv) : 0;
-  if (affine && (!workspace || workspace_bytes < need)) return GLA_ERR_WORKSPACE;
+  if (affine && need > 0 && (!workspace || workspace_bytes < need)) return GLA_ERR_WORKSPACE;
   const int io = prob->io == GLA_BF16 ? gla::IO_BF16 : gla::IO_F32;
   return hip_status(gla::launch_outgate_bwd(prob->B, prob->H, prob->T, prob->dv, io, o, g, ln_w, ln_b, eps, dy,
                                             d_o, dg, dln_w, dln_b, (float *)workspace, (hipStream_t)stream));

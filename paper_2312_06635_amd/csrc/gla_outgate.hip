@@ -4,14 +4,18 @@
 // with g_t the output-gate pre-activation and w, b per-channel affine
 // parameters of the concatenated heads ([H][d_v], optional).
 //
-// Rows are independent and d_v <= 1024, so one wave owns one row: lane l
-// holds the EPL consecutive features EPL l .. +EPL-1 in registers, the row's
-// mean and variance are two-pass wave reductions in fp32, and every tensor is
-// read and written once with one buffer access per lane (rows and features
-// outside the tensors fall outside the buffer ranges).  The backward also
-// forms the per-channel gradients of w and b: each workgroup sums its rows'
-// contributions (one head, 64 consecutive time steps) and writes one partial
-// row; a second kernel adds the partials of each head in a fixed order.
+// Rows are independent and d_v <= 1024, so one wave owns one row at a time:
+// lane l holds the EPL consecutive features EPL l .. +EPL-1 in registers (d_v
+// is a multiple of 16, so a lane's features are all inside the row or all
+// outside it), the row's mean and variance are two-pass wave reductions in
+// fp32 (DPP within 16-lane rows, then the four row sums), and every tensor is
+// read and written once with one buffer access per lane.  A wave loads a batch
+// of consecutive rows of one head before it reduces any of them, so enough
+// bytes are in flight to stream at HBM rate; rows and features outside the
+// tensors fall outside the buffer ranges (loads give zero, stores drop).
+// The backward also forms the per-channel gradients of w and b: each
+// workgroup sums its 64 rows' contributions and writes one partial row; a
+// second kernel adds the partials of each head in a fixed order.
 #include "gla_common.hpp"
 #include "gla_launch.hpp"
 
@@ -19,18 +23,30 @@ namespace gla {
 
 namespace {
 
-constexpr int kOgWaves = 4;      // rows in flight per workgroup
-constexpr int kOgRowsPerWg = 64; // rows of one (batch, head) per backward workgroup
+constexpr int kOgWaves = 4;        // waves per forward / backward workgroup
+constexpr int kOgRowsPerWg = 64;   // rows of one (batch, head) per backward workgroup
+constexpr int kOgRedWaves = 16;    // waves per affine-reduction workgroup
+
+// Rows a wave loads per batch: up to 64 bytes of each tensor per lane in the
+// forward (two tensors in), half that in the backward (three in, more live).
+template <typename T, int EPL>
+constexpr int og_rows() {
+  return EPL * (int)sizeof(T) >= 64 ? 1 : (EPL * (int)sizeof(T) >= 32 ? 2 : 4);
+}
+template <typename T, int EPL>
+constexpr int og_rows_bwd() {
+  return og_rows<T, EPL>() > 1 ? og_rows<T, EPL>() / 2 : 1;
+}
 
 struct OgArgs {
   const void *o, *g, *dy;
   const float *w, *b;
   void *y, *d_o, *dg;
   float *stats;        // forward: [rows][2] (mean, rstd), nullable
-  float *part;         // backward: [nwg][2][V] partial (dw, db), nullable
+  float *part;         // backward: [B H tblocks][2][V] partial (dw, db), nullable
   float *dw, *db;      // backward: [H][V], nullable
-  int H, T, V, rows, tblocks;
-  float eps;
+  int H, T, V, tblocks;
+  float eps, inv_v;
 };
 
 template <typename T, int EPL>
@@ -89,117 +105,165 @@ __device__ __forceinline__ void og_store(__amdgpu_buffer_rsrc_t rs, uint32_t off
   }
 }
 
+// Lane value of the DPP-permuted register (all lanes take part).
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+
+__device__ __forceinline__ float lane_value(float x, int lane) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), lane));
+}
+
+// Sum over the wave, the same bits in every lane: a butterfly inside each
+// 16-lane row (partners lane^1, lane^2, then the mirrored quad and half row),
+// then the four row sums.
 __device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m);
-  return x;
+  x += dpp<0xB1>(x);   // quad_perm [1,0,3,2]
+  x += dpp<0x4E>(x);   // quad_perm [2,3,0,1]
+  x += dpp<0x141>(x);  // row_half_mirror
+  x += dpp<0x140>(x);  // row_mirror
+  return (lane_value(x, 0) + lane_value(x, 16)) + (lane_value(x, 32) + lane_value(x, 48));
 }
 
 __device__ __forceinline__ float sigmoid(float x) { return 1.f / (1.f + __expf(-x)); }
 
-// Row statistics of x (features beyond V are zero and excluded): mean and
-// 1 / sqrt(biased variance + eps), the variance taken about the mean.
+// Row statistics of x (lanes past the row hold zeros and are excluded): mean
+// and 1 / sqrt(biased variance + eps), the variance taken about the mean.
 template <int EPL>
-__device__ __forceinline__ void row_stats(const float (&x)[EPL], bool (&in)[EPL], int V, float eps, float &mean,
+__device__ __forceinline__ void row_stats(const float (&x)[EPL], bool lv, float inv_v, float eps, float &mean,
                                           float &rstd) {
   float s = 0.f;
 #pragma unroll
   for (int i = 0; i < EPL; ++i) s += x[i];
-  mean = wave_sum(s) / (float)V;
+  mean = wave_sum(s) * inv_v;
   float q = 0.f;
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
-    const float d = in[i] ? x[i] - mean : 0.f;
+    const float d = lv ? x[i] - mean : 0.f;
     q += d * d;
   }
-  rstd = rsqrtf(wave_sum(q) / (float)V + eps);
+  rstd = rsqrtf(wave_sum(q) * inv_v + eps);
 }
 
+// The per-channel affine of head h for this lane's features (1 and 0 when
+// absent).
+template <int EPL>
+__device__ __forceinline__ void load_affine(const OgArgs &a, int h, uint32_t foff, float (&wf)[EPL],
+                                            float (&bf)[EPL]) {
+  const uint32_t vb = (uint32_t)a.V * 4u;
+  if (a.w) {
+    og_load<float, EPL>(make_rsrc(a.w + (int64_t)h * a.V, vb), foff, wf);
+  } else {
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) wf[i] = 1.f;
+  }
+  if (a.b) {
+    og_load<float, EPL>(make_rsrc(a.b + (int64_t)h * a.V, vb), foff, bf);
+  } else {
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) bf[i] = 0.f;
+  }
+}
+
+// Workgroup = (batch-head bh, time block tb) as blockIdx.x = bh tblocks + tb;
+// wave w takes the R consecutive rows from (kOgWaves tb + w) R.
 template <typename T, int EPL>
 __global__ void __launch_bounds__(64 * kOgWaves) outgate_fwd_kernel(OgArgs a) {
+  constexpr int R = og_rows<T, EPL>();
   const int w = wave_id(), l = lane_id();
-  const int row = blockIdx.x * kOgWaves + w;
-  if (row >= a.rows) return;  // whole waves leave together
-  const int V = a.V, h = (row / a.T) % a.H, f0 = EPL * l;
-  const int esz = sizeof(T);
-  const uint32_t rb = (uint32_t)(V * esz);
-  const uint32_t off = f0 < V ? (uint32_t)(f0 * esz) : 0x80000000u;
-  const int64_t base = (int64_t)row * V;
-  float x[EPL], gg[EPL];
-  bool in[EPL];
-  og_load<T, EPL>(make_rsrc((const T *)a.o + base, rb), off, x);
-  og_load<T, EPL>(make_rsrc((const T *)a.g + base, rb), off, gg);
+  const int bh = blockIdx.x / a.tblocks, tb = blockIdx.x - bh * a.tblocks;
+  const int t0 = (tb * kOgWaves + w) * R;
+  if (t0 >= a.T) return;  // whole waves leave together
+  const int V = a.V, h = bh % a.H, f0 = EPL * l, nr = min(R, a.T - t0);
+  const bool lv = f0 < V;
+  constexpr uint32_t esz = sizeof(T);
+  const uint32_t rowb = (uint32_t)V * esz, off = lv ? (uint32_t)f0 * esz : 0x80000000u;
+  const int64_t base = ((int64_t)bh * a.T + t0) * V;
+  const auto ro = make_rsrc((const T *)a.o + base, nr * rowb), rg = make_rsrc((const T *)a.g + base, nr * rowb);
+  float x[R][EPL], gg[R][EPL], wf[EPL], bf[EPL];
 #pragma unroll
-  for (int i = 0; i < EPL; ++i) in[i] = f0 + i < V;
-  float mean, rstd;
-  row_stats<EPL>(x, in, V, a.eps, mean, rstd);
-  float y[EPL];
+  for (int r = 0; r < R; ++r) og_load<T, EPL>(ro, off + r * rowb, x[r]);
 #pragma unroll
-  for (int i = 0; i < EPL; ++i) {
-    const int f = f0 + i;
-    const float wf = (a.w && in[i]) ? a.w[h * V + f] : 1.f;
-    const float bf = (a.b && in[i]) ? a.b[h * V + f] : 0.f;
-    const float ln = (x[i] - mean) * rstd * wf + bf;
-    y[i] = gg[i] * sigmoid(gg[i]) * ln;
-  }
-  og_store<T, EPL>(make_rsrc((T *)a.y + base, rb), off, y);
-  if (a.stats && l == 0) {
-    a.stats[2 * (int64_t)row] = mean;
-    a.stats[2 * (int64_t)row + 1] = rstd;
+  for (int r = 0; r < R; ++r) og_load<T, EPL>(rg, off + r * rowb, gg[r]);
+  load_affine<EPL>(a, h, lv ? (uint32_t)f0 * 4u : 0x80000000u, wf, bf);
+  const auto ry = make_rsrc((T *)a.y + base, nr * rowb);
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    float mean, rstd, y[EPL];
+    row_stats<EPL>(x[r], lv, a.inv_v, a.eps, mean, rstd);
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+      const float ln = (x[r][i] - mean) * rstd * wf[i] + bf[i];
+      y[i] = gg[r][i] * sigmoid(gg[r][i]) * ln;
+    }
+    og_store<T, EPL>(ry, off + r * rowb, y);
+    if (a.stats && l == 0 && r < nr) {
+      a.stats[2 * ((int64_t)bh * a.T + t0 + r)] = mean;
+      a.stats[2 * ((int64_t)bh * a.T + t0 + r) + 1] = rstd;
+    }
   }
 }
 
-// Workgroup (time block tb, batch-head bh): rows bh T + 64 tb .. +63, wave w
-// taking every fourth.  Per-lane partial sums of the affine gradients are
-// combined across the waves in LDS and written as one partial row.
+// Workgroup = (batch-head bh, time block tb) as blockIdx.x = bh tblocks + tb:
+// rows 64 tb .. +63 of bh, wave w taking 16 consecutive ones in batches of
+// R.  Per-lane partial sums of the affine gradients are combined across the
+// waves in LDS and written as one partial row.
 template <typename T, int EPL>
 __global__ void __launch_bounds__(64 * kOgWaves) outgate_bwd_kernel(OgArgs a) {
+  constexpr int R = og_rows_bwd<T, EPL>(), RPW = kOgRowsPerWg / kOgWaves;
   __shared__ float sPart[kOgWaves][2][64 * EPL];
   const int w = wave_id(), l = lane_id();
-  const int tb = blockIdx.x, bh = blockIdx.y;
+  const int bh = blockIdx.x / a.tblocks, tb = blockIdx.x - bh * a.tblocks;
   const int V = a.V, h = bh % a.H, f0 = EPL * l;
-  const int esz = sizeof(T);
-  const uint32_t rb = (uint32_t)(V * esz);
-  const uint32_t off = f0 < V ? (uint32_t)(f0 * esz) : 0x80000000u;
-  bool in[EPL];
+  const bool lv = f0 < V;
+  constexpr uint32_t esz = sizeof(T);
+  const uint32_t rowb = (uint32_t)V * esz, off = lv ? (uint32_t)f0 * esz : 0x80000000u;
+  const int t0 = tb * kOgRowsPerWg + w * RPW, nr = max(0, min(RPW, a.T - t0));
   float wf[EPL], bf[EPL], pw[EPL], pb[EPL];
+  load_affine<EPL>(a, h, lv ? (uint32_t)f0 * 4u : 0x80000000u, wf, bf);
 #pragma unroll
-  for (int i = 0; i < EPL; ++i) {
-    in[i] = f0 + i < V;
-    wf[i] = (a.w && in[i]) ? a.w[h * V + f0 + i] : 1.f;
-    bf[i] = (a.b && in[i]) ? a.b[h * V + f0 + i] : 0.f;
-    pw[i] = pb[i] = 0.f;
-  }
-  const int t_end = min(a.T, kOgRowsPerWg * (tb + 1));
-  for (int t = kOgRowsPerWg * tb + w; t < t_end; t += kOgWaves) {
-    const int64_t base = ((int64_t)bh * a.T + t) * V;
-    float x[EPL], gg[EPL], dy[EPL];
-    og_load<T, EPL>(make_rsrc((const T *)a.o + base, rb), off, x);
-    og_load<T, EPL>(make_rsrc((const T *)a.g + base, rb), off, gg);
-    og_load<T, EPL>(make_rsrc((const T *)a.dy + base, rb), off, dy);
-    float mean, rstd;
-    row_stats<EPL>(x, in, V, a.eps, mean, rstd);
-    float xh[EPL], dxh[EPL], dg[EPL], s1 = 0.f, s2 = 0.f;
+  for (int i = 0; i < EPL; ++i) pw[i] = pb[i] = 0.f;
+  const int64_t base = ((int64_t)bh * a.T + t0) * V;
+  // (nr is wave-uniform; readfirstlane keeps the descriptors in SGPRs)
+  const uint32_t nb = __builtin_amdgcn_readfirstlane((uint32_t)nr * rowb);
+  const auto ro = make_rsrc((const T *)a.o + base, nb), rg = make_rsrc((const T *)a.g + base, nb);
+  const auto rdy = make_rsrc((const T *)a.dy + base, nb);
+  const auto rdo = make_rsrc((T *)a.d_o + base, nb), rdg = make_rsrc((T *)a.dg + base, nb);
+  for (int r0 = 0; r0 < nr; r0 += R) {
+    float x[R][EPL], gg[R][EPL], dy[R][EPL];
 #pragma unroll
-    for (int i = 0; i < EPL; ++i) {
-      xh[i] = in[i] ? (x[i] - mean) * rstd : 0.f;
-      const float sg = sigmoid(gg[i]);
-      const float r = gg[i] * sg;
-      const float ln = xh[i] * wf[i] + bf[i];
-      dg[i] = dy[i] * ln * (sg * (1.f + gg[i] * (1.f - sg)));  // d Swish(g) / dg
-      const float dln = dy[i] * r;
-      pw[i] += dln * xh[i];
-      pb[i] += dln;
-      dxh[i] = dln * wf[i];
-      s1 += dxh[i];
-      s2 += dxh[i] * xh[i];
+    for (int r = 0; r < R; ++r) og_load<T, EPL>(ro, off + (r0 + r) * rowb, x[r]);
+#pragma unroll
+    for (int r = 0; r < R; ++r) og_load<T, EPL>(rg, off + (r0 + r) * rowb, gg[r]);
+#pragma unroll
+    for (int r = 0; r < R; ++r) og_load<T, EPL>(rdy, off + (r0 + r) * rowb, dy[r]);
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      // rows past the tensor load as zeros and add nothing to pw, pb
+      float mean, rstd;
+      row_stats<EPL>(x[r], lv, a.inv_v, a.eps, mean, rstd);
+      float xh[EPL], dxh[EPL], dg[EPL], s1 = 0.f, s2 = 0.f;
+#pragma unroll
+      for (int i = 0; i < EPL; ++i) {
+        xh[i] = lv ? (x[r][i] - mean) * rstd : 0.f;
+        const float sg = sigmoid(gg[r][i]);
+        const float ln = xh[i] * wf[i] + bf[i];
+        dg[i] = dy[r][i] * ln * (sg * (1.f + gg[r][i] * (1.f - sg)));  // d Swish(g) / dg
+        const float dln = dy[r][i] * gg[r][i] * sg;
+        pw[i] += dln * xh[i];
+        pb[i] += dln;
+        dxh[i] = dln * wf[i];
+        s1 += dxh[i];
+        s2 += dxh[i] * xh[i];
+      }
+      const float m1 = wave_sum(s1) * a.inv_v, m2 = wave_sum(s2) * a.inv_v;
+      float d_o[EPL];
+#pragma unroll
+      for (int i = 0; i < EPL; ++i) d_o[i] = rstd * (dxh[i] - m1 - xh[i] * m2);
+      og_store<T, EPL>(rdo, off + (r0 + r) * rowb, d_o);
+      og_store<T, EPL>(rdg, off + (r0 + r) * rowb, dg);
     }
-    const float m1 = wave_sum(s1) / (float)V, m2 = wave_sum(s2) / (float)V;
-    float d_o[EPL];
-#pragma unroll
-    for (int i = 0; i < EPL; ++i) d_o[i] = rstd * (dxh[i] - m1 - xh[i] * m2);
-    og_store<T, EPL>(make_rsrc((T *)a.d_o + base, rb), off, d_o);
-    og_store<T, EPL>(make_rsrc((T *)a.dg + base, rb), off, dg);
   }
   if (!a.part) return;  // uniform: no affine gradients wanted
 #pragma unroll
@@ -208,7 +272,7 @@ __global__ void __launch_bounds__(64 * kOgWaves) outgate_bwd_kernel(OgArgs a) {
     sPart[w][1][f0 + i] = pb[i];
   }
   __syncthreads();
-  float *dst = a.part + ((int64_t)bh * a.tblocks + tb) * 2 * V;
+  float *dst = a.part + (int64_t)blockIdx.x * 2 * V;
   for (int e = threadIdx.x; e < 2 * V; e += 64 * kOgWaves) {
     const int c = e / V, f = e - c * V;
     float s = 0.f;
@@ -218,19 +282,43 @@ __global__ void __launch_bounds__(64 * kOgWaves) outgate_bwd_kernel(OgArgs a) {
   }
 }
 
-// dw[h][f], db[h][f] = sums of the partial rows of head h over batch rows and
-// time blocks, in a fixed order.
-__global__ void __launch_bounds__(256) outgate_affine_kernel(OgArgs a, int B) {
-  const int h = blockIdx.y, e = blockIdx.x * 256 + threadIdx.x;
-  if (e >= 2 * a.V) return;
-  float s = 0.f;
-  for (int b = 0; b < B; ++b) {
-    const float *p = a.part + ((int64_t)(b * a.H + h) * a.tblocks) * 2 * a.V + e;
-    for (int tb = 0; tb < a.tblocks; ++tb) s += p[(int64_t)tb * 2 * a.V];
+// dw[h][f], db[h][f] = sums of the B tblocks partial rows of head h.
+// Workgroup = (head h, 64 of the 2V columns) as blockIdx.x = h ncol + col;
+// wave w sums partial rows w, w + 16, ... eight loads at a time into four
+// accumulators, and the 16 wave sums are added in LDS: a fixed order, so the
+// result is reproducible.
+__global__ void __launch_bounds__(64 * kOgRedWaves) outgate_affine_kernel(OgArgs a, int B) {
+  __shared__ float sRed[kOgRedWaves][64];
+  const int ncol = (2 * a.V + 63) / 64;
+  const int h = blockIdx.x / ncol, e = (blockIdx.x - h * ncol) * 64 + lane_id(), w = wave_id();
+  const int P = B * a.tblocks, V2 = 2 * a.V;
+  auto ld = [&](int p) {
+    const int b = p / a.tblocks, tb = p - b * a.tblocks;
+    return a.part[(((int64_t)b * a.H + h) * a.tblocks + tb) * V2 + e];
+  };
+  float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+  if (e < V2) {
+    int p = w;
+    for (; p + 7 * kOgRedWaves < P; p += 8 * kOgRedWaves) {
+      float x[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) x[i] = ld(p + i * kOgRedWaves);
+      s0 += x[0] + x[4];
+      s1 += x[1] + x[5];
+      s2 += x[2] + x[6];
+      s3 += x[3] + x[7];
+    }
+    for (; p < P; p += kOgRedWaves) s0 += ld(p);
   }
+  sRed[w][lane_id()] = (s0 + s1) + (s2 + s3);
+  __syncthreads();
+  if (w != 0 || e >= V2) return;
+  float s = 0.f;
+#pragma unroll
+  for (int q = 0; q < kOgRedWaves; ++q) s += sRed[q][lane_id()];
   const int c = e / a.V, f = e - c * a.V;
   float *dst = c == 0 ? a.dw : a.db;
-  if (dst) dst[h * a.V + f] = s;
+  if (dst) dst[(int64_t)h * a.V + f] = s;
 }
 
 int og_epl(int V) {
@@ -239,29 +327,37 @@ int og_epl(int V) {
 }
 
 template <typename T, int EPL>
-hipError_t og_fwd_t(const OgArgs &a, hipStream_t st) {
-  hipLaunchKernelGGL((outgate_fwd_kernel<T, EPL>), dim3((a.rows + kOgWaves - 1) / kOgWaves), dim3(64 * kOgWaves),
-                     0, st, a);
+hipError_t og_fwd_t(OgArgs a, int B, hipStream_t st) {
+  a.tblocks = (a.T + kOgWaves * og_rows<T, EPL>() - 1) / (kOgWaves * og_rows<T, EPL>());
+  hipLaunchKernelGGL((outgate_fwd_kernel<T, EPL>), dim3((unsigned)((int64_t)B * a.H * a.tblocks)),
+                     dim3(64 * kOgWaves), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t og_affine(const OgArgs &a, int B, hipStream_t st) {
+  const int ncol = (2 * a.V + 63) / 64;
+  hipLaunchKernelGGL(outgate_affine_kernel, dim3((unsigned)((int64_t)a.H * ncol)), dim3(64 * kOgRedWaves), 0, st,
+                     a, B);
   return hipGetLastError();
 }
 
 template <typename T, int EPL>
 hipError_t og_bwd_t(const OgArgs &a, int B, hipStream_t st) {
-  hipLaunchKernelGGL((outgate_bwd_kernel<T, EPL>), dim3(a.tblocks, B * a.H), dim3(64 * kOgWaves), 0, st, a);
+  hipLaunchKernelGGL((outgate_bwd_kernel<T, EPL>), dim3((unsigned)((int64_t)B * a.H * a.tblocks)),
+                     dim3(64 * kOgWaves), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !a.part) return e;
-  hipLaunchKernelGGL(outgate_affine_kernel, dim3((2 * a.V + 255) / 256, a.H), dim3(256), 0, st, a, B);
-  return hipGetLastError();
+  return og_affine(a, B, st);
 }
 
 template <typename T>
 hipError_t og_dispatch(bool fwd, const OgArgs &a, int B, hipStream_t st) {
   switch (og_epl(a.V)) {
-    case 1: return fwd ? og_fwd_t<T, 1>(a, st) : og_bwd_t<T, 1>(a, B, st);
-    case 2: return fwd ? og_fwd_t<T, 2>(a, st) : og_bwd_t<T, 2>(a, B, st);
-    case 4: return fwd ? og_fwd_t<T, 4>(a, st) : og_bwd_t<T, 4>(a, B, st);
-    case 8: return fwd ? og_fwd_t<T, 8>(a, st) : og_bwd_t<T, 8>(a, B, st);
-    default: return fwd ? og_fwd_t<T, 16>(a, st) : og_bwd_t<T, 16>(a, B, st);
+    case 1: return fwd ? og_fwd_t<T, 1>(a, B, st) : og_bwd_t<T, 1>(a, B, st);
+    case 2: return fwd ? og_fwd_t<T, 2>(a, B, st) : og_bwd_t<T, 2>(a, B, st);
+    case 4: return fwd ? og_fwd_t<T, 4>(a, B, st) : og_bwd_t<T, 4>(a, B, st);
+    case 8: return fwd ? og_fwd_t<T, 8>(a, B, st) : og_bwd_t<T, 8>(a, B, st);
+    default: return fwd ? og_fwd_t<T, 16>(a, B, st) : og_bwd_t<T, 16>(a, B, st);
   }
 }
 
@@ -276,7 +372,7 @@ hipError_t launch_outgate_fwd(int B, int H, int T, int V, int io, const void *o,
                               const float *b, float eps, void *y, float *stats, hipStream_t st) {
   OgArgs a{};
   a.o = o; a.g = g; a.w = w; a.b = b; a.y = y; a.stats = stats;
-  a.H = H; a.T = T; a.V = V; a.rows = B * H * T; a.eps = eps;
+  a.H = H; a.T = T; a.V = V; a.eps = eps; a.inv_v = 1.f / (float)V;
   return io == IO_BF16 ? og_dispatch<bf16>(true, a, B, st) : og_dispatch<float>(true, a, B, st);
 }
 
@@ -286,13 +382,12 @@ hipError_t launch_outgate_bwd(int B, int H, int T, int V, int io, const void *o,
   OgArgs a{};
   a.o = o; a.g = g; a.w = w; a.b = b; a.dy = dy; a.d_o = d_o; a.dg = dg; a.dw = dw; a.db = db;
   a.part = (dw || db) ? part : nullptr;
-  a.H = H; a.T = T; a.V = V; a.rows = B * H * T; a.eps = eps;
+  a.H = H; a.T = T; a.V = V; a.eps = eps; a.inv_v = 1.f / (float)V;
   a.tblocks = (T + kOgRowsPerWg - 1) / kOgRowsPerWg;
-  if (a.rows == 0) {
+  if ((int64_t)B * H * T == 0) {
     // no rows: the affine gradients are sums over nothing
-    if (!a.part || H == 0) return hipSuccess;
-    hipLaunchKernelGGL(outgate_affine_kernel, dim3((2 * V + 255) / 256, H), dim3(256), 0, st, a, B);
-    return hipGetLastError();
+    if (!(dw || db) || H == 0) return hipSuccess;
+    return og_affine(a, B, st);  // reads no partials when there are none
   }
   return io == IO_BF16 ? og_dispatch<bf16>(false, a, B, st) : og_dispatch<float>(false, a, B, st);
 }
