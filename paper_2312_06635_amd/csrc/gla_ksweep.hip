@@ -509,11 +509,6 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
     __syncthreads();
 
     // ---- slabs: dP tiles, dq_inter partials (state before the chunk), update
-    frag_t<T> bh_[NST], bl_[NST];
-#pragma unroll
-    for (int st = 0; st < NST; ++st) {
-
-    }
     const float gam = sG[j];
     f16v acc[2], accP;
 #pragma unroll
