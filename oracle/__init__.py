@@ -180,3 +180,30 @@ def output_gate_bwd(o, g, dy, w=None, b=None, eps=1e-5):
     dxh = dln * wv[:, None, :]
     do = rstd * (dxh - dxh.mean(axis=-1, keepdims=True) - xh * (dxh * xh).mean(axis=-1, keepdims=True))
     return {"do": do, "dg": dg, "dw": dw, "db": db}
+
+
+# ---------------------------------------------------------------- scalar gates
+# Data-dependent scalar gates (Table 1: the Mamba-2, mLSTM and Gated Retention
+# rows, G_t = gamma_t 1^T 1): one decay per step and head, shared by every key
+# feature.  As a GLA layer this is alpha_t = gamma_t 1 (Sec. 4.1, Eq. 3), and
+# by the chain rule of that broadcast dL/dlog gamma_t = sum over the key
+# features of dL/dlog alpha_t.
+
+def _broadcast_gate(log_gamma, K):
+    lg = _as_f64(log_gamma)
+    return np.ascontiguousarray(np.broadcast_to(lg[..., None], lg.shape + (K,)))
+
+
+def scalar_gate_fwd(q, k, v, log_gamma, S0=None, want_state=True, nthreads=None):
+    """Forward recurrence with G_t = gamma_t 1^T 1; log_gamma: [..., T]."""
+    K = _as_f64(q).shape[-1]
+    return fwd(q, k, v, _broadcast_gate(log_gamma, K), S0, want_state=want_state, nthreads=nthreads)
+
+
+def scalar_gate_bwd(q, k, v, log_gamma, dO, S0=None, dST=None, nthreads=None, ckpt=64):
+    """Reverse mode of scalar_gate_fwd; returns dq, dk, dv, dS0 and
+    dlog_gamma ([..., T])."""
+    K = _as_f64(q).shape[-1]
+    g = bwd(q, k, v, _broadcast_gate(log_gamma, K), dO, S0=S0, dST=dST, nthreads=nthreads, ckpt=ckpt)
+    g["dlog_gamma"] = g.pop("dlog_alpha").sum(axis=-1)
+    return g

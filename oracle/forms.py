@@ -178,3 +178,24 @@ def chunk_bwd(q, k, v, log_alpha, dO, C, c, S0=None, dST=None):
         dS = gam[:, None] * dS + (qc * Lam).T @ dOc
     dla = dlog_alpha_closed_form(q, k, dq, dk, ST, dST)
     return {"dq": dq, "dk": dk, "dv": dv, "dlog_alpha": dla, "dS0": dS}
+
+
+def scalar_decay_attention(q, k, v, log_gamma, S0=None):
+    """Parallel form of linear attention with a data-dependent scalar decay
+    (the scalar-gate rows of Table 1, G_t = gamma_t 1^T 1): with
+    c_t = sum_{s <= t} log gamma_s, O = ((Q K^T) (.) D) V, D_ij = exp(c_i - c_j)
+    for i >= j, else 0; an initial state adds exp(c_i) q_i S0.  Also returns
+    the final state S_T = sum_s exp(c_T - c_s) k_s^T v_s + exp(c_T) S0."""
+    q, k, v, lg, S0 = map(_f64, (q, k, v, log_gamma, S0))
+    T = q.shape[0]
+    c = np.cumsum(lg)
+    i = np.arange(T)[:, None]
+    j = np.arange(T)[None, :]
+    D = np.where(i >= j, np.exp(np.where(i >= j, c[:, None] - c[None, :], 0.0)), 0.0)
+    o = ((q @ k.T) * D) @ v
+    cT = c[-1] if T else 0.0
+    ST = (k * np.exp(cT - c)[:, None]).T @ v
+    if S0 is not None:
+        o = o + np.exp(c)[:, None] * (q @ S0)
+        ST = ST + np.exp(cT) * S0
+    return o, ST

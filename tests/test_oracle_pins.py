@@ -371,3 +371,56 @@ def test_output_gate_gradients_match_central_finite_differences(affine):
                        - L(am["o"], am["g"], am.get("w"), am.get("b"))) / (2 * h)
         key = {"o": "do", "g": "dg", "w": "dw", "b": "db"}[name]
         assert rel(got[key], fd) < 1e-7, name
+
+
+# ---------------------------------------------------------------- scalar gates
+
+def _scalar_case(rng, T=23, K=5, V=4, mu=1.0):
+    q = rng.standard_normal((T, K))
+    k = rng.standard_normal((T, K)) / np.sqrt(K)
+    v = rng.standard_normal((T, V))
+    lg = -np.logaddexp(0.0, -(rng.standard_normal(T) + mu))  # log sigmoid, <= 0
+    S0 = rng.standard_normal((K, V)) * 0.3
+    return q, k, v, lg, S0
+
+
+def test_scalar_gate_equals_scalar_decay_attention():
+    rng = np.random.default_rng(51)
+    q, k, v, lg, S0 = _scalar_case(rng)
+    o, ST = oracle.scalar_gate_fwd(q, k, v, lg, S0, nthreads=1)
+    ro, rST = forms.scalar_decay_attention(q, k, v, lg, S0)
+    assert rel(o, ro) < 1e-12 and rel(ST, rST) < 1e-12
+    # a constant gamma is RetNet's decay mask
+    g = 0.83
+    o2, _ = oracle.scalar_gate_fwd(q, k, v, np.full(q.shape[0], np.log(g)), nthreads=1)
+    assert rel(o2, forms.decay_mask_attention(q, k, v, g)) < 1e-12
+    # batched leading dims are independent heads
+    qb = np.stack([q, 2.0 * q]); kb = np.stack([k, k]); vb = np.stack([v, -v]); lb = np.stack([lg, 0.5 * lg])
+    ob, _ = oracle.scalar_gate_fwd(qb, kb, vb, lb, nthreads=2)
+    assert rel(ob[1], forms.scalar_decay_attention(2.0 * q, k, -v, 0.5 * lg)[0]) < 1e-12
+
+
+def test_scalar_gate_gradients_match_central_finite_differences():
+    """Every gradient of L = sum(o dO) + sum(S_T dS_T) under scalar gates, by
+    central differences of the parallel form (which shares nothing with the
+    recurrence)."""
+    rng = np.random.default_rng(52)
+    q, k, v, lg, S0 = _scalar_case(rng, T=7, K=3, V=2)
+    dO = rng.standard_normal((7, 2))
+    dST = rng.standard_normal((3, 2))
+    g = oracle.scalar_gate_bwd(q, k, v, lg, dO, S0=S0, dST=dST, nthreads=1, ckpt=3)
+    args = {"q": q, "k": k, "v": v, "log_gamma": lg, "S0": S0}
+
+    def loss(a):
+        o, ST = forms.scalar_decay_attention(a["q"], a["k"], a["v"], a["log_gamma"], a["S0"])
+        return float((o * dO).sum() + (ST * dST).sum())
+
+    h = 1e-6
+    for name, gname in (("q", "dq"), ("k", "dk"), ("v", "dv"), ("log_gamma", "dlog_gamma"), ("S0", "dS0")):
+        fd = np.zeros_like(args[name])
+        for idx in np.ndindex(args[name].shape):
+            ap = {n: x.copy() for n, x in args.items()}; ap[name][idx] += h
+            am = {n: x.copy() for n, x in args.items()}; am[name][idx] -= h
+            fd[idx] = (loss(ap) - loss(am)) / (2 * h)
+        assert g[gname].shape == fd.shape, name
+        assert rel(g[gname], fd) < 1e-7, name
