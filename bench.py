@@ -43,12 +43,12 @@ STAGES = [("prep", "fwd", 1), ("fwd_main", "fwd", 2), ("bwd_dq", "bwd", 2), ("bw
 STAGES_OG = STAGES[:2] + [("og_fwd", "og", 0), ("og_bwd", "og", 1)] + STAGES[2:]
 
 
-def algorithmic(cfg, gate=True):
+def algorithmic(cfg, gate=True, scalar_gate=False):
     """Algorithmic FLOPs and HBM bytes per launch of each stage (and totals);
     gate=False is the alpha = 1 layer, which reads no gate tensor and writes no
-    gate gradient."""
+    gate gradient; scalar_gate has one gate value per step and head."""
     B, H, T, K, V, C = cfg["B"], cfg["H"], cfg["T"], cfg["dk"], cfg["dv"], cfg["chunk"]
-    ga = 1 if gate else 0
+    ga = (1.0 / K if scalar_gate else 1.0) if gate else 0.0  # gate elements per step, in units of K
     s = 2 if cfg["io"] == "bf16" else 4
     n = B * H * T                       # token-heads
     g = B * H * ((T + C - 1) // C) * K * 4  # chunk decays (fp32)
@@ -165,6 +165,8 @@ def main():
                     help="the alpha = 1 (ungated) layer: log_alpha passed as NULL")
     ap.add_argument("--gate-tau", type=float, default=0.0,
                     help="> 0: pass the gate pre-activation z (alpha = sigmoid(z)^(1/tau)) instead of log alpha")
+    ap.add_argument("--scalar-gate", action="store_true",
+                    help="one gate value per step and head (log gamma [B, H, T], Table 1's scalar gates)")
     ap.add_argument("--output-gate", action="store_true",
                     help="include the output side (per-head LN + Swish gate, Sec. 4.4) in the step")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -187,21 +189,29 @@ def main():
     torch.cuda.set_device(dev)
     inp_cpu = W.make_inputs(cfg, alpha_one=args.no_gate)
     d = {k: (v.to(dev) if v is not None else None) for k, v in inp_cpu.items()}
+    if args.scalar_gate:
+        # log gamma = logsigmoid(x) / 16 per (batch row, head, step), the
+        # per-feature recipe with one draw per step
+        gs = torch.Generator().manual_seed(cfg["seed"] + 5)
+        lg = torch.nn.functional.logsigmoid(torch.randn(cfg["B"], cfg["H"], cfg["T"], generator=gs)) / 16.0
+        inp_cpu["log_alpha"] = lg.to(inp_cpu["q"].dtype)
+        d["log_alpha"] = inp_cpu["log_alpha"].to(dev)
     if args.no_gate:
         d["log_alpha"] = None
     elif args.gate_tau > 0:
         # gate pre-activations; log alpha = logsigmoid(z) / tau is formed in the kernels
         gz = torch.Generator().manual_seed(cfg["seed"] + 7)
-        z = torch.randn(inp_cpu["log_alpha"].shape, generator=gz) * 2.0 + 1.0
+        z = torch.randn(inp_cpu["log_alpha"].shape, generator=gz) * 2.0 + 1.0  # [B, H, T] with --scalar-gate
         d["log_alpha"] = z.to(dtype=d["q"].dtype, device=dev)
         inp_cpu["log_alpha"] = torch.nn.functional.logsigmoid(z.double()).div(args.gate_tau).to(inp_cpu["q"].dtype)
     B, H, T, K, V, C, c = (cfg[x] for x in ("B", "H", "T", "dk", "dv", "chunk", "subchunk"))
     dt = d["q"].dtype
-    ws = torch.empty(gla.workspace_bytes(B, H, T, K, V, C, c, dt, op=1), dtype=torch.uint8, device=dev)
+    ws = torch.empty(gla.workspace_bytes(B, H, T, K, V, C, c, dt, op=1, scalar_gate=args.scalar_gate),
+                     dtype=torch.uint8, device=dev)
     o = torch.empty_like(d["v"])
     ST = torch.empty(B, H, K, V, dtype=torch.float32, device=dev) if cfg["want_state"] else None
     grads = {"dq": torch.empty_like(d["q"]), "dk": torch.empty_like(d["k"]), "dv": torch.empty_like(d["v"]),
-             "dlog_alpha": torch.empty_like(d["q"]) if d["log_alpha"] is not None else None,
+             "dlog_alpha": torch.empty_like(d["log_alpha"]) if d["log_alpha"] is not None else None,
              "dS0": torch.empty(B, H, K, V, dtype=torch.float32, device=dev) if d["S0"] is not None else None}
     stream = torch.cuda.current_stream(dev)
     stages = STAGES_OG if args.output_gate else STAGES
@@ -256,7 +266,7 @@ def main():
     for s in range(args.steps):
         for i, (nm, _, _) in enumerate(stages):
             stage_ms[nm] += evs[s][i].elapsed_time(evs[s][i + 1]) / args.steps
-    st_alg, fwd_flops, bwd_flops, io_bytes = algorithmic(cfg, gate=not args.no_gate)
+    st_alg, fwd_flops, bwd_flops, io_bytes = algorithmic(cfg, gate=not args.no_gate, scalar_gate=args.scalar_gate)
     if args.output_gate:
         io_bytes += st_alg["og_fwd"]["bytes"] + st_alg["og_bwd"]["bytes"]
     ms_per_step = 1e3 * elapsed / args.steps
@@ -278,7 +288,7 @@ def main():
 
     dom = max(stage_ms, key=stage_ms.get)
     roof = roofline(dom)
-    plain = not (args.no_gate or args.gate_tau > 0 or args.output_gate)
+    plain = not (args.no_gate or args.gate_tau > 0 or args.output_gate or args.scalar_gate)
     roof["traffic"] = measured_traffic(args.workload, dom) if plain else None
     roof["avg_ms"] = stage_ms[dom]
     stage_frac = {nm: f"{r['frac']:.3f} of {r['bound']}" for nm, r in ((nm, roofline(nm)) for nm in stage_ms)}
@@ -293,6 +303,7 @@ def main():
                    **({"gate": "none (alpha = 1, log_alpha NULL)"} if args.no_gate else {}),
                    **({"gate": f"pre-activation z, alpha = sigmoid(z)^(1/{args.gate_tau:g})"}
                       if args.gate_tau > 0 else {}),
+                   **({"gate_shape": "scalar per step and head, log gamma [B, H, T]"} if args.scalar_gate else {}),
                    **({"output_side": "per-head LN (affine) + Swish output gate, fwd + bwd"}
                       if args.output_gate else {})},
         "tflops": tflops, "mfma_peak_frac": tflops * 1e12 / peak,
@@ -301,7 +312,7 @@ def main():
         "stage_roofline_frac": stage_frac,
         "roofline": roof,
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not args.scalar_gate:
         out["cpu_baseline"] = cpu_baseline(cfg, inp_cpu)
     print(json.dumps(out), flush=True)
 

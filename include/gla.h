@@ -21,6 +21,7 @@
  *       S0, S_T, dS_T, dS0                  : [B, H, d_k, d_v] (fp32 always)
  *     and 16-byte aligned.  "Nullable" pointers may be NULL: an absent S0 or
  *     dS_T means zero, an absent S_T or dS0 means "not wanted".
+ *     With GLA_FLAG_SCALAR_GATE, log_alpha and dlog_alpha are [B, H, T].
  *   - log_alpha is nullable everywhere: NULL means alpha = 1 for every t and
  *     feature, i.e. ungated linear attention (the alpha = 1 case that the
  *     paper's FLA algorithms of Sec. 3.3 and App. A compute).  No gate tensor
@@ -77,6 +78,16 @@ enum {
    * the backward skips recomputing them (paper, Sec. 3.3: materialize once
    * vs. recompute). */
   GLA_FLAG_REUSE_FWD_WORKSPACE = 1u << 0,
+  /* Data-dependent scalar gates (Table 1: the Mamba-2, mLSTM and Gated
+   * Retention rows, G_t = gamma_t 1^T 1): log_alpha holds one log gamma per
+   * step and head, [B, H, T] (io dtype), shared by every key feature, i.e.
+   * alpha_t = gamma_t 1; the backward's dlog_alpha is then [B, H, T] too, the
+   * sum over the key features of the per-feature gate gradient (summed in a
+   * fixed order: reproducible bits).  Combines with gate_tau (z then [B, H, T]:
+   * gamma = sigmoid(z)^(1/tau), Gated Retention; tau = 1, mLSTM).  Every entry
+   * point honours it, gla_workspace_bytes included (the backward then needs
+   * B H ceil(d_k/32) T fp32 more). */
+  GLA_FLAG_SCALAR_GATE = 1u << 1,
   /* Bits 8..11 select a single stage of an entry point's launch sequence (0 =
    * the whole sequence), so that a profiler or benchmark can time each kernel
    * on its own stream with events.  Running the stages 1, 2, ... in order with

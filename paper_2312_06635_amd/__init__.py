@@ -20,7 +20,7 @@ import torch
 __all__ = [
     "chunk_fwd", "chunk_bwd", "recurrent_fwd", "workspace_bytes", "GlaError", "library_path",
     "GLA_OK", "GLA_ERR_NULL", "GLA_ERR_SHAPE", "GLA_ERR_DTYPE", "GLA_ERR_UNSUPPORTED",
-    "GLA_ERR_WORKSPACE", "GLA_ERR_HIP", "FLAG_REUSE_FWD_WORKSPACE", "GlaProblem", "lib",
+    "GLA_ERR_WORKSPACE", "GLA_ERR_HIP", "FLAG_REUSE_FWD_WORKSPACE", "FLAG_SCALAR_GATE", "GlaProblem", "lib",
     "output_gate_fwd", "output_gate_bwd", "output_gate_workspace_bytes",
 ]
 
@@ -31,6 +31,7 @@ GLA_OK, GLA_ERR_NULL, GLA_ERR_SHAPE, GLA_ERR_DTYPE = 0, 1, 2, 3
 GLA_ERR_UNSUPPORTED, GLA_ERR_WORKSPACE, GLA_ERR_HIP = 4, 5, 6
 GLA_F32, GLA_BF16 = 0, 1
 FLAG_REUSE_FWD_WORKSPACE = 1
+FLAG_SCALAR_GATE = 2
 STAGE_SHIFT = 8
 
 
@@ -89,8 +90,11 @@ def _io_code(dt: torch.dtype) -> int:
     raise TypeError(f"unsupported dtype {dt}; use torch.bfloat16 or torch.float32")
 
 
-def _problem(q, v, chunk, subchunk, flags=0, gate_tau=0.0) -> GlaProblem:
+def _problem(q, v, chunk, subchunk, flags=0, gate_tau=0.0, la=None) -> GlaProblem:
+    """la: the gate tensor; a [B, H, T] one selects scalar gates."""
     B, H, T, dk = q.shape
+    if la is not None and la.dim() == 3:
+        flags |= FLAG_SCALAR_GATE
     return GlaProblem(B, H, T, dk, v.shape[-1], chunk, subchunk, _io_code(q.dtype), flags, float(gate_tau))
 
 
@@ -105,11 +109,17 @@ def _check(q, k, v, la, extra=(), states=()):
     dev = q.device
     if dev.type != "cuda":
         raise ValueError("tensors must be on a HIP device")
-    gate = (("log_alpha", la, dk),) if la is not None else ()
+    if la is not None and la.dim() == 3:
+        # scalar gate: one value per step and head
+        if tuple(la.shape) != (B, H, T) or la.device != dev or la.dtype != q.dtype or not la.is_contiguous():
+            raise ValueError(f"a scalar log_alpha must be a contiguous {q.dtype} [B, H, T] tensor on {dev}")
+        gate = ()
+    else:
+        gate = (("log_alpha", la, dk),) if la is not None else ()
     for name, t, last in (("k", k, dk),) + gate + (("v", v, None),) + tuple(extra):
         if t.device != dev or t.dtype != q.dtype or not t.is_contiguous():
             raise ValueError(f"{name} must be a contiguous {q.dtype} tensor on {dev}")
-        if t.shape[:3] != (B, H, T) or (last is not None and t.shape[3] != last):
+        if t.dim() != 4 or t.shape[:3] != (B, H, T) or (last is not None and t.shape[3] != last):
             raise ValueError(f"{name} has shape {tuple(t.shape)}")
     if not q.is_contiguous():
         raise ValueError("q must be contiguous")
@@ -126,9 +136,10 @@ def _stream(dev):
     return torch.cuda.current_stream(dev).cuda_stream
 
 
-def workspace_bytes(B, H, T, dk, dv, chunk, subchunk, dtype=torch.bfloat16, op=1) -> int:
-    """Workspace bytes for the forward (op=0) or backward (op=1)."""
-    p = GlaProblem(B, H, T, dk, dv, chunk, subchunk, _io_code(dtype), 0)
+def workspace_bytes(B, H, T, dk, dv, chunk, subchunk, dtype=torch.bfloat16, op=1, scalar_gate=False) -> int:
+    """Workspace bytes for the forward (op=0) or backward (op=1); scalar_gate
+    for a [B, H, T] gate."""
+    p = GlaProblem(B, H, T, dk, dv, chunk, subchunk, _io_code(dtype), FLAG_SCALAR_GATE if scalar_gate else 0)
     return int(lib().gla_workspace_bytes(ctypes.byref(p), op))
 
 
@@ -146,14 +157,15 @@ def chunk_fwd(q, k, v, log_alpha, chunk=64, subchunk=16, S0=None, output_final_s
     """Chunkwise GLA forward.  Returns (o, S_T or None).
 
     log_alpha=None means alpha = 1 (ungated linear attention): no gate tensor
-    is read.  gate_tau > 0 means log_alpha holds the gate pre-activation z of
+    is read.  A [B, H, T] log_alpha is a scalar gate per step and head (alpha_t =
+    gamma_t 1, the scalar-gate rows of Table 1).  gate_tau > 0 means log_alpha holds the gate pre-activation z of
     alpha = sigmoid(z)^(1/gate_tau) (the GLA gate).  stage selects one kernel of the launch sequence (see
     GLA_STAGE_* in include/gla.h); out=(o, S_T) reuses caller-provided output
     tensors."""
     _check(q, k, v, log_alpha, states=(("S0", S0),))
     B, H, T, dk = q.shape
     dv = v.shape[3]
-    p = _problem(q, v, chunk, subchunk, stage << STAGE_SHIFT, gate_tau)
+    p = _problem(q, v, chunk, subchunk, stage << STAGE_SHIFT, gate_tau, log_alpha)
     if out is not None:
         o, ST = out
     else:
@@ -174,7 +186,8 @@ def chunk_bwd(q, k, v, log_alpha, dO, chunk=64, subchunk=16, S0=None, dST=None,
     """Chunkwise GLA backward for L = sum(o * dO) + sum(S_T * dS_T).
 
     Returns dict(dq, dk, dv, dlog_alpha, dS0); dlog_alpha is None when
-    log_alpha is None (alpha = 1, no gate gradient), and dL/dz when gate_tau > 0
+    log_alpha is None (alpha = 1, no gate gradient), shaped like log_alpha
+    ([B, H, T] for a scalar gate), and dL/dz when gate_tau > 0
     (log_alpha then holds the gate pre-activation z).  With reuse_fwd_workspace the
     given workspace must still hold what chunk_fwd left for the same inputs.
     stage and out as in chunk_fwd (out is a dict shaped like the result)."""
@@ -182,7 +195,7 @@ def chunk_bwd(q, k, v, log_alpha, dO, chunk=64, subchunk=16, S0=None, dST=None,
     B, H, T, dk = q.shape
     dv = v.shape[3]
     flags = (FLAG_REUSE_FWD_WORKSPACE if reuse_fwd_workspace else 0) | (stage << STAGE_SHIFT)
-    p = _problem(q, v, chunk, subchunk, flags, gate_tau)
+    p = _problem(q, v, chunk, subchunk, flags, gate_tau, log_alpha)
     if reuse_fwd_workspace and workspace is None:
         raise ValueError("reuse_fwd_workspace needs the workspace the forward used")
     if out is not None:
@@ -209,7 +222,7 @@ def recurrent_fwd(q, k, v, log_alpha, S0=None, output_final_state=False, gate_ta
     _check(q, k, v, log_alpha, states=(("S0", S0),))
     B, H, T, dk = q.shape
     dv = v.shape[3]
-    p = _problem(q, v, 16, 16, 0, gate_tau)
+    p = _problem(q, v, 16, 16, 0, gate_tau, log_alpha)
     o = torch.empty_like(v)
     ST = torch.empty(B, H, dk, dv, dtype=torch.float32, device=q.device) if output_final_state else None
     st = lib().gla_recurrent_fwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha),

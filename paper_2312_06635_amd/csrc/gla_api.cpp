@@ -41,6 +41,7 @@ gla_status make_shape(const gla_problem *p, Shape &s) {
   // gate_tau: 0 (the gate argument is log alpha) or a finite tau > 0
   if (!(p->gate_tau == 0.f || (p->gate_tau > 0.f && p->gate_tau < 3.0e38f))) return GLA_ERR_SHAPE;
   s.inv_tau = p->gate_tau == 0.f ? 0.f : 1.f / p->gate_tau;
+  s.sgate = (p->flags & GLA_FLAG_SCALAR_GATE) != 0;
   if (s.N > 65535) return GLA_ERR_UNSUPPORTED;
   // one head's rows of any tensor must span less than 2 GiB (32-bit buffer offsets)
   const int64_t wmax = p->dk > p->dv ? p->dk : p->dv;
@@ -74,15 +75,16 @@ size_t layout(const Shape &s, int op, char *base, Work *w) {
   void *P = take(chunks * s.C * s.C * es);
   void *gam = take(chunks * s.K * sizeof(float));
   void *wflag = take(chunks * 4);
-  void *dP = nullptr, *cST = nullptr, *dq_lo = nullptr;
+  void *dP = nullptr, *cST = nullptr, *dq_lo = nullptr, *dla_part = nullptr;
   if (op == 1) {
     dP = take(chunks * s.C * s.C * sizeof(float));
     cST = take((size_t)s.BH * s.K * sizeof(float));
     if (s.io == gla::IO_BF16) dq_lo = take(rows * s.K * 2);
+    if (s.sgate) dla_part = take(rows * ((s.K + 31) / 32) * sizeof(float));
   }
   if (w) {
     w->Qt = Qt; w->Kt = Kt; w->P = P; w->gam = (float *)gam; w->wflag = (unsigned char *)wflag;
-    w->dP = (float *)dP; w->cST = (float *)cST; w->dq_lo = dq_lo;
+    w->dP = (float *)dP; w->cST = (float *)cST; w->dq_lo = dq_lo; w->dla_part = (float *)dla_part;
   }
   return off;
 }
@@ -117,6 +119,7 @@ GLA_EXPORT gla_status gla_chunk_fwd(const gla_problem *prob, const void *q, cons
   Shape s;
   gla_status st = make_shape(prob, s);
   if (st != GLA_OK) return st;
+  if (!log_alpha) s.inv_tau = 0.f;  // no gate: alpha = 1 whatever gate_tau says
   if ((st = check_lds(s, false)) != GLA_OK) return st;
   const unsigned stage = (prob->flags & GLA_STAGE_MASK) >> GLA_STAGE_SHIFT;
   if (stage > 2) return GLA_ERR_SHAPE;
@@ -144,6 +147,7 @@ GLA_EXPORT gla_status gla_chunk_bwd(const gla_problem *prob, const void *q, cons
   Shape s;
   gla_status st = make_shape(prob, s);
   if (st != GLA_OK) return st;
+  if (!log_alpha) s.inv_tau = 0.f;  // no gate: alpha = 1 whatever gate_tau says
   if ((st = check_lds(s, true)) != GLA_OK) return st;
   const unsigned stage = (prob->flags & GLA_STAGE_MASK) >> GLA_STAGE_SHIFT;
   if (stage > 4) return GLA_ERR_SHAPE;
@@ -178,6 +182,7 @@ GLA_EXPORT gla_status gla_recurrent_fwd(const gla_problem *prob, const void *q, 
   Shape s;
   gla_status st = make_shape(&p, s);
   if (st != GLA_OK) return st;
+  if (!log_alpha) s.inv_tau = 0.f;  // no gate: alpha = 1 whatever gate_tau says
   const bool any = (int64_t)s.BH * s.T > 0;
   if (any && (!q || !k || !v || !o)) return GLA_ERR_NULL;
   hipStream_t hs = (hipStream_t)stream;

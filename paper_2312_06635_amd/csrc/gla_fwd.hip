@@ -15,6 +15,7 @@ struct RecArgs {
   void *o;
   float *ST;
   int T, K, V;
+  int sg;         // scalar gate: la is [BH][T], one value per step shared by every feature
   float inv_tau;  // gate epilogue (0: la holds log alpha)
 };
 
@@ -32,13 +33,14 @@ __global__ void __launch_bounds__(256) recurrent_kernel(RecArgs a) {
     S[i] = (a.S0 && i < KQ && kr < K && colv) ? a.S0[((int64_t)bh * K + kr) * V + col] : 0.f;
   }
   const T *q = (const T *)a.q + (int64_t)bh * a.T * K, *k = (const T *)a.k + (int64_t)bh * a.T * K;
-  const T *la = (const T *)a.la + (int64_t)bh * a.T * K, *v = (const T *)a.v + (int64_t)bh * a.T * V;
+  const int lrow = a.sg ? 1 : K, lf = a.sg ? 0 : 1;  // gate elements per step, per feature
+  const T *la = (const T *)a.la + (int64_t)bh * a.T * lrow, *v = (const T *)a.v + (int64_t)bh * a.T * V;
   T *o = (T *)a.o + (int64_t)bh * a.T * V;
   for (int t = 0; t < a.T; ++t) {
     for (int i = tid; i < K; i += 256) {
       sq[i] = (float)q[(int64_t)t * K + i];
       sk[i] = (float)k[(int64_t)t * K + i];
-      sa[i] = a.la ? __expf(gate_la((float)la[(int64_t)t * K + i], a.inv_tau, true)) : 1.f;  // no gate: alpha = 1
+      sa[i] = a.la ? __expf(gate_la((float)la[(int64_t)t * lrow + i * lf], a.inv_tau, true)) : 1.f;  // no gate: alpha = 1
     }
     const float vt = colv ? (float)v[(int64_t)t * V + col] : 0.f;
     __syncthreads();
@@ -66,7 +68,7 @@ __global__ void __launch_bounds__(256) recurrent_kernel(RecArgs a) {
 
 hipError_t launch_recurrent(const Shape &s, const void *q, const void *k, const void *v,
                             const void *la, const float *S0, void *o, float *ST, hipStream_t st) {
-  RecArgs a{q, k, v, la, S0, o, ST, s.T, s.K, s.V, s.inv_tau};
+  RecArgs a{q, k, v, la, S0, o, ST, s.T, s.K, s.V, s.sgate ? 1 : 0, s.inv_tau};
   dim3 grid((s.V + 63) / 64, s.BH);
   if (s.io == IO_BF16)
     hipLaunchKernelGGL(recurrent_kernel<bf16>, grid, dim3(256), 0, st, a);

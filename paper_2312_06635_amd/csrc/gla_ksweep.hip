@@ -56,7 +56,9 @@ struct KsArgs {
   const float *S0, *dST;
   void *dq, *dq_lo, *dk, *dla;
   float *dP, *cST;
+  float *dla_part;  // scalar gate: [BH][KT][T] per-tile feature sums of the gate gradient
   int BH, T, K, V, C, N, KT;
+  int sg;         // scalar gate: la is [BH][T], one value per step shared by every feature
   float inv_tau;  // gate epilogue (0: la holds log alpha)
 };
 
@@ -264,6 +266,23 @@ template <typename T> __device__ __forceinline__ void st_elem(__amdgpu_buffer_rs
     __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned int, v), rs, off, 0, 0);
 }
 
+// Byte offset of the i-th of a thread's four gate elements: the element's own
+// offset `eoff` (per-feature gate), or the row's single value (scalar gate)
+// at `sbase` + i elements, sbase = the thread's first row, or out of range for
+// masked threads.
+template <typename T> __device__ __forceinline__ uint32_t gate_off(int sg, uint32_t eoff, uint32_t sbase, int i) {
+  return sg ? sbase + (uint32_t)(i * (int)sizeof(T)) : eoff;
+}
+
+// Sum over the 32 lanes of each half wave (every lane gets its half's sum).
+__device__ __forceinline__ float half_wave_sum(float x) {
+  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0xB1, 0xF, 0xF, false));
+  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x4E, 0xF, 0xF, false));
+  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x141, 0xF, 0xF, false));
+  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x140, 0xF, 0xF, false));
+  return x + __shfl_xor(x, 16);
+}
+
 // ------------------------------------------------------------- gate factors
 // Cumulative-sum bookkeeping of one factor thread (feature fk, rows 4 frg ..
 // +3 of the chunk), from the chunk's row-group totals in LDS.
@@ -412,7 +431,8 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
     }
 
   // ---- input streams
-  const T *kh_ = (const T *)a.k + (int64_t)bh * a.T * K, *lah = (const T *)a.la + (int64_t)bh * a.T * K;
+  const int lrow = a.sg ? 1 : K;  // gate elements per step
+  const T *kh_ = (const T *)a.k + (int64_t)bh * a.T * K, *lah = (const T *)a.la + (int64_t)bh * a.T * lrow;
   const T *vh = (const T *)a.v + (int64_t)bh * a.T * V, *dOh = (const T *)a.dO + (int64_t)bh * a.T * V;
   uint32_t eoff[4];
 #pragma unroll
@@ -420,16 +440,19 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
     const int row = 4 * frg + i;
     eoff[i] = (fthr && row < C && fv) ? (uint32_t)((row * K + kf) * esz) : 0x80000000u;
   }
+  // (C is a multiple of 4: a thread's four rows are all inside or all outside)
+  const uint32_t sbase = (fthr && 4 * frg < C && fv) ? (uint32_t)(4 * frg * esz) : 0x80000000u;
   uint32_t fin_la[4], fin_k[4];
   auto fetch_factors = [&](int n) {
     const int t0 = n * C;
     const uint32_t bytes = rsrc_bytes((int64_t)(a.T - t0) * K * esz);
     // an absent gate (alpha = 1) reads as log alpha = 0 from an empty range
-    const auto rs_la = make_rsrc(a.la ? lah + (int64_t)t0 * K : kh_, a.la ? bytes : 0u);
+    const auto rs_la = make_rsrc(a.la ? lah + (int64_t)t0 * lrow : kh_,
+                                 a.la ? rsrc_bytes((int64_t)(a.T - t0) * lrow * esz) : 0u);
     const auto rs_k = make_rsrc(kh_ + (int64_t)t0 * K, bytes);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      fin_la[i] = ld_elem<T>(rs_la, eoff[i]);
+      fin_la[i] = ld_elem<T>(rs_la, gate_off<T>(a.sg, eoff[i], sbase, i));
       fin_k[i] = ld_elem<T>(rs_k, eoff[i]);
     }
   };
@@ -718,7 +741,8 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
     }
 
   const T *qh_ = (const T *)a.q + (int64_t)bh * a.T * K, *kh_ = (const T *)a.k + (int64_t)bh * a.T * K;
-  const T *lah = (const T *)a.la + (int64_t)bh * a.T * K;
+  const int lrow = a.sg ? 1 : K;  // gate elements per step
+  const T *lah = (const T *)a.la + (int64_t)bh * a.T * lrow;
   const T *dqh = (const T *)a.dq_in + (int64_t)bh * a.T * K;
   const T *dqlh = SPLIT ? (const T *)a.dq_lo_in + (int64_t)bh * a.T * K : dqh;
   const T *vh = (const T *)a.v + (int64_t)bh * a.T * V, *dOh = (const T *)a.dO + (int64_t)bh * a.T * V;
@@ -729,6 +753,8 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
     const int row = 4 * frg + i;
     eoff[i] = (fthr && row < C && fv) ? (uint32_t)((row * K + kf) * esz) : 0x80000000u;
   }
+  // (C is a multiple of 4: a thread's four rows are all inside or all outside)
+  const uint32_t sbase = (fthr && 4 * frg < C && fv) ? (uint32_t)(4 * frg * esz) : 0x80000000u;
   uint32_t fin_la[4], fin_q[4], fin_k[4], fin_dq[4], fin_dql[4];
   TileLd<float, CP, CP, kKT> pp;
   pp.init(C, C, C);
@@ -736,14 +762,15 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
     const int t0 = n * C;
     const uint32_t bytes = rsrc_bytes((int64_t)(a.T - t0) * K * esz);
     // an absent gate (alpha = 1) reads as log alpha = 0 from an empty range
-    const auto rs_la = make_rsrc(a.la ? lah + (int64_t)t0 * K : kh_, a.la ? bytes : 0u);
+    const auto rs_la = make_rsrc(a.la ? lah + (int64_t)t0 * lrow : kh_,
+                                 a.la ? rsrc_bytes((int64_t)(a.T - t0) * lrow * esz) : 0u);
     const auto rs_q = make_rsrc(qh_ + (int64_t)t0 * K, bytes);
     const auto rs_k = make_rsrc(kh_ + (int64_t)t0 * K, bytes);
     const auto rs_dq = make_rsrc(dqh + (int64_t)t0 * K, bytes);
     const auto rs_dql = make_rsrc(dqlh + (int64_t)t0 * K, bytes);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      fin_la[i] = ld_elem<T>(rs_la, eoff[i]);
+      fin_la[i] = ld_elem<T>(rs_la, gate_off<T>(a.sg, eoff[i], sbase, i));
       fin_q[i] = ld_elem<T>(rs_q, eoff[i]);
       fin_k[i] = ld_elem<T>(rs_k, eoff[i]);
       fin_dq[i] = ld_elem<T>(rs_dq, eoff[i]);
@@ -942,18 +969,54 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
           if (p + e > frg) later += v[e];
         }
       }
-      // an absent gate gradient is dropped through an empty range
-      const auto rs_dla = make_rsrc(a.dla ? dlao + (int64_t)t0 * K : dko, a.dla ? rsrc_bytes((int64_t)(a.T - t0) * K * esz) : 0u);
 #pragma unroll
       for (int i = 0; i < 4; ++i) dA[i] += later;
-      if constexpr (PRE) {  // gate epilogue: dL/dz = dL/dlog alpha * sigmoid(-z) / tau
+      if (a.sg) {
+        // scalar gate: this tile's sum over its features, per row (rows past
+        // the sequence end fall outside the range); the key tiles are added,
+        // and the gate epilogue's chain rule applied, by sgate_dla_kernel
+        if (a.dla) {
+          float r[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) dA[i] *= gate_dla_dg(zc[i], a.inv_tau);
+          for (int i = 0; i < 4; ++i) r[i] = half_wave_sum(fv ? dA[i] : 0.f);
+          if (fk == 0) {
+            const auto rs_p = make_rsrc(a.dla_part + ((int64_t)bh * a.KT + kt) * a.T + t0,
+                                        rsrc_bytes((int64_t)(a.T - t0) * 4));
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, r[i]), rs_p,
+                                                    (uint32_t)((4 * frg + i) * 4), 0, 0);
+          }
+        }
+      } else {
+        // an absent gate gradient is dropped through an empty range
+        const auto rs_dla = make_rsrc(a.dla ? dlao + (int64_t)t0 * K : dko,
+                                      a.dla ? rsrc_bytes((int64_t)(a.T - t0) * K * esz) : 0u);
+        if constexpr (PRE) {  // gate epilogue: dL/dz = dL/dlog alpha * sigmoid(-z) / tau
+#pragma unroll
+          for (int i = 0; i < 4; ++i) dA[i] *= gate_dla_dg(zc[i], a.inv_tau);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) st_elem<T>(rs_dla, eoff[i], cvt<T>(dA[i]));
       }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) st_elem<T>(rs_dla, eoff[i], cvt<T>(dA[i]));
       if (frg == 0) sCar[((it + 1) & 1) * kKF + fk] = all;
     }
+  }
+}
+
+// Scalar gate: dlog gamma[bh][t] = sum over the key tiles of the per-tile
+// feature sums, in tile order; with the gate epilogue, times
+// sigmoid(-z) / tau of the scalar pre-activation z.
+template <typename T>
+__global__ void __launch_bounds__(256) sgate_dla_kernel(const float *part, const void *z, void *dla, int64_t n,
+                                                        int steps, int KT, float inv_tau) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+    const int64_t bh = i / steps, t = i - bh * steps;
+    const float *p = part + bh * KT * steps + t;
+    float s = 0.f;
+    for (int kt = 0; kt < KT; ++kt) s += p[(int64_t)kt * steps];
+    if (inv_tau != 0.f) s *= gate_dla_dg((float)((const T *)z)[i], inv_tau);
+    ((T *)dla)[i] = cvt<T>(s);
   }
 }
 
@@ -977,6 +1040,7 @@ KsArgs ks_args(const Shape &s) {
   KsArgs a{};
   a.BH = s.BH; a.T = s.T; a.K = s.K; a.V = s.V; a.C = s.C; a.N = s.N;
   a.inv_tau = s.inv_tau;
+  a.sg = s.sgate ? 1 : 0;
   a.KT = (s.K + kKF - 1) / kKF;
   return a;
 }
@@ -1045,8 +1109,18 @@ hipError_t launch_bwd_dk(const Shape &s, const void *q, const void *k, const voi
                          void *dk, void *dla, const Work &w, hipStream_t st) {
   KsArgs a = ks_args(s);
   a.q = q; a.k = k; a.la = la; a.v = v; a.dO = dO; a.dST = dST; a.dq_in = dq; a.dq_lo_in = w.dq_lo;
-  a.dk = dk; a.dla = dla; a.dP = w.dP; a.cST = dST ? w.cST : nullptr;
-  return dispatch_ks<false>(s, a, st);
+  a.dk = dk; a.dla = dla; a.dP = w.dP; a.cST = dST ? w.cST : nullptr; a.dla_part = w.dla_part;
+  hipError_t e = dispatch_ks<false>(s, a, st);
+  if (e != hipSuccess || !s.sgate || !dla) return e;
+  const int64_t n = (int64_t)s.BH * s.T;
+  const int blocks = (int)((n + 255) / 256 < 8192 ? (n + 255) / 256 : 8192);
+  if (s.io == IO_BF16)
+    hipLaunchKernelGGL(sgate_dla_kernel<bf16>, dim3(blocks), dim3(256), 0, st, w.dla_part, la, dla, n, s.T, a.KT,
+                       s.inv_tau);
+  else
+    hipLaunchKernelGGL(sgate_dla_kernel<float>, dim3(blocks), dim3(256), 0, st, w.dla_part, la, dla, n, s.T, a.KT,
+                       s.inv_tau);
+  return hipGetLastError();
 }
 
 }  // namespace gla

@@ -13,7 +13,9 @@ struct Shape {
   int BH, T, K, V, C, c, N;
   int io;
   float inv_tau;  // 0: the gate argument is log alpha; else 1 / tau of the gate epilogue
+  bool sgate;     // scalar gate: one gate value per (head, step), [BH][T]
   int esz() const { return io == IO_BF16 ? 2 : 4; }
+  int la_row() const { return sgate ? 1 : K; }  // gate elements per step
 };
 
 // Device workspace regions (see gla_api.cpp for the layout).
@@ -27,6 +29,8 @@ struct Work {
   float *cST = nullptr;   // [BH][K] fp32 : rowsum(S_T (.) dS_T) (backward)
   void *dq_lo = nullptr;  // [BH][T][K] bf16 : dq - bf16(dq), so dq reaches the gate gradient
                           //   with ~16 mantissa bits (bf16 io only)
+  float *dla_part = nullptr;  // [BH][ceil(K/32)][T] fp32 : per key tile sums of the gate
+                              //   gradient over its features (scalar gate only)
 };
 
 // Returns hipSuccess or the launch error.  Shapes are validated by the caller.

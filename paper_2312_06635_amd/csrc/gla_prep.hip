@@ -35,6 +35,7 @@ struct PrepArgs {
   float *gam;
   unsigned char *wflag;  // [BH][N][4]: diagonal block needs pairwise decays
   int T, K, Kp, C, N, ldk;
+  int sg;         // scalar gate: la is [BH][T], one value per step shared by every feature
   float inv_tau;  // gate epilogue (0: la holds log alpha)
 };
 
@@ -152,7 +153,8 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
   float *sG = sTot + 4 * Kp;              // [3][Kp] exp(sum of tot strictly between I and J)
   float *sEup = sG + 3 * Kp;              // [nb][Kp] exp(-tot): pink operand scale
 
-  const T *q = (const T *)a.q + base, *k = (const T *)a.k + base, *la = (const T *)a.la + base;
+  const T *q = (const T *)a.q + base, *k = (const T *)a.k + base;
+  const T *la = (const T *)a.la + (a.sg ? (int64_t)bh * a.T + t0 : base);
   T *Qt = (T *)a.Qt + base, *Kt = (T *)a.Kt + base;
   T *Pg = (T *)a.P + ((int64_t)bh * a.N + n) * C * C;
   // lane l owns the FPL consecutive features k0 .. k0 + FPL - 1
@@ -166,12 +168,33 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
   const int esz = sizeof(T);
   const uint32_t bytes = rsrc_bytes((int64_t)(a.T - t0) * K * esz);
   // an absent gate (alpha = 1) reads as log alpha = 0 from an empty range
-  const auto rs_la = make_rsrc(a.la ? la : q, a.la ? bytes : 0u), rs_q = make_rsrc(q, bytes), rs_k = make_rsrc(k, bytes);
+  const uint32_t la_bytes = a.sg ? rsrc_bytes((int64_t)(a.T - t0) * esz) : bytes;
+  const auto rs_la = make_rsrc(a.la ? la : q, a.la ? la_bytes : 0u), rs_q = make_rsrc(q, bytes), rs_k = make_rsrc(k, bytes);
   const uint32_t lane_off = fv ? (uint32_t)((16 * w * K + k0) * esz) : 0x80000000u;
   const uint32_t row_step = (uint32_t)(K * esz);
   uint32_t rla[16][NW], rq[16][NW], rk[16][NW];
+  if (a.sg) {
+    // scalar gate: the row's one value, broadcast to the features when unpacked
+    const uint32_t o1 = fv ? (uint32_t)(16 * w * esz) : 0x80000000u;
 #pragma unroll
-  for (int r = 0; r < 16; ++r) ldraw<T, FPL>(rs_la, lane_off + r * row_step, rla[r]);
+    for (int r = 0; r < 16; ++r) {
+      if constexpr (sizeof(T) == 2) rla[r][0] = __builtin_amdgcn_raw_buffer_load_b16(rs_la, o1 + r * esz, 0, 0);
+      else rla[r][0] = __builtin_amdgcn_raw_buffer_load_b32(rs_la, o1 + r * esz, 0, 0);
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) ldraw<T, FPL>(rs_la, lane_off + r * row_step, rla[r]);
+  }
+  auto unpack_la = [&](int r, float (&x)[FPL]) {
+    if (a.sg) {
+      const float e = sizeof(T) == 2 ? __builtin_bit_cast(float, (rla[r][0] & 0xFFFFu) << 16)
+                                     : __builtin_bit_cast(float, rla[r][0]);
+#pragma unroll
+      for (int f = 0; f < FPL; ++f) x[f] = e;
+    } else {
+      unpack<T, FPL>(rla[r], x);
+    }
+  };
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     ldraw<T, FPL>(rs_q, lane_off + r * row_step, rq[r]);
@@ -187,7 +210,7 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       float x[FPL];
-      unpack<T, FPL>(rla[r], x);
+      unpack_la(r, x);
 #pragma unroll
       for (int f = 0; f < FPL; ++f) {
         if constexpr (PRE) {
@@ -244,7 +267,7 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
   for (int r = 0; r < 16; ++r) {
     const int row = 16 * w + r;
     float xl[FPL], qv[FPL], kv[FPL], o1[FPL], o2[FPL], o3[FPL], o4[FPL];
-    unpack<T, FPL>(rla[r], xl);
+    unpack_la(r, xl);
     unpack<T, FPL>(rq[r], qv);
     unpack<T, FPL>(rk[r], kv);
 #pragma unroll
@@ -329,6 +352,7 @@ __global__ void __launch_bounds__(256) prep_wide_kernel(PrepArgs a) {
   const int t0 = n * C, rv = min(C, a.T - t0), d0 = 16 * w;
   const int64_t base = ((int64_t)bh * a.T + t0) * K;
   const T *q = (const T *)a.q + base, *k = (const T *)a.k + base, *la = (const T *)a.la + base;
+  const T *las = (const T *)a.la + (int64_t)bh * a.T + t0;  // scalar gate rows
   T *Pg = (T *)a.P + ((int64_t)bh * a.N + n) * C * C;
   const int k0 = FPL * l;
   const bool fv = k0 < K;
@@ -340,7 +364,13 @@ __global__ void __launch_bounds__(256) prep_wide_kernel(PrepArgs a) {
     const int row = d0 + r;
     const bool ok = fv && row < rv;
     float xl[FPL];
-    ldvec<T, FPL>(la + row * K + k0, ok, xl);
+    if (a.sg) {
+      const float e = ok ? (float)las[row] : 0.f;
+#pragma unroll
+      for (int f = 0; f < FPL; ++f) xl[f] = e;
+    } else {
+      ldvec<T, FPL>(la + row * K + k0, ok, xl);
+    }
     ldvec<T, FPL>(q + row * K + k0, ok, qv[r]);
     ldvec<T, FPL>(k + row * K + k0, ok, kv[r]);
 #pragma unroll
@@ -418,6 +448,7 @@ hipError_t launch_prep(const Shape &s, const void *q, const void *k, const void 
   a.Qt = w.Qt; a.Kt = w.Kt; a.P = w.P; a.gam = w.gam; a.wflag = w.wflag;
   a.T = s.T; a.K = s.K; a.Kp = round_up(s.K, 32); a.C = s.C; a.N = s.N;
   a.inv_tau = s.inv_tau;
+  a.sg = s.sgate ? 1 : 0;
   a.ldk = a.Kp + 32 / s.esz();
   const size_t lds = lds_prep(s);
   const int fpl = (s.K + 63) / 64;

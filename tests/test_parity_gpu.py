@@ -185,12 +185,20 @@ def test_absent_gate_is_alpha_one(io):
                       want_dS0=True, workspace=ws, reuse_fwd_workspace=True)
     r1, R1 = g.recurrent_fwd(d["q"], d["k"], d["v"], d["log_alpha"], S0=d["S0"], output_final_state=True)
     r2, R2 = g.recurrent_fwd(d["q"], d["k"], d["v"], None, S0=d["S0"], output_final_state=True)
+    # gate_tau does not apply to an absent gate: still alpha = 1
+    o3, ST3 = g.chunk_fwd(d["q"], d["k"], d["v"], None, 64, 16, S0=d["S0"], output_final_state=True,
+                          workspace=ws, gate_tau=16.0)
+    gr3 = g.chunk_bwd(d["q"], d["k"], d["v"], None, d["dO"], 64, 16, S0=d["S0"], dST=d["dST"],
+                      want_dS0=True, workspace=ws, reuse_fwd_workspace=True, gate_tau=16.0)
+    r3, R3 = g.recurrent_fwd(d["q"], d["k"], d["v"], None, S0=d["S0"], output_final_state=True, gate_tau=16.0)
     torch.cuda.synchronize()
     assert gr2["dlog_alpha"] is None
     assert torch.equal(o, o2) and torch.equal(ST, ST2), "forward"
     assert torch.equal(r1, r2) and torch.equal(R1, R2), "recurrent"
+    assert torch.equal(o, o3) and torch.equal(ST, ST3) and torch.equal(r1, r3) and torch.equal(R1, R3), "tau"
     for name in ("dq", "dk", "dv", "dS0"):
         assert torch.equal(gr[name], gr2[name]), name
+        assert torch.equal(gr[name], gr3[name]), name + " (tau)"
     gr2["dlog_alpha"] = gr["dlog_alpha"]
     compare(inp, o2, ST2, gr2, [0, 1], io, cfg["name"])
 
@@ -232,6 +240,93 @@ def test_gate_preactivation_epilogue(io):
     say(cfg["name"], {k2: f"{v2:.2e}" for k2, v2 in errs.items()})
     bad = {k2: v2 for k2, v2 in errs.items() if not v2 <= TOL[io]}
     assert not bad, f"{cfg['name']}: {bad} > {TOL[io]}"
+
+
+SG_CASES = [
+    ("f32", 1, 2, 150, 64, 128, 64, 16, "mild"),
+    ("bf16", 1, 2, 200, 256, 512, 64, 16, "mild"),
+    ("bf16", 2, 1, 100, 48, 80, 64, 16, "mild"),      # a key tile only partly inside d_k
+    ("bf16", 1, 2, 96, 128, 256, 32, 8, "mild"),
+    ("bf16", 1, 1, 128, 64, 64, 64, 16, "strong"),    # pairwise exponentials on the diagonal
+]
+
+
+@pytest.mark.parametrize("io,B,H,T,K,V,C,c,decay", SG_CASES,
+                         ids=[f"{x[0]}_K{x[4]}_V{x[5]}_T{x[3]}_{x[8]}" for x in SG_CASES])
+def test_scalar_gate(io, B, H, T, K, V, C, c, decay):
+    """Data-dependent scalar gates (Table 1: G_t = gamma_t 1^T 1) through a
+    [B, H, T] log gamma: every output against the oracle (dlog gamma is the
+    sum over the key features of the per-feature gate gradient), the
+    recurrent form too, and o, S_T, dq, dk, dv, dS0 bit-identical to the
+    per-feature path fed the broadcast gate."""
+    g = gla()
+    cfg = small_case(f"sg_{io}_{K}_{V}_{T}", io, B, H, T, K, V, C, c, 60 + K + T, s0_std=0.1)
+    inp = W.make_inputs(cfg, dST_std=0.1)
+    gen = torch.Generator().manual_seed(70 + T)
+    if decay == "strong":
+        lg = -torch.rand(B, H, T, generator=gen) * 8.0
+    else:
+        lg = torch.nn.functional.logsigmoid(torch.randn(B, H, T, generator=gen) + 2.0)
+    inp["log_alpha"] = lg.to(inp["q"].dtype)
+    d = to_dev(inp)
+    ws = torch.empty(g.workspace_bytes(B, H, T, K, V, C, c, d["q"].dtype, op=1, scalar_gate=True),
+                     dtype=torch.uint8, device="cuda")
+    o, ST = g.chunk_fwd(d["q"], d["k"], d["v"], d["log_alpha"], C, c, S0=d["S0"], output_final_state=True,
+                        workspace=ws)
+    gr = g.chunk_bwd(d["q"], d["k"], d["v"], d["log_alpha"], d["dO"], C, c, S0=d["S0"], dST=d["dST"],
+                     want_dS0=True, workspace=ws, reuse_fwd_workspace=True)
+    r, R = g.recurrent_fwd(d["q"], d["k"], d["v"], d["log_alpha"], S0=d["S0"], output_final_state=True)
+    full = d["log_alpha"][..., None].expand(B, H, T, K).contiguous()
+    o2, ST2 = g.chunk_fwd(d["q"], d["k"], d["v"], full, C, c, S0=d["S0"], output_final_state=True)
+    gr2 = g.chunk_bwd(d["q"], d["k"], d["v"], full, d["dO"], C, c, S0=d["S0"], dST=d["dST"], want_dS0=True)
+    torch.cuda.synchronize()
+    assert gr["dlog_alpha"].shape == (B, H, T)
+    assert torch.equal(o, o2) and torch.equal(ST, ST2), "forward vs broadcast gate"
+    for name in ("dq", "dk", "dv", "dS0"):
+        assert torch.equal(gr[name], gr2[name]), name + " vs broadcast gate"
+    idx = list(range(B * H))
+    q, k, v, lgh, dO = (heads(inp[n], idx) for n in ("q", "k", "v", "log_alpha", "dO"))
+    S0, dST = heads(inp["S0"], idx), heads(inp["dST"], idx)
+    ro, rST = oracle.scalar_gate_fwd(q, k, v, lgh, S0)
+    rg = oracle.scalar_gate_bwd(q, k, v, lgh, dO, S0=S0, dST=dST)
+    errs = {"o": rel(heads(o, idx), ro), "S_T": rel(heads(ST, idx), rST), "rec_o": rel(heads(r, idx), ro),
+            "rec_S_T": rel(heads(R, idx), rST), "dlog_gamma": rel(heads(gr["dlog_alpha"], idx), rg["dlog_gamma"])}
+    for name in ("dq", "dk", "dv", "dS0"):
+        errs[name] = rel(heads(gr[name], idx), rg[name])
+    say("scalar gate", cfg["name"], decay, {k2: f"{v2:.2e}" for k2, v2 in errs.items()})
+    bad = {k2: v2 for k2, v2 in errs.items() if not v2 <= TOL[io]}
+    assert not bad, bad
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_scalar_gate_with_epilogue(io):
+    """A scalar gate from its pre-activation (gamma = sigmoid(z)^(1/tau), the
+    Gated Retention row of Table 1): dL/dz against the oracle's chain rule."""
+    g = gla()
+    tau, B, H, T, K, V = 16.0, 1, 2, 170, 64, 128
+    cfg = small_case("sg_pre_" + io, io, B, H, T, K, V, 64, 16, 81, s0_std=0.1)
+    inp = W.make_inputs(cfg, dST_std=0.1)
+    z = (torch.randn(B, H, T, generator=torch.Generator().manual_seed(82)) * 2.0 + 1.0).to(inp["q"].dtype)
+    d = to_dev(inp)
+    zd = z.cuda()
+    o, ST = g.chunk_fwd(d["q"], d["k"], d["v"], zd, 64, 16, S0=d["S0"], output_final_state=True, gate_tau=tau)
+    gr = g.chunk_bwd(d["q"], d["k"], d["v"], zd, d["dO"], 64, 16, S0=d["S0"], dST=d["dST"], want_dS0=True,
+                     gate_tau=tau)
+    r, _ = g.recurrent_fwd(d["q"], d["k"], d["v"], zd, S0=d["S0"], gate_tau=tau)
+    torch.cuda.synchronize()
+    idx = [0, 1]
+    q, k, v, dO = (heads(inp[n], idx) for n in ("q", "k", "v", "dO"))
+    S0, dST, zh = heads(inp["S0"], idx), heads(inp["dST"], idx), heads(z, idx)
+    lg = oracle.gate_log_alpha(zh, tau)
+    ro, rST = oracle.scalar_gate_fwd(q, k, v, lg, S0)
+    rg = oracle.scalar_gate_bwd(q, k, v, lg, dO, S0=S0, dST=dST)
+    errs = {"o": rel(heads(o, idx), ro), "S_T": rel(heads(ST, idx), rST), "rec_o": rel(heads(r, idx), ro),
+            "dz": rel(heads(gr["dlog_alpha"], idx), oracle.gate_grad(zh, tau, rg["dlog_gamma"]))}
+    for name in ("dq", "dk", "dv", "dS0"):
+        errs[name] = rel(heads(gr[name], idx), rg[name])
+    say("scalar gate epilogue", io, {k2: f"{v2:.2e}" for k2, v2 in errs.items()})
+    bad = {k2: v2 for k2, v2 in errs.items() if not v2 <= TOL[io]}
+    assert not bad, bad
 
 
 OG_CASES = [("f32", 2, 3, 70, 48, True), ("f32", 1, 2, 130, 1024, False), ("bf16", 2, 4, 100, 512, True),
