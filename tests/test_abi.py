@@ -74,6 +74,17 @@ def test_workspace_bytes(L):
     assert L.gla_workspace_bytes(ctypes.byref(P(dk=24)), 0) == 0
 
 
+def test_scalar_gate_workspace(L):
+    """A scalar gate adds the per-key-tile gate-gradient sums to the backward's
+    workspace (B H ceil(d_k/32) T fp32) and nothing to the forward's."""
+    for dk, T in ((64, 200), (48, 77), (256, 2048)):
+        p, ps = P(dk=dk, T=T), P(dk=dk, T=T, flags=gla.FLAG_SCALAR_GATE)
+        assert L.gla_workspace_bytes(ctypes.byref(ps), 0) == L.gla_workspace_bytes(ctypes.byref(p), 0)
+        extra = L.gla_workspace_bytes(ctypes.byref(ps), 1) - L.gla_workspace_bytes(ctypes.byref(p), 1)
+        need = 6 * ((dk + 31) // 32) * T * 4
+        assert need <= extra < need + 256
+
+
 def fwd_call(L, p, ptr=1, ws=1, ws_bytes=1 << 40):
     return L.gla_chunk_fwd(ctypes.byref(p) if p is not None else None, ptr, ptr, ptr, ptr, None,
                            ptr, None, ws, ws_bytes, None)
