@@ -207,3 +207,56 @@ def scalar_gate_bwd(q, k, v, log_gamma, dO, S0=None, dST=None, nthreads=None, ck
     g = bwd(q, k, v, _broadcast_gate(log_gamma, K), dO, S0=S0, dST=dST, nthreads=nthreads, ckpt=ckpt)
     g["dlog_gamma"] = g.pop("dlog_alpha").sum(axis=-1)
     return g
+
+
+# ---------------------------------------------------------------- general gates
+# The general gated form of App. C: G_t = alpha_t^T beta_t, a key-side gate
+# alpha_t in (0,1]^{d_k} and a value-side gate beta_t in (0,1]^{d_v},
+#     S_t = (alpha_t^T beta_t) (.) S_{t-1} + k_t^T v_t,    o_t = q_t S_t.
+# Plain numpy, one step at a time (all leading dims at once), fp64.
+
+def general_gate_fwd(q, k, v, log_alpha, log_beta, S0=None):
+    """Returns (o, S_T); q, k, log_alpha: [..., T, d_k]; v, log_beta:
+    [..., T, d_v]; S0: [..., d_k, d_v] or None."""
+    q, k, v, la, lb, S0 = (_as_f64(x) for x in (q, k, v, log_alpha, log_beta, S0))
+    T, K = q.shape[-2:]
+    V = v.shape[-1]
+    S = np.zeros(q.shape[:-2] + (K, V)) if S0 is None else S0.copy()
+    o = np.empty(q.shape[:-1] + (V,))
+    for t in range(T):
+        S = np.exp(la[..., t, :, None] + lb[..., t, None, :]) * S + k[..., t, :, None] * v[..., t, None, :]
+        o[..., t, :] = np.einsum("...a,...aj->...j", q[..., t, :], S)
+    return o, S
+
+
+def general_gate_bwd(q, k, v, log_alpha, log_beta, dO, S0=None, dST=None):
+    """Back-propagation through general_gate_fwd for L = sum(o dO) +
+    sum(S_T dS_T), keeping every state.  With G_t = dL/dS_t and
+    M_t = alpha_t^T beta_t: G_t = q_t^T do_t + M_{t+1} (.) G_{t+1} (G_T also
+    holds dS_T), dq_t = S_t do_t^T, dk_t = G_t v_t^T, dv_t = k_t G_t,
+    d log alpha_t = rowsum(G_t (.) M_t (.) S_{t-1}), d log beta_t the column
+    sums of the same product, dS0 = M_1 (.) G_1.  Returns dq, dk, dv,
+    dlog_alpha, dlog_beta, dS0."""
+    q, k, v, la, lb, dO, S0, dST = (_as_f64(x) for x in (q, k, v, log_alpha, log_beta, dO, S0, dST))
+    T, K = q.shape[-2:]
+    V = v.shape[-1]
+    lead = q.shape[:-2]
+    S = [np.zeros(lead + (K, V)) if S0 is None else S0.copy()]
+    M = []
+    for t in range(T):
+        M.append(np.exp(la[..., t, :, None] + lb[..., t, None, :]))
+        S.append(M[t] * S[t] + k[..., t, :, None] * v[..., t, None, :])
+    G = np.zeros(lead + (K, V)) if dST is None else dST.copy()
+    out = {n: np.zeros_like(x) for n, x in (("dq", q), ("dk", k), ("dv", v), ("dlog_alpha", la),
+                                               ("dlog_beta", lb))}
+    for t in range(T - 1, -1, -1):
+        G = G + q[..., t, :, None] * dO[..., t, None, :]
+        out["dq"][..., t, :] = np.einsum("...aj,...j->...a", S[t + 1], dO[..., t, :])
+        out["dk"][..., t, :] = np.einsum("...aj,...j->...a", G, v[..., t, :])
+        out["dv"][..., t, :] = np.einsum("...a,...aj->...j", k[..., t, :], G)
+        dM = G * M[t] * S[t]
+        out["dlog_alpha"][..., t, :] = dM.sum(axis=-1)
+        out["dlog_beta"][..., t, :] = dM.sum(axis=-2)
+        G = M[t] * G
+    out["dS0"] = G
+    return out

@@ -199,3 +199,34 @@ def scalar_decay_attention(q, k, v, log_gamma, S0=None):
         o = o + np.exp(c)[:, None] * (q @ S0)
         ST = ST + np.exp(cT) * S0
     return o, ST
+
+
+def general_gate_parallel(q, k, v, log_alpha, log_beta, S0=None):
+    """Parallel form of the general gate G_t = alpha_t^T beta_t (App. C): with
+    A, D the cumulative sums of log alpha and log beta,
+    o_t[j] = sum_{s <= t} sum_a q_t[a] k_s[a] v_s[j] exp(A_t[a] - A_s[a] + D_t[j] - D_s[j])
+             + sum_a q_t[a] exp(A_t[a] + D_t[j]) S0[a, j]."""
+    q, k, v, la, lb, S0 = map(_f64, (q, k, v, log_alpha, log_beta, S0))
+    T = q.shape[0]
+    A, D = np.cumsum(la, axis=0), np.cumsum(lb, axis=0)
+    mask = np.tril(np.ones((T, T), bool))
+    ea = np.where(mask[:, :, None], np.exp(np.where(mask[:, :, None], A[:, None, :] - A[None, :, :], 0.0)), 0.0)
+    ed = np.where(mask[:, :, None], np.exp(np.where(mask[:, :, None], D[:, None, :] - D[None, :, :], 0.0)), 0.0)
+    o = np.einsum("ta,sa,tsa,sj,tsj->tj", q, k, ea, v, ed)
+    if S0 is not None:
+        o = o + np.einsum("ta,ta,aj,tj->tj", q, np.exp(A), S0, np.exp(D))
+    return o
+
+
+def general_gate_closed_form(q, k, v, o, dq, dk, dv, dO, ST=None, dST=None):
+    """Gate gradients of the general form without the states (App. C):
+    dlog alpha_t = sum_{i >= t} (q_i dq_i - k_i dk_i) + rowsum(S_T dS_T) and,
+    on the value side, dlog beta_t = sum_{i >= t} (o_i do_i - v_i dv_i)
+    + colsum(S_T dS_T)."""
+    q, k, v, o, dq, dk, dv, dO, ST, dST = map(_f64, (q, k, v, o, dq, dk, dv, dO, ST, dST))
+    ra = np.cumsum((q * dq - k * dk)[::-1], axis=0)[::-1]
+    rb = np.cumsum((o * dO - v * dv)[::-1], axis=0)[::-1]
+    if ST is not None and dST is not None:
+        ra = ra + (ST * dST).sum(axis=1)[None, :]
+        rb = rb + (ST * dST).sum(axis=0)[None, :]
+    return ra, rb

@@ -424,3 +424,75 @@ def test_scalar_gate_gradients_match_central_finite_differences():
             fd[idx] = (loss(ap) - loss(am)) / (2 * h)
         assert g[gname].shape == fd.shape, name
         assert rel(g[gname], fd) < 1e-7, name
+
+
+# ---------------------------------------------------------------- general gates
+
+def _general_case(rng, T=9, K=4, V=3):
+    q = rng.standard_normal((T, K))
+    k = rng.standard_normal((T, K)) / np.sqrt(K)
+    v = rng.standard_normal((T, V))
+    la = -np.logaddexp(0.0, -(rng.standard_normal((T, K)) + 1.0))
+    lb = -np.logaddexp(0.0, -(rng.standard_normal((T, V)) + 1.0))
+    S0 = rng.standard_normal((K, V)) * 0.3
+    return q, k, v, la, lb, S0
+
+
+def test_general_gate_forward_pins():
+    rng = np.random.default_rng(61)
+    q, k, v, la, lb, S0 = _general_case(rng)
+    o, ST = oracle.general_gate_fwd(q, k, v, la, lb, S0)
+    assert rel(o, forms.general_gate_parallel(q, k, v, la, lb, S0)) < 1e-12
+    # beta = 1 is the GLA layer of Eq. 3
+    o1, S1 = oracle.general_gate_fwd(q, k, v, la, np.zeros_like(v), S0)
+    r1, R1 = oracle.fwd(q, k, v, la, S0, nthreads=1)
+    assert rel(o1, r1) < 1e-12 and rel(S1, R1) < 1e-12
+    # a constant value-side gate gamma on an ungated key side is the decay mask
+    o2, _ = oracle.general_gate_fwd(q, k, v, np.zeros_like(q), np.full(v.shape, np.log(0.7)))
+    assert rel(o2, forms.decay_mask_attention(q, k, v, 0.7)) < 1e-12
+    # leading dims are independent heads
+    ob, _ = oracle.general_gate_fwd(np.stack([q, -q]), np.stack([k, k]), np.stack([v, 2 * v]),
+                                    np.stack([la, la]), np.stack([lb, 0.5 * lb]))
+    assert rel(ob[1], forms.general_gate_parallel(-q, k, 2 * v, la, 0.5 * lb)) < 1e-12
+
+
+def test_general_gate_gradients_match_central_finite_differences():
+    rng = np.random.default_rng(62)
+    q, k, v, la, lb, S0 = _general_case(rng, T=5, K=3, V=2)
+    dO = rng.standard_normal((5, 2))
+    dST = rng.standard_normal((3, 2))
+    g = oracle.general_gate_bwd(q, k, v, la, lb, dO, S0, dST)
+    args = {"q": q, "k": k, "v": v, "la": la, "lb": lb, "S0": S0}
+
+    def loss(a):
+        o, ST = oracle.general_gate_fwd(a["q"], a["k"], a["v"], a["la"], a["lb"], a["S0"])
+        return float((o * dO).sum() + (ST * dST).sum())
+
+    h = 1e-6
+    for name, gname in (("q", "dq"), ("k", "dk"), ("v", "dv"), ("la", "dlog_alpha"), ("lb", "dlog_beta"),
+                        ("S0", "dS0")):
+        fd = np.zeros_like(args[name])
+        for idx in np.ndindex(args[name].shape):
+            ap = {n: x.copy() for n, x in args.items()}; ap[name][idx] += h
+            am = {n: x.copy() for n, x in args.items()}; am[name][idx] -= h
+            fd[idx] = (loss(ap) - loss(am)) / (2 * h)
+        assert rel(g[gname], fd) < 1e-7, name
+    # beta = 1 reduces the backward to the GLA one
+    g1 = oracle.general_gate_bwd(q, k, v, la, np.zeros_like(v), dO, S0, dST)
+    r1 = oracle.bwd(q, k, v, la, dO, S0=S0, dST=dST, nthreads=1, ckpt=2)
+    for name in ("dq", "dk", "dv", "dlog_alpha", "dS0"):
+        assert rel(g1[name], r1[name]) < 1e-12, name
+
+
+def test_general_gate_gradients_equal_closed_form():
+    """App. C: both gate gradients follow from the other gradients and the
+    outputs, without the states."""
+    rng = np.random.default_rng(63)
+    q, k, v, la, lb, S0 = _general_case(rng, T=17, K=5, V=4)
+    dO = rng.standard_normal((17, 4))
+    dST = rng.standard_normal((5, 4))
+    o, ST = oracle.general_gate_fwd(q, k, v, la, lb, S0)
+    g = oracle.general_gate_bwd(q, k, v, la, lb, dO, S0, dST)
+    ra, rb = forms.general_gate_closed_form(q, k, v, o, g["dq"], g["dk"], g["dv"], dO, ST, dST)
+    assert rel(g["dlog_alpha"], ra) < 1e-12
+    assert rel(g["dlog_beta"], rb) < 1e-12
