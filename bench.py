@@ -43,7 +43,7 @@ STAGES = [("prep", "fwd", 1), ("fwd_main", "fwd", 2), ("bwd_dq", "bwd", 2), ("bw
 STAGES_OG = STAGES[:2] + [("og_fwd", "og", 0), ("og_bwd", "og", 1)] + STAGES[2:]
 
 
-def algorithmic(cfg, gate=True, scalar_gate=False):
+def algorithmic(cfg, gate=True, scalar_gate=False, value_gate=False):
     """Algorithmic FLOPs and HBM bytes per launch of each stage (and totals);
     gate=False is the alpha = 1 layer, which reads no gate tensor and writes no
     gate gradient; scalar_gate has one gate value per step and head."""
@@ -58,7 +58,7 @@ def algorithmic(cfg, gate=True, scalar_gate=False):
         # gate factors, Q (.) Lambda, K (.) Gamma, P: reads q, k, log_alpha
         "prep": dict(flops=n * (C + 1) * K, bytes=n * s * (2 + ga) * K + n * s * 2 * K + P + g),
         # state pass + output: reads Qt, Kt, v, P, gamma; writes o
-        "fwd_main": dict(flops=n * (4 * K * V + (C + 1) * V), bytes=n * s * (2 * K + 2 * V) + P + g),
+        "fwd_main": dict(flops=n * (4 * K * V + (C + 1) * V), bytes=n * s * (2 * K + (3 if value_gate else 2) * V) + P + g),
         # dq sweep: reads k, log_alpha, v, dO; writes dq and dP
         "bwd_dq": dict(flops=n * (2 * K * V + (C + 1) * (K + V)), bytes=n * s * ((2 + ga) * K + 2 * V) + dP),
         # dk sweep: reads q, k, log_alpha, v, dO, dq, dP; writes dk, dlog_alpha
@@ -167,6 +167,9 @@ def main():
                     help="> 0: pass the gate pre-activation z (alpha = sigmoid(z)^(1/tau)) instead of log alpha")
     ap.add_argument("--scalar-gate", action="store_true",
                     help="one gate value per step and head (log gamma [B, H, T], Table 1's scalar gates)")
+    ap.add_argument("--value-gate", action="store_true",
+                    help="general form G = alpha^T beta (App. C): adds log beta [B, H, T, d_v]; "
+                         "the step is then the forward only (no backward of the general form)")
     ap.add_argument("--output-gate", action="store_true",
                     help="include the output side (per-head LN + Swish gate, Sec. 4.4) in the step")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -215,6 +218,14 @@ def main():
              "dS0": torch.empty(B, H, K, V, dtype=torch.float32, device=dev) if d["S0"] is not None else None}
     stream = torch.cuda.current_stream(dev)
     stages = STAGES_OG if args.output_gate else STAGES
+    if args.value_gate:
+        if args.output_gate:
+            print("--value-gate times the forward only; it does not combine with --output-gate", file=sys.stderr)
+            sys.exit(2)
+        stages = STAGES[:2]
+        gb = torch.Generator().manual_seed(cfg["seed"] + 13)
+        # log beta = logsigmoid(x) / 16, x ~ N(0, 1), the key gate's recipe on the value side
+        d["log_beta"] = (torch.nn.functional.logsigmoid(torch.randn(B, H, T, V, generator=gb)) / 16.0).to(dt).to(dev)
     if args.output_gate:
         # output-gate pre-activations, the loss gradient at y and the LN affine
         go = torch.Generator().manual_seed(cfg["seed"] + 11)
@@ -236,7 +247,7 @@ def main():
                 gla.output_gate_bwd(o, og["g"], og["dy"], og["w"], og["b"], out=og_out, workspace=og_ws)
         elif which == "fwd":
             gla.chunk_fwd(d["q"], d["k"], d["v"], d["log_alpha"], C, c, S0=d["S0"], workspace=ws,
-                          stage=stage, out=(o, ST), gate_tau=args.gate_tau)
+                          stage=stage, out=(o, ST), gate_tau=args.gate_tau, log_beta=d.get("log_beta"))
         else:
             gla.chunk_bwd(d["q"], d["k"], d["v"], d["log_alpha"], d["dO"], C, c, S0=d["S0"], dST=d["dST"],
                           workspace=ws, reuse_fwd_workspace=True, stage=stage, out=grads,
@@ -266,7 +277,11 @@ def main():
     for s in range(args.steps):
         for i, (nm, _, _) in enumerate(stages):
             stage_ms[nm] += evs[s][i].elapsed_time(evs[s][i + 1]) / args.steps
-    st_alg, fwd_flops, bwd_flops, io_bytes = algorithmic(cfg, gate=not args.no_gate, scalar_gate=args.scalar_gate)
+    st_alg, fwd_flops, bwd_flops, io_bytes = algorithmic(cfg, gate=not args.no_gate, scalar_gate=args.scalar_gate,
+                                                         value_gate=args.value_gate)
+    if args.value_gate:
+        bwd_flops = 0  # forward only
+        io_bytes = st_alg["prep"]["bytes"] + st_alg["fwd_main"]["bytes"]
     if args.output_gate:
         io_bytes += st_alg["og_fwd"]["bytes"] + st_alg["og_bwd"]["bytes"]
     ms_per_step = 1e3 * elapsed / args.steps
@@ -288,13 +303,15 @@ def main():
 
     dom = max(stage_ms, key=stage_ms.get)
     roof = roofline(dom)
-    plain = not (args.no_gate or args.gate_tau > 0 or args.output_gate or args.scalar_gate)
+    plain = not (args.no_gate or args.gate_tau > 0 or args.output_gate or args.scalar_gate or args.value_gate)
     roof["traffic"] = measured_traffic(args.workload, dom) if plain else None
     roof["avg_ms"] = stage_ms[dom]
     stage_frac = {nm: f"{r['frac']:.3f} of {r['bound']}" for nm, r in ((nm, roofline(nm)) for nm in stage_ms)}
 
     out = {
-        "metric": "GLA fwd+bwd tokens/s and TFLOP/s (% bf16 MFMA peak), 1.3B layer, T=2048",
+        "metric": ("GLA forward (general alpha^T beta gate) tokens/s and TFLOP/s, 1.3B layer, T=2048"
+                   if args.value_gate else
+                   "GLA fwd+bwd tokens/s and TFLOP/s (% bf16 MFMA peak), 1.3B layer, T=2048"),
         "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": cfg["io"], "data": "synthetic",
@@ -304,6 +321,8 @@ def main():
                    **({"gate": f"pre-activation z, alpha = sigmoid(z)^(1/{args.gate_tau:g})"}
                       if args.gate_tau > 0 else {}),
                    **({"gate_shape": "scalar per step and head, log gamma [B, H, T]"} if args.scalar_gate else {}),
+                   **({"value_gate": "general form alpha^T beta, log beta [B, H, T, d_v]; step = forward only"}
+                      if args.value_gate else {}),
                    **({"output_side": "per-head LN (affine) + Swish output gate, fwd + bwd"}
                       if args.output_gate else {})},
         "tflops": tflops, "mfma_peak_frac": tflops * 1e12 / peak,
@@ -312,7 +331,7 @@ def main():
         "stage_roofline_frac": stage_frac,
         "roofline": roof,
     }
-    if not args.no_cpu_baseline and not args.scalar_gate:
+    if not args.no_cpu_baseline and not args.scalar_gate and not args.value_gate:
         out["cpu_baseline"] = cpu_baseline(cfg, inp_cpu)
     print(json.dumps(out), flush=True)
 

@@ -156,6 +156,24 @@ gla_status gla_recurrent_fwd(const gla_problem *prob, const void *q, const void 
                              const void *v, const void *log_alpha, const float *S0, void *o,
                              float *S_T, void *stream);
 
+/* General gated form (App. C): G_t = alpha_t^T beta_t with a value-side gate
+ * beta_t in (0, 1]^{d_v} besides the key-side alpha_t,
+ *     S_t = (alpha_t^T beta_t) (.) S_{t-1} + k_t^T v_t,   o_t = q_t S_t.
+ * log_beta: [B, H, T, d_v] (io dtype), finite and <= 0; NULL means beta = 1,
+ * which is exactly gla_chunk_fwd / gla_recurrent_fwd.  Every other argument,
+ * flag (scalar key gate, gate_tau on the key gate) and the workspace are as
+ * for those calls.  The chunkwise form normalises the value side per chunk:
+ * the decay of beta accumulated over one chunk of one value column,
+ * -sum log beta, must stay below ~80, else outputs overflow (a shorter chunk
+ * widens the range; the recurrent form has no such limit).  Forward only: the
+ * backward of the general form is not provided. */
+gla_status gla_chunk_fwd_general(const gla_problem *prob, const void *q, const void *k, const void *v,
+                                 const void *log_alpha, const void *log_beta, const float *S0, void *o,
+                                 float *S_T, void *workspace, size_t workspace_bytes, void *stream);
+gla_status gla_recurrent_fwd_general(const gla_problem *prob, const void *q, const void *k,
+                                     const void *v, const void *log_alpha, const void *log_beta,
+                                     const float *S0, void *o, float *S_T, void *stream);
+
 /* Output side of the layer (Sec. 4.4): per head and row, y_t = Swish(g_t) (.)
  * LN(o_t) with LN(x) = w (.) (x - mean(x)) / sqrt(var(x) + eps) + b over the
  * d_v features of one head (biased variance), g the output-gate

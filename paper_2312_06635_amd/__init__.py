@@ -68,6 +68,10 @@ def lib():
         L.gla_chunk_bwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.gla_chunk_bwd.restype = i32
         L.gla_recurrent_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.gla_chunk_fwd_general.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.gla_chunk_fwd_general.restype = i32
+        L.gla_recurrent_fwd_general.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.gla_recurrent_fwd_general.restype = i32
         L.gla_recurrent_fwd.restype = i32
         L.gla_status_string.argtypes = [i32]
         L.gla_status_string.restype = ctypes.c_char_p
@@ -152,8 +156,15 @@ def _workspace(p, op, dev, workspace):
     return workspace
 
 
+def _check_beta(lb, v):
+    if lb is None:
+        return
+    if lb.shape != v.shape or lb.dtype != v.dtype or lb.device != v.device or not lb.is_contiguous():
+        raise ValueError(f"log_beta must be a contiguous {v.dtype} tensor shaped like v {tuple(v.shape)}")
+
+
 def chunk_fwd(q, k, v, log_alpha, chunk=64, subchunk=16, S0=None, output_final_state=False,
-              workspace=None, stage=0, out=None, gate_tau=0.0):
+              workspace=None, stage=0, out=None, gate_tau=0.0, log_beta=None):
     """Chunkwise GLA forward.  Returns (o, S_T or None).
 
     log_alpha=None means alpha = 1 (ungated linear attention): no gate tensor
@@ -161,8 +172,10 @@ def chunk_fwd(q, k, v, log_alpha, chunk=64, subchunk=16, S0=None, output_final_s
     gamma_t 1, the scalar-gate rows of Table 1).  gate_tau > 0 means log_alpha holds the gate pre-activation z of
     alpha = sigmoid(z)^(1/gate_tau) (the GLA gate).  stage selects one kernel of the launch sequence (see
     GLA_STAGE_* in include/gla.h); out=(o, S_T) reuses caller-provided output
-    tensors."""
+    tensors.  log_beta ([B, H, T, d_v]) adds the value-side gate of the
+    general form G_t = alpha_t^T beta_t (App. C; forward only)."""
     _check(q, k, v, log_alpha, states=(("S0", S0),))
+    _check_beta(log_beta, v)
     B, H, T, dk = q.shape
     dv = v.shape[3]
     p = _problem(q, v, chunk, subchunk, stage << STAGE_SHIFT, gate_tau, log_alpha)
@@ -172,11 +185,16 @@ def chunk_fwd(q, k, v, log_alpha, chunk=64, subchunk=16, S0=None, output_final_s
         o = torch.empty_like(v)
         ST = torch.empty(B, H, dk, dv, dtype=torch.float32, device=q.device) if output_final_state else None
     ws = _workspace(p, 0, q.device, workspace)
-    st = lib().gla_chunk_fwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(S0),
-                             _ptr(o), _ptr(ST), _ptr(ws), ws.numel() * ws.element_size(),
-                             _stream(q.device))
+    if log_beta is not None:
+        st = lib().gla_chunk_fwd_general(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha),
+                                         _ptr(log_beta), _ptr(S0), _ptr(o), _ptr(ST), _ptr(ws),
+                                         ws.numel() * ws.element_size(), _stream(q.device))
+    else:
+        st = lib().gla_chunk_fwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(S0),
+                                 _ptr(o), _ptr(ST), _ptr(ws), ws.numel() * ws.element_size(),
+                                 _stream(q.device))
     if st != GLA_OK:
-        raise GlaError(st, "gla_chunk_fwd")
+        raise GlaError(st, "gla_chunk_fwd_general" if log_beta is not None else "gla_chunk_fwd")
     return o, ST
 
 
@@ -216,17 +234,23 @@ def chunk_bwd(q, k, v, log_alpha, dO, chunk=64, subchunk=16, S0=None, dST=None,
     return {"dq": dq, "dk": dkk, "dv": dvv, "dlog_alpha": dla, "dS0": dS0}
 
 
-def recurrent_fwd(q, k, v, log_alpha, S0=None, output_final_state=False, gate_tau=0.0):
+def recurrent_fwd(q, k, v, log_alpha, S0=None, output_final_state=False, gate_tau=0.0, log_beta=None):
     """Step-by-step recurrent forward (Eq. 3).  Returns (o, S_T or None);
-    log_alpha=None means alpha = 1."""
+    log_alpha=None means alpha = 1; log_beta adds the value-side gate of the
+    general form (App. C)."""
     _check(q, k, v, log_alpha, states=(("S0", S0),))
+    _check_beta(log_beta, v)
     B, H, T, dk = q.shape
     dv = v.shape[3]
     p = _problem(q, v, 16, 16, 0, gate_tau, log_alpha)
     o = torch.empty_like(v)
     ST = torch.empty(B, H, dk, dv, dtype=torch.float32, device=q.device) if output_final_state else None
-    st = lib().gla_recurrent_fwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha),
-                                 _ptr(S0), _ptr(o), _ptr(ST), _stream(q.device))
+    if log_beta is not None:
+        st = lib().gla_recurrent_fwd_general(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha),
+                                             _ptr(log_beta), _ptr(S0), _ptr(o), _ptr(ST), _stream(q.device))
+    else:
+        st = lib().gla_recurrent_fwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha),
+                                     _ptr(S0), _ptr(o), _ptr(ST), _stream(q.device))
     if st != GLA_OK:
         raise GlaError(st, "gla_recurrent_fwd")
     return o, ST

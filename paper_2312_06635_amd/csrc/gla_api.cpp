@@ -112,10 +112,11 @@ GLA_EXPORT size_t gla_workspace_bytes(const gla_problem *prob, int op) {
   return layout(s, op, nullptr, nullptr);
 }
 
-GLA_EXPORT gla_status gla_chunk_fwd(const gla_problem *prob, const void *q, const void *k,
-                                    const void *v, const void *log_alpha, const float *S0,
-                                    void *o, float *S_T, void *workspace, size_t workspace_bytes,
-                                    void *stream) {
+namespace {
+
+gla_status chunk_fwd(const gla_problem *prob, const void *q, const void *k, const void *v,
+                     const void *log_alpha, const void *log_beta, const float *S0, void *o, float *S_T,
+                     void *workspace, size_t workspace_bytes, void *stream) {
   Shape s;
   gla_status st = make_shape(prob, s);
   if (st != GLA_OK) return st;
@@ -135,8 +136,44 @@ GLA_EXPORT gla_status gla_chunk_fwd(const gla_problem *prob, const void *q, cons
   layout(s, 0, (char *)workspace, &w);
   hipError_t e = hipSuccess;
   if (stage == 0 || stage == 1) e = gla::launch_prep(s, q, k, log_alpha, w, hs);
-  if (e == hipSuccess && (stage == 0 || stage == 2)) e = gla::launch_fwd_main(s, v, S0, o, S_T, w, hs);
+  if (e == hipSuccess && (stage == 0 || stage == 2)) e = gla::launch_fwd_main(s, v, log_beta, S0, o, S_T, w, hs);
   return hip_status(e);
+}
+
+gla_status recurrent_fwd(const gla_problem *prob, const void *q, const void *k, const void *v,
+                         const void *log_alpha, const void *log_beta, const float *S0, void *o, float *S_T,
+                         void *stream) {
+  if (!prob) return GLA_ERR_NULL;
+  gla_problem p = *prob;
+  p.chunk = 16;  // the recurrent form ignores the chunk fields
+  p.subchunk = 16;
+  Shape s;
+  gla_status st = make_shape(&p, s);
+  if (st != GLA_OK) return st;
+  if (!log_alpha) s.inv_tau = 0.f;  // no gate: alpha = 1 whatever gate_tau says
+  const bool any = (int64_t)s.BH * s.T > 0;
+  if (any && (!q || !k || !v || !o)) return GLA_ERR_NULL;
+  hipStream_t hs = (hipStream_t)stream;
+  if (s.BH == 0) return GLA_OK;
+  if (s.T == 0)
+    return hip_status(gla::launch_copy_state((int64_t)s.BH * s.K * s.V, S0, S_T, hs));
+  return hip_status(gla::launch_recurrent(s, q, k, v, log_alpha, log_beta, S0, o, S_T, hs));
+}
+
+}  // namespace
+
+GLA_EXPORT gla_status gla_chunk_fwd(const gla_problem *prob, const void *q, const void *k,
+                                    const void *v, const void *log_alpha, const float *S0,
+                                    void *o, float *S_T, void *workspace, size_t workspace_bytes,
+                                    void *stream) {
+  return chunk_fwd(prob, q, k, v, log_alpha, nullptr, S0, o, S_T, workspace, workspace_bytes, stream);
+}
+
+GLA_EXPORT gla_status gla_chunk_fwd_general(const gla_problem *prob, const void *q, const void *k,
+                                            const void *v, const void *log_alpha, const void *log_beta,
+                                            const float *S0, void *o, float *S_T, void *workspace,
+                                            size_t workspace_bytes, void *stream) {
+  return chunk_fwd(prob, q, k, v, log_alpha, log_beta, S0, o, S_T, workspace, workspace_bytes, stream);
 }
 
 GLA_EXPORT gla_status gla_chunk_bwd(const gla_problem *prob, const void *q, const void *k,
@@ -175,21 +212,13 @@ GLA_EXPORT gla_status gla_chunk_bwd(const gla_problem *prob, const void *q, cons
 GLA_EXPORT gla_status gla_recurrent_fwd(const gla_problem *prob, const void *q, const void *k,
                                         const void *v, const void *log_alpha, const float *S0,
                                         void *o, float *S_T, void *stream) {
-  if (!prob) return GLA_ERR_NULL;
-  gla_problem p = *prob;
-  p.chunk = 16;  // the recurrent form ignores the chunk fields
-  p.subchunk = 16;
-  Shape s;
-  gla_status st = make_shape(&p, s);
-  if (st != GLA_OK) return st;
-  if (!log_alpha) s.inv_tau = 0.f;  // no gate: alpha = 1 whatever gate_tau says
-  const bool any = (int64_t)s.BH * s.T > 0;
-  if (any && (!q || !k || !v || !o)) return GLA_ERR_NULL;
-  hipStream_t hs = (hipStream_t)stream;
-  if (s.BH == 0) return GLA_OK;
-  if (s.T == 0)
-    return hip_status(gla::launch_copy_state((int64_t)s.BH * s.K * s.V, S0, S_T, hs));
-  return hip_status(gla::launch_recurrent(s, q, k, v, log_alpha, S0, o, S_T, hs));
+  return recurrent_fwd(prob, q, k, v, log_alpha, nullptr, S0, o, S_T, stream);
+}
+
+GLA_EXPORT gla_status gla_recurrent_fwd_general(const gla_problem *prob, const void *q, const void *k,
+                                                const void *v, const void *log_alpha, const void *log_beta,
+                                                const float *S0, void *o, float *S_T, void *stream) {
+  return recurrent_fwd(prob, q, k, v, log_alpha, log_beta, S0, o, S_T, stream);
 }
 
 // ---------------------------------------------------------------- output side

@@ -1,5 +1,6 @@
-// gla_fwd.hip -- the step-by-step recurrent forward (Sec. 4.1, Eq. 3) and the
-// T = 0 state copy.  The chunkwise state pass lives in gla_vsweep.hip.
+// gla_fwd.hip -- the step-by-step recurrent forward (Sec. 4.1, Eq. 3; with
+// the value-side gate of App. C, G_t = alpha_t^T beta_t) and the T = 0 state
+// copy.  The chunkwise state pass lives in gla_vsweep.hip.
 #include "gla_common.hpp"
 #include "gla_launch.hpp"
 
@@ -10,7 +11,7 @@ namespace gla {
 // (column, quarter) holds the fp32 state rows of its quarter of d_k for its
 // column; o_t is the sum of the four quarters' partial dot products.
 struct RecArgs {
-  const void *q, *k, *v, *la;
+  const void *q, *k, *v, *la, *lb;  // lb: log beta [BH][T][V], value-side gate (nullable)
   const float *S0;
   void *o;
   float *ST;
@@ -35,6 +36,7 @@ __global__ void __launch_bounds__(256) recurrent_kernel(RecArgs a) {
   const T *q = (const T *)a.q + (int64_t)bh * a.T * K, *k = (const T *)a.k + (int64_t)bh * a.T * K;
   const int lrow = a.sg ? 1 : K, lf = a.sg ? 0 : 1;  // gate elements per step, per feature
   const T *la = (const T *)a.la + (int64_t)bh * a.T * lrow, *v = (const T *)a.v + (int64_t)bh * a.T * V;
+  const T *lb = (const T *)a.lb + (int64_t)bh * a.T * V;
   T *o = (T *)a.o + (int64_t)bh * a.T * V;
   for (int t = 0; t < a.T; ++t) {
     for (int i = tid; i < K; i += 256) {
@@ -43,13 +45,15 @@ __global__ void __launch_bounds__(256) recurrent_kernel(RecArgs a) {
       sa[i] = a.la ? __expf(gate_la((float)la[(int64_t)t * lrow + i * lf], a.inv_tau, true)) : 1.f;  // no gate: alpha = 1
     }
     const float vt = colv ? (float)v[(int64_t)t * V + col] : 0.f;
+    // general gate (App. C): the value-side factor of this thread's column
+    const float bt = (a.lb && colv) ? __expf((float)lb[(int64_t)t * V + col]) : 1.f;
     __syncthreads();
     float part = 0.f;
 #pragma unroll
     for (int i = 0; i < 64; ++i) {
       const int kr = qt * KQ + i;
       if (i < KQ && kr < K) {
-        S[i] = sa[kr] * S[i] + sk[kr] * vt;
+        S[i] = sa[kr] * bt * S[i] + sk[kr] * vt;
         part += sq[kr] * S[i];
       }
     }
@@ -67,8 +71,8 @@ __global__ void __launch_bounds__(256) recurrent_kernel(RecArgs a) {
 }
 
 hipError_t launch_recurrent(const Shape &s, const void *q, const void *k, const void *v,
-                            const void *la, const float *S0, void *o, float *ST, hipStream_t st) {
-  RecArgs a{q, k, v, la, S0, o, ST, s.T, s.K, s.V, s.sgate ? 1 : 0, s.inv_tau};
+                            const void *la, const void *lb, const float *S0, void *o, float *ST, hipStream_t st) {
+  RecArgs a{q, k, v, la, lb, S0, o, ST, s.T, s.K, s.V, s.sgate ? 1 : 0, s.inv_tau};
   dim3 grid((s.V + 63) / 64, s.BH);
   if (s.io == IO_BF16)
     hipLaunchKernelGGL(recurrent_kernel<bf16>, grid, dim3(256), 0, st, a);

@@ -36,7 +36,8 @@ struct Work {
 // Returns hipSuccess or the launch error.  Shapes are validated by the caller.
 hipError_t launch_prep(const Shape &s, const void *q, const void *k, const void *la,
                        const Work &w, hipStream_t st);
-hipError_t launch_fwd_main(const Shape &s, const void *v, const float *S0, void *o, float *ST,
+// lb: log beta [BH][T][V] of the value-side gate, nullable (beta = 1)
+hipError_t launch_fwd_main(const Shape &s, const void *v, const void *lb, const float *S0, void *o, float *ST,
                            const Work &w, hipStream_t st);
 hipError_t launch_bwd_dq(const Shape &s, const void *k, const void *la, const void *v,
                          const float *S0, const void *dO, const float *dST, void *dq,
@@ -48,7 +49,7 @@ hipError_t launch_bwd_dk(const Shape &s, const void *q, const void *k, const voi
 hipError_t launch_bwd_dv(const Shape &s, const void *dO, const float *dST, void *dv, float *dS0,
                          const Work &w, hipStream_t st);
 hipError_t launch_recurrent(const Shape &s, const void *q, const void *k, const void *v,
-                            const void *la, const float *S0, void *o, float *ST, hipStream_t st);
+                            const void *la, const void *lb, const float *S0, void *o, float *ST, hipStream_t st);
 // T == 0 edge: S_T = S0 (or 0); dS0 = dS_T (or 0).
 hipError_t launch_copy_state(int64_t n, const float *src, float *dst, hipStream_t st);
 

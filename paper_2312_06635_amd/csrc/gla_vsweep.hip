@@ -36,6 +36,14 @@
 // sets while chunk n computes; each lane's byte offsets are fixed for the
 // whole sweep (rows past the sequence end fall outside the buffer's range and
 // read as zero).
+//
+// Value-side gate (the general form G_t = alpha_t^T beta_t of App. C, forward
+// only): with E = the chunk-local inclusive cumsum of log beta per value
+// column (computed here, per chunk, in LDS) and Vh = V (.) exp(-E),
+//       O_n     = exp(E) (.) ((Q (.) Lambda)_n S_[n] + P_n Vh_n)
+//       S_[n+1] = (Diag(gamma_n) S_[n] + (K (.) Gamma)_n^T Vh_n) Diag(exp(E_last)),
+// which is exact; exp(-E) grows with the decay range of beta inside one chunk,
+// so that range must stay below ~80 (fp32 exponent), e.g. by a shorter chunk.
 #include "gla_common.hpp"
 #include "gla_launch.hpp"
 
@@ -56,6 +64,7 @@ struct SweepArgs {
   const void *X, *Y, *Z, *P;  // X: output operand, Y: update operand, Z: value tile source
   const float *gam;
   const float *R0;  // initial state (nullable)
+  const void *LB;   // log beta [BH][T][V] (value-side gate; the GB variant only)
   void *out;
   float *RN;        // final state (nullable)
   int BH, T, K, V, C, N, ntiles;
@@ -84,6 +93,12 @@ template <typename T, int KP, int CP> struct SweepLayout {
   static constexpr size_t offG = offP + sizeof(T) * CP * LDP;
   static constexpr size_t offO = offG + sizeof(float) * KP;
   static constexpr size_t total = offO + sizeof(f4) * 4 * NI * 64;
+  // value-side gate: log beta tile, its chunk-local cumsum E, scan partials
+  static constexpr int LDE = kTile + 4;
+  static constexpr size_t offLB = total;
+  static constexpr size_t offE = offLB + sizeof(T) * CP * LDZ;
+  static constexpr size_t offScan = offE + sizeof(float) * CP * LDE;
+  static constexpr size_t total_gb = offScan + sizeof(float) * 8 * kTile;
 };
 
 // Fragment whose reduction index runs down a column, like ld_col, but with the
@@ -111,8 +126,10 @@ __device__ __forceinline__ frag_t<T> ld_col_perm(const T *X, int ld, int r0, int
   }
 }
 
-template <typename T, int KP, int CP, bool REV>
+// GB: value-side gate (forward only).
+template <typename T, int KP, int CP, bool REV, bool GB>
 __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
+  static_assert(!(GB && REV), "the value-side gate has a forward sweep only");
   using L = SweepLayout<T, KP, CP>;
   constexpr int KH = KP / 2;     // key features per wave half
   constexpr int NKB = KH / 16;   // state accumulators per wave
@@ -126,6 +143,8 @@ __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
   T *sP = (T *)(smem + L::offP);
   float *sG = (float *)(smem + L::offG);
   f4 *sO = (f4 *)(smem + L::offO);
+  T *sLB = (T *)(smem + L::offLB);
+  float *sE = (float *)(smem + L::offE), *sScan = (float *)(smem + L::offScan);
 
   int bh, tile;
   xcd_map(a.BH, a.ntiles, bh, tile);
@@ -152,7 +171,7 @@ __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
   // sets, so the tiles of chunk it+2 are in flight while chunk it computes
   struct Stage {
     TileLd<T, CP, KP, kThreads> x, y;
-    TileLd<T, CP, kTile, kThreads> z;
+    TileLd<T, CP, kTile, kThreads> z, b;  // b: log beta (GB)
     TileLd<T, CP, CP, kThreads> p;
     float g;
   };
@@ -161,15 +180,18 @@ __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
   st0.y.init(K, C, K);
   st0.z.init(V, C, V - v0);
   st0.p.init(C, C, C);
+  if constexpr (GB) st0.b = st0.z;
   st1.x = st0.x;
   st1.y = st0.y;
   st1.z = st0.z;
   st1.p = st0.p;
+  if constexpr (GB) st1.b = st0.z;
   const int esz = sizeof(T);
   const uint32_t goff = (int)threadIdx.x < K ? 4u * threadIdx.x : 0x80000000u;  // gamma: lanes past K read 0
   const T *Xh = (const T *)a.X + (int64_t)bh * a.T * K;
   const T *Yh = (const T *)a.Y + (int64_t)bh * a.T * K;
   const T *Zh = (const T *)a.Z + (int64_t)bh * a.T * V + v0;
+  const T *LBh = GB ? (const T *)a.LB + (int64_t)bh * a.T * V + v0 : Zh;
   const T *Ph = (const T *)a.P + (int64_t)bh * N * C * C;
   const float *Gh = a.gam + (int64_t)bh * N * K;
   auto chunk_of = [&](int it) { return REV ? N - 1 - it : it; };
@@ -179,7 +201,11 @@ __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
     const uint32_t remK = rsrc_bytes((int64_t)(a.T - t0) * K * esz);
     if (part == 0) S.x.load(make_rsrc(Xh + (int64_t)t0 * K, remK));
     if (part == 1) S.y.load(make_rsrc(Yh + (int64_t)t0 * K, remK));
-    if (part == 2) S.z.load(make_rsrc(Zh + (int64_t)t0 * V, rsrc_bytes(((int64_t)(a.T - t0) * V - v0) * esz)));
+    if (part == 2) {
+      const uint32_t remV = rsrc_bytes(((int64_t)(a.T - t0) * V - v0) * esz);
+      S.z.load(make_rsrc(Zh + (int64_t)t0 * V, remV));
+      if constexpr (GB) S.b.load(make_rsrc(LBh + (int64_t)t0 * V, remV));
+    }
     if (part == 3) {
       S.p.load(make_rsrc(Ph + (int64_t)n * C * C, (uint32_t)(C * C * esz)));
       S.g = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(make_rsrc(Gh + (int64_t)n * K, (uint32_t)(K * 4)), goff, 0, 0));
@@ -198,8 +224,33 @@ __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
     S.y.store(sY, L::LDY);
     S.z.store(sZ, L::LDZ);
     S.p.store(sP, L::LDP);
+    if constexpr (GB) S.b.store(sLB, L::LDZ);
     if ((int)threadIdx.x < KP) sG[threadIdx.x] = S.g;
     __syncthreads();
+    if constexpr (GB) {
+      // E = inclusive cumsum of log beta down each column (thread: column c,
+      // rows RG grp .. +RG-1), then the value tile becomes Vh = V (.) exp(-E)
+      // in place.  Rows past the chunk or the sequence read log beta = 0.
+      constexpr int RG = CP / 8;
+      const int c = threadIdx.x & (kTile - 1), grp = threadIdx.x / kTile;
+      float part = 0.f;
+#pragma unroll
+      for (int r = 0; r < RG; ++r) part += (float)sLB[(grp * RG + r) * L::LDZ + c];
+      sScan[grp * kTile + c] = part;
+      __syncthreads();
+      float pre = 0.f;
+#pragma unroll
+      for (int g2 = 0; g2 < 8; ++g2)
+        if (g2 < grp) pre += sScan[g2 * kTile + c];
+#pragma unroll
+      for (int r = 0; r < RG; ++r) {
+        const int row = grp * RG + r;
+        pre += (float)sLB[row * L::LDZ + c];
+        sE[row * L::LDE + c] = pre;
+        sZ[row * L::LDZ + c] = cvt<T>((float)sZ[row * L::LDZ + c] * __expf(-pre));
+      }
+      __syncthreads();
+    }
 
     // output, transposed: acc[I] = R^T X^T over this wave's key features (a
     // wave past the last value column computes zeros).  The loads of chunk
@@ -238,7 +289,8 @@ __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
 #pragma unroll
         for (int I = 0; I < NI; ++I) sO[(cg * NI + I) * 64 + l] = acc[I];
       }
-      // state update: R <- gamma R + Y^T Z
+      // state update: R <- gamma R + Y^T Z (then, with the value-side gate,
+      // times the chunk decay exp(E_last) of this lane's value column)
       frag_t<T> zf[NSC];
 #pragma unroll
       for (int sc = 0; sc < NSC; ++sc) zf[sc] = ld_col<T>(sZ, L::LDZ, 32 * sc, cbase);
@@ -251,13 +303,23 @@ __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
         for (int sc = 0; sc < NSC; ++sc)
           R[kb] = mma<T>(R[kb], ld_col_perm<T>(sY, L::LDY, 32 * sc, c0, kb & 1), zf[sc]);
       }
+      if constexpr (GB) {
+        const float gb = __expf(sE[(CP - 1) * L::LDE + cbase + j]);
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) R[kb] *= gb;
+      }
     }
     __syncthreads();
     if (active && kh == 0) {
 #pragma unroll
       for (int I = 0; I < NI; ++I) {
-        const f4 o = acc[I] + sO[(cg * NI + I) * 64 + l];
+        f4 o = acc[I] + sO[(cg * NI + I) * 64 + l];
         const int row = 16 * I + j;
+        if constexpr (GB) {
+          const f4 e = *(const f4 *)(sE + row * L::LDE + cbase + 4 * g);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) o[r] *= __expf(e[r]);
+        }
         if (row < rv) {
           T *dst = outh + (int64_t)(t0 + row) * V + v0 + cbase + 4 * g;
           if constexpr (sizeof(T) == 2) {
@@ -291,7 +353,7 @@ int sweep_kp(const Shape &s) { return pow2_at_least(s.K, 64); }
 int sweep_cp(const Shape &s) { return s.C <= 32 ? 32 : 64; }
 
 template <typename T, int KP, int CP>
-size_t sweep_lds() { return SweepLayout<T, KP, CP>::total; }
+size_t sweep_lds() { return SweepLayout<T, KP, CP>::total_gb; }  // the larger, value-gate layout
 
 size_t sweep_lds(const Shape &s) {
   const int KP = sweep_kp(s), CP = sweep_cp(s);
@@ -306,17 +368,25 @@ size_t sweep_lds(const Shape &s) {
   return 0;
 }
 
-template <typename T, int KP, int CP, bool REV>
-hipError_t launch_sweep_t(const SweepArgs &a, hipStream_t st) {
+template <typename T, int KP, int CP, bool REV, bool GB>
+hipError_t launch_sweep_gb(const SweepArgs &a, hipStream_t st) {
   static bool attr = false;
-  const size_t lds = SweepLayout<T, KP, CP>::total;
+  const size_t lds = GB ? SweepLayout<T, KP, CP>::total_gb : SweepLayout<T, KP, CP>::total;
   if (!attr) {
-    (void)hipFuncSetAttribute((const void *)sweep_kernel<T, KP, CP, REV>,
+    (void)hipFuncSetAttribute((const void *)sweep_kernel<T, KP, CP, REV, GB>,
                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     attr = true;
   }
-  hipLaunchKernelGGL((sweep_kernel<T, KP, CP, REV>), dim3(a.BH * a.ntiles), dim3(kThreads), lds, st, a);
+  hipLaunchKernelGGL((sweep_kernel<T, KP, CP, REV, GB>), dim3(a.BH * a.ntiles), dim3(kThreads), lds, st, a);
   return hipGetLastError();
+}
+
+template <typename T, int KP, int CP, bool REV>
+hipError_t launch_sweep_t(const SweepArgs &a, hipStream_t st) {
+  if constexpr (!REV) {
+    if (a.LB) return launch_sweep_gb<T, KP, CP, false, true>(a, st);
+  }
+  return launch_sweep_gb<T, KP, CP, REV, false>(a, st);
 }
 
 template <typename T, bool REV>
@@ -344,10 +414,10 @@ SweepArgs sweep_args(const Shape &s) {
 size_t lds_fwd_main(const Shape &s) { return sweep_lds(s); }
 size_t lds_bwd_dv(const Shape &s) { return sweep_lds(s); }
 
-hipError_t launch_fwd_main(const Shape &s, const void *v, const float *S0, void *o, float *ST,
+hipError_t launch_fwd_main(const Shape &s, const void *v, const void *lb, const float *S0, void *o, float *ST,
                            const Work &w, hipStream_t st) {
   SweepArgs a = sweep_args(s);
-  a.X = w.Qt; a.Y = w.Kt; a.Z = v; a.P = w.P; a.gam = w.gam; a.R0 = S0; a.out = o; a.RN = ST;
+  a.X = w.Qt; a.Y = w.Kt; a.Z = v; a.P = w.P; a.gam = w.gam; a.R0 = S0; a.out = o; a.RN = ST; a.LB = lb;
   return s.io == IO_BF16 ? dispatch_sweep<bf16, false>(s, a, st) : dispatch_sweep<float, false>(s, a, st);
 }
 

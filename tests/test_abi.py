@@ -28,9 +28,10 @@ def declared_functions():
 
 
 def test_header_declares_the_boundary():
-    assert declared_functions() == ["gla_chunk_bwd", "gla_chunk_fwd", "gla_output_gate_bwd",
-                                    "gla_output_gate_fwd", "gla_output_gate_workspace_bytes",
-                                    "gla_recurrent_fwd", "gla_status_string", "gla_workspace_bytes"]
+    assert declared_functions() == ["gla_chunk_bwd", "gla_chunk_fwd", "gla_chunk_fwd_general",
+                                    "gla_output_gate_bwd", "gla_output_gate_fwd",
+                                    "gla_output_gate_workspace_bytes", "gla_recurrent_fwd",
+                                    "gla_recurrent_fwd_general", "gla_status_string", "gla_workspace_bytes"]
 
 
 def test_every_declared_symbol_is_exported(L):
@@ -123,6 +124,18 @@ def test_null_problem_and_pointers(L):
     p = P()
     assert L.gla_recurrent_fwd(None, 1, 1, 1, 1, None, 1, None, None) == gla.GLA_ERR_NULL
     assert L.gla_recurrent_fwd(ctypes.byref(p), None, 1, 1, 1, None, 1, None, None) == gla.GLA_ERR_NULL
+
+
+def test_general_form_entry_points_validate_like_the_others(L):
+    p = P()
+    args = lambda ptr: (ptr, ptr, ptr, ptr, ptr, None, ptr, None)
+    assert L.gla_chunk_fwd_general(None, *args(1), 1, 1 << 40, None) == gla.GLA_ERR_NULL
+    assert L.gla_chunk_fwd_general(ctypes.byref(P(dk=24)), *args(1), 1, 1 << 40, None) == gla.GLA_ERR_UNSUPPORTED
+    assert L.gla_chunk_fwd_general(ctypes.byref(p), *args(None), 1, 1 << 40, None) == gla.GLA_ERR_NULL
+    assert L.gla_chunk_fwd_general(ctypes.byref(p), *args(1), None, 0, None) == gla.GLA_ERR_WORKSPACE
+    assert L.gla_recurrent_fwd_general(None, *args(1), None) == gla.GLA_ERR_NULL
+    assert L.gla_recurrent_fwd_general(ctypes.byref(P(io=9)), *args(1), None) == gla.GLA_ERR_DTYPE
+    assert L.gla_recurrent_fwd_general(ctypes.byref(p), *args(None), None) == gla.GLA_ERR_NULL
 
 
 def test_workspace_is_checked(L):

@@ -329,6 +329,55 @@ def test_scalar_gate_with_epilogue(io):
     assert not bad, bad
 
 
+GG_CASES = [
+    ("f32", 1, 2, 150, 64, 128, 64, 16, "mild"),
+    ("f32", 1, 1, 70, 32, 1024, 16, 16, "mild"),      # chunk shorter than the 32-row tiles
+    ("bf16", 1, 2, 200, 256, 512, 64, 16, "mild"),
+    ("bf16", 2, 1, 100, 48, 80, 64, 16, "strong"),    # partial value tile, ~32 of decay per chunk
+    ("bf16", 1, 2, 96, 128, 256, 32, 8, "mild"),
+]
+
+
+@pytest.mark.parametrize("io,B,H,T,K,V,C,c,decay", GG_CASES,
+                         ids=[f"{x[0]}_K{x[4]}_V{x[5]}_T{x[3]}_C{x[6]}_{x[8]}" for x in GG_CASES])
+def test_general_gate_forward(io, B, H, T, K, V, C, c, decay):
+    """The general form G_t = alpha_t^T beta_t (App. C), forward: chunkwise and
+    recurrent outputs and final state against the oracle; beta = 1 is
+    bit-identical to the plain calls."""
+    g = gla()
+    cfg = small_case(f"gg_{io}_{K}_{V}_{T}", io, B, H, T, K, V, C, c, 90 + K + T, s0_std=0.1)
+    inp = W.make_inputs(cfg)
+    gen = torch.Generator().manual_seed(91 + V)
+    if decay == "strong":
+        lb = -torch.rand(B, H, T, V, generator=gen)
+    else:
+        lb = torch.nn.functional.logsigmoid(torch.randn(B, H, T, V, generator=gen) + 2.0)
+    inp["log_beta"] = lb.to(inp["q"].dtype)
+    d = to_dev(inp)
+    o, ST = g.chunk_fwd(d["q"], d["k"], d["v"], d["log_alpha"], C, c, S0=d["S0"], output_final_state=True,
+                        log_beta=d["log_beta"])
+    r, R = g.recurrent_fwd(d["q"], d["k"], d["v"], d["log_alpha"], S0=d["S0"], output_final_state=True,
+                           log_beta=d["log_beta"])
+    zero = torch.zeros_like(d["log_beta"])
+    o1, S1 = g.chunk_fwd(d["q"], d["k"], d["v"], d["log_alpha"], C, c, S0=d["S0"], output_final_state=True,
+                         log_beta=zero)
+    o0, S0_ = g.chunk_fwd(d["q"], d["k"], d["v"], d["log_alpha"], C, c, S0=d["S0"], output_final_state=True)
+    r1, R1 = g.recurrent_fwd(d["q"], d["k"], d["v"], d["log_alpha"], S0=d["S0"], output_final_state=True,
+                             log_beta=zero)
+    r0, R0 = g.recurrent_fwd(d["q"], d["k"], d["v"], d["log_alpha"], S0=d["S0"], output_final_state=True)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o0) and torch.equal(S1, S0_), "chunkwise, beta = 1"
+    assert torch.equal(r1, r0) and torch.equal(R1, R0), "recurrent, beta = 1"
+    idx = list(range(B * H))
+    ro, rST = oracle.general_gate_fwd(*(heads(inp[n], idx) for n in ("q", "k", "v", "log_alpha", "log_beta")),
+                                      heads(inp["S0"], idx))
+    errs = {"o": rel(heads(o, idx), ro), "S_T": rel(heads(ST, idx), rST), "rec_o": rel(heads(r, idx), ro),
+            "rec_S_T": rel(heads(R, idx), rST)}
+    say("general gate", cfg["name"], decay, {k2: f"{v2:.2e}" for k2, v2 in errs.items()})
+    bad = {k2: v2 for k2, v2 in errs.items() if not v2 <= TOL[io]}
+    assert not bad, bad
+
+
 OG_CASES = [("f32", 2, 3, 70, 48, True), ("f32", 1, 2, 130, 1024, False), ("bf16", 2, 4, 100, 512, True),
             ("bf16", 1, 2, 64, 256, False), ("bf16", 1, 1, 5, 80, True)]
 
