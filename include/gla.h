@@ -120,10 +120,11 @@ typedef struct {
                       * infinite or NaN values return GLA_ERR_SHAPE.         */
 } gla_problem;
 
-/* Bytes of device workspace gla_chunk_fwd (op = 0) or gla_chunk_bwd (op = 1)
- * needs for this problem; 0 if the problem is invalid.  The backward's
- * workspace layout begins with the forward's, so a buffer sized for op = 1
- * can be passed to both (required for GLA_FLAG_REUSE_FWD_WORKSPACE). */
+/* Bytes of device workspace gla_chunk_fwd (op = 0), gla_chunk_bwd (op = 1)
+ * or gla_chunk_bwd_general (op = 2) needs for this problem; 0 if the problem
+ * is invalid.  Each layout begins with the previous one, so a buffer sized
+ * for a larger op can be passed to the smaller ones (required for
+ * GLA_FLAG_REUSE_FWD_WORKSPACE; gla_chunk_fwd_general uses op 0's). */
 size_t gla_workspace_bytes(const gla_problem *prob, int op);
 
 /* Forward, chunkwise form (Sec. 4.2 / 4.3; the non-materialized state pass of
@@ -165,14 +166,29 @@ gla_status gla_recurrent_fwd(const gla_problem *prob, const void *q, const void 
  * for those calls.  The chunkwise form normalises the value side per chunk:
  * the decay of beta accumulated over one chunk of one value column,
  * -sum log beta, must stay below ~80, else outputs overflow (a shorter chunk
- * widens the range; the recurrent form has no such limit).  Forward only: the
- * backward of the general form is not provided. */
+ * widens the range; the recurrent form has no such limit). */
 gla_status gla_chunk_fwd_general(const gla_problem *prob, const void *q, const void *k, const void *v,
                                  const void *log_alpha, const void *log_beta, const float *S0, void *o,
                                  float *S_T, void *workspace, size_t workspace_bytes, void *stream);
 gla_status gla_recurrent_fwd_general(const gla_problem *prob, const void *q, const void *k,
                                      const void *v, const void *log_alpha, const void *log_beta,
                                      const float *S0, void *o, float *S_T, void *stream);
+
+/* Backward of gla_chunk_fwd_general for L = sum(o * dO) + sum(S_T * dS_T):
+ * the outputs of gla_chunk_bwd plus dlog_beta ([B, H, T, d_v], nullable) =
+ * revcumsum(o * dO - v * dv) + colsum(S_T * dS_T) (App. C), which needs the
+ * forward's output o (required when dlog_beta is wanted).  log_beta is
+ * required here.  The key gate may be scalar (GLA_FLAG_SCALAR_GATE) but not
+ * the gate epilogue (gate_tau > 0: GLA_ERR_UNSUPPORTED).  Workspace: at least
+ * gla_workspace_bytes(prob, 2) bytes; GLA_FLAG_REUSE_FWD_WORKSPACE as for
+ * gla_chunk_bwd.  Stage selector: 1 = key-gate factors (as gla_chunk_bwd),
+ * 2 = value-gate operands, 3 = dq sweep, 4 = dk sweep, 5 = dv sweep, 6 = the
+ * value-gate gradient. */
+gla_status gla_chunk_bwd_general(const gla_problem *prob, const void *q, const void *k, const void *v,
+                                 const void *log_alpha, const void *log_beta, const float *S0, const void *o,
+                                 const void *dO, const float *dS_T, void *dq, void *dk, void *dv,
+                                 void *dlog_alpha, void *dlog_beta, float *dS0, void *workspace,
+                                 size_t workspace_bytes, void *stream);
 
 /* Output side of the layer (Sec. 4.4): per head and row, y_t = Swish(g_t) (.)
  * LN(o_t) with LN(x) = w (.) (x - mean(x)) / sqrt(var(x) + eps) + b over the

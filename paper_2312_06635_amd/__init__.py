@@ -21,7 +21,7 @@ __all__ = [
     "chunk_fwd", "chunk_bwd", "recurrent_fwd", "workspace_bytes", "GlaError", "library_path",
     "GLA_OK", "GLA_ERR_NULL", "GLA_ERR_SHAPE", "GLA_ERR_DTYPE", "GLA_ERR_UNSUPPORTED",
     "GLA_ERR_WORKSPACE", "GLA_ERR_HIP", "FLAG_REUSE_FWD_WORKSPACE", "FLAG_SCALAR_GATE", "GlaProblem", "lib",
-    "output_gate_fwd", "output_gate_bwd", "output_gate_workspace_bytes",
+    "output_gate_fwd", "output_gate_bwd", "output_gate_workspace_bytes", "general_workspace_bytes",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -72,6 +72,8 @@ def lib():
         L.gla_chunk_fwd_general.restype = i32
         L.gla_recurrent_fwd_general.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.gla_recurrent_fwd_general.restype = i32
+        L.gla_chunk_bwd_general.argtypes = [P] + [vp] * 16 + [sz, vp]
+        L.gla_chunk_bwd_general.restype = i32
         L.gla_recurrent_fwd.restype = i32
         L.gla_status_string.argtypes = [i32]
         L.gla_status_string.restype = ctypes.c_char_p
@@ -147,6 +149,13 @@ def workspace_bytes(B, H, T, dk, dv, chunk, subchunk, dtype=torch.bfloat16, op=1
     return int(lib().gla_workspace_bytes(ctypes.byref(p), op))
 
 
+def general_workspace_bytes(B, H, T, dk, dv, chunk, subchunk, dtype=torch.bfloat16, scalar_gate=False) -> int:
+    """Workspace bytes for the general form's backward (op=2); enough for
+    every other call on the same problem too."""
+    p = GlaProblem(B, H, T, dk, dv, chunk, subchunk, _io_code(dtype), FLAG_SCALAR_GATE if scalar_gate else 0)
+    return int(lib().gla_workspace_bytes(ctypes.byref(p), 2))
+
+
 def _workspace(p, op, dev, workspace):
     need = int(lib().gla_workspace_bytes(ctypes.byref(p), op))
     if workspace is None:
@@ -200,7 +209,7 @@ def chunk_fwd(q, k, v, log_alpha, chunk=64, subchunk=16, S0=None, output_final_s
 
 def chunk_bwd(q, k, v, log_alpha, dO, chunk=64, subchunk=16, S0=None, dST=None,
               want_dS0=False, workspace=None, reuse_fwd_workspace=False, stage=0, out=None,
-              gate_tau=0.0):
+              gate_tau=0.0, log_beta=None, o=None):
     """Chunkwise GLA backward for L = sum(o * dO) + sum(S_T * dS_T).
 
     Returns dict(dq, dk, dv, dlog_alpha, dS0); dlog_alpha is None when
@@ -208,8 +217,13 @@ def chunk_bwd(q, k, v, log_alpha, dO, chunk=64, subchunk=16, S0=None, dST=None,
     ([B, H, T] for a scalar gate), and dL/dz when gate_tau > 0
     (log_alpha then holds the gate pre-activation z).  With reuse_fwd_workspace the
     given workspace must still hold what chunk_fwd left for the same inputs.
-    stage and out as in chunk_fwd (out is a dict shaped like the result)."""
+    stage and out as in chunk_fwd (out is a dict shaped like the result).
+    log_beta: the general form's value-side gate (App. C); the result then
+    also holds dlog_beta, which needs the forward's output o (without o it is
+    None); the workspace must be sized for op=2 (general_workspace_bytes)."""
     _check(q, k, v, log_alpha, extra=(("dO", dO, v.shape[3]),), states=(("S0", S0), ("dST", dST)))
+    _check_beta(log_beta, v)
+    _check_beta(o, v)
     B, H, T, dk = q.shape
     dv = v.shape[3]
     flags = (FLAG_REUSE_FWD_WORKSPACE if reuse_fwd_workspace else 0) | (stage << STAGE_SHIFT)
@@ -224,6 +238,16 @@ def chunk_bwd(q, k, v, log_alpha, dO, chunk=64, subchunk=16, S0=None, dST=None,
         dvv = torch.empty_like(v)
         dla = torch.empty_like(log_alpha) if log_alpha is not None else None
         dS0 = torch.empty(B, H, dk, dv, dtype=torch.float32, device=q.device) if want_dS0 else None
+    if log_beta is not None:
+        dlb = (out.get("dlog_beta") if out is not None else torch.empty_like(log_beta)) if o is not None else None
+        ws = _workspace(p, 2, q.device, workspace)
+        st = lib().gla_chunk_bwd_general(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha),
+                                         _ptr(log_beta), _ptr(S0), _ptr(o), _ptr(dO), _ptr(dST), _ptr(dq),
+                                         _ptr(dkk), _ptr(dvv), _ptr(dla), _ptr(dlb), _ptr(dS0), _ptr(ws),
+                                         ws.numel() * ws.element_size(), _stream(q.device))
+        if st != GLA_OK:
+            raise GlaError(st, "gla_chunk_bwd_general")
+        return {"dq": dq, "dk": dkk, "dv": dvv, "dlog_alpha": dla, "dS0": dS0, "dlog_beta": dlb}
     ws = _workspace(p, 1, q.device, workspace)
     st = lib().gla_chunk_bwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(S0),
                              _ptr(dO), _ptr(dST), _ptr(dq), _ptr(dkk), _ptr(dvv), _ptr(dla),

@@ -59,8 +59,9 @@ gla_status check_lds(const Shape &s, bool bwd) {
   return GLA_OK;
 }
 
-// Workspace layout; op 1 extends op 0.  Returns the total byte count and, if
-// base is non-null, the region pointers.
+// Workspace layout; op 1 extends op 0, op 2 (the general form's backward)
+// extends op 1.  Returns the total byte count and, if base is non-null, the
+// region pointers.
 size_t layout(const Shape &s, int op, char *base, Work *w) {
   const size_t es = s.esz();
   const size_t rows = (size_t)s.BH * s.T, chunks = (size_t)s.BH * s.N;
@@ -76,15 +77,24 @@ size_t layout(const Shape &s, int op, char *base, Work *w) {
   void *gam = take(chunks * s.K * sizeof(float));
   void *wflag = take(chunks * 4);
   void *dP = nullptr, *cST = nullptr, *dq_lo = nullptr, *dla_part = nullptr;
-  if (op == 1) {
+  void *Vh = nullptr, *Oh = nullptr, *gb = nullptr, *bpart = nullptr, *colpart = nullptr;
+  if (op >= 1) {
     dP = take(chunks * s.C * s.C * sizeof(float));
     cST = take((size_t)s.BH * s.K * sizeof(float));
     if (s.io == gla::IO_BF16) dq_lo = take(rows * s.K * 2);
     if (s.sgate) dla_part = take(rows * ((s.K + 31) / 32) * sizeof(float));
   }
+  if (op == 2) {
+    Vh = take(rows * s.V * es);
+    Oh = take(rows * s.V * es);
+    gb = take(chunks * s.V * sizeof(float));
+    bpart = take(chunks * s.V * sizeof(float));
+    colpart = take((size_t)s.BH * ((s.K + 31) / 32) * s.V * sizeof(float));
+  }
   if (w) {
     w->Qt = Qt; w->Kt = Kt; w->P = P; w->gam = (float *)gam; w->wflag = (unsigned char *)wflag;
     w->dP = (float *)dP; w->cST = (float *)cST; w->dq_lo = dq_lo; w->dla_part = (float *)dla_part;
+    w->Vh = Vh; w->Oh = Oh; w->gb = (float *)gb; w->bpart = (float *)bpart; w->colpart = (float *)colpart;
   }
   return off;
 }
@@ -108,7 +118,7 @@ GLA_EXPORT const char *gla_status_string(gla_status st) {
 
 GLA_EXPORT size_t gla_workspace_bytes(const gla_problem *prob, int op) {
   Shape s;
-  if (make_shape(prob, s) != GLA_OK || (op != 0 && op != 1)) return 0;
+  if (make_shape(prob, s) != GLA_OK || op < 0 || op > 2) return 0;
   return layout(s, op, nullptr, nullptr);
 }
 
@@ -205,7 +215,45 @@ GLA_EXPORT gla_status gla_chunk_bwd(const gla_problem *prob, const void *q, cons
   if (e == hipSuccess && run(2)) e = gla::launch_bwd_dq(s, k, log_alpha, v, S0, dO, dS_T, dq, w, hs);
   if (e == hipSuccess && run(3))
     e = gla::launch_bwd_dk(s, q, k, log_alpha, v, dO, dS_T, dq, dk, dlog_alpha, w, hs);
-  if (e == hipSuccess && run(4)) e = gla::launch_bwd_dv(s, dO, dS_T, dv, dS0, w, hs);
+  if (e == hipSuccess && run(4)) e = gla::launch_bwd_dv(s, dO, nullptr, dS_T, dv, dS0, w, hs);
+  return hip_status(e);
+}
+
+GLA_EXPORT gla_status gla_chunk_bwd_general(const gla_problem *prob, const void *q, const void *k,
+                                            const void *v, const void *log_alpha, const void *log_beta,
+                                            const float *S0, const void *o, const void *dO, const float *dS_T,
+                                            void *dq, void *dk, void *dv, void *dlog_alpha, void *dlog_beta,
+                                            float *dS0, void *workspace, size_t workspace_bytes, void *stream) {
+  Shape s;
+  gla_status st = make_shape(prob, s);
+  if (st != GLA_OK) return st;
+  if (!log_alpha) s.inv_tau = 0.f;
+  if (s.inv_tau != 0.f) return GLA_ERR_UNSUPPORTED;  // no key-gate epilogue with the value-side gate
+  if ((st = check_lds(s, true)) != GLA_OK) return st;
+  const unsigned stage = (prob->flags & GLA_STAGE_MASK) >> GLA_STAGE_SHIFT;
+  if (stage > 6) return GLA_ERR_SHAPE;
+  const bool any = (int64_t)s.BH * s.T > 0;
+  if (any && (!q || !k || !v || !log_beta || !dO || !dq || !dk || !dv)) return GLA_ERR_NULL;
+  if (any && dlog_beta && !o) return GLA_ERR_NULL;
+  const size_t need = layout(s, 2, nullptr, nullptr);
+  if (any && (!workspace || workspace_bytes < need)) return GLA_ERR_WORKSPACE;
+  hipStream_t hs = (hipStream_t)stream;
+  if (s.BH == 0) return GLA_OK;
+  if (s.T == 0)
+    return hip_status(gla::launch_copy_state((int64_t)s.BH * s.K * s.V, dS_T, dS0, hs));
+  auto run = [stage](unsigned k) { return stage == 0 || stage == k; };
+  Work w;
+  layout(s, 2, (char *)workspace, &w);
+  hipError_t e = hipSuccess;
+  if (run(1) && !(prob->flags & GLA_FLAG_REUSE_FWD_WORKSPACE))
+    e = gla::launch_prep(s, q, k, log_alpha, w, hs);
+  if (e == hipSuccess && run(2)) e = gla::launch_beta_prep(s, v, dO, log_beta, w, hs);
+  if (e == hipSuccess && run(3)) e = gla::launch_bwd_dq(s, k, log_alpha, w.Vh, S0, w.Oh, dS_T, dq, w, hs, true);
+  if (e == hipSuccess && run(4))
+    e = gla::launch_bwd_dk(s, q, k, log_alpha, w.Vh, w.Oh, dS_T, dq, dk, dlog_alpha, w, hs, true);
+  if (e == hipSuccess && run(5)) e = gla::launch_bwd_dv(s, dO, log_beta, dS_T, dv, dS0, w, hs);
+  if (e == hipSuccess && run(6) && dlog_beta)
+    e = gla::launch_beta_grad(s, o, dO, v, dv, dS_T != nullptr, dlog_beta, w, hs);
   return hip_status(e);
 }
 

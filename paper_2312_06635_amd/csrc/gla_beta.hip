@@ -1,0 +1,142 @@
+// gla_beta.hip -- value-side gate of the general form (App. C, G_t =
+// alpha_t^T beta_t) in the backward: the chunk-local operands the sweeps use
+// and the gate gradient
+//     dlog beta_t = sum_{i >= t} (o_i (.) do_i - v_i (.) dv_i) + colsum(S_T (.) dS_T).
+// With E the chunk-local inclusive cumsum of log beta per value column,
+//     Vh = V (.) exp(-E),   Oh = dO (.) exp(E),   gb = exp(E_last) per chunk,
+// the backward sweeps keep the structure of the alpha-only layer (dP = Oh Vh^T
+// masked, dq from Oh S^T, dk from Vh (dS gb)^T, the state columns decaying by
+// gb).  Every kernel here is elementwise along value columns: a thread owns
+// one (batch-head, chunk, value column) and walks the chunk's rows, so loads
+// and stores are coalesced across threads.
+#include "gla_common.hpp"
+#include "gla_launch.hpp"
+
+namespace gla {
+
+namespace {
+
+struct BetaArgs {
+  const void *v, *dO, *lb, *o, *dv;
+  void *Vh, *Oh, *dlb;
+  float *gb, *part;
+  const float *colpart;  // [BH][KT][V] per key tile colsum(S_T dS_T), nullable
+  int64_t n;             // BH N V threads
+  int T, V, C, N, KT;
+};
+
+struct Cell {
+  int64_t base;  // element offset of the chunk's first row in this column
+  int64_t cn;    // (bh, chunk) index
+  int rows, col;
+};
+
+__device__ __forceinline__ Cell cell_of(const BetaArgs &a, int64_t i) {
+  Cell c;
+  c.col = (int)(i % a.V);
+  const int64_t r = i / a.V;
+  const int n = (int)(r % a.N);
+  const int64_t bh = r / a.N;
+  const int t0 = n * a.C;
+  c.rows = min(a.C, a.T - t0);
+  c.base = (bh * a.T + t0) * a.V + c.col;
+  c.cn = bh * a.N + n;
+  return c;
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256) beta_prep_kernel(BetaArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= a.n) return;
+  const Cell c = cell_of(a, i);
+  const T *lb = (const T *)a.lb + c.base, *v = (const T *)a.v + c.base, *dO = (const T *)a.dO + c.base;
+  T *Vh = (T *)a.Vh + c.base, *Oh = (T *)a.Oh + c.base;
+  float E = 0.f;
+#pragma unroll 4
+  for (int r = 0; r < c.rows; ++r) {
+    const int64_t o = (int64_t)r * a.V;
+    E += (float)lb[o];
+    Vh[o] = cvt<T>((float)v[o] * __expf(-E));
+    Oh[o] = cvt<T>((float)dO[o] * __expf(E));
+  }
+  a.gb[c.cn * a.V + c.col] = __expf(E);
+}
+
+// Chunk sums of o do - v dv (dv final), and the chunk's E_last.
+template <typename T>
+__global__ void __launch_bounds__(256) beta_grad_sum_kernel(BetaArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= a.n) return;
+  const Cell c = cell_of(a, i);
+  const T *o = (const T *)a.o + c.base, *dO = (const T *)a.dO + c.base;
+  const T *v = (const T *)a.v + c.base, *dv = (const T *)a.dv + c.base;
+  float s = 0.f;
+#pragma unroll 4
+  for (int r = 0; r < c.rows; ++r) {
+    const int64_t e = (int64_t)r * a.V;
+    s += (float)o[e] * (float)dO[e] - (float)v[e] * (float)dv[e];
+  }
+  a.part[c.cn * a.V + c.col] = s;
+}
+
+// Reverse cumsum: the carry into chunk n is the final-state term plus the
+// chunk sums of every later chunk (added in chunk order).
+template <typename T>
+__global__ void __launch_bounds__(256) beta_grad_scan_kernel(BetaArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= a.n) return;
+  const Cell c = cell_of(a, i);
+  const int64_t bh = c.cn / a.N;
+  const int n = (int)(c.cn - bh * a.N);
+  float carry = 0.f;
+  if (a.colpart)
+    for (int kt = 0; kt < a.KT; ++kt) carry += a.colpart[(bh * a.KT + kt) * a.V + c.col];
+  for (int m = a.N - 1; m > n; --m) carry += a.part[(bh * a.N + m) * a.V + c.col];
+  const T *o = (const T *)a.o + c.base, *dO = (const T *)a.dO + c.base;
+  const T *v = (const T *)a.v + c.base, *dv = (const T *)a.dv + c.base;
+  T *dlb = (T *)a.dlb + c.base;
+  for (int r = c.rows - 1; r >= 0; --r) {
+    const int64_t e = (int64_t)r * a.V;
+    carry += (float)o[e] * (float)dO[e] - (float)v[e] * (float)dv[e];
+    dlb[e] = cvt<T>(carry);
+  }
+}
+
+template <typename T>
+hipError_t beta_launch(int which, const BetaArgs &a, hipStream_t st) {
+  const unsigned blocks = (unsigned)((a.n + 255) / 256);
+  if (which == 0) hipLaunchKernelGGL(beta_prep_kernel<T>, dim3(blocks), dim3(256), 0, st, a);
+  if (which == 1) hipLaunchKernelGGL(beta_grad_sum_kernel<T>, dim3(blocks), dim3(256), 0, st, a);
+  if (which == 2) hipLaunchKernelGGL(beta_grad_scan_kernel<T>, dim3(blocks), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+BetaArgs beta_args(const Shape &s) {
+  BetaArgs a{};
+  a.n = (int64_t)s.BH * s.N * s.V;
+  a.T = s.T; a.V = s.V; a.C = s.C; a.N = s.N; a.KT = (s.K + 31) / 32;
+  return a;
+}
+
+}  // namespace
+
+hipError_t launch_beta_prep(const Shape &s, const void *v, const void *dO, const void *lb, const Work &w,
+                            hipStream_t st) {
+  BetaArgs a = beta_args(s);
+  a.v = v; a.dO = dO; a.lb = lb; a.Vh = w.Vh; a.Oh = w.Oh; a.gb = w.gb;
+  if (a.n == 0) return hipSuccess;
+  return s.io == IO_BF16 ? beta_launch<bf16>(0, a, st) : beta_launch<float>(0, a, st);
+}
+
+hipError_t launch_beta_grad(const Shape &s, const void *o, const void *dO, const void *v, const void *dv,
+                            const bool with_final, void *dlb, const Work &w, hipStream_t st) {
+  BetaArgs a = beta_args(s);
+  a.o = o; a.dO = dO; a.v = v; a.dv = dv; a.dlb = dlb; a.part = w.bpart;
+  a.colpart = with_final ? w.colpart : nullptr;
+  if (a.n == 0) return hipSuccess;
+  hipError_t e = s.io == IO_BF16 ? beta_launch<bf16>(1, a, st) : beta_launch<float>(1, a, st);
+  if (e != hipSuccess) return e;
+  return s.io == IO_BF16 ? beta_launch<bf16>(2, a, st) : beta_launch<float>(2, a, st);
+}
+
+}  // namespace gla

@@ -36,6 +36,13 @@
 // For bf16 the state operand, the gated update operand and the dq hand-off are
 // split into bf16 hi + lo so that the gate gradient's long reverse sum keeps
 // fp32 accuracy.
+//
+// General form (GB; App. C, a value-side gate beta as well): v and dO arrive
+// as Vh = V (.) exp(-E) and Oh = dO (.) exp(E) (E the chunk-local cumsum of
+// log beta, formed by gla_beta.hip), and the state's value rows decay by
+// gb = exp(E_last) per chunk: S_[n+1] = (gamma S_[n] + (K (.) Gamma)^T Vh) gb
+// in the dq sweep, D = dS_[n+1] gb before the dk sweep's products; the chunk's
+// gb row is staged in the intra-output tile, which is free during the slabs.
 #include <type_traits>
 
 #include "gla_common.hpp"
@@ -57,6 +64,8 @@ struct KsArgs {
   void *dq, *dq_lo, *dk, *dla;
   float *dP, *cST;
   float *dla_part;  // scalar gate: [BH][KT][T] per-tile feature sums of the gate gradient
+  const float *gbv; // general form: [BH][N][V] chunk decays exp(E_last) of the value-side gate
+  float *colpart;   // general form: [BH][KT][V] per-tile colsum(S_T (.) dS_T)
   int BH, T, K, V, C, N, KT;
   int sg;         // scalar gate: la is [BH][T], one value per step shared by every feature
   float inv_tau;  // gate epilogue (0: la holds log alpha)
@@ -387,7 +396,7 @@ __device__ __forceinline__ void partials_add(const f16v (&acc)[2], float *sRed, 
 }
 
 // ============================================================== dq sweep
-template <typename T, int CP, int NSL, bool PRE>
+template <typename T, int CP, int NSL, bool PRE, bool GB>
 __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   using L = KsLayout<T, CP>;
   constexpr int VS = L::VS, NB = L::NB, NRG = L::NRG, NST = CP / 16, NTT = CP / 32;
@@ -443,6 +452,18 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   // (C is a multiple of 4: a thread's four rows are all inside or all outside)
   const uint32_t sbase = (fthr && 4 * frg < C && fv) ? (uint32_t)(4 * frg * esz) : 0x80000000u;
   uint32_t fin_la[4], fin_k[4];
+  // general form: the chunk's gb row (value v held by thread v mod 512)
+  float gbr[2];
+  auto fetch_gb = [&](int n) {
+    const auto rs = make_rsrc(a.gbv + ((int64_t)bh * N + n) * V, (uint32_t)(V * 4));
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      gbr[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (uint32_t)((tid + kKT * i) * 4), 0, 0));
+  };
+  auto stage_gb = [&]() {  // into the intra-output tile (>= 1152 floats, free until the intra task)
+#pragma unroll
+    for (int i = 0; i < 2; ++i) sOr[tid + kKT * i] = gbr[i];
+  };
   auto fetch_factors = [&](int n) {
     const int t0 = n * C;
     const uint32_t bytes = rsrc_bytes((int64_t)(a.T - t0) * K * esz);
@@ -455,6 +476,7 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
       fin_la[i] = ld_elem<T>(rs_la, gate_off<T>(a.sg, eoff[i], sbase, i));
       fin_k[i] = ld_elem<T>(rs_k, eoff[i]);
     }
+    if constexpr (GB) fetch_gb(n);
   };
   TileLd<T, CP, VS, kKT> pv, pd;
   pv.init(V, C, VS);
@@ -526,6 +548,7 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
       *(f4 *)(sBloc + fk * L::LDT + 4 * frg) = bl4;
       publish_decays<NB, L::LDRG>(sSc, sEt, sG, sGp, f, f.pre, frg, fk, fv);
     }
+    if constexpr (GB) stage_gb();
     // unconditional (the last chunk re-reads itself) so that the wait counts
     // for the slab prefetch below stay exact
     fetch_factors(min(n + 1, N - 1));
@@ -586,6 +609,13 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
         };
         if (dpw) slab_products(std::true_type{});
         else slab_products(std::false_type{});
+        if constexpr (GB) {
+          // S_[n+1] = (gamma S_[n] + K~^T Vh) gb, by value row
+          if (sw) {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) S[sl][e] *= sOr[sl * VS + 32 * w + acc_value(e, g)];
+          }
+        }
       }
       __syncthreads();
     }
@@ -684,6 +714,22 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
           if (vv < V && kq < K) part += S[sl][e] * a.dST[((int64_t)bh * K + kq) * V + vv];
         }
     }
+    if constexpr (GB) {
+      // colsum(S_T (.) dS_T) over this tile's features, per value (all waves
+      // take part in the half-wave sums; waves without state add zeros)
+      const auto rs_c = make_rsrc(a.colpart + ((int64_t)bh * a.KT + kt) * V, (uint32_t)(V * 4));
+#pragma unroll
+      for (int sl = 0; sl < NSL; ++sl)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int vv = sl * VS + 32 * w + acc_value(e, g), kq = k0 + j;
+          const float x = (sw && vv < V && kq < K) ? S[sl][e] * a.dST[((int64_t)bh * K + kq) * V + vv] : 0.f;
+          const float cs = half_wave_sum(x);
+          if (j == 0 && sw)
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, cs), rs_c,
+                                                  vv < V ? (uint32_t)(vv * 4) : 0x80000000u, 0, 0);
+        }
+    }
     part += __shfl_xor(part, 32);
     if (g == 0) sRedS[w * kKF + j] = part;
     __syncthreads();
@@ -697,7 +743,7 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
 }
 
 // ============================================================== dk sweep
-template <typename T, int CP, int NSL, bool PRE>
+template <typename T, int CP, int NSL, bool PRE, bool GB>
 __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
   using L = KsLayout<T, CP>;
   constexpr int VS = L::VS, NB = L::NB, NRG = L::NRG, NST = CP / 16, NTT = CP / 32;
@@ -756,6 +802,18 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
   // (C is a multiple of 4: a thread's four rows are all inside or all outside)
   const uint32_t sbase = (fthr && 4 * frg < C && fv) ? (uint32_t)(4 * frg * esz) : 0x80000000u;
   uint32_t fin_la[4], fin_q[4], fin_k[4], fin_dq[4], fin_dql[4];
+  // general form: the chunk's gb row (value v held by thread v mod 512)
+  float gbr[2];
+  auto fetch_gb = [&](int n) {
+    const auto rs = make_rsrc(a.gbv + ((int64_t)bh * N + n) * V, (uint32_t)(V * 4));
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      gbr[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (uint32_t)((tid + kKT * i) * 4), 0, 0));
+  };
+  auto stage_gb = [&]() {  // into the intra-output tile (>= 1152 floats, free until the intra task)
+#pragma unroll
+    for (int i = 0; i < 2; ++i) sOr[tid + kKT * i] = gbr[i];
+  };
   TileLd<float, CP, CP, kKT> pp;
   pp.init(C, C, C);
   auto fetch_factors = [&](int n) {
@@ -777,6 +835,7 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
       fin_dql[i] = SPLIT ? ld_elem<T>(rs_dql, eoff[i]) : 0u;
     }
     pp.load(make_rsrc(dPg + (int64_t)n * C * C, (uint32_t)(C * C * 4)));
+    if constexpr (GB) fetch_gb(n);
   };
   TileLd<T, CP, VS, kKT> pv, pd;
   pv.init(V, C, VS);
@@ -842,15 +901,11 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
       *(f4 *)(sBloc + fk * L::LDT + 4 * frg) = bl4;
       publish_decays<NB, L::LDRG>(sSc, sEt, sG, sGp, f, f.blast - f.pre - f.tot, frg, fk, fv);
     }
+    if constexpr (GB) stage_gb();
     fetch_factors(max(n - 1, 0));  // unconditional, see the dq sweep
     __syncthreads();
 
     // ---- slabs: dk_inter partials (dS after the chunk), then the dS update
-    frag_t<T> bh_[NST], bl_[NST];
-#pragma unroll
-    for (int st = 0; st < NST; ++st) {
-
-    }
     const float gam = sG[j];
     f16v acc[2];
 #pragma unroll
@@ -860,6 +915,13 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
       const int q = it * NSL + sl;
       pv.store_swz(sV, L::LDV);
       pd.store_swz(sD, L::LDV);
+      if constexpr (GB) {
+        // D = dS_[n+1] gb, by value row, before the chunk's products
+        if (sw) {
+#pragma unroll
+          for (int e = 0; e < 16; ++e) dS[sl][e] *= sOr[sl * VS + 32 * w + acc_value(e, g)];
+        }
+      }
       __syncthreads();
       // the next slab's loads go out in two halves between the dk_inter
       // products (every wave, so that each issues its share of the loads)
@@ -1045,28 +1107,31 @@ KsArgs ks_args(const Shape &s) {
   return a;
 }
 
-template <bool DQ, typename T, int CP, int NSL, bool PRE>
+template <bool DQ, typename T, int CP, int NSL, bool PRE, bool GB>
 hipError_t launch_ks_pre(const KsArgs &a, hipStream_t st) {
   static bool attr = false;
   const size_t lds = KsLayout<T, CP>::total;
   const void *fn;
-  if constexpr (DQ) fn = (const void *)dq_sweep_kernel<T, CP, NSL, PRE>;
-  else fn = (const void *)dk_sweep_kernel<T, CP, NSL, PRE>;
+  if constexpr (DQ) fn = (const void *)dq_sweep_kernel<T, CP, NSL, PRE, GB>;
+  else fn = (const void *)dk_sweep_kernel<T, CP, NSL, PRE, GB>;
   if (!attr) {
     (void)hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     attr = true;
   }
   if constexpr (DQ)
-    hipLaunchKernelGGL((dq_sweep_kernel<T, CP, NSL, PRE>), dim3(a.BH * a.KT), dim3(kKT), lds, st, a);
+    hipLaunchKernelGGL((dq_sweep_kernel<T, CP, NSL, PRE, GB>), dim3(a.BH * a.KT), dim3(kKT), lds, st, a);
   else
-    hipLaunchKernelGGL((dk_sweep_kernel<T, CP, NSL, PRE>), dim3(a.BH * a.KT), dim3(kKT), lds, st, a);
+    hipLaunchKernelGGL((dk_sweep_kernel<T, CP, NSL, PRE, GB>), dim3(a.BH * a.KT), dim3(kKT), lds, st, a);
   return hipGetLastError();
 }
 
-// PRE: the gate argument is the pre-activation of the gate epilogue.
+// PRE: the gate argument is the pre-activation of the gate epilogue.  GB: the
+// general form (value-side gate; the entry point rules out PRE with it).
 template <bool DQ, typename T, int CP, int NSL>
 hipError_t launch_ks_t(const KsArgs &a, hipStream_t st) {
-  return a.inv_tau != 0.f ? launch_ks_pre<DQ, T, CP, NSL, true>(a, st) : launch_ks_pre<DQ, T, CP, NSL, false>(a, st);
+  if (a.gbv) return launch_ks_pre<DQ, T, CP, NSL, false, true>(a, st);
+  return a.inv_tau != 0.f ? launch_ks_pre<DQ, T, CP, NSL, true, false>(a, st)
+                          : launch_ks_pre<DQ, T, CP, NSL, false, false>(a, st);
 }
 
 template <bool DQ, typename T, int CP>
@@ -1096,18 +1161,20 @@ size_t lds_bwd_dk(const Shape &s) { return ks_lds(s); }
 
 hipError_t launch_bwd_dq(const Shape &s, const void *k, const void *la, const void *v,
                          const float *S0, const void *dO, const float *dST, void *dq,
-                         const Work &w, hipStream_t st) {
+                         const Work &w, hipStream_t st, bool gb_on) {
   KsArgs a = ks_args(s);
   a.k = k; a.la = la; a.v = v; a.dO = dO; a.S0 = S0; a.dST = dST; a.dq = dq; a.dq_lo = w.dq_lo;
   a.dP = w.dP; a.cST = w.cST;
+  if (gb_on) { a.gbv = w.gb; a.colpart = w.colpart; }
   if (s.io != IO_BF16) a.dq_lo = dq;  // unused
   return dispatch_ks<true>(s, a, st);
 }
 
 hipError_t launch_bwd_dk(const Shape &s, const void *q, const void *k, const void *la,
                          const void *v, const void *dO, const float *dST, const void *dq,
-                         void *dk, void *dla, const Work &w, hipStream_t st) {
+                         void *dk, void *dla, const Work &w, hipStream_t st, bool gb_on) {
   KsArgs a = ks_args(s);
+  if (gb_on) a.gbv = w.gb;
   a.q = q; a.k = k; a.la = la; a.v = v; a.dO = dO; a.dST = dST; a.dq_in = dq; a.dq_lo_in = w.dq_lo;
   a.dk = dk; a.dla = dla; a.dP = w.dP; a.cST = dST ? w.cST : nullptr; a.dla_part = w.dla_part;
   hipError_t e = dispatch_ks<false>(s, a, st);

@@ -31,6 +31,13 @@ struct Work {
                           //   with ~16 mantissa bits (bf16 io only)
   float *dla_part = nullptr;  // [BH][ceil(K/32)][T] fp32 : per key tile sums of the gate
                               //   gradient over its features (scalar gate only)
+  // value-side gate of the general form (backward only; E = chunk-local
+  // inclusive cumsum of log beta per value column)
+  void *Vh = nullptr;         // [BH][T][V] io : V (.) exp(-E)
+  void *Oh = nullptr;         // [BH][T][V] io : dO (.) exp(E)
+  float *gb = nullptr;        // [BH][N][V] fp32 : chunk decay exp(E_last)
+  float *bpart = nullptr;     // [BH][N][V] fp32 : chunk sums of o (.) do - v (.) dv
+  float *colpart = nullptr;   // [BH][ceil(K/32)][V] fp32 : per key tile colsum(S_T (.) dS_T)
 };
 
 // Returns hipSuccess or the launch error.  Shapes are validated by the caller.
@@ -39,15 +46,22 @@ hipError_t launch_prep(const Shape &s, const void *q, const void *k, const void 
 // lb: log beta [BH][T][V] of the value-side gate, nullable (beta = 1)
 hipError_t launch_fwd_main(const Shape &s, const void *v, const void *lb, const float *S0, void *o, float *ST,
                            const Work &w, hipStream_t st);
+// gb_on: the general form (v, dO are then w.Vh, w.Oh; the states decay by w.gb)
 hipError_t launch_bwd_dq(const Shape &s, const void *k, const void *la, const void *v,
                          const float *S0, const void *dO, const float *dST, void *dq,
-                         const Work &w, hipStream_t st);
+                         const Work &w, hipStream_t st, bool gb_on = false);
 hipError_t launch_bwd_dk(const Shape &s, const void *q, const void *k, const void *la,
                          const void *v, const void *dO, const float *dST, const void *dq,
-                         void *dk, void *dla, const Work &w, hipStream_t st);
+                         void *dk, void *dla, const Work &w, hipStream_t st, bool gb_on = false);
 // (the dq sweep also writes w.dP, w.cST and w.dq_lo; the dk sweep reads them)
-hipError_t launch_bwd_dv(const Shape &s, const void *dO, const float *dST, void *dv, float *dS0,
+// lb: log beta of the general form (nullable)
+hipError_t launch_bwd_dv(const Shape &s, const void *dO, const void *lb, const float *dST, void *dv, float *dS0,
                          const Work &w, hipStream_t st);
+// General form, value side: Vh, Oh, gb into w; then (after the sweeps) dlog beta.
+hipError_t launch_beta_prep(const Shape &s, const void *v, const void *dO, const void *lb, const Work &w,
+                            hipStream_t st);
+hipError_t launch_beta_grad(const Shape &s, const void *o, const void *dO, const void *v, const void *dv,
+                            bool with_final, void *dlb, const Work &w, hipStream_t st);
 hipError_t launch_recurrent(const Shape &s, const void *q, const void *k, const void *v,
                             const void *la, const void *lb, const float *S0, void *o, float *ST, hipStream_t st);
 // T == 0 edge: S_T = S0 (or 0); dS0 = dS_T (or 0).

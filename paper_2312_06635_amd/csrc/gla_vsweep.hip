@@ -37,11 +37,13 @@
 // whole sweep (rows past the sequence end fall outside the buffer's range and
 // read as zero).
 //
-// Value-side gate (the general form G_t = alpha_t^T beta_t of App. C, forward
-// only): with E = the chunk-local inclusive cumsum of log beta per value
-// column (computed here, per chunk, in LDS) and Vh = V (.) exp(-E),
+// Value-side gate (the general form G_t = alpha_t^T beta_t of App. C): with
+// E = the chunk-local inclusive cumsum of log beta per value column (computed
+// here, per chunk, in LDS), Vh = V (.) exp(-E) and Oh = dO (.) exp(E),
 //       O_n     = exp(E) (.) ((Q (.) Lambda)_n S_[n] + P_n Vh_n)
-//       S_[n+1] = (Diag(gamma_n) S_[n] + (K (.) Gamma)_n^T Vh_n) Diag(exp(E_last)),
+//       S_[n+1] = (Diag(gamma_n) S_[n] + (K (.) Gamma)_n^T Vh_n) Diag(exp(E_last))
+//       dV_n    = exp(-E) (.) ((K (.) Gamma)_n D + P_n^T Oh_n),  D = dS_[n+1] Diag(exp(E_last))
+//       dS_[n]  = Diag(gamma_n) D + (Q (.) Lambda)_n^T Oh_n,
 // which is exact; exp(-E) grows with the decay range of beta inside one chunk,
 // so that range must stay below ~80 (fp32 exponent), e.g. by a shorter chunk.
 #include "gla_common.hpp"
@@ -126,10 +128,9 @@ __device__ __forceinline__ frag_t<T> ld_col_perm(const T *X, int ld, int r0, int
   }
 }
 
-// GB: value-side gate (forward only).
+// GB: value-side gate.
 template <typename T, int KP, int CP, bool REV, bool GB>
 __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
-  static_assert(!(GB && REV), "the value-side gate has a forward sweep only");
   using L = SweepLayout<T, KP, CP>;
   constexpr int KH = KP / 2;     // key features per wave half
   constexpr int NKB = KH / 16;   // state accumulators per wave
@@ -230,7 +231,8 @@ __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
     if constexpr (GB) {
       // E = inclusive cumsum of log beta down each column (thread: column c,
       // rows RG grp .. +RG-1), then the value tile becomes Vh = V (.) exp(-E)
-      // in place.  Rows past the chunk or the sequence read log beta = 0.
+      // (forward) or Oh = dO (.) exp(E) (backward) in place.  Rows past the
+      // chunk or the sequence read log beta = 0.
       constexpr int RG = CP / 8;
       const int c = threadIdx.x & (kTile - 1), grp = threadIdx.x / kTile;
       float part = 0.f;
@@ -247,9 +249,15 @@ __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
         const int row = grp * RG + r;
         pre += (float)sLB[row * L::LDZ + c];
         sE[row * L::LDE + c] = pre;
-        sZ[row * L::LDZ + c] = cvt<T>((float)sZ[row * L::LDZ + c] * __expf(-pre));
+        sZ[row * L::LDZ + c] = cvt<T>((float)sZ[row * L::LDZ + c] * __expf(REV ? pre : -pre));
       }
       __syncthreads();
+      if constexpr (REV) {
+        // D = dS_[n+1] Diag(exp(E_last)) before the chunk's products
+        const float gb = __expf(sE[(CP - 1) * L::LDE + cbase + j]);
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) R[kb] *= gb;
+      }
     }
 
     // output, transposed: acc[I] = R^T X^T over this wave's key features (a
@@ -303,7 +311,7 @@ __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
         for (int sc = 0; sc < NSC; ++sc)
           R[kb] = mma<T>(R[kb], ld_col_perm<T>(sY, L::LDY, 32 * sc, c0, kb & 1), zf[sc]);
       }
-      if constexpr (GB) {
+      if constexpr (GB && !REV) {
         const float gb = __expf(sE[(CP - 1) * L::LDE + cbase + j]);
 #pragma unroll
         for (int kb = 0; kb < NKB; ++kb) R[kb] *= gb;
@@ -318,7 +326,7 @@ __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
         if constexpr (GB) {
           const f4 e = *(const f4 *)(sE + row * L::LDE + cbase + 4 * g);
 #pragma unroll
-          for (int r = 0; r < 4; ++r) o[r] *= __expf(e[r]);
+          for (int r = 0; r < 4; ++r) o[r] *= __expf(REV ? -e[r] : e[r]);
         }
         if (row < rv) {
           T *dst = outh + (int64_t)(t0 + row) * V + v0 + cbase + 4 * g;
@@ -383,9 +391,7 @@ hipError_t launch_sweep_gb(const SweepArgs &a, hipStream_t st) {
 
 template <typename T, int KP, int CP, bool REV>
 hipError_t launch_sweep_t(const SweepArgs &a, hipStream_t st) {
-  if constexpr (!REV) {
-    if (a.LB) return launch_sweep_gb<T, KP, CP, false, true>(a, st);
-  }
+  if (a.LB) return launch_sweep_gb<T, KP, CP, REV, true>(a, st);
   return launch_sweep_gb<T, KP, CP, REV, false>(a, st);
 }
 
@@ -421,10 +427,10 @@ hipError_t launch_fwd_main(const Shape &s, const void *v, const void *lb, const 
   return s.io == IO_BF16 ? dispatch_sweep<bf16, false>(s, a, st) : dispatch_sweep<float, false>(s, a, st);
 }
 
-hipError_t launch_bwd_dv(const Shape &s, const void *dO, const float *dST, void *dv, float *dS0,
+hipError_t launch_bwd_dv(const Shape &s, const void *dO, const void *lb, const float *dST, void *dv, float *dS0,
                          const Work &w, hipStream_t st) {
   SweepArgs a = sweep_args(s);
-  a.X = w.Kt; a.Y = w.Qt; a.Z = dO; a.P = w.P; a.gam = w.gam; a.R0 = dST; a.out = dv; a.RN = dS0;
+  a.X = w.Kt; a.Y = w.Qt; a.Z = dO; a.P = w.P; a.gam = w.gam; a.R0 = dST; a.out = dv; a.RN = dS0; a.LB = lb;
   return s.io == IO_BF16 ? dispatch_sweep<bf16, true>(s, a, st) : dispatch_sweep<float, true>(s, a, st);
 }
 

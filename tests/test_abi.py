@@ -28,7 +28,7 @@ def declared_functions():
 
 
 def test_header_declares_the_boundary():
-    assert declared_functions() == ["gla_chunk_bwd", "gla_chunk_fwd", "gla_chunk_fwd_general",
+    assert declared_functions() == ["gla_chunk_bwd", "gla_chunk_bwd_general", "gla_chunk_fwd", "gla_chunk_fwd_general",
                                     "gla_output_gate_bwd", "gla_output_gate_fwd",
                                     "gla_output_gate_workspace_bytes", "gla_recurrent_fwd",
                                     "gla_recurrent_fwd_general", "gla_status_string", "gla_workspace_bytes"]
@@ -70,7 +70,8 @@ def test_workspace_bytes(L):
     assert fwd % 256 == 0 and bwd % 256 == 0
     p32 = P(io=gla.GLA_F32)
     assert L.gla_workspace_bytes(ctypes.byref(p32), 0) > fwd
-    assert L.gla_workspace_bytes(ctypes.byref(p), 2) == 0
+    assert L.gla_workspace_bytes(ctypes.byref(p), 2) > bwd  # the general form's backward
+    assert L.gla_workspace_bytes(ctypes.byref(p), -1) == 0
     assert L.gla_workspace_bytes(None, 0) == 0
     assert L.gla_workspace_bytes(ctypes.byref(P(dk=24)), 0) == 0
 
@@ -136,6 +137,16 @@ def test_general_form_entry_points_validate_like_the_others(L):
     assert L.gla_recurrent_fwd_general(None, *args(1), None) == gla.GLA_ERR_NULL
     assert L.gla_recurrent_fwd_general(ctypes.byref(P(io=9)), *args(1), None) == gla.GLA_ERR_DTYPE
     assert L.gla_recurrent_fwd_general(ctypes.byref(p), *args(None), None) == gla.GLA_ERR_NULL
+    # backward: log beta required, o required for dlog beta, the key-gate epilogue refused, op 2 workspace
+    bw = lambda pp, lb=1, o=1, dlb=1, ws=1, nb=1 << 40: L.gla_chunk_bwd_general(
+        ctypes.byref(pp), 1, 1, 1, 1, lb, None, o, 1, None, 1, 1, 1, 1, dlb, None, ws, nb, None)
+    assert bw(p, lb=None) == gla.GLA_ERR_NULL
+    assert bw(p, o=None) == gla.GLA_ERR_NULL
+    assert bw(P(gate_tau=16.0)) == gla.GLA_ERR_UNSUPPORTED
+    n1, n2 = L.gla_workspace_bytes(ctypes.byref(p), 1), L.gla_workspace_bytes(ctypes.byref(p), 2)
+    assert n2 > n1 + 2 * 6 * 200 * 128 * 2
+    assert bw(p, nb=n1) == gla.GLA_ERR_WORKSPACE
+    assert L.gla_workspace_bytes(ctypes.byref(p), 3) == 0
 
 
 def test_workspace_is_checked(L):
