@@ -41,6 +41,9 @@ STAGES = [("prep", "fwd", 1), ("fwd_main", "fwd", 2), ("bwd_dq", "bwd", 2), ("bw
 # with the output side (Sec. 4.4): LN + Swish gate after the forward, its
 # reverse mode (producing the layer's dO) before the backward sweeps
 STAGES_OG = STAGES[:2] + [("og_fwd", "og", 0), ("og_bwd", "og", 1)] + STAGES[2:]
+# the general form (App. C, value-side gate beta): its backward's stages
+STAGES_GB = STAGES[:2] + [("beta_prep", "bwdg", 2), ("bwd_dq", "bwdg", 3), ("bwd_dk", "bwdg", 4),
+                          ("bwd_dv", "bwdg", 5), ("beta_grad", "bwdg", 6)]
 
 
 def algorithmic(cfg, gate=True, scalar_gate=False, value_gate=False):
@@ -70,7 +73,13 @@ def algorithmic(cfg, gate=True, scalar_gate=False, value_gate=False):
         "og_fwd": dict(flops=n * V * 12, bytes=n * s * 3 * V + H * V * 8),
         # its reverse: reads o, g, dy and the affine; writes dO, dg, dw, db
         "og_bwd": dict(flops=n * V * 24, bytes=n * s * 5 * V + H * V * 16),
+        # general form: Vh, Oh from v, dO, log beta
+        "beta_prep": dict(flops=n * V * 6, bytes=n * s * 5 * V),
+        # dlog beta: reads o, dO, v, dv; writes dlog beta
+        "beta_grad": dict(flops=n * V * 4, bytes=n * s * 5 * V),
     }
+    if value_gate:  # the dv sweep also reads log beta
+        st["bwd_dv"]["bytes"] += n * s * V
     fwd = n * (4 * K * V + (C + 1) * (K + V))
     bwd = n * (8 * K * V + (C + 1) * (3 * K + 2 * V))
     io_bytes = n * s * ((7 + 2 * ga) * K + 5 * V)
@@ -168,8 +177,7 @@ def main():
     ap.add_argument("--scalar-gate", action="store_true",
                     help="one gate value per step and head (log gamma [B, H, T], Table 1's scalar gates)")
     ap.add_argument("--value-gate", action="store_true",
-                    help="general form G = alpha^T beta (App. C): adds log beta [B, H, T, d_v]; "
-                         "the step is then the forward only (no backward of the general form)")
+                    help="general form G = alpha^T beta (App. C): adds log beta [B, H, T, d_v]")
     ap.add_argument("--output-gate", action="store_true",
                     help="include the output side (per-head LN + Swish gate, Sec. 4.4) in the step")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -219,13 +227,16 @@ def main():
     stream = torch.cuda.current_stream(dev)
     stages = STAGES_OG if args.output_gate else STAGES
     if args.value_gate:
-        if args.output_gate:
-            print("--value-gate times the forward only; it does not combine with --output-gate", file=sys.stderr)
+        if args.output_gate or args.gate_tau > 0:
+            print("--value-gate does not combine with --output-gate or --gate-tau", file=sys.stderr)
             sys.exit(2)
-        stages = STAGES[:2]
+        stages = STAGES_GB
         gb = torch.Generator().manual_seed(cfg["seed"] + 13)
         # log beta = logsigmoid(x) / 16, x ~ N(0, 1), the key gate's recipe on the value side
         d["log_beta"] = (torch.nn.functional.logsigmoid(torch.randn(B, H, T, V, generator=gb)) / 16.0).to(dt).to(dev)
+        ws = torch.empty(gla.general_workspace_bytes(B, H, T, K, V, C, c, dt, scalar_gate=args.scalar_gate),
+                         dtype=torch.uint8, device=dev)
+        grads["dlog_beta"] = torch.empty_like(d["v"])
     if args.output_gate:
         # output-gate pre-activations, the loss gradient at y and the LN affine
         go = torch.Generator().manual_seed(cfg["seed"] + 11)
@@ -245,6 +256,10 @@ def main():
                 gla.output_gate_fwd(o, og["g"], og["w"], og["b"], out=(y, None))
             else:
                 gla.output_gate_bwd(o, og["g"], og["dy"], og["w"], og["b"], out=og_out, workspace=og_ws)
+        elif which == "bwdg":
+            gla.chunk_bwd(d["q"], d["k"], d["v"], d["log_alpha"], d["dO"], C, c, S0=d["S0"], dST=d["dST"],
+                          workspace=ws, reuse_fwd_workspace=True, stage=stage, out=grads,
+                          log_beta=d["log_beta"], o=o)
         elif which == "fwd":
             gla.chunk_fwd(d["q"], d["k"], d["v"], d["log_alpha"], C, c, S0=d["S0"], workspace=ws,
                           stage=stage, out=(o, ST), gate_tau=args.gate_tau, log_beta=d.get("log_beta"))
@@ -280,8 +295,7 @@ def main():
     st_alg, fwd_flops, bwd_flops, io_bytes = algorithmic(cfg, gate=not args.no_gate, scalar_gate=args.scalar_gate,
                                                          value_gate=args.value_gate)
     if args.value_gate:
-        bwd_flops = 0  # forward only
-        io_bytes = st_alg["prep"]["bytes"] + st_alg["fwd_main"]["bytes"]
+        io_bytes += 3 * B * H * T * V * (2 if cfg["io"] == "bf16" else 4)  # log beta in, o into the backward, dlog beta out
     if args.output_gate:
         io_bytes += st_alg["og_fwd"]["bytes"] + st_alg["og_bwd"]["bytes"]
     ms_per_step = 1e3 * elapsed / args.steps
@@ -309,9 +323,7 @@ def main():
     stage_frac = {nm: f"{r['frac']:.3f} of {r['bound']}" for nm, r in ((nm, roofline(nm)) for nm in stage_ms)}
 
     out = {
-        "metric": ("GLA forward (general alpha^T beta gate) tokens/s and TFLOP/s, 1.3B layer, T=2048"
-                   if args.value_gate else
-                   "GLA fwd+bwd tokens/s and TFLOP/s (% bf16 MFMA peak), 1.3B layer, T=2048"),
+        "metric": "GLA fwd+bwd tokens/s and TFLOP/s (% bf16 MFMA peak), 1.3B layer, T=2048",
         "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": cfg["io"], "data": "synthetic",
@@ -321,7 +333,7 @@ def main():
                    **({"gate": f"pre-activation z, alpha = sigmoid(z)^(1/{args.gate_tau:g})"}
                       if args.gate_tau > 0 else {}),
                    **({"gate_shape": "scalar per step and head, log gamma [B, H, T]"} if args.scalar_gate else {}),
-                   **({"value_gate": "general form alpha^T beta, log beta [B, H, T, d_v]; step = forward only"}
+                   **({"value_gate": "general form alpha^T beta, log beta [B, H, T, d_v]"}
                       if args.value_gate else {}),
                    **({"output_side": "per-head LN (affine) + Swish output gate, fwd + bwd"}
                       if args.output_gate else {})},

@@ -1,7 +1,8 @@
 // gla_beta.hip -- value-side gate of the general form (App. C, G_t =
 // alpha_t^T beta_t) in the backward: the chunk-local operands the sweeps use
 // and the gate gradient
-//     dlog beta_t = sum_{i >= t} (o_i (.) do_i - v_i (.) dv_i) + colsum(S_T (.) dS_T).
+//     dlog beta_t = sum_{i >= t} (o_i (.) do_i - v_i (.) dv_i) + colsum(S_T (.) dS_T)
+// (S_T as the dq sweep left it in the workspace).
 // With E the chunk-local inclusive cumsum of log beta per value column,
 //     Vh = V (.) exp(-E),   Oh = dO (.) exp(E),   gb = exp(E_last) per chunk,
 // the backward sweeps keep the structure of the alpha-only layer (dP = Oh Vh^T
@@ -20,9 +21,10 @@ struct BetaArgs {
   const void *v, *dO, *lb, *o, *dv;
   void *Vh, *Oh, *dlb;
   float *gb, *part;
-  const float *colpart;  // [BH][KT][V] per key tile colsum(S_T dS_T), nullable
-  int64_t n;             // BH N V threads
-  int T, V, C, N, KT;
+  const float *ST, *dST;  // [BH][K][V]; dST nullable (then no final-state term)
+  float *cst;             // [BH][V] colsum(S_T (.) dS_T)
+  int64_t n;              // BH N V threads
+  int T, K, V, C, N;
 };
 
 struct Cell {
@@ -88,9 +90,7 @@ __global__ void __launch_bounds__(256) beta_grad_scan_kernel(BetaArgs a) {
   const Cell c = cell_of(a, i);
   const int64_t bh = c.cn / a.N;
   const int n = (int)(c.cn - bh * a.N);
-  float carry = 0.f;
-  if (a.colpart)
-    for (int kt = 0; kt < a.KT; ++kt) carry += a.colpart[(bh * a.KT + kt) * a.V + c.col];
+  float carry = a.dST ? a.cst[bh * a.V + c.col] : 0.f;
   for (int m = a.N - 1; m > n; --m) carry += a.part[(bh * a.N + m) * a.V + c.col];
   const T *o = (const T *)a.o + c.base, *dO = (const T *)a.dO + c.base;
   const T *v = (const T *)a.v + c.base, *dv = (const T *)a.dv + c.base;
@@ -100,6 +100,18 @@ __global__ void __launch_bounds__(256) beta_grad_scan_kernel(BetaArgs a) {
     carry += (float)o[e] * (float)dO[e] - (float)v[e] * (float)dv[e];
     dlb[e] = cvt<T>(carry);
   }
+}
+
+// colsum(S_T (.) dS_T): thread per (batch-head, value column), features in order.
+__global__ void __launch_bounds__(256) beta_final_kernel(BetaArgs a, int64_t m) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= m) return;
+  const int64_t bh = i / a.V;
+  const int col = (int)(i - bh * a.V);
+  const float *S = a.ST + bh * a.K * a.V + col, *D = a.dST + bh * a.K * a.V + col;
+  float s = 0.f;
+  for (int f = 0; f < a.K; ++f) s += S[(int64_t)f * a.V] * D[(int64_t)f * a.V];
+  a.cst[i] = s;
 }
 
 template <typename T>
@@ -114,7 +126,7 @@ hipError_t beta_launch(int which, const BetaArgs &a, hipStream_t st) {
 BetaArgs beta_args(const Shape &s) {
   BetaArgs a{};
   a.n = (int64_t)s.BH * s.N * s.V;
-  a.T = s.T; a.V = s.V; a.C = s.C; a.N = s.N; a.KT = (s.K + 31) / 32;
+  a.T = s.T; a.K = s.K; a.V = s.V; a.C = s.C; a.N = s.N;
   return a;
 }
 
@@ -129,11 +141,17 @@ hipError_t launch_beta_prep(const Shape &s, const void *v, const void *dO, const
 }
 
 hipError_t launch_beta_grad(const Shape &s, const void *o, const void *dO, const void *v, const void *dv,
-                            const bool with_final, void *dlb, const Work &w, hipStream_t st) {
+                            const float *dST, void *dlb, const Work &w, hipStream_t st) {
   BetaArgs a = beta_args(s);
   a.o = o; a.dO = dO; a.v = v; a.dv = dv; a.dlb = dlb; a.part = w.bpart;
-  a.colpart = with_final ? w.colpart : nullptr;
+  a.ST = w.STw; a.dST = dST; a.cst = w.gb;  // gb is no longer needed once the sweeps are done
   if (a.n == 0) return hipSuccess;
+  if (dST) {
+    const int64_t m = (int64_t)s.BH * s.V;
+    hipLaunchKernelGGL(beta_final_kernel, dim3((unsigned)((m + 255) / 256)), dim3(256), 0, st, a, m);
+    hipError_t e0 = hipGetLastError();
+    if (e0 != hipSuccess) return e0;
+  }
   hipError_t e = s.io == IO_BF16 ? beta_launch<bf16>(1, a, st) : beta_launch<float>(1, a, st);
   if (e != hipSuccess) return e;
   return s.io == IO_BF16 ? beta_launch<bf16>(2, a, st) : beta_launch<float>(2, a, st);

@@ -65,7 +65,7 @@ struct KsArgs {
   float *dP, *cST;
   float *dla_part;  // scalar gate: [BH][KT][T] per-tile feature sums of the gate gradient
   const float *gbv; // general form: [BH][N][V] chunk decays exp(E_last) of the value-side gate
-  float *colpart;   // general form: [BH][KT][V] per-tile colsum(S_T (.) dS_T)
+  float *STw;       // general form: [BH][K][V] S_T (for colsum(S_T (.) dS_T) in gla_beta.hip)
   int BH, T, K, V, C, N, KT;
   int sg;         // scalar gate: la is [BH][T], one value per step shared by every feature
   float inv_tau;  // gate epilogue (0: la holds log alpha)
@@ -281,6 +281,18 @@ template <typename T> __device__ __forceinline__ void st_elem(__amdgpu_buffer_rs
 // masked threads.
 template <typename T> __device__ __forceinline__ uint32_t gate_off(int sg, uint32_t eoff, uint32_t sbase, int i) {
   return sg ? sbase + (uint32_t)(i * (int)sizeof(T)) : eoff;
+}
+
+// tile *= f by value row: f holds one factor per value; the four entries
+// 4b .. 4b+3 of a lane's accumulator are four consecutive values, so each
+// group is one 16-byte LDS read.
+__device__ __forceinline__ void scale_rows(f16v &t, const float *f, int g) {
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    const f4 x = *(const f4 *)(f + acc_value(4 * b, g));
+#pragma unroll
+    for (int r = 0; r < 4; ++r) t[4 * b + r] *= x[r];
+  }
 }
 
 // Sum over the 32 lanes of each half wave (every lane gets its half's sum).
@@ -611,10 +623,10 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
         else slab_products(std::false_type{});
         if constexpr (GB) {
           // S_[n+1] = (gamma S_[n] + K~^T Vh) gb, by value row
-          if (sw) {
-#pragma unroll
-            for (int e = 0; e < 16; ++e) S[sl][e] *= sOr[sl * VS + 32 * w + acc_value(e, g)];
-          }
+          static_assert(L::offOr % 16 == 0, "aligned factor rows");
+          __builtin_amdgcn_sched_barrier(0);
+          if (sw) scale_rows(S[sl], sOr + sl * VS + 32 * w, g);
+          __builtin_amdgcn_sched_barrier(0);
         }
       }
       __syncthreads();
@@ -715,20 +727,16 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
         }
     }
     if constexpr (GB) {
-      // colsum(S_T (.) dS_T) over this tile's features, per value (all waves
-      // take part in the half-wave sums; waves without state add zeros)
-      const auto rs_c = make_rsrc(a.colpart + ((int64_t)bh * a.KT + kt) * V, (uint32_t)(V * 4));
+      // the final state, for the value-side gate's colsum(S_T (.) dS_T)
+      if (sw) {
 #pragma unroll
-      for (int sl = 0; sl < NSL; ++sl)
+        for (int sl = 0; sl < NSL; ++sl)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int vv = sl * VS + 32 * w + acc_value(e, g), kq = k0 + j;
-          const float x = (sw && vv < V && kq < K) ? S[sl][e] * a.dST[((int64_t)bh * K + kq) * V + vv] : 0.f;
-          const float cs = half_wave_sum(x);
-          if (j == 0 && sw)
-            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, cs), rs_c,
-                                                  vv < V ? (uint32_t)(vv * 4) : 0x80000000u, 0, 0);
-        }
+          for (int e = 0; e < 16; ++e) {
+            const int vv = sl * VS + 32 * w + acc_value(e, g), kq = k0 + j;
+            if (vv < V && kq < K) a.STw[((int64_t)bh * K + kq) * V + vv] = S[sl][e];
+          }
+      }
     }
     part += __shfl_xor(part, 32);
     if (g == 0) sRedS[w * kKF + j] = part;
@@ -917,10 +925,9 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
       pd.store_swz(sD, L::LDV);
       if constexpr (GB) {
         // D = dS_[n+1] gb, by value row, before the chunk's products
-        if (sw) {
-#pragma unroll
-          for (int e = 0; e < 16; ++e) dS[sl][e] *= sOr[sl * VS + 32 * w + acc_value(e, g)];
-        }
+        __builtin_amdgcn_sched_barrier(0);
+        if (sw) scale_rows(dS[sl], sOr + sl * VS + 32 * w, g);
+        __builtin_amdgcn_sched_barrier(0);
       }
       __syncthreads();
       // the next slab's loads go out in two halves between the dk_inter
@@ -1165,7 +1172,7 @@ hipError_t launch_bwd_dq(const Shape &s, const void *k, const void *la, const vo
   KsArgs a = ks_args(s);
   a.k = k; a.la = la; a.v = v; a.dO = dO; a.S0 = S0; a.dST = dST; a.dq = dq; a.dq_lo = w.dq_lo;
   a.dP = w.dP; a.cST = w.cST;
-  if (gb_on) { a.gbv = w.gb; a.colpart = w.colpart; }
+  if (gb_on) { a.gbv = w.gb; a.STw = w.STw; }
   if (s.io != IO_BF16) a.dq_lo = dq;  // unused
   return dispatch_ks<true>(s, a, st);
 }
