@@ -77,7 +77,7 @@ size_t layout(const Shape &s, int op, char *base, Work *w) {
   void *gam = take(chunks * s.K * sizeof(float));
   void *wflag = take(chunks * 4);
   void *dP = nullptr, *cST = nullptr, *dq_lo = nullptr, *dla_part = nullptr;
-  void *Vh = nullptr, *Oh = nullptr, *gb = nullptr, *bpart = nullptr, *STw = nullptr;
+  void *Vh = nullptr, *Oh = nullptr, *gb = nullptr, *Sb = nullptr, *cpart = nullptr;
   if (op >= 1) {
     dP = take(chunks * s.C * s.C * sizeof(float));
     cST = take((size_t)s.BH * s.K * sizeof(float));
@@ -88,13 +88,13 @@ size_t layout(const Shape &s, int op, char *base, Work *w) {
     Vh = take(rows * s.V * es);
     Oh = take(rows * s.V * es);
     gb = take(chunks * s.V * sizeof(float));
-    bpart = take(chunks * s.V * sizeof(float));
-    STw = take((size_t)s.BH * s.K * s.V * sizeof(float));
+    Sb = take(gla::ks_state_bytes(s));
+    cpart = take(chunks * ((s.K + 31) / 32) * s.V * sizeof(float));
   }
   if (w) {
     w->Qt = Qt; w->Kt = Kt; w->P = P; w->gam = (float *)gam; w->wflag = (unsigned char *)wflag;
     w->dP = (float *)dP; w->cST = (float *)cST; w->dq_lo = dq_lo; w->dla_part = (float *)dla_part;
-    w->Vh = Vh; w->Oh = Oh; w->gb = (float *)gb; w->bpart = (float *)bpart; w->STw = (float *)STw;
+    w->Vh = Vh; w->Oh = Oh; w->gb = (float *)gb; w->Sb = Sb; w->cpart = (float *)cpart;
   }
   return off;
 }
@@ -253,7 +253,7 @@ GLA_EXPORT gla_status gla_chunk_bwd_general(const gla_problem *prob, const void 
     e = gla::launch_bwd_dk(s, q, k, log_alpha, w.Vh, w.Oh, dS_T, dq, dk, dlog_alpha, w, hs, true);
   if (e == hipSuccess && run(5)) e = gla::launch_bwd_dv(s, dO, log_beta, dS_T, dv, dS0, w, hs);
   if (e == hipSuccess && run(6) && dlog_beta)
-    e = gla::launch_beta_grad(s, o, dO, v, dv, dS_T, dlog_beta, w, hs);
+    e = gla::launch_beta_grad(s, o, dO, v, dv, dlog_beta, w, hs);
   return hip_status(e);
 }
 

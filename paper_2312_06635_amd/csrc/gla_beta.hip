@@ -1,8 +1,12 @@
 // gla_beta.hip -- value-side gate of the general form (App. C, G_t =
 // alpha_t^T beta_t) in the backward: the chunk-local operands the sweeps use
 // and the gate gradient
-//     dlog beta_t = sum_{i >= t} (o_i (.) do_i - v_i (.) dv_i) + colsum(S_T (.) dS_T)
-// (S_T as the dq sweep left it in the workspace).
+//     dlog beta_t = sum_{i >= t} (o_i (.) do_i - v_i (.) dv_i) + colsum(S_T (.) dS_T).
+// The part of that sum beyond chunk n equals colsum(S_[n+1] (.) dS_[n+1])
+// exactly (the state-form gate gradient at the next chunk's first step), so
+// the carry into each chunk comes from the chunk-end states (summed over the
+// key tiles by the dk sweep) and only the chunk's own rows are summed here:
+// no rounding accumulates over the sequence.
 // With E the chunk-local inclusive cumsum of log beta per value column,
 //     Vh = V (.) exp(-E),   Oh = dO (.) exp(E),   gb = exp(E_last) per chunk,
 // the backward sweeps keep the structure of the alpha-only layer (dP = Oh Vh^T
@@ -20,11 +24,10 @@ namespace {
 struct BetaArgs {
   const void *v, *dO, *lb, *o, *dv;
   void *Vh, *Oh, *dlb;
-  float *gb, *part;
-  const float *ST, *dST;  // [BH][K][V]; dST nullable (then no final-state term)
-  float *cst;             // [BH][V] colsum(S_T (.) dS_T)
+  float *gb;
+  const float *cpart;     // [BH][N][KT][V] per key tile colsum(S_[n+1] (.) dS_[n+1])
   int64_t n;              // BH N V threads
-  int T, K, V, C, N;
+  int T, V, C, N, KT;
 };
 
 struct Cell {
@@ -64,34 +67,15 @@ __global__ void __launch_bounds__(256) beta_prep_kernel(BetaArgs a) {
   a.gb[c.cn * a.V + c.col] = __expf(E);
 }
 
-// Chunk sums of o do - v dv (dv final), and the chunk's E_last.
-template <typename T>
-__global__ void __launch_bounds__(256) beta_grad_sum_kernel(BetaArgs a) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= a.n) return;
-  const Cell c = cell_of(a, i);
-  const T *o = (const T *)a.o + c.base, *dO = (const T *)a.dO + c.base;
-  const T *v = (const T *)a.v + c.base, *dv = (const T *)a.dv + c.base;
-  float s = 0.f;
-#pragma unroll 4
-  for (int r = 0; r < c.rows; ++r) {
-    const int64_t e = (int64_t)r * a.V;
-    s += (float)o[e] * (float)dO[e] - (float)v[e] * (float)dv[e];
-  }
-  a.part[c.cn * a.V + c.col] = s;
-}
-
-// Reverse cumsum: the carry into chunk n is the final-state term plus the
-// chunk sums of every later chunk (added in chunk order).
+// Reverse cumsum inside each chunk, starting from the chunk's carry (key
+// tiles added in order).
 template <typename T>
 __global__ void __launch_bounds__(256) beta_grad_scan_kernel(BetaArgs a) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= a.n) return;
   const Cell c = cell_of(a, i);
-  const int64_t bh = c.cn / a.N;
-  const int n = (int)(c.cn - bh * a.N);
-  float carry = a.dST ? a.cst[bh * a.V + c.col] : 0.f;
-  for (int m = a.N - 1; m > n; --m) carry += a.part[(bh * a.N + m) * a.V + c.col];
+  float carry = 0.f;
+  for (int kt = 0; kt < a.KT; ++kt) carry += a.cpart[(c.cn * a.KT + kt) * a.V + c.col];
   const T *o = (const T *)a.o + c.base, *dO = (const T *)a.dO + c.base;
   const T *v = (const T *)a.v + c.base, *dv = (const T *)a.dv + c.base;
   T *dlb = (T *)a.dlb + c.base;
@@ -102,23 +86,10 @@ __global__ void __launch_bounds__(256) beta_grad_scan_kernel(BetaArgs a) {
   }
 }
 
-// colsum(S_T (.) dS_T): thread per (batch-head, value column), features in order.
-__global__ void __launch_bounds__(256) beta_final_kernel(BetaArgs a, int64_t m) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= m) return;
-  const int64_t bh = i / a.V;
-  const int col = (int)(i - bh * a.V);
-  const float *S = a.ST + bh * a.K * a.V + col, *D = a.dST + bh * a.K * a.V + col;
-  float s = 0.f;
-  for (int f = 0; f < a.K; ++f) s += S[(int64_t)f * a.V] * D[(int64_t)f * a.V];
-  a.cst[i] = s;
-}
-
 template <typename T>
 hipError_t beta_launch(int which, const BetaArgs &a, hipStream_t st) {
   const unsigned blocks = (unsigned)((a.n + 255) / 256);
   if (which == 0) hipLaunchKernelGGL(beta_prep_kernel<T>, dim3(blocks), dim3(256), 0, st, a);
-  if (which == 1) hipLaunchKernelGGL(beta_grad_sum_kernel<T>, dim3(blocks), dim3(256), 0, st, a);
   if (which == 2) hipLaunchKernelGGL(beta_grad_scan_kernel<T>, dim3(blocks), dim3(256), 0, st, a);
   return hipGetLastError();
 }
@@ -126,7 +97,7 @@ hipError_t beta_launch(int which, const BetaArgs &a, hipStream_t st) {
 BetaArgs beta_args(const Shape &s) {
   BetaArgs a{};
   a.n = (int64_t)s.BH * s.N * s.V;
-  a.T = s.T; a.K = s.K; a.V = s.V; a.C = s.C; a.N = s.N;
+  a.T = s.T; a.V = s.V; a.C = s.C; a.N = s.N; a.KT = (s.K + 31) / 32;
   return a;
 }
 
@@ -141,19 +112,10 @@ hipError_t launch_beta_prep(const Shape &s, const void *v, const void *dO, const
 }
 
 hipError_t launch_beta_grad(const Shape &s, const void *o, const void *dO, const void *v, const void *dv,
-                            const float *dST, void *dlb, const Work &w, hipStream_t st) {
+                            void *dlb, const Work &w, hipStream_t st) {
   BetaArgs a = beta_args(s);
-  a.o = o; a.dO = dO; a.v = v; a.dv = dv; a.dlb = dlb; a.part = w.bpart;
-  a.ST = w.STw; a.dST = dST; a.cst = w.gb;  // gb is no longer needed once the sweeps are done
+  a.o = o; a.dO = dO; a.v = v; a.dv = dv; a.dlb = dlb; a.cpart = w.cpart;
   if (a.n == 0) return hipSuccess;
-  if (dST) {
-    const int64_t m = (int64_t)s.BH * s.V;
-    hipLaunchKernelGGL(beta_final_kernel, dim3((unsigned)((m + 255) / 256)), dim3(256), 0, st, a, m);
-    hipError_t e0 = hipGetLastError();
-    if (e0 != hipSuccess) return e0;
-  }
-  hipError_t e = s.io == IO_BF16 ? beta_launch<bf16>(1, a, st) : beta_launch<float>(1, a, st);
-  if (e != hipSuccess) return e;
   return s.io == IO_BF16 ? beta_launch<bf16>(2, a, st) : beta_launch<float>(2, a, st);
 }
 

@@ -43,6 +43,10 @@
 // gb = exp(E_last) per chunk: S_[n+1] = (gamma S_[n] + (K (.) Gamma)^T Vh) gb
 // in the dq sweep, D = dS_[n+1] gb before the dk sweep's products; the chunk's
 // gb row is staged in the intra-output tile, which is free during the slabs.
+// For the value-side gate gradient the dq sweep also stores every chunk-end
+// state S_[n+1] (io dtype, in the accumulators' own lane order), and the dk
+// sweep, holding dS_[n+1] in the same order, forms this tile's
+// colsum(S_[n+1] (.) dS_[n+1]): the exact carry of dlog beta into chunk n.
 #include <type_traits>
 
 #include "gla_common.hpp"
@@ -65,7 +69,8 @@ struct KsArgs {
   float *dP, *cST;
   float *dla_part;  // scalar gate: [BH][KT][T] per-tile feature sums of the gate gradient
   const float *gbv; // general form: [BH][N][V] chunk decays exp(E_last) of the value-side gate
-  float *STw;       // general form: [BH][K][V] S_T (for colsum(S_T (.) dS_T) in gla_beta.hip)
+  void *Sb;         // general form: chunk-end states S_[n+1], accumulator-native layout (sb_index)
+  float *cpart;     // general form: [BH][N][KT][V] per key tile colsum(S_[n+1] (.) dS_[n+1])
   int BH, T, K, V, C, N, KT;
   int sg;         // scalar gate: la is [BH][T], one value per step shared by every feature
   float inv_tau;  // gate epilogue (0: la holds log alpha)
@@ -293,6 +298,37 @@ __device__ __forceinline__ void scale_rows(f16v &t, const float *f, int g) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) t[4 * b + r] *= x[r];
   }
+}
+
+// Element index of lane l's 16 accumulator entries of state tile (bh, chunk
+// n, key tile kt, slab sl, wave w) in the chunk-end state buffer.
+__device__ __forceinline__ int64_t sb_index(int bh, int n, int N, int kt, int KT, int sl, int NSL, int w, int NWS,
+                                            int l) {
+  return (((((int64_t)bh * N + n) * KT + kt) * NSL + sl) * NWS + w) * 1024 + (int64_t)l * 16;
+}
+
+template <typename T> struct Tile16 { u32x4 r[sizeof(T) * 16 / 16]; };
+
+// (each 16-byte vector is built whole: assigning its lanes one by one inside
+// an unrolled loop was compiled into copies of the first lane for fp32)
+template <typename T> __device__ __forceinline__ void store_tile16(T *p, const f16v &t) {
+  if constexpr (sizeof(T) == 2) {
+    auto pk = [&](int i) {
+      return (uint32_t)__builtin_bit_cast(unsigned short, cvt<bf16>(t[2 * i])) |
+             ((uint32_t)__builtin_bit_cast(unsigned short, cvt<bf16>(t[2 * i + 1])) << 16);
+    };
+    ((u32x4 *)p)[0] = u32x4{pk(0), pk(1), pk(2), pk(3)};
+    ((u32x4 *)p)[1] = u32x4{pk(4), pk(5), pk(6), pk(7)};
+  } else {
+#pragma unroll
+    for (int b = 0; b < 4; ++b) ((f4 *)p)[b] = f4{t[4 * b], t[4 * b + 1], t[4 * b + 2], t[4 * b + 3]};
+  }
+}
+
+template <typename T> __device__ __forceinline__ float tile16_elem(const Tile16<T> &x, int e) {
+  const uint32_t w = x.r[sizeof(T) == 2 ? e / 8 : e / 4][sizeof(T) == 2 ? (e / 2) % 4 : e % 4];
+  if constexpr (sizeof(T) == 2) return __builtin_bit_cast(float, (e & 1) ? (w & 0xFFFF0000u) : (w << 16));
+  else return __builtin_bit_cast(float, w);
 }
 
 // Sum over the 32 lanes of each half wave (every lane gets its half's sum).
@@ -625,7 +661,10 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
           // S_[n+1] = (gamma S_[n] + K~^T Vh) gb, by value row
           static_assert(L::offOr % 16 == 0, "aligned factor rows");
           __builtin_amdgcn_sched_barrier(0);
-          if (sw) scale_rows(S[sl], sOr + sl * VS + 32 * w, g);
+          if (sw) {
+            scale_rows(S[sl], sOr + sl * VS + 32 * w, g);
+            store_tile16<T>((T *)a.Sb + sb_index(bh, n, N, kt, a.KT, sl, NSL, w, L::NWS, l), S[sl]);
+          }
           __builtin_amdgcn_sched_barrier(0);
         }
       }
@@ -726,18 +765,6 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
           if (vv < V && kq < K) part += S[sl][e] * a.dST[((int64_t)bh * K + kq) * V + vv];
         }
     }
-    if constexpr (GB) {
-      // the final state, for the value-side gate's colsum(S_T (.) dS_T)
-      if (sw) {
-#pragma unroll
-        for (int sl = 0; sl < NSL; ++sl)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int vv = sl * VS + 32 * w + acc_value(e, g), kq = k0 + j;
-            if (vv < V && kq < K) a.STw[((int64_t)bh * K + kq) * V + vv] = S[sl][e];
-          }
-      }
-    }
     part += __shfl_xor(part, 32);
     if (g == 0) sRedS[w * kKF + j] = part;
     __syncthreads();
@@ -822,6 +849,15 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) sOr[tid + kKT * i] = gbr[i];
   };
+  // general form: the dq sweep's chunk-end state tile, one slab ahead
+  Tile16<T> svr;
+  auto fetch_sv = [&](int n, int sl) {
+    if (sw) {
+      const u32x4 *p = (const u32x4 *)((const T *)a.Sb + sb_index(bh, n, N, kt, a.KT, sl, NSL, w, L::NWS, l));
+#pragma unroll
+      for (int i = 0; i < (int)(sizeof(svr.r) / 16); ++i) svr.r[i] = p[i];
+    }
+  };
   TileLd<float, CP, CP, kKT> pp;
   pp.init(C, C, C);
   auto fetch_factors = [&](int n) {
@@ -866,6 +902,7 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
   for (int it = 0; it < N; ++it) {
     const int n = N - 1 - it;
     const int t0 = n * C, rv = min(C, a.T - t0);
+    if constexpr (GB) fetch_sv(n, 0);
     // ---- factors
     float c[4], kv[4], qdq[4], zc[4];  // zc: the gate argument, for the gate gradient
     {
@@ -924,6 +961,16 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
       pv.store_swz(sV, L::LDV);
       pd.store_swz(sD, L::LDV);
       if constexpr (GB) {
+        // this tile's colsum(S_[n+1] (.) dS_[n+1]) per value: the carry of the
+        // value-side gate gradient into chunk n
+        float *cp = a.cpart + (((int64_t)bh * N + n) * a.KT + kt) * V;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float cs = half_wave_sum(sw ? dS[sl][e] * tile16_elem<T>(svr, e) : 0.f);
+          const int vv = sl * VS + 32 * w + acc_value(e, g);
+          if (sw && j == 0 && vv < V) cp[vv] = cs;
+        }
+        if (sl + 1 < NSL) fetch_sv(n, sl + 1);
         // D = dS_[n+1] gb, by value row, before the chunk's products
         __builtin_amdgcn_sched_barrier(0);
         if (sw) scale_rows(dS[sl], sOr + sl * VS + 32 * w, g);
@@ -1164,6 +1211,12 @@ hipError_t dispatch_ks(const Shape &s, const KsArgs &a, hipStream_t st) {
 }  // namespace
 
 size_t lds_bwd_dq(const Shape &s) { return ks_lds(s); }
+
+size_t ks_state_bytes(const Shape &s) {
+  const int vs = s.io == IO_BF16 ? 256 : 128;
+  const int64_t kt = (s.K + kKF - 1) / kKF;
+  return (size_t)s.BH * s.N * kt * ks_nsl(s) * vs * kKF * s.esz();
+}
 size_t lds_bwd_dk(const Shape &s) { return ks_lds(s); }
 
 hipError_t launch_bwd_dq(const Shape &s, const void *k, const void *la, const void *v,
@@ -1172,7 +1225,7 @@ hipError_t launch_bwd_dq(const Shape &s, const void *k, const void *la, const vo
   KsArgs a = ks_args(s);
   a.k = k; a.la = la; a.v = v; a.dO = dO; a.S0 = S0; a.dST = dST; a.dq = dq; a.dq_lo = w.dq_lo;
   a.dP = w.dP; a.cST = w.cST;
-  if (gb_on) { a.gbv = w.gb; a.STw = w.STw; }
+  if (gb_on) { a.gbv = w.gb; a.Sb = w.Sb; }
   if (s.io != IO_BF16) a.dq_lo = dq;  // unused
   return dispatch_ks<true>(s, a, st);
 }
@@ -1181,7 +1234,7 @@ hipError_t launch_bwd_dk(const Shape &s, const void *q, const void *k, const voi
                          const void *v, const void *dO, const float *dST, const void *dq,
                          void *dk, void *dla, const Work &w, hipStream_t st, bool gb_on) {
   KsArgs a = ks_args(s);
-  if (gb_on) a.gbv = w.gb;
+  if (gb_on) { a.gbv = w.gb; a.Sb = w.Sb; a.cpart = w.cpart; }
   a.q = q; a.k = k; a.la = la; a.v = v; a.dO = dO; a.dST = dST; a.dq_in = dq; a.dq_lo_in = w.dq_lo;
   a.dk = dk; a.dla = dla; a.dP = w.dP; a.cST = dST ? w.cST : nullptr; a.dla_part = w.dla_part;
   hipError_t e = dispatch_ks<false>(s, a, st);

@@ -36,8 +36,8 @@ struct Work {
   void *Vh = nullptr;         // [BH][T][V] io : V (.) exp(-E)
   void *Oh = nullptr;         // [BH][T][V] io : dO (.) exp(E)
   float *gb = nullptr;        // [BH][N][V] fp32 : chunk decay exp(E_last)
-  float *bpart = nullptr;     // [BH][N][V] fp32 : chunk sums of o (.) do - v (.) dv
-  float *STw = nullptr;       // [BH][K][V] fp32 : the final state, written by the dq sweep
+  void *Sb = nullptr;         // chunk-end states S_[n+1] (io), written by the dq sweep (ks_state_bytes)
+  float *cpart = nullptr;     // [BH][N][ceil(K/32)][V] fp32 : per key tile colsum(S_[n+1] (.) dS_[n+1])
 };
 
 // Returns hipSuccess or the launch error.  Shapes are validated by the caller.
@@ -61,7 +61,8 @@ hipError_t launch_bwd_dv(const Shape &s, const void *dO, const void *lb, const f
 hipError_t launch_beta_prep(const Shape &s, const void *v, const void *dO, const void *lb, const Work &w,
                             hipStream_t st);
 hipError_t launch_beta_grad(const Shape &s, const void *o, const void *dO, const void *v, const void *dv,
-                            const float *dST, void *dlb, const Work &w, hipStream_t st);
+                            void *dlb, const Work &w, hipStream_t st);
+size_t ks_state_bytes(const Shape &s);
 hipError_t launch_recurrent(const Shape &s, const void *q, const void *k, const void *v,
                             const void *la, const void *lb, const float *S0, void *o, float *ST, hipStream_t st);
 // T == 0 edge: S_T = S0 (or 0); dS0 = dS_T (or 0).

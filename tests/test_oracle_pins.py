@@ -503,8 +503,9 @@ def test_general_gate_closed_form_with_bf16_outputs_has_a_precision_floor():
     sequence of o (.) do - v (.) dv.  With o and dv rounded to bf16 (every
     other value exact) its error at T = 2048 is already 2-3e-2 of its
     magnitude (2.7e-2 here): the floor any bf16 evaluation of that closed
-    form inherits.
-    Unrounded, the closed form is exact (checked above)."""
+    form over the whole sequence inherits.  Unrounded, the closed form is
+    exact (checked above); the state form at chunk boundaries (next test)
+    avoids the long sum."""
     import torch
     rng = np.random.default_rng(64)
     T, K, V = 2048, 16, 32
@@ -518,3 +519,24 @@ def test_general_gate_closed_form_with_bf16_outputs_has_a_precision_floor():
     _, rb = forms.general_gate_closed_form(q, k, v, bf(o), g["dq"], g["dk"], bf(g["dv"]), dO)
     err = rel(rb, g["dlog_beta"])
     assert 5e-3 < err < 6e-2, err
+
+
+def test_value_gate_gradient_carry_is_the_chunk_boundary_state_product():
+    """The part of dlog beta beyond a chunk boundary tau is
+    colsum(S_tau (.) dS_tau), with dS_tau = dL/dS_tau through the later steps
+    (for the last boundary, colsum(S_T (.) dS_T)): the carry the kernels use."""
+    rng = np.random.default_rng(65)
+    T, K, V, C = 150, 6, 5, 64
+    q, k, v, la, lb, S0 = _general_case(rng, T=T, K=K, V=V)
+    dO = rng.standard_normal((T, V)); dST = rng.standard_normal((K, V)) * 0.1
+    g = oracle.general_gate_bwd(q, k, v, la, lb, dO, S0, dST)
+    for tau in (C, 2 * C, T):
+        o_a, S_tau = oracle.general_gate_fwd(q[:tau], k[:tau], v[:tau], la[:tau], lb[:tau], S0)
+        if tau == T:
+            carry = (S_tau * dST).sum(axis=0)
+            assert rel(carry, g["dlog_beta"][-1] - (o_a[-1] * dO[-1] - v[-1] * g["dv"][-1])) < 1e-12
+        else:
+            # dL/dS_tau through the later steps: the backward of the remainder started from S_tau
+            rest = oracle.general_gate_bwd(q[tau:], k[tau:], v[tau:], la[tau:], lb[tau:], dO[tau:], S_tau, dST)
+            carry = (S_tau * rest["dS0"]).sum(axis=0)
+            assert rel(carry, g["dlog_beta"][tau]) < 1e-12

@@ -421,11 +421,11 @@ def test_general_gate_backward(io, B, H, T, K, V, C, c, decay):
 
 @pytest.mark.parametrize("io", ["f32", "bf16"])
 def test_general_gate_backward_long(io):
-    """T = 2048 with the value-side gate.  Every gradient meets the bar except
-    bf16 dlog beta: its closed form (App. C) sums o (.) do - v (.) dv over the
-    whole sequence, and bf16 rounding of o and dv alone (exact values
-    otherwise) already leaves 2-3e-2 at this length (oracle-side check in
-    test_oracle_pins.py), so it is held to 4e-2 here; fp32 holds 1e-4."""
+    """T = 2048 with the value-side gate: every gradient at the bar, dlog beta
+    included.  App. C's closed form summed over the whole sequence would not
+    be (bf16 rounding of o and dv alone leaves 2-3e-2 at this length, pinned
+    in test_oracle_pins.py); the kernels carry it across chunks exactly, as
+    colsum(S_[n+1] (.) dS_[n+1]), and sum o do - v dv only inside a chunk."""
     g = gla()
     T, K, V = 2048, 64, 128
     cfg = small_case("ggb_long_" + io, io, 1, 1, T, K, V, 64, 16, 5, s0_std=0.1)
@@ -442,10 +442,7 @@ def test_general_gate_backward_long(io):
     rg = oracle.general_gate_bwd(*args, heads(inp["dO"], idx), heads(inp["S0"], idx), heads(inp["dST"], idx))
     errs = {n: rel(heads(gr[n], idx), rg[n]) for n in ("dq", "dk", "dv", "dlog_alpha", "dlog_beta", "dS0")}
     say("general gate bwd long", io, {k2: f"{v2:.2e}" for k2, v2 in errs.items()})
-    tol = {n: TOL[io] for n in errs}
-    if io == "bf16":
-        tol["dlog_beta"] = 4e-2
-    bad = {k2: v2 for k2, v2 in errs.items() if not v2 <= tol[k2]}
+    bad = {k2: v2 for k2, v2 in errs.items() if not v2 <= TOL[io]}
     assert not bad, bad
 
 
