@@ -229,34 +229,43 @@ def general_gate_fwd(q, k, v, log_alpha, log_beta, S0=None):
     return o, S
 
 
-def general_gate_bwd(q, k, v, log_alpha, log_beta, dO, S0=None, dST=None):
+def general_gate_bwd(q, k, v, log_alpha, log_beta, dO, S0=None, dST=None, ckpt=64):
     """Back-propagation through general_gate_fwd for L = sum(o dO) +
-    sum(S_T dS_T), keeping every state.  With G_t = dL/dS_t and
-    M_t = alpha_t^T beta_t: G_t = q_t^T do_t + M_{t+1} (.) G_{t+1} (G_T also
-    holds dS_T), dq_t = S_t do_t^T, dk_t = G_t v_t^T, dv_t = k_t G_t,
+    sum(S_T dS_T).  With G_t = dL/dS_t and M_t = alpha_t^T beta_t:
+    G_t = q_t^T do_t + M_{t+1} (.) G_{t+1} (G_T also holds dS_T),
+    dq_t = S_t do_t^T, dk_t = G_t v_t^T, dv_t = k_t G_t,
     d log alpha_t = rowsum(G_t (.) M_t (.) S_{t-1}), d log beta_t the column
-    sums of the same product, dS0 = M_1 (.) G_1.  Returns dq, dk, dv,
-    dlog_alpha, dlog_beta, dS0."""
+    sums of the same product, dS0 = M_1 (.) G_1.  States are kept every ckpt
+    steps and recomputed segment by segment.  Returns dq, dk, dv, dlog_alpha,
+    dlog_beta, dS0."""
     q, k, v, la, lb, dO, S0, dST = (_as_f64(x) for x in (q, k, v, log_alpha, log_beta, dO, S0, dST))
     T, K = q.shape[-2:]
     V = v.shape[-1]
     lead = q.shape[:-2]
-    S = [np.zeros(lead + (K, V)) if S0 is None else S0.copy()]
-    M = []
+    M = lambda t: np.exp(la[..., t, :, None] + lb[..., t, None, :])
+    step = lambda S, t: M(t) * S + k[..., t, :, None] * v[..., t, None, :]
+    S = np.zeros(lead + (K, V)) if S0 is None else S0.copy()
+    ck = {0: S}
     for t in range(T):
-        M.append(np.exp(la[..., t, :, None] + lb[..., t, None, :]))
-        S.append(M[t] * S[t] + k[..., t, :, None] * v[..., t, None, :])
+        S = step(S, t)
+        if (t + 1) % ckpt == 0:
+            ck[t + 1] = S
     G = np.zeros(lead + (K, V)) if dST is None else dST.copy()
     out = {n: np.zeros_like(x) for n, x in (("dq", q), ("dk", k), ("dv", v), ("dlog_alpha", la),
                                                ("dlog_beta", lb))}
-    for t in range(T - 1, -1, -1):
-        G = G + q[..., t, :, None] * dO[..., t, None, :]
-        out["dq"][..., t, :] = np.einsum("...aj,...j->...a", S[t + 1], dO[..., t, :])
-        out["dk"][..., t, :] = np.einsum("...aj,...j->...a", G, v[..., t, :])
-        out["dv"][..., t, :] = np.einsum("...a,...aj->...j", k[..., t, :], G)
-        dM = G * M[t] * S[t]
-        out["dlog_alpha"][..., t, :] = dM.sum(axis=-1)
-        out["dlog_beta"][..., t, :] = dM.sum(axis=-2)
-        G = M[t] * G
+    for s0 in range(((T - 1) // ckpt) * ckpt if T else 0, -1, -ckpt):
+        seg = [ck[s0]]  # seg[i] = S_{s0 + i}
+        for t in range(s0, min(s0 + ckpt, T)):
+            seg.append(step(seg[-1], t))
+        for t in range(min(s0 + ckpt, T) - 1, s0 - 1, -1):
+            Sp, Sc, Mt = seg[t - s0], seg[t - s0 + 1], M(t)
+            G = G + q[..., t, :, None] * dO[..., t, None, :]
+            out["dq"][..., t, :] = np.einsum("...aj,...j->...a", Sc, dO[..., t, :])
+            out["dk"][..., t, :] = np.einsum("...aj,...j->...a", G, v[..., t, :])
+            out["dv"][..., t, :] = np.einsum("...a,...aj->...j", k[..., t, :], G)
+            dM = G * Mt * Sp
+            out["dlog_alpha"][..., t, :] = dM.sum(axis=-1)
+            out["dlog_beta"][..., t, :] = dM.sum(axis=-2)
+            G = Mt * G
     out["dS0"] = G
     return out

@@ -496,6 +496,10 @@ def test_general_gate_gradients_equal_closed_form():
     ra, rb = forms.general_gate_closed_form(q, k, v, o, g["dq"], g["dk"], g["dv"], dO, ST, dST)
     assert rel(g["dlog_alpha"], ra) < 1e-12
     assert rel(g["dlog_beta"], rb) < 1e-12
+    # state checkpoints every 4 steps instead of 64 recompute the same states
+    g4 = oracle.general_gate_bwd(q, k, v, la, lb, dO, S0, dST, ckpt=4)
+    for name in g:
+        assert np.array_equal(g[name], g4[name]), name
 
 
 def test_general_gate_closed_form_with_bf16_outputs_has_a_precision_floor():

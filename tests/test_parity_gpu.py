@@ -565,6 +565,76 @@ def test_full_size_sampled_heads(name, alpha_one, dst):
     compare(inp, o, ST, gr, idx, cfg["io"], name)
 
 
+@pytest.mark.parametrize("mode", ["scalar_gate", "general_gate", "output_gate"])
+def test_full_size_extensions_sampled_heads(mode):
+    """The extension modes at the 1.3B workload in the benchmark's launch
+    configuration (its input recipe for the extra tensors), checked on sampled
+    heads against the oracle."""
+    g = gla()
+    cfg = W.CONFIGS["gla1p3b_T2048"]
+    B, H, T, K, V, C, c = (cfg[x] for x in ("B", "H", "T", "dk", "dv", "chunk", "subchunk"))
+    say("full-size extension", mode)
+    inp = W.make_inputs(cfg)
+    dt = inp["q"].dtype
+    d = to_dev(inp)
+    BH = B * H
+    if mode == "scalar_gate":
+        lg = torch.nn.functional.logsigmoid(torch.randn(B, H, T, generator=torch.Generator().manual_seed(cfg["seed"] + 5))) / 16.0
+        inp["log_alpha"] = lg.to(dt)
+        d["log_alpha"] = inp["log_alpha"].cuda()
+        ws = torch.empty(g.workspace_bytes(B, H, T, K, V, C, c, dt, op=1, scalar_gate=True), dtype=torch.uint8, device="cuda")
+        o, ST = g.chunk_fwd(d["q"], d["k"], d["v"], d["log_alpha"], C, c, output_final_state=True, workspace=ws)
+        gr = g.chunk_bwd(d["q"], d["k"], d["v"], d["log_alpha"], d["dO"], C, c, want_dS0=True, workspace=ws,
+                         reuse_fwd_workspace=True)
+        torch.cuda.synchronize()
+        idx = [0, BH - 1]
+        args = [heads(inp[n], idx) for n in ("q", "k", "v", "log_alpha")]
+        ro, rST = oracle.scalar_gate_fwd(*args)
+        rg = oracle.scalar_gate_bwd(*args, heads(inp["dO"], idx))
+        errs = {"o": rel(heads(o, idx), ro), "S_T": rel(heads(ST, idx), rST),
+                "dlog_gamma": rel(heads(gr["dlog_alpha"], idx), rg["dlog_gamma"])}
+        for n in ("dq", "dk", "dv", "dS0"):
+            errs[n] = rel(heads(gr[n], idx), rg[n])
+    elif mode == "general_gate":
+        lb = torch.nn.functional.logsigmoid(torch.randn(B, H, T, V, generator=torch.Generator().manual_seed(cfg["seed"] + 13))) / 16.0
+        inp["log_beta"] = lb.to(dt)
+        d["log_beta"] = inp["log_beta"].cuda()
+        ws = torch.empty(g.general_workspace_bytes(B, H, T, K, V, C, c, dt), dtype=torch.uint8, device="cuda")
+        o, ST = g.chunk_fwd(d["q"], d["k"], d["v"], d["log_alpha"], C, c, output_final_state=True, workspace=ws,
+                            log_beta=d["log_beta"])
+        gr = g.chunk_bwd(d["q"], d["k"], d["v"], d["log_alpha"], d["dO"], C, c, want_dS0=True, workspace=ws,
+                         reuse_fwd_workspace=True, log_beta=d["log_beta"], o=o)
+        torch.cuda.synchronize()
+        idx = [BH - 1]
+        args = [heads(inp[n], idx) for n in ("q", "k", "v", "log_alpha", "log_beta")]
+        ro, rST = oracle.general_gate_fwd(*args)
+        rg = oracle.general_gate_bwd(*args, heads(inp["dO"], idx))
+        errs = {"o": rel(heads(o, idx), ro), "S_T": rel(heads(ST, idx), rST)}
+        for n in ("dq", "dk", "dv", "dlog_alpha", "dlog_beta", "dS0"):
+            errs[n] = rel(heads(gr[n], idx), rg[n])
+    else:
+        go = torch.Generator().manual_seed(cfg["seed"] + 11)
+        gg = torch.randn(B, H, T, V, generator=go).to(dt)
+        dy = torch.randn(B, H, T, V, generator=go).to(dt)
+        w = 1.0 + 0.1 * torch.randn(H, V, generator=go)
+        b = 0.1 * torch.randn(H, V, generator=go)
+        o, _ = g.chunk_fwd(d["q"], d["k"], d["v"], d["log_alpha"], C, c)
+        y, _ = g.output_gate_fwd(o, gg.cuda(), w.cuda(), b.cuda())
+        og = g.output_gate_bwd(o, gg.cuda(), dy.cuda(), w.cuda(), b.cuda())
+        torch.cuda.synchronize()
+        h = H - 1  # every batch row of the last head (the affine gradients sum over them)
+        sel = lambda t: t[:, h:h + 1].float().cpu().double().numpy()
+        oo, g_, dy_ = sel(o), sel(gg), sel(dy)
+        ry, _, _ = oracle.output_gate_fwd(oo, g_, w[h:h + 1].double().numpy(), b[h:h + 1].double().numpy())
+        rg = oracle.output_gate_bwd(oo, g_, dy_, w[h:h + 1].double().numpy(), b[h:h + 1].double().numpy())
+        errs = {"y": rel(sel(y), ry), "do": rel(sel(og["do"]), rg["do"]), "dg": rel(sel(og["dg"]), rg["dg"]),
+                "dw": rel(og["dln_w"][h:h + 1].cpu().double().numpy(), rg["dw"]),
+                "db": rel(og["dln_b"][h:h + 1].cpu().double().numpy(), rg["db"])}
+    say("full-size extension", mode, {k2: f"{v2:.2e}" for k2, v2 in errs.items()})
+    bad = {k2: v2 for k2, v2 in errs.items() if not v2 <= TOL[cfg["io"]]}
+    assert not bad, bad
+
+
 def test_stage_by_stage_equals_whole_call():
     """The stage selector (used by the benchmark to time each kernel) runs the
     same kernels: stages in order reproduce the whole call exactly."""
