@@ -56,13 +56,27 @@ __global__ void __launch_bounds__(256) beta_prep_kernel(BetaArgs a) {
   const Cell c = cell_of(a, i);
   const T *lb = (const T *)a.lb + c.base, *v = (const T *)a.v + c.base, *dO = (const T *)a.dO + c.base;
   T *Vh = (T *)a.Vh + c.base, *Oh = (T *)a.Oh + c.base;
+  constexpr int RB = 8;  // rows whose loads are issued together
   float E = 0.f;
-#pragma unroll 4
-  for (int r = 0; r < c.rows; ++r) {
-    const int64_t o = (int64_t)r * a.V;
-    E += (float)lb[o];
-    Vh[o] = cvt<T>((float)v[o] * __expf(-E));
-    Oh[o] = cvt<T>((float)dO[o] * __expf(E));
+  for (int r0 = 0; r0 < c.rows; r0 += RB) {
+    float x[RB], y[RB], z[RB];
+#pragma unroll
+    for (int r = 0; r < RB; ++r) {
+      const bool ok = r0 + r < c.rows;
+      const int64_t o = (int64_t)(ok ? r0 + r : r0) * a.V;
+      x[r] = ok ? (float)lb[o] : 0.f;
+      y[r] = (float)v[o];
+      z[r] = (float)dO[o];
+    }
+#pragma unroll
+    for (int r = 0; r < RB; ++r) {
+      E += x[r];
+      if (r0 + r < c.rows) {
+        const int64_t o = (int64_t)(r0 + r) * a.V;
+        Vh[o] = cvt<T>(y[r] * __expf(-E));
+        Oh[o] = cvt<T>(z[r] * __expf(E));
+      }
+    }
   }
   a.gb[c.cn * a.V + c.col] = __expf(E);
 }
