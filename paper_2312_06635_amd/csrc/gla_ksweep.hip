@@ -899,10 +899,10 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
   fetch_slab(0, 0);
   fetch_slab(0, 1);
 
+  if constexpr (GB) fetch_sv(N - 1, 0);
   for (int it = 0; it < N; ++it) {
     const int n = N - 1 - it;
     const int t0 = n * C, rv = min(C, a.T - t0);
-    if constexpr (GB) fetch_sv(n, 0);
     // ---- factors
     float c[4], kv[4], qdq[4], zc[4];  // zc: the gate argument, for the gate gradient
     {
@@ -1009,6 +1009,8 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
       __syncthreads();
     }
 
+    // the next chunk's first state tile, in flight during the combine phases
+    if constexpr (GB) fetch_sv(max(n - 1, 0), 0);
     // ---- dk_inter partials, pre-scaled by exp(B_last - B at the block's end)
     partials_publish<L>(acc, sSc, sRed, w, g, j);
     __syncthreads();
