@@ -59,10 +59,47 @@ gla_status check_lds(const Shape &s, bool bwd) {
   return GLA_OK;
 }
 
-// Workspace layout; op 1 extends op 0, op 2 (the general form's backward)
-// extends op 1.  Returns the total byte count and, if base is non-null, the
-// region pointers.
-size_t layout(const Shape &s, int op, char *base, Work *w) {
+// Sequence segments: with few heads and long sequences, each head's
+// sequence is split into nseg segments of whole chunks (at least four each),
+// processed as separate heads and joined by the segment scans of
+// gla_segment.hip (App. A.2's two-stage form).  nseg minimises a simple cost:
+// the chunks each sweep walks in sequence times the rounds of 256 workgroups
+// it needs (key sweeps weighted 2 against 1 for the value sweeps, which run
+// twice when segmented); ties keep fewer segments.  Decided from the shape
+// alone, so forward and backward agree.  The general form (value-side gate)
+// is not segmented.
+int choose_nseg(const Shape &s) {
+  if (s.T <= 0 || s.T % s.C != 0) return 1;
+  const int64_t KT = (s.K + 31) / 32, VT = (s.V + 63) / 64;
+  auto rounds = [](int64_t wgs) { return (wgs + 255) / 256; };
+  auto cost = [&](int n) {
+    const int64_t steps = s.N / n;
+    return 4 * rounds((int64_t)s.BH * n * KT) * steps + (n > 1 ? 4 : 2) * rounds((int64_t)s.BH * n * VT) * steps;
+  };
+  int best = 1;
+  int64_t best_cost = cost(1);
+  for (int n = 2; s.N % n == 0 && s.N / n >= 4 && (int64_t)s.BH * n <= (1 << 24); n *= 2) {
+    const int64_t c = cost(n);
+    if (c < best_cost) {
+      best = n;
+      best_cost = c;
+    }
+  }
+  return best;
+}
+
+Shape seg_shape(const Shape &s, int nseg) {
+  Shape t = s;
+  t.BH = s.BH * nseg;
+  t.T = s.T / nseg;
+  t.N = s.N / nseg;
+  return t;
+}
+
+// Workspace layout of the (segmented) shape s; op 1 extends op 0, op 2 (the
+// general form's backward) extends op 1.  Returns the total byte count and, if
+// base is non-null, the region pointers.
+size_t layout(const Shape &s, int op, char *base, Work *w, int nseg) {
   const size_t es = s.esz();
   const size_t rows = (size_t)s.BH * s.T, chunks = (size_t)s.BH * s.N;
   size_t off = 0;
@@ -76,6 +113,13 @@ size_t layout(const Shape &s, int op, char *base, Work *w) {
   void *P = take(chunks * s.C * s.C * es);
   void *gam = take(chunks * s.K * sizeof(float));
   void *wflag = take(chunks * 4);
+  const size_t states = (size_t)s.BH * s.K * s.V * sizeof(float);  // s.BH counts the segments
+  void *Sin = nullptr, *Sloc = nullptr, *dec = nullptr, *dSout = nullptr;
+  if (nseg > 1) {
+    Sin = take(states);
+    Sloc = take(states);
+    dec = take((size_t)s.BH * s.K * sizeof(float));
+  }
   void *dP = nullptr, *cST = nullptr, *dq_lo = nullptr, *dla_part = nullptr;
   void *Vh = nullptr, *Oh = nullptr, *gb = nullptr, *Sb = nullptr, *cpart = nullptr;
   if (op >= 1) {
@@ -83,6 +127,7 @@ size_t layout(const Shape &s, int op, char *base, Work *w) {
     cST = take((size_t)s.BH * s.K * sizeof(float));
     if (s.io == gla::IO_BF16) dq_lo = take(rows * s.K * 2);
     if (s.sgate) dla_part = take(rows * ((s.K + 31) / 32) * sizeof(float));
+    if (nseg > 1) dSout = take(states);
   }
   if (op == 2) {
     Vh = take(rows * s.V * es);
@@ -95,6 +140,7 @@ size_t layout(const Shape &s, int op, char *base, Work *w) {
     w->Qt = Qt; w->Kt = Kt; w->P = P; w->gam = (float *)gam; w->wflag = (unsigned char *)wflag;
     w->dP = (float *)dP; w->cST = (float *)cST; w->dq_lo = dq_lo; w->dla_part = (float *)dla_part;
     w->Vh = Vh; w->Oh = Oh; w->gb = (float *)gb; w->Sb = Sb; w->cpart = (float *)cpart;
+    w->Sin = (float *)Sin; w->Sloc = (float *)Sloc; w->dec = (float *)dec; w->dSout = (float *)dSout;
   }
   return off;
 }
@@ -119,7 +165,8 @@ GLA_EXPORT const char *gla_status_string(gla_status st) {
 GLA_EXPORT size_t gla_workspace_bytes(const gla_problem *prob, int op) {
   Shape s;
   if (make_shape(prob, s) != GLA_OK || op < 0 || op > 2) return 0;
-  return layout(s, op, nullptr, nullptr);
+  const int nseg = op == 2 ? 1 : choose_nseg(s);
+  return layout(seg_shape(s, nseg), op, nullptr, nullptr, nseg);
 }
 
 namespace {
@@ -136,17 +183,30 @@ gla_status chunk_fwd(const gla_problem *prob, const void *q, const void *k, cons
   if (stage > 2) return GLA_ERR_SHAPE;
   const bool any = (int64_t)s.BH * s.T > 0;
   if (any && (!q || !k || !v || !o)) return GLA_ERR_NULL;
-  const size_t need = layout(s, 0, nullptr, nullptr);
+  const int nseg = log_beta ? 1 : choose_nseg(s);
+  const Shape s2 = seg_shape(s, nseg);
+  const size_t need = layout(s2, 0, nullptr, nullptr, nseg);
   if (any && (!workspace || workspace_bytes < need)) return GLA_ERR_WORKSPACE;
   hipStream_t hs = (hipStream_t)stream;
   if (s.BH == 0) return GLA_OK;
   if (s.T == 0)
     return hip_status(gla::launch_copy_state((int64_t)s.BH * s.K * s.V, S0, S_T, hs));
   Work w;
-  layout(s, 0, (char *)workspace, &w);
+  layout(s2, 0, (char *)workspace, &w, nseg);
   hipError_t e = hipSuccess;
-  if (stage == 0 || stage == 1) e = gla::launch_prep(s, q, k, log_alpha, w, hs);
-  if (e == hipSuccess && (stage == 0 || stage == 2)) e = gla::launch_fwd_main(s, v, log_beta, S0, o, S_T, w, hs);
+  if (stage == 0 || stage == 1) e = gla::launch_prep(s2, q, k, log_alpha, w, hs);
+  if (e == hipSuccess && (stage == 0 || stage == 2)) {
+    if (nseg == 1) {
+      e = gla::launch_fwd_main(s, v, log_beta, S0, o, S_T, w, hs);
+    } else {
+      // local final states, the segment scan, then the outputs from each
+      // segment's true initial state
+      e = gla::launch_fwd_main(s2, v, nullptr, nullptr, o, w.Sloc, w, hs);
+      if (e == hipSuccess) e = gla::launch_seg_decay(s2, w.gam, w.dec, hs);
+      if (e == hipSuccess) e = gla::launch_seg_fwd_scan(s.BH, nseg, s.K, s.V, w.dec, S0, w.Sloc, w.Sin, S_T, hs);
+      if (e == hipSuccess) e = gla::launch_fwd_main(s2, v, nullptr, w.Sin, o, nullptr, w, hs);
+    }
+  }
   return hip_status(e);
 }
 
@@ -200,7 +260,9 @@ GLA_EXPORT gla_status gla_chunk_bwd(const gla_problem *prob, const void *q, cons
   if (stage > 4) return GLA_ERR_SHAPE;
   const bool any = (int64_t)s.BH * s.T > 0;
   if (any && (!q || !k || !v || !dO || !dq || !dk || !dv)) return GLA_ERR_NULL;
-  const size_t need = layout(s, 1, nullptr, nullptr);
+  const int nseg = choose_nseg(s);
+  const Shape s2 = seg_shape(s, nseg);
+  const size_t need = layout(s2, 1, nullptr, nullptr, nseg);
   if (any && (!workspace || workspace_bytes < need)) return GLA_ERR_WORKSPACE;
   hipStream_t hs = (hipStream_t)stream;
   if (s.BH == 0) return GLA_OK;
@@ -208,14 +270,34 @@ GLA_EXPORT gla_status gla_chunk_bwd(const gla_problem *prob, const void *q, cons
     return hip_status(gla::launch_copy_state((int64_t)s.BH * s.K * s.V, dS_T, dS0, hs));
   auto run = [stage](unsigned k) { return stage == 0 || stage == k; };
   Work w;
-  layout(s, 1, (char *)workspace, &w);
+  layout(s2, 1, (char *)workspace, &w, nseg);
   hipError_t e = hipSuccess;
-  if (run(1) && !(prob->flags & GLA_FLAG_REUSE_FWD_WORKSPACE))
-    e = gla::launch_prep(s, q, k, log_alpha, w, hs);
-  if (e == hipSuccess && run(2)) e = gla::launch_bwd_dq(s, k, log_alpha, v, S0, dO, dS_T, dq, w, hs);
+  if (run(1) && !(prob->flags & GLA_FLAG_REUSE_FWD_WORKSPACE)) {
+    e = gla::launch_prep(s2, q, k, log_alpha, w, hs);
+    if (nseg > 1) {
+      // each segment's initial state, as in the forward (dv serves as scratch
+      // for the outputs, which are not needed here)
+      if (e == hipSuccess) e = gla::launch_fwd_main(s2, v, nullptr, nullptr, dv, w.Sloc, w, hs);
+      if (e == hipSuccess) e = gla::launch_seg_decay(s2, w.gam, w.dec, hs);
+      if (e == hipSuccess) e = gla::launch_seg_fwd_scan(s.BH, nseg, s.K, s.V, w.dec, S0, w.Sloc, w.Sin, nullptr, hs);
+    }
+  }
+  // per segment: initial state and final-state gradient (the head's own S0
+  // and dS_T when unsegmented)
+  const float *S0s = nseg > 1 ? w.Sin : S0, *dSTs = nseg > 1 ? w.dSout : dS_T;
+  if (e == hipSuccess && run(2)) {
+    if (nseg > 1) {
+      // local initial-state gradients from a zero final-state gradient, then
+      // the reverse segment scan (which also gives the head's dS0)
+      e = gla::launch_bwd_dv(s2, dO, nullptr, nullptr, dv, w.Sloc, w, hs);
+      if (e == hipSuccess)
+        e = gla::launch_seg_bwd_scan(s.BH, nseg, s.K, s.V, w.dec, dS_T, w.Sloc, w.dSout, dS0, hs);
+    }
+    if (e == hipSuccess) e = gla::launch_bwd_dq(s2, k, log_alpha, v, S0s, dO, dSTs, dq, w, hs);
+  }
   if (e == hipSuccess && run(3))
-    e = gla::launch_bwd_dk(s, q, k, log_alpha, v, dO, dS_T, dq, dk, dlog_alpha, w, hs);
-  if (e == hipSuccess && run(4)) e = gla::launch_bwd_dv(s, dO, nullptr, dS_T, dv, dS0, w, hs);
+    e = gla::launch_bwd_dk(s2, q, k, log_alpha, v, dO, dSTs, dq, dk, dlog_alpha, w, hs);
+  if (e == hipSuccess && run(4)) e = gla::launch_bwd_dv(s2, dO, nullptr, dSTs, dv, nseg > 1 ? nullptr : dS0, w, hs);
   return hip_status(e);
 }
 
@@ -235,7 +317,7 @@ GLA_EXPORT gla_status gla_chunk_bwd_general(const gla_problem *prob, const void 
   const bool any = (int64_t)s.BH * s.T > 0;
   if (any && (!q || !k || !v || !log_beta || !dO || !dq || !dk || !dv)) return GLA_ERR_NULL;
   if (any && dlog_beta && !o) return GLA_ERR_NULL;
-  const size_t need = layout(s, 2, nullptr, nullptr);
+  const size_t need = layout(s, 2, nullptr, nullptr, 1);
   if (any && (!workspace || workspace_bytes < need)) return GLA_ERR_WORKSPACE;
   hipStream_t hs = (hipStream_t)stream;
   if (s.BH == 0) return GLA_OK;
@@ -243,7 +325,7 @@ GLA_EXPORT gla_status gla_chunk_bwd_general(const gla_problem *prob, const void 
     return hip_status(gla::launch_copy_state((int64_t)s.BH * s.K * s.V, dS_T, dS0, hs));
   auto run = [stage](unsigned k) { return stage == 0 || stage == k; };
   Work w;
-  layout(s, 2, (char *)workspace, &w);
+  layout(s, 2, (char *)workspace, &w, 1);
   hipError_t e = hipSuccess;
   if (run(1) && !(prob->flags & GLA_FLAG_REUSE_FWD_WORKSPACE))
     e = gla::launch_prep(s, q, k, log_alpha, w, hs);

@@ -36,6 +36,12 @@ struct Work {
   void *Vh = nullptr;         // [BH][T][V] io : V (.) exp(-E)
   void *Oh = nullptr;         // [BH][T][V] io : dO (.) exp(E)
   float *gb = nullptr;        // [BH][N][V] fp32 : chunk decay exp(E_last)
+  // sequence segments (few heads, long sequences; the kernels then run on the
+  // segmented shape, whose heads are the segments)
+  float *Sin = nullptr;       // [BH nseg][K][V] fp32 : each segment's initial state
+  float *Sloc = nullptr;      // [BH nseg][K][V] fp32 : local final states; then local dS0
+  float *dec = nullptr;       // [BH nseg][K] fp32 : each segment's decay
+  float *dSout = nullptr;     // [BH nseg][K][V] fp32 : each segment's final-state gradient
   void *Sb = nullptr;         // chunk-end states S_[n+1] (io), written by the dq sweep (ks_state_bytes)
   float *cpart = nullptr;     // [BH][N][ceil(K/32)][V] fp32 : per key tile colsum(S_[n+1] (.) dS_[n+1])
 };
@@ -76,6 +82,12 @@ hipError_t launch_outgate_bwd(int B, int H, int T, int V, int io, const void *o,
                               const float *b, float eps, const void *dy, void *d_o, void *dg, float *dw,
                               float *db, float *part, hipStream_t st);
 
+// Sequence segments (gla_segment.hip); s2 is the segmented shape.
+hipError_t launch_seg_decay(const Shape &s2, const float *gam, float *dec, hipStream_t st);
+hipError_t launch_seg_fwd_scan(int BH, int nseg, int K, int V, const float *dec, const float *S0, const float *Sloc,
+                               float *Sin, float *ST, hipStream_t st);
+hipError_t launch_seg_bwd_scan(int BH, int nseg, int K, int V, const float *dec, const float *dST,
+                               const float *dS0loc, float *dSout, float *dS0, hipStream_t st);
 // LDS bytes each kernel needs (0 means the shape is not supported).
 size_t lds_prep(const Shape &s);
 size_t lds_fwd_main(const Shape &s);

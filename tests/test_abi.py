@@ -87,6 +87,21 @@ def test_scalar_gate_workspace(L):
         assert need <= extra < need + 256
 
 
+def test_sequence_segments_workspace(L):
+    """Few heads and a long sequence: the workspace holds the segments'
+    initial and local final states (forward) and final-state gradients
+    (backward) -- 8 segments for 4 heads of 16384 steps at d_k 256, d_v 512 --
+    and none when the sequence does not divide into whole chunks."""
+    p = P(B=1, H=4, T=16384, dk=256, dv=512)
+    f, b = L.gla_workspace_bytes(ctypes.byref(p), 0), L.gla_workspace_bytes(ctypes.byref(p), 1)
+    states = 4 * 8 * 256 * 512 * 4
+    kernels_fwd = 2 * 4 * 16384 * 256 * 2 + 4 * 256 * 64 * 64 * 2
+    assert f >= kernels_fwd + 2 * states
+    assert b >= f + states
+    q = P(B=1, H=4, T=16384 - 16, dk=256, dv=512)  # a ragged last chunk: not segmented
+    assert L.gla_workspace_bytes(ctypes.byref(q), 0) < kernels_fwd + states
+
+
 def fwd_call(L, p, ptr=1, ws=1, ws_bytes=1 << 40):
     return L.gla_chunk_fwd(ctypes.byref(p) if p is not None else None, ptr, ptr, ptr, ptr, None,
                            ptr, None, ws, ws_bytes, None)

@@ -635,6 +635,69 @@ def test_full_size_extensions_sampled_heads(mode):
     assert not bad, bad
 
 
+@pytest.mark.parametrize("mode", ["log_alpha", "scalar", "preact"])
+def test_sequence_segments(mode):
+    """One head and 1024 steps: the sequence is split into segments processed
+    as separate heads and joined by the segment scans (the two-stage form of
+    App. A.2); every output against the oracle, with S0 and dS_T, also for
+    scalar gates and the gate epilogue; the stage selector still reproduces
+    the whole call."""
+    g = gla()
+    tau = 16.0
+    cfg = small_case("seg_" + mode, "bf16", 1, 1, 1024, 64, 128, 64, 16, 31, s0_std=0.1)
+    inp = W.make_inputs(cfg, dST_std=0.1)
+    gen = torch.Generator().manual_seed(32)
+    if mode == "scalar":
+        inp["log_alpha"] = torch.nn.functional.logsigmoid(torch.randn(1, 1, 1024, generator=gen) + 1.0).to(torch.bfloat16)
+    z = None
+    if mode == "preact":
+        z = (torch.randn(inp["log_alpha"].shape, generator=gen) * 2.0 + 1.0).to(torch.bfloat16)
+    d = to_dev(inp)
+    gate = z.cuda() if z is not None else d["log_alpha"]
+    gt = tau if mode == "preact" else 0.0
+    ws = torch.empty(g.workspace_bytes(1, 1, 1024, 64, 128, 64, 16, torch.bfloat16, op=1, scalar_gate=mode == "scalar"),
+                     dtype=torch.uint8, device="cuda")
+    o, ST = g.chunk_fwd(d["q"], d["k"], d["v"], gate, 64, 16, S0=d["S0"], output_final_state=True, workspace=ws,
+                        gate_tau=gt)
+    gr = g.chunk_bwd(d["q"], d["k"], d["v"], gate, d["dO"], 64, 16, S0=d["S0"], dST=d["dST"], want_dS0=True,
+                     workspace=ws, reuse_fwd_workspace=True, gate_tau=gt)
+    gr2 = g.chunk_bwd(d["q"], d["k"], d["v"], gate, d["dO"], 64, 16, S0=d["S0"], dST=d["dST"], want_dS0=True,
+                      gate_tau=gt)
+    o3, ST3 = torch.empty_like(o), torch.empty_like(ST)
+    for st in (1, 2):
+        g.chunk_fwd(d["q"], d["k"], d["v"], gate, 64, 16, S0=d["S0"], workspace=ws, stage=st, out=(o3, ST3),
+                    gate_tau=gt)
+    out = {k2: (torch.empty_like(v2) if v2 is not None else None) for k2, v2 in gr.items()}
+    for st in (2, 3, 4):
+        g.chunk_bwd(d["q"], d["k"], d["v"], gate, d["dO"], 64, 16, S0=d["S0"], dST=d["dST"], workspace=ws,
+                    reuse_fwd_workspace=True, stage=st, out=out, gate_tau=gt)
+    torch.cuda.synchronize()
+    assert torch.equal(o, o3) and torch.equal(ST, ST3), "stages, forward"
+    for k2 in gr:
+        assert torch.equal(gr[k2], out[k2]), "stages, " + k2
+        assert torch.equal(gr[k2], gr2[k2]), "reuse, " + k2
+    idx = [0]
+    q, k, v, dO = (heads(inp[n], idx) for n in ("q", "k", "v", "dO"))
+    S0, dST = heads(inp["S0"], idx), heads(inp["dST"], idx)
+    if mode == "scalar":
+        lg = heads(inp["log_alpha"], idx)
+        ro, rST = oracle.scalar_gate_fwd(q, k, v, lg, S0)
+        rg = oracle.scalar_gate_bwd(q, k, v, lg, dO, S0=S0, dST=dST)
+        rg["dlog_alpha"] = rg.pop("dlog_gamma")
+    else:
+        la = oracle.gate_log_alpha(heads(z, idx), tau) if mode == "preact" else heads(inp["log_alpha"], idx)
+        ro, rST = oracle.fwd(q, k, v, la, S0)
+        rg = oracle.bwd(q, k, v, la, dO, S0=S0, dST=dST)
+        if mode == "preact":
+            rg["dlog_alpha"] = oracle.gate_grad(heads(z, idx), tau, rg["dlog_alpha"])
+    errs = {"o": rel(heads(o, idx), ro), "S_T": rel(heads(ST, idx), rST)}
+    for n in ("dq", "dk", "dv", "dlog_alpha", "dS0"):
+        errs[n] = rel(heads(gr[n], idx), rg[n])
+    say("segments", mode, {k2: f"{v2:.2e}" for k2, v2 in errs.items()})
+    bad = {k2: v2 for k2, v2 in errs.items() if not v2 <= TOL["bf16"]}
+    assert not bad, bad
+
+
 def test_stage_by_stage_equals_whole_call():
     """The stage selector (used by the benchmark to time each kernel) runs the
     same kernels: stages in order reproduce the whole call exactly."""
