@@ -43,6 +43,17 @@
  *     to pairwise exponentials when a sub-chunk's decay range is large).
  *   - There is no scale argument (Eq. 3 has none): pre-scale k if desired.
  *
+ * Few heads, long sequences: when B*H is too small to fill the GPU and T is
+ * a multiple of the chunk, the chunkwise calls split each head's sequence into
+ * segments of whole chunks, run them as separate heads and join them with
+ * segment scans over the chunk decays (the two-stage form of App. A.2).  This
+ * is decided from the shape alone (so gla_workspace_bytes accounts for it and
+ * a forward's workspace stays valid for the backward's reuse flag), changes
+ * only the summation order, and keeps the stage selector's meaning (forward
+ * stage 2 then holds both state passes and the scan; backward stage 1 also
+ * rebuilds the segments' initial states, stage 2 also their final-state
+ * gradients).  The general form (value-side gate) is never segmented.
+ *
  * Supported shapes: d_k and d_v multiples of 16 with d_k <= 256 and
  * d_v <= 1024 (fp32 io additionally needs d_k <= 128); chunk C in {16, 32, 64}; sub-chunk c a divisor of 16 that also
  * divides C; any T >= 0 (a last, shorter chunk is handled by masking).
