@@ -1165,15 +1165,12 @@ KsArgs ks_args(const Shape &s) {
 
 template <bool DQ, typename T, int CP, int NSL, bool PRE, bool GB>
 hipError_t launch_ks_pre(const KsArgs &a, hipStream_t st) {
-  static bool attr = false;
   const size_t lds = KsLayout<T, CP>::total;
-  const void *fn;
-  if constexpr (DQ) fn = (const void *)dq_sweep_kernel<T, CP, NSL, PRE, GB>;
-  else fn = (const void *)dk_sweep_kernel<T, CP, NSL, PRE, GB>;
-  if (!attr) {
-    (void)hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    attr = true;
-  }
+  // once per instantiation (thread-safe static initialisation), at the maximum
+  static const hipError_t attr = hipFuncSetAttribute(
+      DQ ? (const void *)dq_sweep_kernel<T, CP, NSL, PRE, GB> : (const void *)dk_sweep_kernel<T, CP, NSL, PRE, GB>,
+      hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
+  (void)attr;
   if constexpr (DQ)
     hipLaunchKernelGGL((dq_sweep_kernel<T, CP, NSL, PRE, GB>), dim3(a.BH * a.KT), dim3(kKT), lds, st, a);
   else

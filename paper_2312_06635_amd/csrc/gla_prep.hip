@@ -421,12 +421,11 @@ size_t lds_prep(const Shape &s) {
 
 template <typename T, int FPL, bool PRE>
 static hipError_t launch_prep_pre(const Shape &s, const PrepArgs &a, size_t lds, hipStream_t st) {
-  static bool attr = false;
-  if (!attr) {
-    (void)hipFuncSetAttribute((const void *)prep_kernel<T, FPL, PRE>,
-                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    attr = true;
-  }
+  // once per instantiation (thread-safe static initialisation), at the
+  // maximum, since the LDS size depends on the shape
+  static const hipError_t attr = hipFuncSetAttribute((const void *)prep_kernel<T, FPL, PRE>,
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
+  (void)attr;
   dim3 grid(s.N, s.BH), block(64 * (s.C / 16));
   hipLaunchKernelGGL((prep_kernel<T, FPL, PRE>), grid, block, lds, st, a);
   hipError_t e = hipGetLastError();

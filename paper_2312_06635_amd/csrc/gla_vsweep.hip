@@ -378,13 +378,11 @@ size_t sweep_lds(const Shape &s) {
 
 template <typename T, int KP, int CP, bool REV, bool GB>
 hipError_t launch_sweep_gb(const SweepArgs &a, hipStream_t st) {
-  static bool attr = false;
   const size_t lds = GB ? SweepLayout<T, KP, CP>::total_gb : SweepLayout<T, KP, CP>::total;
-  if (!attr) {
-    (void)hipFuncSetAttribute((const void *)sweep_kernel<T, KP, CP, REV, GB>,
-                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    attr = true;
-  }
+  // once per instantiation (thread-safe static initialisation), at the maximum
+  static const hipError_t attr = hipFuncSetAttribute((const void *)sweep_kernel<T, KP, CP, REV, GB>,
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
+  (void)attr;
   hipLaunchKernelGGL((sweep_kernel<T, KP, CP, REV, GB>), dim3(a.BH * a.ntiles), dim3(kThreads), lds, st, a);
   return hipGetLastError();
 }
