@@ -54,7 +54,7 @@
  * rebuilds the segments' initial states, stage 2 also their final-state
  * gradients).  The general form (value-side gate) is never segmented.
  *
- * Supported shapes: d_k and d_v multiples of 16 with d_k <= 256 and
+ * Supported shapes: B*H <= 65535; d_k and d_v multiples of 16 with d_k <= 256 and
  * d_v <= 1024 (fp32 io additionally needs d_k <= 128); chunk C in {16, 32, 64}; sub-chunk c a divisor of 16 that also
  * divides C; any T >= 0 (a last, shorter chunk is handled by masking).
  * Other values return GLA_ERR_UNSUPPORTED.

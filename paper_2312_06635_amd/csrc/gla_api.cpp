@@ -29,7 +29,7 @@ gla_status make_shape(const gla_problem *p, Shape &s) {
   if (p->chunk != 16 && p->chunk != 32 && p->chunk != 64) return GLA_ERR_UNSUPPORTED;
   if (16 % p->subchunk != 0) return GLA_ERR_UNSUPPORTED;
   const int64_t BH = (int64_t)p->B * p->H;
-  if (BH > (1 << 24)) return GLA_ERR_UNSUPPORTED;
+  if (BH > 65535) return GLA_ERR_UNSUPPORTED;  // heads are a grid dimension of the prep and recurrent kernels
   s.BH = (int)BH;
   s.T = p->T;
   s.K = p->dk;
@@ -78,7 +78,7 @@ int choose_nseg(const Shape &s) {
   };
   int best = 1;
   int64_t best_cost = cost(1);
-  for (int n = 2; s.N % n == 0 && s.N / n >= 4 && (int64_t)s.BH * n <= (1 << 24); n *= 2) {
+  for (int n = 2; s.N % n == 0 && s.N / n >= 4 && (int64_t)s.BH * n <= 65535; n *= 2) {
     const int64_t c = cost(n);
     if (c < best_cost) {
       best = n;

@@ -124,6 +124,8 @@ def bwd_call(L, p, ptr=1, ws=1, ws_bytes=1 << 40):
     (dict(chunk=128, subchunk=16), gla.GLA_ERR_UNSUPPORTED),
     (dict(chunk=64, subchunk=32), gla.GLA_ERR_UNSUPPORTED),
     (dict(io=gla.GLA_F32, dk=256), gla.GLA_ERR_UNSUPPORTED),
+    (dict(B=65536, H=1), gla.GLA_ERR_UNSUPPORTED),
+    (dict(B=256, H=256), gla.GLA_ERR_UNSUPPORTED),
     (dict(gate_tau=-16.0), gla.GLA_ERR_SHAPE),
     (dict(gate_tau=float("inf")), gla.GLA_ERR_SHAPE),
     (dict(gate_tau=float("nan")), gla.GLA_ERR_SHAPE),
