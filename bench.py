@@ -183,6 +183,9 @@ def main():
                     help="general form G = alpha^T beta (App. C): adds log beta [B, H, T, d_v]")
     ap.add_argument("--output-gate", action="store_true",
                     help="include the output side (per-head LN + Swish gate, Sec. 4.4) in the step")
+    ap.add_argument("--segments", type=int, default=0,
+                    help="fix the sequence segments per head (GLA_SEGMENTS: 1 = states on chip, T/chunk = every "
+                         "chunk's state materialized in HBM); 0 = the library's choice")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (reference for HBM traffic counters)")
     args = ap.parse_args()
@@ -220,8 +223,12 @@ def main():
         inp_cpu["log_alpha"] = torch.nn.functional.logsigmoid(z.double()).div(args.gate_tau).to(inp_cpu["q"].dtype)
     B, H, T, K, V, C, c = (cfg[x] for x in ("B", "H", "T", "dk", "dv", "chunk", "subchunk"))
     dt = d["q"].dtype
-    ws = torch.empty(gla.workspace_bytes(B, H, T, K, V, C, c, dt, op=1, scalar_gate=args.scalar_gate),
-                     dtype=torch.uint8, device=dev)
+    ws = torch.empty(gla.workspace_bytes(B, H, T, K, V, C, c, dt, op=1, scalar_gate=args.scalar_gate,
+                                         segments=args.segments), dtype=torch.uint8, device=dev)
+    if ws.numel() == 0:
+        print(f"--segments {args.segments} does not fit this workload (it must divide T/chunk = {T // C})",
+              file=sys.stderr)
+        sys.exit(2)
     o = torch.empty_like(d["v"])
     ST = torch.empty(B, H, K, V, dtype=torch.float32, device=dev) if cfg["want_state"] else None
     grads = {"dq": torch.empty_like(d["q"]), "dk": torch.empty_like(d["k"]), "dv": torch.empty_like(d["v"]),
@@ -230,8 +237,8 @@ def main():
     stream = torch.cuda.current_stream(dev)
     stages = STAGES_OG if args.output_gate else STAGES
     if args.value_gate:
-        if args.output_gate or args.gate_tau > 0:
-            print("--value-gate does not combine with --output-gate or --gate-tau", file=sys.stderr)
+        if args.output_gate or args.gate_tau > 0 or args.segments > 1:
+            print("--value-gate does not combine with --output-gate, --gate-tau or --segments", file=sys.stderr)
             sys.exit(2)
         stages = STAGES_GB
         gb = torch.Generator().manual_seed(cfg["seed"] + 13)
@@ -265,11 +272,12 @@ def main():
                           log_beta=d["log_beta"], o=o)
         elif which == "fwd":
             gla.chunk_fwd(d["q"], d["k"], d["v"], d["log_alpha"], C, c, S0=d["S0"], workspace=ws,
-                          stage=stage, out=(o, ST), gate_tau=args.gate_tau, log_beta=d.get("log_beta"))
+                          stage=stage, out=(o, ST), gate_tau=args.gate_tau, log_beta=d.get("log_beta"),
+                          segments=args.segments)
         else:
             gla.chunk_bwd(d["q"], d["k"], d["v"], d["log_alpha"], d["dO"], C, c, S0=d["S0"], dST=d["dST"],
                           workspace=ws, reuse_fwd_workspace=True, stage=stage, out=grads,
-                          gate_tau=args.gate_tau)
+                          gate_tau=args.gate_tau, segments=args.segments)
 
     def step(events=None):
         if events is not None:
@@ -320,7 +328,8 @@ def main():
 
     dom = max(stage_ms, key=stage_ms.get)
     roof = roofline(dom)
-    plain = not (args.no_gate or args.gate_tau > 0 or args.output_gate or args.scalar_gate or args.value_gate)
+    plain = not (args.no_gate or args.gate_tau > 0 or args.output_gate or args.scalar_gate or args.value_gate or
+                 args.segments)
     roof["traffic"] = measured_traffic(args.workload, dom) if plain else None
     roof["avg_ms"] = stage_ms[dom]
     stage_frac = {nm: f"{r['frac']:.3f} of {r['bound']}" for nm, r in ((nm, roofline(nm)) for nm in stage_ms)}
@@ -339,7 +348,8 @@ def main():
                    **({"value_gate": "general form alpha^T beta, log beta [B, H, T, d_v]"}
                       if args.value_gate else {}),
                    **({"output_side": "per-head LN (affine) + Swish output gate, fwd + bwd"}
-                      if args.output_gate else {})},
+                      if args.output_gate else {}),
+                   **({"segments": args.segments} if args.segments else {})},
         "tflops": tflops, "mfma_peak_frac": tflops * 1e12 / peak,
         "hbm_io_roofline_frac": (io_bytes / PEAK_HBM) / (elapsed / args.steps),
         "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},

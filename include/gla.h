@@ -52,7 +52,9 @@
  * only the summation order, and keeps the stage selector's meaning (forward
  * stage 2 then holds both state passes and the scan; backward stage 1 also
  * rebuilds the segments' initial states, stage 2 also their final-state
- * gradients).  The general form (value-side gate) is never segmented.
+ * gradients).  GLA_SEGMENTS(n) in the flags fixes the segment count instead,
+ * up to one chunk per segment (materialized chunk states).  The general form
+ * (value-side gate) is never segmented.
  *
  * Supported shapes: B*H <= 65535; d_k and d_v multiples of 16 with d_k <= 256 and
  * d_v <= 1024 (fp32 io additionally needs d_k <= 128); chunk C in {16, 32, 64}; sub-chunk c a divisor of 16 that also
@@ -111,8 +113,28 @@ enum {
    *                  4 = reverse sweep over value-column tiles: dv, dS0
    * Out-of-range stage numbers return GLA_ERR_SHAPE. */
   GLA_STAGE_SHIFT = 8,
-  GLA_STAGE_MASK = 0xFu << 8
+  GLA_STAGE_MASK = 0xFu << 8,
+  /* Bits 16..30 fix the number of sequence segments per head of the chunkwise
+   * calls (the split described under "Few heads, long sequences" above)
+   * instead of letting the shape decide; 0 = decided from the shape.  This is
+   * the choice of Sec. 3.3 between keeping the chunk-level states on chip and
+   * materializing them in HBM: 1 keeps each head's state in the workgroups
+   * for the whole sequence (the non-materialization version: no state is
+   * written), T/C (one chunk per segment) writes every chunk's initial state
+   * S_[n] to the workspace and computes all chunks in parallel (the
+   * materialization version), and a value in between materializes the state
+   * at the start of every (T/C)/n-th chunk.  The value must divide T/C, T
+   * must be a multiple of C (when T > 0), and B*H times the value must not
+   * exceed 65535; else GLA_ERR_UNSUPPORTED (and gla_workspace_bytes gives
+   * 0).  gla_workspace_bytes honours it (the states take
+   * 2 B H n d_k d_v fp32 in the forward's workspace, one more such array in
+   * the backward's); a forward and the backward that reuses its workspace
+   * must be given the same value.  The general form accepts only 0 and 1;
+   * the recurrent calls ignore it.  GLA_SEGMENTS(n) builds the field. */
+  GLA_SEGMENTS_SHIFT = 16,
+  GLA_SEGMENTS_MASK = 0x7FFF << 16
 };
+#define GLA_SEGMENTS(n) ((uint32_t)(n) << GLA_SEGMENTS_SHIFT)
 
 typedef struct {
   int32_t B, H;      /* batch rows and heads; heads are independent            */

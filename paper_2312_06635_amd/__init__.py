@@ -33,6 +33,8 @@ GLA_F32, GLA_BF16 = 0, 1
 FLAG_REUSE_FWD_WORKSPACE = 1
 FLAG_SCALAR_GATE = 2
 STAGE_SHIFT = 8
+SEGMENTS_SHIFT = 16
+SEGMENTS_MAX = 0x7FFF
 
 
 class GlaProblem(ctypes.Structure):
@@ -142,10 +144,20 @@ def _stream(dev):
     return torch.cuda.current_stream(dev).cuda_stream
 
 
-def workspace_bytes(B, H, T, dk, dv, chunk, subchunk, dtype=torch.bfloat16, op=1, scalar_gate=False) -> int:
+def _segments_flag(segments):
+    """GLA_SEGMENTS(n): 0 lets the library decide from the shape."""
+    n = int(segments)
+    if not 0 <= n <= SEGMENTS_MAX:
+        raise ValueError(f"segments must be in [0, {SEGMENTS_MAX}]")
+    return n << SEGMENTS_SHIFT
+
+
+def workspace_bytes(B, H, T, dk, dv, chunk, subchunk, dtype=torch.bfloat16, op=1, scalar_gate=False,
+                    segments=0) -> int:
     """Workspace bytes for the forward (op=0) or backward (op=1); scalar_gate
-    for a [B, H, T] gate."""
-    p = GlaProblem(B, H, T, dk, dv, chunk, subchunk, _io_code(dtype), FLAG_SCALAR_GATE if scalar_gate else 0)
+    for a [B, H, T] gate; segments as in chunk_fwd (0 if it does not fit)."""
+    flags = (FLAG_SCALAR_GATE if scalar_gate else 0) | _segments_flag(segments)
+    p = GlaProblem(B, H, T, dk, dv, chunk, subchunk, _io_code(dtype), flags)
     return int(lib().gla_workspace_bytes(ctypes.byref(p), op))
 
 
@@ -173,7 +185,7 @@ def _check_beta(lb, v):
 
 
 def chunk_fwd(q, k, v, log_alpha, chunk=64, subchunk=16, S0=None, output_final_state=False,
-              workspace=None, stage=0, out=None, gate_tau=0.0, log_beta=None):
+              workspace=None, stage=0, out=None, gate_tau=0.0, log_beta=None, segments=0):
     """Chunkwise GLA forward.  Returns (o, S_T or None).
 
     log_alpha=None means alpha = 1 (ungated linear attention): no gate tensor
@@ -182,12 +194,15 @@ def chunk_fwd(q, k, v, log_alpha, chunk=64, subchunk=16, S0=None, output_final_s
     alpha = sigmoid(z)^(1/gate_tau) (the GLA gate).  stage selects one kernel of the launch sequence (see
     GLA_STAGE_* in include/gla.h); out=(o, S_T) reuses caller-provided output
     tensors.  log_beta ([B, H, T, d_v]) adds the value-side gate of the
-    general form G_t = alpha_t^T beta_t (App. C; forward only)."""
+    general form G_t = alpha_t^T beta_t (App. C; forward only).  segments
+    fixes the sequence segments per head (GLA_SEGMENTS in include/gla.h: 1 =
+    states on chip, T/chunk = every chunk's state materialized; 0 = decided
+    from the shape)."""
     _check(q, k, v, log_alpha, states=(("S0", S0),))
     _check_beta(log_beta, v)
     B, H, T, dk = q.shape
     dv = v.shape[3]
-    p = _problem(q, v, chunk, subchunk, stage << STAGE_SHIFT, gate_tau, log_alpha)
+    p = _problem(q, v, chunk, subchunk, (stage << STAGE_SHIFT) | _segments_flag(segments), gate_tau, log_alpha)
     if out is not None:
         o, ST = out
     else:
@@ -209,7 +224,7 @@ def chunk_fwd(q, k, v, log_alpha, chunk=64, subchunk=16, S0=None, output_final_s
 
 def chunk_bwd(q, k, v, log_alpha, dO, chunk=64, subchunk=16, S0=None, dST=None,
               want_dS0=False, workspace=None, reuse_fwd_workspace=False, stage=0, out=None,
-              gate_tau=0.0, log_beta=None, o=None):
+              gate_tau=0.0, log_beta=None, o=None, segments=0):
     """Chunkwise GLA backward for L = sum(o * dO) + sum(S_T * dS_T).
 
     Returns dict(dq, dk, dv, dlog_alpha, dS0); dlog_alpha is None when
@@ -220,13 +235,16 @@ def chunk_bwd(q, k, v, log_alpha, dO, chunk=64, subchunk=16, S0=None, dST=None,
     stage and out as in chunk_fwd (out is a dict shaped like the result).
     log_beta: the general form's value-side gate (App. C); the result then
     also holds dlog_beta, which needs the forward's output o (without o it is
-    None); the workspace must be sized for op=2 (general_workspace_bytes)."""
+    None); the workspace must be sized for op=2 (general_workspace_bytes).
+    segments as in chunk_fwd (the same value as the forward's when its
+    workspace is reused)."""
     _check(q, k, v, log_alpha, extra=(("dO", dO, v.shape[3]),), states=(("S0", S0), ("dST", dST)))
     _check_beta(log_beta, v)
     _check_beta(o, v)
     B, H, T, dk = q.shape
     dv = v.shape[3]
-    flags = (FLAG_REUSE_FWD_WORKSPACE if reuse_fwd_workspace else 0) | (stage << STAGE_SHIFT)
+    flags = (FLAG_REUSE_FWD_WORKSPACE if reuse_fwd_workspace else 0) | (stage << STAGE_SHIFT) | \
+        _segments_flag(segments)
     p = _problem(q, v, chunk, subchunk, flags, gate_tau, log_alpha)
     if reuse_fwd_workspace and workspace is None:
         raise ValueError("reuse_fwd_workspace needs the workspace the forward used")

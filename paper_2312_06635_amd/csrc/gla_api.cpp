@@ -88,6 +88,17 @@ int choose_nseg(const Shape &s) {
   return best;
 }
 
+// The segment count a call runs with: the caller's (GLA_SEGMENTS), else the
+// cost model's; 0 when the caller's does not fit the shape.  general: the
+// value-gate calls, which run unsegmented.
+int resolve_nseg(const Shape &s, uint32_t flags, bool general) {
+  const int want = (int)((flags & GLA_SEGMENTS_MASK) >> GLA_SEGMENTS_SHIFT);
+  if (want == 0) return general ? 1 : choose_nseg(s);
+  if (want == 1 || (s.T == 0 && !general)) return 1;
+  if (general || s.T % s.C != 0 || s.N % want != 0 || (int64_t)s.BH * want > 65535) return 0;
+  return want;
+}
+
 Shape seg_shape(const Shape &s, int nseg) {
   Shape t = s;
   t.BH = s.BH * nseg;
@@ -165,7 +176,8 @@ GLA_EXPORT const char *gla_status_string(gla_status st) {
 GLA_EXPORT size_t gla_workspace_bytes(const gla_problem *prob, int op) {
   Shape s;
   if (make_shape(prob, s) != GLA_OK || op < 0 || op > 2) return 0;
-  const int nseg = op == 2 ? 1 : choose_nseg(s);
+  const int nseg = resolve_nseg(s, prob->flags, op == 2);
+  if (nseg == 0) return 0;
   return layout(seg_shape(s, nseg), op, nullptr, nullptr, nseg);
 }
 
@@ -183,7 +195,8 @@ gla_status chunk_fwd(const gla_problem *prob, const void *q, const void *k, cons
   if (stage > 2) return GLA_ERR_SHAPE;
   const bool any = (int64_t)s.BH * s.T > 0;
   if (any && (!q || !k || !v || !o)) return GLA_ERR_NULL;
-  const int nseg = log_beta ? 1 : choose_nseg(s);
+  const int nseg = resolve_nseg(s, prob->flags, log_beta != nullptr);
+  if (nseg == 0) return GLA_ERR_UNSUPPORTED;
   const Shape s2 = seg_shape(s, nseg);
   const size_t need = layout(s2, 0, nullptr, nullptr, nseg);
   if (any && (!workspace || workspace_bytes < need)) return GLA_ERR_WORKSPACE;
@@ -260,7 +273,8 @@ GLA_EXPORT gla_status gla_chunk_bwd(const gla_problem *prob, const void *q, cons
   if (stage > 4) return GLA_ERR_SHAPE;
   const bool any = (int64_t)s.BH * s.T > 0;
   if (any && (!q || !k || !v || !dO || !dq || !dk || !dv)) return GLA_ERR_NULL;
-  const int nseg = choose_nseg(s);
+  const int nseg = resolve_nseg(s, prob->flags, false);
+  if (nseg == 0) return GLA_ERR_UNSUPPORTED;
   const Shape s2 = seg_shape(s, nseg);
   const size_t need = layout(s2, 1, nullptr, nullptr, nseg);
   if (any && (!workspace || workspace_bytes < need)) return GLA_ERR_WORKSPACE;
@@ -317,6 +331,7 @@ GLA_EXPORT gla_status gla_chunk_bwd_general(const gla_problem *prob, const void 
   const bool any = (int64_t)s.BH * s.T > 0;
   if (any && (!q || !k || !v || !log_beta || !dO || !dq || !dk || !dv)) return GLA_ERR_NULL;
   if (any && dlog_beta && !o) return GLA_ERR_NULL;
+  if (resolve_nseg(s, prob->flags, true) != 1) return GLA_ERR_UNSUPPORTED;
   const size_t need = layout(s, 2, nullptr, nullptr, 1);
   if (any && (!workspace || workspace_bytes < need)) return GLA_ERR_WORKSPACE;
   hipStream_t hs = (hipStream_t)stream;

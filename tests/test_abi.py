@@ -102,6 +102,50 @@ def test_sequence_segments_workspace(L):
     assert L.gla_workspace_bytes(ctypes.byref(q), 0) < kernels_fwd + states
 
 
+def test_segment_count_can_be_fixed(L):
+    """GLA_SEGMENTS(n) overrides the shape's choice: 1 keeps every state on
+    chip (no state arrays), T/C materializes every chunk's initial state (two
+    [B H n d_k d_v] fp32 arrays in the forward's workspace, a third in the
+    backward's); a count that does not divide T/C, a ragged T, too many heads
+    or a segmented general form is refused."""
+    seg = lambda n: n << gla.SEGMENTS_SHIFT
+    long_ = dict(B=1, H=4, T=16384, dk=256, dv=512)
+    auto = L.gla_workspace_bytes(ctypes.byref(P(**long_)), 0)
+    one = L.gla_workspace_bytes(ctypes.byref(P(**long_, flags=seg(1))), 0)
+    eight = L.gla_workspace_bytes(ctypes.byref(P(**long_, flags=seg(8))), 0)
+    assert eight == auto  # the cost model's own choice for this shape
+    state = 4 * 256 * 512 * 4  # one [B H d_k d_v] fp32 array
+    for n in (2, 16, 256):
+        f = L.gla_workspace_bytes(ctypes.byref(P(**long_, flags=seg(n))), 0)
+        b = L.gla_workspace_bytes(ctypes.byref(P(**long_, flags=seg(n))), 1)
+        assert 2 * n * state <= f - one < 2 * n * state + n * 4 * 256 * 4 + 3 * 256
+        b1 = L.gla_workspace_bytes(ctypes.byref(P(**long_, flags=seg(1))), 1)
+        assert 3 * n * state <= b - b1 < 3 * n * state + 2 * n * 4 * 256 * 4 + 4 * 256  # + decays, cST
+    short = dict(T=256)  # N = 4 chunks of 64
+    for n, ok in ((1, True), (2, True), (4, True), (3, False), (8, False)):
+        p = P(**short, flags=seg(n))
+        assert (L.gla_workspace_bytes(ctypes.byref(p), 1) > 0) == ok
+        if not ok:  # (a valid problem would launch: never with these fake pointers)
+            assert fwd_call(L, p) == gla.GLA_ERR_UNSUPPORTED
+            assert bwd_call(L, p) == gla.GLA_ERR_UNSUPPORTED
+    ragged = P(T=200, flags=seg(2))
+    assert L.gla_workspace_bytes(ctypes.byref(ragged), 0) == 0
+    assert fwd_call(L, ragged) == gla.GLA_ERR_UNSUPPORTED and bwd_call(L, ragged) == gla.GLA_ERR_UNSUPPORTED
+    assert L.gla_workspace_bytes(ctypes.byref(P(T=200, flags=seg(1))), 0) > 0
+    heads = P(B=1024, H=32, T=4096, flags=seg(2))  # 32768 heads x 2 segments > 65535
+    assert L.gla_workspace_bytes(ctypes.byref(heads), 0) == 0
+    assert fwd_call(L, heads) == gla.GLA_ERR_UNSUPPORTED
+    # empty sequences accept any count; the general form only 0 and 1
+    assert L.gla_workspace_bytes(ctypes.byref(P(T=0, flags=seg(3))), 1) >= 0
+    assert L.gla_workspace_bytes(ctypes.byref(P(T=256, flags=seg(2))), 2) == 0
+    assert L.gla_workspace_bytes(ctypes.byref(P(T=256, flags=seg(1))), 2) == \
+        L.gla_workspace_bytes(ctypes.byref(P(T=256)), 2)
+    args = (1, 1, 1, 1, 1, None, 1, None, 1, 1 << 40, None)
+    assert L.gla_chunk_fwd_general(ctypes.byref(P(T=256, flags=seg(2))), *args) == gla.GLA_ERR_UNSUPPORTED
+    assert L.gla_chunk_bwd_general(ctypes.byref(P(T=256, flags=seg(2))), 1, 1, 1, 1, 1, None, 1, 1, None, 1, 1, 1,
+                                   1, 1, None, 1, 1 << 40, None) == gla.GLA_ERR_UNSUPPORTED
+
+
 def fwd_call(L, p, ptr=1, ws=1, ws_bytes=1 << 40):
     return L.gla_chunk_fwd(ctypes.byref(p) if p is not None else None, ptr, ptr, ptr, ptr, None,
                            ptr, None, ws, ws_bytes, None)

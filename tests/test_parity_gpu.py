@@ -721,3 +721,44 @@ def test_stage_by_stage_equals_whole_call():
     assert torch.equal(o, o2) and torch.equal(ST, ST2)
     for k in ref:
         assert torch.equal(ref[k], out[k]), k
+
+
+@pytest.mark.parametrize("io,nseg", [("bf16", 1), ("bf16", 2), ("bf16", 8), ("f32", 1), ("f32", 8)])
+def test_fixed_segment_counts(io, nseg):
+    """GLA_SEGMENTS(n): the caller fixes the segments per head, from 1 (every
+    state on chip, the non-materialization version of Sec. 3.3) to one chunk
+    per segment (every chunk's initial state materialized in the workspace,
+    the materialization version); with S0 and dS_T, every output against the
+    oracle, and the backward that reuses the forward's workspace equals the
+    one that rebuilds it."""
+    g = gla()
+    B, H, T, K, V = 1, 2, 512, 64, 128
+    cfg = small_case(f"nseg{nseg}_{io}", io, B, H, T, K, V, 64, 16, 40 + nseg, s0_std=0.1)
+    inp = W.make_inputs(cfg, dST_std=0.1)
+    d = to_dev(inp)
+    dt = d["q"].dtype
+    ws = torch.empty(g.workspace_bytes(B, H, T, K, V, 64, 16, dt, op=1, segments=nseg), dtype=torch.uint8,
+                     device="cuda")
+    if nseg > 1:
+        assert ws.numel() >= g.workspace_bytes(B, H, T, K, V, 64, 16, dt, op=1, segments=1) + \
+            3 * B * H * nseg * K * V * 4
+    o, ST = g.chunk_fwd(d["q"], d["k"], d["v"], d["log_alpha"], 64, 16, S0=d["S0"], output_final_state=True,
+                        workspace=ws, segments=nseg)
+    gr = g.chunk_bwd(d["q"], d["k"], d["v"], d["log_alpha"], d["dO"], 64, 16, S0=d["S0"], dST=d["dST"],
+                     want_dS0=True, workspace=ws, reuse_fwd_workspace=True, segments=nseg)
+    gr2 = g.chunk_bwd(d["q"], d["k"], d["v"], d["log_alpha"], d["dO"], 64, 16, S0=d["S0"], dST=d["dST"],
+                      want_dS0=True, segments=nseg)
+    torch.cuda.synchronize()
+    for k2 in gr:
+        assert torch.equal(gr[k2], gr2[k2]), "reuse, " + k2
+    idx = list(range(B * H))
+    q, k, v, la, dO = (heads(inp[n], idx) for n in ("q", "k", "v", "log_alpha", "dO"))
+    S0, dST = heads(inp["S0"], idx), heads(inp["dST"], idx)
+    ro, rST = oracle.fwd(q, k, v, la, S0)
+    rg = oracle.bwd(q, k, v, la, dO, S0=S0, dST=dST)
+    errs = {"o": rel(heads(o, idx), ro), "S_T": rel(heads(ST, idx), rST)}
+    for n in ("dq", "dk", "dv", "dlog_alpha", "dS0"):
+        errs[n] = rel(heads(gr[n], idx), rg[n])
+    say("fixed segments", io, nseg, {k2: f"{v2:.2e}" for k2, v2 in errs.items()})
+    bad = {k2: v2 for k2, v2 in errs.items() if not v2 <= TOL[io]}
+    assert not bad, bad
