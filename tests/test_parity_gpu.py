@@ -134,6 +134,28 @@ def test_small_parity(case):
     compare(inp, o, ST, gr, list(range(cfg["B"] * cfg["H"])), cfg["io"], cfg["name"])
 
 
+@pytest.mark.parametrize("io,dk,dv", [("f32", 16, 32), ("bf16", 32, 48)])
+def test_most_heads(io, dk, dv):
+    """B*H = 65535, the largest head count (a grid dimension of the prep and
+    recurrent kernels, the whole grid of the sweeps), with a ragged chunk,
+    S0 and dS_T: sampled heads from both ends and the middle against the
+    oracle, chunkwise and recurrent."""
+    cfg = small_case(f"heads65535_{io}", io, 65535, 1, 20, dk, dv, 16, 8, 26, s0_std=0.1)
+    say("case", cfg["name"])
+    inp = W.make_inputs(cfg, dST_std=0.1)
+    o, ST, gr = run_gpu(inp, 16, 8, want_state=True)
+    idx = [0, 1, 32768, 65533, 65534]
+    compare(inp, o, ST, gr, idx, io, cfg["name"])
+    d = to_dev(inp)
+    ro_gpu, rST_gpu = gla().recurrent_fwd(d["q"], d["k"], d["v"], d["log_alpha"], S0=d["S0"],
+                                          output_final_state=True)
+    torch.cuda.synchronize()
+    ro, rST = oracle.fwd(*(heads(inp[n], idx) for n in ("q", "k", "v", "log_alpha")), heads(inp["S0"], idx))
+    e1, e2 = rel(heads(ro_gpu, idx), ro), rel(heads(rST_gpu, idx), rST)
+    say("recurrent, most heads", io, e1, e2)
+    assert e1 <= TOL[io] and e2 <= TOL[io]
+
+
 @pytest.mark.parametrize("io", ["f32", "bf16"])
 def test_strong_decay_uses_pairwise_exponentials(io):
     """Per-step log gates down to -8 push a 16-row block's decay far past the
