@@ -195,6 +195,19 @@ template <typename T, int ROWS, int COLS, int NT> struct TileLd {
       if (ROWS % RSTEP == 0 || row < ROWS) *(u32x4 *)(dst + row * ld + cs * EV) = r[i];
     }
   }
+  // store() into a 2-byte tile whose 8-byte units are XOR-permuted per row:
+  // unit u of row r lands at unit u ^ sw(r) (sw(r) below the row's unit count).
+  template <typename F> __device__ __forceinline__ void store_xor8(T *dst, int ld, F sw) const {
+    static_assert(sizeof(T) == 2, "8-byte units of 2-byte elements");
+    const int row0 = (int)threadIdx.x / VPR, ch = (int)threadIdx.x % VPR;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int row = row0 + i * RSTEP;
+      const int s = sw(row);
+      const u32x4 v = (s & 1) ? u32x4{r[i][2], r[i][3], r[i][0], r[i][1]} : r[i];
+      if (ROWS % RSTEP == 0 || row < ROWS) *(u32x4 *)(dst + row * ld + ((ch ^ (s >> 1)) * EV)) = v;
+    }
+  }
   __device__ __forceinline__ void store(T *dst, int ld) const {
     const int row0 = (int)threadIdx.x / VPR, c = ((int)threadIdx.x % VPR) * EV;
 #pragma unroll

@@ -128,6 +128,36 @@ __device__ __forceinline__ frag_t<T> ld_col_perm(const T *X, int ld, int r0, int
   }
 }
 
+// bf16 tiles read with transpose loads (the update's key tile Y, the value
+// tile Z and, backward, P) are stored with their 8-byte units XOR-permuted per
+// row instead of padded.  A 32-lane phase of those loads touches rows
+// 8g + 0..3 (g = 0, 1) of a 32-row block, four lanes per row, and with any
+// padded stride rows r and r + 8 share LDS banks (a 2-way conflict on every
+// load).  The permutations below give the eight rows disjoint banks; they use
+// row bits 0, 1 and 3 only, so the second load of a fragment (rows + 4) and
+// every 32-row block reuse the lane's base.  Stores stay conflict-free: each
+// row's units are only permuted among themselves.
+//   key rows of 2 KP bytes: unit u of row r at u ^ swz_key(r)
+//   value / P rows of 128 (64) bytes: unit u at u ^ swz_val(r)
+template <int KP> __device__ __forceinline__ int swz_key(int r) {
+  if constexpr (KP >= 128) return (r & 1) | ((r & 2) << 2) | ((r & 8) << 1);
+  else return ((r & 2) >> 1) | (r & 8);  // 128-byte rows: odd rows already use the other bank half
+}
+template <int RB> __device__ __forceinline__ int swz_val(int r) {
+  if constexpr (RB >= 128) return ((r & 2) << 1) | (r & 8);
+  else return (r & 8) >> 1;
+}
+
+// Transposed fragment (the ld_col / ld_col_perm element order) from such a
+// tile: rb = row bytes, lb = the lane's base offset for a block starting at
+// row 0 and column 0 (the column start c0 is XORed in).
+__device__ __forceinline__ bf16x8 ld_tr_xor8(const bf16 *X, int rb, int r0, int c0, int lb) {
+  const char *p = (const char *)X + r0 * rb + (lb ^ (2 * c0));
+  s4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4 *)p);
+  s4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4 *)(p + 4 * rb));
+  return __builtin_bit_cast(bf16x8, s8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]});
+}
+
 // GB: value-side gate.
 template <typename T, int KP, int CP, bool REV, bool GB>
 __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
@@ -157,6 +187,22 @@ __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
   const bool active = v0 + cbase < V;       // V is a multiple of 16
   const int fbase = kh * KH;
   const int col = v0 + cbase + j;
+  // bf16 transposed-read lane bases (see swz_key / swz_val): row 8g + j/4 of
+  // the block, four lanes per row
+  constexpr bool XS = sizeof(T) == 2;
+  constexpr int RBY = 2 * KP, RBZ = 2 * kTile, RBP = 2 * CP;
+  const int Rl = 8 * g + (j >> 2), bq = j & 3;
+  const int lbY0 = Rl * RBY + 8 * ((2 * bq) ^ swz_key<KP>(Rl)), lbY1 = Rl * RBY + 8 * ((2 * bq + 1) ^ swz_key<KP>(Rl));
+  const int lbZ = Rl * RBZ + ((8 * bq) | (8 * swz_val<RBZ>(Rl)));
+  const int lbP = Rl * RBP + ((8 * bq) | (8 * swz_val<RBP>(Rl)));
+  auto col_z = [&](int r0, int c0) -> frag_t<T> {  // ld_col(sZ)
+    if constexpr (XS) return ld_tr_xor8(sZ, RBZ, r0, c0, lbZ);
+    else return ld_col<T>(sZ, L::LDZ, r0, c0);
+  };
+  auto zel = [&](int row, int c) {  // element (row, c) of the value tile
+    if constexpr (XS) return row * kTile + (c ^ (swz_val<RBZ>(row) << 2));
+    else return row * L::LDZ + c;
+  };
 
   // ---- state
   f4 R[NKB];
@@ -222,9 +268,16 @@ __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
     const int n = chunk_of(it);
     const int t0 = n * C, rv = min(C, a.T - t0);
     S.x.store(sX, L::LDX);
-    S.y.store(sY, L::LDY);
-    S.z.store(sZ, L::LDZ);
-    S.p.store(sP, L::LDP);
+    if constexpr (XS) {
+      S.y.store_xor8(sY, KP, [](int r) { return swz_key<KP>(r); });
+      S.z.store_xor8(sZ, kTile, [](int r) { return swz_val<RBZ>(r); });
+      if constexpr (REV) S.p.store_xor8(sP, CP, [](int r) { return swz_val<RBP>(r); });
+      else S.p.store(sP, L::LDP);  // read by rows (forward), padded
+    } else {
+      S.y.store(sY, L::LDY);
+      S.z.store(sZ, L::LDZ);
+      S.p.store(sP, L::LDP);
+    }
     if constexpr (GB) S.b.store(sLB, L::LDZ);
     if ((int)threadIdx.x < KP) sG[threadIdx.x] = S.g;
     __syncthreads();
@@ -249,7 +302,7 @@ __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
         const int row = grp * RG + r;
         pre += (float)sLB[row * L::LDZ + c];
         sE[row * L::LDE + c] = pre;
-        sZ[row * L::LDZ + c] = cvt<T>((float)sZ[row * L::LDZ + c] * __expf(REV ? pre : -pre));
+        sZ[zel(row, c)] = cvt<T>((float)sZ[zel(row, c)] * __expf(REV ? pre : -pre));
       }
       __syncthreads();
       if constexpr (REV) {
@@ -286,11 +339,16 @@ __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
           if constexpr (!REV) {
 #pragma unroll
             for (int sc = 0; sc <= (16 * I + 15) / 32; ++sc)
-              acc[I] = mma<T>(acc[I], ld_col<T>(sZ, L::LDZ, 32 * sc, cbase), ld_row<T>(sP, L::LDP, 16 * I, 32 * sc));
+              acc[I] = mma<T>(acc[I], col_z(32 * sc, cbase), ld_row<T>(sP, L::LDP, 16 * I, 32 * sc));
           } else {
 #pragma unroll
             for (int sc = (16 * I) / 32; sc < NSC; ++sc)
-              acc[I] = mma<T>(acc[I], ld_col<T>(sZ, L::LDZ, 32 * sc, cbase), ld_col<T>(sP, L::LDP, 32 * sc, 16 * I));
+            {
+              frag_t<T> pf;
+              if constexpr (XS) pf = ld_tr_xor8(sP, RBP, 32 * sc, 16 * I, lbP);
+              else pf = ld_col<T>(sP, L::LDP, 32 * sc, 16 * I);
+              acc[I] = mma<T>(acc[I], col_z(32 * sc, cbase), pf);
+            }
           }
         }
       } else {
@@ -301,7 +359,7 @@ __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
       // times the chunk decay exp(E_last) of this lane's value column)
       frag_t<T> zf[NSC];
 #pragma unroll
-      for (int sc = 0; sc < NSC; ++sc) zf[sc] = ld_col<T>(sZ, L::LDZ, 32 * sc, cbase);
+      for (int sc = 0; sc < NSC; ++sc) zf[sc] = col_z(32 * sc, cbase);
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb) {
         const int c0 = fbase + 32 * (kb >> 1);
@@ -309,7 +367,12 @@ __global__ void __launch_bounds__(kThreads) sweep_kernel(SweepArgs a) {
         R[kb] *= gm;
 #pragma unroll
         for (int sc = 0; sc < NSC; ++sc)
-          R[kb] = mma<T>(R[kb], ld_col_perm<T>(sY, L::LDY, 32 * sc, c0, kb & 1), zf[sc]);
+        {
+          frag_t<T> yf;
+          if constexpr (XS) yf = ld_tr_xor8(sY, RBY, 32 * sc, c0, (kb & 1) ? lbY1 : lbY0);
+          else yf = ld_col_perm<T>(sY, L::LDY, 32 * sc, c0, kb & 1);
+          R[kb] = mma<T>(R[kb], yf, zf[sc]);
+        }
       }
       if constexpr (GB && !REV) {
         const float gb = __expf(sE[(CP - 1) * L::LDE + cbase + j]);
