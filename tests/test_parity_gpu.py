@@ -570,7 +570,7 @@ def test_segment_split_matches_one_call():
 
 FULL = [("gla1p3b_T2048", False, 0.0), ("gla340m_T2048", False, 0.0), ("gla340m_T2048", True, 0.0),
         ("long_T16384", False, 0.0), ("long_T16384", False, 0.1)] + \
-       [(f"sweep_T{T}", False, 0.0) for T in W.SWEEP_T]
+       [(f"sweep_T{T}", False, 0.0) for T in W.SWEEP_T] + [("fig2_T2048", True, 0.0)]
 
 
 @pytest.mark.parametrize("name,alpha_one,dst", FULL,

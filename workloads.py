@@ -42,6 +42,9 @@ CONFIGS = {
 for _i, _T in enumerate(SWEEP_T):
     CONFIGS[f"sweep_T{_T}"] = _cfg(f"sweep_T{_T}", 32768 // _T, 16, _T, 128, 128, 64, 16, "bf16",
                                    4 + _i)
+# Context only: the shape of the paper's speed comparison of its chunkwise
+# kernels (Fig. 2: batch 32, 16 heads of dimension 64, chunk 64, ungated).
+CONFIGS["fig2_T2048"] = _cfg("fig2_T2048", 32, 16, 2048, 64, 64, 64, 16, "bf16", 9)
 
 
 def torch_dtype(io: str) -> torch.dtype:
