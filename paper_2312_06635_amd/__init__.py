@@ -9,6 +9,14 @@ raises if ``libgla.so`` has not been built.
 
 Layer (paper Sec. 4.1, Eq. 3), per batch row and head:
     S_t = Diag(exp(log_alpha_t)) S_{t-1} + k_t^T v_t,   o_t = q_t S_t.
+
+Example (tensors [B, H, T, d] on the HIP device, bf16 or fp32):
+    o, S_T = chunk_fwd(q, k, v, log_alpha, chunk=64, subchunk=16, output_final_state=True)
+    g = chunk_bwd(q, k, v, log_alpha, dO, chunk=64, subchunk=16)
+    g["dq"], g["dk"], g["dv"], g["dlog_alpha"]
+To let the backward reuse the forward's gated operands, size one workspace
+with workspace_bytes(..., op=1), pass it to both calls and set
+reuse_fwd_workspace=True on the backward.
 """
 from __future__ import annotations
 
@@ -22,6 +30,7 @@ __all__ = [
     "GLA_OK", "GLA_ERR_NULL", "GLA_ERR_SHAPE", "GLA_ERR_DTYPE", "GLA_ERR_UNSUPPORTED",
     "GLA_ERR_WORKSPACE", "GLA_ERR_HIP", "FLAG_REUSE_FWD_WORKSPACE", "FLAG_SCALAR_GATE", "GlaProblem", "lib",
     "output_gate_fwd", "output_gate_bwd", "output_gate_workspace_bytes", "general_workspace_bytes",
+    "SEGMENTS_SHIFT",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
