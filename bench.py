@@ -186,6 +186,8 @@ def main():
     ap.add_argument("--segments", type=int, default=0,
                     help="fix the sequence segments per head (GLA_SEGMENTS: 1 = states on chip, T/chunk = every "
                          "chunk's state materialized in HBM); 0 = the library's choice")
+    ap.add_argument("--fp32-diagonal", action="store_true",
+                    help="every diagonal sub-chunk block in fp32 log space (GLA_FLAG_FP32_DIAGONAL)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (reference for HBM traffic counters)")
     args = ap.parse_args()
@@ -269,15 +271,15 @@ def main():
         elif which == "bwdg":
             gla.chunk_bwd(d["q"], d["k"], d["v"], d["log_alpha"], d["dO"], C, c, S0=d["S0"], dST=d["dST"],
                           workspace=ws, reuse_fwd_workspace=True, stage=stage, out=grads,
-                          log_beta=d["log_beta"], o=o)
+                          log_beta=d["log_beta"], o=o, fp32_diagonal=args.fp32_diagonal)
         elif which == "fwd":
             gla.chunk_fwd(d["q"], d["k"], d["v"], d["log_alpha"], C, c, S0=d["S0"], workspace=ws,
                           stage=stage, out=(o, ST), gate_tau=args.gate_tau, log_beta=d.get("log_beta"),
-                          segments=args.segments)
+                          segments=args.segments, fp32_diagonal=args.fp32_diagonal)
         else:
             gla.chunk_bwd(d["q"], d["k"], d["v"], d["log_alpha"], d["dO"], C, c, S0=d["S0"], dST=d["dST"],
                           workspace=ws, reuse_fwd_workspace=True, stage=stage, out=grads,
-                          gate_tau=args.gate_tau, segments=args.segments)
+                          gate_tau=args.gate_tau, segments=args.segments, fp32_diagonal=args.fp32_diagonal)
 
     def step(events=None):
         if events is not None:
@@ -329,7 +331,7 @@ def main():
     dom = max(stage_ms, key=stage_ms.get)
     roof = roofline(dom)
     plain = not (args.no_gate or args.gate_tau > 0 or args.output_gate or args.scalar_gate or args.value_gate or
-                 args.segments)
+                 args.segments or args.fp32_diagonal)
     roof["traffic"] = measured_traffic(args.workload, dom) if plain else None
     roof["avg_ms"] = stage_ms[dom]
     stage_frac = {nm: f"{r['frac']:.3f} of {r['bound']}" for nm, r in ((nm, roofline(nm)) for nm in stage_ms)}
@@ -349,7 +351,8 @@ def main():
                       if args.value_gate else {}),
                    **({"output_side": "per-head LN (affine) + Swish output gate, fwd + bwd"}
                       if args.output_gate else {}),
-                   **({"segments": args.segments} if args.segments else {})},
+                   **({"segments": args.segments} if args.segments else {}),
+                   **({"diagonal_blocks": "fp32 log space"} if args.fp32_diagonal else {})},
         "tflops": tflops, "mfma_peak_frac": tflops * 1e12 / peak,
         "hbm_io_roofline_frac": (io_bytes / PEAK_HBM) / (elapsed / args.steps),
         "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},

@@ -101,6 +101,16 @@ enum {
    * point honours it, gla_workspace_bytes included (the backward then needs
    * B H ceil(d_k/32) T fp32 more). */
   GLA_FLAG_SCALAR_GATE = 1u << 1,
+  /* Every diagonal (within one sub-chunk) block of the intra-chunk terms,
+   * forward and backward, in fp32 log space: one exponential exp(B_i - B_j)
+   * per pair and feature on the vector ALUs, as the paper prescribes for these
+   * blocks (Sec. 4.3).  Without it they run on the matrix cores through the
+   * factorised decay exp(B_i - z) exp(z - B_j) with bf16 operands, and only
+   * blocks whose decay range is too wide for that fall back to the fp32 form.
+   * Slower; results differ at rounding level.  The chunkwise calls honour it
+   * (a backward that reuses a forward's workspace takes P as that forward
+   * formed it); the recurrent calls ignore it. */
+  GLA_FLAG_FP32_DIAGONAL = 1u << 2,
   /* Bits 8..11 select a single stage of an entry point's launch sequence (0 =
    * the whole sequence), so that a profiler or benchmark can time each kernel
    * on its own stream with events.  Running the stages 1, 2, ... in order with

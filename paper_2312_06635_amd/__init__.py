@@ -30,7 +30,7 @@ __all__ = [
     "GLA_OK", "GLA_ERR_NULL", "GLA_ERR_SHAPE", "GLA_ERR_DTYPE", "GLA_ERR_UNSUPPORTED",
     "GLA_ERR_WORKSPACE", "GLA_ERR_HIP", "FLAG_REUSE_FWD_WORKSPACE", "FLAG_SCALAR_GATE", "GlaProblem", "lib",
     "output_gate_fwd", "output_gate_bwd", "output_gate_workspace_bytes", "general_workspace_bytes",
-    "SEGMENTS_SHIFT",
+    "SEGMENTS_SHIFT", "FLAG_FP32_DIAGONAL",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -41,6 +41,7 @@ GLA_ERR_UNSUPPORTED, GLA_ERR_WORKSPACE, GLA_ERR_HIP = 4, 5, 6
 GLA_F32, GLA_BF16 = 0, 1
 FLAG_REUSE_FWD_WORKSPACE = 1
 FLAG_SCALAR_GATE = 2
+FLAG_FP32_DIAGONAL = 4
 STAGE_SHIFT = 8
 SEGMENTS_SHIFT = 16
 SEGMENTS_MAX = 0x7FFF
@@ -194,7 +195,8 @@ def _check_beta(lb, v):
 
 
 def chunk_fwd(q, k, v, log_alpha, chunk=64, subchunk=16, S0=None, output_final_state=False,
-              workspace=None, stage=0, out=None, gate_tau=0.0, log_beta=None, segments=0):
+              workspace=None, stage=0, out=None, gate_tau=0.0, log_beta=None, segments=0,
+              fp32_diagonal=False):
     """Chunkwise GLA forward.  Returns (o, S_T or None).
 
     log_alpha=None means alpha = 1 (ungated linear attention): no gate tensor
@@ -206,12 +208,14 @@ def chunk_fwd(q, k, v, log_alpha, chunk=64, subchunk=16, S0=None, output_final_s
     general form G_t = alpha_t^T beta_t (App. C; forward only).  segments
     fixes the sequence segments per head (GLA_SEGMENTS in include/gla.h: 1 =
     states on chip, T/chunk = every chunk's state materialized; 0 = decided
-    from the shape)."""
+    from the shape).  fp32_diagonal evaluates every diagonal sub-chunk block
+    in fp32 log space (GLA_FLAG_FP32_DIAGONAL) instead of on the matrix cores."""
     _check(q, k, v, log_alpha, states=(("S0", S0),))
     _check_beta(log_beta, v)
     B, H, T, dk = q.shape
     dv = v.shape[3]
-    p = _problem(q, v, chunk, subchunk, (stage << STAGE_SHIFT) | _segments_flag(segments), gate_tau, log_alpha)
+    flags = (stage << STAGE_SHIFT) | _segments_flag(segments) | (FLAG_FP32_DIAGONAL if fp32_diagonal else 0)
+    p = _problem(q, v, chunk, subchunk, flags, gate_tau, log_alpha)
     if out is not None:
         o, ST = out
     else:
@@ -233,7 +237,7 @@ def chunk_fwd(q, k, v, log_alpha, chunk=64, subchunk=16, S0=None, output_final_s
 
 def chunk_bwd(q, k, v, log_alpha, dO, chunk=64, subchunk=16, S0=None, dST=None,
               want_dS0=False, workspace=None, reuse_fwd_workspace=False, stage=0, out=None,
-              gate_tau=0.0, log_beta=None, o=None, segments=0):
+              gate_tau=0.0, log_beta=None, o=None, segments=0, fp32_diagonal=False):
     """Chunkwise GLA backward for L = sum(o * dO) + sum(S_T * dS_T).
 
     Returns dict(dq, dk, dv, dlog_alpha, dS0); dlog_alpha is None when
@@ -245,15 +249,15 @@ def chunk_bwd(q, k, v, log_alpha, dO, chunk=64, subchunk=16, S0=None, dST=None,
     log_beta: the general form's value-side gate (App. C); the result then
     also holds dlog_beta, which needs the forward's output o (without o it is
     None); the workspace must be sized for op=2 (general_workspace_bytes).
-    segments as in chunk_fwd (the same value as the forward's when its
-    workspace is reused)."""
+    segments and fp32_diagonal as in chunk_fwd (the same segments as the
+    forward's when its workspace is reused)."""
     _check(q, k, v, log_alpha, extra=(("dO", dO, v.shape[3]),), states=(("S0", S0), ("dST", dST)))
     _check_beta(log_beta, v)
     _check_beta(o, v)
     B, H, T, dk = q.shape
     dv = v.shape[3]
     flags = (FLAG_REUSE_FWD_WORKSPACE if reuse_fwd_workspace else 0) | (stage << STAGE_SHIFT) | \
-        _segments_flag(segments)
+        _segments_flag(segments) | (FLAG_FP32_DIAGONAL if fp32_diagonal else 0)
     p = _problem(q, v, chunk, subchunk, flags, gate_tau, log_alpha)
     if reuse_fwd_workspace and workspace is None:
         raise ValueError("reuse_fwd_workspace needs the workspace the forward used")

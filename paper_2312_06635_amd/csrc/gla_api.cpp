@@ -42,6 +42,7 @@ gla_status make_shape(const gla_problem *p, Shape &s) {
   if (!(p->gate_tau == 0.f || (p->gate_tau > 0.f && p->gate_tau < 3.0e38f))) return GLA_ERR_SHAPE;
   s.inv_tau = p->gate_tau == 0.f ? 0.f : 1.f / p->gate_tau;
   s.sgate = (p->flags & GLA_FLAG_SCALAR_GATE) != 0;
+  s.fp32_diag = (p->flags & GLA_FLAG_FP32_DIAGONAL) != 0;
   if (s.N > 65535) return GLA_ERR_UNSUPPORTED;
   // one head's rows of any tensor must span less than 2 GiB (32-bit buffer offsets)
   const int64_t wmax = p->dk > p->dv ? p->dk : p->dv;

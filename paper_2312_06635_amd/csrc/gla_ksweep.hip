@@ -73,7 +73,8 @@ struct KsArgs {
   float *cpart;     // general form: [BH][N][KT][V] per key tile colsum(S_[n+1] (.) dS_[n+1])
   int BH, T, K, V, C, N, KT;
   int sg;         // scalar gate: la is [BH][T], one value per step shared by every feature
-  float inv_tau;  // gate epilogue (0: la holds log alpha)
+  float wide_thr;  // a diagonal block takes pairwise decays when its decay range exceeds this
+  float inv_tau;   // gate epilogue (0: la holds log alpha)
 };
 
 template <typename T, int CP> struct KsLayout {
@@ -354,7 +355,7 @@ struct Factors {
 
 template <int NRG, int LDRG>
 __device__ __forceinline__ Factors chunk_factors(const float *sRg, const float (&c)[4], int frg, int blk,
-                                                 int fk, bool fv) {
+                                                 int fk, bool fv, float wide_thr) {
   // blk (the thread's 16-row block) is uniform across the wave; frg % 4 (its
   // row group inside the block) is not
   Factors f;
@@ -378,7 +379,7 @@ __device__ __forceinline__ Factors chunk_factors(const float *sRg, const float (
   const float ex = q == 0 ? 0.f : (q == 1 ? in_blk[0] : (q == 2 ? in_blk[0] + in_blk[1] : in_blk[0] + in_blk[1] + in_blk[2]));
 #pragma unroll
   for (int i = 0; i < 4; ++i) f.Bloc[i] = ex + c[i];
-  f.wide = fv && (-f.tot > kWide);
+  f.wide = fv && -f.tot > wide_thr;
   return f;
 }
 
@@ -576,7 +577,7 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
     }
     __syncthreads();
     if (fthr) {
-      const Factors f = chunk_factors<NRG, L::LDRG>(sRg, c, frg, w >> 1, fk, fv);
+      const Factors f = chunk_factors<NRG, L::LDRG>(sRg, c, frg, w >> 1, fk, fv, a.wide_thr);
       sFt[frg * kKF + fk] = f.tot;
       const float ekt = __expf(f.blast - f.pre - f.tot);
       f4 ko4, bl4;
@@ -724,7 +725,7 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
     // ---- dq = Lambda (.) inter + intra, per (row, feature)
     if (fthr) {
       const int blk = frg >> 2;
-      const bool wide = fv && (-sFt[frg * kKF + fk] > kWide);
+      const bool wide = fv && -sFt[frg * kKF + fk] > a.wide_thr;
       f4 in4 = *(const f4 *)(sOr + fk * L::LDT + 4 * frg);
 #pragma unroll
       for (int p = 0; p < L::NP; ++p) in4 += *(const f4 *)(sRed + (p * kKF + fk) * L::LDT + 4 * frg);
@@ -926,7 +927,7 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
     __syncthreads();
     pp.store(sdP, L::LDP);  // dP of this chunk, stored transposed ([s][t])
     if (fthr) {
-      const Factors f = chunk_factors<NRG, L::LDRG>(sRg, c, frg, w >> 1, fk, fv);
+      const Factors f = chunk_factors<NRG, L::LDRG>(sRg, c, frg, w >> 1, fk, fv, a.wide_thr);
       sFt[frg * kKF + fk] = f.tot;
       const float epre = __expf(f.pre);
       f4 qo4, bl4;
@@ -1044,7 +1045,7 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
     if (fthr) {
       const int blk = frg >> 2;
       const float tot = sFt[frg * kKF + fk];
-      const bool wide = fv && (-tot > kWide);
+      const bool wide = fv && -tot > a.wide_thr;
       f4 in4 = *(const f4 *)(sOr + fk * L::LDT + 4 * frg);
 #pragma unroll
       for (int p = 0; p < L::NP; ++p) in4 += *(const f4 *)(sRed + (p * kKF + fk) * L::LDT + 4 * frg);
@@ -1159,6 +1160,7 @@ KsArgs ks_args(const Shape &s) {
   a.BH = s.BH; a.T = s.T; a.K = s.K; a.V = s.V; a.C = s.C; a.N = s.N;
   a.inv_tau = s.inv_tau;
   a.sg = s.sgate ? 1 : 0;
+  a.wide_thr = s.fp32_diag ? -3.0e38f : kWide;
   a.KT = (s.K + kKF - 1) / kKF;
   return a;
 }

@@ -14,6 +14,7 @@ struct Shape {
   int io;
   float inv_tau;  // 0: the gate argument is log alpha; else 1 / tau of the gate epilogue
   bool sgate;     // scalar gate: one gate value per (head, step), [BH][T]
+  bool fp32_diag; // every diagonal sub-chunk block in fp32 log space (pairwise decays)
   int esz() const { return io == IO_BF16 ? 2 : 4; }
   int la_row() const { return sgate ? 1 : K; }  // gate elements per step
 };

@@ -36,6 +36,7 @@ struct PrepArgs {
   unsigned char *wflag;  // [BH][N][4]: diagonal block needs pairwise decays
   int T, K, Kp, C, N, ldk;
   int sg;         // scalar gate: la is [BH][T], one value per step shared by every feature
+  int fp32_diag;  // every diagonal block by pairwise decays (prep_wide_kernel)
   float inv_tau;  // gate epilogue (0: la holds log alpha)
 };
 
@@ -254,7 +255,7 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
   for (int f = 0; f < FPL; ++f) {
     ez[f] = __expf(pre[f]);                    // b_{block start} / b_{chunk start}
     ekt[f] = __expf(Bl[f] - pre[f] - tot[f]);  // b_{chunk end} / b_{block end}
-    if (fv && -tot[f] > kWideRange) wide = true;
+    if (fv && (a.fp32_diag || -tot[f] > kWideRange)) wide = true;
     if (fp) sEup[w * Kp + k0 + f] = __expf(-tot[f]);  // b_{block start} / b_{block end} >= 1
   }
   const bool wide_blk = __any(wide);
@@ -347,12 +348,14 @@ template <typename T, int FPL, bool PRE>
 __global__ void __launch_bounds__(256) prep_wide_kernel(PrepArgs a) {
   const int n = blockIdx.x, bh = blockIdx.y;
   const int w = wave_id(), l = lane_id();
-  if (!a.la || !a.wflag[((int64_t)bh * a.N + n) * 4 + w]) return;  // no gate: no wide block
+  // (without a gate only the fp32 option flags blocks)
+  if (!a.wflag[((int64_t)bh * a.N + n) * 4 + w]) return;
   const int C = a.C, K = a.K;
   const int t0 = n * C, rv = min(C, a.T - t0), d0 = 16 * w;
   const int64_t base = ((int64_t)bh * a.T + t0) * K;
-  const T *q = (const T *)a.q + base, *k = (const T *)a.k + base, *la = (const T *)a.la + base;
-  const T *las = (const T *)a.la + (int64_t)bh * a.T + t0;  // scalar gate rows
+  const T *q = (const T *)a.q + base, *k = (const T *)a.k + base;
+  const T *la = a.la ? (const T *)a.la + base : nullptr;
+  const T *las = a.la ? (const T *)a.la + (int64_t)bh * a.T + t0 : nullptr;  // scalar gate rows
   T *Pg = (T *)a.P + ((int64_t)bh * a.N + n) * C * C;
   const int k0 = FPL * l;
   const bool fv = k0 < K;
@@ -364,7 +367,10 @@ __global__ void __launch_bounds__(256) prep_wide_kernel(PrepArgs a) {
     const int row = d0 + r;
     const bool ok = fv && row < rv;
     float xl[FPL];
-    if (a.sg) {
+    if (!la) {  // no gate: log alpha = 0
+#pragma unroll
+      for (int f = 0; f < FPL; ++f) xl[f] = 0.f;
+    } else if (a.sg) {
       const float e = ok ? (float)las[row] : 0.f;
 #pragma unroll
       for (int f = 0; f < FPL; ++f) xl[f] = e;
@@ -448,6 +454,7 @@ hipError_t launch_prep(const Shape &s, const void *q, const void *k, const void 
   a.T = s.T; a.K = s.K; a.Kp = round_up(s.K, 32); a.C = s.C; a.N = s.N;
   a.inv_tau = s.inv_tau;
   a.sg = s.sgate ? 1 : 0;
+  a.fp32_diag = s.fp32_diag ? 1 : 0;
   a.ldk = a.Kp + 32 / s.esz();
   const size_t lds = lds_prep(s);
   const int fpl = (s.K + 63) / 64;

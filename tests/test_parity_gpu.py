@@ -784,3 +784,55 @@ def test_fixed_segment_counts(io, nseg):
     say("fixed segments", io, nseg, {k2: f"{v2:.2e}" for k2, v2 in errs.items()})
     bad = {k2: v2 for k2, v2 in errs.items() if not v2 <= TOL[io]}
     assert not bad, bad
+
+
+FD_CASES = [("f32", "gated", 200, 64, 16), ("bf16", "gated", 200, 64, 16), ("bf16", "ungated", 200, 64, 16),
+            ("bf16", "scalar", 200, 64, 16), ("bf16", "gated", 96, 32, 8)]
+
+
+@pytest.mark.parametrize("io,mode,T,C,c", FD_CASES, ids=[f"{a}-{b}-T{t}-C{cc}" for a, b, t, cc, _ in FD_CASES])
+def test_fp32_diagonal(io, mode, T, C, c):
+    """GLA_FLAG_FP32_DIAGONAL: every diagonal sub-chunk block in fp32 log
+    space (pairwise decays, Sec. 4.3) in the forward and the backward; every
+    output against the oracle with S0 and dS_T, a ragged chunk, also ungated,
+    with scalar gates and with 8-step sub-chunks; with a gate the option
+    changes the outputs (it is not ignored), within the bar."""
+    g = gla()
+    cfg = small_case(f"fp32diag_{io}_{mode}", io, 1, 2, T, 64, 96, C, c, 50, s0_std=0.1)
+    inp = W.make_inputs(cfg, alpha_one=(mode == "ungated"), dST_std=0.1)
+    if mode == "scalar":
+        gen = torch.Generator().manual_seed(51)
+        inp["log_alpha"] = torch.nn.functional.logsigmoid(torch.randn(1, 2, T, generator=gen)).to(inp["q"].dtype)
+    d = to_dev(inp)
+    gate = None if mode == "ungated" else d["log_alpha"]
+    res = {}
+    for fd in (False, True):
+        o, ST = g.chunk_fwd(d["q"], d["k"], d["v"], gate, C, c, S0=d["S0"], output_final_state=True,
+                            fp32_diagonal=fd)
+        gr = g.chunk_bwd(d["q"], d["k"], d["v"], gate, d["dO"], C, c, S0=d["S0"], dST=d["dST"], want_dS0=True,
+                         fp32_diagonal=fd)
+        res[fd] = (o, ST, gr)
+    torch.cuda.synchronize()
+    o, ST, gr = res[True]
+    if mode != "ungated":  # (with alpha = 1 the factorised form is exact and may round alike)
+        assert not torch.equal(o, res[False][0]), "the option changed nothing"
+    idx = [0, 1]
+    q, k, v, dO = (heads(inp[n], idx) for n in ("q", "k", "v", "dO"))
+    S0, dST = heads(inp["S0"], idx), heads(inp["dST"], idx)
+    if mode == "scalar":
+        lg = heads(inp["log_alpha"], idx)
+        ro, rST = oracle.scalar_gate_fwd(q, k, v, lg, S0)
+        rg = oracle.scalar_gate_bwd(q, k, v, lg, dO, S0=S0, dST=dST)
+        rg["dlog_alpha"] = rg.pop("dlog_gamma")
+    else:
+        la = heads(inp["log_alpha"], idx)
+        ro, rST = oracle.fwd(q, k, v, la, S0)
+        rg = oracle.bwd(q, k, v, la, dO, S0=S0, dST=dST)
+    errs = {"o": rel(heads(o, idx), ro), "S_T": rel(heads(ST, idx), rST)}
+    for n in ("dq", "dk", "dv", "dlog_alpha", "dS0"):
+        if mode == "ungated" and n == "dlog_alpha":
+            continue
+        errs[n] = rel(heads(gr[n], idx), rg[n])
+    say("fp32 diagonal", io, mode, T, C, c, {k2: f"{v2:.2e}" for k2, v2 in errs.items()})
+    bad = {k2: v2 for k2, v2 in errs.items() if not v2 <= TOL[io]}
+    assert not bad, bad
