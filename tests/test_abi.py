@@ -34,6 +34,27 @@ def test_header_declares_the_boundary():
                                     "gla_recurrent_fwd_general", "gla_status_string", "gla_workspace_bytes"]
 
 
+def test_header_is_plain_c(tmp_path):
+    """include/gla.h compiles as strict C99 and C++17 (no warnings), with every
+    flag and macro usable from C."""
+    src = tmp_path / "use.c"
+    src.write_text(
+        '#include "gla.h"\n'
+        "int main(void) {\n"
+        "  gla_problem p = {1, 1, 64, 16, 32, 16, 8, GLA_BF16, 0, 0.0f};\n"
+        "  p.flags = GLA_FLAG_REUSE_FWD_WORKSPACE | GLA_FLAG_SCALAR_GATE | GLA_FLAG_FP32_DIAGONAL |\n"
+        "            (2u << GLA_STAGE_SHIFT) | GLA_SEGMENTS(4);\n"
+        "  return (p.flags & (unsigned)GLA_SEGMENTS_MASK) == GLA_SEGMENTS(4) &&\n"
+        "         (p.flags & (unsigned)GLA_STAGE_MASK) >> GLA_STAGE_SHIFT == 2u ? 0 : 1;\n"
+        "}\n")
+    inc = os.path.join(ROOT, "include")
+    for cmd in (["gcc", "-std=c99"], ["g++", "-std=c++17", "-x", "c++"]):
+        exe = tmp_path / cmd[0]
+        subprocess.run(cmd + ["-Wall", "-Wextra", "-pedantic", "-Werror", "-I", inc, str(src), "-o", str(exe)],
+                       check=True, capture_output=True, text=True)
+        assert subprocess.run([str(exe)]).returncode == 0
+
+
 def test_every_declared_symbol_is_exported(L):
     for name in declared_functions():
         assert hasattr(L, name), name
