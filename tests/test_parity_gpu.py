@@ -892,3 +892,40 @@ def test_callers_stream_and_graph_replay():
         for t, r in zip(outs, ref):
             assert torch.equal(t, r), f"graph replay {rep}"
     say("streams and graph replay: bit-identical")
+
+
+def test_chunk_and_subchunk_invariance():
+    """The tiling does not change the layer (Sec. 4.2/4.3): for C = 16, 32, 64
+    every output meets the bar against the oracle, and for a given C every
+    sub-chunk length c (1, 2, 4, 8, 16) gives the same bits (sub-chunks
+    shorter than the 16-row blocks lie inside the diagonal blocks)."""
+    g = gla()
+    cfg = small_case("tiling", "bf16", 1, 2, 200, 64, 96, 64, 16, 61, s0_std=0.1)
+    inp = W.make_inputs(cfg, dST_std=0.1)
+    d = to_dev(inp)
+    idx = [0, 1]
+    q, k, v, la, dO = (heads(inp[n], idx) for n in ("q", "k", "v", "log_alpha", "dO"))
+    S0, dST = heads(inp["S0"], idx), heads(inp["dST"], idx)
+    ro, rST = oracle.fwd(q, k, v, la, S0)
+    rg = oracle.bwd(q, k, v, la, dO, S0=S0, dST=dST)
+    for C in (16, 32, 64):
+        first = None
+        for c in (1, 2, 4, 8, 16):
+            if C % c:
+                continue
+            o, ST = g.chunk_fwd(d["q"], d["k"], d["v"], d["log_alpha"], C, c, S0=d["S0"], output_final_state=True)
+            gr = g.chunk_bwd(d["q"], d["k"], d["v"], d["log_alpha"], d["dO"], C, c, S0=d["S0"], dST=d["dST"],
+                             want_dS0=True)
+            torch.cuda.synchronize()
+            outs = [o, ST] + [gr[n] for n in ("dq", "dk", "dv", "dlog_alpha", "dS0")]
+            if first is None:
+                first = outs
+                errs = {"o": rel(heads(o, idx), ro), "S_T": rel(heads(ST, idx), rST)}
+                for n in ("dq", "dk", "dv", "dlog_alpha", "dS0"):
+                    errs[n] = rel(heads(gr[n], idx), rg[n])
+                say("tiling C", C, {k2: f"{v2:.2e}" for k2, v2 in errs.items()})
+                bad = {k2: v2 for k2, v2 in errs.items() if not v2 <= TOL["bf16"]}
+                assert not bad, (C, bad)
+            else:
+                for a, b in zip(outs, first):
+                    assert torch.equal(a, b), (C, c)
