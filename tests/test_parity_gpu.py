@@ -929,3 +929,34 @@ def test_chunk_and_subchunk_invariance():
             else:
                 for a, b in zip(outs, first):
                     assert torch.equal(a, b), (C, c)
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_fp32_diagonal_general_form(io):
+    """GLA_FLAG_FP32_DIAGONAL with the general form (App. C): forward and
+    backward, every output and gradient including dlog beta against the
+    oracle, with S0 and dS_T and a ragged chunk."""
+    g = gla()
+    B, H, T, K, V, C, c = 1, 2, 150, 64, 80, 64, 16
+    cfg = small_case(f"fd_gg_{io}", io, B, H, T, K, V, C, c, 62, s0_std=0.1)
+    inp = W.make_inputs(cfg, dST_std=0.1)
+    gen = torch.Generator().manual_seed(63)
+    inp["log_beta"] = torch.nn.functional.logsigmoid(torch.randn(B, H, T, V, generator=gen) + 2.0).to(inp["q"].dtype)
+    d = to_dev(inp)
+    ws = torch.empty(g.general_workspace_bytes(B, H, T, K, V, C, c, d["q"].dtype), dtype=torch.uint8, device="cuda")
+    o, ST = g.chunk_fwd(d["q"], d["k"], d["v"], d["log_alpha"], C, c, S0=d["S0"], output_final_state=True,
+                        workspace=ws, log_beta=d["log_beta"], fp32_diagonal=True)
+    gr = g.chunk_bwd(d["q"], d["k"], d["v"], d["log_alpha"], d["dO"], C, c, S0=d["S0"], dST=d["dST"],
+                     want_dS0=True, workspace=ws, reuse_fwd_workspace=True, log_beta=d["log_beta"], o=o,
+                     fp32_diagonal=True)
+    torch.cuda.synchronize()
+    idx = list(range(B * H))
+    args = [heads(inp[n], idx) for n in ("q", "k", "v", "log_alpha", "log_beta")]
+    ro, rST = oracle.general_gate_fwd(*args, heads(inp["S0"], idx))
+    rg = oracle.general_gate_bwd(*args, heads(inp["dO"], idx), heads(inp["S0"], idx), heads(inp["dST"], idx))
+    errs = {"o": rel(heads(o, idx), ro), "S_T": rel(heads(ST, idx), rST)}
+    for n in ("dq", "dk", "dv", "dlog_alpha", "dlog_beta", "dS0"):
+        errs[n] = rel(heads(gr[n], idx), rg[n])
+    say("fp32 diagonal, general form", io, {k2: f"{v2:.2e}" for k2, v2 in errs.items()})
+    bad = {k2: v2 for k2, v2 in errs.items() if not v2 <= TOL[io]}
+    assert not bad, bad
