@@ -42,7 +42,6 @@ gla_status make_shape(const gla_problem *p, Shape &s) {
   if (!(p->gate_tau == 0.f || (p->gate_tau > 0.f && p->gate_tau < 3.0e38f))) return GLA_ERR_SHAPE;
   s.inv_tau = p->gate_tau == 0.f ? 0.f : 1.f / p->gate_tau;
   s.sgate = (p->flags & GLA_FLAG_SCALAR_GATE) != 0;
-  s.fp32_diag = (p->flags & GLA_FLAG_FP32_DIAGONAL) != 0;
   if (s.N > 65535) return GLA_ERR_UNSUPPORTED;
   // one head's rows of any tensor must span less than 2 GiB (32-bit buffer offsets)
   const int64_t wmax = p->dk > p->dv ? p->dk : p->dv;
@@ -124,7 +123,6 @@ size_t layout(const Shape &s, int op, char *base, Work *w, int nseg) {
   void *Kt = take(rows * s.K * es);
   void *P = take(chunks * s.C * s.C * es);
   void *gam = take(chunks * s.K * sizeof(float));
-  void *wflag = take(chunks * 4);
   const size_t states = (size_t)s.BH * s.K * s.V * sizeof(float);  // s.BH counts the segments
   void *Sin = nullptr, *Sloc = nullptr, *dec = nullptr, *dSout = nullptr;
   if (nseg > 1) {
@@ -149,7 +147,7 @@ size_t layout(const Shape &s, int op, char *base, Work *w, int nseg) {
     cpart = take(chunks * ((s.K + 31) / 32) * s.V * sizeof(float));
   }
   if (w) {
-    w->Qt = Qt; w->Kt = Kt; w->P = P; w->gam = (float *)gam; w->wflag = (unsigned char *)wflag;
+    w->Qt = Qt; w->Kt = Kt; w->P = P; w->gam = (float *)gam;
     w->dP = (float *)dP; w->cST = (float *)cST; w->dq_lo = dq_lo; w->dla_part = (float *)dla_part;
     w->Vh = Vh; w->Oh = Oh; w->gb = (float *)gb; w->Sb = Sb; w->cpart = (float *)cpart;
     w->Sin = (float *)Sin; w->Sloc = (float *)Sloc; w->dec = (float *)dec; w->dSout = (float *)dSout;

@@ -62,6 +62,11 @@ template <> __device__ __forceinline__ bf16 cvt<bf16>(float x) { return (bf16)x;
 
 __device__ __forceinline__ f4 zero4() { return f4{0.f, 0.f, 0.f, 0.f}; }
 
+constexpr float kLog2e = 1.4426950408889634f;
+// 2^x by the hardware exponential (v_exp_f32): exponents held in units of
+// log2 save the multiply by log2(e) that an exp() would add.
+__device__ __forceinline__ float exp2f_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
 // log alpha from the gate argument g: g itself when inv_tau == 0, else the
 // GLA gate epilogue alpha = sigmoid(g)^(1/tau) of Sec. 4.4, i.e. log alpha =
 // logsigmoid(g) / tau with logsigmoid(g) = min(g, 0) - log1p(e), e =

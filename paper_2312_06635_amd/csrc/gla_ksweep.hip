@@ -1160,7 +1160,7 @@ KsArgs ks_args(const Shape &s) {
   a.BH = s.BH; a.T = s.T; a.K = s.K; a.V = s.V; a.C = s.C; a.N = s.N;
   a.inv_tau = s.inv_tau;
   a.sg = s.sgate ? 1 : 0;
-  a.wide_thr = s.fp32_diag ? -3.0e38f : kWide;
+  a.wide_thr = -3.0e38f;
   a.KT = (s.K + kKF - 1) / kKF;
   return a;
 }

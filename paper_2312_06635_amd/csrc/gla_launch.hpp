@@ -14,7 +14,6 @@ struct Shape {
   int io;
   float inv_tau;  // 0: the gate argument is log alpha; else 1 / tau of the gate epilogue
   bool sgate;     // scalar gate: one gate value per (head, step), [BH][T]
-  bool fp32_diag; // every diagonal sub-chunk block in fp32 log space (pairwise decays)
   int esz() const { return io == IO_BF16 ? 2 : 4; }
   int la_row() const { return sgate ? 1 : K; }  // gate elements per step
 };
@@ -25,7 +24,6 @@ struct Work {
   void *Kt = nullptr;     // [BH][T][K] io : k (.) Gamma    (Gamma  = b_{chunk end} / b_t)
   void *P = nullptr;      // [BH][N][C][C] io : intra-chunk matrix, lower triangle
   float *gam = nullptr;   // [BH][N][K] fp32 : chunk decay gamma = b_{chunk end} / b_{chunk start}
-  unsigned char *wflag = nullptr;  // [BH][N][4] : diagonal block of P needs pairwise decays
   float *dP = nullptr;    // [BH][N][C][C] fp32 : (dO V^T) (.) M per chunk, stored transposed (backward)
   float *cST = nullptr;   // [BH][K] fp32 : rowsum(S_T (.) dS_T) (backward)
   void *dq_lo = nullptr;  // [BH][T][K] bf16 : dq - bf16(dq), so dq reaches the gate gradient

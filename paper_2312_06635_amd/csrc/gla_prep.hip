@@ -2,41 +2,38 @@
 // matrix P of the chunkwise GLA form (paper Sec. 4.2 and 4.3).
 //
 // One workgroup per (chunk, head); wave w owns the 16-row block w of the
-// chunk and each lane owns the features k = lane + 64 f.  With B the
+// chunk and each lane owns the features k = FPL lane .. +FPL-1.  With B the
 // chunk-local inclusive cumsum of log alpha (so exp(B) = b_t / b_{chunk start}):
 //   Qt    = q (.) exp(B)              (Q (.) Lambda)
 //   Kt    = k (.) exp(B_last - B)      (K (.) Gamma)
 //   gamma = exp(B_last)                (chunk decay)
 //   P[i][j] = sum_k q_ik k_jk exp(B_ik - B_jk) for j <= i, else 0  (Eq. 4)
 // P is tiled in 16x16 blocks (I, J):
-//   * I > J ("orange", between sub-chunks): a matrix-core product of operands
-//     normalised at block boundaries, so that every exponent is <= 0:
+//   * I > J ("orange", between sub-chunks): a bf16 (fp32 for fp32 io)
+//     matrix-core product of operands normalised at block boundaries, so that
+//     every exponent is <= 0:
 //       (q_I (.) exp(B - z_I)) diag(exp(z_I - zend_J)) (k_J (.) exp(zend_J - B))^T
 //     with z_I the log decay at the start of block I and zend_J at the end of J.
-//   * I = J ("pink", inside a sub-chunk): the pairwise decay exp(B_i - B_j) is
-//     split at the block start as exp(B_i - z) exp(z - B_j), which makes the
-//     block a matrix-core product of (q (.) exp(B - z)) and (k (.) exp(z - B));
-//     the second factor grows with the block's own decay, so when that
-//     exceeds exp(kWideRange) for any feature the block is left to
-//     prep_wide_kernel, which forms one exponential per (i, j, k) triple in
-//     fp32 on the vector ALUs.  A per-block flag in the workspace marks those
-//     blocks.
-// Sub-chunks shorter than 16 (c < 16) lie inside the diagonal blocks.
+//   * I = J ("pink", inside a sub-chunk): Eq. 4 itself in fp32 on the vector
+//     ALUs, one exponential of the log-space difference B_ik - B_jk per pair
+//     and feature (Sec. 4.3: full precision, no division by a cumulative
+//     decay), the partial sums of a lane's features then reduced across the
+//     wave.  Any gate, however steep, is exact here: every exponent is <= 0.
+// Sub-chunks shorter than 16 (c < 16) lie inside the diagonal blocks, whose
+// fp32 evaluation is the same for any such c.
+#include <type_traits>
+
 #include "gla_common.hpp"
 #include "gla_launch.hpp"
 
 namespace gla {
 
-constexpr float kWideRange = 60.0f;
-
 struct PrepArgs {
   const void *q, *k, *la;
   void *Qt, *Kt, *P;
   float *gam;
-  unsigned char *wflag;  // [BH][N][4]: diagonal block needs pairwise decays
   int T, K, Kp, C, N, ldk;
   int sg;         // scalar gate: la is [BH][T], one value per step shared by every feature
-  int fp32_diag;  // every diagonal block by pairwise decays (prep_wide_kernel)
   float inv_tau;  // gate epilogue (0: la holds log alpha)
 };
 
@@ -48,9 +45,10 @@ __host__ __device__ constexpr int tri_row(int e) {
 }
 __host__ __device__ constexpr int tri_col(int e) { return e - tri_row(e) * (tri_row(e) + 1) / 2; }
 
-// Reduce-scatter across the 64 lanes of a wave: on return, lane l holds the
-// sum over all lanes of x[l].
-template <int H> __device__ __forceinline__ void rs_step(float (&x)[64], int l) {
+// Reduce-scatter of N (<= 32) partial sums per lane across the 64 lanes of a
+// wave: the two half-waves are added first, then on return lane l (and lane
+// l + 32) holds the wave's sum of x[l % N].
+template <int H, int N> __device__ __forceinline__ void rs_step(float (&x)[N], int l) {
   const bool up = (l & H) != 0;
 #pragma unroll
   for (int e = 0; e < H; ++e) {
@@ -59,9 +57,10 @@ template <int H> __device__ __forceinline__ void rs_step(float (&x)[64], int l) 
     x[e] = keep + __shfl_xor(send, H);
   }
 }
-__device__ __forceinline__ float reduce_scatter64(float (&x)[64]) {
+__device__ __forceinline__ float reduce_scatter32(float (&x)[32]) {
   const int l = lane_id();
-  rs_step<32>(x, l);
+#pragma unroll
+  for (int e = 0; e < 32; ++e) x[e] += __shfl_xor(x[e], 32);
   rs_step<16>(x, l);
   rs_step<8>(x, l);
   rs_step<4>(x, l);
@@ -140,7 +139,7 @@ __device__ __forceinline__ void straw(__amdgpu_buffer_rsrc_t rs, uint32_t off, c
 
 // PRE: the gate argument is the pre-activation of the gate epilogue.
 template <typename T, int FPL, bool PRE>
-__global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) prep_kernel(PrepArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int n = blockIdx.x, bh = blockIdx.y;
   const int w = wave_id(), l = lane_id(), g = l >> 4, j16 = l & 15;
@@ -152,7 +151,6 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
   T *sKs = sQh + C * ldk;
   float *sTot = (float *)(sKs + C * ldk);  // [nb][Kp] per-block sums of log alpha
   float *sG = sTot + 4 * Kp;              // [3][Kp] exp(sum of tot strictly between I and J)
-  float *sEup = sG + 3 * Kp;              // [nb][Kp] exp(-tot): pink operand scale
 
   const T *q = (const T *)a.q + base, *k = (const T *)a.k + base;
   const T *la = (const T *)a.la + (a.sg ? (int64_t)bh * a.T + t0 : base);
@@ -248,20 +246,16 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
     }
   }
 
-  // 2. gated operands, from the block-local inclusive cumsum Bloc.
-  bool wide = false;
+  // 2. gated operands, from the block-local inclusive cumsum Bloc (kept, in
+  // units of log2, for the diagonal block of step 4).
   float ez[FPL], ekt[FPL];
 #pragma unroll
   for (int f = 0; f < FPL; ++f) {
     ez[f] = __expf(pre[f]);                    // b_{block start} / b_{chunk start}
     ekt[f] = __expf(Bl[f] - pre[f] - tot[f]);  // b_{chunk end} / b_{block end}
-    if (fv && (a.fp32_diag || -tot[f] > kWideRange)) wide = true;
-    if (fp) sEup[w * Kp + k0 + f] = __expf(-tot[f]);  // b_{block start} / b_{block end} >= 1
   }
-  const bool wide_blk = __any(wide);
-  if (l == 0) a.wflag[((int64_t)bh * a.N + n) * 4 + w] = wide_blk ? 1 : 0;
   const auto rs_Qt = make_rsrc(Qt, bytes), rs_Kt = make_rsrc(Kt, bytes);
-  float c[FPL];
+  float c[FPL], B2[16][FPL];
 #pragma unroll
   for (int f = 0; f < FPL; ++f) c[f] = 0.f;
 #pragma unroll
@@ -275,6 +269,7 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
     for (int f = 0; f < FPL; ++f) {
       if constexpr (PRE) c[f] += lav[r][f];
       else c[f] += xl[f];
+      B2[r][f] = c[f] * kLog2e;
       const float qhv = qv[f] * __expf(c[f]);           // <= |q|
       const float ksv = kv[f] * __expf(tot[f] - c[f]);  // <= |k|
       o1[f] = qhv * ez[f];
@@ -314,10 +309,8 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
   }
   __syncthreads();
 
-  // 3. blocks (w, J <= w) on the matrix cores: orange below the diagonal,
-  //    pink on it (unless the block needs pairwise decays).
-  for (int J = 0; J <= w; ++J) {
-    if (J == w && wide_blk) break;
+  // 3. blocks (w, J < w) below the diagonal on the matrix cores.
+  for (int J = 0; J < w; ++J) {
     f4 acc = zero4();
     for (int s = 0; s < Kp / 32; ++s) {
       frag_t<T> af = ld_row(sQh, ldk, d0, 32 * s);
@@ -326,103 +319,70 @@ __global__ void __launch_bounds__(256) prep_kernel(PrepArgs a) {
         const float *gp = sG + pair_index(w, J) * Kp + 32 * s + 8 * g;
 #pragma unroll
         for (int i = 0; i < 8; ++i) af[i] = cvt<T>((float)af[i] * gp[i]);
-      } else if (J == w) {
-        const float *ep = sEup + w * Kp + 32 * s + 8 * g;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) bf[i] = cvt<T>((float)bf[i] * ep[i]);
       }
       acc = mma<T>(acc, af, bf);
     }
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = 4 * g + r;
-      if (J < w || j16 <= row) Pg[(d0 + row) * C + 16 * J + j16] = cvt<T>(acc[r]);
-    }
+    for (int r = 0; r < 4; ++r) Pg[(d0 + 4 * g + r) * C + 16 * J + j16] = cvt<T>(acc[r]);
   }
-}
 
-// Diagonal blocks whose decay range is too large for the factorised form:
-// P[i][j] = sum_k q_ik k_jk exp(B_ik - B_jk), one exponential per term, fp32,
-// reduced across the lanes that own the features.
-template <typename T, int FPL, bool PRE>
-__global__ void __launch_bounds__(256) prep_wide_kernel(PrepArgs a) {
-  const int n = blockIdx.x, bh = blockIdx.y;
-  const int w = wave_id(), l = lane_id();
-  // (without a gate only the fp32 option flags blocks)
-  if (!a.wflag[((int64_t)bh * a.N + n) * 4 + w]) return;
-  const int C = a.C, K = a.K;
-  const int t0 = n * C, rv = min(C, a.T - t0), d0 = 16 * w;
-  const int64_t base = ((int64_t)bh * a.T + t0) * K;
-  const T *q = (const T *)a.q + base, *k = (const T *)a.k + base;
-  const T *la = a.la ? (const T *)a.la + base : nullptr;
-  const T *las = a.la ? (const T *)a.la + (int64_t)bh * a.T + t0 : nullptr;  // scalar gate rows
-  T *Pg = (T *)a.P + ((int64_t)bh * a.N + n) * C * C;
-  const int k0 = FPL * l;
-  const bool fv = k0 < K;
-  float qv[16][FPL], kv[16][FPL], Bv[16][FPL], c[FPL];
+  // 4. the diagonal block in fp32 log space (Eq. 4): pair p = (i, j), j <= i,
+  // of the block's 136 is sum_k q_ik k_jk 2^(B2_ik - B2_jk); each lane sums
+  // its own features for 32 pairs at a time, then the wave reduces (pairs
+  // 0..127 by reduce-scatter, lane l ending with pair p0 + l % 32; pairs
+  // 128..135 by all-reduce).  The q, k values are the io-dtype inputs
+  // themselves.
+  auto pink = [&](auto p0, auto np, float (&x)[32]) {
+    constexpr int P0 = decltype(p0)::value, NP = decltype(np)::value;
 #pragma unroll
-  for (int f = 0; f < FPL; ++f) c[f] = 0.f;
-#pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int row = d0 + r;
-    const bool ok = fv && row < rv;
-    float xl[FPL];
-    if (!la) {  // no gate: log alpha = 0
-#pragma unroll
-      for (int f = 0; f < FPL; ++f) xl[f] = 0.f;
-    } else if (a.sg) {
-      const float e = ok ? (float)las[row] : 0.f;
-#pragma unroll
-      for (int f = 0; f < FPL; ++f) xl[f] = e;
-    } else {
-      ldvec<T, FPL>(la + row * K + k0, ok, xl);
-    }
-    ldvec<T, FPL>(q + row * K + k0, ok, qv[r]);
-    ldvec<T, FPL>(k + row * K + k0, ok, kv[r]);
+    for (int e = 0; e < NP; ++e) x[e] = 0.f;
 #pragma unroll
     for (int f = 0; f < FPL; ++f) {
-      c[f] += PRE ? gate_la(xl[f], a.inv_tau, ok) : xl[f];
-      Bv[r][f] = c[f];
+      float qf[16], kf[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float t[FPL];
+        unpack<T, FPL>(rq[r], t);
+        qf[r] = t[f];
+        unpack<T, FPL>(rk[r], t);
+        kf[r] = t[f];
+      }
+#pragma unroll
+      for (int e = 0; e < NP; ++e) {
+        const int i = tri_row(P0 + e), jj = tri_col(P0 + e);
+        x[e] += qf[i] * kf[jj] * exp2f_fast(B2[i][f] - B2[jj][f]);
+      }
     }
+  };
+  auto pink32 = [&](auto p0) {
+    constexpr int P0 = decltype(p0)::value;
+    float x[32];
+    pink(p0, std::integral_constant<int, 32>{}, x);
+    const float r = reduce_scatter32(x);
+    if (l < 32) Pg[(d0 + tri_row(P0 + l)) * C + d0 + tri_col(P0 + l)] = cvt<T>(r);
+  };
+  pink32(std::integral_constant<int, 0>{});
+  pink32(std::integral_constant<int, 32>{});
+  pink32(std::integral_constant<int, 64>{});
+  pink32(std::integral_constant<int, 96>{});
+  {
+    float x[32];
+    pink(std::integral_constant<int, 128>{}, std::integral_constant<int, 8>{}, x);
+    float rt = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float s = allreduce64(x[e]);
+      if (l == e) rt = s;
+    }
+    if (l < 8) Pg[(d0 + 15) * C + d0 + 8 + l] = cvt<T>(rt);
   }
-  float x[64], r0, r1, rt = 0.f;
-#pragma unroll
-  for (int e = 0; e < 64; ++e) {
-    float s = 0.f;
-    const int i = tri_row(e), jj = tri_col(e);
-#pragma unroll
-    for (int f = 0; f < FPL; ++f) s += qv[i][f] * kv[jj][f] * __expf(Bv[i][f] - Bv[jj][f]);
-    x[e] = s;
-  }
-  r0 = reduce_scatter64(x);
-#pragma unroll
-  for (int e = 0; e < 64; ++e) {
-    float s = 0.f;
-    const int i = tri_row(64 + e), jj = tri_col(64 + e);
-#pragma unroll
-    for (int f = 0; f < FPL; ++f) s += qv[i][f] * kv[jj][f] * __expf(Bv[i][f] - Bv[jj][f]);
-    x[e] = s;
-  }
-  r1 = reduce_scatter64(x);
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    float s = 0.f;
-    const int i = tri_row(128 + e), jj = tri_col(128 + e);
-#pragma unroll
-    for (int f = 0; f < FPL; ++f) s += qv[i][f] * kv[jj][f] * __expf(Bv[i][f] - Bv[jj][f]);
-    s = allreduce64(s);
-    if (l == e) rt = s;
-  }
-  Pg[(d0 + tri_row(l)) * C + d0 + tri_col(l)] = cvt<T>(r0);
-  Pg[(d0 + tri_row(64 + l)) * C + d0 + tri_col(64 + l)] = cvt<T>(r1);
-  if (l < 8) Pg[(d0 + tri_row(128 + l)) * C + d0 + tri_col(128 + l)] = cvt<T>(rt);
 }
 
 static int round_up(int x, int m) { return (x + m - 1) / m * m; }
 
 size_t lds_prep(const Shape &s) {
   const int Kp = round_up(s.K, 32), ldk = Kp + 32 / s.esz();
-  return (size_t)2 * s.C * ldk * s.esz() + (size_t)11 * Kp * sizeof(float);
+  return (size_t)2 * s.C * ldk * s.esz() + (size_t)7 * Kp * sizeof(float);
 }
 
 template <typename T, int FPL, bool PRE>
@@ -434,9 +394,6 @@ static hipError_t launch_prep_pre(const Shape &s, const PrepArgs &a, size_t lds,
   (void)attr;
   dim3 grid(s.N, s.BH), block(64 * (s.C / 16));
   hipLaunchKernelGGL((prep_kernel<T, FPL, PRE>), grid, block, lds, st, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((prep_wide_kernel<T, FPL, PRE>), grid, block, 0, st, a);
   return hipGetLastError();
 }
 
@@ -450,11 +407,10 @@ hipError_t launch_prep(const Shape &s, const void *q, const void *k, const void 
                        const Work &w, hipStream_t st) {
   PrepArgs a;
   a.q = q; a.k = k; a.la = la;
-  a.Qt = w.Qt; a.Kt = w.Kt; a.P = w.P; a.gam = w.gam; a.wflag = w.wflag;
+  a.Qt = w.Qt; a.Kt = w.Kt; a.P = w.P; a.gam = w.gam;
   a.T = s.T; a.K = s.K; a.Kp = round_up(s.K, 32); a.C = s.C; a.N = s.N;
   a.inv_tau = s.inv_tau;
   a.sg = s.sgate ? 1 : 0;
-  a.fp32_diag = s.fp32_diag ? 1 : 0;
   a.ldk = a.Kp + 32 / s.esz();
   const size_t lds = lds_prep(s);
   const int fpl = (s.K + 63) / 64;
