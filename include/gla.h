@@ -78,7 +78,9 @@ typedef enum {
   GLA_ERR_DTYPE = 3,       /* unknown io dtype                                 */
   GLA_ERR_UNSUPPORTED = 4, /* valid, but outside what the kernels implement    */
   GLA_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than required          */
-  GLA_ERR_HIP = 6          /* a HIP runtime call or kernel launch failed       */
+  GLA_ERR_HIP = 6,         /* a HIP runtime call or kernel launch failed       */
+  GLA_ERR_SCRATCH = 7      /* gla_chunk_fwd_noalloc: the problem needs more
+                            * workspace than the library's fixed scratch array */
 } gla_status;
 
 typedef enum { GLA_F32 = 0, GLA_BF16 = 1 } gla_dtype;
@@ -179,6 +181,25 @@ size_t gla_workspace_bytes(const gla_problem *prob, int op);
 gla_status gla_chunk_fwd(const gla_problem *prob, const void *q, const void *k, const void *v,
                          const void *log_alpha, const float *S0, void *o, float *S_T,
                          void *workspace, size_t workspace_bytes, void *stream);
+
+/* gla_chunk_fwd without any allocation, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, results (bit for bit) and kernels
+ * as gla_chunk_fwd, minus the workspace: the library uses a fixed device
+ * array of GLA_NOALLOC_SCRATCH_BYTES bytes in its code object instead, which
+ * every GPU the library runs on holds from the library's load until the
+ * process ends.  The caller still provides every input and output buffer.
+ * Problems whose forward workspace (gla_workspace_bytes(prob, 0)) exceeds
+ * that size return GLA_ERR_SCRATCH before anything is enqueued.  The call
+ * allocates, frees and clears nothing; its first call on a device looks up
+ * that device's address of the array (hipGetSymbolAddress).  Every call on
+ * one GPU uses that GPU's one array, so calls whose work overlaps on a GPU
+ * (other streams, other host threads) race and give undefined results;
+ * calls ordered on one stream are safe.  The array keeps the last call's
+ * contents, which no call reads before writing. */
+#define GLA_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+gla_status gla_chunk_fwd_noalloc(const gla_problem *prob, const void *q, const void *k, const void *v,
+                                 const void *log_alpha, const float *S0, void *o, float *S_T, void *stream);
 
 /* Backward of gla_chunk_fwd for the loss L = sum(o * dO) + sum(S_T * dS_T)
  * (App. B, Alg. 4/6 with the closed-form gate gradient of Sec. 4.3):

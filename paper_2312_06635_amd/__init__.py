@@ -30,14 +30,15 @@ __all__ = [
     "GLA_OK", "GLA_ERR_NULL", "GLA_ERR_SHAPE", "GLA_ERR_DTYPE", "GLA_ERR_UNSUPPORTED",
     "GLA_ERR_WORKSPACE", "GLA_ERR_HIP", "FLAG_REUSE_FWD_WORKSPACE", "FLAG_SCALAR_GATE", "GlaProblem", "lib",
     "output_gate_fwd", "output_gate_bwd", "output_gate_workspace_bytes", "general_workspace_bytes",
-    "SEGMENTS_SHIFT", "FLAG_FP32_DIAGONAL",
+    "SEGMENTS_SHIFT", "FLAG_FP32_DIAGONAL", "chunk_fwd_noalloc", "GLA_ERR_SCRATCH", "NOALLOC_SCRATCH_BYTES",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 library_path = os.path.join(_HERE, "libgla.so")
 
 GLA_OK, GLA_ERR_NULL, GLA_ERR_SHAPE, GLA_ERR_DTYPE = 0, 1, 2, 3
-GLA_ERR_UNSUPPORTED, GLA_ERR_WORKSPACE, GLA_ERR_HIP = 4, 5, 6
+GLA_ERR_UNSUPPORTED, GLA_ERR_WORKSPACE, GLA_ERR_HIP, GLA_ERR_SCRATCH = 4, 5, 6, 7
+NOALLOC_SCRATCH_BYTES = 128 << 20  # GLA_NOALLOC_SCRATCH_BYTES of include/gla.h
 GLA_F32, GLA_BF16 = 0, 1
 FLAG_REUSE_FWD_WORKSPACE = 1
 FLAG_SCALAR_GATE = 2
@@ -77,6 +78,8 @@ def lib():
         L.gla_workspace_bytes.restype = sz
         L.gla_chunk_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.gla_chunk_fwd.restype = i32
+        L.gla_chunk_fwd_noalloc.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.gla_chunk_fwd_noalloc.restype = i32
         L.gla_chunk_bwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.gla_chunk_bwd.restype = i32
         L.gla_recurrent_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp]
@@ -232,6 +235,27 @@ def chunk_fwd(q, k, v, log_alpha, chunk=64, subchunk=16, S0=None, output_final_s
                                  _stream(q.device))
     if st != GLA_OK:
         raise GlaError(st, "gla_chunk_fwd_general" if log_beta is not None else "gla_chunk_fwd")
+    return o, ST
+
+
+def chunk_fwd_noalloc(q, k, v, log_alpha, chunk=64, subchunk=16, S0=None, out=None, gate_tau=0.0):
+    """gla_chunk_fwd_noalloc: the chunkwise forward with the library's fixed
+    scratch array as its workspace (nothing is allocated by the library).
+    out=(o, S_T or None) must be given (caller-owned outputs); returns it.
+    Problems whose forward workspace exceeds NOALLOC_SCRATCH_BYTES raise
+    GlaError with status GLA_ERR_SCRATCH."""
+    _check(q, k, v, log_alpha, states=(("S0", S0),))
+    if out is None:
+        raise ValueError("chunk_fwd_noalloc needs out=(o, S_T or None)")
+    o, ST = out
+    _check(q, k, o, None, states=(("S_T", ST),))
+    if o.shape != v.shape:
+        raise ValueError("o must be shaped like v")
+    p = _problem(q, v, chunk, subchunk, 0, gate_tau, log_alpha)
+    st = lib().gla_chunk_fwd_noalloc(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(S0),
+                                     _ptr(o), _ptr(ST), _stream(q.device))
+    if st != GLA_OK:
+        raise GlaError(st, "gla_chunk_fwd_noalloc")
     return o, ST
 
 

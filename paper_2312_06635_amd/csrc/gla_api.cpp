@@ -168,6 +168,7 @@ GLA_EXPORT const char *gla_status_string(gla_status st) {
     case GLA_ERR_UNSUPPORTED: return "GLA_ERR_UNSUPPORTED: shape outside what the kernels implement";
     case GLA_ERR_WORKSPACE: return "GLA_ERR_WORKSPACE: workspace NULL or too small";
     case GLA_ERR_HIP: return "GLA_ERR_HIP: a HIP call or kernel launch failed";
+    case GLA_ERR_SCRATCH: return "GLA_ERR_SCRATCH: the problem's workspace exceeds the fixed scratch array";
   }
   return "GLA_ERR_UNKNOWN";
 }

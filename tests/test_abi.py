@@ -29,6 +29,7 @@ def declared_functions():
 
 def test_header_declares_the_boundary():
     assert declared_functions() == ["gla_chunk_bwd", "gla_chunk_bwd_general", "gla_chunk_fwd", "gla_chunk_fwd_general",
+                                    "gla_chunk_fwd_noalloc",
                                     "gla_output_gate_bwd", "gla_output_gate_fwd",
                                     "gla_output_gate_workspace_bytes", "gla_recurrent_fwd",
                                     "gla_recurrent_fwd_general", "gla_status_string", "gla_workspace_bytes"]
@@ -69,7 +70,7 @@ def test_only_the_boundary_is_exported(L):
 
 
 def test_status_strings(L):
-    for code in range(7):
+    for code in range(8):
         s = L.gla_status_string(code).decode()
         assert s.startswith("GLA_OK" if code == 0 else "GLA_ERR")
     assert L.gla_status_string(99).decode() == "GLA_ERR_UNKNOWN"
@@ -288,3 +289,18 @@ def test_output_gate_checks_pointers_and_workspace(L):
     assert og_bwd_call(L, p, ws=None) == gla.GLA_ERR_WORKSPACE
     assert og_bwd_call(L, p, ws_bytes=need - 1) == gla.GLA_ERR_WORKSPACE
     assert og_fwd_call(L, P(B=0), ptr=None) == gla.GLA_OK
+
+
+def test_noalloc_refuses_oversized_problems_before_any_launch(L):
+    """gla_chunk_fwd_noalloc: a problem whose forward workspace exceeds the
+    fixed scratch array gets GLA_ERR_SCRATCH without a HIP call (the dummy
+    pointers are never touched); invalid problems get the forward's own
+    validation errors."""
+    p = P(B=64, H=4, T=4096, dk=256, dv=512)
+    assert L.gla_workspace_bytes(ctypes.byref(p), 0) > gla.NOALLOC_SCRATCH_BYTES
+    st = L.gla_chunk_fwd_noalloc(ctypes.byref(p), 16, 16, 16, None, None, 16, None, None)
+    assert st == gla.GLA_ERR_SCRATCH
+    assert L.gla_chunk_fwd_noalloc(None, 16, 16, 16, None, None, 16, None, None) == gla.GLA_ERR_NULL
+    bad = P(dk=24)
+    assert L.gla_chunk_fwd_noalloc(ctypes.byref(bad), 16, 16, 16, None, None, 16, None, None) == \
+        gla.GLA_ERR_UNSUPPORTED
