@@ -36,54 +36,102 @@ PEAK_F32_FLOPS = 157.3e12
 PEAK_HBM = 8.0e12
 RIDGE = PEAK_BF16_FLOPS / PEAK_HBM
 
-STAGES = [("prep", "fwd", 1), ("fwd_main", "fwd", 2), ("bwd_dq", "bwd", 2), ("bwd_dk", "bwd", 3),
-          ("bwd_dv", "bwd", 4)]
+STAGES = [("prep", "fwd", 1), ("fwd_main", "fwd", 2), ("bwd_intra", "bwd", 2), ("bwd_dq", "bwd", 3),
+          ("bwd_dk", "bwd", 4), ("bwd_dv", "bwd", 5)]
 # with the output side (Sec. 4.4): LN + Swish gate after the forward, its
 # reverse mode (producing the layer's dO) before the backward sweeps
 STAGES_OG = STAGES[:2] + [("og_fwd", "og", 0), ("og_bwd", "og", 1)] + STAGES[2:]
 # the general form (App. C, value-side gate beta): its backward's stages
-STAGES_GB = STAGES[:2] + [("beta_prep", "bwdg", 2), ("bwd_dq", "bwdg", 3), ("bwd_dk", "bwdg", 4),
-                          ("bwd_dv", "bwdg", 5), ("beta_grad", "bwdg", 6)]
+STAGES_GB = STAGES[:2] + [("beta_prep", "bwdg", 2), ("bwd_intra", "bwdg", 3), ("bwd_dq", "bwdg", 4),
+                          ("bwd_dk", "bwdg", 5), ("bwd_dv", "bwdg", 6), ("beta_grad", "bwdg", 7)]
 
 
 def algorithmic(cfg, gate=True, scalar_gate=False, value_gate=False):
-    """Algorithmic FLOPs and HBM bytes per launch of each stage (and totals);
-    gate=False is the alpha = 1 layer, which reads no gate tensor and writes no
-    gate gradient; scalar_gate has one gate value per step and head."""
+    """Algorithmic FLOPs and HBM bytes per launch of each stage (and totals).
+
+    "bytes" counts only the layer's own I/O that the kernel reads or writes
+    (q, k, log alpha, v, dO in; o, dq, dk, dv, dlog alpha out; s bytes per
+    element), the per-kernel share of the s (9 d_k + 5 d_v) per token-head of
+    the whole layer; "bytes_all" adds the intermediates the kernel moves
+    through the workspace (gated operands, P, the backward's hand-offs), which
+    the measured traffic is compared against.  FLOPs split the chunk form's
+    algorithmic count over the kernels (fwd 4 d_k d_v + (C+1)(d_k + d_v), bwd
+    8 d_k d_v + (C+1)(3 d_k + 2 d_v) per token-head).  gate=False is the
+    alpha = 1 layer (no gate read, no gate gradient); scalar_gate has one gate
+    value per step and head."""
     B, H, T, K, V, C = cfg["B"], cfg["H"], cfg["T"], cfg["dk"], cfg["dv"], cfg["chunk"]
     ga = (1.0 / K if scalar_gate else 1.0) if gate else 0.0  # gate elements per step, in units of K
     s = 2 if cfg["io"] == "bf16" else 4
     n = B * H * T                       # token-heads
-    g = B * H * ((T + C - 1) // C) * K * 4  # chunk decays (fp32)
+    N = (T + C - 1) // C
+    g = B * H * N * K * 4               # chunk decays (fp32)
     P = n * C * s                       # intra-chunk matrices
-    dP = n * C * 4
+    qk = n * s * K                      # one [B, H, T, d_k] io tensor
+    vv = n * s * V                      # one [B, H, T, d_v] io tensor
+    la = qk * ga                        # the gate tensor (or its gradient)
     st = {
-        # gate factors, Q (.) Lambda, K (.) Gamma, P: reads q, k, log_alpha
-        "prep": dict(flops=n * (C + 1) * K, bytes=n * s * (2 + ga) * K + n * s * 2 * K + P + g),
-        # state pass + output: reads Qt, Kt, v, P, gamma; writes o
-        "fwd_main": dict(flops=n * (4 * K * V + (C + 1) * V), bytes=n * s * (2 * K + (3 if value_gate else 2) * V) + P + g),
-        # dq sweep: reads k, log_alpha, v, dO; writes dq and dP
-        "bwd_dq": dict(flops=n * (2 * K * V + (C + 1) * (K + V)), bytes=n * s * ((2 + ga) * K + 2 * V) + dP),
-        # dk sweep: reads q, k, log_alpha, v, dO, dq, dP; writes dk, dlog_alpha
-        "bwd_dk": dict(flops=n * (4 * K * V + (C + 1) * K),
-                       bytes=n * s * ((4 + 2 * ga) * K + 2 * V) + dP),
-        # dv sweep: reads Qt, Kt, P, gamma, dO; writes dv
-        "bwd_dv": dict(flops=n * (2 * K * V + (C + 1) * V), bytes=n * s * (2 * K + 2 * V) + P + g),
+        # gate factors, Q (.) Lambda, K (.) Gamma, P: reads q, k, log alpha
+        "prep": dict(flops=n * (C + 1) * K, bytes=2 * qk + la, inter=2 * qk + P + g),
+        # state pass + output: reads v (and log beta); writes o
+        "fwd_main": dict(flops=n * (4 * K * V + (C + 1) * V), bytes=(3 if value_gate else 2) * vv,
+                         inter=2 * qk + P + g),
+        # intra-chunk terms: reads q, k, log alpha, v, dO
+        "bwd_intra": dict(flops=n * (C + 1) * (3 * K + V), bytes=2 * qk + la + 2 * vv,
+                          inter=3 * qk + B * H * N * K * 4),
+        # dq sweep: reads k, log alpha, v, dO; writes dq
+        "bwd_dq": dict(flops=n * 2 * K * V, bytes=qk + la + 2 * vv + qk, inter=qk + n * K * 4),
+        # dk sweep: reads q, k, log alpha, v, dO; writes dk, dlog alpha
+        "bwd_dk": dict(flops=n * 4 * K * V, bytes=2 * qk + la + 2 * vv + qk + la,
+                       inter=2 * qk + n * K * 4 + B * H * N * K * 4),
+        # dv sweep: reads dO; writes dv
+        "bwd_dv": dict(flops=n * (2 * K * V + (C + 1) * V), bytes=2 * vv, inter=2 * qk + P + g),
         # output side: reads o, g and the [H, d_v] affine; writes y
-        "og_fwd": dict(flops=n * V * 12, bytes=n * s * 3 * V + H * V * 8),
+        "og_fwd": dict(flops=n * V * 12, bytes=3 * vv + H * V * 8, inter=0),
         # its reverse: reads o, g, dy and the affine; writes dO, dg, dw, db
-        "og_bwd": dict(flops=n * V * 24, bytes=n * s * 5 * V + H * V * 16),
+        "og_bwd": dict(flops=n * V * 24, bytes=5 * vv + H * V * 16, inter=0),
         # general form: Vh, Oh from v, dO, log beta
-        "beta_prep": dict(flops=n * V * 6, bytes=n * s * 5 * V),
+        "beta_prep": dict(flops=n * V * 6, bytes=3 * vv, inter=2 * vv),
         # dlog beta: reads o, dO, v, dv; writes dlog beta
-        "beta_grad": dict(flops=n * V * 4, bytes=n * s * 5 * V),
+        "beta_grad": dict(flops=n * V * 4, bytes=5 * vv, inter=0),
     }
     if value_gate:  # the dv sweep also reads log beta
-        st["bwd_dv"]["bytes"] += n * s * V
+        st["bwd_dv"]["bytes"] += vv
+    for a in st.values():
+        a["bytes_all"] = a["bytes"] + a.pop("inter")
     fwd = n * (4 * K * V + (C + 1) * (K + V))
     bwd = n * (8 * K * V + (C + 1) * (3 * K + 2 * V))
     io_bytes = n * s * ((7 + 2 * ga) * K + 5 * V)
     return st, fwd, bwd, io_bytes
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def tiny_single_thread_ms(reps=20):
+    """The oracle's forward + backward on the tiny fp32 workload (B=1, H=1,
+    T=64, d_k=16, d_v=32) with one thread: median wall time of reps runs."""
+    import oracle
+    cfg = W.CONFIGS["tiny_fp32"]
+    inp = W.make_inputs(cfg)
+    f = lambda t: None if t is None else t.float().reshape(-1, *t.shape[2:]).double().numpy()
+    q, k, v, la, dO = (f(inp[n]) for n in ("q", "k", "v", "log_alpha", "dO"))
+    times = []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        oracle.fwd(q, k, v, la, nthreads=1)
+        oracle.bwd(q, k, v, la, dO, nthreads=1)
+        times.append(time.perf_counter() - t0)
+    times.sort()
+    return 1e3 * times[len(times) // 2]
 
 
 def cpu_baseline(cfg, inputs, target_s=15.0):
@@ -116,7 +164,9 @@ def cpu_baseline(cfg, inputs, target_s=15.0):
     del np
     return {"value": tokens / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": f"{heads} of {BH} heads (full T={cfg['T']}) x {reps} passes, fwd+bwd fp64 recurrence + "
-                      f"BPTT, {el:.1f} s wall; tokens counted as heads*T/H per pass"}
+                      f"BPTT, {el:.1f} s wall; tokens counted as heads*T/H per pass",
+            "cpu_model": cpu_model(),
+            "tiny_fp32_single_thread_ms": round(tiny_single_thread_ms(), 4)}
 
 
 COPY_BYTES = 1 << 30
@@ -334,6 +384,12 @@ def main():
                  args.segments or args.fp32_diagonal)
     roof["traffic"] = measured_traffic(args.workload, dom) if plain else None
     roof["avg_ms"] = stage_ms[dom]
+    # the kernel's own share of the layer I/O (what "achieved" divides) and the
+    # bytes it moves including workspace intermediates; measured traffic is
+    # compared with the former
+    roof["algorithmic_bytes"] = st_alg[dom]["bytes"]
+    roof["bytes_with_intermediates"] = st_alg[dom]["bytes_all"]
+    roof["traffic_ratio"] = (roof["traffic"] / st_alg[dom]["bytes"]) if roof["traffic"] else None
     stage_frac = {nm: f"{r['frac']:.3f} of {r['bound']}" for nm, r in ((nm, roofline(nm)) for nm in stage_ms)}
 
     out = {

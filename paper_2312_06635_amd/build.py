@@ -19,7 +19,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libgla.so")
-SOURCES = ["gla_prep.hip", "gla_fwd.hip", "gla_vsweep.hip", "gla_ksweep.hip", "gla_outgate.hip", "gla_beta.hip", "gla_segment.hip", "gla_noalloc.hip", "gla_api.cpp"]
+SOURCES = ["gla_prep.hip", "gla_fwd.hip", "gla_vsweep.hip", "gla_ksweep.hip", "gla_intra.hip", "gla_outgate.hip", "gla_beta.hip", "gla_segment.hip", "gla_noalloc.hip", "gla_api.cpp"]
 ARCH = "gfx950"
 
 

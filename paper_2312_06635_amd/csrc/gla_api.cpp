@@ -45,7 +45,8 @@ gla_status make_shape(const gla_problem *p, Shape &s) {
   if (s.N > 65535) return GLA_ERR_UNSUPPORTED;
   // one head's rows of any tensor must span less than 2 GiB (32-bit buffer offsets)
   const int64_t wmax = p->dk > p->dv ? p->dk : p->dv;
-  if ((int64_t)p->T * wmax * s.esz() >= (int64_t)1 << 31) return GLA_ERR_UNSUPPORTED;
+  // (fp32 workspace rows included: 4 bytes per element)
+  if ((int64_t)p->T * wmax * 4 >= (int64_t)1 << 31) return GLA_ERR_UNSUPPORTED;
   return GLA_OK;
 }
 
@@ -54,7 +55,8 @@ bool lds_bad(size_t bytes) { return bytes == 0 || bytes > gla::kMaxLds; }
 
 gla_status check_lds(const Shape &s, bool bwd) {
   if (lds_bad(gla::lds_prep(s)) || lds_bad(gla::lds_fwd_main(s))) return GLA_ERR_UNSUPPORTED;
-  if (bwd && (lds_bad(gla::lds_bwd_dq(s)) || lds_bad(gla::lds_bwd_dk(s)) || lds_bad(gla::lds_bwd_dv(s))))
+  if (bwd && (lds_bad(gla::lds_bwd_intra(s)) || lds_bad(gla::lds_bwd_dq(s)) || lds_bad(gla::lds_bwd_dk(s)) ||
+              lds_bad(gla::lds_bwd_dv(s))))
     return GLA_ERR_UNSUPPORTED;
   return GLA_OK;
 }
@@ -130,12 +132,16 @@ size_t layout(const Shape &s, int op, char *base, Work *w, int nseg) {
     Sloc = take(states);
     dec = take((size_t)s.BH * s.K * sizeof(float));
   }
-  void *dP = nullptr, *cST = nullptr, *dq_lo = nullptr, *dla_part = nullptr;
+  void *dqi = nullptr, *dki = nullptr, *dai = nullptr, *dat = nullptr, *dqr = nullptr;
+  void *cST = nullptr, *dla_part = nullptr;
   void *Vh = nullptr, *Oh = nullptr, *gb = nullptr, *Sb = nullptr, *cpart = nullptr;
   if (op >= 1) {
-    dP = take(chunks * s.C * s.C * sizeof(float));
+    dqi = take(rows * s.K * es);
+    dki = take(rows * s.K * es);
+    dai = take(rows * s.K * es);
+    dat = take(chunks * s.K * sizeof(float));
+    dqr = take(rows * s.K * sizeof(float));
     cST = take((size_t)s.BH * s.K * sizeof(float));
-    if (s.io == gla::IO_BF16) dq_lo = take(rows * s.K * 2);
     if (s.sgate) dla_part = take(rows * ((s.K + 31) / 32) * sizeof(float));
     if (nseg > 1) dSout = take(states);
   }
@@ -148,7 +154,8 @@ size_t layout(const Shape &s, int op, char *base, Work *w, int nseg) {
   }
   if (w) {
     w->Qt = Qt; w->Kt = Kt; w->P = P; w->gam = (float *)gam;
-    w->dP = (float *)dP; w->cST = (float *)cST; w->dq_lo = dq_lo; w->dla_part = (float *)dla_part;
+    w->dqi = dqi; w->dki = dki; w->dai = dai; w->dat = (float *)dat; w->dqr = (float *)dqr;
+    w->cST = (float *)cST; w->dla_part = (float *)dla_part;
     w->Vh = Vh; w->Oh = Oh; w->gb = (float *)gb; w->Sb = Sb; w->cpart = (float *)cpart;
     w->Sin = (float *)Sin; w->Sloc = (float *)Sloc; w->dec = (float *)dec; w->dSout = (float *)dSout;
   }
@@ -270,7 +277,7 @@ GLA_EXPORT gla_status gla_chunk_bwd(const gla_problem *prob, const void *q, cons
   if (!log_alpha) s.inv_tau = 0.f;  // no gate: alpha = 1 whatever gate_tau says
   if ((st = check_lds(s, true)) != GLA_OK) return st;
   const unsigned stage = (prob->flags & GLA_STAGE_MASK) >> GLA_STAGE_SHIFT;
-  if (stage > 4) return GLA_ERR_SHAPE;
+  if (stage > 5) return GLA_ERR_SHAPE;
   const bool any = (int64_t)s.BH * s.T > 0;
   if (any && (!q || !k || !v || !dO || !dq || !dk || !dv)) return GLA_ERR_NULL;
   const int nseg = resolve_nseg(s, prob->flags, false);
@@ -299,7 +306,8 @@ GLA_EXPORT gla_status gla_chunk_bwd(const gla_problem *prob, const void *q, cons
   // per segment: initial state and final-state gradient (the head's own S0
   // and dS_T when unsegmented)
   const float *S0s = nseg > 1 ? w.Sin : S0, *dSTs = nseg > 1 ? w.dSout : dS_T;
-  if (e == hipSuccess && run(2)) {
+  if (e == hipSuccess && run(2)) e = gla::launch_bwd_intra(s2, q, k, log_alpha, v, dO, w, hs);
+  if (e == hipSuccess && run(3)) {
     if (nseg > 1) {
       // local initial-state gradients from a zero final-state gradient, then
       // the reverse segment scan (which also gives the head's dS0)
@@ -309,9 +317,9 @@ GLA_EXPORT gla_status gla_chunk_bwd(const gla_problem *prob, const void *q, cons
     }
     if (e == hipSuccess) e = gla::launch_bwd_dq(s2, k, log_alpha, v, S0s, dO, dSTs, dq, w, hs);
   }
-  if (e == hipSuccess && run(3))
+  if (e == hipSuccess && run(4))
     e = gla::launch_bwd_dk(s2, q, k, log_alpha, v, dO, dSTs, dq, dk, dlog_alpha, w, hs);
-  if (e == hipSuccess && run(4)) e = gla::launch_bwd_dv(s2, dO, nullptr, dSTs, dv, nseg > 1 ? nullptr : dS0, w, hs);
+  if (e == hipSuccess && run(5)) e = gla::launch_bwd_dv(s2, dO, nullptr, dSTs, dv, nseg > 1 ? nullptr : dS0, w, hs);
   return hip_status(e);
 }
 
@@ -327,7 +335,7 @@ GLA_EXPORT gla_status gla_chunk_bwd_general(const gla_problem *prob, const void 
   if (s.inv_tau != 0.f) return GLA_ERR_UNSUPPORTED;  // no key-gate epilogue with the value-side gate
   if ((st = check_lds(s, true)) != GLA_OK) return st;
   const unsigned stage = (prob->flags & GLA_STAGE_MASK) >> GLA_STAGE_SHIFT;
-  if (stage > 6) return GLA_ERR_SHAPE;
+  if (stage > 7) return GLA_ERR_SHAPE;
   const bool any = (int64_t)s.BH * s.T > 0;
   if (any && (!q || !k || !v || !log_beta || !dO || !dq || !dk || !dv)) return GLA_ERR_NULL;
   if (any && dlog_beta && !o) return GLA_ERR_NULL;
@@ -345,11 +353,12 @@ GLA_EXPORT gla_status gla_chunk_bwd_general(const gla_problem *prob, const void 
   if (run(1) && !(prob->flags & GLA_FLAG_REUSE_FWD_WORKSPACE))
     e = gla::launch_prep(s, q, k, log_alpha, w, hs);
   if (e == hipSuccess && run(2)) e = gla::launch_beta_prep(s, v, dO, log_beta, w, hs);
-  if (e == hipSuccess && run(3)) e = gla::launch_bwd_dq(s, k, log_alpha, w.Vh, S0, w.Oh, dS_T, dq, w, hs, true);
-  if (e == hipSuccess && run(4))
+  if (e == hipSuccess && run(3)) e = gla::launch_bwd_intra(s, q, k, log_alpha, w.Vh, w.Oh, w, hs);
+  if (e == hipSuccess && run(4)) e = gla::launch_bwd_dq(s, k, log_alpha, w.Vh, S0, w.Oh, dS_T, dq, w, hs, true);
+  if (e == hipSuccess && run(5))
     e = gla::launch_bwd_dk(s, q, k, log_alpha, w.Vh, w.Oh, dS_T, dq, dk, dlog_alpha, w, hs, true);
-  if (e == hipSuccess && run(5)) e = gla::launch_bwd_dv(s, dO, log_beta, dS_T, dv, dS0, w, hs);
-  if (e == hipSuccess && run(6) && dlog_beta)
+  if (e == hipSuccess && run(6)) e = gla::launch_bwd_dv(s, dO, log_beta, dS_T, dv, dS0, w, hs);
+  if (e == hipSuccess && run(7) && dlog_beta)
     e = gla::launch_beta_grad(s, o, dO, v, dv, dlog_beta, w, hs);
   return hip_status(e);
 }

@@ -4,12 +4,15 @@
 //
 // Per chunk n (S_[n] = state before the chunk, dS_[n+1] = dL/dS after it, B =
 // chunk-local inclusive cumsum of log alpha, Lambda = exp(B), Gamma =
-// exp(B_last - B), dP = (dO V^T) (.) M):
-//   dq_sweep (forward):  dq = Lambda (.) (dO S_[n]^T) + intra(dP, k)
+// exp(B_last - B)):
+//   dq_sweep (forward):  dq_inter = Lambda (.) (dO S_[n]^T),  dq = dq_inter + dq_intra
 //                        S_[n+1] = Diag(gamma) S_[n] + (K (.) Gamma)^T V
-//   dk_sweep (reverse):  dk = Gamma (.) (V dS_[n+1]^T) + intra(dP^T, q)
+//   dk_sweep (reverse):  dk_inter = Gamma (.) (V dS_[n+1]^T), dk = dk_inter + dk_intra
 //                        dS_[n] = Diag(gamma) dS_[n+1] + (Q (.) Lambda)^T dO
 //                        dlog alpha = revcumsum(q (.) dq - k (.) dk) + rowsum(S_T (.) dS_T)
+// The intra-chunk terms (dq_intra, dk_intra and their share of the gate
+// gradient) depend on no state; gla_intra.hip computes them chunk-parallel
+// and the sweeps add them per (row, feature).
 // dq, dk and the gate gradient reduce over d_v, so a workgroup owns 32 key
 // features of one head for the whole sequence and holds the transposed state
 // (value rows x 32 features, fp32) in matrix-core accumulators.
@@ -26,23 +29,17 @@
 // columns.  Slab tiles are XOR-swizzled per row so that both read patterns are
 // bank-conflict free.  The products that reduce over d_v leave one partial per
 // state wave; these are pre-scaled and summed in two steps through LDS, then
-// combined per (row, feature) with the intra-chunk terms:
-//   sub-chunk blocks below the diagonal and, via the factorised decay
-//   exp(B_i - z) exp(z - B_j), the diagonal ones: 16x16 matrix-core products
-//   of fp32 operands split into bf16 hi + lo (three cross terms), scaled by
-//   the decay of the blocks in between (every exponent <= 0);
-//   diagonal blocks whose decay range exceeds kWide: pairwise exp(B_i - B_j)
-//   in fp32.
-// For bf16 the state operand, the gated update operand and the dq hand-off are
-// split into bf16 hi + lo so that the gate gradient's long reverse sum keeps
-// fp32 accuracy.
+// scaled per (row, feature) and added to the intra-chunk term.
+// For bf16 the state operand and the gated update operand are split into bf16
+// hi + lo, and dq_inter reaches the dk sweep in fp32, so that the gate
+// gradient's long reverse sum keeps fp32 accuracy.
 //
 // General form (GB; App. C, a value-side gate beta as well): v and dO arrive
 // as Vh = V (.) exp(-E) and Oh = dO (.) exp(E) (E the chunk-local cumsum of
 // log beta, formed by gla_beta.hip), and the state's value rows decay by
 // gb = exp(E_last) per chunk: S_[n+1] = (gamma S_[n] + (K (.) Gamma)^T Vh) gb
 // in the dq sweep, D = dS_[n+1] gb before the dk sweep's products; the chunk's
-// gb row is staged in the intra-output tile, which is free during the slabs.
+// gb row is staged in LDS.
 // For the value-side gate gradient the dq sweep also stores every chunk-end
 // state S_[n+1] (io dtype, in the accumulators' own lane order), and the dk
 // sweep, holding dS_[n+1] in the same order, forms this tile's
@@ -63,17 +60,19 @@ constexpr float kWide = 60.f;
 typedef float f16v __attribute__((ext_vector_type(16)));
 
 struct KsArgs {
-  const void *q, *k, *la, *v, *dO, *dq_in, *dq_lo_in;
+  const void *q, *k, *la, *v, *dO;
+  const void *dqi, *dki, *dai;  // intra-chunk dq, dk and in-chunk dA sums [BH][T][K] io (gla_intra.hip)
+  const float *dat;             // [BH][N][K] chunk totals of the intra-chunk dA
   const float *S0, *dST;
-  void *dq, *dq_lo, *dk, *dla;
-  float *dP, *cST;
+  void *dq, *dk, *dla;
+  float *dqr;                   // [BH][T][K] fp32 dq_inter: written by the dq sweep, read by the dk sweep
+  float *cST;
   float *dla_part;  // scalar gate: [BH][KT][T] per-tile feature sums of the gate gradient
   const float *gbv; // general form: [BH][N][V] chunk decays exp(E_last) of the value-side gate
   void *Sb;         // general form: chunk-end states S_[n+1], accumulator-native layout (sb_index)
   float *cpart;     // general form: [BH][N][KT][V] per key tile colsum(S_[n+1] (.) dS_[n+1])
   int BH, T, K, V, C, N, KT;
   int sg;         // scalar gate: la is [BH][T], one value per step shared by every feature
-  float wide_thr;  // a diagonal block takes pairwise decays when its decay range exceeds this
   float inv_tau;   // gate epilogue (0: la holds log alpha)
 };
 
@@ -88,31 +87,24 @@ template <typename T, int CP> struct KsLayout {
   // fragment's eight consecutive rows are single 8/16-byte LDS accesses.
   static constexpr int LDT = CP + 4;                          // fp32 feature-major tiles
   static constexpr int LDTB = CP + (sizeof(T) == 2 ? 8 : 4);  // T feature-major tiles
-  static constexpr int LDP = CP + 4;                          // dP (dq: [t][s]; dk: [s][t])
   static constexpr int LDRG = NRG + 4;                        // row-group sums [32][NRG]
   static constexpr size_t slab = sizeof(T) * CP * LDV;
   static constexpr size_t offV = 0;
   static constexpr size_t offD = offV + slab;
   static constexpr size_t offBh = offD + slab;                          // gated update operand (hi)
   static constexpr size_t offBl = offBh + sizeof(T) * kKF * LDTB;       // (lo, bf16 only)
-  static constexpr size_t offO = offBl + (sizeof(T) == 2 ? sizeof(T) * kKF * LDTB : 0);  // intra operand
-  static constexpr size_t offBloc = offO + 4 * kKF * LDT;               // block-local cumsum
-  static constexpr size_t offdP = offBloc + 4 * kKF * LDT;
-  static constexpr size_t offRed = offdP + 4 * CP * LDP;                // partial sums [NP]
-  static constexpr size_t offOr = offRed + 4 * NP * kKF * LDT;          // intra-chunk results
+  static constexpr size_t offBloc = offBl + (sizeof(T) == 2 ? sizeof(T) * kKF * LDTB : 0);  // block-local cumsum
+  static constexpr size_t offRed = offBloc + 4 * kKF * LDT;             // partial sums [NP]
+  static constexpr size_t offOr = offRed + 4 * NP * kKF * LDT;          // general form: the chunk's gb row
   static constexpr size_t offRg = offOr + 4 * kKF * LDT;                // row-group totals
   static constexpr size_t offSc = offRg + 4 * kKF * LDRG;               // per-block scale [NB][32]
-  static constexpr size_t offEt = offSc + 4 * NB * kKF;                 // diagonal-block scale [NB][32]
-  static constexpr size_t offGp = offEt + 4 * NB * kKF;                 // pair factors [3][32]
-  static constexpr size_t offG = offGp + 4 * 3 * kKF;                   // gamma [32]
+  static constexpr size_t offG = offSc + 4 * NB * kKF;                  // gamma [32]
   static constexpr size_t offCar = offG + 4 * kKF;                      // carry [2][32]
   static constexpr size_t offRedS = offCar + 4 * 2 * kKF;               // final-state sums [8][32]
   static constexpr size_t offFt = offRedS + 4 * 8 * kKF;               // per-thread block decay [NRG][32]
   static constexpr size_t offGrp = offFt + 4 * NRG * kKF;               // dk: row-group sums of dA
   static constexpr size_t total = offGrp + 4 * kKF * LDRG;
 };
-
-__device__ __forceinline__ int pair_idx(int I, int J) { return I == 2 ? 0 : (J == 0 ? 1 : 2); }
 
 // ------------------------------------------------------------- 32x32 tiles
 // v_mfma_f32_32x32x16_bf16 (or 8 x v_mfma_f32_32x32x2f32): lane l = 32 g + j
@@ -350,12 +342,11 @@ struct Factors {
   float tot;      // log decay of this thread's 16-row block
   float blast;    // log decay of the whole chunk
   float bs[4];    // log decay of each 16-row block
-  bool wide;
 };
 
 template <int NRG, int LDRG>
 __device__ __forceinline__ Factors chunk_factors(const float *sRg, const float (&c)[4], int frg, int blk,
-                                                 int fk, bool fv, float wide_thr) {
+                                                 int fk) {
   // blk (the thread's 16-row block) is uniform across the wave; frg % 4 (its
   // row group inside the block) is not
   Factors f;
@@ -379,30 +370,15 @@ __device__ __forceinline__ Factors chunk_factors(const float *sRg, const float (
   const float ex = q == 0 ? 0.f : (q == 1 ? in_blk[0] : (q == 2 ? in_blk[0] + in_blk[1] : in_blk[0] + in_blk[1] + in_blk[2]));
 #pragma unroll
   for (int i = 0; i < 4; ++i) f.Bloc[i] = ex + c[i];
-  f.wide = fv && -f.tot > wide_thr;
   return f;
 }
 
 // Per-chunk gate data the factor threads publish: the block-level scale of the
-// inter partials, the diagonal-block operand scale exp(-tot) (zero where the
-// block needs pairwise decays), gamma and the decays between non-adjacent
-// blocks.
-template <int NB, int LDRG>
-__device__ __forceinline__ void publish_decays(float *sSc, float *sEt, float *sG, float *sGp,
-                                               const Factors &f, float scale_log,
+// inter partials and gamma.
+__device__ __forceinline__ void publish_decays(float *sSc, float *sG, const Factors &f, float scale_log,
                                                int frg, int fk, bool fv) {
-  if ((frg & 3) == 0) {
-    sSc[(frg >> 2) * kKF + fk] = __expf(scale_log);
-    sEt[(frg >> 2) * kKF + fk] = f.wide ? 0.f : __expf(-f.tot);
-  }
-  if (frg == 0) {
-    sG[fk] = fv ? __expf(f.blast) : 0.f;
-    if constexpr (NB == 4) {
-      sGp[0 * kKF + fk] = __expf(f.bs[1]);
-      sGp[1 * kKF + fk] = __expf(f.bs[1] + f.bs[2]);
-      sGp[2 * kKF + fk] = __expf(f.bs[2]);
-    }
-  }
+  if ((frg & 3) == 0) sSc[(frg >> 2) * kKF + fk] = __expf(scale_log);
+  if (frg == 0) sG[fk] = fv ? __expf(f.blast) : 0.f;
 }
 
 // Reduction of the d_v-reducing partials (rows t, feature j; 32-row tiles th):
@@ -449,19 +425,16 @@ template <typename T, int CP, int NSL, bool PRE, bool GB>
 __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   using L = KsLayout<T, CP>;
   constexpr int VS = L::VS, NB = L::NB, NRG = L::NRG, NST = CP / 16, NTT = CP / 32;
-  constexpr int NDT = CP == 64 ? 3 : 1;  // dP tiles on or below the diagonal, one per wave 0..NDT-1
   constexpr bool SPLIT = sizeof(T) == 2;
   static_assert(VS * sizeof(T) == kRowB, "slab row size");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   T *sV = (T *)(smem + L::offV), *sD = (T *)(smem + L::offD);
   T *sBh = (T *)(smem + L::offBh), *sBl = (T *)(smem + L::offBl);
-  float *sKo = (float *)(smem + L::offO);
-  float *sBloc = (float *)(smem + L::offBloc), *sdP = (float *)(smem + L::offdP);
+  float *sBloc = (float *)(smem + L::offBloc);
   float *sRed = (float *)(smem + L::offRed), *sOr = (float *)(smem + L::offOr);
   float *sRg = (float *)(smem + L::offRg), *sSc = (float *)(smem + L::offSc);
-  float *sEt = (float *)(smem + L::offEt);
-  float *sGp = (float *)(smem + L::offGp), *sG = (float *)(smem + L::offG);
-  float *sRedS = (float *)(smem + L::offRedS), *sFt = (float *)(smem + L::offFt);
+  float *sG = (float *)(smem + L::offG);
+  float *sRedS = (float *)(smem + L::offRedS);
 
   int bh, kt;
   xcd_map(a.BH, a.KT, bh, kt);
@@ -477,8 +450,6 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   const int lb0 = row_lane_base<T>(0), lb1 = row_lane_base<T>(1);
   const int lt0 = tr_lane_base(0), lt1 = tr_lane_base(4);
 
-  for (int i = tid; i < CP * L::LDP; i += kKT) sdP[i] = 0.f;
-
   f16v S[NSL];
 #pragma unroll
   for (int sl = 0; sl < NSL; ++sl)
@@ -492,6 +463,7 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   const int lrow = a.sg ? 1 : K;  // gate elements per step
   const T *kh_ = (const T *)a.k + (int64_t)bh * a.T * K, *lah = (const T *)a.la + (int64_t)bh * a.T * lrow;
   const T *vh = (const T *)a.v + (int64_t)bh * a.T * V, *dOh = (const T *)a.dO + (int64_t)bh * a.T * V;
+  const T *dqih = (const T *)a.dqi + (int64_t)bh * a.T * K;
   uint32_t eoff[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -500,7 +472,7 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   }
   // (C is a multiple of 4: a thread's four rows are all inside or all outside)
   const uint32_t sbase = (fthr && 4 * frg < C && fv) ? (uint32_t)(4 * frg * esz) : 0x80000000u;
-  uint32_t fin_la[4], fin_k[4];
+  uint32_t fin_la[4], fin_k[4], fin_dqi[4];
   // general form: the chunk's gb row (value v held by thread v mod 512)
   float gbr[2];
   auto fetch_gb = [&](int n) {
@@ -520,10 +492,12 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
     const auto rs_la = make_rsrc(a.la ? lah + (int64_t)t0 * lrow : kh_,
                                  a.la ? rsrc_bytes((int64_t)(a.T - t0) * lrow * esz) : 0u);
     const auto rs_k = make_rsrc(kh_ + (int64_t)t0 * K, bytes);
+    const auto rs_i = make_rsrc(dqih + (int64_t)t0 * K, bytes);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       fin_la[i] = ld_elem<T>(rs_la, gate_off<T>(a.sg, eoff[i], sbase, i));
       fin_k[i] = ld_elem<T>(rs_k, eoff[i]);
+      fin_dqi[i] = ld_elem<T>(rs_i, eoff[i]);
     }
     if constexpr (GB) fetch_gb(n);
   };
@@ -540,15 +514,8 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
     else pd.load(make_rsrc(dOh + (int64_t)t0 * V + c0, bytes), V - c0);
   };
 
-  T *dqo = (T *)a.dq + (int64_t)bh * a.T * K, *dqlo = (T *)a.dq_lo + (int64_t)bh * a.T * K;
-  float *dPg = a.dP + (int64_t)bh * N * C * C;
-  // waves 0..NDT-1 each accumulate one whole 32x32 dP tile (t rows 32 tr..,
-  // s columns 32 tc..: T00, T10, T11) over every slab; the tile above the
-  // diagonal is zero.  Each SIMD still issues at most 48 products per slab.
-  const bool dpw = w < NDT;
-  const int tr = (w == 1 || w == 2) ? 1 : 0, tc = w == 2 ? 1 : 0;
-  const int pA = lb0 + 32 * tr * kRowB, pB = lb0 + 32 * tc * kRowB;
-  const int pA1 = lb1 + 32 * tr * kRowB, pB1 = lb1 + 32 * tc * kRowB;
+  T *dqo = (T *)a.dq + (int64_t)bh * a.T * K;
+  float *dqro = a.dqr + (int64_t)bh * a.T * K;
 
   fetch_factors(0);
   fetch_slab(0, 0);
@@ -557,11 +524,14 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   for (int n = 0; n < N; ++n) {
     const int t0 = n * C, rv = min(C, a.T - t0);
     // ---- factors: cumsum of log alpha, gated operands
-    float c[4], kv[4];
+    float c[4], kv[4], dqi[4];
     {
       float x[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) x[i] = elem_f<T>(fin_la[i]);
+      for (int i = 0; i < 4; ++i) {
+        x[i] = elem_f<T>(fin_la[i]);
+        dqi[i] = elem_f<T>(fin_dqi[i]);
+      }
       if constexpr (PRE) {  // gate epilogue
 #pragma unroll
         for (int i = 0; i < 4; ++i) x[i] = gate_la(x[i], a.inv_tau, fthr && fv && 4 * frg + i < rv);
@@ -577,25 +547,21 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
     }
     __syncthreads();
     if (fthr) {
-      const Factors f = chunk_factors<NRG, L::LDRG>(sRg, c, frg, w >> 1, fk, fv, a.wide_thr);
-      sFt[frg * kKF + fk] = f.tot;
+      const Factors f = chunk_factors<NRG, L::LDRG>(sRg, c, frg, w >> 1, fk);
       const float ekt = __expf(f.blast - f.pre - f.tot);
-      f4 ko4, bl4;
+      f4 bl4;
       T hi4[4], lo4[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float ks = kv[i] * __expf(f.tot - f.Bloc[i]);
-        const float kt_ = ks * ekt;
+        const float kt_ = kv[i] * __expf(f.tot - f.Bloc[i]) * ekt;
         hi4[i] = cvt<T>(kt_);
         lo4[i] = cvt<T>(kt_ - (float)hi4[i]);
-        ko4[i] = ks;
         bl4[i] = f.Bloc[i];
       }
       store4<T>(sBh + fk * L::LDTB + 4 * frg, hi4);
       if constexpr (SPLIT) store4<T>(sBl + fk * L::LDTB + 4 * frg, lo4);
-      *(f4 *)(sKo + fk * L::LDT + 4 * frg) = ko4;
       *(f4 *)(sBloc + fk * L::LDT + 4 * frg) = bl4;
-      publish_decays<NB, L::LDRG>(sSc, sEt, sG, sGp, f, f.pre, frg, fk, fv);
+      publish_decays(sSc, sG, f, f.pre, frg, fk, fv);
     }
     if constexpr (GB) stage_gb();
     // unconditional (the last chunk re-reads itself) so that the wait counts
@@ -603,11 +569,11 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
     fetch_factors(min(n + 1, N - 1));
     __syncthreads();
 
-    // ---- slabs: dP tiles, dq_inter partials (state before the chunk), update
+    // ---- slabs: dq_inter partials (state before the chunk), update
     const float gam = sG[j];
-    f16v acc[2], accP;
+    f16v acc[2];
 #pragma unroll
-    for (int e = 0; e < 16; ++e) acc[0][e] = acc[1][e] = accP[e] = 0.f;
+    for (int e = 0; e < 16; ++e) acc[0][e] = acc[1][e] = 0.f;
 #pragma unroll
     for (int sl = 0; sl < NSL; ++sl) {
       const int q = n * NSL + sl;
@@ -630,34 +596,22 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
           }
           S[sl] *= gam;
         }
-        // dP = dO V^T for this wave's tile (waves 0..NDT-1), interleaved with
-        // the state update S^T <- gamma S^T + V^T (K (.) Gamma) so that the
-        // two independent accumulation chains hide each other's operand
-        // reads; the next slab's loads are issued in two halves between these
-        // products (pinned by scheduling barriers) so that the memory
-        // pipeline drains meanwhile
-        constexpr int NDS = VS / 16;   // dP steps per slab
-        constexpr int UPD = NDS / NST;  // dP steps per update step
-        auto slab_products = [&](auto with_dp) {
+        // the state update S^T <- gamma S^T + V^T (K (.) Gamma); the next
+        // slab's loads are issued in two halves between its products (pinned
+        // by scheduling barriers) so that the memory pipeline drains meanwhile
 #pragma unroll
-          for (int st = 0; st < NDS; ++st) {
-            if constexpr (decltype(with_dp)::value)
-              accP = mma32<T>(accP, ld_slab_row<T>(sD, pA, pA1, 0, 16 * st), ld_slab_row<T>(sV, pB, pB1, 0, 16 * st));
-            if (st == 0 || st == NDS / 2) {
-              __builtin_amdgcn_sched_barrier(0);
-              fetch_slab(q + 1, st == 0 ? 0 : 1);
-              __builtin_amdgcn_sched_barrier(0);
-            }
-            if (sw && (st + 1) % UPD == 0) {
-              const int u = (st + 1) / UPD - 1;
-              const frag_t<T> av = ld_slab_col_perm<T>(sV, lt0, lt1, 16 * u, 32 * w);
-              S[sl] = mma32<T>(S[sl], av, ld_row32<T>(sBh, L::LDTB, 0, 16 * u));
-              if constexpr (SPLIT) S[sl] = mma32<T>(S[sl], av, ld_row32<T>(sBl, L::LDTB, 0, 16 * u));
-            }
+        for (int u = 0; u < NST; ++u) {
+          if (u == 0 || u == NST / 2) {
+            __builtin_amdgcn_sched_barrier(0);
+            fetch_slab(q + 1, u == 0 ? 0 : 1);
+            __builtin_amdgcn_sched_barrier(0);
           }
-        };
-        if (dpw) slab_products(std::true_type{});
-        else slab_products(std::false_type{});
+          if (sw) {
+            const frag_t<T> av = ld_slab_col_perm<T>(sV, lt0, lt1, 16 * u, 32 * w);
+            S[sl] = mma32<T>(S[sl], av, ld_row32<T>(sBh, L::LDTB, 0, 16 * u));
+            if constexpr (SPLIT) S[sl] = mma32<T>(S[sl], av, ld_row32<T>(sBl, L::LDTB, 0, 16 * u));
+          }
+        }
         if constexpr (GB) {
           // S_[n+1] = (gamma S_[n] + K~^T Vh) gb, by value row
           static_assert(L::offOr % 16 == 0, "aligned factor rows");
@@ -672,84 +626,29 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
       __syncthreads();
     }
 
-    // ---- dP: mask, publish (and hand it to the dk sweep transposed; the
-    // zero tile above the diagonal is written there by wave NDT)
-    if (dpw || (CP == 64 && w == NDT && kt == 0)) {
-      const bool zero_tile = !dpw;
-      const int rt = zero_tile ? 0 : tr, ct = zero_tile ? 1 : tc;
-      float *pd0 = sdP + (32 * rt + 4 * g) * L::LDP + 32 * ct + j;
-      const int col = 32 * ct + j;
-      const auto rs_dp = make_rsrc(dPg + (int64_t)n * C * C, (uint32_t)(C * C * 4));
-#pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const int t4 = 32 * rt + 8 * b + 4 * g;
-        f4 v4;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) v4[r] = (zero_tile || col > t4 + r) ? 0.f : accP[4 * b + r];
-        if (!zero_tile) {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) pd0[(8 * b + r) * L::LDP] = v4[r];
-        }
-        if (kt == 0) {
-          const uint32_t off = (t4 < C && col < C) ? (uint32_t)((col * C + t4) * 4) : 0x80000000u;
-          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v4), rs_dp, off, 0, 0);
-        }
-      }
-    }
     // ---- dq_inter partials, pre-scaled by exp(log decay before the block)
     partials_publish<L>(acc, sSc, sRed, w, g, j);
     __syncthreads();
     partials_add<L>(acc, sRed, w, g, j);
-    // intra-chunk term by sub-chunk blocks, for row block I: sum over J <= I of
-    // dP_IJ x_J with x_J = (k (.) exp(tot_J - Bloc)) g_IJ below the diagonal and
-    // k (.) exp(-Bloc) on it (zero where the block needs pairwise decays)
-    for (int t = w; t < 2 * NB; t += 8) {
-      const int I = t >> 1, kq = t & 1, j16 = l & 15, g16 = l >> 4;
-      f4 o = zero4();
-#pragma unroll
-      for (int s = 0; s < CP / 32; ++s) {
-        if (32 * s > 16 * I) continue;
-        const int J = 2 * s + (g16 >> 1);
-        const float sc = J > I ? 0.f
-                               : (J == I ? sEt[I * kKF + 16 * kq + j16]
-                                         : (J <= I - 2 ? sGp[pair_idx(I, J) * kKF + 16 * kq + j16] : 1.f));
-        f8 bf = ldf_row(sKo, L::LDT, 16 * kq, 32 * s);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) bf[i] *= sc;
-        o = mma_split3<T>(o, ldf_row(sdP, L::LDP, 16 * I, 32 * s), bf);
-      }
-      *(f4 *)(sOr + (16 * kq + j16) * L::LDT + 16 * I + 4 * g16) = o;
-    }
     __syncthreads();
 
-    // ---- dq = Lambda (.) inter + intra, per (row, feature)
+    // ---- dq_inter = Lambda (.) inter; dq = dq_inter + dq_intra, per (row, feature)
     if (fthr) {
-      const int blk = frg >> 2;
-      const bool wide = fv && -sFt[frg * kKF + fk] > a.wide_thr;
-      f4 in4 = *(const f4 *)(sOr + fk * L::LDT + 4 * frg);
+      f4 in4 = *(const f4 *)(sRed + fk * L::LDT + 4 * frg);
 #pragma unroll
-      for (int p = 0; p < L::NP; ++p) in4 += *(const f4 *)(sRed + (p * kKF + fk) * L::LDT + 4 * frg);
+      for (int p = 1; p < L::NP; ++p) in4 += *(const f4 *)(sRed + (p * kKF + fk) * L::LDT + 4 * frg);
       const f4 bl4 = *(const f4 *)(sBloc + fk * L::LDT + 4 * frg);
       const uint32_t obytes = rsrc_bytes((int64_t)(a.T - t0) * K * esz);
       const auto rs_dq = make_rsrc(dqo + (int64_t)t0 * K, obytes);
-      const auto rs_dql = make_rsrc(dqlo + (int64_t)t0 * K, obytes);
+      const auto rs_dqr = make_rsrc(dqro + (int64_t)t0 * K, rsrc_bytes((int64_t)(a.T - t0) * K * 4));
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int row = 4 * frg + i;
-        const float bloc = bl4[i];
-        float dq = __expf(bloc) * in4[i];
-        if (wide && row < rv) {
-          // diagonal block with pairwise decays exp(B_row - B_s)
-#pragma unroll 1
-          for (int s = 16 * blk; s <= row; ++s)
-            dq += sdP[row * L::LDP + s] * (float)kh_[(int64_t)(t0 + s) * K + kf] *
-                  __expf(bloc - sBloc[fk * L::LDT + s]);
-        }
+        const float dqe = __expf(bl4[i]) * in4[i];
         // rows past the sequence end, past the chunk or of absent features
         // fall outside the buffer range and are dropped
-        const T hi = cvt<T>(dq);
-        st_elem<T>(rs_dq, eoff[i], hi);
-        if constexpr (SPLIT) st_elem<T>(rs_dql, eoff[i], cvt<T>(dq - (float)hi));
+        st_elem<T>(rs_dq, eoff[i], cvt<T>(dqe + dqi[i]));
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, dqe), rs_dqr,
+                                              eoff[i] == 0x80000000u ? eoff[i] : eoff[i] / esz * 4, 0, 0);
       }
     }
   }
@@ -788,12 +687,10 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   T *sV = (T *)(smem + L::offV), *sD = (T *)(smem + L::offD);
   T *sBh = (T *)(smem + L::offBh), *sBl = (T *)(smem + L::offBl);
-  float *sQo = (float *)(smem + L::offO);
-  float *sBloc = (float *)(smem + L::offBloc), *sdP = (float *)(smem + L::offdP);
+  float *sBloc = (float *)(smem + L::offBloc);
   float *sRed = (float *)(smem + L::offRed), *sOr = (float *)(smem + L::offOr);
   float *sRg = (float *)(smem + L::offRg), *sSc = (float *)(smem + L::offSc);
-  float *sEt = (float *)(smem + L::offEt);
-  float *sGp = (float *)(smem + L::offGp), *sG = (float *)(smem + L::offG);
+  float *sG = (float *)(smem + L::offG);
   float *sCar = (float *)(smem + L::offCar), *sFt = (float *)(smem + L::offFt);
   float *sGrp = (float *)(smem + L::offGrp);
 
@@ -825,10 +722,10 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
   const T *qh_ = (const T *)a.q + (int64_t)bh * a.T * K, *kh_ = (const T *)a.k + (int64_t)bh * a.T * K;
   const int lrow = a.sg ? 1 : K;  // gate elements per step
   const T *lah = (const T *)a.la + (int64_t)bh * a.T * lrow;
-  const T *dqh = (const T *)a.dq_in + (int64_t)bh * a.T * K;
-  const T *dqlh = SPLIT ? (const T *)a.dq_lo_in + (int64_t)bh * a.T * K : dqh;
+  const float *dqrh = a.dqr + (int64_t)bh * a.T * K;
+  const T *dkih = (const T *)a.dki + (int64_t)bh * a.T * K, *daih = (const T *)a.dai + (int64_t)bh * a.T * K;
+  const float *dath = a.dat + (int64_t)bh * N * K;
   const T *vh = (const T *)a.v + (int64_t)bh * a.T * V, *dOh = (const T *)a.dO + (int64_t)bh * a.T * V;
-  const float *dPg = a.dP + (int64_t)bh * N * C * C;
   uint32_t eoff[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -837,7 +734,7 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
   }
   // (C is a multiple of 4: a thread's four rows are all inside or all outside)
   const uint32_t sbase = (fthr && 4 * frg < C && fv) ? (uint32_t)(4 * frg * esz) : 0x80000000u;
-  uint32_t fin_la[4], fin_q[4], fin_k[4], fin_dq[4], fin_dql[4];
+  uint32_t fin_la[4], fin_q[4], fin_k[4], fin_dqr[4], fin_dki[4], fin_dai[4], fin_dat;
   // general form: the chunk's gb row (value v held by thread v mod 512)
   float gbr[2];
   auto fetch_gb = [&](int n) {
@@ -859,8 +756,6 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
       for (int i = 0; i < (int)(sizeof(svr.r) / 16); ++i) svr.r[i] = p[i];
     }
   };
-  TileLd<float, CP, CP, kKT> pp;
-  pp.init(C, C, C);
   auto fetch_factors = [&](int n) {
     const int t0 = n * C;
     const uint32_t bytes = rsrc_bytes((int64_t)(a.T - t0) * K * esz);
@@ -869,17 +764,20 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
                                  a.la ? rsrc_bytes((int64_t)(a.T - t0) * lrow * esz) : 0u);
     const auto rs_q = make_rsrc(qh_ + (int64_t)t0 * K, bytes);
     const auto rs_k = make_rsrc(kh_ + (int64_t)t0 * K, bytes);
-    const auto rs_dq = make_rsrc(dqh + (int64_t)t0 * K, bytes);
-    const auto rs_dql = make_rsrc(dqlh + (int64_t)t0 * K, bytes);
+    const auto rs_dqr = make_rsrc(dqrh + (int64_t)t0 * K, rsrc_bytes((int64_t)(a.T - t0) * K * 4));
+    const auto rs_dki = make_rsrc(dkih + (int64_t)t0 * K, bytes);
+    const auto rs_dai = make_rsrc(daih + (int64_t)t0 * K, bytes);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       fin_la[i] = ld_elem<T>(rs_la, gate_off<T>(a.sg, eoff[i], sbase, i));
       fin_q[i] = ld_elem<T>(rs_q, eoff[i]);
       fin_k[i] = ld_elem<T>(rs_k, eoff[i]);
-      fin_dq[i] = ld_elem<T>(rs_dq, eoff[i]);
-      fin_dql[i] = SPLIT ? ld_elem<T>(rs_dql, eoff[i]) : 0u;
+      fin_dqr[i] = __builtin_amdgcn_raw_buffer_load_b32(rs_dqr, eoff[i] == 0x80000000u ? eoff[i] : eoff[i] / esz * 4, 0, 0);
+      fin_dki[i] = ld_elem<T>(rs_dki, eoff[i]);
+      fin_dai[i] = ld_elem<T>(rs_dai, eoff[i]);
     }
-    pp.load(make_rsrc(dPg + (int64_t)n * C * C, (uint32_t)(C * C * 4)));
+    fin_dat = __builtin_amdgcn_raw_buffer_load_b32(make_rsrc(dath + (int64_t)n * K, (uint32_t)(K * 4)),
+                                                   fv ? (uint32_t)(kf * 4) : 0x80000000u, 0, 0);
     if constexpr (GB) fetch_gb(n);
   };
   TileLd<T, CP, VS, kKT> pv, pd;
@@ -905,11 +803,18 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
     const int n = N - 1 - it;
     const int t0 = n * C, rv = min(C, a.T - t0);
     // ---- factors
-    float c[4], kv[4], qdq[4], zc[4];  // zc: the gate argument, for the gate gradient
+    // zc: the gate argument, for the gate gradient; dki, dai, dat: the
+    // chunk's intra-chunk terms
+    float c[4], kv[4], qdq[4], zc[4], dki[4], dai[4];
+    const float dat = __builtin_bit_cast(float, fin_dat);
     {
       float x[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) x[i] = zc[i] = elem_f<T>(fin_la[i]);
+      for (int i = 0; i < 4; ++i) {
+        x[i] = zc[i] = elem_f<T>(fin_la[i]);
+        dki[i] = elem_f<T>(fin_dki[i]);
+        dai[i] = elem_f<T>(fin_dai[i]);
+      }
       if constexpr (PRE) {  // gate epilogue
 #pragma unroll
         for (int i = 0; i < 4; ++i) x[i] = gate_la(x[i], a.inv_tau, fthr && fv && 4 * frg + i < rv);
@@ -920,32 +825,28 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
         s += x[i];
         c[i] = s;
         kv[i] = elem_f<T>(fin_k[i]);
-        qdq[i] = elem_f<T>(fin_q[i]) * (elem_f<T>(fin_dq[i]) + (SPLIT ? elem_f<T>(fin_dql[i]) : 0.f));
+        qdq[i] = elem_f<T>(fin_q[i]) * __builtin_bit_cast(float, fin_dqr[i]);
       }
       if (fthr) sRg[fk * L::LDRG + frg] = s;
     }
     __syncthreads();
-    pp.store(sdP, L::LDP);  // dP of this chunk, stored transposed ([s][t])
     if (fthr) {
-      const Factors f = chunk_factors<NRG, L::LDRG>(sRg, c, frg, w >> 1, fk, fv, a.wide_thr);
+      const Factors f = chunk_factors<NRG, L::LDRG>(sRg, c, frg, w >> 1, fk);
       sFt[frg * kKF + fk] = f.tot;
       const float epre = __expf(f.pre);
-      f4 qo4, bl4;
+      f4 bl4;
       T hi4[4], lo4[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float qh = elem_f<T>(fin_q[i]) * __expf(f.Bloc[i]);
-        const float qt = qh * epre;
+        const float qt = elem_f<T>(fin_q[i]) * __expf(f.Bloc[i]) * epre;
         hi4[i] = cvt<T>(qt);
         lo4[i] = cvt<T>(qt - (float)hi4[i]);
-        qo4[i] = qh;
         bl4[i] = f.Bloc[i];
       }
       store4<T>(sBh + fk * L::LDTB + 4 * frg, hi4);
       if constexpr (SPLIT) store4<T>(sBl + fk * L::LDTB + 4 * frg, lo4);
-      *(f4 *)(sQo + fk * L::LDT + 4 * frg) = qo4;
       *(f4 *)(sBloc + fk * L::LDT + 4 * frg) = bl4;
-      publish_decays<NB, L::LDRG>(sSc, sEt, sG, sGp, f, f.blast - f.pre - f.tot, frg, fk, fv);
+      publish_decays(sSc, sG, f, f.blast - f.pre - f.tot, frg, fk, fv);
     }
     if constexpr (GB) stage_gb();
     fetch_factors(max(n - 1, 0));  // unconditional, see the dq sweep
@@ -1016,56 +917,23 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
     partials_publish<L>(acc, sSc, sRed, w, g, j);
     __syncthreads();
     partials_add<L>(acc, sRed, w, g, j);
-    // intra-chunk term by sub-chunk blocks, for column block J: sum over I >= J
-    // of dP_IJ^T y_I with y_I = (q (.) exp(Bloc)) g_IJ below the diagonal and
-    // q (.) exp(Bloc - tot_J) on it (zero where the block needs pairwise decays)
-    for (int t = w; t < 2 * NB; t += 8) {
-      // the heavier early column blocks go to waves 4..7, which have no
-      // partial to add
-      const int J = NB - 1 - (t >> 1), kq = t & 1, j16 = l & 15, g16 = l >> 4;
-      f4 o = zero4();
-#pragma unroll
-      for (int s = 0; s < CP / 32; ++s) {
-        if (32 * s + 31 < 16 * J) continue;
-        const int I = 2 * s + (g16 >> 1);
-        const float sc = I < J ? 0.f
-                               : (I == J ? sEt[J * kKF + 16 * kq + j16]
-                                         : (I >= J + 2 ? sGp[pair_idx(I, J) * kKF + 16 * kq + j16] : 1.f));
-        f8 bf = ldf_row(sQo, L::LDT, 16 * kq, 32 * s);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) bf[i] *= sc;
-        o = mma_split3<T>(o, ldf_row(sdP, L::LDP, 16 * J, 32 * s), bf);
-      }
-      *(f4 *)(sOr + (16 * kq + j16) * L::LDT + 16 * J + 4 * g16) = o;
-    }
     __syncthreads();
 
-    // ---- dk = Gamma (.) inter + intra; dA = q dq - k dk; in-chunk reverse sums
+    // ---- dk_inter = Gamma (.) inter; dk = dk_inter + dk_intra; dA = q dq - k dk
+    // (inter parts here; the intra parts arrive summed) and in-chunk reverse sums
     float dA[4];
     if (fthr) {
-      const int blk = frg >> 2;
       const float tot = sFt[frg * kKF + fk];
-      const bool wide = fv && -tot > a.wide_thr;
-      f4 in4 = *(const f4 *)(sOr + fk * L::LDT + 4 * frg);
+      f4 in4 = *(const f4 *)(sRed + fk * L::LDT + 4 * frg);
 #pragma unroll
-      for (int p = 0; p < L::NP; ++p) in4 += *(const f4 *)(sRed + (p * kKF + fk) * L::LDT + 4 * frg);
+      for (int p = 1; p < L::NP; ++p) in4 += *(const f4 *)(sRed + (p * kKF + fk) * L::LDT + 4 * frg);
       const f4 bl4 = *(const f4 *)(sBloc + fk * L::LDT + 4 * frg);
       const auto rs_dk = make_rsrc(dko + (int64_t)t0 * K, rsrc_bytes((int64_t)(a.T - t0) * K * esz));
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int row = 4 * frg + i;
-        const float bloc = bl4[i];
-        float dk = __expf(tot - bloc) * in4[i];
-        if (wide && row < rv) {
-          // diagonal block with pairwise decays exp(B_t - B_row)
-          const int tend = min(16 * blk + 16, rv);
-#pragma unroll 1
-          for (int tt = row; tt < tend; ++tt)
-            dk += sdP[row * L::LDP + tt] * (float)qh_[(int64_t)(t0 + tt) * K + kf] *
-                  __expf(sBloc[fk * L::LDT + tt] - bloc);
-        }
-        dA[i] = qdq[i] - kv[i] * dk;
-        st_elem<T>(rs_dk, eoff[i], cvt<T>(dk));
+        const float dke = __expf(tot - bl4[i]) * in4[i];
+        dA[i] = qdq[i] - kv[i] * dke;
+        st_elem<T>(rs_dk, eoff[i], cvt<T>(dke + dki[i]));
       }
       float s = 0.f;
 #pragma unroll
@@ -1089,7 +957,7 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
         }
       }
 #pragma unroll
-      for (int i = 0; i < 4; ++i) dA[i] += later;
+      for (int i = 0; i < 4; ++i) dA[i] += later + dai[i];
       if (a.sg) {
         // scalar gate: this tile's sum over its features, per row (rows past
         // the sequence end fall outside the range); the key tiles are added,
@@ -1118,7 +986,7 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) st_elem<T>(rs_dla, eoff[i], cvt<T>(dA[i]));
       }
-      if (frg == 0) sCar[((it + 1) & 1) * kKF + fk] = all;
+      if (frg == 0) sCar[((it + 1) & 1) * kKF + fk] = all + dat;
     }
   }
 }
@@ -1160,7 +1028,6 @@ KsArgs ks_args(const Shape &s) {
   a.BH = s.BH; a.T = s.T; a.K = s.K; a.V = s.V; a.C = s.C; a.N = s.N;
   a.inv_tau = s.inv_tau;
   a.sg = s.sgate ? 1 : 0;
-  a.wide_thr = -3.0e38f;
   a.KT = (s.K + kKF - 1) / kKF;
   return a;
 }
@@ -1224,10 +1091,9 @@ hipError_t launch_bwd_dq(const Shape &s, const void *k, const void *la, const vo
                          const float *S0, const void *dO, const float *dST, void *dq,
                          const Work &w, hipStream_t st, bool gb_on) {
   KsArgs a = ks_args(s);
-  a.k = k; a.la = la; a.v = v; a.dO = dO; a.S0 = S0; a.dST = dST; a.dq = dq; a.dq_lo = w.dq_lo;
-  a.dP = w.dP; a.cST = w.cST;
+  a.k = k; a.la = la; a.v = v; a.dO = dO; a.S0 = S0; a.dST = dST; a.dq = dq; a.dqr = w.dqr;
+  a.dqi = w.dqi; a.cST = w.cST;
   if (gb_on) { a.gbv = w.gb; a.Sb = w.Sb; }
-  if (s.io != IO_BF16) a.dq_lo = dq;  // unused
   return dispatch_ks<true>(s, a, st);
 }
 
@@ -1236,8 +1102,9 @@ hipError_t launch_bwd_dk(const Shape &s, const void *q, const void *k, const voi
                          void *dk, void *dla, const Work &w, hipStream_t st, bool gb_on) {
   KsArgs a = ks_args(s);
   if (gb_on) { a.gbv = w.gb; a.Sb = w.Sb; a.cpart = w.cpart; }
-  a.q = q; a.k = k; a.la = la; a.v = v; a.dO = dO; a.dST = dST; a.dq_in = dq; a.dq_lo_in = w.dq_lo;
-  a.dk = dk; a.dla = dla; a.dP = w.dP; a.cST = dST ? w.cST : nullptr; a.dla_part = w.dla_part;
+  a.q = q; a.k = k; a.la = la; a.v = v; a.dO = dO; a.dST = dST; a.dqr = w.dqr;
+  a.dki = w.dki; a.dai = w.dai; a.dat = w.dat;
+  a.dk = dk; a.dla = dla; a.cST = dST ? w.cST : nullptr; a.dla_part = w.dla_part;
   hipError_t e = dispatch_ks<false>(s, a, st);
   if (e != hipSuccess || !s.sgate || !dla) return e;
   const int64_t n = (int64_t)s.BH * s.T;

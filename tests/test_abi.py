@@ -249,7 +249,7 @@ def test_empty_batch_needs_nothing(L):
 
 def test_stage_selector_is_validated(L):
     assert fwd_call(L, P(flags=3 << 8)) == gla.GLA_ERR_SHAPE
-    assert bwd_call(L, P(flags=5 << 8)) == gla.GLA_ERR_SHAPE
+    assert bwd_call(L, P(flags=6 << 8)) == gla.GLA_ERR_SHAPE
     assert fwd_call(L, P(B=0, flags=3 << 8), ptr=None, ws=None, ws_bytes=0) == gla.GLA_ERR_SHAPE
 
 

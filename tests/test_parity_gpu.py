@@ -693,7 +693,7 @@ def test_sequence_segments(mode):
         g.chunk_fwd(d["q"], d["k"], d["v"], gate, 64, 16, S0=d["S0"], workspace=ws, stage=st, out=(o3, ST3),
                     gate_tau=gt)
     out = {k2: (torch.empty_like(v2) if v2 is not None else None) for k2, v2 in gr.items()}
-    for st in (2, 3, 4):
+    for st in (2, 3, 4, 5):
         g.chunk_bwd(d["q"], d["k"], d["v"], gate, d["dO"], 64, 16, S0=d["S0"], dST=d["dST"], workspace=ws,
                     reuse_fwd_workspace=True, stage=st, out=out, gate_tau=gt)
     torch.cuda.synchronize()
@@ -739,7 +739,7 @@ def test_stage_by_stage_equals_whole_call():
     for s in (1, 2):
         g.chunk_fwd(*args, 64, 16, S0=d["S0"], workspace=ws, stage=s, out=(o2, ST2))
     out = {k: torch.empty_like(v) for k, v in ref.items()}
-    for s in (2, 3, 4):
+    for s in (2, 3, 4, 5):
         g.chunk_bwd(*args, d["dO"], 64, 16, S0=d["S0"], dST=d["dST"], workspace=ws,
                     reuse_fwd_workspace=True, stage=s, out=out)
     torch.cuda.synchronize()
