@@ -36,13 +36,13 @@ PEAK_F32_FLOPS = 157.3e12
 PEAK_HBM = 8.0e12
 RIDGE = PEAK_BF16_FLOPS / PEAK_HBM
 
-STAGES = [("prep", "fwd", 1), ("fwd_main", "fwd", 2), ("bwd_intra", "bwd", 2), ("bwd_dq", "bwd", 3),
+STAGES = [("prep", "fwd", 1), ("fwd_main", "fwd", 2), ("bwd_dq", "bwd", 2), ("bwd_intra", "bwd", 3),
           ("bwd_dk", "bwd", 4), ("bwd_dv", "bwd", 5)]
 # with the output side (Sec. 4.4): LN + Swish gate after the forward, its
 # reverse mode (producing the layer's dO) before the backward sweeps
 STAGES_OG = STAGES[:2] + [("og_fwd", "og", 0), ("og_bwd", "og", 1)] + STAGES[2:]
 # the general form (App. C, value-side gate beta): its backward's stages
-STAGES_GB = STAGES[:2] + [("beta_prep", "bwdg", 2), ("bwd_intra", "bwdg", 3), ("bwd_dq", "bwdg", 4),
+STAGES_GB = STAGES[:2] + [("beta_prep", "bwdg", 2), ("bwd_dq", "bwdg", 3), ("bwd_intra", "bwdg", 4),
                           ("bwd_dk", "bwdg", 5), ("bwd_dv", "bwdg", 6), ("beta_grad", "bwdg", 7)]
 
 
@@ -75,11 +75,11 @@ def algorithmic(cfg, gate=True, scalar_gate=False, value_gate=False):
         # state pass + output: reads v (and log beta); writes o
         "fwd_main": dict(flops=n * (4 * K * V + (C + 1) * V), bytes=(3 if value_gate else 2) * vv,
                          inter=2 * qk + P + g),
-        # intra-chunk terms: reads q, k, log alpha, v, dO
-        "bwd_intra": dict(flops=n * (C + 1) * (3 * K + V), bytes=2 * qk + la + 2 * vv,
-                          inter=3 * qk + B * H * N * K * 4),
-        # dq sweep: reads k, log alpha, v, dO; writes dq
-        "bwd_dq": dict(flops=n * 2 * K * V, bytes=qk + la + 2 * vv + qk, inter=qk + n * K * 4),
+        # dq sweep (and dP): reads k, log alpha, v, dO
+        "bwd_dq": dict(flops=n * (2 * K * V + (C + 1) * V), bytes=qk + la + 2 * vv, inter=n * K * 4 + n * C * 4),
+        # intra-chunk terms: reads q, k, log alpha; writes dq
+        "bwd_intra": dict(flops=n * (C + 1) * 3 * K, bytes=2 * qk + la + qk,
+                          inter=n * C * 4 + n * K * 4 + 2 * qk + B * H * N * K * 4),
         # dk sweep: reads q, k, log alpha, v, dO; writes dk, dlog alpha
         "bwd_dk": dict(flops=n * 4 * K * V, bytes=2 * qk + la + 2 * vv + qk + la,
                        inter=2 * qk + n * K * 4 + B * H * N * K * 4),

@@ -132,11 +132,11 @@ size_t layout(const Shape &s, int op, char *base, Work *w, int nseg) {
     Sloc = take(states);
     dec = take((size_t)s.BH * s.K * sizeof(float));
   }
-  void *dqi = nullptr, *dki = nullptr, *dai = nullptr, *dat = nullptr, *dqr = nullptr;
+  void *dP = nullptr, *dki = nullptr, *dai = nullptr, *dat = nullptr, *dqr = nullptr;
   void *cST = nullptr, *dla_part = nullptr;
   void *Vh = nullptr, *Oh = nullptr, *gb = nullptr, *Sb = nullptr, *cpart = nullptr;
   if (op >= 1) {
-    dqi = take(rows * s.K * es);
+    dP = take(chunks * s.C * s.C * sizeof(float));
     dki = take(rows * s.K * es);
     dai = take(rows * s.K * es);
     dat = take(chunks * s.K * sizeof(float));
@@ -154,7 +154,7 @@ size_t layout(const Shape &s, int op, char *base, Work *w, int nseg) {
   }
   if (w) {
     w->Qt = Qt; w->Kt = Kt; w->P = P; w->gam = (float *)gam;
-    w->dqi = dqi; w->dki = dki; w->dai = dai; w->dat = (float *)dat; w->dqr = (float *)dqr;
+    w->dP = (float *)dP; w->dki = dki; w->dai = dai; w->dat = (float *)dat; w->dqr = (float *)dqr;
     w->cST = (float *)cST; w->dla_part = (float *)dla_part;
     w->Vh = Vh; w->Oh = Oh; w->gb = (float *)gb; w->Sb = Sb; w->cpart = (float *)cpart;
     w->Sin = (float *)Sin; w->Sloc = (float *)Sloc; w->dec = (float *)dec; w->dSout = (float *)dSout;
@@ -306,8 +306,7 @@ GLA_EXPORT gla_status gla_chunk_bwd(const gla_problem *prob, const void *q, cons
   // per segment: initial state and final-state gradient (the head's own S0
   // and dS_T when unsegmented)
   const float *S0s = nseg > 1 ? w.Sin : S0, *dSTs = nseg > 1 ? w.dSout : dS_T;
-  if (e == hipSuccess && run(2)) e = gla::launch_bwd_intra(s2, q, k, log_alpha, v, dO, w, hs);
-  if (e == hipSuccess && run(3)) {
+  if (e == hipSuccess && run(2)) {
     if (nseg > 1) {
       // local initial-state gradients from a zero final-state gradient, then
       // the reverse segment scan (which also gives the head's dS0)
@@ -315,8 +314,9 @@ GLA_EXPORT gla_status gla_chunk_bwd(const gla_problem *prob, const void *q, cons
       if (e == hipSuccess)
         e = gla::launch_seg_bwd_scan(s.BH, nseg, s.K, s.V, w.dec, dS_T, w.Sloc, w.dSout, dS0, hs);
     }
-    if (e == hipSuccess) e = gla::launch_bwd_dq(s2, k, log_alpha, v, S0s, dO, dSTs, dq, w, hs);
+    if (e == hipSuccess) e = gla::launch_bwd_dq(s2, k, log_alpha, v, S0s, dO, dSTs, w, hs);
   }
+  if (e == hipSuccess && run(3)) e = gla::launch_bwd_intra(s2, q, k, log_alpha, dq, w, hs);
   if (e == hipSuccess && run(4))
     e = gla::launch_bwd_dk(s2, q, k, log_alpha, v, dO, dSTs, dq, dk, dlog_alpha, w, hs);
   if (e == hipSuccess && run(5)) e = gla::launch_bwd_dv(s2, dO, nullptr, dSTs, dv, nseg > 1 ? nullptr : dS0, w, hs);
@@ -353,8 +353,8 @@ GLA_EXPORT gla_status gla_chunk_bwd_general(const gla_problem *prob, const void 
   if (run(1) && !(prob->flags & GLA_FLAG_REUSE_FWD_WORKSPACE))
     e = gla::launch_prep(s, q, k, log_alpha, w, hs);
   if (e == hipSuccess && run(2)) e = gla::launch_beta_prep(s, v, dO, log_beta, w, hs);
-  if (e == hipSuccess && run(3)) e = gla::launch_bwd_intra(s, q, k, log_alpha, w.Vh, w.Oh, w, hs);
-  if (e == hipSuccess && run(4)) e = gla::launch_bwd_dq(s, k, log_alpha, w.Vh, S0, w.Oh, dS_T, dq, w, hs, true);
+  if (e == hipSuccess && run(3)) e = gla::launch_bwd_dq(s, k, log_alpha, w.Vh, S0, w.Oh, dS_T, w, hs, true);
+  if (e == hipSuccess && run(4)) e = gla::launch_bwd_intra(s, q, k, log_alpha, dq, w, hs);
   if (e == hipSuccess && run(5))
     e = gla::launch_bwd_dk(s, q, k, log_alpha, w.Vh, w.Oh, dS_T, dq, dk, dlog_alpha, w, hs, true);
   if (e == hipSuccess && run(6)) e = gla::launch_bwd_dv(s, dO, log_beta, dS_T, dv, dS0, w, hs);

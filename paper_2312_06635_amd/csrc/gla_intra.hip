@@ -8,14 +8,15 @@
 //   dq_intra[i] = sum_{j <= i} dP_ij k_j (.) exp(B_i - B_j)
 //   dk_intra[j] = sum_{i >= j} dP_ij q_i (.) exp(B_i - B_j)
 //   dA_intra[t] = q_t (.) dq_intra[t] - k_t (.) dk_intra[t]   (Sec. 4.3)
-// and the chunk writes dq_intra, dk_intra, the in-chunk reverse cumsum of
-// dA_intra (io dtype: each is added once to an fp32 inter-chunk term) and the
-// chunk total of dA_intra (fp32: the gate gradient carries it across chunks).
+// It runs between the key sweeps: it writes dq = dq_inter + dq_intra (the dq
+// sweep's fp32 dq_inter in), and for the dk sweep dk_intra, the in-chunk
+// reverse cumsum of dA_intra (io dtype: each is added once to an fp32
+// inter-chunk term) and the chunk total of dA_intra (fp32: the gate gradient
+// carries it across chunks).  dP comes from the dq sweep, which streams V and
+// dO anyway.
 //
 // One workgroup per (chunk, head), wave w = the 16-row block w of the chunk.
-//   1. dP: wave w forms the 16 x 16 blocks (w, J <= w) of dO V^T on the
-//      matrix cores (bf16, fp32 accumulate; fp32 MFMA for fp32 io), operands
-//      straight from memory, and stores its 16 rows (masked) to LDS.
+//   1. The chunk's dP (fp32, masked, stored transposed) into LDS.
 //   2. For each group of 64 key features (lane = feature):
 //      - gate cumsums of the wave's block; the sub-chunk ("pink") diagonal
 //        block in fp32 log space on the vector ALUs: one exponential
@@ -40,10 +41,13 @@ namespace gla {
 namespace {
 
 struct IntraArgs {
-  const void *q, *k, *la, *v, *dO;
-  void *dqi, *dki, *dai;  // [BH][T][K] io
+  const void *q, *k, *la;
+  const float *dP;        // [BH][N][C][C] fp32, transposed ([s][t])
+  const float *dqr;       // [BH][T][K] fp32 dq_inter
+  void *dq;               // [BH][T][K] io: the layer's dq
+  void *dki, *dai;        // [BH][T][K] io
   float *dat;             // [BH][N][K] fp32
-  int T, K, V, C, N;
+  int T, K, C, N;
   int sg;         // scalar gate: la is [BH][T]
   float inv_tau;  // gate epilogue (0: la holds log alpha)
 };
@@ -61,17 +65,6 @@ template <typename T> __device__ __forceinline__ void st_el(__amdgpu_buffer_rsrc
     __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, cvt<bf16>(x)), rs, off, 0, 0);
   else
     __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, x), rs, off, 0, 0);
-}
-
-// One fragment (8 consecutive elements of a row) straight from memory.
-template <typename T> __device__ __forceinline__ frag_t<T> ld_frag(__amdgpu_buffer_rsrc_t rs, uint32_t off) {
-  if constexpr (sizeof(T) == 2) {
-    return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
-  } else {
-    const f4 a = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
-    const f4 b = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(rs, off + 16, 0, 0));
-    return f8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
-  }
 }
 
 // acc += a b for fp32 operands: on the bf16 path both are split into hi + lo
@@ -109,7 +102,7 @@ template <int C> struct IntraLayout {
 };
 
 template <typename T, int C, bool PRE>
-__global__ void __launch_bounds__(64 * (C / 16)) intra_kernel(IntraArgs a) {
+__global__ void __launch_bounds__(64 * (C / 16)) __attribute__((amdgpu_waves_per_eu(2))) intra_kernel(IntraArgs a) {
   using L = IntraLayout<C>;
   constexpr int NB = L::NB, LDD = L::LDD, LDO = L::LDO;
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -120,47 +113,12 @@ __global__ void __launch_bounds__(64 * (C / 16)) intra_kernel(IntraArgs a) {
 
   const int n = blockIdx.x, bh = blockIdx.y;
   const int w = wave_id(), l = lane_id(), g16 = l >> 4, j16 = l & 15;
-  const int K = a.K, V = a.V, T_ = a.T;
+  const int K = a.K, T_ = a.T;
   const int t0 = n * C, rv = min(C, T_ - t0);
   const int esz = sizeof(T);
 
-  // ---- 1. dP rows of block w: blocks (w, J <= w) of dO V^T
-  {
-    const T *dOc = (const T *)a.dO + ((int64_t)bh * T_ + t0) * V;
-    const T *vc = (const T *)a.v + ((int64_t)bh * T_ + t0) * V;
-    const uint32_t vb = rsrc_bytes((int64_t)(T_ - t0) * V * esz);
-    const auto rs_do = make_rsrc(dOc, vb), rs_v = make_rsrc(vc, vb);
-    f4 acc[NB];
-#pragma unroll
-    for (int J = 0; J < NB; ++J) acc[J] = zero4();
-    const uint32_t arow = (uint32_t)((16 * w + j16) * V) * esz;
-#pragma unroll 2
-    for (int s = 0; s < (V + 31) / 32; ++s) {
-      const int col = 32 * s + 8 * g16;
-      const bool cv = col < V;  // V is a multiple of 16: a lane's 8 columns are all inside or outside
-      const uint32_t co = (uint32_t)col * esz;
-      const frag_t<T> af = ld_frag<T>(rs_do, cv ? arow + co : 0x80000000u);
-#pragma unroll
-      for (int J = 0; J < NB; ++J) {
-        if (J <= w) {
-          const uint32_t brow = (uint32_t)((16 * J + j16) * V) * esz;
-          acc[J] = mma<T>(acc[J], af, ld_frag<T>(rs_v, cv ? brow + co : 0x80000000u));
-        }
-      }
-    }
-    // rows 16 w + 4 g16 + r, column 16 J + j16; the causal mask inside the
-    // diagonal block, zeros right of it
-#pragma unroll
-    for (int J = 0; J < NB; ++J)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = 4 * g16 + r;
-        const float x = (J < w || (J == w && j16 <= row)) ? acc[J][r] : 0.f;
-        sdP[(16 * w + row) * LDD + 16 * J + j16] = x;
-      }
-  }
-
-  // ---- 2. feature groups
+  // ---- inputs of the feature groups (lane = feature): the next group's rows
+  // of q, k and the gate are always in flight one group ahead
   const int lrow = a.sg ? 1 : K;  // gate elements per step
   const T *qc = (const T *)a.q + ((int64_t)bh * T_ + t0) * K;
   const T *kc = (const T *)a.k + ((int64_t)bh * T_ + t0) * K;
@@ -169,25 +127,61 @@ __global__ void __launch_bounds__(64 * (C / 16)) intra_kernel(IntraArgs a) {
   // an absent gate (alpha = 1) reads as log alpha = 0 from an empty range
   const auto rs_la = make_rsrc(a.la ? (const T *)a.la + ((int64_t)bh * T_ + t0) * lrow : qc,
                                a.la ? rsrc_bytes((int64_t)(T_ - t0) * lrow * esz) : 0u);
-  const auto rs_dqi = make_rsrc((T *)a.dqi + ((int64_t)bh * T_ + t0) * K, kbytes);
+  const auto rs_dq = make_rsrc((T *)a.dq + ((int64_t)bh * T_ + t0) * K, kbytes);
   const auto rs_dki = make_rsrc((T *)a.dki + ((int64_t)bh * T_ + t0) * K, kbytes);
   const auto rs_dai = make_rsrc((T *)a.dai + ((int64_t)bh * T_ + t0) * K, kbytes);
   float *datc = a.dat + ((int64_t)bh * a.N + n) * K;
   const int NG = (K + 63) / 64;
 
-  for (int gi = 0; gi < NG; ++gi) {
+  const auto rs_dqr = make_rsrc(a.dqr + ((int64_t)bh * T_ + t0) * K, rsrc_bytes((int64_t)(T_ - t0) * K * 4));
+  uint32_t nq[16], nk[16], nl[16];
+  auto issue_group = [&](int gi) {
     const int f = 64 * gi + l;
     const bool fv = f < K;
-    // the block's rows of q, k and the gate, for this lane's feature
-    uint32_t rq[16], rk[16], rl[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int row = 16 * w + r;
       const uint32_t off = fv ? (uint32_t)((row * K + f) * esz) : 0x80000000u;
-      rq[r] = ld_el<T>(rs_q, off);
-      rk[r] = ld_el<T>(rs_k, off);
-      rl[r] = ld_el<T>(rs_la, a.sg ? (fv ? (uint32_t)(row * esz) : 0x80000000u) : off);
+      nq[r] = ld_el<T>(rs_q, off);
+      nk[r] = ld_el<T>(rs_k, off);
+      nl[r] = ld_el<T>(rs_la, a.sg ? (fv ? (uint32_t)(row * esz) : 0x80000000u) : off);
     }
+  };
+  issue_group(0);
+
+  // ---- 1. the chunk's dP, transposed back into rows (thread: C/4
+  // consecutive t of one s)
+  {
+    constexpr int PER = C / 4;  // floats per thread: C * C over 64 NB = 4 C threads
+    const int e0 = (int)threadIdx.x * PER, sc = e0 / C, tb = e0 % C;
+    const float *src = a.dP + ((int64_t)bh * a.N + n) * C * C + e0;
+#pragma unroll
+    for (int u = 0; u < PER; u += 4) {
+      const f4 x = *(const f4 *)(src + u);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sdP[(tb + u + r) * LDD + sc] = x[r];
+    }
+  }
+
+  // ---- 2. feature groups
+  for (int gi = 0; gi < NG; ++gi) {
+    const int f = 64 * gi + l;
+    const bool fv = f < K;
+    // the block's rows of q, k and the gate, for this lane's feature (loaded
+    // one group ahead); then the next group's go out (unconditionally: the
+    // last group re-reads itself, keeping the wait counts exact)
+    uint32_t rq[16], rk[16], rl[16], rr[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      rq[r] = nq[r];
+      rk[r] = nk[r];
+      rl[r] = nl[r];
+    }
+    issue_group(min(gi + 1, NG - 1));
+    // dq_inter of this group's rows: needed only at the combine
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      rr[r] = __builtin_amdgcn_raw_buffer_load_b32(rs_dqr, fv ? (uint32_t)(((16 * w + r) * K + f) * 4) : 0x80000000u, 0, 0);
     float q[16], kk[16], c[16];
     float run = 0.f;
 #pragma unroll
@@ -312,7 +306,7 @@ __global__ void __launch_bounds__(64 * (C / 16)) intra_kernel(IntraArgs a) {
       const float dq = __expf(c[r]) * oqw[l * LDO + r] + dqp[r];
       const float dk = __expf(tot - c[r]) * okw[l * LDO + r] + dkp[r];
       const uint32_t off = fv ? (uint32_t)((row * K + f) * esz) : 0x80000000u;
-      st_el<T>(rs_dqi, off, dq);
+      st_el<T>(rs_dq, off, __builtin_bit_cast(float, rr[r]) + dq);
       st_el<T>(rs_dki, off, dk);
       dA[r] = q[r] * dq - kk[r] * dk;
     }
@@ -364,12 +358,12 @@ size_t lds_bwd_intra(const Shape &s) {
   return s.C == 16 ? IntraLayout<16>::total : (s.C == 32 ? IntraLayout<32>::total : IntraLayout<64>::total);
 }
 
-hipError_t launch_bwd_intra(const Shape &s, const void *q, const void *k, const void *la, const void *v,
-                            const void *dO, const Work &w, hipStream_t st) {
+hipError_t launch_bwd_intra(const Shape &s, const void *q, const void *k, const void *la, void *dq, const Work &w,
+                            hipStream_t st) {
   IntraArgs a;
-  a.q = q; a.k = k; a.la = la; a.v = v; a.dO = dO;
-  a.dqi = w.dqi; a.dki = w.dki; a.dai = w.dai; a.dat = w.dat;
-  a.T = s.T; a.K = s.K; a.V = s.V; a.C = s.C; a.N = s.N;
+  a.q = q; a.k = k; a.la = la; a.dP = w.dP; a.dqr = w.dqr; a.dq = dq;
+  a.dki = w.dki; a.dai = w.dai; a.dat = w.dat;
+  a.T = s.T; a.K = s.K; a.C = s.C; a.N = s.N;
   a.sg = s.sgate ? 1 : 0;
   a.inv_tau = s.inv_tau;
   return s.io == IO_BF16 ? launch_intra_io<bf16>(s, a, st) : launch_intra_io<float>(s, a, st);

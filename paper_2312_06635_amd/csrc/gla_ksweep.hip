@@ -5,14 +5,18 @@
 // Per chunk n (S_[n] = state before the chunk, dS_[n+1] = dL/dS after it, B =
 // chunk-local inclusive cumsum of log alpha, Lambda = exp(B), Gamma =
 // exp(B_last - B)):
-//   dq_sweep (forward):  dq_inter = Lambda (.) (dO S_[n]^T),  dq = dq_inter + dq_intra
+//   dq_sweep (forward):  dq_inter = Lambda (.) (dO S_[n]^T)      (dq = dq_inter + dq_intra)
 //                        S_[n+1] = Diag(gamma) S_[n] + (K (.) Gamma)^T V
 //   dk_sweep (reverse):  dk_inter = Gamma (.) (V dS_[n+1]^T), dk = dk_inter + dk_intra
 //                        dS_[n] = Diag(gamma) dS_[n+1] + (Q (.) Lambda)^T dO
 //                        dlog alpha = revcumsum(q (.) dq - k (.) dk) + rowsum(S_T (.) dS_T)
 // The intra-chunk terms (dq_intra, dk_intra and their share of the gate
 // gradient) depend on no state; gla_intra.hip computes them chunk-parallel
-// and the sweeps add them per (row, feature).
+// between the two sweeps: it adds dq_intra to the dq sweep's dq_inter and
+// hands dk_intra and the gate-gradient share to the dk sweep.  Their one
+// d_v-reducing input, dP = (dO V^T) (.) M, is formed here in the dq sweep,
+// which streams V and dO through LDS anyway: for chunk n by the key tile
+// n mod (number of key tiles) only, so each tile takes an equal share.
 // dq, dk and the gate gradient reduce over d_v, so a workgroup owns 32 key
 // features of one head for the whole sequence and holds the transposed state
 // (value rows x 32 features, fp32) in matrix-core accumulators.
@@ -61,11 +65,12 @@ typedef float f16v __attribute__((ext_vector_type(16)));
 
 struct KsArgs {
   const void *q, *k, *la, *v, *dO;
-  const void *dqi, *dki, *dai;  // intra-chunk dq, dk and in-chunk dA sums [BH][T][K] io (gla_intra.hip)
+  const void *dki, *dai;        // intra-chunk dk and in-chunk dA sums [BH][T][K] io (gla_intra.hip)
   const float *dat;             // [BH][N][K] chunk totals of the intra-chunk dA
   const float *S0, *dST;
-  void *dq, *dk, *dla;
-  float *dqr;                   // [BH][T][K] fp32 dq_inter: written by the dq sweep, read by the dk sweep
+  void *dk, *dla;
+  float *dqr;                   // [BH][T][K] fp32 dq_inter: written by the dq sweep
+  float *dP;                    // [BH][N][C][C] fp32 (dO V^T) (.) M per chunk, stored transposed ([s][t])
   float *cST;
   float *dla_part;  // scalar gate: [BH][KT][T] per-tile feature sums of the gate gradient
   const float *gbv; // general form: [BH][N][V] chunk decays exp(E_last) of the value-side gate
@@ -425,6 +430,7 @@ template <typename T, int CP, int NSL, bool PRE, bool GB>
 __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   using L = KsLayout<T, CP>;
   constexpr int VS = L::VS, NB = L::NB, NRG = L::NRG, NST = CP / 16, NTT = CP / 32;
+  constexpr int NDT = CP == 64 ? 3 : 1;  // dP tiles on or below the diagonal, one per wave 0..NDT-1
   constexpr bool SPLIT = sizeof(T) == 2;
   static_assert(VS * sizeof(T) == kRowB, "slab row size");
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -463,7 +469,6 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   const int lrow = a.sg ? 1 : K;  // gate elements per step
   const T *kh_ = (const T *)a.k + (int64_t)bh * a.T * K, *lah = (const T *)a.la + (int64_t)bh * a.T * lrow;
   const T *vh = (const T *)a.v + (int64_t)bh * a.T * V, *dOh = (const T *)a.dO + (int64_t)bh * a.T * V;
-  const T *dqih = (const T *)a.dqi + (int64_t)bh * a.T * K;
   uint32_t eoff[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -472,7 +477,7 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   }
   // (C is a multiple of 4: a thread's four rows are all inside or all outside)
   const uint32_t sbase = (fthr && 4 * frg < C && fv) ? (uint32_t)(4 * frg * esz) : 0x80000000u;
-  uint32_t fin_la[4], fin_k[4], fin_dqi[4];
+  uint32_t fin_la[4], fin_k[4];
   // general form: the chunk's gb row (value v held by thread v mod 512)
   float gbr[2];
   auto fetch_gb = [&](int n) {
@@ -492,12 +497,10 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
     const auto rs_la = make_rsrc(a.la ? lah + (int64_t)t0 * lrow : kh_,
                                  a.la ? rsrc_bytes((int64_t)(a.T - t0) * lrow * esz) : 0u);
     const auto rs_k = make_rsrc(kh_ + (int64_t)t0 * K, bytes);
-    const auto rs_i = make_rsrc(dqih + (int64_t)t0 * K, bytes);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       fin_la[i] = ld_elem<T>(rs_la, gate_off<T>(a.sg, eoff[i], sbase, i));
       fin_k[i] = ld_elem<T>(rs_k, eoff[i]);
-      fin_dqi[i] = ld_elem<T>(rs_i, eoff[i]);
     }
     if constexpr (GB) fetch_gb(n);
   };
@@ -514,8 +517,15 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
     else pd.load(make_rsrc(dOh + (int64_t)t0 * V + c0, bytes), V - c0);
   };
 
-  T *dqo = (T *)a.dq + (int64_t)bh * a.T * K;
   float *dqro = a.dqr + (int64_t)bh * a.T * K;
+  float *dPg = a.dP + (int64_t)bh * N * C * C;
+  // dP tiles: waves 0..NDT-1 each accumulate one whole 32x32 tile (t rows
+  // 32 tr.., s columns 32 tc..: T00, T10, T11) over every slab of the chunks
+  // this key tile forms dP for; wave NDT writes the zero tile above the diagonal
+  const bool dpw = w < NDT;
+  const int tr = (w == 1 || w == 2) ? 1 : 0, tc = w == 2 ? 1 : 0;
+  const int pA = lb0 + 32 * tr * kRowB, pB = lb0 + 32 * tc * kRowB;
+  const int pA1 = lb1 + 32 * tr * kRowB, pB1 = lb1 + 32 * tc * kRowB;
 
   fetch_factors(0);
   fetch_slab(0, 0);
@@ -524,14 +534,11 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   for (int n = 0; n < N; ++n) {
     const int t0 = n * C, rv = min(C, a.T - t0);
     // ---- factors: cumsum of log alpha, gated operands
-    float c[4], kv[4], dqi[4];
+    float c[4], kv[4];
     {
       float x[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        x[i] = elem_f<T>(fin_la[i]);
-        dqi[i] = elem_f<T>(fin_dqi[i]);
-      }
+      for (int i = 0; i < 4; ++i) x[i] = elem_f<T>(fin_la[i]);
       if constexpr (PRE) {  // gate epilogue
 #pragma unroll
         for (int i = 0; i < 4; ++i) x[i] = gate_la(x[i], a.inv_tau, fthr && fv && 4 * frg + i < rv);
@@ -569,11 +576,13 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
     fetch_factors(min(n + 1, N - 1));
     __syncthreads();
 
-    // ---- slabs: dq_inter partials (state before the chunk), update
+    // ---- slabs: dq_inter partials (state before the chunk), update (and, for
+    // one chunk in KT, the dP tiles)
     const float gam = sG[j];
-    f16v acc[2];
+    const bool mine = n % a.KT == kt;  // this key tile forms the chunk's dP
+    f16v acc[2], accP;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) acc[0][e] = acc[1][e] = 0.f;
+    for (int e = 0; e < 16; ++e) acc[0][e] = acc[1][e] = accP[e] = 0.f;
 #pragma unroll
     for (int sl = 0; sl < NSL; ++sl) {
       const int q = n * NSL + sl;
@@ -596,22 +605,34 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
           }
           S[sl] *= gam;
         }
-        // the state update S^T <- gamma S^T + V^T (K (.) Gamma); the next
-        // slab's loads are issued in two halves between its products (pinned
-        // by scheduling barriers) so that the memory pipeline drains meanwhile
+        // dP = dO V^T for this wave's tile (waves 0..NDT-1, chunks of this
+        // key tile only), interleaved with the state update S^T <- gamma S^T
+        // + V^T (K (.) Gamma) so that the two independent accumulation chains
+        // hide each other's operand reads; the next slab's loads are issued
+        // in two halves between these products (pinned by scheduling
+        // barriers) so that the memory pipeline drains meanwhile
+        constexpr int NDS = VS / 16;    // dP steps per slab
+        constexpr int UPD = NDS / NST;  // dP steps per update step
+        auto slab_products = [&](auto with_dp) {
 #pragma unroll
-        for (int u = 0; u < NST; ++u) {
-          if (u == 0 || u == NST / 2) {
-            __builtin_amdgcn_sched_barrier(0);
-            fetch_slab(q + 1, u == 0 ? 0 : 1);
-            __builtin_amdgcn_sched_barrier(0);
+          for (int st = 0; st < NDS; ++st) {
+            if constexpr (decltype(with_dp)::value)
+              accP = mma32<T>(accP, ld_slab_row<T>(sD, pA, pA1, 0, 16 * st), ld_slab_row<T>(sV, pB, pB1, 0, 16 * st));
+            if (st == 0 || st == NDS / 2) {
+              __builtin_amdgcn_sched_barrier(0);
+              fetch_slab(q + 1, st == 0 ? 0 : 1);
+              __builtin_amdgcn_sched_barrier(0);
+            }
+            if (sw && (st + 1) % UPD == 0) {
+              const int u = (st + 1) / UPD - 1;
+              const frag_t<T> av = ld_slab_col_perm<T>(sV, lt0, lt1, 16 * u, 32 * w);
+              S[sl] = mma32<T>(S[sl], av, ld_row32<T>(sBh, L::LDTB, 0, 16 * u));
+              if constexpr (SPLIT) S[sl] = mma32<T>(S[sl], av, ld_row32<T>(sBl, L::LDTB, 0, 16 * u));
+            }
           }
-          if (sw) {
-            const frag_t<T> av = ld_slab_col_perm<T>(sV, lt0, lt1, 16 * u, 32 * w);
-            S[sl] = mma32<T>(S[sl], av, ld_row32<T>(sBh, L::LDTB, 0, 16 * u));
-            if constexpr (SPLIT) S[sl] = mma32<T>(S[sl], av, ld_row32<T>(sBl, L::LDTB, 0, 16 * u));
-          }
-        }
+        };
+        if (dpw && mine) slab_products(std::true_type{});
+        else slab_products(std::false_type{});
         if constexpr (GB) {
           // S_[n+1] = (gamma S_[n] + K~^T Vh) gb, by value row
           static_assert(L::offOr % 16 == 0, "aligned factor rows");
@@ -626,27 +647,40 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
       __syncthreads();
     }
 
+    // ---- dP of this key tile's chunks: masked, handed over transposed ([s][t])
+    if (mine && (dpw || (CP == 64 && w == NDT))) {
+      const bool zero_tile = !dpw;
+      const int rt = zero_tile ? 0 : tr, ct = zero_tile ? 1 : tc;
+      const int col = 32 * ct + j;
+      const auto rs_dp = make_rsrc(dPg + (int64_t)n * C * C, (uint32_t)(C * C * 4));
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int t4 = 32 * rt + 8 * b + 4 * g;
+        f4 v4;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v4[r] = (zero_tile || col > t4 + r) ? 0.f : accP[4 * b + r];
+        const uint32_t off = (t4 < C && col < C) ? (uint32_t)((col * C + t4) * 4) : 0x80000000u;
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v4), rs_dp, off, 0, 0);
+      }
+    }
     // ---- dq_inter partials, pre-scaled by exp(log decay before the block)
     partials_publish<L>(acc, sSc, sRed, w, g, j);
     __syncthreads();
     partials_add<L>(acc, sRed, w, g, j);
     __syncthreads();
 
-    // ---- dq_inter = Lambda (.) inter; dq = dq_inter + dq_intra, per (row, feature)
+    // ---- dq_inter = Lambda (.) inter, per (row, feature)
     if (fthr) {
       f4 in4 = *(const f4 *)(sRed + fk * L::LDT + 4 * frg);
 #pragma unroll
       for (int p = 1; p < L::NP; ++p) in4 += *(const f4 *)(sRed + (p * kKF + fk) * L::LDT + 4 * frg);
       const f4 bl4 = *(const f4 *)(sBloc + fk * L::LDT + 4 * frg);
-      const uint32_t obytes = rsrc_bytes((int64_t)(a.T - t0) * K * esz);
-      const auto rs_dq = make_rsrc(dqo + (int64_t)t0 * K, obytes);
       const auto rs_dqr = make_rsrc(dqro + (int64_t)t0 * K, rsrc_bytes((int64_t)(a.T - t0) * K * 4));
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float dqe = __expf(bl4[i]) * in4[i];
         // rows past the sequence end, past the chunk or of absent features
         // fall outside the buffer range and are dropped
-        st_elem<T>(rs_dq, eoff[i], cvt<T>(dqe + dqi[i]));
         __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, dqe), rs_dqr,
                                               eoff[i] == 0x80000000u ? eoff[i] : eoff[i] / esz * 4, 0, 0);
       }
@@ -1088,11 +1122,11 @@ size_t ks_state_bytes(const Shape &s) {
 size_t lds_bwd_dk(const Shape &s) { return ks_lds(s); }
 
 hipError_t launch_bwd_dq(const Shape &s, const void *k, const void *la, const void *v,
-                         const float *S0, const void *dO, const float *dST, void *dq,
+                         const float *S0, const void *dO, const float *dST,
                          const Work &w, hipStream_t st, bool gb_on) {
   KsArgs a = ks_args(s);
-  a.k = k; a.la = la; a.v = v; a.dO = dO; a.S0 = S0; a.dST = dST; a.dq = dq; a.dqr = w.dqr;
-  a.dqi = w.dqi; a.cST = w.cST;
+  a.k = k; a.la = la; a.v = v; a.dO = dO; a.S0 = S0; a.dST = dST; a.dqr = w.dqr;
+  a.dP = w.dP; a.cST = w.cST;
   if (gb_on) { a.gbv = w.gb; a.Sb = w.Sb; }
   return dispatch_ks<true>(s, a, st);
 }

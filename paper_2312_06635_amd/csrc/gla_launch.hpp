@@ -24,12 +24,12 @@ struct Work {
   void *Kt = nullptr;     // [BH][T][K] io : k (.) Gamma    (Gamma  = b_{chunk end} / b_t)
   void *P = nullptr;      // [BH][N][C][C] io : intra-chunk matrix, lower triangle
   float *gam = nullptr;   // [BH][N][K] fp32 : chunk decay gamma = b_{chunk end} / b_{chunk start}
-  // backward: the intra-chunk terms (gla_intra.hip) and the dq sweep's hand-off
-  void *dqi = nullptr;    // [BH][T][K] io : intra-chunk part of dq
+  // backward: the dq sweep's hand-offs and the intra-chunk terms (gla_intra.hip)
+  float *dP = nullptr;    // [BH][N][C][C] fp32 : (dO V^T) (.) M per chunk, transposed ([s][t])
   void *dki = nullptr;    // [BH][T][K] io : intra-chunk part of dk
   void *dai = nullptr;    // [BH][T][K] io : in-chunk reverse cumsum of q dq_intra - k dk_intra
   float *dat = nullptr;   // [BH][N][K] fp32 : its chunk totals
-  float *dqr = nullptr;   // [BH][T][K] fp32 : dq_inter, for the gate gradient in the dk sweep
+  float *dqr = nullptr;   // [BH][T][K] fp32 : dq_inter (for dq and the gate gradient in the dk sweep)
   float *cST = nullptr;   // [BH][K] fp32 : rowsum(S_T (.) dS_T) (backward)
   float *dla_part = nullptr;  // [BH][ceil(K/32)][T] fp32 : per key tile sums of the gate
                               //   gradient over its features (scalar gate only)
@@ -55,17 +55,17 @@ hipError_t launch_prep(const Shape &s, const void *q, const void *k, const void 
 hipError_t launch_fwd_main(const Shape &s, const void *v, const void *lb, const float *S0, void *o, float *ST,
                            const Work &w, hipStream_t st);
 // gb_on: the general form (v, dO are then w.Vh, w.Oh; the states decay by w.gb)
-// The intra-chunk terms of the backward (w.dqi, w.dki, w.dai, w.dat); v, dO
-// are Vh, Oh in the general form.
-hipError_t launch_bwd_intra(const Shape &s, const void *q, const void *k, const void *la, const void *v,
-                            const void *dO, const Work &w, hipStream_t st);
+// The dq sweep: w.dqr (dq_inter), w.dP, w.cST.
 hipError_t launch_bwd_dq(const Shape &s, const void *k, const void *la, const void *v,
-                         const float *S0, const void *dO, const float *dST, void *dq,
+                         const float *S0, const void *dO, const float *dST,
                          const Work &w, hipStream_t st, bool gb_on = false);
+// The intra-chunk terms of the backward, after the dq sweep: dq, and w.dki,
+// w.dai, w.dat for the dk sweep.
+hipError_t launch_bwd_intra(const Shape &s, const void *q, const void *k, const void *la, void *dq, const Work &w,
+                            hipStream_t st);
 hipError_t launch_bwd_dk(const Shape &s, const void *q, const void *k, const void *la,
                          const void *v, const void *dO, const float *dST, const void *dq,
                          void *dk, void *dla, const Work &w, hipStream_t st, bool gb_on = false);
-// (the dq sweep also writes w.dqr and w.cST; the dk sweep reads them)
 // lb: log beta of the general form (nullable)
 hipError_t launch_bwd_dv(const Shape &s, const void *dO, const void *lb, const float *dST, void *dv, float *dS0,
                          const Work &w, hipStream_t st);
