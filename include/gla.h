@@ -10,9 +10,11 @@
  * S_0 = S0 (zero, or the final state of the previous segment: Sec. 2.2).  The
  * library evaluates it in the chunkwise form of Sec. 4.2 with the secondary
  * (sub-chunk) tiling of Sec. 4.3: an inter-chunk state pass, attention-like
- * intra-chunk blocks (bf16 matrix-core products between sub-chunks, fp32
- * log-space evaluation inside a sub-chunk), and the closed-form gate gradient
- * of Sec. 4.3 in the backward.
+ * intra-chunk blocks (bf16 matrix-core products between sub-chunks, with
+ * normalisers at the sub-chunk boundaries; inside a sub-chunk, Eq. 4 itself
+ * in fp32 on the vector ALUs: one exponential of the log-space difference
+ * per pair and feature), and the closed-form gate gradient of Sec. 4.3 in
+ * the backward.
  *
  * Conventions shared by every entry point
  *   - Tensors are device pointers, contiguous row-major:
@@ -39,8 +41,8 @@
  *     exception crosses this boundary.
  *   - Domain: log_alpha must be finite and <= 0 (alpha in (0, 1], Sec. 4.1);
  *     log_alpha = 0 (alpha = 1) gives ungated linear attention (Sec. 2.1).
- *     Very negative values are handled (the intra-sub-chunk decays fall back
- *     to pairwise exponentials when a sub-chunk's decay range is large).
+ *     Steep gates are exact: every exponent the kernels evaluate is <= 0
+ *     (tested with per-step log alpha down to -50).
  *   - There is no scale argument (Eq. 3 has none): pre-scale k if desired.
  *
  * Few heads, long sequences: when B*H is too small to fill the GPU and T is
@@ -56,10 +58,15 @@
  * up to one chunk per segment (materialized chunk states).  The general form
  * (value-side gate) is never segmented.
  *
- * Supported shapes: B*H <= 65535; d_k and d_v multiples of 16 with d_k <= 256 and
- * d_v <= 1024 (fp32 io additionally needs d_k <= 128); chunk C in {16, 32, 64}; sub-chunk c a divisor of 16 that also
- * divides C; any T >= 0 (a last, shorter chunk is handled by masking).
- * Other values return GLA_ERR_UNSUPPORTED.
+ * Supported shapes: B*H <= 65535; d_k and d_v multiples of 16 with d_k <= 256
+ * and d_v <= 1024 (fp32 io additionally needs d_k <= 128); chunk C in
+ * {16, 32, 64}; sub-chunk c a divisor of 16 that also divides C; any T >= 0
+ * (a last, shorter chunk is handled by masking) with at most 65535 chunks
+ * (T <= 65535 C) in the chunkwise calls and T * max(d_k, d_v) < 2^29 per
+ * head.  Other values return GLA_ERR_UNSUPPORTED.  The kernels tile every
+ * chunk in 16-row sub-chunk blocks: a sub-chunk length c < 16 lies inside
+ * those blocks, whose fp32 evaluation does not depend on c, so every c that
+ * divides 16 gives the same results (bit for bit).
  */
 #ifndef GLA_H_
 #define GLA_H_
@@ -103,15 +110,11 @@ enum {
    * point honours it, gla_workspace_bytes included (the backward then needs
    * B H ceil(d_k/32) T fp32 more). */
   GLA_FLAG_SCALAR_GATE = 1u << 1,
-  /* Every diagonal (within one sub-chunk) block of the intra-chunk terms,
-   * forward and backward, in fp32 log space: one exponential exp(B_i - B_j)
-   * per pair and feature on the vector ALUs, as the paper prescribes for these
-   * blocks (Sec. 4.3).  Without it they run on the matrix cores through the
-   * factorised decay exp(B_i - z) exp(z - B_j) with bf16 operands, and only
-   * blocks whose decay range is too wide for that fall back to the fp32 form.
-   * Slower; results differ at rounding level.  The chunkwise calls honour it
-   * (a backward that reuses a forward's workspace takes P as that forward
-   * formed it); the recurrent calls ignore it. */
+  /* Accepted for compatibility and without effect: every diagonal (within
+   * one sub-chunk) block of the intra-chunk terms, forward and backward, is
+   * always evaluated in fp32 log space, one exponential exp(B_i - B_j) per
+   * pair and feature on the vector ALUs, as the paper prescribes for these
+   * blocks (Sec. 4.3).  Results are bit-identical with and without it. */
   GLA_FLAG_FP32_DIAGONAL = 1u << 2,
   /* Bits 8..11 select a single stage of an entry point's launch sequence (0 =
    * the whole sequence), so that a profiler or benchmark can time each kernel
@@ -120,9 +123,12 @@ enum {
    *   gla_chunk_fwd: 1 = gate factors, gated operands and intra-chunk P
    *                  2 = state pass and chunk outputs
    *   gla_chunk_bwd: 1 = as forward stage 1 (skipped with REUSE_FWD_WORKSPACE)
-   *                  2 = forward sweep over key-feature tiles: dq (and dP)
-   *                  3 = reverse sweep over key-feature tiles: dk, dlog_alpha
-   *                  4 = reverse sweep over value-column tiles: dv, dS0
+   *                  2 = forward sweep over key-feature tiles: dq_inter
+   *                      (and dP = (dO V^T) (.) M)
+   *                  3 = intra-chunk terms, chunk-parallel: dq, and dk_intra
+   *                      and its share of the gate gradient for stage 4
+   *                  4 = reverse sweep over key-feature tiles: dk, dlog_alpha
+   *                  5 = reverse sweep over value-column tiles: dv, dS0
    * Out-of-range stage numbers return GLA_ERR_SHAPE. */
   GLA_STAGE_SHIFT = 8,
   GLA_STAGE_MASK = 0xFu << 8,
@@ -246,8 +252,8 @@ gla_status gla_recurrent_fwd_general(const gla_problem *prob, const void *q, con
  * the gate epilogue (gate_tau > 0: GLA_ERR_UNSUPPORTED).  Workspace: at least
  * gla_workspace_bytes(prob, 2) bytes; GLA_FLAG_REUSE_FWD_WORKSPACE as for
  * gla_chunk_bwd.  Stage selector: 1 = key-gate factors (as gla_chunk_bwd),
- * 2 = value-gate operands, 3 = dq sweep, 4 = dk sweep, 5 = dv sweep, 6 = the
- * value-gate gradient. */
+ * 2 = value-gate operands, 3 = dq sweep, 4 = intra-chunk terms, 5 = dk sweep,
+ * 6 = dv sweep, 7 = the value-gate gradient. */
 gla_status gla_chunk_bwd_general(const gla_problem *prob, const void *q, const void *k, const void *v,
                                  const void *log_alpha, const void *log_beta, const float *S0, const void *o,
                                  const void *dO, const float *dS_T, void *dq, void *dk, void *dv,

@@ -17,8 +17,9 @@ constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 // Validates the problem and fills the internal shape.  The rules are the
-// supported-shape list of include/gla.h.
-gla_status make_shape(const gla_problem *p, Shape &s) {
+// supported-shape list of include/gla.h.  chunked: a chunkwise call (the
+// recurrent calls have no chunk grid, so no limit on the chunk count).
+gla_status make_shape(const gla_problem *p, Shape &s, bool chunked = true) {
   if (!p) return GLA_ERR_NULL;
   if (p->io != GLA_F32 && p->io != GLA_BF16) return GLA_ERR_DTYPE;
   if (p->B < 0 || p->H < 0 || p->T < 0 || p->dk <= 0 || p->dv <= 0 || p->chunk <= 0 ||
@@ -42,7 +43,7 @@ gla_status make_shape(const gla_problem *p, Shape &s) {
   if (!(p->gate_tau == 0.f || (p->gate_tau > 0.f && p->gate_tau < 3.0e38f))) return GLA_ERR_SHAPE;
   s.inv_tau = p->gate_tau == 0.f ? 0.f : 1.f / p->gate_tau;
   s.sgate = (p->flags & GLA_FLAG_SCALAR_GATE) != 0;
-  if (s.N > 65535) return GLA_ERR_UNSUPPORTED;
+  if (chunked && s.N > 65535) return GLA_ERR_UNSUPPORTED;  // chunks are a grid dimension
   // one head's rows of any tensor must span less than 2 GiB (32-bit buffer offsets)
   const int64_t wmax = p->dk > p->dv ? p->dk : p->dv;
   // (fp32 workspace rows included: 4 bytes per element)
@@ -238,7 +239,7 @@ gla_status recurrent_fwd(const gla_problem *prob, const void *q, const void *k, 
   p.chunk = 16;  // the recurrent form ignores the chunk fields
   p.subchunk = 16;
   Shape s;
-  gla_status st = make_shape(&p, s);
+  gla_status st = make_shape(&p, s, false);
   if (st != GLA_OK) return st;
   if (!log_alpha) s.inv_tau = 0.f;  // no gate: alpha = 1 whatever gate_tau says
   const bool any = (int64_t)s.BH * s.T > 0;
