@@ -87,6 +87,41 @@ template <typename T> __device__ __forceinline__ f4 mma3(f4 acc, const f8 &a, co
   }
 }
 
+// An fp32 operand of mma3, split once when it is reused: bf16 hi + lo (the
+// fp32 path keeps the value itself in hi).
+template <typename T> struct Split {
+  frag_t<T> hi, lo;
+};
+template <typename T> __device__ __forceinline__ Split<T> split8(const f8 &a) {
+  Split<T> r;
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      r.hi[i] = cvt<T>(a[i]);
+      r.lo[i] = cvt<T>(a[i] - (float)r.hi[i]);
+    }
+  } else {
+    r.hi = a;
+  }
+  return r;
+}
+// mma3 with the first operand already split.
+template <typename T> __device__ __forceinline__ f4 mma3s(f4 acc, const Split<T> &a, const f8 &b) {
+  if constexpr (sizeof(T) == 2) {
+    frag_t<T> bh, bl;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      bh[i] = cvt<T>(b[i]);
+      bl[i] = cvt<T>(b[i] - (float)bh[i]);
+    }
+    acc = mma<T>(acc, a.hi, bh);
+    acc = mma<T>(acc, a.hi, bl);
+    return mma<T>(acc, a.lo, bh);
+  } else {
+    return mma<T>(acc, a.hi, b);
+  }
+}
+
 template <int C> struct IntraLayout {
   static constexpr int NB = C / 16;
   static constexpr int LDD = C + 4;   // dP rows; per-feature rows of the group tiles
@@ -117,8 +152,8 @@ __global__ void __launch_bounds__(64 * (C / 16)) __attribute__((amdgpu_waves_per
   const int t0 = n * C, rv = min(C, T_ - t0);
   const int esz = sizeof(T);
 
-  // ---- inputs of the feature groups (lane = feature): the next group's rows
-  // of q, k and the gate are always in flight one group ahead
+  // ---- inputs of the feature groups (lane = feature): the group's rows of
+  // q, k and the gate
   const int lrow = a.sg ? 1 : K;  // gate elements per step
   const T *qc = (const T *)a.q + ((int64_t)bh * T_ + t0) * K;
   const T *kc = (const T *)a.k + ((int64_t)bh * T_ + t0) * K;
@@ -147,7 +182,6 @@ __global__ void __launch_bounds__(64 * (C / 16)) __attribute__((amdgpu_waves_per
       nl[r] = ld_el<T>(rs_la, a.sg ? (fv ? (uint32_t)(row * esz) : 0x80000000u) : off);
     }
   };
-  issue_group(0);
 
   // ---- 1. the chunk's dP, transposed back into rows (thread: C/4
   // consecutive t of one s)
@@ -163,21 +197,21 @@ __global__ void __launch_bounds__(64 * (C / 16)) __attribute__((amdgpu_waves_per
     }
   }
 
+  __syncthreads();  // the chunk's dP rows are complete
+
   // ---- 2. feature groups
   for (int gi = 0; gi < NG; ++gi) {
     const int f = 64 * gi + l;
     const bool fv = f < K;
-    // the block's rows of q, k and the gate, for this lane's feature (loaded
-    // one group ahead); then the next group's go out (unconditionally: the
-    // last group re-reads itself, keeping the wait counts exact)
+    // the block's rows of q, k and the gate, for this lane's feature
     uint32_t rq[16], rk[16], rl[16], rr[16];
+    issue_group(gi);
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       rq[r] = nq[r];
       rk[r] = nk[r];
       rl[r] = nl[r];
     }
-    issue_group(min(gi + 1, NG - 1));
     // dq_inter of this group's rows: needed only at the combine
 #pragma unroll
     for (int r = 0; r < 16; ++r)
@@ -194,8 +228,9 @@ __global__ void __launch_bounds__(64 * (C / 16)) __attribute__((amdgpu_waves_per
       kk[r] = el_f<T>(rk[r]);
     }
     const float tot = run;
+    // (block sums and group tiles are read after B2; the previous group's
+    // result tiles, which the group tiles overlay, were consumed before its B4)
     sTot[w * 64 + l] = tot;
-    __syncthreads();  // B1: block sums published; the previous group's result tiles are consumed
 
     // operands of the orange blocks, feature-major
 #pragma unroll
@@ -242,7 +277,20 @@ __global__ void __launch_bounds__(64 * (C / 16)) __attribute__((amdgpu_waves_per
     __syncthreads();  // B2: group tiles complete
 
     // orange on the matrix cores: wave w forms dq for row block I = w and dk
-    // for column block J = w, four 16-feature tiles each
+    // for column block J = w, four 16-feature tiles each.  The dP operands
+    // (the same for every tile) are split once.
+    constexpr int NSTEP = NB / 2 > 0 ? NB / 2 : 1;
+    Split<T> aq[NSTEP], ak[NSTEP];
+#pragma unroll
+    for (int s = 0; s < NB / 2; ++s) {
+      const float *ap = sdP + (16 * w + j16) * LDD + 32 * s + 8 * g16;
+      const f4 a0 = *(const f4 *)ap, a1 = *(const f4 *)(ap + 4);
+      aq[s] = split8<T>(f8{a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]});
+      f8 at;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) at[u] = sdP[(32 * s + 8 * g16 + u) * LDD + 16 * w + j16];
+      ak[s] = split8<T>(at);
+    }
     f4 oq[4], ok[4];
 #pragma unroll
     for (int ft = 0; ft < 4; ++ft) {
@@ -261,13 +309,10 @@ __global__ void __launch_bounds__(64 * (C / 16)) __attribute__((amdgpu_waves_per
         for (int b = 0; b < NB; ++b)
           if (b > J && b < w) lg += sTot[b * 64 + fl];
         const float sc = J < w ? __expf(lg) : 0.f;
-        const float *ap = sdP + (16 * w + j16) * LDD + 32 * s + 8 * g16;
         const float *bp = sKz + fl * LDD + 32 * s + 8 * g16;
-        const f4 a0 = *(const f4 *)ap, a1 = *(const f4 *)(ap + 4);
         const f4 b0 = *(const f4 *)bp, b1 = *(const f4 *)(bp + 4);
-        const f8 af = f8{a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
         const f8 bf = f8{b0[0] * sc, b0[1] * sc, b0[2] * sc, b0[3] * sc, b1[0] * sc, b1[1] * sc, b1[2] * sc, b1[3] * sc};
-        oq[ft] = mma3<T>(oq[ft], af, bf);
+        oq[ft] = mma3s<T>(oq[ft], aq[s], bf);
       }
       // dk: sum over I > w of dP_Iw^T (qz_I g_Iw)
 #pragma unroll
@@ -279,13 +324,10 @@ __global__ void __launch_bounds__(64 * (C / 16)) __attribute__((amdgpu_waves_per
         for (int b = 0; b < NB; ++b)
           if (b > w && b < I) lg += sTot[b * 64 + fl];
         const float sc = I > w ? __expf(lg) : 0.f;
-        f8 af;
-#pragma unroll
-        for (int u = 0; u < 8; ++u) af[u] = sdP[(32 * s + 8 * g16 + u) * LDD + 16 * w + j16];
         const float *bp = sQz + fl * LDD + 32 * s + 8 * g16;
         const f4 b0 = *(const f4 *)bp, b1 = *(const f4 *)(bp + 4);
         const f8 bf = f8{b0[0] * sc, b0[1] * sc, b0[2] * sc, b0[3] * sc, b1[0] * sc, b1[1] * sc, b1[2] * sc, b1[3] * sc};
-        ok[ft] = mma3<T>(ok[ft], af, bf);
+        ok[ft] = mma3s<T>(ok[ft], ak[s], bf);
       }
     }
     __syncthreads();  // B3: every wave is done with the group tiles, which the result tiles overlay

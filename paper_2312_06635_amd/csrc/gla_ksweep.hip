@@ -574,11 +574,11 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
     // unconditional (the last chunk re-reads itself) so that the wait counts
     // for the slab prefetch below stay exact
     fetch_factors(min(n + 1, N - 1));
-    __syncthreads();
+    // (no barrier here: the slab loop's first barrier also publishes the
+    // factor tiles, and gamma is read after it)
 
     // ---- slabs: dq_inter partials (state before the chunk), update (and, for
     // one chunk in KT, the dP tiles)
-    const float gam = sG[j];
     const bool mine = n % a.KT == kt;  // this key tile forms the chunk's dP
     f16v acc[2], accP;
 #pragma unroll
@@ -603,7 +603,7 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
               if constexpr (SPLIT) acc[th] = mma32<T>(acc[th], ad, slo);
             }
           }
-          S[sl] *= gam;
+          S[sl] *= sG[j];
         }
         // dP = dO V^T for this wave's tile (waves 0..NDT-1, chunks of this
         // key tile only), interleaved with the state update S^T <- gamma S^T
@@ -884,10 +884,11 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
     }
     if constexpr (GB) stage_gb();
     fetch_factors(max(n - 1, 0));  // unconditional, see the dq sweep
-    __syncthreads();
+    // the slab loop's first barrier also publishes the factor tiles (gamma is
+    // read after it); the general form reads the staged gb row before it
+    if constexpr (GB) __syncthreads();
 
     // ---- slabs: dk_inter partials (dS after the chunk), then the dS update
-    const float gam = sG[j];
     f16v acc[2];
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[0][e] = acc[1][e] = 0.f;
@@ -934,7 +935,7 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
       }
       if (sw) {
         // dS^T <- gamma dS^T + dO^T (Q (.) Lambda)
-        dS[sl] *= gam;
+        dS[sl] *= sG[j];
 #pragma unroll
         for (int st = 0; st < NST; ++st) {
           const frag_t<T> ad = ld_slab_col_perm<T>(sD, lt0, lt1, 16 * st, 32 * w);
