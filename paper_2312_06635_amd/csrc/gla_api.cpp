@@ -165,6 +165,15 @@ size_t layout(const Shape &s, int op, char *base, Work *w, int nseg) {
 
 gla_status hip_status(hipError_t e) { return e == hipSuccess ? GLA_OK : GLA_ERR_HIP; }
 
+// Without a gate the gated operands Q (.) Lambda, K (.) Gamma are q and k
+// themselves: the kernels read the inputs in their place (the prep kernel
+// then does not write them).
+void alias_ungated(Work &w, const void *log_alpha, const void *q, const void *k) {
+  if (log_alpha) return;
+  w.Qt = const_cast<void *>(q);
+  w.Kt = const_cast<void *>(k);
+}
+
 }  // namespace
 
 GLA_EXPORT const char *gla_status_string(gla_status st) {
@@ -214,6 +223,7 @@ gla_status chunk_fwd(const gla_problem *prob, const void *q, const void *k, cons
     return hip_status(gla::launch_copy_state((int64_t)s.BH * s.K * s.V, S0, S_T, hs));
   Work w;
   layout(s2, 0, (char *)workspace, &w, nseg);
+  alias_ungated(w, log_alpha, q, k);
   hipError_t e = hipSuccess;
   if (stage == 0 || stage == 1) e = gla::launch_prep(s2, q, k, log_alpha, w, hs);
   if (e == hipSuccess && (stage == 0 || stage == 2)) {
@@ -293,6 +303,7 @@ GLA_EXPORT gla_status gla_chunk_bwd(const gla_problem *prob, const void *q, cons
   auto run = [stage](unsigned k) { return stage == 0 || stage == k; };
   Work w;
   layout(s2, 1, (char *)workspace, &w, nseg);
+  alias_ungated(w, log_alpha, q, k);
   hipError_t e = hipSuccess;
   if (run(1) && !(prob->flags & GLA_FLAG_REUSE_FWD_WORKSPACE)) {
     e = gla::launch_prep(s2, q, k, log_alpha, w, hs);
@@ -350,6 +361,7 @@ GLA_EXPORT gla_status gla_chunk_bwd_general(const gla_problem *prob, const void 
   auto run = [stage](unsigned k) { return stage == 0 || stage == k; };
   Work w;
   layout(s, 2, (char *)workspace, &w, 1);
+  alias_ungated(w, log_alpha, q, k);
   hipError_t e = hipSuccess;
   if (run(1) && !(prob->flags & GLA_FLAG_REUSE_FWD_WORKSPACE))
     e = gla::launch_prep(s, q, k, log_alpha, w, hs);

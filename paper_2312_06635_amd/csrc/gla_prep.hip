@@ -378,6 +378,128 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) p
   }
 }
 
+// Scalar gates (Table 1's scalar rows, alpha_t = gamma_t 1) and the absent
+// gate (alpha = 1): the decay no longer depends on the feature, so with c the
+// chunk-local inclusive cumsum of log gamma (one value per step)
+//   Qt = q exp(c),  Kt = k exp(c_last - c),  gamma = exp(c_last) 1,
+//   P = (q k^T) (.) D,  D_ij = exp(c_i - c_j) for j <= i, else 0,
+// i.e. every block of P, the diagonal ones included, is a plain fp32-accumulated
+// matrix-core product of the io-dtype inputs scaled by one fp32 exponential
+// per entry -- no factorised operands, no block normalisers, no per-feature
+// exponentials.  NG (no gate): c = 0, so D is the causal mask, gamma = 1, and
+// Qt, Kt equal q, k: they are not written (the caller passes q and k in their
+// place to the kernels that read them).
+template <typename T, int FPL, bool PRE, bool NG>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) prep_plain_kernel(PrepArgs a) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int n = blockIdx.x, bh = blockIdx.y;
+  const int w = wave_id(), l = lane_id(), g = l >> 4, j16 = l & 15;
+  const int C = a.C, K = a.K, Kp = a.Kp, ldk = a.ldk;
+  const int t0 = n * C;
+  const int rv = min(C, a.T - t0);
+  const int64_t base = ((int64_t)bh * a.T + t0) * K;
+  T *sQ = (T *)smem;
+  T *sK = sQ + C * ldk;
+  const T *q = (const T *)a.q + base, *k = (const T *)a.k + base;
+  T *Qt = (T *)a.Qt + base, *Kt = (T *)a.Kt + base;
+  T *Pg = (T *)a.P + ((int64_t)bh * a.N + n) * C * C;
+  const int k0 = FPL * l;
+  const bool fv = k0 < K, fp = k0 < Kp;
+  constexpr int NW = (FPL * (int)sizeof(T) + 3) / 4;
+  const int esz = sizeof(T);
+  const uint32_t bytes = rsrc_bytes((int64_t)(a.T - t0) * K * esz);
+  const auto rs_q = make_rsrc(q, bytes), rs_k = make_rsrc(k, bytes);
+  const uint32_t lane_off = fv ? (uint32_t)((16 * w * K + k0) * esz) : 0x80000000u;
+  const uint32_t row_step = (uint32_t)(K * esz);
+  uint32_t rq[16][NW], rk[16][NW];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    ldraw<T, FPL>(rs_q, lane_off + r * row_step, rq[r]);
+    ldraw<T, FPL>(rs_k, lane_off + r * row_step, rk[r]);
+  }
+
+  // chunk-local inclusive cumsum of log gamma, in units of log2: lane t holds
+  // step t's (every wave forms the whole chunk's; steps past the sequence end
+  // or the chunk contribute 0)
+  float c2 = 0.f;
+  if constexpr (!NG) {
+    const T *la = (const T *)a.la + (int64_t)bh * a.T + t0;
+    const auto rs_la = make_rsrc(la, rsrc_bytes((int64_t)(a.T - t0) * esz));
+    uint32_t raw;
+    const uint32_t o1 = l < C ? (uint32_t)(l * esz) : 0x80000000u;
+    if constexpr (sizeof(T) == 2) raw = __builtin_amdgcn_raw_buffer_load_b16(rs_la, o1, 0, 0) << 16;
+    else raw = __builtin_amdgcn_raw_buffer_load_b32(rs_la, o1, 0, 0);
+    float x = __builtin_bit_cast(float, raw);
+    if constexpr (PRE) x = gate_la(x, a.inv_tau, l < rv);
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const float y = __shfl_up(x, o);
+      if (l >= o) x += y;
+    }
+    c2 = x * kLog2e;
+  }
+  const float clast2 = NG ? 0.f : __shfl(c2, C - 1);
+
+  // gated operands (scalar gates only), and the raw inputs into LDS
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int row = 16 * w + r;
+    if constexpr (!NG) {
+      const float cr = __shfl(c2, row);
+      const float eq = exp2f_fast(cr), ek = exp2f_fast(clast2 - cr);
+      float qv[FPL], kv[FPL], o1[FPL], o2[FPL];
+      unpack<T, FPL>(rq[r], qv);
+      unpack<T, FPL>(rk[r], kv);
+#pragma unroll
+      for (int f = 0; f < FPL; ++f) {
+        o1[f] = qv[f] * eq;
+        o2[f] = kv[f] * ek;
+      }
+      straw<T, FPL>(make_rsrc(Qt, bytes), lane_off + r * row_step, o1);
+      straw<T, FPL>(make_rsrc(Kt, bytes), lane_off + r * row_step, o2);
+    }
+    if (fp) {
+      float qv[FPL], kv[FPL];  // (exact round trip to the io dtype)
+      unpack<T, FPL>(rq[r], qv);
+      unpack<T, FPL>(rk[r], kv);
+      stvec<T, FPL>(sQ + row * ldk + k0, qv);
+      stvec<T, FPL>(sK + row * ldk + k0, kv);
+    }
+  }
+  if (w == 0) {
+    const float gv = exp2f_fast(clast2);
+    float *gp = a.gam + ((int64_t)bh * a.N + n) * K;
+    for (int kk = l; kk < K; kk += 64) gp[kk] = gv;
+  }
+
+  // zeros: every block J > w
+  const int d0 = 16 * w;
+  for (int idx = l; idx < 16 * (C - d0 - 16); idx += 64) {
+    const int rr = idx / (C - d0 - 16), cc = idx - rr * (C - d0 - 16);
+    Pg[(d0 + rr) * C + d0 + 16 + cc] = cvt<T>(0.f);
+  }
+  __syncthreads();
+
+  // blocks (w, J <= w): q k^T on the matrix cores, then D
+  float cr2[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) cr2[r] = NG ? 0.f : __shfl(c2, d0 + 4 * g + r);
+  for (int J = 0; J <= w; ++J) {
+    f4 acc = zero4();
+    for (int s = 0; s < Kp / 32; ++s)
+      acc = mma<T>(acc, ld_row(sQ, ldk, d0, 32 * s), ld_row(sK, ldk, 16 * J, 32 * s));
+    const int col = 16 * J + j16;
+    const float cc2 = NG ? 0.f : __shfl(c2, col);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = d0 + 4 * g + r;
+      float v = 0.f;
+      if (col <= row) v = NG ? acc[r] : acc[r] * exp2f_fast(cr2[r] - cc2);
+      Pg[row * C + col] = cvt<T>(v);
+    }
+  }
+}
+
 static int round_up(int x, int m) { return (x + m - 1) / m * m; }
 
 size_t lds_prep(const Shape &s) {
@@ -397,8 +519,22 @@ static hipError_t launch_prep_pre(const Shape &s, const PrepArgs &a, size_t lds,
   return hipGetLastError();
 }
 
+template <typename T, int FPL, bool PRE, bool NG>
+static hipError_t launch_prep_plain(const Shape &s, const PrepArgs &a, size_t lds, hipStream_t st) {
+  static const hipError_t attr = hipFuncSetAttribute((const void *)prep_plain_kernel<T, FPL, PRE, NG>,
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
+  (void)attr;
+  dim3 grid(s.N, s.BH), block(64 * (s.C / 16));
+  hipLaunchKernelGGL((prep_plain_kernel<T, FPL, PRE, NG>), grid, block, lds, st, a);
+  return hipGetLastError();
+}
+
 template <typename T, int FPL>
 static hipError_t launch_prep_t(const Shape &s, const PrepArgs &a, size_t lds, hipStream_t st) {
+  if (!a.la) return launch_prep_plain<T, FPL, false, true>(s, a, lds, st);
+  if (a.sg)
+    return a.inv_tau != 0.f ? launch_prep_plain<T, FPL, true, false>(s, a, lds, st)
+                            : launch_prep_plain<T, FPL, false, false>(s, a, lds, st);
   return a.inv_tau != 0.f ? launch_prep_pre<T, FPL, true>(s, a, lds, st)
                           : launch_prep_pre<T, FPL, false>(s, a, lds, st);
 }

@@ -239,8 +239,10 @@ def test_recurrent_forward(io):
 def test_absent_gate_is_alpha_one(io):
     """log_alpha = NULL is the ungated layer (alpha = 1, the case the FLA
     algorithms of Sec. 3.3 compute): no gate tensor is read and no gate
-    gradient written, the results are bit-identical to an all-zero gate tensor
-    and at parity with the oracle's alpha = 1 recurrence."""
+    gradient written; the results are at parity with the oracle's alpha = 1
+    recurrence and agree with the gated path fed an all-zero gate tensor (a
+    different evaluation: plain masked q k^T blocks, no decay factors), and
+    gate_tau leaves them bit for bit unchanged."""
     g = gla()
     cfg = small_case("nogate_" + io, io, 1, 2, 150, 64, 128, 64, 16, 26, s0_std=0.1)
     inp = W.make_inputs(cfg, alpha_one=True, dST_std=0.1)
@@ -263,12 +265,14 @@ def test_absent_gate_is_alpha_one(io):
     r3, R3 = g.recurrent_fwd(d["q"], d["k"], d["v"], None, S0=d["S0"], output_final_state=True, gate_tau=16.0)
     torch.cuda.synchronize()
     assert gr2["dlog_alpha"] is None
-    assert torch.equal(o, o2) and torch.equal(ST, ST2), "forward"
     assert torch.equal(r1, r2) and torch.equal(R1, R2), "recurrent"
-    assert torch.equal(o, o3) and torch.equal(ST, ST3) and torch.equal(r1, r3) and torch.equal(R1, R3), "tau"
+    assert torch.equal(o2, o3) and torch.equal(ST2, ST3) and torch.equal(r1, r3) and torch.equal(R1, R3), "tau"
+    idx = [0, 1]
+    pairs = {"o": (heads(o2, idx), heads(o, idx)), "S_T": (heads(ST2, idx), heads(ST, idx))}
     for name in ("dq", "dk", "dv", "dS0"):
-        assert torch.equal(gr[name], gr2[name]), name
-        assert torch.equal(gr[name], gr3[name]), name + " (tau)"
+        assert torch.equal(gr2[name], gr3[name]), name + " (tau)"
+        pairs[name] = (heads(gr2[name], idx), heads(gr[name], idx))
+    judge("no gate vs zero gate " + io, pairs, TOL[io])
     gr2["dlog_alpha"] = gr["dlog_alpha"]
     compare(inp, o2, ST2, gr2, [0, 1], io, cfg["name"])
 
@@ -325,8 +329,9 @@ def test_scalar_gate(io, B, H, T, K, V, C, c, decay):
     """Data-dependent scalar gates (Table 1: G_t = gamma_t 1^T 1) through a
     [B, H, T] log gamma: every output against the oracle (dlog gamma is the
     sum over the key features of the per-feature gate gradient), the
-    recurrent form too, and o, S_T, dq, dk, dv, dS0 bit-identical to the
-    per-feature path fed the broadcast gate."""
+    recurrent form too, and o, S_T, dq, dk, dv, dS0 in agreement with the
+    per-feature path fed the broadcast gate (a different evaluation: the
+    scalar path forms the plain decay matrix D_ij = exp(c_i - c_j))."""
     g = gla()
     cfg = small_case(f"sg_{io}_{K}_{V}_{T}", io, B, H, T, K, V, C, c, 60 + K + T, s0_std=0.1)
     inp = W.make_inputs(cfg, dST_std=0.1)
@@ -349,10 +354,12 @@ def test_scalar_gate(io, B, H, T, K, V, C, c, decay):
     gr2 = g.chunk_bwd(d["q"], d["k"], d["v"], full, d["dO"], C, c, S0=d["S0"], dST=d["dST"], want_dS0=True)
     torch.cuda.synchronize()
     assert gr["dlog_alpha"].shape == (B, H, T)
-    assert torch.equal(o, o2) and torch.equal(ST, ST2), "forward vs broadcast gate"
-    for name in ("dq", "dk", "dv", "dS0"):
-        assert torch.equal(gr[name], gr2[name]), name + " vs broadcast gate"
     idx = list(range(B * H))
+    pairs = {"o": (heads(o, idx), heads(o2, idx)), "S_T": (heads(ST, idx), heads(ST2, idx)),
+             "dlog_gamma": (heads(gr["dlog_alpha"], idx), heads(gr2["dlog_alpha"].float().sum(-1), idx))}
+    for name in ("dq", "dk", "dv", "dS0"):
+        pairs[name] = (heads(gr[name], idx), heads(gr2[name], idx))
+    judge("scalar vs broadcast gate " + cfg["name"], pairs, TOL[io])
     q, k, v, lgh, dO = (heads(inp[n], idx) for n in ("q", "k", "v", "log_alpha", "dO"))
     S0, dST = heads(inp["S0"], idx), heads(inp["dST"], idx)
     ro, rST = oracle.scalar_gate_fwd(q, k, v, lgh, S0)
