@@ -301,6 +301,8 @@ GLA_EXPORT gla_status gla_chunk_bwd(const gla_problem *prob, const void *q, cons
   if (s.T == 0)
     return hip_status(gla::launch_copy_state((int64_t)s.BH * s.K * s.V, dS_T, dS0, hs));
   auto run = [stage](unsigned k) { return stage == 0 || stage == k; };
+  // no gate and no gate gradient: the kernels' alpha = 1 variants
+  const bool ng = !log_alpha && !dlog_alpha;
   Work w;
   layout(s2, 1, (char *)workspace, &w, nseg);
   alias_ungated(w, log_alpha, q, k);
@@ -326,9 +328,9 @@ GLA_EXPORT gla_status gla_chunk_bwd(const gla_problem *prob, const void *q, cons
       if (e == hipSuccess)
         e = gla::launch_seg_bwd_scan(s.BH, nseg, s.K, s.V, w.dec, dS_T, w.Sloc, w.dSout, dS0, hs);
     }
-    if (e == hipSuccess) e = gla::launch_bwd_dq(s2, k, log_alpha, v, S0s, dO, dSTs, w, hs);
+    if (e == hipSuccess) e = gla::launch_bwd_dq(s2, k, log_alpha, v, S0s, dO, dSTs, w, hs, ng);
   }
-  if (e == hipSuccess && run(3)) e = gla::launch_bwd_intra(s2, q, k, log_alpha, dq, w, hs);
+  if (e == hipSuccess && run(3)) e = gla::launch_bwd_intra(s2, q, k, log_alpha, dq, w, hs, ng);
   if (e == hipSuccess && run(4))
     e = gla::launch_bwd_dk(s2, q, k, log_alpha, v, dO, dSTs, dq, dk, dlog_alpha, w, hs);
   if (e == hipSuccess && run(5)) e = gla::launch_bwd_dv(s2, dO, nullptr, dSTs, dv, nseg > 1 ? nullptr : dS0, w, hs);
@@ -366,8 +368,8 @@ GLA_EXPORT gla_status gla_chunk_bwd_general(const gla_problem *prob, const void 
   if (run(1) && !(prob->flags & GLA_FLAG_REUSE_FWD_WORKSPACE))
     e = gla::launch_prep(s, q, k, log_alpha, w, hs);
   if (e == hipSuccess && run(2)) e = gla::launch_beta_prep(s, v, dO, log_beta, w, hs);
-  if (e == hipSuccess && run(3)) e = gla::launch_bwd_dq(s, k, log_alpha, w.Vh, S0, w.Oh, dS_T, w, hs, true);
-  if (e == hipSuccess && run(4)) e = gla::launch_bwd_intra(s, q, k, log_alpha, dq, w, hs);
+  if (e == hipSuccess && run(3)) e = gla::launch_bwd_dq(s, k, log_alpha, w.Vh, S0, w.Oh, dS_T, w, hs, false, true);
+  if (e == hipSuccess && run(4)) e = gla::launch_bwd_intra(s, q, k, log_alpha, dq, w, hs, false);
   if (e == hipSuccess && run(5))
     e = gla::launch_bwd_dk(s, q, k, log_alpha, w.Vh, w.Oh, dS_T, dq, dk, dlog_alpha, w, hs, true);
   if (e == hipSuccess && run(6)) e = gla::launch_bwd_dv(s, dO, log_beta, dS_T, dv, dS0, w, hs);

@@ -49,6 +49,7 @@ struct IntraArgs {
   float *dat;             // [BH][N][K] fp32
   int T, K, C, N;
   int sg;         // scalar gate: la is [BH][T]
+  int ng;         // no gate and no gate gradient
   float inv_tau;  // gate epilogue (0: la holds log alpha)
 };
 
@@ -373,6 +374,220 @@ __global__ void __launch_bounds__(64 * (C / 16)) __attribute__((amdgpu_waves_per
   }
 }
 
+// acc += a b with a split once and b exact in the io dtype (bf16: hi b + lo b).
+template <typename T> __device__ __forceinline__ f4 mma2s(f4 acc, const Split<T> &a, const frag_t<T> &b) {
+  acc = mma<T>(acc, a.hi, b);
+  if constexpr (sizeof(T) == 2) acc = mma<T>(acc, a.lo, b);
+  return acc;
+}
+
+// Scalar gates and the absent gate: the decay D_ij = exp(c_i - c_j) (c the
+// chunk-local cumsum of log gamma; D = 1 without a gate) is shared by every
+// feature, so with dPD = dP (.) D (.) M
+//   dq_intra = dPD K,   dk_intra = dPD^T Q,
+// each one matrix-core product per 16x16 output tile and 32-row slab: dPD is
+// split into bf16 hi + lo once per chunk, q and k enter exactly (no
+// factorised operands, no per-feature exponentials).  The gate gradient's
+// parts (dai, dat) are formed as in the per-feature kernel; NG (no gate)
+// skips them.
+template <typename T, int C, bool PRE, bool NG>
+__global__ void __launch_bounds__(64 * (C / 16)) __attribute__((amdgpu_waves_per_eu(2)))
+intra_plain_kernel(IntraArgs a) {
+  using L = IntraLayout<C>;
+  constexpr int NB = L::NB, LDD = L::LDD, LDO = L::LDO;
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  float *sdP = (float *)(smem + L::offdP), *sTA = (float *)(smem + L::offTA);
+  float *sQz = (float *)(smem + L::offQz), *sKz = (float *)(smem + L::offKz);
+  float *sO = (float *)(smem + L::offO);
+
+  const int n = blockIdx.x, bh = blockIdx.y;
+  const int w = wave_id(), l = lane_id(), g16 = l >> 4, j16 = l & 15;
+  const int K = a.K, T_ = a.T;
+  const int t0 = n * C, rv = min(C, T_ - t0);
+  const int esz = sizeof(T);
+  const T *qc = (const T *)a.q + ((int64_t)bh * T_ + t0) * K;
+  const T *kc = (const T *)a.k + ((int64_t)bh * T_ + t0) * K;
+  const uint32_t kbytes = rsrc_bytes((int64_t)(T_ - t0) * K * esz);
+  const auto rs_q = make_rsrc(qc, kbytes), rs_k = make_rsrc(kc, kbytes);
+  const auto rs_dq = make_rsrc((T *)a.dq + ((int64_t)bh * T_ + t0) * K, kbytes);
+  const auto rs_dki = make_rsrc((T *)a.dki + ((int64_t)bh * T_ + t0) * K, kbytes);
+  const auto rs_dqr = make_rsrc(a.dqr + ((int64_t)bh * T_ + t0) * K, rsrc_bytes((int64_t)(T_ - t0) * K * 4));
+
+  // chunk-local inclusive cumsum of log gamma in units of log2, lane t = step t
+  float c2 = 0.f;
+  if constexpr (!NG) {
+    // (an absent gate whose gradient is wanted reads as log alpha = 0 from an
+    // empty range; the per-feature dA below is then that gradient's share)
+    const auto rs_la = make_rsrc(a.la ? (const T *)a.la + (int64_t)bh * T_ + t0 : qc,
+                                 a.la ? rsrc_bytes((int64_t)(T_ - t0) * esz) : 0u);
+    float x = el_f<T>(ld_el<T>(rs_la, l < C ? (uint32_t)(l * esz) : 0x80000000u));
+    if constexpr (PRE) x = gate_la(x, a.inv_tau, l < rv);
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const float y = __shfl_up(x, o);
+      if (l >= o) x += y;
+    }
+    c2 = x * kLog2e;
+  }
+
+  // ---- 1. dPD rows into LDS (thread: C/4 consecutive t of one s; dP is
+  // stored transposed and already masked)
+  {
+    constexpr int PER = C / 4;
+    const int e0 = (int)threadIdx.x * PER, sc = e0 / C, tb = e0 % C;
+    const float *src = a.dP + ((int64_t)bh * a.N + n) * C * C + e0;
+    const float cs = NG ? 0.f : __shfl(c2, sc);
+#pragma unroll
+    for (int u = 0; u < PER; u += 4) {
+      const f4 x = *(const f4 *)(src + u);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int t = tb + u + r;
+        float v = x[r];
+        if constexpr (!NG) {
+          // (the cross-lane read runs in every lane: a lane that skipped it
+          // would hand its readers no value)
+          const float ct = __shfl(c2, t);
+          v = sc <= t ? v * exp2f_fast(ct - cs) : 0.f;
+        }
+        sdP[t * LDD + sc] = v;
+      }
+    }
+  }
+  __syncthreads();
+
+  // the dPD operands of this wave's row block (dq) and column block (dk),
+  // split once for every feature tile
+  // (32-row slabs; with C = 16 the slots past the chunk are zeros)
+  constexpr int NSB = (C + 31) / 32;
+  const bool slot_in = C >= 32 || g16 < 2;
+  Split<T> aq[NSB], ak[NSB];
+#pragma unroll
+  for (int s = 0; s < NSB; ++s) {
+    f8 aw = f8{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f}, at = aw;
+    if (slot_in) {
+      const float *ap = sdP + (16 * w + j16) * LDD + 32 * s + 8 * g16;
+      const f4 a0 = *(const f4 *)ap, a1 = *(const f4 *)(ap + 4);
+      aw = f8{a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
+#pragma unroll
+      for (int u = 0; u < 8; ++u) at[u] = sdP[(32 * s + 8 * g16 + u) * LDD + 16 * w + j16];
+    }
+    aq[s] = split8<T>(aw);
+    ak[s] = split8<T>(at);
+  }
+
+  // ---- 2. feature groups (lane = feature)
+  const int NGR = (K + 63) / 64;
+  for (int gi = 0; gi < NGR; ++gi) {
+    const int f = 64 * gi + l;
+    const bool fv = f < K;
+    uint32_t rq[16], rk[16], rr[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const uint32_t off = fv ? (uint32_t)(((16 * w + r) * K + f) * esz) : 0x80000000u;
+      rq[r] = ld_el<T>(rs_q, off);
+      rk[r] = ld_el<T>(rs_k, off);
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      rr[r] = __builtin_amdgcn_raw_buffer_load_b32(rs_dqr, fv ? (uint32_t)(((16 * w + r) * K + f) * 4) : 0x80000000u, 0, 0);
+    float q[16], kk[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      q[r] = el_f<T>(rq[r]);
+      kk[r] = el_f<T>(rk[r]);
+    }
+    // (the previous group's result tiles, which these overlay, were consumed
+    // before its last barrier)
+#pragma unroll
+    for (int r = 0; r < 16; r += 4) {
+      *(f4 *)(sQz + l * LDD + 16 * w + r) = f4{q[r], q[r + 1], q[r + 2], q[r + 3]};
+      *(f4 *)(sKz + l * LDD + 16 * w + r) = f4{kk[r], kk[r + 1], kk[r + 2], kk[r + 3]};
+    }
+    __syncthreads();  // group tiles complete
+
+    f4 oq[4], ok[4];
+#pragma unroll
+    for (int ft = 0; ft < 4; ++ft) {
+      __builtin_amdgcn_sched_barrier(0);
+      oq[ft] = ok[ft] = zero4();
+      const int fl = 16 * ft + j16;
+      // dq of row block w: slabs holding a block J <= w
+#pragma unroll
+      for (int s = 0; s < NSB; ++s) {
+        if (32 * s > 16 * w + 15) continue;
+        const float *bp = sKz + fl * LDD + 32 * s + 8 * g16;
+        const f4 b0 = slot_in ? *(const f4 *)bp : zero4(), b1 = slot_in ? *(const f4 *)(bp + 4) : zero4();
+        frag_t<T> bf;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          bf[u] = cvt<T>(b0[u]);
+          bf[4 + u] = cvt<T>(b1[u]);
+        }
+        oq[ft] = mma2s<T>(oq[ft], aq[s], bf);
+      }
+      // dk of column block w: slabs holding a block I >= w
+#pragma unroll
+      for (int s = 0; s < NSB; ++s) {
+        if (32 * s + 31 < 16 * w) continue;
+        const float *bp = sQz + fl * LDD + 32 * s + 8 * g16;
+        const f4 b0 = slot_in ? *(const f4 *)bp : zero4(), b1 = slot_in ? *(const f4 *)(bp + 4) : zero4();
+        frag_t<T> bf;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          bf[u] = cvt<T>(b0[u]);
+          bf[4 + u] = cvt<T>(b1[u]);
+        }
+        ok[ft] = mma2s<T>(ok[ft], ak[s], bf);
+      }
+    }
+    __syncthreads();  // every wave is done with the group tiles, which the result tiles overlay
+
+    float *oqw = sO + (w * 2 + 0) * 64 * LDO, *okw = sO + (w * 2 + 1) * 64 * LDO;
+#pragma unroll
+    for (int ft = 0; ft < 4; ++ft)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        oqw[(16 * ft + j16) * LDO + 4 * g16 + r] = oq[ft][r];
+        okw[(16 * ft + j16) * LDO + 4 * g16 + r] = ok[ft][r];
+      }
+    // (the wave reads back only what it wrote: LDS keeps one wave's accesses in order)
+    float dA[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = 16 * w + r;
+      const float dq = oqw[l * LDO + r], dk = okw[l * LDO + r];
+      const uint32_t off = fv ? (uint32_t)((row * K + f) * esz) : 0x80000000u;
+      st_el<T>(rs_dq, off, __builtin_bit_cast(float, rr[r]) + dq);
+      st_el<T>(rs_dki, off, dk);
+      dA[r] = q[r] * dq - kk[r] * dk;
+    }
+    if constexpr (!NG) {
+      const auto rs_dai = make_rsrc((T *)a.dai + ((int64_t)bh * T_ + t0) * K, kbytes);
+      float sa = 0.f;
+#pragma unroll
+      for (int r = 15; r >= 0; --r) {
+        sa += dA[r];
+        dA[r] = sa;
+      }
+      sTA[w * 64 + l] = sa;
+      __syncthreads();  // block sums of dA published
+      float later = 0.f;
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+        if (b > w) later += sTA[b * 64 + l];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = 16 * w + r;
+        st_el<T>(rs_dai, fv ? (uint32_t)((row * K + f) * esz) : 0x80000000u, dA[r] + later);
+      }
+      if (w == 0 && fv) a.dat[((int64_t)bh * a.N + n) * K + f] = sa + later;
+    } else {
+      __syncthreads();  // result tiles consumed before the next group's tiles overlay them
+    }
+  }
+}
+
 template <typename T, int C, bool PRE>
 hipError_t launch_intra_t(const Shape &s, const IntraArgs &a, hipStream_t st) {
   static const hipError_t attr = hipFuncSetAttribute((const void *)intra_kernel<T, C, PRE>,
@@ -382,8 +597,22 @@ hipError_t launch_intra_t(const Shape &s, const IntraArgs &a, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <typename T, int C, bool PRE, bool NG>
+hipError_t launch_intra_plain(const Shape &s, const IntraArgs &a, hipStream_t st) {
+  static const hipError_t attr = hipFuncSetAttribute((const void *)intra_plain_kernel<T, C, PRE, NG>,
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
+  (void)attr;
+  hipLaunchKernelGGL((intra_plain_kernel<T, C, PRE, NG>), dim3(s.N, s.BH), dim3(64 * (C / 16)), IntraLayout<C>::total,
+                     st, a);
+  return hipGetLastError();
+}
+
 template <typename T, int C>
 hipError_t launch_intra_c(const Shape &s, const IntraArgs &a, hipStream_t st) {
+  if (a.ng) return launch_intra_plain<T, C, false, true>(s, a, st);
+  if (a.sg || !a.la)
+    return a.inv_tau != 0.f ? launch_intra_plain<T, C, true, false>(s, a, st)
+                            : launch_intra_plain<T, C, false, false>(s, a, st);
   return a.inv_tau != 0.f ? launch_intra_t<T, C, true>(s, a, st) : launch_intra_t<T, C, false>(s, a, st);
 }
 
@@ -401,12 +630,13 @@ size_t lds_bwd_intra(const Shape &s) {
 }
 
 hipError_t launch_bwd_intra(const Shape &s, const void *q, const void *k, const void *la, void *dq, const Work &w,
-                            hipStream_t st) {
+                            hipStream_t st, bool ng) {
   IntraArgs a;
   a.q = q; a.k = k; a.la = la; a.dP = w.dP; a.dqr = w.dqr; a.dq = dq;
   a.dki = w.dki; a.dai = w.dai; a.dat = w.dat;
   a.T = s.T; a.K = s.K; a.C = s.C; a.N = s.N;
   a.sg = s.sgate ? 1 : 0;
+  a.ng = ng ? 1 : 0;
   a.inv_tau = s.inv_tau;
   return s.io == IO_BF16 ? launch_intra_io<bf16>(s, a, st) : launch_intra_io<float>(s, a, st);
 }

@@ -38,6 +38,12 @@
 // hi + lo, and dq_inter reaches the dk sweep in fp32, so that the gate
 // gradient's long reverse sum keeps fp32 accuracy.
 //
+// NG (no gate and no gate gradient wanted: alpha = 1): every decay factor is
+// 1 and the gated operands are k and q themselves, so the factor phase only
+// stages k (q), the partials need no pre-scaling, the state needs no decay,
+// and with no gate gradient to protect the state and update operands are
+// used as single bf16 values (as the forward's inter-chunk products use them).
+//
 // General form (GB; App. C, a value-side gate beta as well): v and dO arrive
 // as Vh = V (.) exp(-E) and Oh = dO (.) exp(E) (E the chunk-local cumsum of
 // log beta, formed by gla_beta.hip), and the state's value rows decay by
@@ -78,6 +84,7 @@ struct KsArgs {
   float *cpart;     // general form: [BH][N][KT][V] per key tile colsum(S_[n+1] (.) dS_[n+1])
   int BH, T, K, V, C, N, KT;
   int sg;         // scalar gate: la is [BH][T], one value per step shared by every feature
+  int ng;         // no gate and no gate gradient (la and dla NULL)
   float inv_tau;   // gate epilogue (0: la holds log alpha)
 };
 
@@ -389,19 +396,21 @@ __device__ __forceinline__ void publish_decays(float *sSc, float *sG, const Fact
 // Reduction of the d_v-reducing partials (rows t, feature j; 32-row tiles th):
 // pre-scale by the per-(16-row block, feature) factor, then the upper half of
 // the state waves publishes to LDS ...
-template <typename L>
+template <typename L, bool SCALE = true>
 __device__ __forceinline__ void partials_publish(f16v (&acc)[2], const float *sSc, float *sRed, int w,
                                                  int g, int j) {
   constexpr int NTT = L::NB / 2;
-  float sc[L::NB];
+  if constexpr (SCALE) {
+    float sc[L::NB];
 #pragma unroll
-  for (int J = 0; J < L::NB; ++J) sc[J] = sSc[J * kKF + j];
+    for (int J = 0; J < L::NB; ++J) sc[J] = sSc[J * kKF + j];
 #pragma unroll
-  for (int th = 0; th < NTT; ++th)
+    for (int th = 0; th < NTT; ++th)
 #pragma unroll
-    for (int b = 0; b < 4; ++b)
+      for (int b = 0; b < 4; ++b)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) acc[th][4 * b + r] *= sc[2 * th + (b >> 1)];
+        for (int r = 0; r < 4; ++r) acc[th][4 * b + r] *= sc[2 * th + (b >> 1)];
+  }
   if (w >= L::NP && w < L::NWS) {
 #pragma unroll
     for (int th = 0; th < NTT; ++th)
@@ -426,12 +435,12 @@ __device__ __forceinline__ void partials_add(const f16v (&acc)[2], float *sRed, 
 }
 
 // ============================================================== dq sweep
-template <typename T, int CP, int NSL, bool PRE, bool GB>
+template <typename T, int CP, int NSL, bool PRE, bool GB, bool NG>
 __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   using L = KsLayout<T, CP>;
   constexpr int VS = L::VS, NB = L::NB, NRG = L::NRG, NST = CP / 16, NTT = CP / 32;
   constexpr int NDT = CP == 64 ? 3 : 1;  // dP tiles on or below the diagonal, one per wave 0..NDT-1
-  constexpr bool SPLIT = sizeof(T) == 2;
+  constexpr bool SPLIT = sizeof(T) == 2 && !NG;
   static_assert(VS * sizeof(T) == kRowB, "slab row size");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   T *sV = (T *)(smem + L::offV), *sD = (T *)(smem + L::offD);
@@ -499,7 +508,7 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
     const auto rs_k = make_rsrc(kh_ + (int64_t)t0 * K, bytes);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      fin_la[i] = ld_elem<T>(rs_la, gate_off<T>(a.sg, eoff[i], sbase, i));
+      if constexpr (!NG) fin_la[i] = ld_elem<T>(rs_la, gate_off<T>(a.sg, eoff[i], sbase, i));
       fin_k[i] = ld_elem<T>(rs_k, eoff[i]);
     }
     if constexpr (GB) fetch_gb(n);
@@ -534,6 +543,16 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   for (int n = 0; n < N; ++n) {
     const int t0 = n * C, rv = min(C, a.T - t0);
     // ---- factors: cumsum of log alpha, gated operands
+    if constexpr (NG) {
+      // K~ = k (the previous chunk's slab loop ended with a barrier, so the
+      // tile is free; the slab loop's first barrier publishes it)
+      if (fthr) {
+        T hi4[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) hi4[i] = cvt<T>(elem_f<T>(fin_k[i]));
+        store4<T>(sBh + fk * L::LDTB + 4 * frg, hi4);
+      }
+    } else {
     float c[4], kv[4];
     {
       float x[4];
@@ -570,6 +589,7 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
       *(f4 *)(sBloc + fk * L::LDT + 4 * frg) = bl4;
       publish_decays(sSc, sG, f, f.pre, frg, fk, fv);
     }
+    }
     if constexpr (GB) stage_gb();
     // unconditional (the last chunk re-reads itself) so that the wait counts
     // for the slab prefetch below stay exact
@@ -603,7 +623,7 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
               if constexpr (SPLIT) acc[th] = mma32<T>(acc[th], ad, slo);
             }
           }
-          S[sl] *= sG[j];
+          if constexpr (!NG) S[sl] *= sG[j];
         }
         // dP = dO V^T for this wave's tile (waves 0..NDT-1, chunks of this
         // key tile only), interleaved with the state update S^T <- gamma S^T
@@ -664,7 +684,7 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
       }
     }
     // ---- dq_inter partials, pre-scaled by exp(log decay before the block)
-    partials_publish<L>(acc, sSc, sRed, w, g, j);
+    partials_publish<L, !NG>(acc, sSc, sRed, w, g, j);
     __syncthreads();
     partials_add<L>(acc, sRed, w, g, j);
     __syncthreads();
@@ -674,11 +694,11 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
       f4 in4 = *(const f4 *)(sRed + fk * L::LDT + 4 * frg);
 #pragma unroll
       for (int p = 1; p < L::NP; ++p) in4 += *(const f4 *)(sRed + (p * kKF + fk) * L::LDT + 4 * frg);
-      const f4 bl4 = *(const f4 *)(sBloc + fk * L::LDT + 4 * frg);
+      const f4 bl4 = NG ? zero4() : *(const f4 *)(sBloc + fk * L::LDT + 4 * frg);
       const auto rs_dqr = make_rsrc(dqro + (int64_t)t0 * K, rsrc_bytes((int64_t)(a.T - t0) * K * 4));
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float dqe = __expf(bl4[i]) * in4[i];
+        const float dqe = NG ? in4[i] : __expf(bl4[i]) * in4[i];
         // rows past the sequence end, past the chunk or of absent features
         // fall outside the buffer range and are dropped
         __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, dqe), rs_dqr,
@@ -688,7 +708,7 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   }
 
   // ---- final-state term of the gate gradient: rowsum(S_T (.) dS_T) per feature
-  if (a.dST) {
+  if (!NG && a.dST) {
     float part = 0.f;
     if (sw) {
 #pragma unroll
@@ -712,11 +732,11 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
 }
 
 // ============================================================== dk sweep
-template <typename T, int CP, int NSL, bool PRE, bool GB>
+template <typename T, int CP, int NSL, bool PRE, bool GB, bool NG>
 __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
   using L = KsLayout<T, CP>;
   constexpr int VS = L::VS, NB = L::NB, NRG = L::NRG, NST = CP / 16, NTT = CP / 32;
-  constexpr bool SPLIT = sizeof(T) == 2;
+  constexpr bool SPLIT = sizeof(T) == 2 && !NG;
   static_assert(VS * sizeof(T) == kRowB, "slab row size");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   T *sV = (T *)(smem + L::offV), *sD = (T *)(smem + L::offD);
@@ -803,15 +823,18 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
     const auto rs_dai = make_rsrc(daih + (int64_t)t0 * K, bytes);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      fin_la[i] = ld_elem<T>(rs_la, gate_off<T>(a.sg, eoff[i], sbase, i));
       fin_q[i] = ld_elem<T>(rs_q, eoff[i]);
-      fin_k[i] = ld_elem<T>(rs_k, eoff[i]);
-      fin_dqr[i] = __builtin_amdgcn_raw_buffer_load_b32(rs_dqr, eoff[i] == 0x80000000u ? eoff[i] : eoff[i] / esz * 4, 0, 0);
       fin_dki[i] = ld_elem<T>(rs_dki, eoff[i]);
-      fin_dai[i] = ld_elem<T>(rs_dai, eoff[i]);
+      if constexpr (!NG) {
+        fin_la[i] = ld_elem<T>(rs_la, gate_off<T>(a.sg, eoff[i], sbase, i));
+        fin_k[i] = ld_elem<T>(rs_k, eoff[i]);
+        fin_dqr[i] = __builtin_amdgcn_raw_buffer_load_b32(rs_dqr, eoff[i] == 0x80000000u ? eoff[i] : eoff[i] / esz * 4, 0, 0);
+        fin_dai[i] = ld_elem<T>(rs_dai, eoff[i]);
+      }
     }
-    fin_dat = __builtin_amdgcn_raw_buffer_load_b32(make_rsrc(dath + (int64_t)n * K, (uint32_t)(K * 4)),
-                                                   fv ? (uint32_t)(kf * 4) : 0x80000000u, 0, 0);
+    if constexpr (!NG)
+      fin_dat = __builtin_amdgcn_raw_buffer_load_b32(make_rsrc(dath + (int64_t)n * K, (uint32_t)(K * 4)),
+                                                     fv ? (uint32_t)(kf * 4) : 0x80000000u, 0, 0);
     if constexpr (GB) fetch_gb(n);
   };
   TileLd<T, CP, VS, kKT> pv, pd;
@@ -840,7 +863,19 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
     // zc: the gate argument, for the gate gradient; dki, dai, dat: the
     // chunk's intra-chunk terms
     float c[4], kv[4], qdq[4], zc[4], dki[4], dai[4];
-    const float dat = __builtin_bit_cast(float, fin_dat);
+    float dat = 0.f;
+    if constexpr (NG) {
+      // Q~ = q (the tile is free after the previous chunk's last barrier)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) dki[i] = elem_f<T>(fin_dki[i]);
+      if (fthr) {
+        T hi4[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) hi4[i] = cvt<T>(elem_f<T>(fin_q[i]));
+        store4<T>(sBh + fk * L::LDTB + 4 * frg, hi4);
+      }
+    } else {
+    dat = __builtin_bit_cast(float, fin_dat);
     {
       float x[4];
 #pragma unroll
@@ -881,6 +916,7 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
       if constexpr (SPLIT) store4<T>(sBl + fk * L::LDTB + 4 * frg, lo4);
       *(f4 *)(sBloc + fk * L::LDT + 4 * frg) = bl4;
       publish_decays(sSc, sG, f, f.blast - f.pre - f.tot, frg, fk, fv);
+    }
     }
     if constexpr (GB) stage_gb();
     fetch_factors(max(n - 1, 0));  // unconditional, see the dq sweep
@@ -935,7 +971,7 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
       }
       if (sw) {
         // dS^T <- gamma dS^T + dO^T (Q (.) Lambda)
-        dS[sl] *= sG[j];
+        if constexpr (!NG) dS[sl] *= sG[j];
 #pragma unroll
         for (int st = 0; st < NST; ++st) {
           const frag_t<T> ad = ld_slab_col_perm<T>(sD, lt0, lt1, 16 * st, 32 * w);
@@ -949,10 +985,23 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
     // the next chunk's first state tile, in flight during the combine phases
     if constexpr (GB) fetch_sv(max(n - 1, 0), 0);
     // ---- dk_inter partials, pre-scaled by exp(B_last - B at the block's end)
-    partials_publish<L>(acc, sSc, sRed, w, g, j);
+    partials_publish<L, !NG>(acc, sSc, sRed, w, g, j);
     __syncthreads();
     partials_add<L>(acc, sRed, w, g, j);
     __syncthreads();
+
+    if constexpr (NG) {
+      // dk = dk_inter + dk_intra
+      if (fthr) {
+        f4 in4 = *(const f4 *)(sRed + fk * L::LDT + 4 * frg);
+#pragma unroll
+        for (int p = 1; p < L::NP; ++p) in4 += *(const f4 *)(sRed + (p * kKF + fk) * L::LDT + 4 * frg);
+        const auto rs_dk = make_rsrc(dko + (int64_t)t0 * K, rsrc_bytes((int64_t)(a.T - t0) * K * esz));
+#pragma unroll
+        for (int i = 0; i < 4; ++i) st_elem<T>(rs_dk, eoff[i], cvt<T>(in4[i] + dki[i]));
+      }
+      continue;
+    }
 
     // ---- dk_inter = Gamma (.) inter; dk = dk_inter + dk_intra; dA = q dq - k dk
     // (inter parts here; the intra parts arrive summed) and in-chunk reverse sums
@@ -1067,28 +1116,31 @@ KsArgs ks_args(const Shape &s) {
   return a;
 }
 
-template <bool DQ, typename T, int CP, int NSL, bool PRE, bool GB>
+template <bool DQ, typename T, int CP, int NSL, bool PRE, bool GB, bool NG>
 hipError_t launch_ks_pre(const KsArgs &a, hipStream_t st) {
   const size_t lds = KsLayout<T, CP>::total;
   // once per instantiation (thread-safe static initialisation), at the maximum
-  static const hipError_t attr = hipFuncSetAttribute(
-      DQ ? (const void *)dq_sweep_kernel<T, CP, NSL, PRE, GB> : (const void *)dk_sweep_kernel<T, CP, NSL, PRE, GB>,
-      hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
+  static const hipError_t attr =
+      hipFuncSetAttribute(DQ ? (const void *)dq_sweep_kernel<T, CP, NSL, PRE, GB, NG>
+                             : (const void *)dk_sweep_kernel<T, CP, NSL, PRE, GB, NG>,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
   (void)attr;
   if constexpr (DQ)
-    hipLaunchKernelGGL((dq_sweep_kernel<T, CP, NSL, PRE, GB>), dim3(a.BH * a.KT), dim3(kKT), lds, st, a);
+    hipLaunchKernelGGL((dq_sweep_kernel<T, CP, NSL, PRE, GB, NG>), dim3(a.BH * a.KT), dim3(kKT), lds, st, a);
   else
-    hipLaunchKernelGGL((dk_sweep_kernel<T, CP, NSL, PRE, GB>), dim3(a.BH * a.KT), dim3(kKT), lds, st, a);
+    hipLaunchKernelGGL((dk_sweep_kernel<T, CP, NSL, PRE, GB, NG>), dim3(a.BH * a.KT), dim3(kKT), lds, st, a);
   return hipGetLastError();
 }
 
 // PRE: the gate argument is the pre-activation of the gate epilogue.  GB: the
-// general form (value-side gate; the entry point rules out PRE with it).
+// general form (value-side gate; the entry point rules out PRE with it).  NG:
+// no gate and no gate gradient (never with GB).
 template <bool DQ, typename T, int CP, int NSL>
 hipError_t launch_ks_t(const KsArgs &a, hipStream_t st) {
-  if (a.gbv) return launch_ks_pre<DQ, T, CP, NSL, false, true>(a, st);
-  return a.inv_tau != 0.f ? launch_ks_pre<DQ, T, CP, NSL, true, false>(a, st)
-                          : launch_ks_pre<DQ, T, CP, NSL, false, false>(a, st);
+  if (a.gbv) return launch_ks_pre<DQ, T, CP, NSL, false, true, false>(a, st);
+  if (a.ng) return launch_ks_pre<DQ, T, CP, NSL, false, false, true>(a, st);
+  return a.inv_tau != 0.f ? launch_ks_pre<DQ, T, CP, NSL, true, false, false>(a, st)
+                          : launch_ks_pre<DQ, T, CP, NSL, false, false, false>(a, st);
 }
 
 template <bool DQ, typename T, int CP>
@@ -1124,10 +1176,11 @@ size_t lds_bwd_dk(const Shape &s) { return ks_lds(s); }
 
 hipError_t launch_bwd_dq(const Shape &s, const void *k, const void *la, const void *v,
                          const float *S0, const void *dO, const float *dST,
-                         const Work &w, hipStream_t st, bool gb_on) {
+                         const Work &w, hipStream_t st, bool ng, bool gb_on) {
   KsArgs a = ks_args(s);
   a.k = k; a.la = la; a.v = v; a.dO = dO; a.S0 = S0; a.dST = dST; a.dqr = w.dqr;
   a.dP = w.dP; a.cST = w.cST;
+  a.ng = ng && !gb_on;
   if (gb_on) { a.gbv = w.gb; a.Sb = w.Sb; }
   return dispatch_ks<true>(s, a, st);
 }
@@ -1140,6 +1193,7 @@ hipError_t launch_bwd_dk(const Shape &s, const void *q, const void *k, const voi
   a.q = q; a.k = k; a.la = la; a.v = v; a.dO = dO; a.dST = dST; a.dqr = w.dqr;
   a.dki = w.dki; a.dai = w.dai; a.dat = w.dat;
   a.dk = dk; a.dla = dla; a.cST = dST ? w.cST : nullptr; a.dla_part = w.dla_part;
+  a.ng = !la && !dla && !gb_on;
   hipError_t e = dispatch_ks<false>(s, a, st);
   if (e != hipSuccess || !s.sgate || !dla) return e;
   const int64_t n = (int64_t)s.BH * s.T;

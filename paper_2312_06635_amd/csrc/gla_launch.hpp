@@ -55,14 +55,15 @@ hipError_t launch_prep(const Shape &s, const void *q, const void *k, const void 
 hipError_t launch_fwd_main(const Shape &s, const void *v, const void *lb, const float *S0, void *o, float *ST,
                            const Work &w, hipStream_t st);
 // gb_on: the general form (v, dO are then w.Vh, w.Oh; the states decay by w.gb)
+// ng: no gate and no gate gradient wanted (la and the backward's dla NULL)
 // The dq sweep: w.dqr (dq_inter), w.dP, w.cST.
 hipError_t launch_bwd_dq(const Shape &s, const void *k, const void *la, const void *v,
                          const float *S0, const void *dO, const float *dST,
-                         const Work &w, hipStream_t st, bool gb_on = false);
+                         const Work &w, hipStream_t st, bool ng, bool gb_on = false);
 // The intra-chunk terms of the backward, after the dq sweep: dq, and w.dki,
-// w.dai, w.dat for the dk sweep.
+// w.dai, w.dat for the dk sweep (w.dki only with ng).
 hipError_t launch_bwd_intra(const Shape &s, const void *q, const void *k, const void *la, void *dq, const Work &w,
-                            hipStream_t st);
+                            hipStream_t st, bool ng);
 hipError_t launch_bwd_dk(const Shape &s, const void *q, const void *k, const void *la,
                          const void *v, const void *dO, const float *dST, const void *dq,
                          void *dk, void *dla, const Work &w, hipStream_t st, bool gb_on = false);
