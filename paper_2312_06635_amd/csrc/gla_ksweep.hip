@@ -106,8 +106,12 @@ template <typename T, int CP> struct KsLayout {
   static constexpr size_t offBh = offD + slab;                          // gated update operand (hi)
   static constexpr size_t offBl = offBh + sizeof(T) * kKF * LDTB;       // (lo, bf16 only)
   static constexpr size_t offBloc = offBl + (sizeof(T) == 2 ? sizeof(T) * kKF * LDTB : 0);  // block-local cumsum
-  static constexpr size_t offRed = offBloc + 4 * kKF * LDT;             // partial sums [NP]
-  static constexpr size_t offOr = offRed + 4 * NP * kKF * LDT;          // general form: the chunk's gb row
+  // per-wave partial sums [NWS][32 features][CP rows] fp32, 16-byte units
+  // XOR-swizzled per row: aliased over the two slab tiles, which are free
+  // from the slab loop's last barrier until the next chunk's first slab store
+  static constexpr size_t offRed = offV;
+  static_assert(4 * NWS * kKF * CP <= 2 * slab, "partials fit over the slab tiles");
+  static constexpr size_t offOr = offBloc + 4 * kKF * LDT;              // general form: the chunk's gb row
   static constexpr size_t offRg = offOr + 4 * kKF * LDT;                // row-group totals
   static constexpr size_t offSc = offRg + 4 * kKF * LDRG;               // per-block scale [NB][32]
   static constexpr size_t offG = offSc + 4 * NB * kKF;                  // gamma [32]
@@ -394,12 +398,14 @@ __device__ __forceinline__ void publish_decays(float *sSc, float *sG, const Fact
 }
 
 // Reduction of the d_v-reducing partials (rows t, feature j; 32-row tiles th):
-// pre-scale by the per-(16-row block, feature) factor, then the upper half of
-// the state waves publishes to LDS ...
+// pre-scaled by the per-(16-row block, feature) factor, every state wave
+// stores its tiles to its own slot; after one barrier the combine threads add
+// the slots, pairwise (w, w + NP) in the order p = 0 .. NP-1.  Unit u (four
+// rows) of feature row j sits at unit u ^ (j mod CP/4).
 template <typename L, bool SCALE = true>
-__device__ __forceinline__ void partials_publish(f16v (&acc)[2], const float *sSc, float *sRed, int w,
-                                                 int g, int j) {
-  constexpr int NTT = L::NB / 2;
+__device__ __forceinline__ void partials_store(f16v (&acc)[2], const float *sSc, float *sRed, int w, int g,
+                                               int j) {
+  constexpr int NTT = L::NB / 2, CP = L::NB * 16, UM = CP / 4 - 1;
   if constexpr (SCALE) {
     float sc[L::NB];
 #pragma unroll
@@ -411,27 +417,26 @@ __device__ __forceinline__ void partials_publish(f16v (&acc)[2], const float *sS
 #pragma unroll
         for (int r = 0; r < 4; ++r) acc[th][4 * b + r] *= sc[2 * th + (b >> 1)];
   }
-  if (w >= L::NP && w < L::NWS) {
+  if (w < L::NWS) {
 #pragma unroll
     for (int th = 0; th < NTT; ++th)
 #pragma unroll
-      for (int b = 0; b < 4; ++b)
-        *(f4 *)(sRed + ((w - L::NP) * kKF + j) * L::LDT + 32 * th + 8 * b + 4 * g) =
+      for (int b = 0; b < 4; ++b) {
+        const int u = 8 * th + 2 * b + g;
+        *(f4 *)(sRed + (w * kKF + j) * CP + 4 * (u ^ (j & UM))) =
             f4{acc[th][4 * b], acc[th][4 * b + 1], acc[th][4 * b + 2], acc[th][4 * b + 3]};
+      }
   }
 }
-// ... and, after a barrier, the lower half adds its partial in place.
-template <typename L>
-__device__ __forceinline__ void partials_add(const f16v (&acc)[2], float *sRed, int w, int g, int j) {
-  constexpr int NTT = L::NB / 2;
-  if (w < L::NP) {
+// The sum of the slots for rows 4 frg .. +3 of feature fk.
+template <typename L> __device__ __forceinline__ f4 partials_sum(const float *sRed, int fk, int frg) {
+  constexpr int CP = L::NB * 16, UM = CP / 4 - 1;
+  const int off = fk * CP + 4 * (frg ^ (fk & UM));
+  auto slot = [&](int p) { return *(const f4 *)(sRed + p * kKF * CP + off); };
+  f4 s = slot(0) + slot(L::NP);
 #pragma unroll
-    for (int th = 0; th < NTT; ++th)
-#pragma unroll
-      for (int b = 0; b < 4; ++b)
-        *(f4 *)(sRed + (w * kKF + j) * L::LDT + 32 * th + 8 * b + 4 * g) +=
-            f4{acc[th][4 * b], acc[th][4 * b + 1], acc[th][4 * b + 2], acc[th][4 * b + 3]};
-  }
+  for (int p = 1; p < L::NP; ++p) s += slot(p) + slot(p + L::NP);
+  return s;
 }
 
 // ============================================================== dq sweep
@@ -684,16 +689,12 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
       }
     }
     // ---- dq_inter partials, pre-scaled by exp(log decay before the block)
-    partials_publish<L, !NG>(acc, sSc, sRed, w, g, j);
-    __syncthreads();
-    partials_add<L>(acc, sRed, w, g, j);
+    partials_store<L, !NG>(acc, sSc, sRed, w, g, j);
     __syncthreads();
 
     // ---- dq_inter = Lambda (.) inter, per (row, feature)
     if (fthr) {
-      f4 in4 = *(const f4 *)(sRed + fk * L::LDT + 4 * frg);
-#pragma unroll
-      for (int p = 1; p < L::NP; ++p) in4 += *(const f4 *)(sRed + (p * kKF + fk) * L::LDT + 4 * frg);
+      const f4 in4 = partials_sum<L>(sRed, fk, frg);
       const f4 bl4 = NG ? zero4() : *(const f4 *)(sBloc + fk * L::LDT + 4 * frg);
       const auto rs_dqr = make_rsrc(dqro + (int64_t)t0 * K, rsrc_bytes((int64_t)(a.T - t0) * K * 4));
 #pragma unroll
@@ -705,6 +706,9 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
                                               eoff[i] == 0x80000000u ? eoff[i] : eoff[i] / esz * 4, 0, 0);
       }
     }
+    // (without a gate there is no factor barrier: the slots are read before
+    // the next chunk's slab store overwrites them)
+    if constexpr (NG) __syncthreads();
   }
 
   // ---- final-state term of the gate gradient: rowsum(S_T (.) dS_T) per feature
@@ -985,21 +989,20 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
     // the next chunk's first state tile, in flight during the combine phases
     if constexpr (GB) fetch_sv(max(n - 1, 0), 0);
     // ---- dk_inter partials, pre-scaled by exp(B_last - B at the block's end)
-    partials_publish<L, !NG>(acc, sSc, sRed, w, g, j);
-    __syncthreads();
-    partials_add<L>(acc, sRed, w, g, j);
+    partials_store<L, !NG>(acc, sSc, sRed, w, g, j);
     __syncthreads();
 
     if constexpr (NG) {
       // dk = dk_inter + dk_intra
       if (fthr) {
-        f4 in4 = *(const f4 *)(sRed + fk * L::LDT + 4 * frg);
-#pragma unroll
-        for (int p = 1; p < L::NP; ++p) in4 += *(const f4 *)(sRed + (p * kKF + fk) * L::LDT + 4 * frg);
+        const f4 in4 = partials_sum<L>(sRed, fk, frg);
         const auto rs_dk = make_rsrc(dko + (int64_t)t0 * K, rsrc_bytes((int64_t)(a.T - t0) * K * esz));
 #pragma unroll
         for (int i = 0; i < 4; ++i) st_elem<T>(rs_dk, eoff[i], cvt<T>(in4[i] + dki[i]));
       }
+      // (no factor barrier follows: the slots are read before the next
+      // chunk's slab store overwrites them)
+      __syncthreads();
       continue;
     }
 
@@ -1008,9 +1011,7 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
     float dA[4];
     if (fthr) {
       const float tot = sFt[frg * kKF + fk];
-      f4 in4 = *(const f4 *)(sRed + fk * L::LDT + 4 * frg);
-#pragma unroll
-      for (int p = 1; p < L::NP; ++p) in4 += *(const f4 *)(sRed + (p * kKF + fk) * L::LDT + 4 * frg);
+      const f4 in4 = partials_sum<L>(sRed, fk, frg);
       const f4 bl4 = *(const f4 *)(sBloc + fk * L::LDT + 4 * frg);
       const auto rs_dk = make_rsrc(dko + (int64_t)t0 * K, rsrc_bytes((int64_t)(a.T - t0) * K * esz));
 #pragma unroll
