@@ -166,6 +166,10 @@ def cpu_baseline(cfg, inputs, target_s=15.0):
             "sample": f"{heads} of {BH} heads (full T={cfg['T']}) x {reps} passes, fwd+bwd fp64 recurrence + "
                       f"BPTT, {el:.1f} s wall; tokens counted as heads*T/H per pass",
             "cpu_model": cpu_model(),
+            # one thread, this workload: one head's fwd+bwd measured (the
+            # calibration run above), the whole step as BH independent heads
+            "single_thread_one_head_s": round(t1, 3),
+            "single_thread_step_s": round(t1 * BH, 1),
             "tiny_fp32_single_thread_ms": round(tiny_single_thread_ms(), 4)}
 
 
