@@ -13,7 +13,9 @@
  * intra-chunk blocks (bf16 matrix-core products between sub-chunks, with
  * normalisers at the sub-chunk boundaries; inside a sub-chunk, Eq. 4 itself
  * in fp32 on the vector ALUs: one exponential of the log-space difference
- * per pair and feature), and the closed-form gate gradient of Sec. 4.3 in
+ * per pair and feature; with a scalar gate or none, every block is the
+ * plain (Q K^T) (.) D, D_ij = exp(c_i - c_j), in fp32 on the matrix cores),
+ * and the closed-form gate gradient of Sec. 4.3 in
  * the backward.
  *
  * Conventions shared by every entry point
@@ -28,7 +30,11 @@
  *     feature, i.e. ungated linear attention (the alpha = 1 case that the
  *     paper's FLA algorithms of Sec. 3.3 and App. A compute).  No gate tensor
  *     is then read, and the backward's dlog_alpha may be NULL too.  A NULL
- *     dlog_alpha always means the gate gradient is not wanted.
+ *     dlog_alpha always means the gate gradient is not wanted.  With no gate
+ *     the intra-chunk blocks are plain masked q k^T products and q, k are
+ *     read in place of the gated operands; with no gate and no gate gradient
+ *     the backward also multiplies its states as single bf16 operands (as the
+ *     forward does), since no gate-gradient sum needs their extra precision.
  *   - The caller owns every buffer; the library never allocates or frees
  *     device memory and keeps no mutable global state, so calls are
  *     re-entrant.  Outputs are overwritten, never accumulated into, and must
