@@ -88,7 +88,10 @@ struct KsArgs {
   float inv_tau;   // gate epilogue (0: la holds log alpha)
 };
 
-template <typename T, int CP> struct KsLayout {
+// NBUF = 2 (the dq sweep): two slab buffers, so that the next slab is stored
+// while the current one is multiplied, and the block-local cumsum is kept in
+// registers instead of an LDS tile.
+template <typename T, int CP, int NBUF = 1> struct KsLayout {
   static constexpr int VS = sizeof(T) == 2 ? 256 : 128;  // value columns per slab
   static constexpr int NWS = VS / 32;                     // waves holding state
   static constexpr int NP = NWS / 2;                      // partials left by the first reduction step
@@ -103,7 +106,7 @@ template <typename T, int CP> struct KsLayout {
   static constexpr size_t slab = sizeof(T) * CP * LDV;
   static constexpr size_t offV = 0;
   static constexpr size_t offD = offV + slab;
-  static constexpr size_t offBh = offD + slab;                          // gated update operand (hi)
+  static constexpr size_t offBh = NBUF * 2 * slab;                      // gated update operand (hi)
   static constexpr size_t offBl = offBh + sizeof(T) * kKF * LDTB;       // (lo, bf16 only)
   static constexpr size_t offBloc = offBl + (sizeof(T) == 2 ? sizeof(T) * kKF * LDTB : 0);  // block-local cumsum
   // per-wave partial sums [NWS][32 features][CP rows] fp32, 16-byte units
@@ -111,8 +114,8 @@ template <typename T, int CP> struct KsLayout {
   // from the slab loop's last barrier until the next chunk's first slab store
   static constexpr size_t offRed = offV;
   static_assert(4 * NWS * kKF * CP <= 2 * slab, "partials fit over the slab tiles");
-  static constexpr size_t offOr = offBloc + 4 * kKF * LDT;              // general form: the chunk's gb row
-  static constexpr size_t offRg = offOr + 4 * kKF * LDT;                // row-group totals
+  static constexpr size_t offOr = offBloc + (NBUF == 1 ? 4 * kKF * LDT : 0);  // general form: the chunk's gb row
+  static constexpr size_t offRg = offOr + 4 * 1024;                     // row-group totals
   static constexpr size_t offSc = offRg + 4 * kKF * LDRG;               // per-block scale [NB][32]
   static constexpr size_t offG = offSc + 4 * NB * kKF;                  // gamma [32]
   static constexpr size_t offCar = offG + 4 * kKF;                      // carry [2][32]
@@ -442,16 +445,17 @@ template <typename L> __device__ __forceinline__ f4 partials_sum(const float *sR
 // ============================================================== dq sweep
 template <typename T, int CP, int NSL, bool PRE, bool GB, bool NG>
 __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
-  using L = KsLayout<T, CP>;
+  using L = KsLayout<T, CP, 2>;
   constexpr int VS = L::VS, NB = L::NB, NRG = L::NRG, NST = CP / 16, NTT = CP / 32;
   constexpr int NDT = CP == 64 ? 3 : 1;  // dP tiles on or below the diagonal, one per wave 0..NDT-1
   constexpr bool SPLIT = sizeof(T) == 2 && !NG;
   static_assert(VS * sizeof(T) == kRowB, "slab row size");
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  T *sV = (T *)(smem + L::offV), *sD = (T *)(smem + L::offD);
+  // slab buffer b: V tile at b * 2 slab, dO tile right after it
+  T *sV0 = (T *)(smem + L::offV), *sD0 = (T *)(smem + L::offD);
+  T *sV1 = (T *)(smem + L::offV + 2 * L::slab), *sD1 = (T *)(smem + L::offD + 2 * L::slab);
   T *sBh = (T *)(smem + L::offBh), *sBl = (T *)(smem + L::offBl);
-  float *sBloc = (float *)(smem + L::offBloc);
-  float *sRed = (float *)(smem + L::offRed), *sOr = (float *)(smem + L::offOr);
+  float *sOr = (float *)(smem + L::offOr);
   float *sRg = (float *)(smem + L::offRg), *sSc = (float *)(smem + L::offSc);
   float *sG = (float *)(smem + L::offG);
   float *sRedS = (float *)(smem + L::offRedS);
@@ -500,7 +504,7 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
     for (int i = 0; i < 2; ++i)
       gbr[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (uint32_t)((tid + kKT * i) * 4), 0, 0));
   };
-  auto stage_gb = [&]() {  // into the intra-output tile (>= 1152 floats, free until the intra task)
+  auto stage_gb = [&]() {  // into its 1024-float tile (d_v <= 1024)
 #pragma unroll
     for (int i = 0; i < 2; ++i) sOr[tid + kKT * i] = gbr[i];
   };
@@ -541,25 +545,16 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
   const int pA = lb0 + 32 * tr * kRowB, pB = lb0 + 32 * tc * kRowB;
   const int pA1 = lb1 + 32 * tr * kRowB, pB1 = lb1 + 32 * tc * kRowB;
 
-  fetch_factors(0);
-  fetch_slab(0, 0);
-  fetch_slab(0, 1);
-
-  for (int n = 0; n < N; ++n) {
-    const int t0 = n * C, rv = min(C, a.T - t0);
-    // ---- factors: cumsum of log alpha, gated operands
-    if constexpr (NG) {
-      // K~ = k (the previous chunk's slab loop ended with a barrier, so the
-      // tile is free; the slab loop's first barrier publishes it)
-      if (fthr) {
-        T hi4[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) hi4[i] = cvt<T>(elem_f<T>(fin_k[i]));
-        store4<T>(sBh + fk * L::LDTB + 4 * frg, hi4);
-      }
-    } else {
-    float c[4], kv[4];
-    {
+  // The gate factors of chunk n, in two parts around a barrier (the
+  // row-group totals of log alpha are exchanged through LDS): part 1 forms the
+  // cumsum of the thread's four rows from the prefetched gate rows, part 2
+  // the gated keys K~ (hi/lo) in LDS, gamma and the block scales, and keeps
+  // the block-local cumsum in registers for the chunk's combine.
+  float c1[4], kv1[4];
+  f4 bl4 = zero4();
+  auto factors_part1 = [&](int n) {
+    if constexpr (!NG) {
+      const int rv = min(C, a.T - n * C);
       float x[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) x[i] = elem_f<T>(fin_la[i]);
@@ -571,37 +566,56 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         s += x[i];
-        c[i] = s;
-        kv[i] = elem_f<T>(fin_k[i]);
+        c1[i] = s;
+        kv1[i] = elem_f<T>(fin_k[i]);
       }
       if (fthr) sRg[fk * L::LDRG + frg] = s;
     }
-    __syncthreads();
+  };
+  auto factors_part2 = [&]() {
     if (fthr) {
-      const Factors f = chunk_factors<NRG, L::LDRG>(sRg, c, frg, w >> 1, fk);
-      const float ekt = __expf(f.blast - f.pre - f.tot);
-      f4 bl4;
       T hi4[4], lo4[4];
+      if constexpr (NG) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float kt_ = kv[i] * __expf(f.tot - f.Bloc[i]) * ekt;
-        hi4[i] = cvt<T>(kt_);
-        lo4[i] = cvt<T>(kt_ - (float)hi4[i]);
-        bl4[i] = f.Bloc[i];
+        for (int i = 0; i < 4; ++i) hi4[i] = cvt<T>(elem_f<T>(fin_k[i]));  // K~ = k
+      } else {
+        const Factors f = chunk_factors<NRG, L::LDRG>(sRg, c1, frg, w >> 1, fk);
+        const float ekt = __expf(f.blast - f.pre - f.tot);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float kt_ = kv1[i] * __expf(f.tot - f.Bloc[i]) * ekt;
+          hi4[i] = cvt<T>(kt_);
+          lo4[i] = cvt<T>(kt_ - (float)hi4[i]);
+          bl4[i] = f.Bloc[i];
+        }
+        publish_decays(sSc, sG, f, f.pre, frg, fk, fv);
       }
       store4<T>(sBh + fk * L::LDTB + 4 * frg, hi4);
       if constexpr (SPLIT) store4<T>(sBl + fk * L::LDTB + 4 * frg, lo4);
-      *(f4 *)(sBloc + fk * L::LDT + 4 * frg) = bl4;
-      publish_decays(sSc, sG, f, f.pre, frg, fk, fv);
-    }
     }
     if constexpr (GB) stage_gb();
-    // unconditional (the last chunk re-reads itself) so that the wait counts
-    // for the slab prefetch below stay exact
-    fetch_factors(min(n + 1, N - 1));
-    // (no barrier here: the slab loop's first barrier also publishes the
-    // factor tiles, and gamma is read after it)
+  };
 
+  // Slabs are multiplied from one LDS buffer while the next slab, loaded one
+  // step earlier, is stored into the other: one barrier per slab.  Prologue:
+  // chunk 0's factors and slab 0 in LDS, slab 1 in flight.
+  fetch_factors(0);
+  fetch_slab(0, 0);
+  fetch_slab(0, 1);
+  factors_part1(0);
+  pv.store_swz(sV0, L::LDV);
+  pd.store_swz(sD0, L::LDV);
+  fetch_slab(1, 0);
+  fetch_slab(1, 1);
+  __syncthreads();
+  factors_part2();
+  // unconditional (the last chunk re-reads itself) so that the wait counts
+  // for the slab prefetches stay exact
+  fetch_factors(min(1, N - 1));
+  __syncthreads();
+
+  for (int n = 0; n < N; ++n) {
+    const int t0 = n * C;
     // ---- slabs: dq_inter partials (state before the chunk), update (and, for
     // one chunk in KT, the dP tiles)
     const bool mine = n % a.KT == kt;  // this key tile forms the chunk's dP
@@ -611,9 +625,14 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
 #pragma unroll
     for (int sl = 0; sl < NSL; ++sl) {
       const int q = n * NSL + sl;
-      pv.store_swz(sV, L::LDV);
-      pd.store_swz(sD, L::LDV);
-      __syncthreads();
+      const bool b1 = (q & 1) != 0;  // this slab's buffer (even NSL: sl's parity)
+      T *sV = b1 ? sV1 : sV0, *sD = b1 ? sD1 : sD0;    // this slab
+      T *sVn = b1 ? sV0 : sV1, *sDn = b1 ? sD0 : sD1;  // the next one's buffer
+      // the next slab (loaded during the previous step) into the other
+      // buffer, which the previous step's barrier freed; no barrier before
+      // this slab's products
+      pv.store_swz(sVn, L::LDV);
+      pd.store_swz(sDn, L::LDV);
       {
         if (sw) {
           // dq_inter += dO[:, this wave's 32 value rows] S^T
@@ -633,9 +652,9 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
         // dP = dO V^T for this wave's tile (waves 0..NDT-1, chunks of this
         // key tile only), interleaved with the state update S^T <- gamma S^T
         // + V^T (K (.) Gamma) so that the two independent accumulation chains
-        // hide each other's operand reads; the next slab's loads are issued
-        // in two halves between these products (pinned by scheduling
-        // barriers) so that the memory pipeline drains meanwhile
+        // hide each other's operand reads; the loads of the slab after the
+        // next are issued in two halves between these products (pinned by
+        // scheduling barriers) so that the memory pipeline drains meanwhile
         constexpr int NDS = VS / 16;    // dP steps per slab
         constexpr int UPD = NDS / NST;  // dP steps per update step
         auto slab_products = [&](auto with_dp) {
@@ -645,7 +664,7 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
               accP = mma32<T>(accP, ld_slab_row<T>(sD, pA, pA1, 0, 16 * st), ld_slab_row<T>(sV, pB, pB1, 0, 16 * st));
             if (st == 0 || st == NDS / 2) {
               __builtin_amdgcn_sched_barrier(0);
-              fetch_slab(q + 1, st == 0 ? 0 : 1);
+              fetch_slab(q + 2, st == 0 ? 0 : 1);
               __builtin_amdgcn_sched_barrier(0);
             }
             if (sw && (st + 1) % UPD == 0) {
@@ -669,6 +688,7 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
           __builtin_amdgcn_sched_barrier(0);
         }
       }
+      // (publishes the next slab; every read of this slab's buffer is done)
       __syncthreads();
     }
 
@@ -688,14 +708,17 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
         __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v4), rs_dp, off, 0, 0);
       }
     }
-    // ---- dq_inter partials, pre-scaled by exp(log decay before the block)
+    // ---- dq_inter partials, pre-scaled by exp(log decay before the block),
+    // into the buffer of the chunk's last slab (the other one holds the next
+    // chunk's first slab); the next chunk's factor part 1 alongside
+    float *sRed = (float *)(smem + L::offRed + (((n * NSL + NSL - 1) & 1) ? 2 * L::slab : 0));
     partials_store<L, !NG>(acc, sSc, sRed, w, g, j);
+    factors_part1(min(n + 1, N - 1));
     __syncthreads();
 
     // ---- dq_inter = Lambda (.) inter, per (row, feature)
     if (fthr) {
       const f4 in4 = partials_sum<L>(sRed, fk, frg);
-      const f4 bl4 = NG ? zero4() : *(const f4 *)(sBloc + fk * L::LDT + 4 * frg);
       const auto rs_dqr = make_rsrc(dqro + (int64_t)t0 * K, rsrc_bytes((int64_t)(a.T - t0) * K * 4));
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -706,9 +729,12 @@ __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
                                               eoff[i] == 0x80000000u ? eoff[i] : eoff[i] / esz * 4, 0, 0);
       }
     }
-    // (without a gate there is no factor barrier: the slots are read before
-    // the next chunk's slab store overwrites them)
-    if constexpr (NG) __syncthreads();
+    // ---- the next chunk's factor part 2 (the last chunk redoes its own);
+    // the barrier publishes its tiles and orders the combine's reads of the
+    // partials before the next slab store into their buffer
+    factors_part2();
+    fetch_factors(min(n + 2, N - 1));
+    __syncthreads();
   }
 
   // ---- final-state term of the gate gradient: rowsum(S_T (.) dS_T) per feature
@@ -801,7 +827,7 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
     for (int i = 0; i < 2; ++i)
       gbr[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (uint32_t)((tid + kKT * i) * 4), 0, 0));
   };
-  auto stage_gb = [&]() {  // into the intra-output tile (>= 1152 floats, free until the intra task)
+  auto stage_gb = [&]() {  // into its 1024-float tile (d_v <= 1024)
 #pragma unroll
     for (int i = 0; i < 2; ++i) sOr[tid + kKT * i] = gbr[i];
   };
@@ -1100,12 +1126,17 @@ int ks_nsl(const Shape &s) {
   return n <= 1 ? 1 : (n <= 2 ? 2 : (n <= 4 ? 4 : 8));
 }
 
-template <typename T, int CP> size_t ks_lds_t() { return KsLayout<T, CP>::total; }
+template <typename T, int CP, int NBUF> size_t ks_lds_t() { return KsLayout<T, CP, NBUF>::total; }
 
-size_t ks_lds(const Shape &s) {
+// dq: the dq sweep's layout (two slab buffers)
+size_t ks_lds(const Shape &s, bool dq) {
   const bool b = s.io == IO_BF16;
-  if (ks_cp(s) == 32) return b ? ks_lds_t<bf16, 32>() : ks_lds_t<float, 32>();
-  return b ? ks_lds_t<bf16, 64>() : ks_lds_t<float, 64>();
+  if (dq) {
+    if (ks_cp(s) == 32) return b ? ks_lds_t<bf16, 32, 2>() : ks_lds_t<float, 32, 2>();
+    return b ? ks_lds_t<bf16, 64, 2>() : ks_lds_t<float, 64, 2>();
+  }
+  if (ks_cp(s) == 32) return b ? ks_lds_t<bf16, 32, 1>() : ks_lds_t<float, 32, 1>();
+  return b ? ks_lds_t<bf16, 64, 1>() : ks_lds_t<float, 64, 1>();
 }
 
 KsArgs ks_args(const Shape &s) {
@@ -1119,7 +1150,7 @@ KsArgs ks_args(const Shape &s) {
 
 template <bool DQ, typename T, int CP, int NSL, bool PRE, bool GB, bool NG>
 hipError_t launch_ks_pre(const KsArgs &a, hipStream_t st) {
-  const size_t lds = KsLayout<T, CP>::total;
+  const size_t lds = KsLayout<T, CP, DQ ? 2 : 1>::total;
   // once per instantiation (thread-safe static initialisation), at the maximum
   static const hipError_t attr =
       hipFuncSetAttribute(DQ ? (const void *)dq_sweep_kernel<T, CP, NSL, PRE, GB, NG>
@@ -1166,14 +1197,14 @@ hipError_t dispatch_ks(const Shape &s, const KsArgs &a, hipStream_t st) {
 
 }  // namespace
 
-size_t lds_bwd_dq(const Shape &s) { return ks_lds(s); }
+size_t lds_bwd_dq(const Shape &s) { return ks_lds(s, true); }
 
 size_t ks_state_bytes(const Shape &s) {
   const int vs = s.io == IO_BF16 ? 256 : 128;
   const int64_t kt = (s.K + kKF - 1) / kKF;
   return (size_t)s.BH * s.N * kt * ks_nsl(s) * vs * kKF * s.esz();
 }
-size_t lds_bwd_dk(const Shape &s) { return ks_lds(s); }
+size_t lds_bwd_dk(const Shape &s) { return ks_lds(s, false); }
 
 hipError_t launch_bwd_dq(const Shape &s, const void *k, const void *la, const void *v,
                          const float *S0, const void *dO, const float *dST,
