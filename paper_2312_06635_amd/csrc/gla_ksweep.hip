@@ -88,40 +88,38 @@ struct KsArgs {
   float inv_tau;   // gate epilogue (0: la holds log alpha)
 };
 
-// NBUF = 2 (the dq sweep): two slab buffers, so that the next slab is stored
-// while the current one is multiplied, and the block-local cumsum is kept in
-// registers instead of an LDS tile.
-template <typename T, int CP, int NBUF = 1> struct KsLayout {
+// Two slab buffers, so that the next slab is stored while the current one is
+// multiplied; the per-(row, feature) gate values stay in registers.
+template <typename T, int CP> struct KsLayout {
   static constexpr int VS = sizeof(T) == 2 ? 256 : 128;  // value columns per slab
   static constexpr int NWS = VS / 32;                     // waves holding state
-  static constexpr int NP = NWS / 2;                      // partials left by the first reduction step
+  static constexpr int NP = NWS / 2;                      // partial slots are added in pairs (p, p + NP)
   static constexpr int LDV = VS;                          // slab rows are XOR-swizzled, not padded
   static constexpr int NB = CP / 16, NRG = CP / 4;
-  // Per-(row, feature) tiles are stored feature-major ([32 features][rows]),
-  // so a factor/final thread's four consecutive rows of one feature and a
+  // The gated update operand is stored feature-major ([32 features][rows]),
+  // so a factor thread's four consecutive rows of one feature and a
   // fragment's eight consecutive rows are single 8/16-byte LDS accesses.
-  static constexpr int LDT = CP + 4;                          // fp32 feature-major tiles
-  static constexpr int LDTB = CP + (sizeof(T) == 2 ? 8 : 4);  // T feature-major tiles
+  static constexpr int LDTB = CP + (sizeof(T) == 2 ? 8 : 4);
   static constexpr int LDRG = NRG + 4;                        // row-group sums [32][NRG]
   static constexpr size_t slab = sizeof(T) * CP * LDV;
+  // slab buffer b: the V tile at offV + 2 b slab, the dO tile after it
   static constexpr size_t offV = 0;
   static constexpr size_t offD = offV + slab;
-  static constexpr size_t offBh = NBUF * 2 * slab;                      // gated update operand (hi)
+  static constexpr size_t offBh = 4 * slab;                             // gated update operand (hi)
   static constexpr size_t offBl = offBh + sizeof(T) * kKF * LDTB;       // (lo, bf16 only)
-  static constexpr size_t offBloc = offBl + (sizeof(T) == 2 ? sizeof(T) * kKF * LDTB : 0);  // block-local cumsum
   // per-wave partial sums [NWS][32 features][CP rows] fp32, 16-byte units
-  // XOR-swizzled per row: aliased over the two slab tiles, which are free
-  // from the slab loop's last barrier until the next chunk's first slab store
+  // XOR-swizzled per row: aliased over the slab buffer of the chunk's last
+  // slab, which is free from that slab's barrier until the next slab store
+  // into it (two barriers later)
   static constexpr size_t offRed = offV;
-  static_assert(4 * NWS * kKF * CP <= 2 * slab, "partials fit over the slab tiles");
-  static constexpr size_t offOr = offBloc + (NBUF == 1 ? 4 * kKF * LDT : 0);  // general form: the chunk's gb row
+  static_assert(4 * NWS * kKF * CP <= 2 * slab, "partials fit over a slab buffer");
+  static constexpr size_t offOr = offBl + (sizeof(T) == 2 ? sizeof(T) * kKF * LDTB : 0);  // general form: gb row
   static constexpr size_t offRg = offOr + 4 * 1024;                     // row-group totals
   static constexpr size_t offSc = offRg + 4 * kKF * LDRG;               // per-block scale [NB][32]
   static constexpr size_t offG = offSc + 4 * NB * kKF;                  // gamma [32]
   static constexpr size_t offCar = offG + 4 * kKF;                      // carry [2][32]
   static constexpr size_t offRedS = offCar + 4 * 2 * kKF;               // final-state sums [8][32]
-  static constexpr size_t offFt = offRedS + 4 * 8 * kKF;               // per-thread block decay [NRG][32]
-  static constexpr size_t offGrp = offFt + 4 * NRG * kKF;               // dk: row-group sums of dA
+  static constexpr size_t offGrp = offRedS + 4 * 8 * kKF;               // dk: row-group sums of dA
   static constexpr size_t total = offGrp + 4 * kKF * LDRG;
 };
 
@@ -445,7 +443,7 @@ template <typename L> __device__ __forceinline__ f4 partials_sum(const float *sR
 // ============================================================== dq sweep
 template <typename T, int CP, int NSL, bool PRE, bool GB, bool NG>
 __global__ void __launch_bounds__(kKT) dq_sweep_kernel(KsArgs a) {
-  using L = KsLayout<T, CP, 2>;
+  using L = KsLayout<T, CP>;
   constexpr int VS = L::VS, NB = L::NB, NRG = L::NRG, NST = CP / 16, NTT = CP / 32;
   constexpr int NDT = CP == 64 ? 3 : 1;  // dP tiles on or below the diagonal, one per wave 0..NDT-1
   constexpr bool SPLIT = sizeof(T) == 2 && !NG;
@@ -769,13 +767,14 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
   constexpr bool SPLIT = sizeof(T) == 2 && !NG;
   static_assert(VS * sizeof(T) == kRowB, "slab row size");
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  T *sV = (T *)(smem + L::offV), *sD = (T *)(smem + L::offD);
+  // slab buffer b: V tile at b * 2 slab, dO tile right after it
+  T *sV0 = (T *)(smem + L::offV), *sD0 = (T *)(smem + L::offD);
+  T *sV1 = (T *)(smem + L::offV + 2 * L::slab), *sD1 = (T *)(smem + L::offD + 2 * L::slab);
   T *sBh = (T *)(smem + L::offBh), *sBl = (T *)(smem + L::offBl);
-  float *sBloc = (float *)(smem + L::offBloc);
-  float *sRed = (float *)(smem + L::offRed), *sOr = (float *)(smem + L::offOr);
+  float *sOr = (float *)(smem + L::offOr);
   float *sRg = (float *)(smem + L::offRg), *sSc = (float *)(smem + L::offSc);
   float *sG = (float *)(smem + L::offG);
-  float *sCar = (float *)(smem + L::offCar), *sFt = (float *)(smem + L::offFt);
+  float *sCar = (float *)(smem + L::offCar);
   float *sGrp = (float *)(smem + L::offGrp);
 
   int bh, kt;
@@ -881,38 +880,28 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
 
   T *dko = (T *)a.dk + (int64_t)bh * a.T * K, *dlao = (T *)a.dla + (int64_t)bh * a.T * K;
 
-  fetch_factors(N - 1);
-  fetch_slab(0, 0);
-  fetch_slab(0, 1);
-
-  if constexpr (GB) fetch_sv(N - 1, 0);
-  for (int it = 0; it < N; ++it) {
-    const int n = N - 1 - it;
-    const int t0 = n * C, rv = min(C, a.T - t0);
-    // ---- factors
-    // zc: the gate argument, for the gate gradient; dki, dai, dat: the
-    // chunk's intra-chunk terms
-    float c[4], kv[4], qdq[4], zc[4], dki[4], dai[4];
-    float dat = 0.f;
-    if constexpr (NG) {
-      // Q~ = q (the tile is free after the previous chunk's last barrier)
+  // Per-(row, feature) values of a chunk, kept in registers from its factor
+  // phase to its combine (cur: the chunk being swept, nxt: the next one in
+  // the sweep, formed at the boundary before it): the gate argument zc (for
+  // the gate gradient), the block-local cumsum, the block total, k, q dq_inter,
+  // and the intra kernel's dk_intra, dA_intra share and chunk total.
+  struct ChunkVals {
+    float c[4], kv[4], qdq[4], zc[4], dki[4], dai[4], dat, tot;
+  };
+  ChunkVals cur, nxt;
+  // factor part 1 of chunk n: its values from the prefetched rows, and the
+  // row-group totals of log alpha into LDS
+  auto factors_part1 = [&](int n) {
+    const int rv = min(C, a.T - n * C);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) dki[i] = elem_f<T>(fin_dki[i]);
-      if (fthr) {
-        T hi4[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) hi4[i] = cvt<T>(elem_f<T>(fin_q[i]));
-        store4<T>(sBh + fk * L::LDTB + 4 * frg, hi4);
-      }
-    } else {
-    dat = __builtin_bit_cast(float, fin_dat);
-    {
+    for (int i = 0; i < 4; ++i) nxt.dki[i] = elem_f<T>(fin_dki[i]);
+    if constexpr (!NG) {
+      nxt.dat = __builtin_bit_cast(float, fin_dat);
       float x[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        x[i] = zc[i] = elem_f<T>(fin_la[i]);
-        dki[i] = elem_f<T>(fin_dki[i]);
-        dai[i] = elem_f<T>(fin_dai[i]);
+        x[i] = nxt.zc[i] = elem_f<T>(fin_la[i]);
+        nxt.dai[i] = elem_f<T>(fin_dai[i]);
       }
       if constexpr (PRE) {  // gate epilogue
 #pragma unroll
@@ -922,37 +911,61 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         s += x[i];
-        c[i] = s;
-        kv[i] = elem_f<T>(fin_k[i]);
-        qdq[i] = elem_f<T>(fin_q[i]) * __builtin_bit_cast(float, fin_dqr[i]);
+        nxt.c[i] = s;
+        nxt.kv[i] = elem_f<T>(fin_k[i]);
+        nxt.qdq[i] = elem_f<T>(fin_q[i]) * __builtin_bit_cast(float, fin_dqr[i]);
       }
       if (fthr) sRg[fk * L::LDRG + frg] = s;
     }
-    __syncthreads();
+  };
+  // factor part 2: Q~ (hi/lo) into LDS, gamma and the block scales; the
+  // block-local cumsum replaces the chunk's cumsum in nxt.c
+  auto factors_part2 = [&]() {
     if (fthr) {
-      const Factors f = chunk_factors<NRG, L::LDRG>(sRg, c, frg, w >> 1, fk);
-      sFt[frg * kKF + fk] = f.tot;
-      const float epre = __expf(f.pre);
-      f4 bl4;
       T hi4[4], lo4[4];
+      if constexpr (NG) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float qt = elem_f<T>(fin_q[i]) * __expf(f.Bloc[i]) * epre;
-        hi4[i] = cvt<T>(qt);
-        lo4[i] = cvt<T>(qt - (float)hi4[i]);
-        bl4[i] = f.Bloc[i];
+        for (int i = 0; i < 4; ++i) hi4[i] = cvt<T>(elem_f<T>(fin_q[i]));  // Q~ = q
+      } else {
+        const Factors f = chunk_factors<NRG, L::LDRG>(sRg, nxt.c, frg, w >> 1, fk);
+        nxt.tot = f.tot;
+        const float epre = __expf(f.pre);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float qt = elem_f<T>(fin_q[i]) * __expf(f.Bloc[i]) * epre;
+          hi4[i] = cvt<T>(qt);
+          lo4[i] = cvt<T>(qt - (float)hi4[i]);
+          nxt.c[i] = f.Bloc[i];
+        }
+        publish_decays(sSc, sG, f, f.blast - f.pre - f.tot, frg, fk, fv);
       }
       store4<T>(sBh + fk * L::LDTB + 4 * frg, hi4);
       if constexpr (SPLIT) store4<T>(sBl + fk * L::LDTB + 4 * frg, lo4);
-      *(f4 *)(sBloc + fk * L::LDT + 4 * frg) = bl4;
-      publish_decays(sSc, sG, f, f.blast - f.pre - f.tot, frg, fk, fv);
-    }
     }
     if constexpr (GB) stage_gb();
-    fetch_factors(max(n - 1, 0));  // unconditional, see the dq sweep
-    // the slab loop's first barrier also publishes the factor tiles (gamma is
-    // read after it); the general form reads the staged gb row before it
-    if constexpr (GB) __syncthreads();
+  };
+
+  // Slabs are multiplied from one LDS buffer while the next is stored into the
+  // other (as in the dq sweep).  Prologue: the last chunk's factors and its
+  // first slab in LDS, the second in flight.
+  fetch_factors(N - 1);
+  fetch_slab(0, 0);
+  fetch_slab(0, 1);
+  factors_part1(N - 1);
+  pv.store_swz(sV0, L::LDV);
+  pd.store_swz(sD0, L::LDV);
+  fetch_slab(1, 0);
+  fetch_slab(1, 1);
+  __syncthreads();
+  factors_part2();
+  fetch_factors(max(N - 2, 0));  // unconditional, see the dq sweep
+  cur = nxt;
+  if constexpr (GB) fetch_sv(N - 1, 0);
+  __syncthreads();
+
+  for (int it = 0; it < N; ++it) {
+    const int n = N - 1 - it;
+    const int t0 = n * C;
 
     // ---- slabs: dk_inter partials (dS after the chunk), then the dS update
     f16v acc[2];
@@ -961,8 +974,11 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
 #pragma unroll
     for (int sl = 0; sl < NSL; ++sl) {
       const int q = it * NSL + sl;
-      pv.store_swz(sV, L::LDV);
-      pd.store_swz(sD, L::LDV);
+      const bool b1 = (q & 1) != 0;  // this slab's buffer
+      T *sV = b1 ? sV1 : sV0, *sD = b1 ? sD1 : sD0;
+      // the next slab into the other buffer (freed by the previous barrier)
+      pv.store_swz(b1 ? sV0 : sV1, L::LDV);
+      pd.store_swz(b1 ? sD0 : sD1, L::LDV);
       if constexpr (GB) {
         // this tile's colsum(S_[n+1] (.) dS_[n+1]) per value: the carry of the
         // value-side gate gradient into chunk n
@@ -979,9 +995,8 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
         if (sw) scale_rows(dS[sl], sOr + sl * VS + 32 * w, g);
         __builtin_amdgcn_sched_barrier(0);
       }
-      __syncthreads();
-      // the next slab's loads go out in two halves between the dk_inter
-      // products (every wave, so that each issues its share of the loads)
+      // the loads of the slab after the next go out in two halves between
+      // the dk_inter products (every wave, so that each issues its share)
 #pragma unroll
       for (int st = 0; st < 2; ++st) {
         if (sw) {
@@ -996,7 +1011,7 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
           }
         }
         __builtin_amdgcn_sched_barrier(0);
-        fetch_slab(q + 1, st);
+        fetch_slab(q + 2, st);
         __builtin_amdgcn_sched_barrier(0);
       }
       if (sw) {
@@ -1009,42 +1024,48 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
           if constexpr (SPLIT) dS[sl] = mma32<T>(dS[sl], ad, ld_row32<T>(sBl, L::LDTB, 0, 16 * st));
         }
       }
+      // (publishes the next slab; every read of this slab's buffer is done)
       __syncthreads();
     }
 
     // the next chunk's first state tile, in flight during the combine phases
     if constexpr (GB) fetch_sv(max(n - 1, 0), 0);
-    // ---- dk_inter partials, pre-scaled by exp(B_last - B at the block's end)
+    // ---- dk_inter partials, pre-scaled by exp(B_last - B at the block's end),
+    // into the buffer of the chunk's last slab
+    float *sRed = (float *)(smem + L::offRed + (((it * NSL + NSL - 1) & 1) ? 2 * L::slab : 0));
     partials_store<L, !NG>(acc, sSc, sRed, w, g, j);
     __syncthreads();
 
     if constexpr (NG) {
-      // dk = dk_inter + dk_intra
+      // dk = dk_inter + dk_intra; the next chunk's factors
       if (fthr) {
         const f4 in4 = partials_sum<L>(sRed, fk, frg);
         const auto rs_dk = make_rsrc(dko + (int64_t)t0 * K, rsrc_bytes((int64_t)(a.T - t0) * K * esz));
 #pragma unroll
-        for (int i = 0; i < 4; ++i) st_elem<T>(rs_dk, eoff[i], cvt<T>(in4[i] + dki[i]));
+        for (int i = 0; i < 4; ++i) st_elem<T>(rs_dk, eoff[i], cvt<T>(in4[i] + cur.dki[i]));
       }
-      // (no factor barrier follows: the slots are read before the next
-      // chunk's slab store overwrites them)
+      factors_part1(max(n - 1, 0));
+      factors_part2();
+      fetch_factors(max(n - 2, 0));
+      cur = nxt;
+      // (publishes Q~; orders the reads of the partials before the next
+      // slab store into their buffer)
       __syncthreads();
       continue;
     }
 
     // ---- dk_inter = Gamma (.) inter; dk = dk_inter + dk_intra; dA = q dq - k dk
-    // (inter parts here; the intra parts arrive summed) and in-chunk reverse sums
+    // (inter parts here; the intra parts arrive summed) and in-chunk reverse
+    // sums; the next chunk's factor part 1 alongside
     float dA[4];
     if (fthr) {
-      const float tot = sFt[frg * kKF + fk];
       const f4 in4 = partials_sum<L>(sRed, fk, frg);
-      const f4 bl4 = *(const f4 *)(sBloc + fk * L::LDT + 4 * frg);
       const auto rs_dk = make_rsrc(dko + (int64_t)t0 * K, rsrc_bytes((int64_t)(a.T - t0) * K * esz));
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float dke = __expf(tot - bl4[i]) * in4[i];
-        dA[i] = qdq[i] - kv[i] * dke;
-        st_elem<T>(rs_dk, eoff[i], cvt<T>(dke + dki[i]));
+        const float dke = __expf(cur.tot - cur.c[i]) * in4[i];
+        dA[i] = cur.qdq[i] - cur.kv[i] * dke;
+        st_elem<T>(rs_dk, eoff[i], cvt<T>(dke + cur.dki[i]));
       }
       float s = 0.f;
 #pragma unroll
@@ -1054,6 +1075,7 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
       }
       sGrp[fk * L::LDRG + frg] = s;
     }
+    factors_part1(max(n - 1, 0));
     __syncthreads();
     if (fthr) {
       const float *car = sCar + (it & 1) * kKF;
@@ -1068,21 +1090,21 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
         }
       }
 #pragma unroll
-      for (int i = 0; i < 4; ++i) dA[i] += later + dai[i];
+      for (int i = 0; i < 4; ++i) dA[i] += later + cur.dai[i];
       if (a.sg) {
         // scalar gate: this tile's sum over its features, per row (rows past
         // the sequence end fall outside the range); the key tiles are added,
         // and the gate epilogue's chain rule applied, by sgate_dla_kernel
         if (a.dla) {
-          float r[4];
+          float rr[4];
 #pragma unroll
-          for (int i = 0; i < 4; ++i) r[i] = half_wave_sum(fv ? dA[i] : 0.f);
+          for (int i = 0; i < 4; ++i) rr[i] = half_wave_sum(fv ? dA[i] : 0.f);
           if (fk == 0) {
             const auto rs_p = make_rsrc(a.dla_part + ((int64_t)bh * a.KT + kt) * a.T + t0,
                                         rsrc_bytes((int64_t)(a.T - t0) * 4));
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-              __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, r[i]), rs_p,
+              __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, rr[i]), rs_p,
                                                     (uint32_t)((4 * frg + i) * 4), 0, 0);
           }
         }
@@ -1092,13 +1114,19 @@ __global__ void __launch_bounds__(kKT) dk_sweep_kernel(KsArgs a) {
                                       a.dla ? rsrc_bytes((int64_t)(a.T - t0) * K * esz) : 0u);
         if constexpr (PRE) {  // gate epilogue: dL/dz = dL/dlog alpha * sigmoid(-z) / tau
 #pragma unroll
-          for (int i = 0; i < 4; ++i) dA[i] *= gate_dla_dg(zc[i], a.inv_tau);
+          for (int i = 0; i < 4; ++i) dA[i] *= gate_dla_dg(cur.zc[i], a.inv_tau);
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i) st_elem<T>(rs_dla, eoff[i], cvt<T>(dA[i]));
       }
-      if (frg == 0) sCar[((it + 1) & 1) * kKF + fk] = all + dat;
+      if (frg == 0) sCar[((it + 1) & 1) * kKF + fk] = all + cur.dat;
     }
+    // ---- the next chunk's factor part 2 (the last chunk redoes its own); the
+    // barrier publishes its tiles before the next chunk's products
+    factors_part2();
+    fetch_factors(max(n - 2, 0));
+    cur = nxt;
+    __syncthreads();
   }
 }
 
@@ -1126,17 +1154,12 @@ int ks_nsl(const Shape &s) {
   return n <= 1 ? 1 : (n <= 2 ? 2 : (n <= 4 ? 4 : 8));
 }
 
-template <typename T, int CP, int NBUF> size_t ks_lds_t() { return KsLayout<T, CP, NBUF>::total; }
+template <typename T, int CP> size_t ks_lds_t() { return KsLayout<T, CP>::total; }
 
-// dq: the dq sweep's layout (two slab buffers)
-size_t ks_lds(const Shape &s, bool dq) {
+size_t ks_lds(const Shape &s) {
   const bool b = s.io == IO_BF16;
-  if (dq) {
-    if (ks_cp(s) == 32) return b ? ks_lds_t<bf16, 32, 2>() : ks_lds_t<float, 32, 2>();
-    return b ? ks_lds_t<bf16, 64, 2>() : ks_lds_t<float, 64, 2>();
-  }
-  if (ks_cp(s) == 32) return b ? ks_lds_t<bf16, 32, 1>() : ks_lds_t<float, 32, 1>();
-  return b ? ks_lds_t<bf16, 64, 1>() : ks_lds_t<float, 64, 1>();
+  if (ks_cp(s) == 32) return b ? ks_lds_t<bf16, 32>() : ks_lds_t<float, 32>();
+  return b ? ks_lds_t<bf16, 64>() : ks_lds_t<float, 64>();
 }
 
 KsArgs ks_args(const Shape &s) {
@@ -1150,7 +1173,7 @@ KsArgs ks_args(const Shape &s) {
 
 template <bool DQ, typename T, int CP, int NSL, bool PRE, bool GB, bool NG>
 hipError_t launch_ks_pre(const KsArgs &a, hipStream_t st) {
-  const size_t lds = KsLayout<T, CP, DQ ? 2 : 1>::total;
+  const size_t lds = KsLayout<T, CP>::total;
   // once per instantiation (thread-safe static initialisation), at the maximum
   static const hipError_t attr =
       hipFuncSetAttribute(DQ ? (const void *)dq_sweep_kernel<T, CP, NSL, PRE, GB, NG>
@@ -1197,14 +1220,14 @@ hipError_t dispatch_ks(const Shape &s, const KsArgs &a, hipStream_t st) {
 
 }  // namespace
 
-size_t lds_bwd_dq(const Shape &s) { return ks_lds(s, true); }
+size_t lds_bwd_dq(const Shape &s) { return ks_lds(s); }
 
 size_t ks_state_bytes(const Shape &s) {
   const int vs = s.io == IO_BF16 ? 256 : 128;
   const int64_t kt = (s.K + kKF - 1) / kKF;
   return (size_t)s.BH * s.N * kt * ks_nsl(s) * vs * kKF * s.esz();
 }
-size_t lds_bwd_dk(const Shape &s) { return ks_lds(s, false); }
+size_t lds_bwd_dk(const Shape &s) { return ks_lds(s); }
 
 hipError_t launch_bwd_dq(const Shape &s, const void *k, const void *la, const void *v,
                          const float *S0, const void *dO, const float *dST,
