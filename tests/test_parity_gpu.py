@@ -277,6 +277,72 @@ def test_absent_gate_is_alpha_one(io):
     compare(inp, o2, ST2, gr2, [0, 1], io, cfg["name"])
 
 
+NG_CASES = [
+    ("bf16", 1, 2, 200, 256, 512, 64, 16, 0),   # the 1.3B widths, ragged tail
+    ("bf16", 1, 2, 96, 128, 256, 32, 8, 0),     # C = 32
+    ("f32", 1, 1, 70, 32, 1024, 16, 16, 0),     # C = 16, d_v = 1024
+    ("bf16", 2, 1, 100, 48, 80, 64, 16, 0),     # a key tile only partly inside d_k
+    ("bf16", 1, 2, 1024, 64, 128, 64, 16, 4),   # four sequence segments per head
+]
+
+
+@pytest.mark.parametrize("io,B,H,T,K,V,C,c,nseg", NG_CASES,
+                         ids=[f"{x[0]}_K{x[4]}_V{x[5]}_T{x[3]}_C{x[6]}_seg{x[8]}" for x in NG_CASES])
+def test_ungated_kernels(io, B, H, T, K, V, C, c, nseg):
+    """log_alpha = NULL and no gate gradient: the alpha = 1 kernel variants
+    (P = tril(q k^T) on the matrix cores, q and k read in place of the gated
+    operands, the intra blocks as masked dP K and dP^T Q, key sweeps without
+    decay factors or operand splits) against the oracle's alpha = 1
+    recurrence, with S0 and dS_T; the stage selector reproduces the whole call
+    and reusing the forward's workspace equals rebuilding it."""
+    g = gla()
+    cfg = small_case(f"ng_{io}_{K}_{V}_{T}_{C}", io, B, H, T, K, V, C, c, 150 + K + T, s0_std=0.1)
+    inp = W.make_inputs(cfg, alpha_one=True, dST_std=0.1)
+    d = to_dev(inp)
+    dt = d["q"].dtype
+    ws = torch.empty(g.workspace_bytes(B, H, T, K, V, C, c, dt, op=1, segments=nseg), dtype=torch.uint8,
+                     device="cuda")
+    args = (d["q"], d["k"], d["v"], None)
+    o, ST = g.chunk_fwd(*args, C, c, S0=d["S0"], output_final_state=True, workspace=ws, segments=nseg)
+    gr = g.chunk_bwd(*args, d["dO"], C, c, S0=d["S0"], dST=d["dST"], want_dS0=True, workspace=ws,
+                     reuse_fwd_workspace=True, segments=nseg)
+    gr2 = g.chunk_bwd(*args, d["dO"], C, c, S0=d["S0"], dST=d["dST"], want_dS0=True, segments=nseg)
+    o3, ST3 = torch.empty_like(o), torch.empty_like(ST)
+    for st in (1, 2):
+        g.chunk_fwd(*args, C, c, S0=d["S0"], workspace=ws, stage=st, out=(o3, ST3), segments=nseg)
+    out = {k2: (torch.empty_like(v2) if v2 is not None else None) for k2, v2 in gr.items()}
+    for st in (2, 3, 4, 5):
+        g.chunk_bwd(*args, d["dO"], C, c, S0=d["S0"], dST=d["dST"], workspace=ws, reuse_fwd_workspace=True,
+                    stage=st, out=out, segments=nseg)
+    torch.cuda.synchronize()
+    assert gr["dlog_alpha"] is None
+    assert torch.equal(o, o3) and torch.equal(ST, ST3), "stages, forward"
+    for k2 in ("dq", "dk", "dv", "dS0"):
+        assert torch.equal(gr[k2], out[k2]), "stages, " + k2
+        assert torch.equal(gr[k2], gr2[k2]), "reuse, " + k2
+    compare(inp, o, ST, gr, list(range(B * H)), io, "ungated " + cfg["name"])
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_absent_gate_with_gate_gradient(io):
+    """log_alpha = NULL with a dlog_alpha output (allowed by the C ABI): the
+    gate gradient at alpha = 1, through the gated backward with log alpha
+    read as 0, against the oracle's."""
+    g = gla()
+    B, H, T, K, V = 1, 2, 150, 64, 128
+    cfg = small_case("ngg_" + io, io, B, H, T, K, V, 64, 16, 28, s0_std=0.1)
+    inp = W.make_inputs(cfg, alpha_one=True, dST_std=0.1)
+    d = to_dev(inp)
+    o, ST = g.chunk_fwd(d["q"], d["k"], d["v"], None, 64, 16, S0=d["S0"], output_final_state=True)
+    out = {"dq": torch.empty_like(d["q"]), "dk": torch.empty_like(d["k"]), "dv": torch.empty_like(d["v"]),
+           "dlog_alpha": torch.empty_like(d["log_alpha"]),
+           "dS0": torch.empty(B, H, K, V, dtype=torch.float32, device="cuda")}
+    g.chunk_bwd(d["q"], d["k"], d["v"], None, d["dO"], 64, 16, S0=d["S0"], dST=d["dST"], want_dS0=True,
+                out=out)
+    torch.cuda.synchronize()
+    compare(inp, o, ST, out, [0, 1], io, "absent gate, gradient wanted " + io)
+
+
 @pytest.mark.parametrize("io", ["f32", "bf16"])
 def test_gate_preactivation_epilogue(io):
     """gate_tau > 0: the gate argument holds the pre-activation z of the GLA
@@ -628,7 +694,7 @@ def test_full_size_sampled_heads(name, alpha_one, dst):
     compare(inp, o, ST, gr, idx, cfg["io"], name)
 
 
-@pytest.mark.parametrize("mode", ["scalar_gate", "general_gate", "output_gate"])
+@pytest.mark.parametrize("mode", ["scalar_gate", "no_gate", "general_gate", "output_gate"])
 def test_full_size_extensions_sampled_heads(mode):
     """The extension modes at the 1.3B workload in the benchmark's launch
     configuration (its input recipe for the extra tensors), checked on sampled
@@ -656,6 +722,22 @@ def test_full_size_extensions_sampled_heads(mode):
         rg = oracle.scalar_gate_bwd(*args, heads(inp["dO"], idx))
         errs = {"o": (heads(o, idx), ro), "S_T": (heads(ST, idx), rST),
                 "dlog_gamma": (heads(gr["dlog_alpha"], idx), rg["dlog_gamma"])}
+        for n in ("dq", "dk", "dv", "dS0"):
+            errs[n] = (heads(gr[n], idx), rg[n])
+    elif mode == "no_gate":
+        # log_alpha = NULL: the alpha = 1 kernel variants (bench.py --no-gate)
+        ws = torch.empty(g.workspace_bytes(B, H, T, K, V, C, c, dt, op=1), dtype=torch.uint8, device="cuda")
+        o, ST = g.chunk_fwd(d["q"], d["k"], d["v"], None, C, c, output_final_state=True, workspace=ws)
+        gr = g.chunk_bwd(d["q"], d["k"], d["v"], None, d["dO"], C, c, want_dS0=True, workspace=ws,
+                         reuse_fwd_workspace=True)
+        torch.cuda.synchronize()
+        assert gr["dlog_alpha"] is None
+        idx = [0, BH - 1]
+        q, k, v, dO = (heads(inp[n], idx) for n in ("q", "k", "v", "dO"))
+        la0 = np.zeros_like(q)
+        ro, rST = oracle.fwd(q, k, v, la0)
+        rg = oracle.bwd(q, k, v, la0, dO)
+        errs = {"o": (heads(o, idx), ro), "S_T": (heads(ST, idx), rST)}
         for n in ("dq", "dk", "dv", "dS0"):
             errs[n] = (heads(gr[n], idx), rg[n])
     elif mode == "general_gate":
