@@ -148,6 +148,11 @@ SMALL = [
     dict(cfg=small_case("bf16_K48_V80", "bf16", 2, 1, 100, 48, 80, 64, 16, 24, s0_std=0.1),
          dST_std=0.1),
     dict(cfg=small_case("bf16_V1024", "bf16", 1, 1, 130, 64, 1024, 64, 16, 25)),
+    # 32-row chunk tiles with two and four value slabs per chunk in the key
+    # sweeps (the 1.3B head width at C = 32; C = 16 with the widest d_v)
+    dict(cfg=small_case("bf16_C32_K256_V512", "bf16", 1, 2, 200, 256, 512, 32, 16, 33, s0_std=0.1),
+         dST_std=0.1),
+    dict(cfg=small_case("bf16_C16_V1024", "bf16", 1, 1, 100, 64, 1024, 16, 8, 34)),
     # the smallest widths: one 16-feature key tile, one 16-column value tile
     dict(cfg=small_case("bf16_K16_V16", "bf16", 2, 2, 150, 16, 16, 64, 16, 27, s0_std=0.1), dST_std=0.1),
     dict(cfg=small_case("f32_K16_V16_C32", "f32", 1, 3, 75, 16, 16, 32, 8, 28, s0_std=0.1), dST_std=0.1),
