@@ -129,6 +129,10 @@ SMALL = [
     dict(cfg=small_case("f32_ragged", "f32", 1, 2, 200, 64, 128, 64, 16, 11)),
     dict(cfg=small_case("f32_C32_c8", "f32", 1, 1, 96, 128, 256, 32, 8, 12)),
     dict(cfg=small_case("f32_C16_wideV", "f32", 1, 1, 70, 32, 1024, 16, 16, 13)),
+    # fp32 key sweeps over two and four 128-column value slabs per 64-row chunk
+    dict(cfg=small_case("f32_C64_V256", "f32", 1, 2, 140, 64, 256, 64, 16, 36)),
+    dict(cfg=small_case("f32_C64_K128_V512", "f32", 1, 1, 150, 128, 512, 64, 16, 35, s0_std=0.1),
+         dST_std=0.1),
     dict(cfg=small_case("f32_state", "f32", 2, 1, 130, 64, 64, 64, 4, 14, s0_std=0.1),
          dST_std=0.1),
     # bf16 at the workload shapes, shorter sequences
