@@ -703,7 +703,7 @@ def test_full_size_sampled_heads(name, alpha_one, dst):
     compare(inp, o, ST, gr, idx, cfg["io"], name)
 
 
-@pytest.mark.parametrize("mode", ["scalar_gate", "no_gate", "general_gate", "output_gate"])
+@pytest.mark.parametrize("mode", ["scalar_gate", "no_gate", "gate_tau", "general_gate", "output_gate"])
 def test_full_size_extensions_sampled_heads(mode):
     """The extension modes at the 1.3B workload in the benchmark's launch
     configuration (its input recipe for the extra tensors), checked on sampled
@@ -747,6 +747,29 @@ def test_full_size_extensions_sampled_heads(mode):
         ro, rST = oracle.fwd(q, k, v, la0)
         rg = oracle.bwd(q, k, v, la0, dO)
         errs = {"o": (heads(o, idx), ro), "S_T": (heads(ST, idx), rST)}
+        for n in ("dq", "dk", "dv", "dS0"):
+            errs[n] = (heads(gr[n], idx), rg[n])
+    elif mode == "gate_tau":
+        # gate pre-activations z (bench.py --gate-tau 16): alpha = sigmoid(z)^(1/16),
+        # log alpha formed in the kernels, dL/dz returned
+        tau = 16.0
+        gz = torch.Generator().manual_seed(cfg["seed"] + 7)
+        z = (torch.randn(inp["log_alpha"].shape, generator=gz) * 2.0 + 1.0).to(dt)
+        zd = z.cuda()
+        ws = torch.empty(g.workspace_bytes(B, H, T, K, V, C, c, dt, op=1), dtype=torch.uint8, device="cuda")
+        o, ST = g.chunk_fwd(d["q"], d["k"], d["v"], zd, C, c, output_final_state=True, workspace=ws,
+                            gate_tau=tau)
+        gr = g.chunk_bwd(d["q"], d["k"], d["v"], zd, d["dO"], C, c, want_dS0=True, workspace=ws,
+                         reuse_fwd_workspace=True, gate_tau=tau)
+        torch.cuda.synchronize()
+        idx = [0, BH - 1]
+        q, k, v, dO = (heads(inp[n], idx) for n in ("q", "k", "v", "dO"))
+        zz = heads(z, idx)
+        la = oracle.gate_log_alpha(zz, tau)
+        ro, rST = oracle.fwd(q, k, v, la)
+        rg = oracle.bwd(q, k, v, la, dO)
+        errs = {"o": (heads(o, idx), ro), "S_T": (heads(ST, idx), rST),
+                "dz": (heads(gr["dlog_alpha"], idx), oracle.gate_grad(zz, tau, rg["dlog_alpha"]))}
         for n in ("dq", "dk", "dv", "dS0"):
             errs[n] = (heads(gr[n], idx), rg[n])
     elif mode == "general_gate":
